@@ -1,0 +1,130 @@
+"""Float64 CPU oracle for batched linear-chain CRF inference.
+
+TEST INFRASTRUCTURE ONLY: the slow, plain checker the HIP path is compared against.
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import it.  The product package never does.
+
+The arithmetic lives in ``oracle.c`` (sequential forward-backward and Viterbi DP in
+float64, following Torch-Struct Sec. 5.1-5.2); this module only marshals numpy arrays
+through ctypes.  Build with ``build()`` (gcc, no fast-math).
+"""
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def compile_source(src, lib):
+    """gcc -O2 -fopenmp (no fast-math) of one oracle source file into a shared library."""
+    tmp = lib + ".tmp"
+    subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11",
+                           "-Wall", "-Wextra", src, "-o", tmp, "-lm"])
+    os.replace(tmp, lib)
+    return lib
+
+
+def build(force=True):
+    """Compile oracle.c into liboracle.so."""
+    if not force and os.path.exists(_LIB):
+        return _LIB
+    return compile_source(_SRC, _LIB)
+
+
+def load_library(path):
+    """Load a compiled oracle library (the default one, or a test's variant of it)."""
+    lib = ctypes.CDLL(path)
+    i64, p = ctypes.c_int64, ctypes.c_void_p
+    for name in ("orc_logpartition", "orc_logpartition_f64"):
+        getattr(lib, name).argtypes = [p, p, i64, i64, i64, p]
+    for name in ("orc_marginals", "orc_marginals_f64"):
+        getattr(lib, name).argtypes = [p, p, i64, i64, i64, p, p]
+    for name in ("orc_viterbi", "orc_viterbi_f64"):
+        getattr(lib, name).argtypes = [p, p, i64, i64, i64, p, p]
+    lib.orc_marginals_seq.argtypes = [p, p, i64, i64, i64, i64, i64, i64, p, p]
+    return lib
+
+
+def _load(lib=None):
+    global _lib
+    if lib is not None:
+        return lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        _lib = load_library(_LIB)
+    return _lib
+
+
+def _prep(pot, lengths):
+    pot = np.asarray(pot)
+    if pot.ndim != 4 or pot.shape[2] != pot.shape[3]:
+        raise ValueError("potentials must be [B, N-1, C, C]")
+    if pot.dtype == np.float64:
+        pot = np.ascontiguousarray(pot)
+        f64 = True
+    else:
+        pot = np.ascontiguousarray(pot, dtype=np.float32)
+        f64 = False
+    B, E, C, _ = pot.shape
+    N = E + 1
+    if lengths is not None:
+        lengths = np.ascontiguousarray(lengths, dtype=np.int32)
+        if lengths.shape != (B,):
+            raise ValueError("lengths must be [B]")
+    return pot, lengths, f64, B, N, C
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def _check(rc):
+    if rc != 0:
+        raise ValueError(f"oracle rejected its arguments (code {rc})")
+
+
+def logpartition(pot, lengths=None, lib=None):
+    """log Z[b] (float64 [B]) for potentials [B, N-1, C, C] and token lengths [B]."""
+    pot, lengths, f64, B, N, C = _prep(pot, lengths)
+    out = np.empty(B, np.float64)
+    fn = _load(lib).orc_logpartition_f64 if f64 else _load(lib).orc_logpartition
+    _check(fn(_ptr(pot), _ptr(lengths), B, N, C, _ptr(out)))
+    return out
+
+
+def marginals(pot, lengths=None, lib=None):
+    """(log Z [B], edge marginals [B, N-1, C, C]) in float64."""
+    pot, lengths, f64, B, N, C = _prep(pot, lengths)
+    logz = np.empty(B, np.float64)
+    marg = np.empty((B, max(N - 1, 0), C, C), np.float64)
+    fn = _load(lib).orc_marginals_f64 if f64 else _load(lib).orc_marginals
+    _check(fn(_ptr(pot), _ptr(lengths), B, N, C, _ptr(logz), _ptr(marg)))
+    return logz, marg
+
+
+def viterbi(pot, lengths=None, lib=None):
+    """(path int32 [B, N], -1 past each length; score float64 [B])."""
+    pot, lengths, f64, B, N, C = _prep(pot, lengths)
+    path = np.empty((B, N), np.int32)
+    score = np.empty(B, np.float64)
+    fn = _load(lib).orc_viterbi_f64 if f64 else _load(lib).orc_viterbi
+    _check(fn(_ptr(pot), _ptr(lengths), B, N, C, _ptr(path), _ptr(score)))
+    return path, score
+
+
+def marginals_seq(pot, lengths, b, t0, t1):
+    """Marginals of edges [t0, t1) of sequence b only (fp32 potentials), and log Z[b]."""
+    pot, lengths, f64, B, N, C = _prep(pot, lengths)
+    if f64:
+        raise ValueError("marginals_seq takes fp32 potentials")
+    out = np.empty((t1 - t0, C, C), np.float64)
+    logz = ctypes.c_double()
+    _check(_load().orc_marginals_seq(_ptr(pot), _ptr(lengths), B, N, C, b, t0, t1, _ptr(out),
+                                     ctypes.addressof(logz)))
+    return out, logz.value

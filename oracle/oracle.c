@@ -1,0 +1,278 @@
+/*
+ * oracle.c -- reference CPU implementation of batched linear-chain CRF inference.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the slow, plain, float64 checker that the
+ * GPU path is compared against.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load it; the product path never does.
+ * It shares no code, header, table or helper with the HIP library.
+ *
+ * What it computes (Torch-Struct, Rush 2020, Sec. 5.1 and 5.2):
+ *   - a sequence of L tokens z_0..z_{L-1}, each taking one of C labels, scored by
+ *     edge log-potentials l[t, z_t, z_{t+1}] for t = 0..L-2 (Sec. 5.2, the linear-chain
+ *     example: the first index of an edge potential is the earlier label, summed first);
+ *   - the log-partition A(l) = log sum_z exp sum_t l[t, z_t, z_{t+1}]  (Sec. 5.1, CRF
+ *     definition; Sec. 5.2, forward algorithm in the (logsumexp, +) semiring);
+ *   - the edge marginals p(z_t = i, z_{t+1} = j) = dA/dl[t,i,j] (Sec. 5.1, gradient
+ *     identity), here by the classical two-pass forward-backward recursion;
+ *   - the max score A*(l) = max_z sum_t l[t,z_t,z_{t+1}] and its argmax path, the
+ *     (max, +) instance of the same recursion (Sec. 5.2; Table 2, "Max" semiring),
+ *     with ties resolved by taking the lowest label index at every backtrace step.
+ *
+ * Conventions (the paper leaves these open; the readings are listed in the design notes):
+ *   - pot is [B, N-1, C, C] row-major: pot[((b*(N-1)+t)*C+i)*C+j] = l[b, t, i, j].
+ *   - lengths[b] counts tokens, 1 <= lengths[b] <= N; edges t >= lengths[b]-1 are padding
+ *     (the semiring identity, Sec. 6a / Fig. 3) and get marginal 0.
+ *   - no start or end potentials: the first and last labels are summed over freely, so
+ *     a single token gives A = log C.
+ *   - -inf potentials are allowed (the semiring zero); an all -inf row of sums gives -inf.
+ *
+ * Arithmetic: float64 throughout, libm exp/log, no fast-math.  fp32 inputs are widened
+ * exactly on read.  Viterbi compares float64 sums exactly.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_OK 0
+#define ORC_ERR_ARG -1
+#define ORC_ERR_MEM -2
+
+/* element (b,t,i,j) of the potentials, widened to double */
+static inline double pot_at(const float* pf, const double* pd, int64_t N, int64_t C,
+                            int64_t b, int64_t t, int64_t i, int64_t j) {
+    int64_t idx = ((b * (N - 1) + t) * C + i) * C + j;
+    return pd ? pd[idx] : (double)pf[idx];
+}
+
+/* log(sum_k exp(x[k])) with the usual max shift; all -inf gives -inf (Sec. 5.1, LSE). */
+static double lse(const double* x, int64_t n) {
+    double m = -INFINITY;
+    for (int64_t k = 0; k < n; ++k)
+        if (x[k] > m) m = x[k];
+    if (m == -INFINITY) return -INFINITY;
+    double s = 0.0;
+    for (int64_t k = 0; k < n; ++k) s += exp(x[k] - m);
+    return m + log(s);
+}
+
+static int check_args(const void* pf, const void* pd, const int32_t* lengths, int64_t B,
+                      int64_t N, int64_t C) {
+    if ((!pf && !pd) || B < 1 || N < 1 || C < 1) return ORC_ERR_ARG;
+    if (lengths)
+        for (int64_t b = 0; b < B; ++b)
+            if (lengths[b] < 1 || lengths[b] > N) return ORC_ERR_ARG;
+    return ORC_OK;
+}
+
+/*
+ * Forward and backward log-messages of one sequence (Sec. 5.2, forward algorithm and
+ * its reverse):
+ *   alpha_0(i) = 0,     alpha_{t+1}(j) = LSE_i [alpha_t(i) + l[t,i,j]]
+ *   beta_{L-1}(j) = 0,  beta_t(i)      = LSE_j [l[t,i,j] + beta_{t+1}(j)]
+ *   A = LSE_j alpha_{L-1}(j)
+ * alpha and beta are [L, C]; tmp is [C].
+ */
+static double fwd_bwd_seq(const float* pf, const double* pd, int64_t N, int64_t C, int64_t b,
+                          int64_t L, double* alpha, double* beta, double* tmp) {
+    for (int64_t i = 0; i < C; ++i) alpha[i] = 0.0;
+    for (int64_t t = 0; t + 1 < L; ++t)
+        for (int64_t j = 0; j < C; ++j) {
+            for (int64_t i = 0; i < C; ++i)
+                tmp[i] = alpha[t * C + i] + pot_at(pf, pd, N, C, b, t, i, j);
+            alpha[(t + 1) * C + j] = lse(tmp, C);
+        }
+    for (int64_t j = 0; j < C; ++j) beta[(L - 1) * C + j] = 0.0;
+    for (int64_t t = L - 2; t >= 0; --t)
+        for (int64_t i = 0; i < C; ++i) {
+            for (int64_t j = 0; j < C; ++j)
+                tmp[j] = pot_at(pf, pd, N, C, b, t, i, j) + beta[(t + 1) * C + j];
+            beta[t * C + i] = lse(tmp, C);
+        }
+    return lse(alpha + (L - 1) * C, C);
+}
+
+/* mu[t,i,j] = exp(alpha_t(i) + l[t,i,j] + beta_{t+1}(j) - A)  (Sec. 5.1: p(z_p=1) = dA/dl_p) */
+static void edge_marginal(const float* pf, const double* pd, int64_t N, int64_t C, int64_t b,
+                          int64_t t, const double* alpha, const double* beta, double logZ,
+                          double* out) {
+    for (int64_t i = 0; i < C; ++i)
+        for (int64_t j = 0; j < C; ++j) {
+            double v = 0.0;
+            if (logZ != -INFINITY)
+                v = exp(alpha[t * C + i] + pot_at(pf, pd, N, C, b, t, i, j) +
+                        beta[(t + 1) * C + j] - logZ);
+            out[i * C + j] = v;
+        }
+}
+
+static int logpartition_impl(const float* pf, const double* pd, const int32_t* lengths,
+                             int64_t B, int64_t N, int64_t C, double* logZ) {
+    int rc = check_args(pf, pd, lengths, B, N, C);
+    if (rc) return rc;
+    int err = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        int64_t L = lengths ? lengths[b] : N;
+        double* alpha = malloc(sizeof(double) * L * C);
+        double* beta = malloc(sizeof(double) * L * C);
+        double* tmp = malloc(sizeof(double) * C);
+        if (!alpha || !beta || !tmp) {
+#pragma omp atomic write
+            err = 1;
+        } else {
+            logZ[b] = fwd_bwd_seq(pf, pd, N, C, b, L, alpha, beta, tmp);
+        }
+        free(alpha); free(beta); free(tmp);
+    }
+    return err ? ORC_ERR_MEM : ORC_OK;
+}
+
+static int marginals_impl(const float* pf, const double* pd, const int32_t* lengths, int64_t B,
+                          int64_t N, int64_t C, double* logZ, double* marg) {
+    int rc = check_args(pf, pd, lengths, B, N, C);
+    if (rc) return rc;
+    if (N == 1) return logpartition_impl(pf, pd, lengths, B, N, C, logZ);
+    int err = 0;
+    double* alpha = malloc(sizeof(double) * B * N * C);
+    double* beta = malloc(sizeof(double) * B * N * C);
+    if (!alpha || !beta) { free(alpha); free(beta); return ORC_ERR_MEM; }
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        int64_t L = lengths ? lengths[b] : N;
+        double* tmp = malloc(sizeof(double) * C);
+        if (!tmp) {
+#pragma omp atomic write
+            err = 1;
+        } else {
+            logZ[b] = fwd_bwd_seq(pf, pd, N, C, b, L, alpha + b * N * C, beta + b * N * C, tmp);
+        }
+        free(tmp);
+    }
+    if (!err) {
+#pragma omp parallel for collapse(2) schedule(static)
+        for (int64_t b = 0; b < B; ++b)
+            for (int64_t t = 0; t < N - 1; ++t) {
+                int64_t L = lengths ? lengths[b] : N;
+                double* out = marg + (b * (N - 1) + t) * C * C;
+                if (t + 1 < L)
+                    edge_marginal(pf, pd, N, C, b, t, alpha + b * N * C, beta + b * N * C,
+                                  logZ[b], out);
+                else
+                    memset(out, 0, sizeof(double) * C * C);
+            }
+    }
+    free(alpha); free(beta);
+    return err ? ORC_ERR_MEM : ORC_OK;
+}
+
+/*
+ * Viterbi DP, the (max, +) instance (Sec. 5.1 A*, Sec. 5.2, Table 2 "Max"):
+ *   delta_0(i) = 0,  delta_{t+1}(j) = max_i [delta_t(i) + l[t,i,j]],
+ *   bp_{t+1}(j) = the smallest i that attains the max;
+ *   score = max_j delta_{L-1}(j), z_{L-1} = the smallest j that attains it,
+ *   z_t = bp_{t+1}(z_{t+1});  path[n] = -1 for n >= L.
+ */
+static int viterbi_impl(const float* pf, const double* pd, const int32_t* lengths, int64_t B,
+                        int64_t N, int64_t C, int32_t* path, double* score) {
+    int rc = check_args(pf, pd, lengths, B, N, C);
+    if (rc) return rc;
+    int err = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        int64_t L = lengths ? lengths[b] : N;
+        double* delta = malloc(sizeof(double) * L * C);
+        int32_t* bp = malloc(sizeof(int32_t) * L * C);
+        if (!delta || !bp) {
+#pragma omp atomic write
+            err = 1;
+            free(delta); free(bp);
+            continue;
+        }
+        for (int64_t i = 0; i < C; ++i) delta[i] = 0.0;
+        for (int64_t t = 0; t + 1 < L; ++t)
+            for (int64_t j = 0; j < C; ++j) {
+                double best = delta[t * C] + pot_at(pf, pd, N, C, b, t, 0, j);
+                int32_t arg = 0;
+                for (int64_t i = 1; i < C; ++i) {
+                    double v = delta[t * C + i] + pot_at(pf, pd, N, C, b, t, i, j);
+                    if (v > best) { best = v; arg = (int32_t)i; }
+                }
+                delta[(t + 1) * C + j] = best;
+                bp[(t + 1) * C + j] = arg;
+            }
+        double best = delta[(L - 1) * C];
+        int32_t z = 0;
+        for (int64_t j = 1; j < C; ++j)
+            if (delta[(L - 1) * C + j] > best) { best = delta[(L - 1) * C + j]; z = (int32_t)j; }
+        score[b] = best;
+        int32_t* p = path + b * N;
+        for (int64_t n = L; n < N; ++n) p[n] = -1;
+        p[L - 1] = z;
+        for (int64_t t = L - 2; t >= 0; --t) {
+            z = bp[(t + 1) * C + z];
+            p[t] = z;
+        }
+        free(delta); free(bp);
+    }
+    return err ? ORC_ERR_MEM : ORC_OK;
+}
+
+/* ---------------- exported entry points ---------------- */
+
+/* fp32 potentials, widened exactly */
+int orc_logpartition(const float* pot, const int32_t* lengths, int64_t B, int64_t N, int64_t C,
+                     double* logZ) {
+    return logpartition_impl(pot, NULL, lengths, B, N, C, logZ);
+}
+int orc_marginals(const float* pot, const int32_t* lengths, int64_t B, int64_t N, int64_t C,
+                  double* logZ, double* marg) {
+    return marginals_impl(pot, NULL, lengths, B, N, C, logZ, marg);
+}
+int orc_viterbi(const float* pot, const int32_t* lengths, int64_t B, int64_t N, int64_t C,
+                int32_t* path, double* score) {
+    return viterbi_impl(pot, NULL, lengths, B, N, C, path, score);
+}
+
+/* float64 potentials (used by the finite-difference pins) */
+int orc_logpartition_f64(const double* pot, const int32_t* lengths, int64_t B, int64_t N,
+                         int64_t C, double* logZ) {
+    return logpartition_impl(NULL, pot, lengths, B, N, C, logZ);
+}
+int orc_marginals_f64(const double* pot, const int32_t* lengths, int64_t B, int64_t N,
+                      int64_t C, double* logZ, double* marg) {
+    return marginals_impl(NULL, pot, lengths, B, N, C, logZ, marg);
+}
+int orc_viterbi_f64(const double* pot, const int32_t* lengths, int64_t B, int64_t N, int64_t C,
+                    int32_t* path, double* score) {
+    return viterbi_impl(NULL, pot, lengths, B, N, C, path, score);
+}
+
+/*
+ * Marginals of edges t0 <= t < t1 of sequence b only (fp32 potentials), for sampled
+ * comparisons at sizes where the full float64 marginal tensor is too large to keep.
+ * out is [(t1-t0), C, C]; edges at or past the sequence's last edge get 0.
+ * logZ_out (nullable) receives A for sequence b.
+ */
+int orc_marginals_seq(const float* pot, const int32_t* lengths, int64_t B, int64_t N, int64_t C,
+                      int64_t b, int64_t t0, int64_t t1, double* out, double* logZ_out) {
+    if (!pot || b < 0 || b >= B || t0 < 0 || t1 < t0 || t1 > N - 1 || C < 1) return ORC_ERR_ARG;
+    int64_t L = lengths ? lengths[b] : N;
+    if (L < 1 || L > N) return ORC_ERR_ARG;
+    double* alpha = malloc(sizeof(double) * L * C);
+    double* beta = malloc(sizeof(double) * L * C);
+    double* tmp = malloc(sizeof(double) * C);
+    if (!alpha || !beta || !tmp) { free(alpha); free(beta); free(tmp); return ORC_ERR_MEM; }
+    double logZ = fwd_bwd_seq(pot, NULL, N, C, b, L, alpha, beta, tmp);
+    if (logZ_out) *logZ_out = logZ;
+#pragma omp parallel for schedule(static)
+    for (int64_t t = t0; t < t1; ++t) {
+        double* o = out + (t - t0) * C * C;
+        if (t + 1 < L)
+            edge_marginal(pot, NULL, N, C, b, t, alpha, beta, logZ, o);
+        else
+            memset(o, 0, sizeof(double) * C * C);
+    }
+    free(alpha); free(beta); free(tmp);
+    return ORC_OK;
+}
