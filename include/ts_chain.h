@@ -1,0 +1,116 @@
+/*
+ * ts_chain.h -- C ABI of the MI355X (gfx950) batched linear-chain CRF library.
+ *
+ * The library computes, for a batch of linear-chain CRFs (Torch-Struct, Rush 2020):
+ *   - the log-partition  A(l) = log sum_z exp sum_t l[t, z_t, z_{t+1}]    (Sec. 5.1-5.2),
+ *   - the edge marginals p(z_t = i, z_{t+1} = j) = dA/dl[t,i,j]          (Sec. 5.1),
+ *   - the max score A*(l) and its argmax label sequence (Viterbi)        (Sec. 5.1-5.2,
+ *     Table 2 "Max" semiring),
+ * each as a balanced tree of C x C semiring matrix products over the edges of every
+ * sequence, padded with the semiring identity (Sec. 6a, Fig. 3).  All arithmetic runs in
+ * HIP kernels on the device; the host only validates arguments and enqueues work.
+ *
+ * Common arguments
+ *   pot      device pointer, float32 [B, N-1, C, C], row-major and contiguous:
+ *            pot[((b*(N-1) + t)*C + i)*C + j] is the log-potential of the labelled edge
+ *            z_t = i -> z_{t+1} = j of sequence b (the earlier label is the row).  Finite
+ *            values and -inf (the semiring zero) are allowed; +inf and NaN are not.
+ *            May be NULL only when N == 1 (no edges).
+ *   lengths  device pointer, int32 [B]: number of tokens of each sequence,
+ *            1 <= lengths[b] <= N.  Edges t >= lengths[b]-1 are padding: they are never
+ *            read and act as the identity.  NULL means every length is N.  Values are not
+ *            read on the host: out-of-range values are clamped to [1, N] by the kernels,
+ *            unless the environment variable TS_CHECK=1 is set, in which case the call
+ *            copies the lengths to the host synchronously and returns TS_ERR_LENGTHS.
+ *   B, N, C  batch size, maximum number of tokens, number of labels:
+ *            B >= 1, N >= 1, 1 <= C <= ts_chain_max_labels().
+ *   ws       device workspace of at least ts_chain_workspace_bytes(op, B, N, C) bytes,
+ *            aligned to 256 bytes (any hipMalloc / PyTorch CUDA allocation is).  May be
+ *            NULL when that size is 0.  Its contents on entry are ignored.
+ *   stream   the hipStream_t to enqueue on (NULL = the default stream).
+ *
+ * Ownership and synchronisation: every pointer is owned by the caller.  The library
+ * allocates nothing, keeps no pointer after returning, and only enqueues kernels on
+ * `stream`; results are ready once that stream is synchronised.  Calls with distinct
+ * workspaces may run concurrently on different streams.  Results are bitwise
+ * reproducible for identical inputs (no floating-point atomics).
+ *
+ * Errors: every call returns a ts_status.  On an error nothing has been enqueued
+ * (TS_ERR_HIP aside, which reports a failed launch) and outputs are unspecified.
+ * ts_last_error() returns a message for the last non-OK status of the calling thread.
+ */
+#ifndef TS_CHAIN_H
+#define TS_CHAIN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int ts_status;
+#define TS_OK 0
+#define TS_ERR_NULL_ARG -1  /* a required pointer is NULL */
+#define TS_ERR_BAD_DIM -2   /* B, N or C out of range, or a size overflows */
+#define TS_ERR_WORKSPACE -3 /* ws_bytes below ts_chain_workspace_bytes() */
+#define TS_ERR_LENGTHS -4   /* TS_CHECK=1 and a length lies outside [1, N] */
+#define TS_ERR_HIP -5       /* a HIP runtime call or kernel launch failed */
+
+/* operation codes for ts_chain_workspace_bytes */
+#define TS_OP_LOGPARTITION 0
+#define TS_OP_MARGINALS 1
+#define TS_OP_VITERBI 2
+
+/* Largest supported number of labels C. */
+int ts_chain_max_labels(void);
+
+/* Workspace bytes that operation `op` needs for (B, N, C); 0 for invalid arguments
+ * (check with the call itself, which reports why). */
+size_t ts_chain_workspace_bytes(int op, int64_t B, int64_t N, int64_t C);
+
+/*
+ * Log-partition (Sec. 5.1 A(l); Sec. 5.2 forward algorithm, evaluated as the tree of
+ * log-semiring (logsumexp, +) matrix products of Sec. 6a).
+ *   logZ  device float32 [B]: log Z of each sequence.  A sequence of one token has no
+ *         edges and log Z = log C (its label is free: no start or end potentials).
+ *         log Z = -inf when no label sequence has a finite score.
+ */
+ts_status ts_chain_logpartition(const float* pot, const int32_t* lengths, int64_t B,
+                                int64_t N, int64_t C, float* logZ, void* ws, size_t ws_bytes,
+                                void* stream);
+
+/*
+ * Edge marginals, the gradient of A (Sec. 5.1: p(z_p = 1) = dA/dl_p), computed by the
+ * outside (down) sweep of the same tree followed by a per-edge local normaliser.
+ *   logZ  device float32 [B] or NULL: as for ts_chain_logpartition.
+ *   marg  device float32 [B, N-1, C, C], same layout as pot: p(z_t=i, z_{t+1}=j).
+ *         Padding edges are written as exactly 0; every entry of a sequence whose
+ *         log Z is -inf is 0.  May be NULL only when N == 1.
+ */
+ts_status ts_chain_marginals(const float* pot, const int32_t* lengths, int64_t B, int64_t N,
+                             int64_t C, float* logZ, float* marg, void* ws, size_t ws_bytes,
+                             void* stream);
+
+/*
+ * Viterbi: the (max, +) instance of the same tree (Sec. 5.1 A*; Sec. 5.2; Table 2 "Max"),
+ * with float64 accumulation, followed by a lowest-index backtrace.
+ *   path  device int32 [B, N]: the argmax label sequence; path[b*N + n] = -1 for
+ *         n >= lengths[b].  Ties are broken by the lowest label index at each backtrace
+ *         step: z_{L-1} is the lowest label of maximal forward score and
+ *         z_t is the lowest i maximising delta_t(i) + l[t, i, z_{t+1}].
+ *   score device float32 [B]: max_z sum_t l[t, z_t, z_{t+1}] (0 for a single token,
+ *         -inf when no sequence is finite).
+ */
+ts_status ts_chain_viterbi(const float* pot, const int32_t* lengths, int64_t B, int64_t N,
+                           int64_t C, int32_t* path, float* score, void* ws, size_t ws_bytes,
+                           void* stream);
+
+/* Message for the last non-OK status returned to the calling thread ("" if none). */
+const char* ts_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TS_CHAIN_H */

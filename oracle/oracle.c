@@ -66,15 +66,12 @@ static int check_args(const void* pf, const void* pd, const int32_t* lengths, in
 }
 
 /*
- * Forward and backward log-messages of one sequence (Sec. 5.2, forward algorithm and
- * its reverse):
- *   alpha_0(i) = 0,     alpha_{t+1}(j) = LSE_i [alpha_t(i) + l[t,i,j]]
- *   beta_{L-1}(j) = 0,  beta_t(i)      = LSE_j [l[t,i,j] + beta_{t+1}(j)]
- *   A = LSE_j alpha_{L-1}(j)
- * alpha and beta are [L, C]; tmp is [C].
+ * Forward log-messages of one sequence (Sec. 5.2, the forward algorithm):
+ *   alpha_0(i) = 0,  alpha_{t+1}(j) = LSE_i [alpha_t(i) + l[t,i,j]],  A = LSE_j alpha_{L-1}(j)
+ * alpha is [L, C]; tmp is [C].  Returns A.
  */
-static double fwd_bwd_seq(const float* pf, const double* pd, int64_t N, int64_t C, int64_t b,
-                          int64_t L, double* alpha, double* beta, double* tmp) {
+static double fwd_seq(const float* pf, const double* pd, int64_t N, int64_t C, int64_t b,
+                      int64_t L, double* alpha, double* tmp) {
     for (int64_t i = 0; i < C; ++i) alpha[i] = 0.0;
     for (int64_t t = 0; t + 1 < L; ++t)
         for (int64_t j = 0; j < C; ++j) {
@@ -82,6 +79,17 @@ static double fwd_bwd_seq(const float* pf, const double* pd, int64_t N, int64_t 
                 tmp[i] = alpha[t * C + i] + pot_at(pf, pd, N, C, b, t, i, j);
             alpha[(t + 1) * C + j] = lse(tmp, C);
         }
+    return lse(alpha + (L - 1) * C, C);
+}
+
+/*
+ * Forward and backward log-messages of one sequence (the forward algorithm and its
+ * reverse):  beta_{L-1}(j) = 0,  beta_t(i) = LSE_j [l[t,i,j] + beta_{t+1}(j)].
+ * alpha and beta are [L, C]; tmp is [C].  Returns A.
+ */
+static double fwd_bwd_seq(const float* pf, const double* pd, int64_t N, int64_t C, int64_t b,
+                          int64_t L, double* alpha, double* beta, double* tmp) {
+    const double A = fwd_seq(pf, pd, N, C, b, L, alpha, tmp);
     for (int64_t j = 0; j < C; ++j) beta[(L - 1) * C + j] = 0.0;
     for (int64_t t = L - 2; t >= 0; --t)
         for (int64_t i = 0; i < C; ++i) {
@@ -89,7 +97,7 @@ static double fwd_bwd_seq(const float* pf, const double* pd, int64_t N, int64_t 
                 tmp[j] = pot_at(pf, pd, N, C, b, t, i, j) + beta[(t + 1) * C + j];
             beta[t * C + i] = lse(tmp, C);
         }
-    return lse(alpha + (L - 1) * C, C);
+    return A;
 }
 
 /* mu[t,i,j] = exp(alpha_t(i) + l[t,i,j] + beta_{t+1}(j) - A)  (Sec. 5.1: p(z_p=1) = dA/dl_p) */
@@ -115,15 +123,14 @@ static int logpartition_impl(const float* pf, const double* pd, const int32_t* l
     for (int64_t b = 0; b < B; ++b) {
         int64_t L = lengths ? lengths[b] : N;
         double* alpha = malloc(sizeof(double) * L * C);
-        double* beta = malloc(sizeof(double) * L * C);
         double* tmp = malloc(sizeof(double) * C);
-        if (!alpha || !beta || !tmp) {
+        if (!alpha || !tmp) {
 #pragma omp atomic write
             err = 1;
         } else {
-            logZ[b] = fwd_bwd_seq(pf, pd, N, C, b, L, alpha, beta, tmp);
+            logZ[b] = fwd_seq(pf, pd, N, C, b, L, alpha, tmp);
         }
-        free(alpha); free(beta); free(tmp);
+        free(alpha); free(tmp);
     }
     return err ? ORC_ERR_MEM : ORC_OK;
 }

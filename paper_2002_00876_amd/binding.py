@@ -1,0 +1,123 @@
+"""Python binding of libtschain.so: marshals torch tensors (device memory and the
+current HIP stream) into the C ABI of include/ts_chain.h.  No arithmetic happens here;
+every step runs in the library's HIP kernels.  If the library is missing, every call
+raises: there is no fallback."""
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libtschain.so")
+
+OP_LOGPARTITION, OP_MARGINALS, OP_VITERBI = 0, 1, 2
+STATUS = {0: "TS_OK", -1: "TS_ERR_NULL_ARG", -2: "TS_ERR_BAD_DIM", -3: "TS_ERR_WORKSPACE",
+          -4: "TS_ERR_LENGTHS", -5: "TS_ERR_HIP"}
+
+_lib = None
+
+
+class TsError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{STATUS.get(code, code)}: {msg}")
+        self.code = code
+
+
+def lib():
+    """The loaded C library with argument types declared (raises if it was not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: run paper_2002_00876_amd.build.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        i64, p, sz = ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
+        L.ts_chain_max_labels.restype = ctypes.c_int
+        L.ts_chain_workspace_bytes.argtypes = [ctypes.c_int, i64, i64, i64]
+        L.ts_chain_workspace_bytes.restype = sz
+        L.ts_chain_logpartition.argtypes = [p, p, i64, i64, i64, p, p, sz, p]
+        L.ts_chain_marginals.argtypes = [p, p, i64, i64, i64, p, p, p, sz, p]
+        L.ts_chain_viterbi.argtypes = [p, p, i64, i64, i64, p, p, p, sz, p]
+        for f in ("ts_chain_logpartition", "ts_chain_marginals", "ts_chain_viterbi"):
+            getattr(L, f).restype = ctypes.c_int
+        L.ts_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(code):
+    if code != 0:
+        raise TsError(code, lib().ts_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(device):
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _prep(pot, lengths):
+    if not pot.is_cuda:
+        raise ValueError("pot must be a device tensor")
+    if pot.dtype != torch.float32 or pot.dim() != 4 or pot.shape[2] != pot.shape[3]:
+        raise ValueError("pot must be float32 [B, N-1, C, C]")
+    pot = pot.contiguous()
+    B, E, C, _ = pot.shape
+    if lengths is not None:
+        if lengths.device != pot.device or lengths.dtype != torch.int32 or lengths.shape != (B,):
+            raise ValueError("lengths must be int32 [B] on the same device as pot")
+        lengths = lengths.contiguous()
+    return pot, lengths, B, E + 1, C
+
+
+def workspace_bytes(op, B, N, C):
+    return lib().ts_chain_workspace_bytes(op, B, N, C)
+
+
+def _workspace(op, B, N, C, device, ws=None):
+    need = workspace_bytes(op, B, N, C)
+    if ws is not None:
+        return ws, ws.numel() * ws.element_size()
+    if need == 0:
+        return None, 0
+    return torch.empty(need, dtype=torch.uint8, device=device), need
+
+
+def logpartition(pot, lengths=None, out=None, ws=None):
+    """log Z [B] (float32) of potentials [B, N-1, C, C] with token lengths [B]."""
+    pot, lengths, B, N, C = _prep(pot, lengths)
+    logz = out if out is not None else torch.empty(B, dtype=torch.float32, device=pot.device)
+    w, nb = _workspace(OP_LOGPARTITION, B, N, C, pot.device, ws)
+    _check(lib().ts_chain_logpartition(_ptr(pot), _ptr(lengths), B, N, C, _ptr(logz), _ptr(w),
+                                       nb, _stream(pot.device)))
+    return logz
+
+
+def marginals(pot, lengths=None, out=None, ws=None, want_logz=True):
+    """(log Z [B] or None, edge marginals [B, N-1, C, C]), float32."""
+    pot, lengths, B, N, C = _prep(pot, lengths)
+    if out is not None:
+        logz, marg = out
+    else:
+        logz = torch.empty(B, dtype=torch.float32, device=pot.device) if want_logz else None
+        marg = torch.empty_like(pot)
+    w, nb = _workspace(OP_MARGINALS, B, N, C, pot.device, ws)
+    _check(lib().ts_chain_marginals(_ptr(pot), _ptr(lengths), B, N, C, _ptr(logz),
+                                    _ptr(marg) if N > 1 else None, _ptr(w), nb,
+                                    _stream(pot.device)))
+    return logz, marg
+
+
+def viterbi(pot, lengths=None, out=None, ws=None):
+    """(path int32 [B, N] with -1 past each length, score float32 [B])."""
+    pot, lengths, B, N, C = _prep(pot, lengths)
+    if out is not None:
+        path, score = out
+    else:
+        path = torch.empty((B, N), dtype=torch.int32, device=pot.device)
+        score = torch.empty(B, dtype=torch.float32, device=pot.device)
+    w, nb = _workspace(OP_VITERBI, B, N, C, pot.device, ws)
+    _check(lib().ts_chain_viterbi(_ptr(pot), _ptr(lengths), B, N, C, _ptr(path), _ptr(score),
+                                  _ptr(w), nb, _stream(pot.device)))
+    return path, score

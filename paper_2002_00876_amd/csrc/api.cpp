@@ -1,0 +1,212 @@
+// api.cpp -- the C ABI declared in include/ts_chain.h: argument validation, workspace
+// planning and the kernel sequence of each call.  All arithmetic happens in the HIP
+// kernels (tree_log.hip, tree_max.hip, small.hip); this file only checks and enqueues.
+#include <hip/hip_runtime.h>
+
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+#include "ts_chain.h"
+
+namespace tsc {
+namespace {
+
+thread_local std::string g_err;
+
+ts_status fail(ts_status code, const std::string& msg) {
+    g_err = msg;
+    return code;
+}
+
+constexpr size_t kAlign = 256;
+
+struct Bump {
+    char* base;
+    size_t off = 0;
+    template <class T>
+    T* take(size_t count) {
+        off = (off + kAlign - 1) / kAlign * kAlign;
+        T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+        off += count * sizeof(T);
+        return p;
+    }
+};
+
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+    if (a < 0 || b < 0) return false;
+    if (a != 0 && b > INT64_MAX / a) return false;
+    *out = a * b;
+    return true;
+}
+
+}  // namespace
+
+bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p) {
+    *p = Plan{};
+    p->B = B; p->N = N; p->C = C; p->E = N - 1; p->op = op;
+    int64_t cc, bcc;
+    // every buffer below is at most B * Np * C * C * 8 bytes; bound that product
+    if (!mul_ok(C, C, &cc) || !mul_ok(B, cc, &bcc) || !mul_ok(bcc, 2 * (N + 1), &cc) ||
+        !mul_ok(cc, 8, &cc) || cc > ((int64_t)1 << 60))
+        return false;
+    if (N == 1) return true;  // no edges: no workspace
+    int64_t Np = 1;
+    int D = 0;
+    while (Np < p->E) { Np <<= 1; ++D; }
+    p->Np = Np; p->D = D;
+    Bump bump{static_cast<char*>(base)};
+    if (op == TS_OP_LOGPARTITION || op == TS_OP_MARGINALS) {
+        for (int l = 1; l <= D; ++l) {
+            const size_t n = (size_t)B * (size_t)(Np >> l);
+            p->core[l] = bump.take<float>(n * C * C);
+            p->ro[l] = bump.take<double>(n * C);
+            p->co[l] = bump.take<double>(n * C);
+        }
+        if (op == TS_OP_MARGINALS)
+            for (int l = 1; l < D; ++l) {
+                const size_t n = (size_t)B * (size_t)(Np >> l);
+                p->u[l] = bump.take<float>(n * C);
+                p->v[l] = bump.take<float>(n * C);
+            }
+    } else {
+        for (int l = 1; l <= D; ++l) {
+            const size_t n = (size_t)B * (size_t)(Np >> l);
+            p->mnode[l] = bump.take<double>(n * C * C);
+        }
+        for (int l = 1; l < D; ++l) {
+            const size_t n = (size_t)B * (size_t)(Np >> l);
+            p->mu[l] = bump.take<double>(n * C);
+        }
+        p->bp = bump.take<uint8_t>((size_t)B * p->E * C);
+        p->zlast = bump.take<int32_t>((size_t)B);
+        // decode chunks: the per-sequence map table (nchunks * C bytes) and one chunk of
+        // backpointers (chunk * C bytes) must each fit in 64 KiB of LDS
+        int64_t K = 64;
+        while (((p->E + K - 1) / K) * C > 65536) K <<= 1;
+        if (K * C > 65536) return false;
+        p->dec_chunk = K;
+        p->dec_nchunks = (p->E + K - 1) / K;
+        p->dec_map = bump.take<uint8_t>((size_t)B * p->dec_nchunks * C);
+        p->dec_zend = bump.take<int32_t>((size_t)B * p->dec_nchunks);
+    }
+    p->bytes = (bump.off + kAlign - 1) / kAlign * kAlign;
+    return true;
+}
+
+namespace {
+
+ts_status check_common(const float* pot, int64_t B, int64_t N, int64_t C, int op, void* ws,
+                       size_t ws_bytes, Plan* plan) {
+    if (B < 1 || N < 1 || C < 1)
+        return fail(TS_ERR_BAD_DIM, "B, N and C must all be >= 1");
+    if (C > kMaxLabels)
+        return fail(TS_ERR_BAD_DIM, "C exceeds ts_chain_max_labels() = " +
+                                        std::to_string(kMaxLabels));
+    if (N > 1 && !pot) return fail(TS_ERR_NULL_ARG, "pot is NULL");
+    if (!make_plan(op, B, N, C, nullptr, plan))
+        return fail(TS_ERR_BAD_DIM, "problem size overflows the supported range");
+    if (plan->bytes > 0) {
+        if (!ws) return fail(TS_ERR_NULL_ARG, "ws is NULL but the call needs a workspace");
+        if (ws_bytes < plan->bytes)
+            return fail(TS_ERR_WORKSPACE, "workspace too small: need " +
+                                              std::to_string(plan->bytes) + " bytes, got " +
+                                              std::to_string(ws_bytes));
+        if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0)
+            return fail(TS_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+        make_plan(op, B, N, C, ws, plan);
+    }
+    return TS_OK;
+}
+
+ts_status check_lengths(const int32_t* lengths, int64_t B, int64_t N, hipStream_t s) {
+    const char* env = std::getenv("TS_CHECK");
+    if (!lengths || !env || std::strcmp(env, "1") != 0) return TS_OK;
+    std::vector<int32_t> h((size_t)B);
+    if (hipMemcpyAsync(h.data(), lengths, sizeof(int32_t) * B, hipMemcpyDeviceToHost, s) !=
+            hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return fail(TS_ERR_HIP, "could not read lengths for TS_CHECK");
+    for (int64_t b = 0; b < B; ++b)
+        if (h[b] < 1 || h[b] > N)
+            return fail(TS_ERR_LENGTHS, "lengths[" + std::to_string(b) + "] = " +
+                                            std::to_string(h[b]) + " is outside [1, N]");
+    return TS_OK;
+}
+
+ts_status hip_status(hipError_t e) {
+    if (e == hipSuccess) return TS_OK;
+    return fail(TS_ERR_HIP, std::string("HIP error: ") + hipGetErrorString(e));
+}
+
+}  // namespace
+}  // namespace tsc
+
+using namespace tsc;
+
+extern "C" {
+
+int ts_chain_max_labels(void) { return kMaxLabels; }
+
+size_t ts_chain_workspace_bytes(int op, int64_t B, int64_t N, int64_t C) {
+    if (op < TS_OP_LOGPARTITION || op > TS_OP_VITERBI || B < 1 || N < 1 || C < 1 ||
+        C > kMaxLabels)
+        return 0;
+    Plan p;
+    if (!make_plan(op, B, N, C, nullptr, &p)) return 0;
+    return p.bytes;
+}
+
+ts_status ts_chain_logpartition(const float* pot, const int32_t* lengths, int64_t B, int64_t N,
+                                int64_t C, float* logZ, void* ws, size_t ws_bytes,
+                                void* stream) {
+    Plan p;
+    ts_status st = check_common(pot, B, N, C, TS_OP_LOGPARTITION, ws, ws_bytes, &p);
+    if (st != TS_OK) return st;
+    if (!logZ) return fail(TS_ERR_NULL_ARG, "logZ is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = check_lengths(lengths, B, N, s)) != TS_OK) return st;
+    if (N == 1) return hip_status(launch_single_token(B, N, C, TS_OP_LOGPARTITION, logZ,
+                                                      nullptr, nullptr, s));
+    return hip_status(launch_logz_tree(p, pot, lengths, logZ, s));
+}
+
+ts_status ts_chain_marginals(const float* pot, const int32_t* lengths, int64_t B, int64_t N,
+                             int64_t C, float* logZ, float* marg, void* ws, size_t ws_bytes,
+                             void* stream) {
+    Plan p;
+    ts_status st = check_common(pot, B, N, C, TS_OP_MARGINALS, ws, ws_bytes, &p);
+    if (st != TS_OK) return st;
+    if (N > 1 && !marg) return fail(TS_ERR_NULL_ARG, "marg is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = check_lengths(lengths, B, N, s)) != TS_OK) return st;
+    if (N == 1) {
+        if (!logZ) return TS_OK;
+        return hip_status(launch_single_token(B, N, C, TS_OP_LOGPARTITION, logZ, nullptr,
+                                              nullptr, s));
+    }
+    // up-sweep (and log Z when requested), then the outside sweep and the marginals
+    hipError_t e = launch_logz_tree(p, pot, lengths, logZ, s);
+    if (e != hipSuccess) return hip_status(e);
+    return hip_status(launch_marginals_tree(p, pot, lengths, marg, s));
+}
+
+ts_status ts_chain_viterbi(const float* pot, const int32_t* lengths, int64_t B, int64_t N,
+                           int64_t C, int32_t* path, float* score, void* ws, size_t ws_bytes,
+                           void* stream) {
+    Plan p;
+    ts_status st = check_common(pot, B, N, C, TS_OP_VITERBI, ws, ws_bytes, &p);
+    if (st != TS_OK) return st;
+    if (!path || !score) return fail(TS_ERR_NULL_ARG, "path or score is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = check_lengths(lengths, B, N, s)) != TS_OK) return st;
+    if (N == 1)
+        return hip_status(launch_single_token(B, N, C, TS_OP_VITERBI, nullptr, path, score, s));
+    return hip_status(launch_viterbi_tree(p, pot, lengths, path, score, s));
+}
+
+const char* ts_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

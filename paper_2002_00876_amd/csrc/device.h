@@ -1,0 +1,114 @@
+// device.h -- small device helpers shared by the HIP kernels (wave64 reductions,
+// numerically guarded log-sum-exp pieces, sequence-length clamping, XCD-aware block
+// numbering).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+namespace tsc {
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ int64_t clamp_len(const int32_t* lengths, int64_t b, int64_t N) {
+    if (!lengths) return N;
+    int64_t L = lengths[b];
+    return L < 1 ? 1 : (L > N ? N : L);
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, kWave));
+    return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, kWave);
+    return x;
+}
+__device__ __forceinline__ double wave_max_d(double x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x = fmax(x, __shfl_xor(x, o, kWave));
+    return x;
+}
+
+// Online log-sum-exp state: value = m + log(s).  m = -inf means the empty sum.
+struct Lse {
+    float m, s;
+};
+__device__ __forceinline__ Lse lse_empty() { return {-INFINITY, 0.f}; }
+__device__ __forceinline__ Lse lse_push(Lse a, float x) {
+    if (x == -INFINITY) return a;
+    if (x <= a.m) {
+        a.s += __expf(x - a.m);
+    } else {
+        a.s = (a.m == -INFINITY ? 0.f : a.s * __expf(a.m - x)) + 1.f;
+        a.m = x;
+    }
+    return a;
+}
+__device__ __forceinline__ Lse lse_merge(Lse a, Lse b) {
+    if (b.m == -INFINITY) return a;
+    if (a.m == -INFINITY) return b;
+    float m = fmaxf(a.m, b.m);
+    return {m, a.s * __expf(a.m - m) + b.s * __expf(b.m - m)};
+}
+__device__ __forceinline__ float lse_value(Lse a) {
+    return a.m == -INFINITY ? -INFINITY : a.m + __logf(a.s);
+}
+__device__ __forceinline__ Lse wave_lse(Lse a) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        Lse b{__shfl_xor(a.m, o, kWave), __shfl_xor(a.s, o, kWave)};
+        a = lse_merge(a, b);
+    }
+    return a;
+}
+
+// Block-wide max of a double over `nthreads` threads (blockDim.x, multiple of 64).
+// `red` is __shared__ scratch of at least nthreads/64 doubles.  Ends with a barrier.
+__device__ __forceinline__ double block_max_d(double x, double* red) {
+    x = wave_max_d(x);
+    const int w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) red[w] = x;
+    __syncthreads();
+    double r = red[0];
+    for (int i = 1; i < nw; ++i) r = fmax(r, red[i]);
+    __syncthreads();
+    return r;
+}
+__device__ __forceinline__ float block_max(float x, float* red) {
+    x = wave_max(x);
+    const int w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) red[w] = x;
+    __syncthreads();
+    float r = red[0];
+    for (int i = 1; i < nw; ++i) r = fmaxf(r, red[i]);
+    __syncthreads();
+    return r;
+}
+__device__ __forceinline__ Lse block_lse(Lse a, float* red) {
+    a = wave_lse(a);
+    const int w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) { red[2 * w] = a.m; red[2 * w + 1] = a.s; }
+    __syncthreads();
+    Lse r{red[0], red[1]};
+    for (int i = 1; i < nw; ++i) r = lse_merge(r, Lse{red[2 * i], red[2 * i + 1]});
+    __syncthreads();
+    return r;
+}
+
+// Shift used before exponentiating: the max, or 0 when everything is -inf (so that
+// -inf - shift stays -inf instead of NaN).
+__device__ __forceinline__ float safe_shift(float m) { return m == -INFINITY ? 0.f : m; }
+__device__ __forceinline__ double safe_shift_d(double m) { return m == -INFINITY ? 0.0 : m; }
+
+// Blocks are dispatched round-robin over the 8 XCDs (block i -> XCD i % 8).  Renumber so
+// that logically consecutive blocks (the tiles of one node) share an XCD and its L2.
+// `nblocks` must be a multiple of 8.
+__device__ __forceinline__ int64_t xcd_swizzle(int64_t bid, int64_t nblocks) {
+    const int64_t per = nblocks >> 3;
+    return (bid & 7) * per + (bid >> 3);
+}
+
+}  // namespace tsc

@@ -1,0 +1,60 @@
+// internal.h -- workspace plan and kernel launchers shared by the C-ABI layer (api.cpp)
+// and the HIP kernels.  Not part of the public interface.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace tsc {
+
+constexpr int kMaxLabels = 256;   // largest C (backpointers are one byte; panels fit LDS)
+constexpr int kMaxLevels = 40;
+
+// Tree over the edges of every sequence: Np = smallest power of two >= N-1 leaves,
+// D = log2(Np) levels above the leaves.  Node k of level l covers edges
+// [k*2^l, (k+1)*2^l); it is present for sequence b iff k*2^l < E_b = len_b - 1.
+// A present node whose right child is absent equals its left child (the right
+// half is all padding, i.e. the semiring identity).
+//
+// Log-semiring node storage (levels 1..D): the node matrix is
+//   P[a][c] = ro[a] + co[c] + core[a][c]
+// with ro, co in float64 and core in float32 (core = log of an exp-shifted product, so
+// it stays small however long the span is).  Leaves (level 0) are the raw potentials
+// with ro = co = 0.
+struct Plan {
+    int64_t B = 0, N = 0, C = 0, E = 0, Np = 1;
+    int D = 0;
+    int op = 0;
+    // log semiring, levels 1..D (index by level)
+    float* core[kMaxLevels] = {};
+    double* ro[kMaxLevels] = {};
+    double* co[kMaxLevels] = {};
+    // outside vectors of the nodes of levels 1..D-1 (normalised to max 0)
+    float* u[kMaxLevels] = {};
+    float* v[kMaxLevels] = {};
+    // max semiring (float64 nodes, levels 1..D) and forward vectors (levels 1..D-1)
+    double* mnode[kMaxLevels] = {};
+    double* mu[kMaxLevels] = {};
+    uint8_t* bp = nullptr;      // [B, E, C] backpointers
+    int32_t* zlast = nullptr;   // [B] label of the last token
+    int64_t dec_chunk = 1;      // edges per decode chunk
+    int64_t dec_nchunks = 0;    // chunks per sequence
+    uint8_t* dec_map = nullptr; // [B, nchunks, C] label at chunk start given label at its end
+    int32_t* dec_zend = nullptr;// [B, nchunks] label at each chunk's end position
+    size_t bytes = 0;
+};
+
+// Fills the plan; with base == nullptr only sizes are computed.  Returns false on overflow.
+bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p);
+
+// ---- launchers (return the first HIP error, hipSuccess otherwise) ----
+hipError_t launch_logz_tree(const Plan& p, const float* pot, const int32_t* lengths,
+                            float* logZ, hipStream_t s);
+hipError_t launch_marginals_tree(const Plan& p, const float* pot, const int32_t* lengths,
+                                 float* marg, hipStream_t s);
+hipError_t launch_viterbi_tree(const Plan& p, const float* pot, const int32_t* lengths,
+                               int32_t* path, float* score, hipStream_t s);
+hipError_t launch_single_token(int64_t B, int64_t N, int64_t C, int op, float* logZ,
+                               int32_t* path, float* score, hipStream_t s);
+
+}  // namespace tsc

@@ -1,0 +1,539 @@
+// tree_log.hip -- log-semiring (logsumexp, +) tree over the edges of each sequence:
+// the up-sweep of C x C semiring matrix products (Torch-Struct Sec. 6a / Fig. 3; the
+// product is the Sec. 6c operation V = log sum_n exp(T + U)), the root log-sum-exp
+// (Sec. 5.2: A sums over the first and last label), the outside (down) sweep that
+// yields every edge's forward and backward messages, and the per-edge marginals
+// (Sec. 5.1: p(z_p = 1) = dA/dl_p).
+//
+// Node representation (levels >= 1): P[a][c] = ro[a] + co[c] + core[a][c], ro/co in
+// float64, core in float32.  The product P = L (x) R is evaluated as an exp-shifted
+// dense GEMM on the fp32 matrix cores:
+//   A'[a][b] = core_L[a][b] + (co_L[b] - max co_L),   B'[b][c] = core_R[b][c] + (ro_R[b] - max ro_R)
+//   rA[a] = max_b A'[a][b],  cB[c] = max_b B'[b][c]
+//   S[a][c] = sum_b exp(A'[a][b] - rA[a]) * exp(B'[b][c] - cB[c])          (MFMA, fp32)
+//   core_P = log S,  ro_P[a] = ro_L[a] + max co_L + rA[a],  co_P[c] = co_R[c] + max ro_R + cB[c]
+// Every exponent is <= 0, so nothing overflows; S < 2^-80 (all terms underflowing) is
+// recomputed exactly by a direct max-shifted log-sum-exp over b.
+#include "device.h"
+#include "internal.h"
+
+namespace tsc {
+
+namespace {
+
+constexpr int kTile = 64;        // output tile rows = cols per workgroup
+constexpr int kUpThreads = 256;  // 4 waves, each owns a 32 x 32 quadrant of the tile
+constexpr float kUnderflow = 0x1p-80f;
+
+typedef float f16v __attribute__((ext_vector_type(16)));
+
+struct UpLogArgs {
+    const float* ccore;   // children (level l-1): core, or the potentials when l == 1
+    const double* cro;    // nullptr for leaves (ro = co = 0)
+    const double* cco;
+    int64_t cnodes;       // child node stride per sequence
+    float* core;          // outputs (level l)
+    double* ro;
+    double* co;
+    int64_t nodes;        // nodes per sequence at level l
+    const int32_t* lengths;
+    int64_t B, N, C;
+    int level;
+    int ntm;              // tiles per matrix dimension
+    int kp;               // C rounded up to a multiple of 8
+    int64_t nlogical;     // B * nodes * ntm * ntm
+    int64_t ngrid;        // nlogical rounded up to a multiple of 8
+};
+
+__device__ __forceinline__ size_t mat_off(int64_t b, int64_t k, int64_t nodes, int64_t C) {
+    return (size_t)(b * nodes + k) * (size_t)C * (size_t)C;
+}
+
+__global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
+    extern __shared__ __align__(16) float smem[];
+    const int64_t lid = xcd_swizzle(blockIdx.x, a.ngrid);
+    if (lid >= a.nlogical) return;
+    const int ntiles = a.ntm * a.ntm;
+    const int tile = (int)(lid % ntiles);
+    const int64_t node = lid / ntiles;
+    const int64_t b = node / a.nodes, k = node % a.nodes;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    const int64_t span = (int64_t)1 << a.level, half = span >> 1;
+    if (k * span >= Eb) return;  // node absent: all padding
+    const int64_t C = a.C;
+    const int tm = tile / a.ntm, tn = tile % a.ntm;
+    const int64_t a0 = (int64_t)tm * kTile, c0 = (int64_t)tn * kTile;
+    const int tid = threadIdx.x;
+
+    const float* Lc = a.ccore + mat_off(b, 2 * k, a.cnodes, C);
+    const double* Lro = a.cro ? a.cro + (size_t)(b * a.cnodes + 2 * k) * C : nullptr;
+    const double* Lco = a.cco ? a.cco + (size_t)(b * a.cnodes + 2 * k) * C : nullptr;
+    float* Pc = a.core + mat_off(b, k, a.nodes, C);
+    double* Pro = a.ro + (size_t)(b * a.nodes + k) * C;
+    double* Pco = a.co + (size_t)(b * a.nodes + k) * C;
+
+    const bool right = (2 * k + 1) * half < Eb;
+    if (!right) {
+        // the right half is padding: the node equals its left child
+        for (int idx = tid; idx < kTile * kTile; idx += kUpThreads) {
+            const int64_t r = a0 + idx / kTile, c = c0 + idx % kTile;
+            if (r < C && c < C) Pc[r * C + c] = Lc[r * C + c];
+        }
+        if (tn == 0)
+            for (int i = tid; i < kTile; i += kUpThreads)
+                if (a0 + i < C) Pro[a0 + i] = Lro ? Lro[a0 + i] : 0.0;
+        if (tm == 0)
+            for (int i = tid; i < kTile; i += kUpThreads)
+                if (c0 + i < C) Pco[c0 + i] = Lco ? Lco[c0 + i] : 0.0;
+        return;
+    }
+    const float* Rc = a.ccore + mat_off(b, 2 * k + 1, a.cnodes, C);
+    const double* Rro = a.cro ? a.cro + (size_t)(b * a.cnodes + 2 * k + 1) * C : nullptr;
+    const double* Rco = a.cco ? a.cco + (size_t)(b * a.cnodes + 2 * k + 1) * C : nullptr;
+
+    const int kp = a.kp, ld = kp + 4;
+    float* As = smem;                  // [kTile][ld]  exp-shifted rows of L
+    float* Bs = As + kTile * ld;       // [kTile][ld]  exp-shifted columns of R (transposed)
+    float* coh = Bs + kTile * ld;      // [kp] co_L - max co_L
+    float* roh = coh + kp;             // [kp] ro_R - max ro_R
+    float* rowm = roh + kp;            // [kTile]
+    float* colm = rowm + kTile;        // [kTile]
+    double* red = (double*)(colm + kTile);  // [4]
+
+    // ---- column offsets of L and row offsets of R, shifted to max 0
+    double lmax = -INFINITY, rmax = -INFINITY;
+    for (int64_t i = tid; i < C; i += kUpThreads) {
+        if (Lco) lmax = fmax(lmax, Lco[i]);
+        if (Rro) rmax = fmax(rmax, Rro[i]);
+    }
+    const double coLshift = Lco ? safe_shift_d(block_max_d(lmax, red)) : 0.0;
+    const double roRshift = Rro ? safe_shift_d(block_max_d(rmax, red)) : 0.0;
+    for (int64_t i = tid; i < kp; i += kUpThreads) {
+        coh[i] = (i < C && Lco) ? (float)(Lco[i] - coLshift) : 0.f;
+        roh[i] = (i < C && Rro) ? (float)(Rro[i] - roRshift) : 0.f;
+    }
+    __syncthreads();
+
+    // ---- stage the operand panels: rows a0.. of L (all b), columns c0.. of R (all b)
+    for (int idx = tid; idx < kTile * kp; idx += kUpThreads) {
+        const int r = idx / kp, bb = idx % kp;
+        const int64_t row = a0 + r;
+        As[r * ld + bb] = (row < C && bb < C) ? Lc[row * C + bb] + coh[bb] : -INFINITY;
+    }
+    for (int idx = tid; idx < kTile * kp; idx += kUpThreads) {
+        const int bb = idx / kTile, cc = idx % kTile;
+        const int64_t col = c0 + cc;
+        Bs[cc * ld + bb] = (col < C && bb < C) ? Rc[(int64_t)bb * C + col] + roh[bb] : -INFINITY;
+    }
+    __syncthreads();
+
+    // ---- row maxima of the A panel and column maxima of the B panel (4 threads each)
+    {
+        const int r = tid >> 2, part = tid & 3;
+        float m1 = -INFINITY, m2 = -INFINITY;
+        for (int bb = part; bb < kp; bb += 4) {
+            m1 = fmaxf(m1, As[r * ld + bb]);
+            m2 = fmaxf(m2, Bs[r * ld + bb]);
+        }
+        m1 = fmaxf(m1, __shfl_xor(m1, 1, kWave));
+        m1 = fmaxf(m1, __shfl_xor(m1, 2, kWave));
+        m2 = fmaxf(m2, __shfl_xor(m2, 1, kWave));
+        m2 = fmaxf(m2, __shfl_xor(m2, 2, kWave));
+        if (part == 0) {
+            rowm[r] = m1;
+            colm[r] = m2;
+        }
+    }
+    __syncthreads();
+    for (int idx = tid; idx < kTile * kp; idx += kUpThreads) {
+        const int r = idx / kp, bb = idx % kp;
+        As[r * ld + bb] = __expf(As[r * ld + bb] - safe_shift(rowm[r]));
+        Bs[r * ld + bb] = __expf(Bs[r * ld + bb] - safe_shift(colm[r]));
+    }
+    __syncthreads();
+
+    // ---- S = expA * expB on the matrix cores.  Within each 8-wide k step, lanes 0-31
+    // contribute k..k+3 and lanes 32-63 k+4..k+7 (one 16-byte LDS read per operand);
+    // A and B use the same k assignment, so the sum over k is unchanged.
+    const int w = tid / kWave, lane = tid % kWave;
+    const int wm = w >> 1, wn = w & 1;
+    f16v acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    const float* ap = As + (wm * 32 + (lane & 31)) * ld + 4 * (lane >> 5);
+    const float* bp = Bs + (wn * 32 + (lane & 31)) * ld + 4 * (lane >> 5);
+    for (int kk = 0; kk < kp; kk += 8) {
+        const float4 av = *(const float4*)(ap + kk);
+        const float4 bv = *(const float4*)(bp + kk);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.x, bv.x, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.y, bv.y, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.z, bv.z, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.w, bv.w, acc, 0, 0, 0);
+    }
+
+    // ---- epilogue: core = log S (exact fallback when S underflows)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int row = wm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        const int col = wn * 32 + (lane & 31);
+        const int64_t gr = a0 + row, gc = c0 + col;
+        if (gr < C && gc < C) {
+            const float S = acc[r];
+            float val;
+            if (S >= kUnderflow) {
+                val = __logf(S);
+            } else {
+                const float sa = safe_shift(rowm[row]), sb = safe_shift(colm[col]);
+                float q = -INFINITY;
+                for (int64_t bb = 0; bb < C; ++bb) {
+                    const float x = (Lc[gr * C + bb] + coh[bb] - sa) +
+                                    (Rc[bb * C + gc] + roh[bb] - sb);
+                    q = fmaxf(q, x);
+                }
+                if (q == -INFINITY) {
+                    val = -INFINITY;
+                } else {
+                    float s = 0.f;
+                    for (int64_t bb = 0; bb < C; ++bb) {
+                        const float x = (Lc[gr * C + bb] + coh[bb] - sa) +
+                                        (Rc[bb * C + gc] + roh[bb] - sb);
+                        s += __expf(x - q);
+                    }
+                    val = q + __logf(s);
+                }
+            }
+            Pc[gr * C + gc] = val;
+        }
+    }
+    if (tn == 0)
+        for (int i = tid; i < kTile; i += kUpThreads)
+            if (a0 + i < C) Pro[a0 + i] = (Lro ? Lro[a0 + i] : 0.0) + coLshift + safe_shift(rowm[i]);
+    if (tm == 0)
+        for (int i = tid; i < kTile; i += kUpThreads)
+            if (c0 + i < C) Pco[c0 + i] = (Rco ? Rco[c0 + i] : 0.0) + roRshift + safe_shift(colm[i]);
+}
+
+// ---------------------------------------------------------------- root: log Z
+struct RootArgs {
+    const float* core;   // level D core, or the potentials when D == 0
+    const double* ro;    // nullptr when D == 0
+    const double* co;
+    int64_t nodes;       // node stride per sequence at that level
+    const int32_t* lengths;
+    int64_t N, C;
+    float* logZ;
+};
+
+__global__ __launch_bounds__(256) void k_root_log(RootArgs a) {
+    __shared__ float red[16];
+    __shared__ double redd[4];
+    const int64_t b = blockIdx.x;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    const int64_t C = a.C;
+    if (Eb == 0) {
+        if (threadIdx.x == 0) a.logZ[b] = logf((float)C);
+        return;
+    }
+    const float* P = a.core + mat_off(b, 0, a.nodes, C);
+    const double* ro = a.ro ? a.ro + (size_t)b * a.nodes * C : nullptr;
+    const double* co = a.co ? a.co + (size_t)b * a.nodes * C : nullptr;
+    double rm = -INFINITY, cm = -INFINITY;
+    for (int64_t i = threadIdx.x; i < C; i += blockDim.x) {
+        if (ro) rm = fmax(rm, ro[i]);
+        if (co) cm = fmax(cm, co[i]);
+    }
+    const double rs = ro ? safe_shift_d(block_max_d(rm, redd)) : 0.0;
+    const double cs = co ? safe_shift_d(block_max_d(cm, redd)) : 0.0;
+    Lse acc = lse_empty();
+    for (int64_t idx = threadIdx.x; idx < C * C; idx += blockDim.x) {
+        const int64_t i = idx / C, j = idx % C;
+        float x = P[idx];
+        if (ro) x += (float)(ro[i] - rs) + (float)(co[j] - cs);
+        acc = lse_push(acc, x);
+    }
+    acc = block_lse(acc, red);
+    if (threadIdx.x == 0) {
+        const float l = lse_value(acc);
+        a.logZ[b] = (l == -INFINITY) ? -INFINITY : (float)(rs + cs + (double)l);
+    }
+}
+
+// ---------------------------------------------------------------- outside sweep
+// For a present node N = L (x) R with outside vectors (u_N, v_N) -- u the forward
+// message into its first edge, v the backward message out of its last edge:
+//   u_L = u_N,  v_L = R (x) v_N,  u_R = u_N (x) L,  v_R = v_N
+// (an absent right child leaves v_L = v_N).  Vectors are stored shifted to max 0.
+struct DownArgs {
+    const float* uN;       // level l vectors (nullptr at the root: zeros)
+    const float* vN;
+    int64_t nodes;         // nodes per sequence at level l
+    const float* ccore;    // children (level l-1 >= 1)
+    const double* cro;
+    const double* cco;
+    int64_t cnodes;
+    float* uC;             // child vectors (level l-1)
+    float* vC;
+    const int32_t* lengths;
+    int64_t N, C;
+    int level;
+};
+
+// y[j] = co[j] + LSE_i (x[i] + ro[i] + core[i][j]),  then shifted to max 0.
+// Column-parallel: thread j walks i.  x: [C] in shared memory.
+__device__ void vec_mat_log(const float* x, const float* core, const double* ro,
+                            const double* co, int64_t C, float* y, float* wsh, double* redd,
+                            float* redf) {
+    // w[i] = x[i] + ro[i], shifted (float64) so that max w = 0
+    double wm = -INFINITY;
+    for (int64_t i = threadIdx.x; i < C; i += blockDim.x)
+        wm = fmax(wm, (double)x[i] + (ro ? ro[i] : 0.0));
+    const double ws = safe_shift_d(block_max_d(wm, redd));
+    for (int64_t i = threadIdx.x; i < C; i += blockDim.x)
+        wsh[i] = (float)((double)x[i] + (ro ? ro[i] : 0.0) - ws);
+    __syncthreads();
+    double zm = -INFINITY;
+    double z = -INFINITY;
+    const int64_t j = threadIdx.x;
+    if (j < C) {
+        Lse acc = lse_empty();
+        for (int64_t i = 0; i < C; ++i) acc = lse_push(acc, wsh[i] + core[i * C + j]);
+        const float yl = lse_value(acc);
+        z = (yl == -INFINITY) ? -INFINITY : (co ? co[j] : 0.0) + (double)yl;
+        zm = z;
+    }
+    const double zs = safe_shift_d(block_max_d(zm, redd));
+    if (j < C) y[j] = (z == -INFINITY) ? -INFINITY : (float)(z - zs);
+    __syncthreads();
+    (void)redf;
+}
+
+// y[i] = ro[i] + LSE_j (core[i][j] + co[j] + x[j]), then shifted to max 0.
+// Row-parallel: one wave per row, lanes over j.
+__device__ void mat_vec_log(const float* core, const double* ro, const double* co,
+                            const float* x, int64_t C, float* y, float* wsh, float* tmp,
+                            double* redd) {
+    double wm = -INFINITY;
+    for (int64_t j = threadIdx.x; j < C; j += blockDim.x)
+        wm = fmax(wm, (double)x[j] + (co ? co[j] : 0.0));
+    const double ws = safe_shift_d(block_max_d(wm, redd));
+    for (int64_t j = threadIdx.x; j < C; j += blockDim.x)
+        wsh[j] = (float)((double)x[j] + (co ? co[j] : 0.0) - ws);
+    __syncthreads();
+    const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave, nw = blockDim.x / kWave;
+    for (int64_t i = w; i < C; i += nw) {
+        Lse acc = lse_empty();
+        for (int64_t j = lane; j < C; j += kWave) acc = lse_push(acc, core[i * C + j] + wsh[j]);
+        acc = wave_lse(acc);
+        if (lane == 0) tmp[i] = lse_value(acc);
+    }
+    __syncthreads();
+    double zm = -INFINITY, z = -INFINITY;
+    const int64_t i = threadIdx.x;
+    if (i < C) {
+        const float yl = tmp[i];
+        z = (yl == -INFINITY) ? -INFINITY : (ro ? ro[i] : 0.0) + (double)yl;
+        zm = z;
+    }
+    const double zs = safe_shift_d(block_max_d(zm, redd));
+    if (i < C) y[i] = (z == -INFINITY) ? -INFINITY : (float)(z - zs);
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(256) void k_down_log(DownArgs a) {
+    __shared__ float su[kMaxLabels], sv[kMaxLabels], sy[kMaxLabels], wsh[kMaxLabels],
+        tmp[kMaxLabels];
+    __shared__ double redd[4];
+    __shared__ float redf[16];
+    const int64_t b = blockIdx.x / a.nodes, k = blockIdx.x % a.nodes;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    const int64_t C = a.C;
+    const int64_t span = (int64_t)1 << a.level, half = span >> 1;
+    if (k * span >= Eb) return;
+    for (int64_t i = threadIdx.x; i < C; i += blockDim.x) {
+        su[i] = a.uN ? a.uN[(size_t)(b * a.nodes + k) * C + i] : 0.f;
+        sv[i] = a.vN ? a.vN[(size_t)(b * a.nodes + k) * C + i] : 0.f;
+    }
+    __syncthreads();
+    const int64_t kl = 2 * k, kr = 2 * k + 1;
+    float* uL = a.uC + (size_t)(b * a.cnodes + kl) * C;
+    float* vL = a.vC + (size_t)(b * a.cnodes + kl) * C;
+    const bool right = kr * half < Eb;
+    for (int64_t i = threadIdx.x; i < C; i += blockDim.x) uL[i] = su[i];
+    if (!right) {
+        for (int64_t i = threadIdx.x; i < C; i += blockDim.x) vL[i] = sv[i];
+        return;
+    }
+    float* uR = a.uC + (size_t)(b * a.cnodes + kr) * C;
+    float* vR = a.vC + (size_t)(b * a.cnodes + kr) * C;
+    for (int64_t i = threadIdx.x; i < C; i += blockDim.x) vR[i] = sv[i];
+    // u_R = u_N (x) L
+    {
+        const float* core = a.ccore + mat_off(b, kl, a.cnodes, C);
+        const double* ro = a.cro + (size_t)(b * a.cnodes + kl) * C;
+        const double* co = a.cco + (size_t)(b * a.cnodes + kl) * C;
+        vec_mat_log(su, core, ro, co, C, sy, wsh, redd, redf);
+        for (int64_t i = threadIdx.x; i < C; i += blockDim.x) uR[i] = sy[i];
+        __syncthreads();
+    }
+    // v_L = R (x) v_N
+    {
+        const float* core = a.ccore + mat_off(b, kr, a.cnodes, C);
+        const double* ro = a.cro + (size_t)(b * a.cnodes + kr) * C;
+        const double* co = a.cco + (size_t)(b * a.cnodes + kr) * C;
+        mat_vec_log(core, ro, co, sv, C, sy, wsh, tmp, redd);
+        for (int64_t i = threadIdx.x; i < C; i += blockDim.x) vL[i] = sy[i];
+    }
+}
+
+// ---------------------------------------------------------------- marginals
+// One block per level-1 node (edges 2k and 2k+1).  With the node's outside vectors
+// (u, v): alpha_{2k} = u, beta_{2k+1} = leaf_{2k+1} (x) v, alpha_{2k+1} = u (x) leaf_{2k},
+// beta_{2k+2} = v.  Each edge's marginal uses its own normaliser
+//   n_t = LSE_{i,j} (alpha_t[i] + l[t][i][j] + beta_{t+1}[j]),
+//   mu[t][i][j] = exp(alpha_t[i] + l[t][i][j] + beta_{t+1}[j] - n_t),
+// exact because alpha_t and beta_{t+1} are the true messages up to constants and
+// log Z = const + n_t for every edge t.
+struct FormArgs {
+    const float* pot;
+    const float* u1;   // level-1 vectors, nullptr when level 1 is the root (D <= 1)
+    const float* v1;
+    int64_t nodes1;    // nodes per sequence at level 1 (Np / 2, or 1 when D == 0)
+    const int32_t* lengths;
+    int64_t N, C;
+    float* marg;
+};
+
+__device__ void form_edge(const float* leaf, const float* al, const float* be, int64_t C,
+                          float* out, float* red) {
+    Lse acc = lse_empty();
+    for (int64_t idx = threadIdx.x; idx < C * C; idx += blockDim.x)
+        acc = lse_push(acc, al[idx / C] + leaf[idx] + be[idx % C]);
+    acc = block_lse(acc, red);
+    const float n = lse_value(acc);
+    for (int64_t idx = threadIdx.x; idx < C * C; idx += blockDim.x)
+        out[idx] = (n == -INFINITY) ? 0.f : __expf(al[idx / C] + leaf[idx] + be[idx % C] - n);
+}
+
+__global__ __launch_bounds__(256) void k_form_log(FormArgs a) {
+    __shared__ float su[kMaxLabels], sv[kMaxLabels], aR[kMaxLabels], bL[kMaxLabels],
+        wsh[kMaxLabels], tmp[kMaxLabels];
+    __shared__ double redd[4];
+    __shared__ float red[16];
+    const int64_t npairs = (a.N - 1 + 1) / 2;
+    const int64_t b = blockIdx.x / npairs, k = blockIdx.x % npairs;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    const int64_t C = a.C, E = a.N - 1;
+    const int64_t tL = 2 * k, tR = 2 * k + 1;
+    const size_t CC = (size_t)C * C;
+    // padding edges are exactly zero
+    for (int64_t t = tL; t <= tR; ++t)
+        if (t < E && t >= Eb) {
+            float* o = a.marg + (size_t)(b * E + t) * CC;
+            for (int64_t idx = threadIdx.x; idx < (int64_t)CC; idx += blockDim.x) o[idx] = 0.f;
+        }
+    if (tL >= Eb) return;
+    for (int64_t i = threadIdx.x; i < C; i += blockDim.x) {
+        su[i] = a.u1 ? a.u1[(size_t)(b * a.nodes1 + k) * C + i] : 0.f;
+        sv[i] = a.v1 ? a.v1[(size_t)(b * a.nodes1 + k) * C + i] : 0.f;
+    }
+    __syncthreads();
+    const float* leafL = a.pot + (size_t)(b * E + tL) * CC;
+    const bool right = tR < Eb;
+    if (right) {
+        const float* leafR = a.pot + (size_t)(b * E + tR) * CC;
+        mat_vec_log(leafR, nullptr, nullptr, sv, C, bL, wsh, tmp, redd);   // beta_{2k+1}
+        vec_mat_log(su, leafL, nullptr, nullptr, C, aR, wsh, redd, red);   // alpha_{2k+1}
+        form_edge(leafL, su, bL, C, a.marg + (size_t)(b * E + tL) * CC, red);
+        form_edge(leafR, aR, sv, C, a.marg + (size_t)(b * E + tR) * CC, red);
+    } else {
+        form_edge(leafL, su, sv, C, a.marg + (size_t)(b * E + tL) * CC, red);
+    }
+}
+
+inline int64_t round8(int64_t x) { return (x + 7) / 8 * 8; }
+
+hipError_t up_sweep(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
+    const int64_t C = p.C;
+    const int ntm = (int)((C + kTile - 1) / kTile);
+    const int kp = (int)((C + 7) / 8 * 8);
+    const size_t lds = sizeof(float) * (2 * kTile * (kp + 4) + 2 * kp + 2 * kTile) +
+                       sizeof(double) * 4;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute((const void*)k_up_log,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           160 * 1024);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    for (int l = 1; l <= p.D; ++l) {
+        UpLogArgs a{};
+        if (l == 1) {
+            a.ccore = pot; a.cro = nullptr; a.cco = nullptr; a.cnodes = p.E;
+        } else {
+            a.ccore = p.core[l - 1]; a.cro = p.ro[l - 1]; a.cco = p.co[l - 1];
+            a.cnodes = p.Np >> (l - 1);
+        }
+        a.core = p.core[l]; a.ro = p.ro[l]; a.co = p.co[l];
+        a.nodes = p.Np >> l;
+        a.lengths = lengths; a.B = p.B; a.N = p.N; a.C = C; a.level = l;
+        a.ntm = ntm; a.kp = kp;
+        a.nlogical = p.B * a.nodes * ntm * ntm;
+        a.ngrid = round8(a.nlogical);
+        hipLaunchKernelGGL(k_up_log, dim3((unsigned)a.ngrid), dim3(kUpThreads), lds, s, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t root(const Plan& p, const float* pot, const int32_t* lengths, float* logZ,
+                hipStream_t s) {
+    RootArgs r{};
+    if (p.D == 0) {
+        r.core = pot; r.ro = nullptr; r.co = nullptr; r.nodes = p.E;
+    } else {
+        r.core = p.core[p.D]; r.ro = p.ro[p.D]; r.co = p.co[p.D]; r.nodes = p.Np >> p.D;
+    }
+    r.lengths = lengths; r.N = p.N; r.C = p.C; r.logZ = logZ;
+    hipLaunchKernelGGL(k_root_log, dim3((unsigned)p.B), dim3(256), 0, s, r);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_logz_tree(const Plan& p, const float* pot, const int32_t* lengths,
+                            float* logZ, hipStream_t s) {
+    hipError_t e = up_sweep(p, pot, lengths, s);
+    if (e != hipSuccess || !logZ) return e;
+    return root(p, pot, lengths, logZ, s);
+}
+
+hipError_t launch_marginals_tree(const Plan& p, const float* pot, const int32_t* lengths,
+                                 float* marg, hipStream_t s) {
+    // (the up-sweep has been enqueued by the caller)
+    for (int l = p.D; l >= 2; --l) {
+        DownArgs d{};
+        d.uN = (l == p.D) ? nullptr : p.u[l];
+        d.vN = (l == p.D) ? nullptr : p.v[l];
+        d.nodes = p.Np >> l;
+        d.ccore = p.core[l - 1]; d.cro = p.ro[l - 1]; d.cco = p.co[l - 1];
+        d.cnodes = p.Np >> (l - 1);
+        d.uC = p.u[l - 1]; d.vC = p.v[l - 1];
+        d.lengths = lengths; d.N = p.N; d.C = p.C; d.level = l;
+        hipLaunchKernelGGL(k_down_log, dim3((unsigned)(p.B * d.nodes)), dim3(256), 0, s, d);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    FormArgs f{};
+    f.pot = pot;
+    f.u1 = (p.D >= 2) ? p.u[1] : nullptr;
+    f.v1 = (p.D >= 2) ? p.v[1] : nullptr;
+    f.nodes1 = (p.D >= 1) ? (p.Np >> 1) : 1;
+    f.lengths = lengths; f.N = p.N; f.C = p.C; f.marg = marg;
+    const int64_t npairs = (p.N - 1 + 1) / 2;
+    hipLaunchKernelGGL(k_form_log, dim3((unsigned)(p.B * npairs)), dim3(256), 0, s, f);
+    return hipGetLastError();
+}
+
+}  // namespace tsc

@@ -1,0 +1,380 @@
+// tree_max.hip -- the (max, +) instance of the edge tree (Torch-Struct Sec. 5.2: the
+// max semiring turns the forward algorithm into the max score; Table 2 "Max"; Sec. 6a
+// tree order), followed by backpointers and a lowest-index backtrace.
+//
+// All sums are float64.  A float64 sum of float32 potentials is exact while the partial
+// sums stay within 53 significant bits (e.g. every |l| >= 2^-14 and |sum| < 2^15), so
+// the tree's forward scores delta_t equal the sequential recursion's bit for bit and
+// every argmax decision (and tie) is the same whatever the association order.
+//
+//   up-sweep:   P[a][c] = max_b L[a][b] + R[b][c]              (nodes of levels 1..D)
+//   down-sweep: u_L = u_N, u_R = u_N (x) L                     (forward scores only)
+//   leaves:     delta_t = u at edge t; bp_t[j] = lowest argmax_i delta_t[i] + l[t][i][j];
+//               the last edge also gives z_{L-1} = lowest argmax_j delta_{L-1}[j] and the score
+//   decode:     z_t = bp_t[z_{t+1}] by chunks: each chunk maps its end label to its start
+//               label for every possible end label; one short serial walk over chunks;
+//               each chunk then emits its labels.
+#include "device.h"
+#include "internal.h"
+
+namespace tsc {
+
+namespace {
+
+constexpr int kMT = 64;    // output tile
+constexpr int kMK = 32;    // k slice
+constexpr int kMThreads = 256;
+
+struct UpMaxArgs {
+    const float* leaves;    // level 1 reads the potentials
+    const double* cnode;    // level >= 2 reads float64 nodes
+    int64_t cnodes;
+    double* node;
+    int64_t nodes;
+    const int32_t* lengths;
+    int64_t B, N, C;
+    int level, ntm;
+    int64_t nlogical, ngrid;
+};
+
+__device__ __forceinline__ double child_at(const UpMaxArgs& a, int64_t b, int64_t k, int64_t r,
+                                           int64_t c) {
+    const size_t off = (size_t)(b * a.cnodes + k) * a.C * a.C + (size_t)(r * a.C + c);
+    return a.cnode ? a.cnode[off] : (double)a.leaves[off];
+}
+
+__global__ __launch_bounds__(kMThreads) void k_up_max(UpMaxArgs a) {
+    __shared__ double As[kMK][kMT];   // As[k][row]
+    __shared__ double Bs[kMK][kMT];   // Bs[k][col]
+    const int64_t lid = xcd_swizzle(blockIdx.x, a.ngrid);
+    if (lid >= a.nlogical) return;
+    const int ntiles = a.ntm * a.ntm;
+    const int tile = (int)(lid % ntiles);
+    const int64_t node = lid / ntiles;
+    const int64_t b = node / a.nodes, k = node % a.nodes;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    const int64_t span = (int64_t)1 << a.level, half = span >> 1;
+    if (k * span >= Eb) return;
+    const int64_t C = a.C;
+    const int tm = tile / a.ntm, tn = tile % a.ntm;
+    const int64_t a0 = (int64_t)tm * kMT, c0 = (int64_t)tn * kMT;
+    const int tid = threadIdx.x;
+    double* P = a.node + (size_t)(b * a.nodes + k) * C * C;
+    const bool right = (2 * k + 1) * half < Eb;
+    if (!right) {
+        for (int idx = tid; idx < kMT * kMT; idx += kMThreads) {
+            const int64_t r = a0 + idx / kMT, c = c0 + idx % kMT;
+            if (r < C && c < C) P[r * C + c] = child_at(a, b, 2 * k, r, c);
+        }
+        return;
+    }
+    const int ty = tid / 16, tx = tid % 16;   // 4 x 4 outputs per thread
+    double acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = -INFINITY;
+    for (int64_t k0 = 0; k0 < C; k0 += kMK) {
+        for (int idx = tid; idx < kMT * kMK; idx += kMThreads) {
+            const int r = idx / kMK, kk = idx % kMK;
+            const int64_t row = a0 + r, kg = k0 + kk;
+            As[kk][r] = (row < C && kg < C) ? child_at(a, b, 2 * k, row, kg) : -INFINITY;
+        }
+        for (int idx = tid; idx < kMT * kMK; idx += kMThreads) {
+            const int kk = idx / kMT, cc = idx % kMT;
+            const int64_t col = c0 + cc, kg = k0 + kk;
+            Bs[kk][cc] = (col < C && kg < C) ? child_at(a, b, 2 * k + 1, kg, col) : -INFINITY;
+        }
+        __syncthreads();
+#pragma unroll 4
+        for (int kk = 0; kk < kMK; ++kk) {
+            double av[4], bv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                av[i] = As[kk][ty * 4 + i];
+                bv[i] = Bs[kk][tx * 4 + i];
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = fmax(acc[i][j], av[i] + bv[j]);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t r = a0 + ty * 4 + i, c = c0 + tx * 4 + j;
+            if (r < C && c < C) P[r * C + c] = acc[i][j];
+        }
+}
+
+// ---- forward scores down the tree: u_L = u_N, u_R = u_N (x) L
+struct DownMaxArgs {
+    const double* uN;    // nullptr at the root (zeros)
+    int64_t nodes;
+    const double* cnode; // children (level l-1 >= 1)
+    int64_t cnodes;
+    double* uC;
+    const int32_t* lengths;
+    int64_t N, C;
+    int level;
+};
+
+__global__ __launch_bounds__(256) void k_down_max(DownMaxArgs a) {
+    __shared__ double su[kMaxLabels];
+    const int64_t b = blockIdx.x / a.nodes, k = blockIdx.x % a.nodes;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    const int64_t C = a.C;
+    const int64_t span = (int64_t)1 << a.level, half = span >> 1;
+    if (k * span >= Eb) return;
+    for (int64_t i = threadIdx.x; i < C; i += blockDim.x)
+        su[i] = a.uN ? a.uN[(size_t)(b * a.nodes + k) * C + i] : 0.0;
+    __syncthreads();
+    double* uL = a.uC + (size_t)(b * a.cnodes + 2 * k) * C;
+    for (int64_t i = threadIdx.x; i < C; i += blockDim.x) uL[i] = su[i];
+    if ((2 * k + 1) * half >= Eb) return;
+    const double* L = a.cnode + (size_t)(b * a.cnodes + 2 * k) * C * C;
+    double* uR = a.uC + (size_t)(b * a.cnodes + 2 * k + 1) * C;
+    const int64_t j = threadIdx.x;
+    if (j < C) {
+        double m = -INFINITY;
+        for (int64_t i = 0; i < C; ++i) m = fmax(m, su[i] + L[i * C + j]);
+        uR[j] = m;
+    }
+}
+
+// ---- leaves: backpointers, last label and score
+struct BpArgs {
+    const float* pot;
+    const double* u1;   // level-1 forward vectors (nullptr when level 1 is the root)
+    int64_t nodes1;
+    const int32_t* lengths;
+    int64_t N, C;
+    uint8_t* bp;        // [B, E, C]
+    int32_t* zlast;     // [B]
+    float* score;       // [B]
+};
+
+// For edge t with forward scores d (shared, [C]): bp[t][j] = lowest argmax_i d[i] + l[t][i][j]
+// and, into dn[j] (shared, may be nullptr), the max itself.
+__device__ void backpointers(const float* leaf, const double* d, int64_t C, uint8_t* bp,
+                             double* dn) {
+    const int64_t j = threadIdx.x;
+    if (j < C) {
+        double best = d[0] + (double)leaf[j];
+        int arg = 0;
+        for (int64_t i = 1; i < C; ++i) {
+            const double v = d[i] + (double)leaf[i * C + j];
+            if (v > best) { best = v; arg = (int)i; }
+        }
+        bp[j] = (uint8_t)arg;
+        if (dn) dn[j] = best;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_bp_max(BpArgs a) {
+    __shared__ double su[kMaxLabels], sr[kMaxLabels], sl[kMaxLabels];
+    __shared__ double rv[4];
+    __shared__ int ri[4];
+    const int64_t npairs = (a.N - 1 + 1) / 2;
+    const int64_t b = blockIdx.x / npairs, k = blockIdx.x % npairs;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    const int64_t C = a.C, E = a.N - 1;
+    if (Eb == 0) {
+        if (k == 0 && threadIdx.x == 0) { a.zlast[b] = 0; a.score[b] = 0.f; }
+        return;
+    }
+    const int64_t tL = 2 * k, tR = 2 * k + 1;
+    if (tL >= Eb) return;
+    for (int64_t i = threadIdx.x; i < C; i += blockDim.x)
+        su[i] = a.u1 ? a.u1[(size_t)(b * a.nodes1 + k) * C + i] : 0.0;
+    __syncthreads();
+    const float* leafL = a.pot + (size_t)(b * E + tL) * C * C;
+    const bool right = tR < Eb;
+    // edge tL: delta_{tL} = u; its max gives delta_{tL+1} = delta_{tR}
+    backpointers(leafL, su, C, a.bp + (size_t)(b * E + tL) * C, sr);
+    __syncthreads();
+    const double* dlast = sr;
+    if (right) {
+        const float* leafR = a.pot + (size_t)(b * E + tR) * C * C;
+        backpointers(leafR, sr, C, a.bp + (size_t)(b * E + tR) * C, sl);
+        __syncthreads();
+        dlast = sl;
+    }
+    const int64_t tlast = right ? tR : tL;
+    if (tlast != Eb - 1) return;
+    // z_{L-1} = lowest argmax_j delta_{L-1}[j]
+    double best = -INFINITY;
+    int arg = 0x7fffffff;
+    for (int64_t j = threadIdx.x; j < C; j += blockDim.x) {
+        const double v = dlast[j];
+        if (v > best || (v == best && j < arg)) { best = v; arg = (int)j; }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const double ov = __shfl_xor(best, o, kWave);
+        const int oi = __shfl_xor(arg, o, kWave);
+        if (ov > best || (ov == best && oi < arg)) { best = ov; arg = oi; }
+    }
+    const int w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) { rv[w] = best; ri[w] = arg; }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int i = 1; i < nw; ++i)
+            if (rv[i] > best || (rv[i] == best && ri[i] < arg)) { best = rv[i]; arg = ri[i]; }
+        // every label ties at -inf when no sequence is finite: the lowest label, 0
+        if (arg >= C) arg = 0;
+        a.zlast[b] = arg;
+        a.score[b] = (float)best;
+    }
+}
+
+// ---- decode
+struct DecArgs {
+    const uint8_t* bp;
+    const int32_t* lengths;
+    int64_t N, C, chunk, nchunks;
+    uint8_t* map;       // [B, nchunks, C]
+    int32_t* zend;      // [B, nchunks]
+    const int32_t* zlast;
+    int32_t* path;      // [B, N]
+};
+
+// chunk c covers edges [c*K, min((c+1)*K, E_b)); it maps the label at position
+// e_c = min((c+1)*K, E_b) to the label at position s_c = c*K, for every label at e_c.
+__global__ __launch_bounds__(256) void k_dec_map(DecArgs a) {
+    extern __shared__ uint8_t sbp[];
+    const int64_t b = blockIdx.x / a.nchunks, c = blockIdx.x % a.nchunks;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1, E = a.N - 1;
+    const int64_t s = c * a.chunk;
+    if (s >= Eb) return;
+    const int64_t e = min((c + 1) * a.chunk, Eb);
+    const int64_t n = (e - s) * a.C;
+    const uint8_t* src = a.bp + (size_t)(b * E + s) * a.C;
+    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) sbp[i] = src[i];
+    __syncthreads();
+    const int64_t j = threadIdx.x;
+    if (j < a.C) {
+        int z = (int)j;
+        for (int64_t t = e - 1; t >= s; --t) z = sbp[(t - s) * a.C + z];
+        a.map[(size_t)(b * a.nchunks + c) * a.C + j] = (uint8_t)z;
+    }
+}
+
+// one wave per sequence: z at every chunk end, walking the chunk maps backwards
+__global__ __launch_bounds__(64) void k_dec_walk(DecArgs a) {
+    extern __shared__ uint8_t smap[];
+    const int64_t b = blockIdx.x;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    if (Eb == 0) {
+        if (threadIdx.x == 0) a.zend[b * a.nchunks] = 0;
+        return;
+    }
+    const int64_t last = (Eb - 1) / a.chunk;
+    const int64_t n = (last + 1) * a.C;
+    const uint8_t* src = a.map + (size_t)b * a.nchunks * a.C;
+    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) smap[i] = src[i];
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int z = a.zlast[b];
+        for (int64_t c = last; c >= 0; --c) {
+            a.zend[b * a.nchunks + c] = z;
+            z = smap[c * a.C + z];
+        }
+    }
+}
+
+// each chunk writes the labels of positions (s_c, e_c] (chunk 0 also position 0) and -1
+// for its positions at or past the length
+__global__ __launch_bounds__(64) void k_dec_emit(DecArgs a) {
+    extern __shared__ uint8_t sbp[];
+    const int64_t b = blockIdx.x / a.nchunks, c = blockIdx.x % a.nchunks;
+    const int64_t L = clamp_len(a.lengths, b, a.N), Eb = L - 1, E = a.N - 1;
+    const int64_t s = c * a.chunk;
+    int32_t* path = a.path + (size_t)b * a.N;
+    // positions s+1 .. min(s+K, N-1) that lie past the last token
+    for (int64_t n = s + 1 + threadIdx.x; n <= min(s + a.chunk, E); n += blockDim.x)
+        if (n >= L) path[n] = -1;
+    if (Eb == 0) {
+        if (c == 0 && threadIdx.x == 0) path[0] = a.zend[b * a.nchunks];
+        return;
+    }
+    if (s >= Eb) return;
+    const int64_t e = min((c + 1) * a.chunk, Eb);
+    const int64_t n = (e - s) * a.C;
+    const uint8_t* src = a.bp + (size_t)(b * E + s) * a.C;
+    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) sbp[i] = src[i];
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int z = a.zend[b * a.nchunks + c];
+        path[e] = z;
+        for (int64_t t = e - 1; t >= s; --t) {
+            z = sbp[(t - s) * a.C + z];
+            if (t > s || c == 0) path[t] = z;
+        }
+    }
+}
+
+inline int64_t round8(int64_t x) { return (x + 7) / 8 * 8; }
+
+}  // namespace
+
+hipError_t launch_viterbi_tree(const Plan& p, const float* pot, const int32_t* lengths,
+                               int32_t* path, float* score, hipStream_t s) {
+    const int64_t C = p.C;
+    const int ntm = (int)((C + kMT - 1) / kMT);
+    for (int l = 1; l <= p.D; ++l) {
+        UpMaxArgs a{};
+        a.leaves = (l == 1) ? pot : nullptr;
+        a.cnode = (l == 1) ? nullptr : p.mnode[l - 1];
+        a.cnodes = (l == 1) ? p.E : (p.Np >> (l - 1));
+        a.node = p.mnode[l];
+        a.nodes = p.Np >> l;
+        a.lengths = lengths; a.B = p.B; a.N = p.N; a.C = C; a.level = l; a.ntm = ntm;
+        a.nlogical = p.B * a.nodes * ntm * ntm;
+        a.ngrid = round8(a.nlogical);
+        hipLaunchKernelGGL(k_up_max, dim3((unsigned)a.ngrid), dim3(kMThreads), 0, s, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    for (int l = p.D; l >= 2; --l) {
+        DownMaxArgs d{};
+        d.uN = (l == p.D) ? nullptr : p.mu[l];
+        d.nodes = p.Np >> l;
+        d.cnode = p.mnode[l - 1];
+        d.cnodes = p.Np >> (l - 1);
+        d.uC = p.mu[l - 1];
+        d.lengths = lengths; d.N = p.N; d.C = C; d.level = l;
+        hipLaunchKernelGGL(k_down_max, dim3((unsigned)(p.B * d.nodes)), dim3(256), 0, s, d);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    BpArgs bpa{};
+    bpa.pot = pot;
+    bpa.u1 = (p.D >= 2) ? p.mu[1] : nullptr;
+    bpa.nodes1 = (p.D >= 1) ? (p.Np >> 1) : 1;
+    bpa.lengths = lengths; bpa.N = p.N; bpa.C = C; bpa.bp = p.bp; bpa.zlast = p.zlast;
+    bpa.score = score;
+    const int64_t npairs = (p.N - 1 + 1) / 2;
+    hipLaunchKernelGGL(k_bp_max, dim3((unsigned)(p.B * npairs)), dim3(256), 0, s, bpa);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+
+    DecArgs d{};
+    d.bp = p.bp; d.lengths = lengths; d.N = p.N; d.C = C; d.chunk = p.dec_chunk;
+    d.nchunks = p.dec_nchunks; d.map = p.dec_map; d.zend = p.dec_zend; d.zlast = p.zlast;
+    d.path = path;
+    const size_t chunk_bytes = (size_t)p.dec_chunk * C;
+    hipLaunchKernelGGL(k_dec_map, dim3((unsigned)(p.B * p.dec_nchunks)), dim3(256), chunk_bytes,
+                       s, d);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_dec_walk, dim3((unsigned)p.B), dim3(64), (size_t)p.dec_nchunks * C, s, d);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_dec_emit, dim3((unsigned)(p.B * p.dec_nchunks)), dim3(64), chunk_bytes,
+                       s, d);
+    return hipGetLastError();
+}
+
+}  // namespace tsc

@@ -1,0 +1,60 @@
+"""Helpers for the GPU parity tests: run the HIP path through the binding (which calls
+the C ABI) and compare with the float64 oracle to the stated tolerances."""
+import sys
+import time
+
+import numpy as np
+
+LOGZ_RTOL = 1e-5     # log Z and Viterbi score: relative (guarded by max(|ref|, 1))
+MARG_ATOL = 1e-5     # marginals: absolute
+
+
+def say(msg):
+    print(f"[{time.strftime('%H:%M:%S')}] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def gpu_all(pot, lens, device="cuda:0"):
+    import torch
+    from paper_2002_00876_amd import binding
+    tp = torch.from_numpy(np.ascontiguousarray(pot)).to(device)
+    tl = torch.from_numpy(np.ascontiguousarray(lens)).to(device)
+    z = binding.logpartition(tp, tl)
+    z2, m = binding.marginals(tp, tl)
+    path, score = binding.viterbi(tp, tl)
+    torch.cuda.synchronize()
+    return (z.cpu().numpy(), z2.cpu().numpy(), m.cpu().numpy(), path.cpu().numpy(),
+            score.cpu().numpy())
+
+
+def check_logz(got, ref, what="logZ"):
+    got = np.asarray(got, np.float64)
+    inf = np.isinf(ref)
+    assert np.array_equal(got[inf], ref[inf]), f"{what}: infinities differ"
+    fin = ~inf
+    err = np.abs(got[fin] - ref[fin]) / np.maximum(np.abs(ref[fin]), 1.0)
+    assert err.size == 0 or err.max() <= LOGZ_RTOL, f"{what}: max rel err {err.max():.3e}"
+
+
+def check_marg(got, ref, lens):
+    B = got.shape[0]
+    for b in range(B):
+        E = int(lens[b]) - 1
+        assert np.all(got[b, E:] == 0), f"padding edges of sequence {b} are not exactly 0"
+    err = np.abs(got.astype(np.float64) - ref)
+    assert err.max(initial=0.0) <= MARG_ATOL, f"marginals: max abs err {err.max():.3e}"
+    return err.max(initial=0.0)
+
+
+def check_all(pot, lens, tag=""):
+    import oracle
+    say(f"case {tag}: B={pot.shape[0]} N={pot.shape[1] + 1} C={pot.shape[2]}")
+    z, z2, m, path, score = gpu_all(pot, lens)
+    zo, mo = oracle.marginals(pot, lens)
+    po, so = oracle.viterbi(pot, lens)
+    check_logz(z, zo)
+    check_logz(z2, zo, "logZ (marginals call)")
+    e = check_marg(m, mo, lens)
+    assert np.array_equal(path, po), f"Viterbi path mismatch in sequences {np.nonzero((path != po).any(1))[0]}"
+    check_logz(score, so, "score")
+    return e

@@ -1,0 +1,103 @@
+"""Host-side checks of the C-ABI library: it loads, exports every entry point that
+include/ts_chain.h declares, sizes workspaces, and rejects bad arguments with the
+documented status codes before touching the device (no compute call is made here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2002_00876_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ts_chain.h")
+
+FAKE = 0x10000          # 256-aligned, never dereferenced: every call below fails validation
+TS_OK, NULL_ARG, BAD_DIM, WORKSPACE = 0, -1, -2, -3
+
+
+@pytest.fixture(scope="module")
+def L():
+    return binding.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ts_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_three_calls():
+    names = declared_functions()
+    for n in ("ts_chain_logpartition", "ts_chain_marginals", "ts_chain_viterbi",
+              "ts_chain_workspace_bytes", "ts_last_error", "ts_chain_max_labels"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+        assert ctypes.cast(getattr(L, name), ctypes.c_void_p).value
+
+
+def test_max_labels(L):
+    assert L.ts_chain_max_labels() == 256
+
+
+def test_workspace_sizes(L):
+    ws = binding.workspace_bytes
+    assert ws(0, 4, 1, 20) == 0 and ws(1, 4, 1, 20) == 0 and ws(2, 4, 1, 20) == 0
+    for op in (0, 1, 2):
+        assert ws(op, 32, 25, 20) > 0
+        assert ws(op, 32, 25, 20) % 256 == 0
+        assert ws(op, 64, 25, 20) > ws(op, 32, 25, 20)
+        assert ws(op, 32, 50, 20) > ws(op, 32, 25, 20)
+    # marginals need the log-partition buffers plus the outside vectors
+    assert ws(1, 32, 25, 20) > ws(0, 32, 25, 20)
+    # the tree over N-1 = 24 edges has levels of 16, 8, 4, 2, 1 nodes of C*C floats
+    core = 32 * (16 + 8 + 4 + 2 + 1) * 20 * 20 * 4
+    assert ws(0, 32, 25, 20) >= core
+    assert ws(3, 32, 25, 20) == 0 and ws(0, 0, 25, 20) == 0 and ws(0, 1, 25, 257) == 0
+
+
+def _err(L):
+    return L.ts_last_error().decode()
+
+
+def test_bad_dimensions_are_rejected(L):
+    for B, N, C in [(0, 5, 3), (2, 0, 3), (2, 5, 0), (2, 5, 257), (-1, 5, 3)]:
+        assert L.ts_chain_logpartition(FAKE, None, B, N, C, FAKE, FAKE, 1 << 30, None) == BAD_DIM
+        assert L.ts_chain_marginals(FAKE, None, B, N, C, FAKE, FAKE, FAKE, 1 << 30, None) == BAD_DIM
+        assert L.ts_chain_viterbi(FAKE, None, B, N, C, FAKE, FAKE, FAKE, 1 << 30, None) == BAD_DIM
+    assert "ts_chain_max_labels" in _err(L) or "must" in _err(L)
+
+
+def test_size_overflow_is_rejected(L):
+    assert L.ts_chain_logpartition(FAKE, None, 1 << 40, 1 << 20, 256, FAKE, FAKE, 1, None) == BAD_DIM
+    assert "overflow" in _err(L)
+
+
+def test_null_pointers_are_rejected(L):
+    need = binding.workspace_bytes(0, 2, 5, 3)
+    assert L.ts_chain_logpartition(None, None, 2, 5, 3, FAKE, FAKE, need, None) == NULL_ARG
+    assert "pot" in _err(L)
+    assert L.ts_chain_logpartition(FAKE, None, 2, 5, 3, None, FAKE, need, None) == NULL_ARG
+    assert "logZ" in _err(L)
+    assert L.ts_chain_logpartition(FAKE, None, 2, 5, 3, FAKE, None, need, None) == NULL_ARG
+    need = binding.workspace_bytes(1, 2, 5, 3)
+    assert L.ts_chain_marginals(FAKE, None, 2, 5, 3, FAKE, None, FAKE, need, None) == NULL_ARG
+    assert "marg" in _err(L)
+    need = binding.workspace_bytes(2, 2, 5, 3)
+    assert L.ts_chain_viterbi(FAKE, None, 2, 5, 3, None, FAKE, FAKE, need, None) == NULL_ARG
+    assert L.ts_chain_viterbi(FAKE, None, 2, 5, 3, FAKE, None, FAKE, need, None) == NULL_ARG
+
+
+def test_small_or_misaligned_workspace_is_rejected(L):
+    for op, fn in ((0, "logpartition"), (1, "marginals"), (2, "viterbi")):
+        need = binding.workspace_bytes(op, 4, 9, 7)
+        f = getattr(L, "ts_chain_" + fn)
+        args = {0: (FAKE,), 1: (FAKE, FAKE), 2: (FAKE, FAKE)}[op]
+        assert f(FAKE, None, 4, 9, 7, *args, FAKE, need - 1, None) == WORKSPACE
+        assert "workspace too small" in _err(L)
+        assert f(FAKE, None, 4, 9, 7, *args, FAKE + 16, need, None) == WORKSPACE
+        assert "aligned" in _err(L)
