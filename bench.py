@@ -1,0 +1,202 @@
+"""Benchmark: tokens/s of batched linear-chain CRF inference on one MI355X.
+
+One step is one pass of the whole hot path over one batch: ts_chain_marginals (log Z and
+edge marginals: tree up-sweep, root, outside sweep, per-edge marginals) followed by
+ts_chain_viterbi (max-plus tree, backpointers, backtrace).  Inputs, outputs and
+workspaces are resident in HBM before the timed region.  Prints one JSON line.
+
+Default workload: the paper-shaped batch (B=32, N=25, C=20, N(0,1) potentials, lengths
+uniform in [13, 25]).  --workload selects another of the five seeded workloads.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK = 8.0e12          # bytes/s
+MFMA_F32_PEAK = 157.3e12   # flop/s, dense fp32 matrix
+VALU_F64_PEAK = 78.6e12    # flop/s, fp64 vector
+
+PAPER_CONTEXT_TOKENS_PER_S = 390e3   # Table 1, K80, batch 32, N=25, C=20 (context only)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="paper",
+                    choices=["tiny", "paper", "mid", "hmm", "long"])
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="bound on the oracle's CPU-baseline run (0 disables it)")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="only run a plain device copy of this size (traffic-counter scale)")
+    return ap.parse_args()
+
+
+def algorithmic(pot, lens):
+    """Algorithmic HBM bytes and semiring work of one call of each entry point."""
+    B, E, C, _ = pot.shape
+    Eb = (lens.astype("int64") - 1)
+    valid = int(Eb.sum())
+    products = int((Eb - 1).clip(min=0).sum())          # tree products, C^3 pairs each
+    marg_bytes = 4 * C * C * valid + 4 * C * C * B * E + 4 * B      # read valid, write all
+    vit_bytes = 4 * C * C * valid + 4 * B * (E + 1) + 4 * B          # read valid, path+score
+    pairs = products * C ** 3
+    return dict(marg_bytes=marg_bytes, vit_bytes=vit_bytes, pairs=pairs,
+                marg_flops=2 * pairs, vit_ops=2 * pairs, valid_edges=valid)
+
+
+def cpu_baseline(pot, lens, seconds):
+    import oracle
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.marginals(pot, lens)
+        oracle.viterbi(pot, lens)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    B, E = pot.shape[0], pot.shape[1]
+    return {"value": B * (E + 1) * reps / el, "unit": "tokens/s",
+            "cores": min(oracle.max_threads(), B), "kind": "oracle",
+            "sample": f"the full batch, oracle marginals + Viterbi repeated {reps}x "
+                      f"({el:.1f} s, float64, OpenMP over sequences)"}
+
+
+def calibrate_copy(mib):
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.randn(n, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4}))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2002_00876_amd import binding, workloads
+
+    if args.calibrate_copy_mib:
+        calibrate_copy(args.calibrate_copy_mib)
+        return
+    binding.lib()   # fail loudly if the HIP library is missing
+    w = workloads.WORKLOADS[args.workload]
+    pot_h, lens_h = workloads.generate(w)
+    dev = torch.device("cuda:0")
+    pot = torch.from_numpy(pot_h).to(dev)
+    lens = torch.from_numpy(lens_h).to(dev)
+    B, E, C, _ = pot.shape
+    N = E + 1
+    logz = torch.empty(B, dtype=torch.float32, device=dev)
+    marg = torch.empty_like(pot)
+    path = torch.empty((B, N), dtype=torch.int32, device=dev)
+    score = torch.empty(B, dtype=torch.float32, device=dev)
+    ws_m = binding._workspace(binding.OP_MARGINALS, B, N, C, dev)[0]
+    ws_v = binding._workspace(binding.OP_VITERBI, B, N, C, dev)[0]
+    stream = torch.cuda.current_stream(dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        binding.marginals(pot, lens, out=(logz, marg), ws=ws_m)
+        if ev is not None:
+            ev[1].record(stream)
+        binding.viterbi(pot, lens, out=(path, score), ws=ws_v)
+        if ev is not None:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # per-call events inside the timed region: [marginals] [viterbi]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for k in range(args.steps):
+        step(evs[k])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_step = total_ms / args.steps
+    ms_marg = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    ms_vit = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+
+    alg = algorithmic(pot_h, lens_h)
+    tokens = B * N
+    value = tokens / (ms_step * 1e-3)
+
+    # dominant call: the slower of the two; each is one kernel launch on the fused path
+    fused = binding.workspace_bytes(binding.OP_MARGINALS, B, N, C) == 0
+    if ms_marg >= ms_vit:
+        dom, dom_ms, dom_bytes = "k_small_log" if fused else "ts_chain_marginals", ms_marg, alg["marg_bytes"]
+        comp_time = alg["marg_flops"] / MFMA_F32_PEAK
+    else:
+        dom, dom_ms, dom_bytes = "k_small_max" if fused else "ts_chain_viterbi", ms_vit, alg["vit_bytes"]
+        comp_time = alg["vit_ops"] / VALU_F64_PEAK
+    mem_time = dom_bytes / HBM_PEAK
+    if mem_time >= comp_time:
+        achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK / 1e9,
+                "unit": "GB/s", "frac": round(achieved / (HBM_PEAK / 1e9), 5), "traffic": None}
+    else:
+        ops = alg["marg_flops"] if dom.endswith("log") or dom.endswith("marginals") else alg["vit_ops"]
+        achieved = ops / (dom_ms * 1e-3) / 1e12
+        peak = MFMA_F32_PEAK if "log" in dom or "marginals" in dom else VALU_F64_PEAK
+        roof = {"bound": "mfma" if peak == MFMA_F32_PEAK else "alu", "achieved": round(achieved, 3),
+                "peak": peak / 1e12, "unit": "TFLOP/s", "frac": round(achieved / (peak / 1e12), 5),
+                "traffic": None}
+    roof["kernel"] = dom
+    roof["kernel_ms"] = round(dom_ms, 5)
+    roof["algorithmic_bytes"] = dom_bytes
+
+    out = {
+        "metric": "tokens/sec for linear-chain logZ+marginals (B,N,C); % of HBM/compute roofline",
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: B={B} N={N} C={C}", "B": B, "N": N, "C": C,
+                   "lengths": "uniform" if w.len_range else "fixed",
+                   "step": "ts_chain_marginals + ts_chain_viterbi",
+                   "path": "fused single launch per call" if fused else "multi-launch tree"},
+        "breakdown": {"marginals_ms": round(ms_marg, 5), "viterbi_ms": round(ms_vit, 5),
+                      "marginals_tokens_per_s": round(tokens / (ms_marg * 1e-3), 1),
+                      "valid_tokens_per_s": round(float(lens_h.sum()) / (ms_step * 1e-3), 1)},
+        "dtype_note": "log semiring in fp32 (fp32 MFMA, float64 row/column offsets); "
+                      "Viterbi max-plus in float64",
+        "paper_context": {"tokens_per_s": PAPER_CONTEXT_TOKENS_PER_S,
+                          "note": "Table 1, K80, B=32 N=25 C=20; not the same metric"},
+        "roofline": roof,
+    }
+    if args.cpu_seconds > 0:
+        out["cpu_baseline"] = cpu_baseline(pot_h, lens_h, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

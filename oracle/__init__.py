@@ -47,6 +47,7 @@ def load_library(path):
     for name in ("orc_viterbi", "orc_viterbi_f64"):
         getattr(lib, name).argtypes = [p, p, i64, i64, i64, p, p]
     lib.orc_marginals_seq.argtypes = [p, p, i64, i64, i64, i64, i64, i64, p, p]
+    lib.orc_max_threads.restype = ctypes.c_int
     return lib
 
 
@@ -128,3 +129,8 @@ def marginals_seq(pot, lengths, b, t0, t1):
     _check(_load().orc_marginals_seq(_ptr(pot), _ptr(lengths), B, N, C, b, t0, t1, _ptr(out),
                                      ctypes.addressof(logz)))
     return out, logz.value
+
+
+def max_threads():
+    """OpenMP threads available to the oracle's parallel loops."""
+    return _load().orc_max_threads()

@@ -30,6 +30,7 @@
  * exactly on read.  Viterbi compares float64 sums exactly.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -226,6 +227,9 @@ static int viterbi_impl(const float* pf, const double* pd, const int32_t* length
 }
 
 /* ---------------- exported entry points ---------------- */
+
+/* OpenMP threads a parallel region of the oracle may use */
+int orc_max_threads(void) { return omp_get_max_threads(); }
 
 /* fp32 potentials, widened exactly */
 int orc_logpartition(const float* pot, const int32_t* lengths, int64_t B, int64_t N, int64_t C,

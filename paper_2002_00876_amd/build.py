@@ -12,6 +12,8 @@ HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     # hand-written code must not be turned into packed fp32 VALU ops
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # NaN inputs are undefined (infinities are honoured): lets fmax map to one v_max
+    "-fno-honor-nans",
     "-Wall",
 ]
 

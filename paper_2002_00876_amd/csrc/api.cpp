@@ -9,6 +9,7 @@
 #include <vector>
 
 #include "internal.h"
+#include "small.h"
 #include "ts_chain.h"
 
 namespace tsc {
@@ -53,6 +54,14 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p) {
         !mul_ok(cc, 8, &cc) || cc > ((int64_t)1 << 60))
         return false;
     if (N == 1) return true;  // no edges: no workspace
+    // small label sets: one fused launch per call, tree kept in LDS, no workspace.
+    // TS_PATH=tree forces the multi-launch tree (used by the tests to cover both paths).
+    const char* path = std::getenv("TS_PATH");
+    const bool force_tree = path && std::strcmp(path, "tree") == 0;
+    if (!force_tree && small_path_fits(N, C)) {
+        p->fused = true;
+        return true;
+    }
     int64_t Np = 1;
     int D = 0;
     while (Np < p->E) { Np <<= 1; ++D; }
@@ -170,6 +179,7 @@ ts_status ts_chain_logpartition(const float* pot, const int32_t* lengths, int64_
     if ((st = check_lengths(lengths, B, N, s)) != TS_OK) return st;
     if (N == 1) return hip_status(launch_single_token(B, N, C, TS_OP_LOGPARTITION, logZ,
                                                       nullptr, nullptr, s));
+    if (p.fused) return hip_status(launch_small_log(pot, lengths, B, N, C, logZ, nullptr, s));
     return hip_status(launch_logz_tree(p, pot, lengths, logZ, s));
 }
 
@@ -187,6 +197,7 @@ ts_status ts_chain_marginals(const float* pot, const int32_t* lengths, int64_t B
         return hip_status(launch_single_token(B, N, C, TS_OP_LOGPARTITION, logZ, nullptr,
                                               nullptr, s));
     }
+    if (p.fused) return hip_status(launch_small_log(pot, lengths, B, N, C, logZ, marg, s));
     // up-sweep (and log Z when requested), then the outside sweep and the marginals
     hipError_t e = launch_logz_tree(p, pot, lengths, logZ, s);
     if (e != hipSuccess) return hip_status(e);
@@ -204,6 +215,7 @@ ts_status ts_chain_viterbi(const float* pot, const int32_t* lengths, int64_t B, 
     if ((st = check_lengths(lengths, B, N, s)) != TS_OK) return st;
     if (N == 1)
         return hip_status(launch_single_token(B, N, C, TS_OP_VITERBI, nullptr, path, score, s));
+    if (p.fused) return hip_status(launch_small_max(pot, lengths, B, N, C, path, score, s));
     return hip_status(launch_viterbi_tree(p, pot, lengths, path, score, s));
 }
 

@@ -32,6 +32,35 @@ __device__ __forceinline__ double wave_max_d(double x) {
     return x;
 }
 
+// Full-wave reductions with DPP inside each row of 16 lanes and readlane across the four
+// rows: the result is wave-uniform and the order of operations is fixed (deterministic).
+__device__ __forceinline__ float dpp_f(float x, int ctrl) {
+    const int v = __float_as_int(x);
+    switch (ctrl) {
+        case 0xB1: return __int_as_float(__builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false));
+        case 0x4E: return __int_as_float(__builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false));
+        case 0x141: return __int_as_float(__builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false));
+        default: return __int_as_float(__builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false));
+    }
+}
+__device__ __forceinline__ float rl(float x, int lane) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), lane));
+}
+__device__ __forceinline__ float wave_max_fast(float x) {
+    x = fmaxf(x, dpp_f(x, 0xB1));   // lanes i ^ 1
+    x = fmaxf(x, dpp_f(x, 0x4E));   // lanes i ^ 2
+    x = fmaxf(x, dpp_f(x, 0x141));  // mirror within 8
+    x = fmaxf(x, dpp_f(x, 0x140));  // mirror within 16
+    return fmaxf(fmaxf(rl(x, 0), rl(x, 16)), fmaxf(rl(x, 32), rl(x, 48)));
+}
+__device__ __forceinline__ float wave_sum_fast(float x) {
+    x += dpp_f(x, 0xB1);
+    x += dpp_f(x, 0x4E);
+    x += dpp_f(x, 0x141);
+    x += dpp_f(x, 0x140);
+    return (rl(x, 0) + rl(x, 16)) + (rl(x, 32) + rl(x, 48));
+}
+
 // Online log-sum-exp state: value = m + log(s).  m = -inf means the empty sum.
 struct Lse {
     float m, s;

@@ -25,6 +25,7 @@ struct Plan {
     int64_t B = 0, N = 0, C = 0, E = 0, Np = 1;
     int D = 0;
     int op = 0;
+    bool fused = false;   // single-launch path of small.hip (no workspace)
     // log semiring, levels 1..D (index by level)
     float* core[kMaxLevels] = {};
     double* ro[kMaxLevels] = {};

@@ -10,6 +10,17 @@ from paper_2002_00876_amd import workloads as W
 pytestmark = pytest.mark.gpu
 
 
+@pytest.fixture(params=["auto", "tree"], autouse=True)
+def path_mode(request, monkeypatch):
+    """Run every case through the default dispatch (the fused single-launch kernels for
+    C <= 32) and through the multi-launch tree forced by TS_PATH=tree."""
+    if request.param == "tree":
+        monkeypatch.setenv("TS_PATH", "tree")
+    else:
+        monkeypatch.delenv("TS_PATH", raising=False)
+    return request.param
+
+
 @pytest.mark.parametrize("name", ["tiny", "paper"])
 def test_named_small_workloads(name):
     pot, lens = W.generate(name)
