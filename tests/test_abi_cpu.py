@@ -14,6 +14,9 @@ HEADER = os.path.join(ROOT, "include", "ts_chain.h")
 
 FAKE = 0x10000          # 256-aligned, never dereferenced: every call below fails validation
 TS_OK, NULL_ARG, BAD_DIM, WORKSPACE = 0, -1, -2, -3
+# C = 40 takes the multi-launch tree, which needs a workspace; the fused path (C <= 32)
+# needs none.  Every call here must fail validation before anything is launched.
+CW = 40
 
 
 @pytest.fixture(scope="module")
@@ -44,20 +47,24 @@ def test_max_labels(L):
     assert L.ts_chain_max_labels() == 256
 
 
-def test_workspace_sizes(L):
+def test_workspace_sizes(L, monkeypatch):
     ws = binding.workspace_bytes
     assert ws(0, 4, 1, 20) == 0 and ws(1, 4, 1, 20) == 0 and ws(2, 4, 1, 20) == 0
     for op in (0, 1, 2):
-        assert ws(op, 32, 25, 20) > 0
-        assert ws(op, 32, 25, 20) % 256 == 0
-        assert ws(op, 64, 25, 20) > ws(op, 32, 25, 20)
-        assert ws(op, 32, 50, 20) > ws(op, 32, 25, 20)
+        assert ws(op, 32, 25, 20) == 0          # fused single-launch path: LDS only
+        assert ws(op, 32, 25, CW) > 0
+        assert ws(op, 32, 25, CW) % 256 == 0
+        assert ws(op, 64, 25, CW) > ws(op, 32, 25, CW)
+        assert ws(op, 32, 50, CW) > ws(op, 32, 25, CW)
     # marginals need the log-partition buffers plus the outside vectors
-    assert ws(1, 32, 25, 20) > ws(0, 32, 25, 20)
+    assert ws(1, 32, 25, CW) > ws(0, 32, 25, CW)
     # the tree over N-1 = 24 edges has levels of 16, 8, 4, 2, 1 nodes of C*C floats
-    core = 32 * (16 + 8 + 4 + 2 + 1) * 20 * 20 * 4
-    assert ws(0, 32, 25, 20) >= core
+    core = 32 * (16 + 8 + 4 + 2 + 1) * CW * CW * 4
+    assert ws(0, 32, 25, CW) >= core
     assert ws(3, 32, 25, 20) == 0 and ws(0, 0, 25, 20) == 0 and ws(0, 1, 25, 257) == 0
+    # TS_PATH=tree forces the multi-launch tree for small C too
+    monkeypatch.setenv("TS_PATH", "tree")
+    assert ws(0, 32, 25, 20) >= 32 * (16 + 8 + 4 + 2 + 1) * 20 * 20 * 4
 
 
 def _err(L):
@@ -78,26 +85,30 @@ def test_size_overflow_is_rejected(L):
 
 
 def test_null_pointers_are_rejected(L):
-    need = binding.workspace_bytes(0, 2, 5, 3)
-    assert L.ts_chain_logpartition(None, None, 2, 5, 3, FAKE, FAKE, need, None) == NULL_ARG
+    need = binding.workspace_bytes(0, 2, 5, CW)
+    assert L.ts_chain_logpartition(None, None, 2, 5, CW, FAKE, FAKE, need, None) == NULL_ARG
     assert "pot" in _err(L)
-    assert L.ts_chain_logpartition(FAKE, None, 2, 5, 3, None, FAKE, need, None) == NULL_ARG
+    assert L.ts_chain_logpartition(FAKE, None, 2, 5, CW, None, FAKE, need, None) == NULL_ARG
     assert "logZ" in _err(L)
-    assert L.ts_chain_logpartition(FAKE, None, 2, 5, 3, FAKE, None, need, None) == NULL_ARG
-    need = binding.workspace_bytes(1, 2, 5, 3)
-    assert L.ts_chain_marginals(FAKE, None, 2, 5, 3, FAKE, None, FAKE, need, None) == NULL_ARG
+    assert L.ts_chain_logpartition(FAKE, None, 2, 5, CW, FAKE, None, need, None) == NULL_ARG
+    assert "ws" in _err(L)
+    need = binding.workspace_bytes(1, 2, 5, CW)
+    assert L.ts_chain_marginals(FAKE, None, 2, 5, CW, FAKE, None, FAKE, need, None) == NULL_ARG
     assert "marg" in _err(L)
-    need = binding.workspace_bytes(2, 2, 5, 3)
-    assert L.ts_chain_viterbi(FAKE, None, 2, 5, 3, None, FAKE, FAKE, need, None) == NULL_ARG
-    assert L.ts_chain_viterbi(FAKE, None, 2, 5, 3, FAKE, None, FAKE, need, None) == NULL_ARG
+    need = binding.workspace_bytes(2, 2, 5, CW)
+    assert L.ts_chain_viterbi(FAKE, None, 2, 5, CW, None, FAKE, FAKE, need, None) == NULL_ARG
+    assert L.ts_chain_viterbi(FAKE, None, 2, 5, CW, FAKE, None, FAKE, need, None) == NULL_ARG
+    # the fused path (no workspace) still rejects missing outputs
+    assert L.ts_chain_marginals(FAKE, None, 2, 5, 3, FAKE, None, None, 0, None) == NULL_ARG
+    assert L.ts_chain_viterbi(FAKE, None, 2, 5, 3, None, FAKE, None, 0, None) == NULL_ARG
 
 
 def test_small_or_misaligned_workspace_is_rejected(L):
     for op, fn in ((0, "logpartition"), (1, "marginals"), (2, "viterbi")):
-        need = binding.workspace_bytes(op, 4, 9, 7)
+        need = binding.workspace_bytes(op, 4, 9, CW)
         f = getattr(L, "ts_chain_" + fn)
         args = {0: (FAKE,), 1: (FAKE, FAKE), 2: (FAKE, FAKE)}[op]
-        assert f(FAKE, None, 4, 9, 7, *args, FAKE, need - 1, None) == WORKSPACE
+        assert f(FAKE, None, 4, 9, CW, *args, FAKE, need - 1, None) == WORKSPACE
         assert "workspace too small" in _err(L)
-        assert f(FAKE, None, 4, 9, 7, *args, FAKE + 16, need, None) == WORKSPACE
+        assert f(FAKE, None, 4, 9, CW, *args, FAKE + 16, need, None) == WORKSPACE
         assert "aligned" in _err(L)
