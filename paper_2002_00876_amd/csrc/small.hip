@@ -35,6 +35,8 @@ __device__ __forceinline__ double& Dd(int off_floats) {
     return reinterpret_cast<double*>(ts_small_lds)[off_floats >> 1];
 }
 __device__ __forceinline__ int align4(int off) { return (off + 3) & ~3; }
+// values that are the same in every lane, moved to scalar registers
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 __device__ __forceinline__ void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -108,18 +110,26 @@ struct LogLayout {
     __device__ int ro(int h) const { return h < 0 ? -1 : slots + h * slotF + ((CC + 1) & ~1); }
 };
 
-// One wave: P = L (x) R, exp-shifted fp32 MFMA product, C <= CP <= 32 (loops over the
-// padded size CP unroll completely).
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+// A team of TS waves computes P = L (x) R, the exp-shifted fp32 MFMA product, for
+// C <= CP <= 32:
 //   A'[a][b] = L[a][b] + (co_L[b] - max co_L), B'[b][c] = R[b][c] + (ro_R[b] - max ro_R)
 //   S = sum_b exp(A' - rowmax) exp(B' - colmax); core_P = log S (exact fallback when S
 //   underflows), ro_P = ro_L + max co_L + rowmax, co_P = co_R + max ro_R + colmax.
-// The offset shifts only need to be near the maximum, so they are reduced in fp32.
-template <int CP>
-__device__ void wave_product_log(const LogLayout& ly, int Lc, int Lro, int Rc, int Rro, int Pc,
-                                 int Pro, int scr) {
-    const int C = ly.C;
+// The output is cut into 16 x 16 blocks (one for CP <= 16, four for CP = 32); team member
+// `mem` computes blocks mem, mem + TS, ... with v_mfma_f32_16x16x4f32.  Every member
+// derives the shifts and row/column maxima itself (same inputs, same results), so the team
+// needs no synchronisation.  The offset shifts only need to be near the maximum, so they
+// are reduced in fp32.
+template <int CP, int TS>
+__device__ __attribute__((noinline)) void team_product_log(const LogLayout& ly, int Lc, int Lro, int Rc, int Rro, int Pc,
+                                 int Pro, int mem, int scr) {
+    constexpr int kNB = CP <= 16 ? 1 : 4;      // 16 x 16 output blocks
+    const int C = uni(ly.C);
+    Lc = uni(Lc); Lro = uni(Lro); Rc = uni(Rc); Rro = uni(Rro); Pc = uni(Pc); Pro = uni(Pro);
+    mem = uni(mem); scr = uni(scr);
     const int lane = threadIdx.x % kWave;
-    const int i = lane & 31, h = lane >> 5;
     const int coh = scr, roh = scr + 32, rA = scr + 64, cB = scr + 96;
     double lm = -INFINITY, rm = -INFINITY;
     if (lane < C) {
@@ -135,6 +145,7 @@ __device__ void wave_product_log(const LogLayout& ly, int Lc, int Lro, int Rc, i
     wave_sync();
     // lanes 0-31: maxima of the rows of A'; lanes 32-63: maxima of the columns of B'
     {
+        const int i = lane & 31, h = lane >> 5;
         const int ic = min(i, C - 1);
         const int base = h == 0 ? Lc + ic * C : Rc + ic;
         const int stride = h == 0 ? 1 : C;
@@ -146,55 +157,68 @@ __device__ void wave_product_log(const LogLayout& ly, int Lc, int Lro, int Rc, i
         F((h == 0 ? rA : cB) + i) = (i < C) ? m : -INFINITY;
     }
     wave_sync();
-    const bool row_ok = i < C;
-    const int ic = row_ok ? i : 0;
-    const float sa = safe_shift(F(rA + ic)), sb = safe_shift(F(cB + ic));
-    f16v acc;
+    const int l16 = lane & 15, kq = lane >> 4;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    for (int blk = mem; blk < kNB; blk += TS) {
+        const int r0 = (blk >> 1) * 16, c0 = (blk & 1) * 16;
+        const int ia = r0 + l16, jb = c0 + l16;
+        const int iac = min(ia, C - 1), jbc = min(jb, C - 1);
+        const float sa = safe_shift(F(rA + iac)), sb = safe_shift(F(cB + jbc));
+        f4v acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kk = 0; kk < CP; kk += 2) {
-        if (kk < C) {
-            const int k = kk + h;
-            const bool ok = row_ok && k < C;
-            const int kc = ok ? k : 0;
-            const float ea = __expf(F(Lc + ic * C + kc) + F(coh + kc) - sa);
-            const float eb = __expf(F(Rc + kc * C + ic) + F(roh + kc) - sb);
-            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(ok ? ea : 0.f, ok ? eb : 0.f, acc, 0, 0, 0);
-        }
-    }
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        const int row = (r >> 2) * 8 + h * 4 + (r & 3), col = i;
-        if (row < C && col < C) {
-            const float S = acc[r];
-            float val;
-            if (S >= kUnderflow) {
-                val = __logf(S);
-            } else {
-                const float ra = safe_shift(F(rA + row)), cb = safe_shift(F(cB + col));
-                float q = -INFINITY;
-                for (int k = 0; k < C; ++k)
-                    q = fmaxf(q, (F(Lc + row * C + k) + F(coh + k) - ra) +
-                                     (F(Rc + k * C + col) + F(roh + k) - cb));
-                if (q == -INFINITY) {
-                    val = -INFINITY;
-                } else {
-                    float s = 0.f;
-                    for (int k = 0; k < C; ++k)
-                        s += __expf((F(Lc + row * C + k) + F(coh + k) - ra) +
-                                    (F(Rc + k * C + col) + F(roh + k) - cb) - q);
-                    val = q + __logf(s);
-                }
+        for (int kk = 0; kk < CP; kk += 4) {
+            if (kk < C) {
+                const int k = kk + kq;
+                const int kc = min(k, C - 1);
+                const float ea = __expf(F(Lc + iac * C + kc) + F(coh + kc) - sa);
+                const float eb = __expf(F(Rc + kc * C + jbc) + F(roh + kc) - sb);
+                const bool ka = k < C;
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32((ka && ia < C) ? ea : 0.f,
+                                                           (ka && jb < C) ? eb : 0.f, acc, 0, 0, 0);
             }
-            F(Pc + row * C + col) = val;
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int row = r0 + 4 * kq + r, col = jb;
+            if (row < C && col < C) {
+                const float S = acc[r];
+                float val;
+                if (S >= kUnderflow) {
+                    val = __logf(S);
+                } else {
+                    const float ra = safe_shift(F(rA + row)), cb = safe_shift(F(cB + col));
+                    float q = -INFINITY;
+                    for (int k = 0; k < C; ++k)
+                        q = fmaxf(q, (F(Lc + row * C + k) + F(coh + k) - ra) +
+                                         (F(Rc + k * C + col) + F(roh + k) - cb));
+                    if (q == -INFINITY) {
+                        val = -INFINITY;
+                    } else {
+                        float s = 0.f;
+                        for (int k = 0; k < C; ++k)
+                            s += __expf((F(Lc + row * C + k) + F(coh + k) - ra) +
+                                        (F(Rc + k * C + col) + F(roh + k) - cb) - q);
+                        val = q + __logf(s);
+                    }
+                }
+                F(Pc + row * C + col) = val;
+            }
         }
     }
-    if (h == 0 && i < C) {
-        Dd(Pro + 2 * i) = (Lro >= 0 ? Dd(Lro + 2 * i) : 0.0) + coLs + (double)sa;
-        Dd(Pro + 2 * C + 2 * i) = (Rro >= 0 ? Dd(Rro + 2 * C + 2 * i) : 0.0) + roRs + (double)sb;
+    if (mem == 0 && lane < C) {
+        Dd(Pro + 2 * lane) =
+            (Lro >= 0 ? Dd(Lro + 2 * lane) : 0.0) + coLs + (double)safe_shift(F(rA + lane));
+        Dd(Pro + 2 * C + 2 * lane) =
+            (Rro >= 0 ? Dd(Rro + 2 * C + 2 * lane) : 0.0) + roRs + (double)safe_shift(F(cB + lane));
     }
     wave_sync();
+}
+
+// team size for a level with np products on kSmallWaves waves: the largest power of two
+// <= waves / np, at most 4
+__device__ __forceinline__ int team_size(int np) {
+    const int per = kSmallWaves / max(np, 1);
+    return per >= 4 ? 4 : (per >= 2 ? 2 : 1);
 }
 
 // One wave, C <= CP <= 32.  kRowSide == false: y[j] = LSE_i x[i] + N[i][j]  (y = x (x) N);
@@ -272,11 +296,15 @@ __global__ __launch_bounds__(kSmallThreads) void k_small_log(SmallLogArgs a) {
     // ---- up-sweep
     for (int l = 1; l <= T.D; ++l) {
         const int np = T.products(l);
-        for (int k = w; k < np; k += kSmallWaves) {
+        const int ts = team_size(np), nteams = kSmallWaves / ts;
+        const int team = w / ts, mem = w % ts;
+        for (int k = team; k < np; k += nteams) {
             const int hl = T.handle(l - 1, 2 * k), hr = T.handle(l - 1, 2 * k + 1);
             const int s = T.pbase[l] + k;
-            wave_product_log<CP>(ly, ly.core(hl), ly.ro(hl), ly.core(hr), ly.ro(hr), ly.core(s),
-                                 ly.ro(s), scr);
+            const int Lc = ly.core(hl), Lro = ly.ro(hl), Rc = ly.core(hr), Rro = ly.ro(hr);
+            if (ts == 4) team_product_log<CP, 4>(ly, Lc, Lro, Rc, Rro, ly.core(s), ly.ro(s), mem, scr);
+            else if (ts == 2) team_product_log<CP, 2>(ly, Lc, Lro, Rc, Rro, ly.core(s), ly.ro(s), mem, scr);
+            else team_product_log<CP, 1>(ly, Lc, Lro, Rc, Rro, ly.core(s), ly.ro(s), mem, scr);
         }
         __syncthreads();
     }
@@ -395,37 +423,53 @@ __device__ __forceinline__ double mx(int base, int idx) {
     else return Dd(base + 2 * idx);
 }
 
-// One wave: P = L (x) R in (max, +), float64.  Lane (r = lane & 31, half g = lane >> 5)
-// computes row r, columns [g*CP/2, (g+1)*CP/2) (those below C).
-template <int CP, bool kLL, bool kRL>
-__device__ void wave_product_max(int C, int Lb, int Rb, int Pb) {
-    constexpr int kH = CP / 2;
+// A team of TS waves computes P = L (x) R in (max, +), float64.  Member `mem` owns
+// columns [mem*CP/TS, (mem+1)*CP/TS); within it lane (r = lane & 31, g = lane >> 5)
+// computes row r on one half of that window.  Indices are clamped into the matrix so that
+// every lane runs the same loads; rows and columns past C are never stored.
+template <int CP, int TS, bool kLL, bool kRL>
+__device__ __attribute__((noinline)) void team_product_max(int C, int Lb, int Rb, int Pb, int mem) {
+    constexpr int kW = CP / TS, kH = kW > 1 ? kW / 2 : 1;   // columns per member / per lane
+    constexpr int kT = kH < 4 ? kH : 4;                     // columns per lane per pass
+    C = uni(C); Lb = uni(Lb); Rb = uni(Rb); Pb = uni(Pb); mem = uni(mem);
     const int lane = threadIdx.x % kWave;
     const int r = lane & 31, g = lane >> 5;
-    const int c0 = g * kH;
-    // indices are clamped into the matrix so that every lane runs the same loads; lanes
-    // and columns past C compute throw-away values that are never stored
+    const int c0 = mem * kW + (kW > 1 ? g * kH : 0);
+    const bool active = (kW > 1 || g == 0) && r < C;
     const int rr = min(r, C - 1);
-    int cc[kH];
 #pragma unroll
-    for (int m = 0; m < kH; ++m) cc[m] = min(c0 + m, C - 1);
-    double acc[kH];
+    for (int p0 = 0; p0 < kH; p0 += kT) {
+        int cc[kT];
+        double acc[kT];
 #pragma unroll
-    for (int m = 0; m < kH; ++m) acc[m] = -INFINITY;
+        for (int m = 0; m < kT; ++m) {
+            cc[m] = min(c0 + p0 + m, C - 1);
+            acc[m] = -INFINITY;
+        }
+        // the loop runs over the padded size with no branch; terms past C are -inf
+#pragma unroll 4
+        for (int q = 0; q < CP; ++q) {
+            const int qc = min(q, C - 1);
+            const double x = q < C ? mx<kLL>(Lb, rr * C + qc) : -INFINITY;
 #pragma unroll
-    for (int q = 0; q < CP; ++q) {
-        if (q < C) {
-            const double x = mx<kLL>(Lb, rr * C + q);
+            for (int m = 0; m < kT; ++m) acc[m] = fmax(acc[m], x + mx<kRL>(Rb, qc * C + cc[m]));
+        }
+        if (active) {
 #pragma unroll
-            for (int m = 0; m < kH; ++m) acc[m] = fmax(acc[m], x + mx<kRL>(Rb, q * C + cc[m]));
+            for (int m = 0; m < kT; ++m)
+                if (p0 + m < kH && c0 + p0 + m < C) Dd(Pb + 2 * (r * C + c0 + p0 + m)) = acc[m];
         }
     }
-    if (r < C) {
-#pragma unroll
-        for (int m = 0; m < kH; ++m)
-            if (c0 + m < C) Dd(Pb + 2 * (r * C + c0 + m)) = acc[m];
-    }
     wave_sync();
+}
+
+template <int CP, int TS>
+__device__ __forceinline__ void team_product_max_any(int C, int hl, int hr, int Lb, int Rb, int Pb,
+                                                     int mem) {
+    if (hl < 0 && hr < 0) team_product_max<CP, TS, true, true>(C, Lb, Rb, Pb, mem);
+    else if (hl < 0) team_product_max<CP, TS, true, false>(C, Lb, Rb, Pb, mem);
+    else if (hr < 0) team_product_max<CP, TS, false, true>(C, Lb, Rb, Pb, mem);
+    else team_product_max<CP, TS, false, false>(C, Lb, Rb, Pb, mem);
 }
 
 // One wave: y[j] = max_i x[i] + N[i][j]  (float64)
@@ -474,13 +518,14 @@ __global__ __launch_bounds__(kSmallThreads) void k_small_max(SmallMaxArgs a) {
     // ---- up-sweep
     for (int l = 1; l <= T.D; ++l) {
         const int np = T.products(l);
-        for (int k = w; k < np; k += kSmallWaves) {
+        const int ts = team_size(np), nteams = kSmallWaves / ts;
+        const int team = w / ts, mem = w % ts;
+        for (int k = team; k < np; k += nteams) {
             const int hl = T.handle(l - 1, 2 * k), hr = T.handle(l - 1, 2 * k + 1);
             const int Pb = ly.slots + (T.pbase[l] + k) * CC * 2;
-            if (hl < 0 && hr < 0) wave_product_max<CP, true, true>(C, base(hl), base(hr), Pb);
-            else if (hl < 0) wave_product_max<CP, true, false>(C, base(hl), base(hr), Pb);
-            else if (hr < 0) wave_product_max<CP, false, true>(C, base(hl), base(hr), Pb);
-            else wave_product_max<CP, false, false>(C, base(hl), base(hr), Pb);
+            if (ts == 4) team_product_max_any<CP, 4>(C, hl, hr, base(hl), base(hr), Pb, mem);
+            else if (ts == 2) team_product_max_any<CP, 2>(C, hl, hr, base(hl), base(hr), Pb, mem);
+            else team_product_max_any<CP, 1>(C, hl, hr, base(hl), base(hr), Pb, mem);
         }
         __syncthreads();
     }
@@ -613,6 +658,7 @@ hipError_t launch_small_log(const float* pot, const int32_t* lengths, int64_t B,
     const size_t lds = small_log_lds_bytes(N - 1, C);
     if (C <= 8) return small_log_cp<8>(a, B, lds, s);
     if (C <= 16) return small_log_cp<16>(a, B, lds, s);
+    if (C <= 24) return small_log_cp<24>(a, B, lds, s);
     return small_log_cp<32>(a, B, lds, s);
 }
 
@@ -622,6 +668,7 @@ hipError_t launch_small_max(const float* pot, const int32_t* lengths, int64_t B,
     const size_t lds = small_max_lds_bytes(N - 1, C);
     if (C <= 8) return small_max_cp<8>(a, B, lds, s);
     if (C <= 16) return small_max_cp<16>(a, B, lds, s);
+    if (C <= 24) return small_max_cp<24>(a, B, lds, s);
     return small_max_cp<32>(a, B, lds, s);
 }
 
