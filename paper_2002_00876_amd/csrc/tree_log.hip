@@ -45,12 +45,21 @@ struct UpLogArgs {
     int64_t ngrid;        // nlogical rounded up to a multiple of 8
 };
 
+inline int64_t round8(int64_t x) { return (x + 7) / 8 * 8; }
+
 __device__ __forceinline__ size_t mat_off(int64_t b, int64_t k, int64_t nodes, int64_t C) {
     return (size_t)(b * nodes + k) * (size_t)C * (size_t)C;
 }
 
+// One tree level: workgroup = one 64 x 64 output tile of one node.  KP is C rounded up
+// to 64, 128 or 256 (compile-time, so every staging loop unrolls into batched loads);
+// VEC selects 16-byte global loads (C % 4 == 0).
+//   LDS: As[64][KP+4]  rows a0.. of A' (k contiguous), then exp(A' - rowmax)
+//        Bs[KP][64+4]  columns c0.. of B' (k-major, as stored in HBM), then exp(B' - colmax)
+template <int KP, bool VEC>
 __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
     extern __shared__ __align__(16) float smem[];
+    constexpr int LDA = KP + 4, LDB = kTile + 4;
     const int64_t lid = xcd_swizzle(blockIdx.x, a.ngrid);
     if (lid >= a.nlogical) return;
     const int ntiles = a.ntm * a.ntm;
@@ -60,9 +69,9 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
     const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
     const int64_t span = (int64_t)1 << a.level, half = span >> 1;
     if (k * span >= Eb) return;  // node absent: all padding
-    const int64_t C = a.C;
+    const int C = (int)a.C;
     const int tm = tile / a.ntm, tn = tile % a.ntm;
-    const int64_t a0 = (int64_t)tm * kTile, c0 = (int64_t)tn * kTile;
+    const int a0 = tm * kTile, c0 = tn * kTile;
     const int tid = threadIdx.x;
 
     const float* Lc = a.ccore + mat_off(b, 2 * k, a.cnodes, C);
@@ -75,8 +84,10 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
     const bool right = (2 * k + 1) * half < Eb;
     if (!right) {
         // the right half is padding: the node equals its left child
-        for (int idx = tid; idx < kTile * kTile; idx += kUpThreads) {
-            const int64_t r = a0 + idx / kTile, c = c0 + idx % kTile;
+#pragma unroll
+        for (int it = 0; it < kTile * kTile / kUpThreads; ++it) {
+            const int idx = tid + it * kUpThreads;
+            const int r = a0 + idx / kTile, c = c0 + idx % kTile;
             if (r < C && c < C) Pc[r * C + c] = Lc[r * C + c];
         }
         if (tn == 0)
@@ -91,84 +102,157 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
     const double* Rro = a.cro ? a.cro + (size_t)(b * a.cnodes + 2 * k + 1) * C : nullptr;
     const double* Rco = a.cco ? a.cco + (size_t)(b * a.cnodes + 2 * k + 1) * C : nullptr;
 
-    const int kp = a.kp, ld = kp + 4;
-    float* As = smem;                  // [kTile][ld]  exp-shifted rows of L
-    float* Bs = As + kTile * ld;       // [kTile][ld]  exp-shifted columns of R (transposed)
-    float* coh = Bs + kTile * ld;      // [kp] co_L - max co_L
-    float* roh = coh + kp;             // [kp] ro_R - max ro_R
-    float* rowm = roh + kp;            // [kTile]
+    float* As = smem;                  // [kTile][LDA]
+    float* Bs = As + kTile * LDA;      // [KP][LDB]
+    float* coh = Bs + KP * LDB;        // [KP] co_L - max co_L
+    float* roh = coh + KP;             // [KP] ro_R - max ro_R
+    float* rowm = roh + KP;            // [kTile]
     float* colm = rowm + kTile;        // [kTile]
     double* red = (double*)(colm + kTile);  // [4]
 
     // ---- column offsets of L and row offsets of R, shifted to max 0
     double lmax = -INFINITY, rmax = -INFINITY;
-    for (int64_t i = tid; i < C; i += kUpThreads) {
+    for (int i = tid; i < C; i += kUpThreads) {
         if (Lco) lmax = fmax(lmax, Lco[i]);
         if (Rro) rmax = fmax(rmax, Rro[i]);
     }
     const double coLshift = Lco ? safe_shift_d(block_max_d(lmax, red)) : 0.0;
     const double roRshift = Rro ? safe_shift_d(block_max_d(rmax, red)) : 0.0;
-    for (int64_t i = tid; i < kp; i += kUpThreads) {
+    for (int i = tid; i < KP; i += kUpThreads) {
         coh[i] = (i < C && Lco) ? (float)(Lco[i] - coLshift) : 0.f;
         roh[i] = (i < C && Rro) ? (float)(Rro[i] - roRshift) : 0.f;
     }
     __syncthreads();
 
-    // ---- stage the operand panels: rows a0.. of L (all b), columns c0.. of R (all b)
-    for (int idx = tid; idx < kTile * kp; idx += kUpThreads) {
-        const int r = idx / kp, bb = idx % kp;
-        const int64_t row = a0 + r;
-        As[r * ld + bb] = (row < C && bb < C) ? Lc[row * C + bb] + coh[bb] : -INFINITY;
+    // ---- stage A' = rows a0.. of L (+coh) and B' = columns c0.. of R (+roh); all loads of
+    // a panel are issued before any store
+    constexpr float NI = -INFINITY;
+    {
+        constexpr int GA = KP / 4, NA = kTile * GA / kUpThreads;
+        float4 v[NA];
+#pragma unroll
+        for (int it = 0; it < NA; ++it) {
+            const int idx = tid + it * kUpThreads;
+            const int r = idx / GA, col = 4 * (idx % GA), row = a0 + r;
+            if (VEC) {
+                v[it] = (row < C && col < C) ? *(const float4*)(Lc + (size_t)row * C + col)
+                                             : make_float4(NI, NI, NI, NI);
+            } else {
+                const float* p = Lc + (size_t)row * C + col;
+                v[it].x = (row < C && col + 0 < C) ? p[0] : NI;
+                v[it].y = (row < C && col + 1 < C) ? p[1] : NI;
+                v[it].z = (row < C && col + 2 < C) ? p[2] : NI;
+                v[it].w = (row < C && col + 3 < C) ? p[3] : NI;
+            }
+        }
+#pragma unroll
+        for (int it = 0; it < NA; ++it) {
+            const int idx = tid + it * kUpThreads;
+            const int r = idx / GA, col = 4 * (idx % GA);
+            float4 x = v[it];
+            x.x += coh[col]; x.y += coh[col + 1]; x.z += coh[col + 2]; x.w += coh[col + 3];
+            *(float4*)(As + r * LDA + col) = x;
+        }
     }
-    for (int idx = tid; idx < kTile * kp; idx += kUpThreads) {
-        const int bb = idx / kTile, cc = idx % kTile;
-        const int64_t col = c0 + cc;
-        Bs[cc * ld + bb] = (col < C && bb < C) ? Rc[(int64_t)bb * C + col] + roh[bb] : -INFINITY;
+    {
+        constexpr int GB = kTile / 4, NB = KP * GB / kUpThreads;
+        float4 v[NB];
+#pragma unroll
+        for (int it = 0; it < NB; ++it) {
+            const int idx = tid + it * kUpThreads;
+            const int kk = idx / GB, cl = 4 * (idx % GB), col = c0 + cl;
+            if (VEC) {
+                v[it] = (kk < C && col < C) ? *(const float4*)(Rc + (size_t)kk * C + col)
+                                            : make_float4(NI, NI, NI, NI);
+            } else {
+                const float* p = Rc + (size_t)kk * C + col;
+                v[it].x = (kk < C && col + 0 < C) ? p[0] : NI;
+                v[it].y = (kk < C && col + 1 < C) ? p[1] : NI;
+                v[it].z = (kk < C && col + 2 < C) ? p[2] : NI;
+                v[it].w = (kk < C && col + 3 < C) ? p[3] : NI;
+            }
+        }
+#pragma unroll
+        for (int it = 0; it < NB; ++it) {
+            const int idx = tid + it * kUpThreads;
+            const int kk = idx / GB, cl = 4 * (idx % GB);
+            float4 x = v[it];
+            const float rh = roh[kk];
+            x.x += rh; x.y += rh; x.z += rh; x.w += rh;
+            *(float4*)(Bs + kk * LDB + cl) = x;
+        }
     }
     __syncthreads();
 
-    // ---- row maxima of the A panel and column maxima of the B panel (4 threads each)
+    // ---- row maxima of A' and column maxima of B' (4 neighbouring lanes per row/column)
     {
         const int r = tid >> 2, part = tid & 3;
         float m1 = -INFINITY, m2 = -INFINITY;
-        for (int bb = part; bb < kp; bb += 4) {
-            m1 = fmaxf(m1, As[r * ld + bb]);
-            m2 = fmaxf(m2, Bs[r * ld + bb]);
+#pragma unroll
+        for (int g = part; g < KP / 4; g += 4) {
+            const float4 x = *(const float4*)(As + r * LDA + 4 * g);
+            m1 = fmaxf(m1, fmaxf(fmaxf(x.x, x.y), fmaxf(x.z, x.w)));
         }
-        m1 = fmaxf(m1, __shfl_xor(m1, 1, kWave));
-        m1 = fmaxf(m1, __shfl_xor(m1, 2, kWave));
-        m2 = fmaxf(m2, __shfl_xor(m2, 1, kWave));
-        m2 = fmaxf(m2, __shfl_xor(m2, 2, kWave));
+#pragma unroll
+        for (int kk = part; kk < KP; kk += 4) m2 = fmaxf(m2, Bs[kk * LDB + r]);
+        m1 = fmaxf(m1, dpp_f(m1, 0xB1));
+        m1 = fmaxf(m1, dpp_f(m1, 0x4E));
+        m2 = fmaxf(m2, dpp_f(m2, 0xB1));
+        m2 = fmaxf(m2, dpp_f(m2, 0x4E));
         if (part == 0) {
             rowm[r] = m1;
             colm[r] = m2;
         }
     }
     __syncthreads();
-    for (int idx = tid; idx < kTile * kp; idx += kUpThreads) {
-        const int r = idx / kp, bb = idx % kp;
-        As[r * ld + bb] = __expf(As[r * ld + bb] - safe_shift(rowm[r]));
-        Bs[r * ld + bb] = __expf(Bs[r * ld + bb] - safe_shift(colm[r]));
+    {
+        constexpr int GA = KP / 4, NA = kTile * GA / kUpThreads;
+#pragma unroll
+        for (int it = 0; it < NA; ++it) {
+            const int idx = tid + it * kUpThreads;
+            const int r = idx / GA, col = 4 * (idx % GA);
+            float4* p = (float4*)(As + r * LDA + col);
+            float4 x = *p;
+            const float s = safe_shift(rowm[r]);
+            x.x = __expf(x.x - s); x.y = __expf(x.y - s); x.z = __expf(x.z - s); x.w = __expf(x.w - s);
+            *p = x;
+        }
+        constexpr int GB = kTile / 4, NB = KP * GB / kUpThreads;
+#pragma unroll
+        for (int it = 0; it < NB; ++it) {
+            const int idx = tid + it * kUpThreads;
+            const int kk = idx / GB, cl = 4 * (idx % GB);
+            float4* p = (float4*)(Bs + kk * LDB + cl);
+            float4 x = *p;
+            x.x = __expf(x.x - safe_shift(colm[cl]));
+            x.y = __expf(x.y - safe_shift(colm[cl + 1]));
+            x.z = __expf(x.z - safe_shift(colm[cl + 2]));
+            x.w = __expf(x.w - safe_shift(colm[cl + 3]));
+            *p = x;
+        }
     }
     __syncthreads();
 
     // ---- S = expA * expB on the matrix cores.  Within each 8-wide k step, lanes 0-31
-    // contribute k..k+3 and lanes 32-63 k+4..k+7 (one 16-byte LDS read per operand);
+    // contribute k..k+3 and lanes 32-63 k+4..k+7 (one 16-byte LDS read of A per lane);
     // A and B use the same k assignment, so the sum over k is unchanged.
     const int w = tid / kWave, lane = tid % kWave;
     const int wm = w >> 1, wn = w & 1;
     f16v acc;
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-    const float* ap = As + (wm * 32 + (lane & 31)) * ld + 4 * (lane >> 5);
-    const float* bp = Bs + (wn * 32 + (lane & 31)) * ld + 4 * (lane >> 5);
-    for (int kk = 0; kk < kp; kk += 8) {
+    const float* ap = As + (wm * 32 + (lane & 31)) * LDA + 4 * (lane >> 5);
+    const float* bp = Bs + (4 * (lane >> 5)) * LDB + wn * 32 + (lane & 31);
+    const int kend = (C + 7) & ~7;
+#pragma unroll 2
+    for (int kk = 0; kk < kend; kk += 8) {
         const float4 av = *(const float4*)(ap + kk);
-        const float4 bv = *(const float4*)(bp + kk);
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.x, bv.x, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.y, bv.y, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.z, bv.z, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.w, bv.w, acc, 0, 0, 0);
+        const float b0 = bp[(kk + 0) * LDB], b1 = bp[(kk + 1) * LDB];
+        const float b2 = bp[(kk + 2) * LDB], b3 = bp[(kk + 3) * LDB];
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.x, b0, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.y, b1, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.z, b2, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.w, b3, acc, 0, 0, 0);
     }
 
     // ---- epilogue: core = log S (exact fallback when S underflows)
@@ -176,7 +260,7 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
     for (int r = 0; r < 16; ++r) {
         const int row = wm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
         const int col = wn * 32 + (lane & 31);
-        const int64_t gr = a0 + row, gc = c0 + col;
+        const int gr = a0 + row, gc = c0 + col;
         if (gr < C && gc < C) {
             const float S = acc[r];
             float val;
@@ -185,24 +269,24 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
             } else {
                 const float sa = safe_shift(rowm[row]), sb = safe_shift(colm[col]);
                 float q = -INFINITY;
-                for (int64_t bb = 0; bb < C; ++bb) {
-                    const float x = (Lc[gr * C + bb] + coh[bb] - sa) +
-                                    (Rc[bb * C + gc] + roh[bb] - sb);
+                for (int bb = 0; bb < C; ++bb) {
+                    const float x = (Lc[(size_t)gr * C + bb] + coh[bb] - sa) +
+                                    (Rc[(size_t)bb * C + gc] + roh[bb] - sb);
                     q = fmaxf(q, x);
                 }
                 if (q == -INFINITY) {
                     val = -INFINITY;
                 } else {
                     float s = 0.f;
-                    for (int64_t bb = 0; bb < C; ++bb) {
-                        const float x = (Lc[gr * C + bb] + coh[bb] - sa) +
-                                        (Rc[bb * C + gc] + roh[bb] - sb);
+                    for (int bb = 0; bb < C; ++bb) {
+                        const float x = (Lc[(size_t)gr * C + bb] + coh[bb] - sa) +
+                                        (Rc[(size_t)bb * C + gc] + roh[bb] - sb);
                         s += __expf(x - q);
                     }
                     val = q + __logf(s);
                 }
             }
-            Pc[gr * C + gc] = val;
+            Pc[(size_t)gr * C + gc] = val;
         }
     }
     if (tn == 0)
@@ -450,22 +534,21 @@ __global__ __launch_bounds__(256) void k_form_log(FormArgs a) {
     }
 }
 
-inline int64_t round8(int64_t x) { return (x + 7) / 8 * 8; }
-
-hipError_t up_sweep(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
-    const int64_t C = p.C;
-    const int ntm = (int)((C + kTile - 1) / kTile);
-    const int kp = (int)((C + 7) / 8 * 8);
-    const size_t lds = sizeof(float) * (2 * kTile * (kp + 4) + 2 * kp + 2 * kTile) +
+template <int KP, bool VEC>
+hipError_t up_sweep_kp(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
+    constexpr int LDA = KP + 4, LDB = kTile + 4;
+    const size_t lds = sizeof(float) * (kTile * LDA + KP * LDB + 2 * KP + 2 * kTile) +
                        sizeof(double) * 4;
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void*)k_up_log,
+        hipError_t e = hipFuncSetAttribute((const void*)k_up_log<KP, VEC>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize,
                                            160 * 1024);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
+    const int64_t C = p.C;
+    const int ntm = (int)((C + kTile - 1) / kTile);
     for (int l = 1; l <= p.D; ++l) {
         UpLogArgs a{};
         if (l == 1) {
@@ -477,14 +560,21 @@ hipError_t up_sweep(const Plan& p, const float* pot, const int32_t* lengths, hip
         a.core = p.core[l]; a.ro = p.ro[l]; a.co = p.co[l];
         a.nodes = p.Np >> l;
         a.lengths = lengths; a.B = p.B; a.N = p.N; a.C = C; a.level = l;
-        a.ntm = ntm; a.kp = kp;
+        a.ntm = ntm; a.kp = KP;
         a.nlogical = p.B * a.nodes * ntm * ntm;
         a.ngrid = round8(a.nlogical);
-        hipLaunchKernelGGL(k_up_log, dim3((unsigned)a.ngrid), dim3(kUpThreads), lds, s, a);
+        hipLaunchKernelGGL((k_up_log<KP, VEC>), dim3((unsigned)a.ngrid), dim3(kUpThreads), lds, s, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+hipError_t up_sweep(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
+    const bool vec = (p.C % 4) == 0;
+    if (p.C <= 64) return vec ? up_sweep_kp<64, true>(p, pot, lengths, s) : up_sweep_kp<64, false>(p, pot, lengths, s);
+    if (p.C <= 128) return vec ? up_sweep_kp<128, true>(p, pot, lengths, s) : up_sweep_kp<128, false>(p, pot, lengths, s);
+    return vec ? up_sweep_kp<256, true>(p, pot, lengths, s) : up_sweep_kp<256, false>(p, pot, lengths, s);
 }
 
 hipError_t root(const Plan& p, const float* pot, const int32_t* lengths, float* logZ,
