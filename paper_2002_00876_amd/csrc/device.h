@@ -32,6 +32,11 @@ __device__ __forceinline__ double wave_max_d(double x) {
     return x;
 }
 
+// Hardware exp/log (v_exp_f32 / v_log_f32 are base 2).  Inputs of the callers are
+// exponents <= 0 and sums >= 2^-80, so no denormal handling is needed.
+__device__ __forceinline__ float fexp(float x) { return __builtin_amdgcn_exp2f(x * 1.4426950408889634f); }
+__device__ __forceinline__ float flog(float x) { return __builtin_amdgcn_logf(x) * 0.6931471805599453f; }
+
 // Full-wave reductions with DPP inside each row of 16 lanes and readlane across the four
 // rows: the result is wave-uniform and the order of operations is fixed (deterministic).
 __device__ __forceinline__ float dpp_f(float x, int ctrl) {

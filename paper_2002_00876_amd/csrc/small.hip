@@ -80,139 +80,34 @@ struct Tree {
     }
 };
 
+// coalesced copy of a sequence's valid edges into LDS, several loads in flight per thread
 __device__ __forceinline__ void stage_leaves(const float* src, int dst, int n) {
-    if ((((uintptr_t)src) & 15) == 0 && (n & 3) == 0) {
+    const int tid = threadIdx.x, nt = blockDim.x;
+    if ((((uintptr_t)src) & 15) == 0 && (n & 3) == 0 && (dst & 3) == 0) {
         const float4* s4 = (const float4*)src;
         float4* d4 = reinterpret_cast<float4*>(ts_small_lds + dst);
-        for (int i = threadIdx.x; i < n / 4; i += blockDim.x) d4[i] = s4[i];
+        const int n4 = n / 4;
+        for (int base = 0; base < n4; base += 4 * nt) {
+            float4 v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) v[u] = s4[min(base + u * nt + tid, n4 - 1)];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (base + u * nt + tid < n4) d4[base + u * nt + tid] = v[u];
+        }
     } else {
-        for (int i = threadIdx.x; i < n; i += blockDim.x) F(dst + i) = src[i];
+        for (int base = 0; base < n; base += 8 * nt) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = src[min(base + u * nt + tid, n - 1)];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (base + u * nt + tid < n) F(dst + base + u * nt + tid) = v[u];
+        }
     }
 }
-
-// ================================================================== log semiring
-// LDS layout (float offsets): leaves [E][C][C] | slots [E-1][slotF] | vectors
-// [nodes][2][C] (u then v) | per-wave scratch [16][128].  A slot holds core [C*C] (padded
-// to a multiple of 2), then ro [C] and co [C] as doubles.
-struct LogLayout {
-    int C, CC, slotF, leaves, slots, vecs, scr;
-    __device__ void init(int c, int E, int nodes) {
-        C = c;
-        CC = c * c;
-        slotF = ((CC + 1) & ~1) + 4 * c;
-        leaves = 0;
-        slots = align4(E * CC);
-        vecs = align4(slots + (E - 1) * slotF);
-        scr = align4(vecs + nodes * 2 * c);
-    }
-    // a node: core offset and ro offset (-1 for a leaf: ro = co = 0)
-    __device__ int core(int h) const { return h < 0 ? leaves + (-h - 1) * CC : slots + h * slotF; }
-    __device__ int ro(int h) const { return h < 0 ? -1 : slots + h * slotF + ((CC + 1) & ~1); }
-};
 
 typedef float f4v __attribute__((ext_vector_type(4)));
-
-// A team of TS waves computes P = L (x) R, the exp-shifted fp32 MFMA product, for
-// C <= CP <= 32:
-//   A'[a][b] = L[a][b] + (co_L[b] - max co_L), B'[b][c] = R[b][c] + (ro_R[b] - max ro_R)
-//   S = sum_b exp(A' - rowmax) exp(B' - colmax); core_P = log S (exact fallback when S
-//   underflows), ro_P = ro_L + max co_L + rowmax, co_P = co_R + max ro_R + colmax.
-// The output is cut into 16 x 16 blocks (one for CP <= 16, four for CP = 32); team member
-// `mem` computes blocks mem, mem + TS, ... with v_mfma_f32_16x16x4f32.  Every member
-// derives the shifts and row/column maxima itself (same inputs, same results), so the team
-// needs no synchronisation.  The offset shifts only need to be near the maximum, so they
-// are reduced in fp32.
-template <int CP, int TS>
-__device__ __attribute__((noinline)) void team_product_log(const LogLayout& ly, int Lc, int Lro, int Rc, int Rro, int Pc,
-                                 int Pro, int mem, int scr) {
-    constexpr int kNB = CP <= 16 ? 1 : 4;      // 16 x 16 output blocks
-    const int C = uni(ly.C);
-    Lc = uni(Lc); Lro = uni(Lro); Rc = uni(Rc); Rro = uni(Rro); Pc = uni(Pc); Pro = uni(Pro);
-    mem = uni(mem); scr = uni(scr);
-    const int lane = threadIdx.x % kWave;
-    const int coh = scr, roh = scr + 32, rA = scr + 64, cB = scr + 96;
-    double lm = -INFINITY, rm = -INFINITY;
-    if (lane < C) {
-        if (Lro >= 0) lm = Dd(Lro + 2 * C + 2 * lane);   // co_L[lane]
-        if (Rro >= 0) rm = Dd(Rro + 2 * lane);           // ro_R[lane]
-    }
-    const double coLs = Lro >= 0 ? (double)safe_shift(wave_max_fast((float)lm)) : 0.0;
-    const double roRs = Rro >= 0 ? (double)safe_shift(wave_max_fast((float)rm)) : 0.0;
-    if (lane < 32) {
-        F(coh + lane) = (lane < C && Lro >= 0) ? (float)(lm - coLs) : 0.f;
-        F(roh + lane) = (lane < C && Rro >= 0) ? (float)(rm - roRs) : 0.f;
-    }
-    wave_sync();
-    // lanes 0-31: maxima of the rows of A'; lanes 32-63: maxima of the columns of B'
-    {
-        const int i = lane & 31, h = lane >> 5;
-        const int ic = min(i, C - 1);
-        const int base = h == 0 ? Lc + ic * C : Rc + ic;
-        const int stride = h == 0 ? 1 : C;
-        const int add = h == 0 ? coh : roh;
-        float m = -INFINITY;
-#pragma unroll
-        for (int k = 0; k < CP; ++k)
-            if (k < C) m = fmaxf(m, F(base + k * stride) + F(add + k));
-        F((h == 0 ? rA : cB) + i) = (i < C) ? m : -INFINITY;
-    }
-    wave_sync();
-    const int l16 = lane & 15, kq = lane >> 4;
-#pragma unroll
-    for (int blk = mem; blk < kNB; blk += TS) {
-        const int r0 = (blk >> 1) * 16, c0 = (blk & 1) * 16;
-        const int ia = r0 + l16, jb = c0 + l16;
-        const int iac = min(ia, C - 1), jbc = min(jb, C - 1);
-        const float sa = safe_shift(F(rA + iac)), sb = safe_shift(F(cB + jbc));
-        f4v acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kk = 0; kk < CP; kk += 4) {
-            if (kk < C) {
-                const int k = kk + kq;
-                const int kc = min(k, C - 1);
-                const float ea = __expf(F(Lc + iac * C + kc) + F(coh + kc) - sa);
-                const float eb = __expf(F(Rc + kc * C + jbc) + F(roh + kc) - sb);
-                const bool ka = k < C;
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32((ka && ia < C) ? ea : 0.f,
-                                                           (ka && jb < C) ? eb : 0.f, acc, 0, 0, 0);
-            }
-        }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int row = r0 + 4 * kq + r, col = jb;
-            if (row < C && col < C) {
-                const float S = acc[r];
-                float val;
-                if (S >= kUnderflow) {
-                    val = __logf(S);
-                } else {
-                    const float ra = safe_shift(F(rA + row)), cb = safe_shift(F(cB + col));
-                    float q = -INFINITY;
-                    for (int k = 0; k < C; ++k)
-                        q = fmaxf(q, (F(Lc + row * C + k) + F(coh + k) - ra) +
-                                         (F(Rc + k * C + col) + F(roh + k) - cb));
-                    if (q == -INFINITY) {
-                        val = -INFINITY;
-                    } else {
-                        float s = 0.f;
-                        for (int k = 0; k < C; ++k)
-                            s += __expf((F(Lc + row * C + k) + F(coh + k) - ra) +
-                                        (F(Rc + k * C + col) + F(roh + k) - cb) - q);
-                        val = q + __logf(s);
-                    }
-                }
-                F(Pc + row * C + col) = val;
-            }
-        }
-    }
-    if (mem == 0 && lane < C) {
-        Dd(Pro + 2 * lane) =
-            (Lro >= 0 ? Dd(Lro + 2 * lane) : 0.0) + coLs + (double)safe_shift(F(rA + lane));
-        Dd(Pro + 2 * C + 2 * lane) =
-            (Rro >= 0 ? Dd(Rro + 2 * C + 2 * lane) : 0.0) + roRs + (double)safe_shift(F(cB + lane));
-    }
-    wave_sync();
-}
 
 // team size for a level with np products on kSmallWaves waves: the largest power of two
 // <= waves / np, at most 4
@@ -221,16 +116,244 @@ __device__ __forceinline__ int team_size(int np) {
     return per >= 4 ? 4 : (per >= 2 ? 2 : 1);
 }
 
-// One wave, C <= CP <= 32.  kRowSide == false: y[j] = LSE_i x[i] + N[i][j]  (y = x (x) N);
-// kRowSide == true: y[i] = LSE_j N[i][j] + x[j]  (y = N (x) x).  y is shifted to max 0.
-template <int CP, bool kRowSide>
-__device__ void wave_vec_log(const LogLayout& ly, int x, int Nc, int Nro, int y, int scr) {
+// ================================================================== log semiring
+// Every node is kept in the form its consumer needs, so a product needs only exp + MFMA:
+//   LEFT operand  (left child of a product):  P[a][b] = ro[a] + core[a][b], max_b core[a][b] = 0
+//   RIGHT operand (right child of a product): P[b][c] = co[c] + core[b][c], max_b core[b][c] = 0
+//   NONE (the root): P[a][c] = ro[a] + co[c] + core[a][c]
+// (an absent right child makes a node equal to its left child, so a node takes the role
+// of its first ancestor that is consumed; the root is consumed by the log-sum-exp).
+// For P = L (x) R with L in LEFT and R in RIGHT form:
+//   S[a][c] = sum_b exp(core_L[a][b]) exp(core_R[b][c])     (fp32 MFMA, every factor <= 1)
+//   P[a][c] = ro_L[a] + co_R[c] + log S[a][c]
+// and the producer then normalises P into the form of its own role.  S < 2^-80 (all
+// terms underflowed) is recomputed exactly by a direct max-shifted log-sum-exp over b.
+//
+// LDS layout (float offsets): slots [2E-1][slotF] (leaves are slots 0..E-1, products
+// follow level by level) | vectors [nodes][2][C] (u then v).  A slot holds core [C*C]
+// (padded to a multiple of 4), then ro [C] and co [C] as doubles.
+constexpr int kLeft = 0, kRight = 1, kNone = 2;
+
+__device__ __forceinline__ int node_role(const Tree& T, int l, int k) {
+    while (l < T.D) {
+        if (k & 1) return kRight;
+        if (k + 1 < T.n[l]) return kLeft;
+        ++l;
+        k >>= 1;
+    }
+    return kNone;
+}
+
+struct LogLayout {
+    int C, CC, slotF, coreF, vecs;
+    __device__ void init(int c, int E) {
+        C = c;
+        CC = c * c;
+        coreF = align4(CC);
+        slotF = coreF + 4 * c;
+        vecs = (2 * E - 1) * slotF;
+    }
+    __device__ int core(int slot) const { return slot * slotF; }
+    __device__ int ro(int slot) const { return slot * slotF + coreF; }   // doubles: ro, then co
+    __device__ int co(int slot) const { return slot * slotF + coreF + 2 * C; }
+};
+
+// slot of node (l, k): leaves are slots 0..E-1, products E + pbase[l] + k
+__device__ __forceinline__ int log_slot(const Tree& T, int l, int k) {
+    const int h = T.handle(l, k);
+    return h < 0 ? (-h - 1) : T.E + h;
+}
+
+// Product of the LEFT node at slot sl and the RIGHT node at slot sr into slot sp, in the
+// form kRole.  Output blocks are 16 x 16 (v_mfma_f32_16x16x4f32): one block for CP <= 16
+// (member 0 only), four for CP > 16 shared by two waves -- by block rows when the result is
+// normalised per row (LEFT, NONE) and by block columns when per column (RIGHT), so each
+// wave holds whole rows (or columns) of what it normalises.
+template <int CP, int kRole>
+__device__ __forceinline__ void prod_log(const LogLayout& ly, int sl, int sr, int sp, int m) {
+    constexpr bool kTwo = CP > 16;
+    constexpr bool kColSplit = kTwo && kRole == kRight;
+    constexpr int kSteps = CP / 4;
     const int C = ly.C;
+    const int Lc = ly.core(sl), Lro = ly.ro(sl);
+    const int Rc = ly.core(sr), Rco = ly.co(sr);
+    const int Pc = ly.core(sp), Pro = ly.ro(sp), Pco = ly.co(sp);
+    const int lane = threadIdx.x % kWave, l16 = lane & 15, kq = lane >> 4;
+    const int rb0 = kTwo ? (kColSplit ? 0 : 16 * m) : 0, cb0 = kColSplit ? 16 * m : 0;
+    const int rb1 = kColSplit ? 16 : rb0, cb1 = kColSplit ? cb0 : 16;
+    const int ia0 = rb0 + l16, ia1 = rb1 + l16, jb0 = cb0 + l16, jb1 = cb1 + l16;
+    // row / column base offsets (clamped into the matrix; masked below)
+    const int arow0 = Lc + min(ia0, C - 1) * C, arow1 = Lc + min(ia1, C - 1) * C;
+    const int bcol0 = Rc + min(jb0, C - 1), bcol1 = Rc + min(jb1, C - 1);
+    float av[kSteps], bv[kSteps], cv[kSteps];
+#pragma unroll
+    for (int st = 0; st < kSteps; ++st) {
+        const int kc = min(4 * st + kq, C - 1);
+        av[st] = F(arow0 + kc);
+        bv[st] = F(bcol0 + kc * C);
+        if (kTwo) cv[st] = kColSplit ? F(arow1 + kc) : F(bcol1 + kc * C);
+    }
+    f4v acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+    const bool a0ok = ia0 < C, b0ok = jb0 < C, c1ok = kColSplit ? ia1 < C : jb1 < C;
+#pragma unroll
+    for (int st = 0; st < kSteps; ++st) {
+        const bool kv = 4 * st + kq < C;
+        const float a0 = (kv && a0ok) ? fexp(av[st]) : 0.f;
+        const float b0 = (kv && b0ok) ? fexp(bv[st]) : 0.f;
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b0, acc0, 0, 0, 0);
+        if (kTwo) {
+            const float c = (kv && c1ok) ? fexp(cv[st]) : 0.f;
+            if (kColSplit) acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(c, b0, acc1, 0, 0, 0);
+            else acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, c, acc1, 0, 0, 0);
+        }
+    }
+    // log S; lane-held entries: block X rows rbX + 4 kq + r, column cbX + l16
+    constexpr int kB = kTwo ? 2 : 1;
+    float ls[kB][4];
+    bool need = false;
+#pragma unroll
+    for (int x = 0; x < kB; ++x)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float S = x ? acc1[r] : acc0[r];
+            const int row = (x ? rb1 : rb0) + 4 * kq + r, col = x ? jb1 : jb0;
+            ls[x][r] = flog(S);
+            need |= row < C && col < C && !(S >= kUnderflow);
+        }
+    if (need) {   // some entry underflowed (or is padding): exact recomputation
+#pragma unroll
+        for (int x = 0; x < kB; ++x)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = (x ? rb1 : rb0) + 4 * kq + r, col = x ? jb1 : jb0;
+                const float S = x ? acc1[r] : acc0[r];
+                if (!(S >= kUnderflow) && row < C && col < C) {
+                    float q = -INFINITY;
+                    for (int k = 0; k < C; ++k) q = fmaxf(q, F(Lc + row * C + k) + F(Rc + k * C + col));
+                    float v = -INFINITY;
+                    if (q != -INFINITY) {
+                        float s = 0.f;
+                        for (int k = 0; k < C; ++k) s += fexp(F(Lc + row * C + k) + F(Rc + k * C + col) - q);
+                        v = q + flog(s);
+                    }
+                    ls[x][r] = v;
+                }
+            }
+    }
+    const int lc = min(lane, C - 1);
+    if constexpr (kRole == kLeft) {
+        // P[a][c] = ro_L[a] + co_R[c] + log S: fold co_R (shifted) in, then shift each row to max 0
+        const float mco = safe_shift(wave_max_fast(lane < C ? (float)Dd(Rco + 2 * lc) : -INFINITY));
+        float coh[kB];
+        coh[0] = (float)(Dd(Rco + 2 * min(jb0, C - 1)) - (double)mco);
+        if (kTwo) coh[kB - 1] = (float)(Dd(Rco + 2 * min(jb1, C - 1)) - (double)mco);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int row = rb0 + 4 * kq + r;
+            float x0 = b0ok ? ls[0][r] + coh[0] : -INFINITY;
+            float x1 = (kTwo && jb1 < C) ? ls[kB - 1][r] + coh[kB - 1] : -INFINITY;
+            float mx = fmaxf(x0, x1);
+            mx = fmaxf(mx, dpp_f(mx, 0xB1));
+            mx = fmaxf(mx, dpp_f(mx, 0x4E));
+            mx = fmaxf(mx, dpp_f(mx, 0x141));
+            mx = fmaxf(mx, dpp_f(mx, 0x140));
+            const float sh = safe_shift(mx);
+            if (row < C) {
+                if (b0ok) F(Pc + row * C + jb0) = x0 - sh;
+                if (kTwo && jb1 < C) F(Pc + row * C + jb1) = x1 - sh;
+                if (l16 == 0) Dd(Pro + 2 * row) = Dd(Lro + 2 * row) + (double)mco + (double)sh;
+            }
+        }
+        if (m == 0 && lane < C) Dd(Pco + 2 * lane) = 0.0;
+    } else if constexpr (kRole == kRight) {
+        // fold ro_L (shifted) in, then shift each column to max 0
+        const float mro = safe_shift(wave_max_fast(lane < C ? (float)Dd(Lro + 2 * lc) : -INFINITY));
+        float xs[kB][4];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int x = 0; x < kB; ++x)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = (x ? rb1 : rb0) + 4 * kq + r;
+                const float roh = (float)(Dd(Lro + 2 * min(row, C - 1)) - (double)mro);
+                xs[x][r] = row < C ? ls[x][r] + roh : -INFINITY;
+                mx = fmaxf(mx, xs[x][r]);
+            }
+        mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+        const float sh = safe_shift(mx);
+        if (b0ok) {
+#pragma unroll
+            for (int x = 0; x < kB; ++x)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int row = (x ? rb1 : rb0) + 4 * kq + r;
+                    if (row < C) F(Pc + row * C + jb0) = xs[x][r] - sh;
+                }
+            if (kq == 0) Dd(Pco + 2 * jb0) = Dd(Rco + 2 * jb0) + (double)mro + (double)sh;
+        }
+        if (m == 0 && lane < C) Dd(Pro + 2 * lane) = 0.0;
+    } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int row = rb0 + 4 * kq + r;
+            if (row < C) {
+                if (b0ok) F(Pc + row * C + jb0) = ls[0][r];
+                if (kTwo && jb1 < C) F(Pc + row * C + jb1) = ls[kB - 1][r];
+            }
+        }
+        if (m == 0 && lane < C) {
+            Dd(Pro + 2 * lane) = Dd(Lro + 2 * lane);
+            Dd(Pco + 2 * lane) = Dd(Rco + 2 * lane);
+        }
+    }
+}
+
+// Put a staged leaf (raw potentials in slot t, ro = co = 0) into the form of its role.
+template <int CP>
+__device__ void normalise_leaf(int C, int slot, int role, int slotF, int coreF) {
+    const int lane = threadIdx.x % kWave;
+    const int c0 = slot * slotF, ro = c0 + coreF, co = ro + 2 * C;
+    const int x = min(lane, C - 1);
+    if (role == kNone) {
+        if (lane < C) {
+            Dd(ro + 2 * lane) = 0.0;
+            Dd(co + 2 * lane) = 0.0;
+        }
+        wave_sync();
+        return;
+    }
+    // LEFT: lane x owns row x; RIGHT: lane x owns column x.  Loads are unconditional
+    // (indices clamped into the matrix) so they issue back to back.
+    const int base = role == kLeft ? c0 + x * C : c0 + x;
+    const int stride = role == kLeft ? 1 : C;
+    float v[CP];
+#pragma unroll
+    for (int j = 0; j < CP; ++j) v[j] = F(base + min(j, C - 1) * stride);
+    float m = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < CP; ++j) m = fmaxf(m, v[j]);   // entries past C repeat entry C-1
+    const float sh = safe_shift(m);
+    if (lane < C) {
+#pragma unroll
+        for (int j = 0; j < CP; ++j)
+            if (j < C) F(base + j * stride) = v[j] - sh;
+        Dd((role == kLeft ? ro : co) + 2 * lane) = (double)sh;
+        Dd((role == kLeft ? co : ro) + 2 * lane) = 0.0;
+    }
+    wave_sync();
+}
+
+// One wave, C <= CP <= 32, node N[a][b] = ro[a] + co[b] + core[a][b] at LDS offsets
+// (Nc, Nro; co follows ro).  kRowSide == false: y[j] = LSE_i x[i] + N[i][j] (y = x (x) N);
+// kRowSide == true: y[i] = LSE_j N[i][j] + x[j] (y = N (x) x).  y is shifted to max 0.
+template <int CP, bool kRowSide>
+__device__ void wave_vec_log(int C, int x, int Nc, int Nro, int y, int scr) {
     const int lane = threadIdx.x % kWave;
     // x on the left pairs with ro and the result picks up co; on the right the reverse
     const int inOff = kRowSide ? 2 * C : 0, outOff = kRowSide ? 0 : 2 * C;
     double w = -INFINITY;
-    if (lane < C) w = (double)F(x + lane) + (Nro >= 0 ? Dd(Nro + inOff + 2 * lane) : 0.0);
+    if (lane < C) w = (double)F(x + lane) + Dd(Nro + inOff + 2 * lane);
     const double ws = (double)safe_shift(wave_max_fast((float)w));
     if (lane < C) F(scr + lane) = (w == -INFINITY) ? -INFINITY : (float)(w - ws);
     wave_sync();
@@ -238,20 +361,22 @@ __device__ void wave_vec_log(const LogLayout& ly, int x, int Nc, int Nro, int y,
     {
         const int lc = min(lane, C - 1);
         float e[CP];
+#pragma unroll
+        for (int t = 0; t < CP; ++t) {
+            const int tc = min(t, C - 1);
+            e[t] = F(scr + tc) + (kRowSide ? F(Nc + lc * C + tc) : F(Nc + tc * C + lc));
+        }
         float m = -INFINITY;
 #pragma unroll
         for (int t = 0; t < CP; ++t) {
-            e[t] = -INFINITY;
-            if (t < C) {
-                e[t] = F(scr + t) + (kRowSide ? F(Nc + lc * C + t) : F(Nc + t * C + lc));
-                m = fmaxf(m, e[t]);
-            }
+            e[t] = t < C ? e[t] : -INFINITY;
+            m = fmaxf(m, e[t]);
         }
         if (m != -INFINITY && lane < C) {
             float s = 0.f;
 #pragma unroll
-            for (int t = 0; t < CP; ++t) s += __expf(e[t] - m);
-            z = (Nro >= 0 ? Dd(Nro + outOff + 2 * lane) : 0.0) + (double)(m + __logf(s));
+            for (int t = 0; t < CP; ++t) s += fexp(e[t] - m);
+            z = Dd(Nro + outOff + 2 * lane) + (double)(m + flog(s));
         }
     }
     const double zs = (double)safe_shift(wave_max_fast((float)z));
@@ -276,6 +401,7 @@ __global__ __launch_bounds__(kSmallThreads) void k_small_log(SmallLogArgs a) {
     const int Eb = (int)(clamp_len(a.lengths, b, a.N) - 1);
     const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int CC = C * C;
+    const float* gleaf = a.pot + (size_t)b * E * CC;
     if (a.marg) {  // padding edges are exactly zero
         float* mz = a.marg + ((size_t)b * E + Eb) * CC;
         const size_t nz = (size_t)(E - Eb) * CC;
@@ -287,63 +413,85 @@ __global__ __launch_bounds__(kSmallThreads) void k_small_log(SmallLogArgs a) {
     }
     __shared__ Tree T;
     if (threadIdx.x == 0) T.init(Eb);
-    stage_leaves(a.pot + (size_t)b * E * CC, 0, Eb * CC);
-    __syncthreads();
     LogLayout ly;
-    ly.init(C, Eb, T.nodes);
-    const int scr = ly.scr + w * 128;
-
-    // ---- up-sweep
+    ly.init(C, Eb);
+    // ---- stage the valid edges into slots 0..Eb-1 (8 loads in flight per thread)
+    {
+        const int n = Eb * CC;
+        for (int base = 0; base < n; base += 8 * kSmallThreads) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = gleaf[min(base + u * kSmallThreads + (int)threadIdx.x, n - 1)];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int idx = base + u * kSmallThreads + threadIdx.x;
+                if (idx < n) {
+                    const int t = idx / CC;
+                    F(t * ly.slotF + idx - t * CC) = v[u];
+                }
+            }
+        }
+    }
+    __syncthreads();
+    for (int t = w; t < Eb; t += kSmallWaves)
+        normalise_leaf<CP>(C, t, node_role(T, 0, t), ly.slotF, ly.coreF);
+    __syncthreads();
+    // ---- up-sweep: one wave per product (two for CP > 16)
+    constexpr int kPer = CP > 16 ? 2 : 1;
     for (int l = 1; l <= T.D; ++l) {
         const int np = T.products(l);
-        const int ts = team_size(np), nteams = kSmallWaves / ts;
-        const int team = w / ts, mem = w % ts;
-        for (int k = team; k < np; k += nteams) {
-            const int hl = T.handle(l - 1, 2 * k), hr = T.handle(l - 1, 2 * k + 1);
-            const int s = T.pbase[l] + k;
-            const int Lc = ly.core(hl), Lro = ly.ro(hl), Rc = ly.core(hr), Rro = ly.ro(hr);
-            if (ts == 4) team_product_log<CP, 4>(ly, Lc, Lro, Rc, Rro, ly.core(s), ly.ro(s), mem, scr);
-            else if (ts == 2) team_product_log<CP, 2>(ly, Lc, Lro, Rc, Rro, ly.core(s), ly.ro(s), mem, scr);
-            else team_product_log<CP, 1>(ly, Lc, Lro, Rc, Rro, ly.core(s), ly.ro(s), mem, scr);
+        for (int task = w; task < np * kPer; task += kSmallWaves) {
+            const int k = task / kPer, m = task % kPer;
+            const int sl = log_slot(T, l - 1, 2 * k), sr = log_slot(T, l - 1, 2 * k + 1);
+            const int sp = T.E + T.pbase[l] + k, role = node_role(T, l, k);
+            if (role == kLeft) prod_log<CP, kLeft>(ly, sl, sr, sp, m);
+            else if (role == kRight) prod_log<CP, kRight>(ly, sl, sr, sp, m);
+            else prod_log<CP, kNone>(ly, sl, sr, sp, m);
+            wave_sync();
         }
         __syncthreads();
     }
-    // ---- root: log Z = LSE_{a,c} ro[a] + co[c] + core[a][c]
-    const int hroot = T.handle(T.D, 0);
-    if (a.logZ && w == 0) {
-        const int rc = ly.core(hroot), rr = ly.ro(hroot);
-        double rm = -INFINITY, cm = -INFINITY;
-        if (lane < C) {
-            rm = rr >= 0 ? Dd(rr + 2 * lane) : 0.0;
-            cm = rr >= 0 ? Dd(rr + 2 * C + 2 * lane) : 0.0;
+    const int rslot = log_slot(T, T.D, 0);
+    auto U = [&](int l, int k) { return ly.vecs + (T.vbase[l] + k) * 2 * C; };
+    // ---- root: log Z = LSE_{a,c} ro[a] + co[c] + core[a][c]   (last wave, overlapping
+    // the first outside level, which does not need it)
+    if (a.logZ && w == kSmallWaves - 1) {
+        const int rc = ly.core(rslot), rr = ly.ro(rslot), rcc = ly.co(rslot);
+        const int lc = min(lane, C - 1);
+        const double rs = (double)safe_shift(wave_max_fast(lane < C ? (float)Dd(rr + 2 * lc) : -INFINITY));
+        const double cs = (double)safe_shift(wave_max_fast(lane < C ? (float)Dd(rcc + 2 * lc) : -INFINITY));
+        constexpr int kRows = CP / 2;
+        const int j = lane & 31, i0 = lane >> 5, jc = min(j, C - 1);
+        const float cj = (float)(Dd(rcc + 2 * jc) - cs);
+        float x[kRows];
+#pragma unroll
+        for (int q = 0; q < kRows; ++q) {
+            const int ic = min(i0 + 2 * q, C - 1);
+            x[q] = F(rc + ic * C + jc) + (float)(Dd(rr + 2 * ic) - rs) + cj;
         }
-        const double rs = (double)safe_shift(wave_max_fast((float)rm));
-        const double cs = (double)safe_shift(wave_max_fast((float)cm));
         float m = -INFINITY;
-        for (int idx = lane; idx < CC; idx += kWave) {
-            const int i = idx / C, j = idx % C;
-            float x = F(rc + idx);
-            if (rr >= 0) x += (float)(Dd(rr + 2 * i) - rs) + (float)(Dd(rr + 2 * C + 2 * j) - cs);
-            m = fmaxf(m, x);
+#pragma unroll
+        for (int q = 0; q < kRows; ++q) {
+            x[q] = (i0 + 2 * q < C && j < C) ? x[q] : -INFINITY;
+            m = fmaxf(m, x[q]);
         }
         m = wave_max_fast(m);
         float s = 0.f;
-        if (m != -INFINITY)
-            for (int idx = lane; idx < CC; idx += kWave) {
-                const int i = idx / C, j = idx % C;
-                float x = F(rc + idx);
-                if (rr >= 0) x += (float)(Dd(rr + 2 * i) - rs) + (float)(Dd(rr + 2 * C + 2 * j) - cs);
-                s += __expf(x - m);
-            }
+        if (m != -INFINITY) {
+#pragma unroll
+            for (int q = 0; q < kRows; ++q) s += fexp(x[q] - m);
+        }
         s = wave_sum_fast(s);
         if (lane == 0)
-            a.logZ[b] = (m == -INFINITY) ? -INFINITY : (float)(rs + cs + (double)(m + __logf(s)));
+            a.logZ[b] = (m == -INFINITY) ? -INFINITY : (float)(rs + cs + (double)(m + flog(s)));
     }
     if (!a.marg) return;
     // ---- outside sweep: u, v of every node (root: zeros)
-    auto U = [&](int l, int k) { return ly.vecs + (T.vbase[l] + k) * 2 * C; };
-    for (int idx = threadIdx.x; idx < 2 * C; idx += kSmallThreads) F(U(T.D, 0) + idx) = 0.f;
+    if (w < kSmallWaves - 1 || !a.logZ)
+        for (int idx = lane; idx < 2 * C; idx += kWave)
+            if (w == 0) F(U(T.D, 0) + idx) = 0.f;
     __syncthreads();
+    const int scr = ly.vecs + T.nodes * 2 * C + w * 64;
     for (int l = T.D; l >= 1; --l) {
         const int nn = T.n[l];
         for (int task = w; task < 3 * nn; task += kSmallWaves) {
@@ -357,45 +505,49 @@ __global__ __launch_bounds__(kSmallThreads) void k_small_log(SmallLogArgs a) {
                     else F(U(l - 1, 2 * k) + C + lane) = F(vN + lane);
                 }
             } else if (which == 1 && right) {   // u_R = u_N (x) L
-                const int hl = T.handle(l - 1, 2 * k);
-                wave_vec_log<CP, false>(ly, uN, ly.core(hl), ly.ro(hl), U(l - 1, 2 * k + 1), scr);
+                const int sl = log_slot(T, l - 1, 2 * k);
+                wave_vec_log<CP, false>(C, uN, ly.core(sl), ly.ro(sl), U(l - 1, 2 * k + 1), scr);
             } else if (which == 2 && right) {   // v_L = R (x) v_N
-                const int hr = T.handle(l - 1, 2 * k + 1);
-                wave_vec_log<CP, true>(ly, vN, ly.core(hr), ly.ro(hr), U(l - 1, 2 * k) + C, scr);
+                const int sr = log_slot(T, l - 1, 2 * k + 1);
+                wave_vec_log<CP, true>(C, vN, ly.core(sr), ly.ro(sr), U(l - 1, 2 * k) + C, scr);
             }
         }
         __syncthreads();
     }
-    // ---- marginals with a per-edge normaliser n_t
-    // lane -> column j = lane & 31 and rows (lane >> 5) + 2q: no integer division, every
-    // lane runs the same (clamped, in-bounds) loads; entries past C are masked
-    constexpr int kPer = CP / 2;
+    // ---- marginals with a per-edge normaliser n_t; the raw edge is re-read from global
+    // memory (L2).  Lane -> column j = lane & 31 and rows (lane >> 5) + 2q.
+    constexpr int kRows = CP / 2;
     const int j = lane & 31, i0 = lane >> 5, jc = min(j, C - 1);
     for (int t = w; t < Eb; t += kSmallWaves) {
-        const int al = U(0, t), be = al + C, leaf = ly.leaves + t * CC;
+        const int al = U(0, t), be = al + C;
+        const float* leaf = gleaf + (size_t)t * CC;
         const float bj = F(be + jc);
-        float x[kPer];
+        float x[kRows];
+#pragma unroll
+        for (int q = 0; q < kRows; ++q) {
+            const int i = i0 + 2 * q, ic = min(i, C - 1);
+            x[q] = leaf[ic * C + jc];
+        }
         float m = -INFINITY;
 #pragma unroll
-        for (int q = 0; q < kPer; ++q) {
+        for (int q = 0; q < kRows; ++q) {
             const int i = i0 + 2 * q, ic = min(i, C - 1);
-            const float v = F(al + ic) + F(leaf + ic * C + jc) + bj;
-            x[q] = (i < C && j < C) ? v : -INFINITY;
+            x[q] = (i < C && j < C) ? F(al + ic) + x[q] + bj : -INFINITY;
             m = fmaxf(m, x[q]);
         }
         m = wave_max_fast(m);
         float s = 0.f;
         if (m != -INFINITY) {
 #pragma unroll
-            for (int q = 0; q < kPer; ++q) s += __expf(x[q] - m);
+            for (int q = 0; q < kRows; ++q) s += fexp(x[q] - m);
         }
         s = wave_sum_fast(s);
-        const float n = (m == -INFINITY) ? -INFINITY : m + __logf(s);
+        const float n = (m == -INFINITY) ? -INFINITY : m + flog(s);
         float* out = a.marg + ((size_t)b * E + t) * CC;
 #pragma unroll
-        for (int q = 0; q < kPer; ++q) {
+        for (int q = 0; q < kRows; ++q) {
             const int i = i0 + 2 * q;
-            if (i < C && j < C) out[i * C + j] = (n == -INFINITY) ? 0.f : __expf(x[q] - n);
+            if (i < C && j < C) out[i * C + j] = (n == -INFINITY) ? 0.f : fexp(x[q] - n);
         }
     }
 }
@@ -450,7 +602,8 @@ __device__ __attribute__((noinline)) void team_product_max(int C, int Lb, int Rb
 #pragma unroll 4
         for (int q = 0; q < CP; ++q) {
             const int qc = min(q, C - 1);
-            const double x = q < C ? mx<kLL>(Lb, rr * C + qc) : -INFINITY;
+            const double xv = mx<kLL>(Lb, rr * C + qc);
+            const double x = q < C ? xv : -INFINITY;
 #pragma unroll
             for (int m = 0; m < kT; ++m) acc[m] = fmax(acc[m], x + mx<kRL>(Rb, qc * C + cc[m]));
         }
@@ -477,10 +630,15 @@ template <int CP, bool kLeaf>
 __device__ void wave_vec_max(int C, int x, int Nb, int y) {
     const int lane = threadIdx.x % kWave;
     const int j = min(lane, C - 1);
+    double v[CP];
+#pragma unroll
+    for (int i = 0; i < CP; ++i) {
+        const int ic = min(i, C - 1);
+        v[i] = Dd(x + 2 * ic) + mx<kLeaf>(Nb, ic * C + j);   // past C: repeats entry C-1
+    }
     double m = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < CP; ++i)
-        if (i < C) m = fmax(m, Dd(x + 2 * i) + mx<kLeaf>(Nb, i * C + j));
+    for (int i = 0; i < CP; ++i) m = fmax(m, v[i]);
     if (lane < C) Dd(y + 2 * lane) = m;
     wave_sync();
 }
@@ -553,16 +711,19 @@ __global__ __launch_bounds__(kSmallThreads) void k_small_max(SmallMaxArgs a) {
     for (int t = w; t < Eb; t += kSmallWaves) {
         const int d = U(0, t), leaf = ly.leaves + t * CC;
         const int j = min(lane, C - 1);
-        double best = Dd(d) + (double)F(leaf + j);
+        double v[CP];
+#pragma unroll
+        for (int i = 0; i < CP; ++i) {
+            const int ic = min(i, C - 1);
+            v[i] = Dd(d + 2 * ic) + (double)F(leaf + ic * C + j);
+        }
+        double best = v[0];
         int arg = 0;
 #pragma unroll
         for (int i = 1; i < CP; ++i) {
-            if (i < C) {
-                const double v = Dd(d + 2 * i) + (double)F(leaf + i * C + j);
-                const bool better = v > best;
-                best = better ? v : best;
-                arg = better ? i : arg;
-            }
+            const bool better = i < C && v[i] > best;   // strict: the lowest index wins ties
+            best = better ? v[i] : best;
+            arg = better ? i : arg;
         }
         if (lane < C) {
             bp[t * C + lane] = (uint8_t)arg;
@@ -598,9 +759,8 @@ __global__ __launch_bounds__(kSmallThreads) void k_small_max(SmallMaxArgs a) {
 // uses a prefix of each region, so the offsets computed in the kernels stay inside.
 size_t small_log_lds_bytes(int64_t E, int64_t C) {
     if (E < 1) return 0;
-    const int64_t CC = C * C, slotF = ((CC + 1) & ~1) + 4 * C;
-    const int64_t floats = (E * CC + 3) + ((E - 1) * slotF + 3) +
-                           (small_tree_nodes(E) * 2 * C + 3) + kSmallWaves * 128;
+    const int64_t slotF = ((C * C + 3) & ~3) + 4 * C;
+    const int64_t floats = (2 * E - 1) * slotF + small_tree_nodes(E) * 2 * C + kSmallWaves * 64;
     return sizeof(float) * (size_t)floats;
 }
 
