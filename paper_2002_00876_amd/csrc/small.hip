@@ -553,16 +553,19 @@ __global__ __launch_bounds__(kSmallThreads) void k_small_log(SmallLogArgs a) {
 }
 
 // ================================================================== max semiring
-// LDS layout (float offsets): leaves fp32 [E][C][C] | slots fp64 [E-1][C][C] | forward
-// scores fp64 [nodes][C] | last scores fp64 [C] | backpointers u8 [E][C].
+// LDS layout (float offsets): leaves fp32 [E][C][C] | product slots fp64 [E-1][C][C] |
+// last leaf again in fp64 [C][C] | forward scores fp64 [nodes][C] | last scores fp64 [C] |
+// backpointers u8 [E][C].  Above level 1 the only leaf that can still be an operand is the
+// last one (through nodes whose right half is padding), so levels >= 2 read fp64 only.
 struct MaxLayout {
-    int C, CC, leaves, slots, vecs, dlast, bp;
+    int C, CC, leaves, slots, lastc, vecs, dlast, bp;
     __device__ void init(int c, int E, int nodes) {
         C = c;
         CC = c * c;
         leaves = 0;
         slots = align4(E * CC);
-        vecs = slots + (E - 1) * CC * 2;
+        lastc = slots + (E - 1) * CC * 2;
+        vecs = lastc + CC * 2;
         dlast = vecs + nodes * c * 2;
         bp = dlast + 2 * c;
     }
@@ -575,57 +578,69 @@ __device__ __forceinline__ double mx(int base, int idx) {
     else return Dd(base + 2 * idx);
 }
 
-// A team of TS waves computes P = L (x) R in (max, +), float64.  Member `mem` owns
-// columns [mem*CP/TS, (mem+1)*CP/TS); within it lane (r = lane & 31, g = lane >> 5)
-// computes row r on one half of that window.  Indices are clamped into the matrix so that
-// every lane runs the same loads; rows and columns past C are never stored.
-template <int CP, int TS, bool kLL, bool kRL>
-__device__ __attribute__((noinline)) void team_product_max(int C, int Lb, int Rb, int Pb, int mem) {
-    constexpr int kW = CP / TS, kH = kW > 1 ? kW / 2 : 1;   // columns per member / per lane
-    constexpr int kT = kH < 4 ? kH : 4;                     // columns per lane per pass
-    C = uni(C); Lb = uni(Lb); Rb = uni(Rb); Pb = uni(Pb); mem = uni(mem);
-    const int lane = threadIdx.x % kWave;
-    const int r = lane & 31, g = lane >> 5;
-    const int c0 = mem * kW + (kW > 1 ? g * kH : 0);
-    const bool active = (kW > 1 || g == 0) && r < C;
-    const int rr = min(r, C - 1);
-#pragma unroll
-    for (int p0 = 0; p0 < kH; p0 += kT) {
-        int cc[kT];
-        double acc[kT];
-#pragma unroll
-        for (int m = 0; m < kT; ++m) {
-            cc[m] = min(c0 + p0 + m, C - 1);
-            acc[m] = -INFINITY;
+// All products of level l, P = L (x) R in (max, +), float64, by the whole workgroup: every
+// thread owns MR x MC output entries of one product (register-tiled loop over the inner
+// index).  kLeaves: the operands are leaves (level 1, fp32); otherwise fp64 slots.
+template <int MR, int MC, bool kLeaves>
+__device__ void block_prod_max(const MaxLayout& ly, const Tree& T, int l) {
+    const int C = ly.C, CC = ly.CC;
+    const int TR = (C + MR - 1) / MR, TC = (C + MC - 1) / MC, tpp = TR * TC;
+    const int total = T.products(l) * tpp;
+    for (int tile = threadIdx.x; tile < total; tile += kSmallThreads) {
+        const int k = tile / tpp, rem = tile - k * tpp, tr = rem / TC, tc = rem - tr * TC;
+        const int hl = T.handle(l - 1, 2 * k), hr = T.handle(l - 1, 2 * k + 1);
+        int lb, rb;
+        if constexpr (kLeaves) {
+            lb = ly.leaves + (-hl - 1) * CC;
+            rb = ly.leaves + (-hr - 1) * CC;
+        } else {
+            lb = hl < 0 ? ly.lastc : ly.slots + hl * CC * 2;
+            rb = hr < 0 ? ly.lastc : ly.slots + hr * CC * 2;
         }
-        // the loop runs over the padded size with no branch; terms past C are -inf
-#pragma unroll 4
-        for (int q = 0; q < CP; ++q) {
-            const int qc = min(q, C - 1);
-            const double xv = mx<kLL>(Lb, rr * C + qc);
-            const double x = q < C ? xv : -INFINITY;
+        const int r0 = tr * MR, c0 = tc * MC;
+        int ra[MR], cb[MC];
 #pragma unroll
-            for (int m = 0; m < kT; ++m) acc[m] = fmax(acc[m], x + mx<kRL>(Rb, qc * C + cc[m]));
-        }
-        if (active) {
+        for (int i = 0; i < MR; ++i) ra[i] = min(r0 + i, C - 1) * C;
 #pragma unroll
-            for (int m = 0; m < kT; ++m)
-                if (p0 + m < kH && c0 + p0 + m < C) Dd(Pb + 2 * (r * C + c0 + p0 + m)) = acc[m];
+        for (int j = 0; j < MC; ++j) cb[j] = min(c0 + j, C - 1);
+        double acc[MR][MC];
+#pragma unroll
+        for (int i = 0; i < MR; ++i)
+#pragma unroll
+            for (int j = 0; j < MC; ++j) acc[i][j] = -INFINITY;
+#pragma unroll 2
+        for (int q = 0; q < C; ++q) {
+            double av[MR], bv[MC];
+#pragma unroll
+            for (int i = 0; i < MR; ++i) av[i] = mx<kLeaves>(lb, ra[i] + q);
+#pragma unroll
+            for (int j = 0; j < MC; ++j) bv[j] = mx<kLeaves>(rb, q * C + cb[j]);
+#pragma unroll
+            for (int i = 0; i < MR; ++i)
+#pragma unroll
+                for (int j = 0; j < MC; ++j) acc[i][j] = fmax(acc[i][j], av[i] + bv[j]);
         }
+        const int Pb = ly.slots + (T.pbase[l] + k) * CC * 2;
+#pragma unroll
+        for (int i = 0; i < MR; ++i)
+#pragma unroll
+            for (int j = 0; j < MC; ++j)
+                if (r0 + i < C && c0 + j < C) Dd(Pb + 2 * ((r0 + i) * C + c0 + j)) = acc[i][j];
     }
-    wave_sync();
 }
 
-template <int CP, int TS>
-__device__ __forceinline__ void team_product_max_any(int C, int hl, int hr, int Lb, int Rb, int Pb,
-                                                     int mem) {
-    if (hl < 0 && hr < 0) team_product_max<CP, TS, true, true>(C, Lb, Rb, Pb, mem);
-    else if (hl < 0) team_product_max<CP, TS, true, false>(C, Lb, Rb, Pb, mem);
-    else if (hr < 0) team_product_max<CP, TS, false, true>(C, Lb, Rb, Pb, mem);
-    else team_product_max<CP, TS, false, false>(C, Lb, Rb, Pb, mem);
+// the smallest register tile that still gives every thread at most one tile
+template <bool kLeaves>
+__device__ void level_prod_max(const MaxLayout& ly, const Tree& T, int l) {
+    const int np = T.products(l), C = ly.C;
+    auto tiles = [&](int mr, int mc) { return np * ((C + mr - 1) / mr) * ((C + mc - 1) / mc); };
+    if (tiles(1, 1) <= kSmallThreads) block_prod_max<1, 1, kLeaves>(ly, T, l);
+    else if (tiles(1, 2) <= kSmallThreads) block_prod_max<1, 2, kLeaves>(ly, T, l);
+    else if (tiles(2, 2) <= kSmallThreads) block_prod_max<2, 2, kLeaves>(ly, T, l);
+    else if (tiles(2, 4) <= kSmallThreads) block_prod_max<2, 4, kLeaves>(ly, T, l);
+    else block_prod_max<4, 4, kLeaves>(ly, T, l);
 }
 
-// One wave: y[j] = max_i x[i] + N[i][j]  (float64)
 template <int CP, bool kLeaf>
 __device__ void wave_vec_max(int C, int x, int Nb, int y) {
     const int lane = threadIdx.x % kWave;
@@ -673,18 +688,13 @@ __global__ __launch_bounds__(kSmallThreads) void k_small_max(SmallMaxArgs a) {
     MaxLayout ly;
     ly.init(C, Eb, T.nodes);
     auto base = [&](int h) { return h < 0 ? ly.leaves + (-h - 1) * CC : ly.slots + h * CC * 2; };
-    // ---- up-sweep
+    // the last leaf in fp64 for levels >= 2 (read only after the level-1 barrier)
+    for (int i = threadIdx.x; i < CC; i += kSmallThreads)
+        Dd(ly.lastc + 2 * i) = (double)F(ly.leaves + (Eb - 1) * CC + i);
+    // ---- up-sweep: all threads share each level's products
     for (int l = 1; l <= T.D; ++l) {
-        const int np = T.products(l);
-        const int ts = team_size(np), nteams = kSmallWaves / ts;
-        const int team = w / ts, mem = w % ts;
-        for (int k = team; k < np; k += nteams) {
-            const int hl = T.handle(l - 1, 2 * k), hr = T.handle(l - 1, 2 * k + 1);
-            const int Pb = ly.slots + (T.pbase[l] + k) * CC * 2;
-            if (ts == 4) team_product_max_any<CP, 4>(C, hl, hr, base(hl), base(hr), Pb, mem);
-            else if (ts == 2) team_product_max_any<CP, 2>(C, hl, hr, base(hl), base(hr), Pb, mem);
-            else team_product_max_any<CP, 1>(C, hl, hr, base(hl), base(hr), Pb, mem);
-        }
+        if (l == 1) level_prod_max<true>(ly, T, l);
+        else level_prod_max<false>(ly, T, l);
         __syncthreads();
     }
     // ---- forward scores: u_L = u_N, u_R = u_N (x) L
@@ -767,7 +777,7 @@ size_t small_log_lds_bytes(int64_t E, int64_t C) {
 size_t small_max_lds_bytes(int64_t E, int64_t C) {
     if (E < 1) return 0;
     const int64_t CC = C * C;
-    const int64_t floats = (E * CC + 3) + (E - 1) * CC * 2 + small_tree_nodes(E) * C * 2 + 2 * C;
+    const int64_t floats = (E * CC + 3) + (E - 1) * CC * 2 + CC * 2 + small_tree_nodes(E) * C * 2 + 2 * C;
     return sizeof(float) * (size_t)floats + (size_t)(E * C);
 }
 
