@@ -61,6 +61,7 @@ typedef int ts_status;
 #define TS_OP_LOGPARTITION 0
 #define TS_OP_MARGINALS 1
 #define TS_OP_VITERBI 2
+#define TS_OP_MARGINALS_VITERBI 3
 
 /* Largest supported number of labels C. */
 int ts_chain_max_labels(void);
@@ -105,6 +106,20 @@ ts_status ts_chain_marginals(const float* pot, const int32_t* lengths, int64_t B
 ts_status ts_chain_viterbi(const float* pot, const int32_t* lengths, int64_t B, int64_t N,
                            int64_t C, int32_t* path, float* score, void* ws, size_t ws_bytes,
                            void* stream);
+
+/*
+ * Marginals and Viterbi of the same potentials in one call: the outputs of
+ * ts_chain_marginals (logZ nullable, marg) and of ts_chain_viterbi (path, score), with the
+ * same meaning, layout and values.  For label sets small enough for the single-launch path
+ * both passes run in one launch (one workgroup per sequence and pass, side by side);
+ * otherwise the two kernel sequences run one after the other on `stream`.  The workspace
+ * is ts_chain_workspace_bytes(TS_OP_MARGINALS_VITERBI, ...): the marginals workspace
+ * followed by the Viterbi workspace.  Errors as for the two separate calls.
+ */
+ts_status ts_chain_marginals_viterbi(const float* pot, const int32_t* lengths, int64_t B,
+                                     int64_t N, int64_t C, float* logZ, float* marg,
+                                     int32_t* path, float* score, void* ws, size_t ws_bytes,
+                                     void* stream);
 
 /* Message for the last non-OK status returned to the calling thread ("" if none). */
 const char* ts_last_error(void);

@@ -10,7 +10,7 @@ import torch
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libtschain.so")
 
-OP_LOGPARTITION, OP_MARGINALS, OP_VITERBI = 0, 1, 2
+OP_LOGPARTITION, OP_MARGINALS, OP_VITERBI, OP_MARGINALS_VITERBI = 0, 1, 2, 3
 STATUS = {0: "TS_OK", -1: "TS_ERR_NULL_ARG", -2: "TS_ERR_BAD_DIM", -3: "TS_ERR_WORKSPACE",
           -4: "TS_ERR_LENGTHS", -5: "TS_ERR_HIP"}
 
@@ -37,7 +37,9 @@ def lib():
         L.ts_chain_logpartition.argtypes = [p, p, i64, i64, i64, p, p, sz, p]
         L.ts_chain_marginals.argtypes = [p, p, i64, i64, i64, p, p, p, sz, p]
         L.ts_chain_viterbi.argtypes = [p, p, i64, i64, i64, p, p, p, sz, p]
-        for f in ("ts_chain_logpartition", "ts_chain_marginals", "ts_chain_viterbi"):
+        L.ts_chain_marginals_viterbi.argtypes = [p, p, i64, i64, i64, p, p, p, p, p, sz, p]
+        for f in ("ts_chain_logpartition", "ts_chain_marginals", "ts_chain_viterbi",
+                  "ts_chain_marginals_viterbi"):
             getattr(L, f).restype = ctypes.c_int
         L.ts_last_error.restype = ctypes.c_char_p
         _lib = L
@@ -121,3 +123,21 @@ def viterbi(pot, lengths=None, out=None, ws=None):
     _check(lib().ts_chain_viterbi(_ptr(pot), _ptr(lengths), B, N, C, _ptr(path), _ptr(score),
                                   _ptr(w), nb, _stream(pot.device)))
     return path, score
+
+
+def marginals_viterbi(pot, lengths=None, out=None, ws=None, want_logz=True):
+    """(log Z [B] or None, marginals [B, N-1, C, C], path [B, N], score [B]) in one call."""
+    pot, lengths, B, N, C = _prep(pot, lengths)
+    if out is not None:
+        logz, marg, path, score = out
+    else:
+        dev = pot.device
+        logz = torch.empty(B, dtype=torch.float32, device=dev) if want_logz else None
+        marg = torch.empty_like(pot)
+        path = torch.empty((B, N), dtype=torch.int32, device=dev)
+        score = torch.empty(B, dtype=torch.float32, device=dev)
+    w, nb = _workspace(OP_MARGINALS_VITERBI, B, N, C, pot.device, ws)
+    _check(lib().ts_chain_marginals_viterbi(_ptr(pot), _ptr(lengths), B, N, C, _ptr(logz),
+                                            _ptr(marg) if N > 1 else None, _ptr(path),
+                                            _ptr(score), _ptr(w), nb, _stream(pot.device)))
+    return logz, marg, path, score

@@ -107,8 +107,7 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p) {
 
 namespace {
 
-ts_status check_common(const float* pot, int64_t B, int64_t N, int64_t C, int op, void* ws,
-                       size_t ws_bytes, Plan* plan) {
+ts_status check_dims(const float* pot, int64_t B, int64_t N, int64_t C, int op, Plan* plan) {
     if (B < 1 || N < 1 || C < 1)
         return fail(TS_ERR_BAD_DIM, "B, N and C must all be >= 1");
     if (C > kMaxLabels)
@@ -117,17 +116,26 @@ ts_status check_common(const float* pot, int64_t B, int64_t N, int64_t C, int op
     if (N > 1 && !pot) return fail(TS_ERR_NULL_ARG, "pot is NULL");
     if (!make_plan(op, B, N, C, nullptr, plan))
         return fail(TS_ERR_BAD_DIM, "problem size overflows the supported range");
-    if (plan->bytes > 0) {
-        if (!ws) return fail(TS_ERR_NULL_ARG, "ws is NULL but the call needs a workspace");
-        if (ws_bytes < plan->bytes)
-            return fail(TS_ERR_WORKSPACE, "workspace too small: need " +
-                                              std::to_string(plan->bytes) + " bytes, got " +
-                                              std::to_string(ws_bytes));
-        if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0)
-            return fail(TS_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-        make_plan(op, B, N, C, ws, plan);
-    }
     return TS_OK;
+}
+
+ts_status check_ws(size_t need, void* ws, size_t ws_bytes) {
+    if (need == 0) return TS_OK;
+    if (!ws) return fail(TS_ERR_NULL_ARG, "ws is NULL but the call needs a workspace");
+    if (ws_bytes < need)
+        return fail(TS_ERR_WORKSPACE, "workspace too small: need " + std::to_string(need) +
+                                          " bytes, got " + std::to_string(ws_bytes));
+    if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0)
+        return fail(TS_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    return TS_OK;
+}
+
+ts_status check_common(const float* pot, int64_t B, int64_t N, int64_t C, int op, void* ws,
+                       size_t ws_bytes, Plan* plan) {
+    ts_status st = check_dims(pot, B, N, C, op, plan);
+    if (st == TS_OK) st = check_ws(plan->bytes, ws, ws_bytes);
+    if (st == TS_OK && plan->bytes > 0) make_plan(op, B, N, C, ws, plan);
+    return st;
 }
 
 ts_status check_lengths(const int32_t* lengths, int64_t B, int64_t N, hipStream_t s) {
@@ -160,10 +168,17 @@ extern "C" {
 int ts_chain_max_labels(void) { return kMaxLabels; }
 
 size_t ts_chain_workspace_bytes(int op, int64_t B, int64_t N, int64_t C) {
-    if (op < TS_OP_LOGPARTITION || op > TS_OP_VITERBI || B < 1 || N < 1 || C < 1 ||
+    if (op < TS_OP_LOGPARTITION || op > TS_OP_MARGINALS_VITERBI || B < 1 || N < 1 || C < 1 ||
         C > kMaxLabels)
         return 0;
-    Plan p;
+    Plan p, q;
+    if (op == TS_OP_MARGINALS_VITERBI) {
+        // the marginals plan first, then the Viterbi plan at the next 256-byte boundary
+        if (!make_plan(TS_OP_MARGINALS, B, N, C, nullptr, &p) ||
+            !make_plan(TS_OP_VITERBI, B, N, C, nullptr, &q))
+            return 0;
+        return p.bytes + q.bytes;
+    }
     if (!make_plan(op, B, N, C, nullptr, &p)) return 0;
     return p.bytes;
 }
@@ -217,6 +232,38 @@ ts_status ts_chain_viterbi(const float* pot, const int32_t* lengths, int64_t B, 
         return hip_status(launch_single_token(B, N, C, TS_OP_VITERBI, nullptr, path, score, s));
     if (p.fused) return hip_status(launch_small_max(pot, lengths, B, N, C, path, score, s));
     return hip_status(launch_viterbi_tree(p, pot, lengths, path, score, s));
+}
+
+ts_status ts_chain_marginals_viterbi(const float* pot, const int32_t* lengths, int64_t B,
+                                     int64_t N, int64_t C, float* logZ, float* marg,
+                                     int32_t* path, float* score, void* ws, size_t ws_bytes,
+                                     void* stream) {
+    Plan pm, pv;
+    ts_status st = check_dims(pot, B, N, C, TS_OP_MARGINALS, &pm);
+    if (st != TS_OK) return st;
+    make_plan(TS_OP_VITERBI, B, N, C, nullptr, &pv);
+    // the marginals plan first, then the Viterbi plan (both sizes are multiples of 256)
+    if ((st = check_ws(pm.bytes + pv.bytes, ws, ws_bytes)) != TS_OK) return st;
+    if (N > 1 && !marg) return fail(TS_ERR_NULL_ARG, "marg is NULL");
+    if (!path || !score) return fail(TS_ERR_NULL_ARG, "path or score is NULL");
+    if (pm.bytes > 0) make_plan(TS_OP_MARGINALS, B, N, C, ws, &pm);
+    if (pv.bytes > 0) make_plan(TS_OP_VITERBI, B, N, C, static_cast<char*>(ws) + pm.bytes, &pv);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = check_lengths(lengths, B, N, s)) != TS_OK) return st;
+    if (N == 1) {
+        if (logZ) {
+            hipError_t e = launch_single_token(B, N, C, TS_OP_LOGPARTITION, logZ, nullptr,
+                                               nullptr, s);
+            if (e != hipSuccess) return hip_status(e);
+        }
+        return hip_status(launch_single_token(B, N, C, TS_OP_VITERBI, nullptr, path, score, s));
+    }
+    if (pm.fused && pv.fused)
+        return hip_status(launch_small_both(pot, lengths, B, N, C, logZ, marg, path, score, s));
+    hipError_t e = launch_logz_tree(pm, pot, lengths, logZ, s);
+    if (e == hipSuccess) e = launch_marginals_tree(pm, pot, lengths, marg, s);
+    if (e == hipSuccess) e = launch_viterbi_tree(pv, pot, lengths, path, score, s);
+    return hip_status(e);
 }
 
 const char* ts_last_error(void) { return g_err.c_str(); }

@@ -27,5 +27,9 @@ hipError_t launch_small_log(const float* pot, const int32_t* lengths, int64_t B,
                             int64_t C, float* logZ, float* marg, hipStream_t s);
 hipError_t launch_small_max(const float* pot, const int32_t* lengths, int64_t B, int64_t N,
                             int64_t C, int32_t* path, float* score, hipStream_t s);
+// both passes in one launch of 2B workgroups (marginals in the first B, Viterbi in the rest)
+hipError_t launch_small_both(const float* pot, const int32_t* lengths, int64_t B, int64_t N,
+                             int64_t C, float* logZ, float* marg, int32_t* path, float* score,
+                             hipStream_t s);
 
 }  // namespace tsc

@@ -394,8 +394,7 @@ struct SmallLogArgs {
 };
 
 template <int CP>
-__global__ __launch_bounds__(kSmallThreads) void k_small_log(SmallLogArgs a) {
-    const int64_t b = blockIdx.x;
+__device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int64_t b) {
     const int C = a.C;
     const int64_t E = a.N - 1;
     const int Eb = (int)(clamp_len(a.lengths, b, a.N) - 1);
@@ -668,8 +667,7 @@ struct SmallMaxArgs {
 };
 
 template <int CP>
-__global__ __launch_bounds__(kSmallThreads) void k_small_max(SmallMaxArgs a) {
-    const int64_t b = blockIdx.x;
+__device__ __forceinline__ void small_max_body(const SmallMaxArgs& a, const int64_t b) {
     const int C = a.C;
     const int64_t E = a.N - 1;
     const int L = (int)clamp_len(a.lengths, b, a.N), Eb = L - 1;
@@ -763,6 +761,27 @@ __global__ __launch_bounds__(kSmallThreads) void k_small_max(SmallMaxArgs a) {
     }
 }
 
+template <int CP>
+__global__ __launch_bounds__(kSmallThreads) void k_small_log(SmallLogArgs a) {
+    small_log_body<CP>(a, blockIdx.x);
+}
+
+template <int CP>
+__global__ __launch_bounds__(kSmallThreads) void k_small_max(SmallMaxArgs a) {
+    small_max_body<CP>(a, blockIdx.x);
+}
+
+// Both computations in one launch: workgroups [0, B) run the log-semiring pass of sequence
+// b, workgroups [B, 2B) the max-plus pass of sequence b - B.  The two halves share nothing
+// but the read-only potentials, so they run side by side on different compute units.
+template <int CP>
+__global__ __launch_bounds__(kSmallThreads) void k_small_both(SmallLogArgs la, SmallMaxArgs ma,
+                                                             int64_t B) {
+    const int64_t g = blockIdx.x;
+    if (g < B) small_log_body<CP>(la, g);
+    else small_max_body<CP>(ma, g - B);
+}
+
 }  // namespace
 
 // Both layouts are sized for the longest sequence (E = N-1 edges); a shorter sequence
@@ -820,6 +839,20 @@ hipError_t small_max_cp(const SmallMaxArgs& a, int64_t B, size_t lds, hipStream_
     return hipGetLastError();
 }
 
+template <int CP>
+hipError_t small_both_cp(const SmallLogArgs& la, const SmallMaxArgs& ma, int64_t B, size_t lds,
+                         hipStream_t s) {
+    static bool attr = false;
+    if (!attr) {
+        hipError_t e = allow_lds(k_small_both<CP>);
+        if (e != hipSuccess) return e;
+        attr = true;
+    }
+    hipLaunchKernelGGL(k_small_both<CP>, dim3((unsigned)(2 * B)), dim3(kSmallThreads), lds, s, la,
+                       ma, B);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_small_log(const float* pot, const int32_t* lengths, int64_t B, int64_t N,
@@ -840,6 +873,18 @@ hipError_t launch_small_max(const float* pot, const int32_t* lengths, int64_t B,
     if (C <= 16) return small_max_cp<16>(a, B, lds, s);
     if (C <= 24) return small_max_cp<24>(a, B, lds, s);
     return small_max_cp<32>(a, B, lds, s);
+}
+
+hipError_t launch_small_both(const float* pot, const int32_t* lengths, int64_t B, int64_t N,
+                             int64_t C, float* logZ, float* marg, int32_t* path, float* score,
+                             hipStream_t s) {
+    SmallLogArgs la{pot, lengths, N, (int)C, logZ, marg};
+    SmallMaxArgs ma{pot, lengths, N, (int)C, path, score};
+    const size_t lds = std::max(small_log_lds_bytes(N - 1, C), small_max_lds_bytes(N - 1, C));
+    if (C <= 8) return small_both_cp<8>(la, ma, B, lds, s);
+    if (C <= 16) return small_both_cp<16>(la, ma, B, lds, s);
+    if (C <= 24) return small_both_cp<24>(la, ma, B, lds, s);
+    return small_both_cp<32>(la, ma, B, lds, s);
 }
 
 }  // namespace tsc

@@ -22,7 +22,13 @@ def gpu_all(pot, lens, device="cuda:0"):
     z = binding.logpartition(tp, tl)
     z2, m = binding.marginals(tp, tl)
     path, score = binding.viterbi(tp, tl)
+    # the combined call runs the same kernels (side by side on the single-launch path):
+    # its outputs must be bitwise those of the two separate calls
+    z3, m3, p3, s3 = binding.marginals_viterbi(tp, tl)
     torch.cuda.synchronize()
+    for got, want, name in ((z3, z2, "logZ"), (m3, m, "marginals"), (p3, path, "path"),
+                            (s3, score, "score")):
+        assert torch.equal(got, want), f"marginals_viterbi: {name} differs from the separate call"
     return (z.cpu().numpy(), z2.cpu().numpy(), m.cpu().numpy(), path.cpu().numpy(),
             score.cpu().numpy())
 

@@ -61,7 +61,10 @@ def test_workspace_sizes(L, monkeypatch):
     # the tree over N-1 = 24 edges has levels of 16, 8, 4, 2, 1 nodes of C*C floats
     core = 32 * (16 + 8 + 4 + 2 + 1) * CW * CW * 4
     assert ws(0, 32, 25, CW) >= core
-    assert ws(3, 32, 25, 20) == 0 and ws(0, 0, 25, 20) == 0 and ws(0, 1, 25, 257) == 0
+    assert ws(4, 32, 25, CW) == 0 and ws(0, 0, 25, 20) == 0 and ws(0, 1, 25, 257) == 0
+    # the combined call: the marginals workspace followed by the Viterbi workspace
+    assert ws(3, 32, 25, 20) == 0
+    assert ws(3, 32, 25, CW) == ws(1, 32, 25, CW) + ws(2, 32, 25, CW)
     # TS_PATH=tree forces the multi-launch tree for small C too
     monkeypatch.setenv("TS_PATH", "tree")
     assert ws(0, 32, 25, 20) >= 32 * (16 + 8 + 4 + 2 + 1) * 20 * 20 * 4
@@ -76,6 +79,8 @@ def test_bad_dimensions_are_rejected(L):
         assert L.ts_chain_logpartition(FAKE, None, B, N, C, FAKE, FAKE, 1 << 30, None) == BAD_DIM
         assert L.ts_chain_marginals(FAKE, None, B, N, C, FAKE, FAKE, FAKE, 1 << 30, None) == BAD_DIM
         assert L.ts_chain_viterbi(FAKE, None, B, N, C, FAKE, FAKE, FAKE, 1 << 30, None) == BAD_DIM
+        assert L.ts_chain_marginals_viterbi(FAKE, None, B, N, C, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                            1 << 30, None) == BAD_DIM
     assert "ts_chain_max_labels" in _err(L) or "must" in _err(L)
 
 
@@ -98,6 +103,18 @@ def test_null_pointers_are_rejected(L):
     need = binding.workspace_bytes(2, 2, 5, CW)
     assert L.ts_chain_viterbi(FAKE, None, 2, 5, CW, None, FAKE, FAKE, need, None) == NULL_ARG
     assert L.ts_chain_viterbi(FAKE, None, 2, 5, CW, FAKE, None, FAKE, need, None) == NULL_ARG
+    need = binding.workspace_bytes(3, 2, 5, CW)
+    mv = L.ts_chain_marginals_viterbi
+    assert mv(None, None, 2, 5, CW, FAKE, FAKE, FAKE, FAKE, FAKE, need, None) == NULL_ARG
+    assert mv(FAKE, None, 2, 5, CW, FAKE, None, FAKE, FAKE, FAKE, need, None) == NULL_ARG
+    assert "marg" in _err(L)
+    assert mv(FAKE, None, 2, 5, CW, FAKE, FAKE, None, FAKE, FAKE, need, None) == NULL_ARG
+    assert mv(FAKE, None, 2, 5, CW, FAKE, FAKE, FAKE, None, FAKE, need, None) == NULL_ARG
+    assert mv(FAKE, None, 2, 5, CW, FAKE, FAKE, FAKE, FAKE, None, need, None) == NULL_ARG
+    assert "ws" in _err(L)
+    assert mv(FAKE, None, 2, 5, CW, FAKE, FAKE, FAKE, FAKE, FAKE, need - 1, None) == WORKSPACE
+    assert mv(FAKE, None, 2, 5, CW, FAKE, FAKE, FAKE, FAKE, FAKE + 16, need, None) == WORKSPACE
+    assert mv(FAKE, None, 2, 5, 3, FAKE, FAKE, None, FAKE, None, 0, None) == NULL_ARG
     # the fused path (no workspace) still rejects missing outputs
     assert L.ts_chain_marginals(FAKE, None, 2, 5, 3, FAKE, None, None, 0, None) == NULL_ARG
     assert L.ts_chain_viterbi(FAKE, None, 2, 5, 3, None, FAKE, None, 0, None) == NULL_ARG
