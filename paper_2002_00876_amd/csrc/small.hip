@@ -28,11 +28,12 @@ constexpr int kSmallThreads = 1024;  // 16 waves
 constexpr int kSmallWaves = kSmallThreads / kWave;
 constexpr float kUnderflow = 0x1p-80f;
 
-typedef float f16v __attribute__((ext_vector_type(16)));
-
 __device__ __forceinline__ float& F(int off) { return ts_small_lds[off]; }
 __device__ __forceinline__ double& Dd(int off_floats) {
     return reinterpret_cast<double*>(ts_small_lds)[off_floats >> 1];
+}
+__device__ __forceinline__ unsigned short& H(int off_halves) {
+    return reinterpret_cast<unsigned short*>(ts_small_lds)[off_halves];
 }
 __device__ __forceinline__ int align4(int off) { return (off + 3) & ~3; }
 // values that are the same in every lane, moved to scalar registers
@@ -107,15 +108,6 @@ __device__ __forceinline__ void stage_leaves(const float* src, int dst, int n) {
     }
 }
 
-typedef float f4v __attribute__((ext_vector_type(4)));
-
-// team size for a level with np products on kSmallWaves waves: the largest power of two
-// <= waves / np, at most 4
-__device__ __forceinline__ int team_size(int np) {
-    const int per = kSmallWaves / max(np, 1);
-    return per >= 4 ? 4 : (per >= 2 ? 2 : 1);
-}
-
 // ================================================================== log semiring
 // Every node is kept in the form its consumer needs, so a product needs only exp + MFMA:
 //   LEFT operand  (left child of a product):  P[a][b] = ro[a] + core[a][b], max_b core[a][b] = 0
@@ -129,258 +121,303 @@ __device__ __forceinline__ int team_size(int np) {
 // and the producer then normalises P into the form of its own role.  S < 2^-80 (all
 // terms underflowed) is recomputed exactly by a direct max-shifted log-sum-exp over b.
 //
+// One wave computes a whole product as one MFMA tile (32 x 32 for CP > 16, 16 x 16
+// otherwise).  The tile's output layout gives each lane one column and a set of rows, so
+// a product that is normalised per column (RIGHT, and the root) is computed as P and one
+// normalised per row (LEFT) as its transpose P^T = R^T L^T: either way the lane owns the
+// line it normalises, and the reduction is over its own values plus the lanes holding the
+// same column.
+//
+// Labels are padded to CP.  A slot holds core [CP][CP + 1] (the odd row stride keeps the
+// strided operand reads free of bank conflicts), then ro [CP] and co [CP] as doubles.
+// Invariants, kept by every producer:
+//   * ro[i] = co[i] = -inf for C <= i < CP;
+//   * LEFT node: core[a][b] = -inf for a < C <= b;  RIGHT node: core[b][c] = -inf for
+//     c < C <= b, so the padded part of the contracted index contributes exp(-inf) = 0;
+//   * the other padding entries are never read: operand rows and columns are read through
+//     indices clamped to C - 1, which makes the padded part of a product a copy of valid
+//     entries (so the underflow test needs no mask).
+// Outside vectors (u, v) have CP entries with -inf padding.
+//
 // LDS layout (float offsets): slots [2E-1][slotF] (leaves are slots 0..E-1, products
-// follow level by level) | vectors [nodes][2][C] (u then v).  A slot holds core [C*C]
-// (padded to a multiple of 4), then ro [C] and co [C] as doubles.
+// follow level by level) | vectors [nodes][2][CP] (u then v) | per-wave scratch [16][64] |
+// node table (16-bit entries).
 constexpr int kLeft = 0, kRight = 1, kNone = 2;
 
-__device__ __forceinline__ int node_role(const Tree& T, int l, int k) {
-    while (l < T.D) {
+// nodes at level l of the tree over E >= 1 leaves: ceil(E / 2^l)
+__device__ __forceinline__ int lvl_n(int E, int l) { return ((E - 1) >> l) + 1; }
+
+// role of node (l, k), from E alone (register arithmetic, no table)
+__device__ __forceinline__ int role_of(int E, int l, int k) {
+    while ((E - 1) >> l) {   // level l has more than one node
         if (k & 1) return kRight;
-        if (k + 1 < T.n[l]) return kLeft;
+        if (k + 1 < lvl_n(E, l)) return kLeft;
         ++l;
         k >>= 1;
     }
     return kNone;
 }
 
+// slot of node (l, k): leaves are slots 0..E-1, products E + (products of levels < l) + k;
+// a node without a right child is its left child
+__device__ __forceinline__ int slot_of(int E, int l, int k) {
+    while (l > 0) {
+        if (k < lvl_n(E, l - 1) / 2) {
+            int base = E;
+            for (int q = 1; q < l; ++q) base += lvl_n(E, q - 1) / 2;
+            return base + k;
+        }
+        --l;
+        k *= 2;
+    }
+    return k;
+}
+
+// The node table: one 16-bit entry per node in level-major order (node (l, k) at
+// vbase[l] + k) holding its slot (bits 0..13) and role (bits 14..15).
+constexpr int kSlotMask = 0x3fff;
+
+__device__ void build_node_table(int E, int nodes, int info) {
+    for (int i = threadIdx.x; i < nodes; i += kSmallThreads) {
+        int l = 0, vb = 0;
+        while (i >= vb + lvl_n(E, l)) vb += lvl_n(E, l++);
+        const int k = i - vb;
+        H(info + i) = (unsigned short)(slot_of(E, l, k) | (role_of(E, l, k) << 14));
+    }
+}
+
+template <int CP>
 struct LogLayout {
-    int C, CC, slotF, coreF, vecs;
+    static constexpr int kLd = CP + 1;                          // core row stride
+    static constexpr int kCoreF = (CP * kLd + 1) & ~1;          // doubles stay 8-byte aligned
+    static constexpr int kSlotF = kCoreF + 4 * CP;
+    int C, vecs, scr, info;
     __device__ void init(int c, int E) {
         C = c;
-        CC = c * c;
-        coreF = align4(CC);
-        slotF = coreF + 4 * c;
-        vecs = (2 * E - 1) * slotF;
+        vecs = (2 * E - 1) * kSlotF;
+        scr = vecs + (int)small_tree_nodes(E) * 2 * CP;
+        info = 2 * (scr + kSmallWaves * 64);   // in halves
     }
-    __device__ int core(int slot) const { return slot * slotF; }
-    __device__ int ro(int slot) const { return slot * slotF + coreF; }   // doubles: ro, then co
-    __device__ int co(int slot) const { return slot * slotF + coreF + 2 * C; }
+    __device__ static int core(int slot) { return slot * kSlotF; }
+    __device__ static int ro(int slot) { return slot * kSlotF + kCoreF; }    // doubles
+    __device__ static int co(int slot) { return slot * kSlotF + kCoreF + 2 * CP; }
 };
 
-// slot of node (l, k): leaves are slots 0..E-1, products E + pbase[l] + k
-__device__ __forceinline__ int log_slot(const Tree& T, int l, int k) {
-    const int h = T.handle(l, k);
-    return h < 0 ? (-h - 1) : T.E + h;
+// max / sum of x over lanes l and l ^ 32 (the same value in both lanes)
+__device__ __forceinline__ float xor32_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                    false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
+__device__ __forceinline__ float xor32_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                    false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// MFMA tile of a CP-padded product: 32 x 32 x 2 (16 values per lane) or 16 x 16 x 4
+// (4 values per lane).  Value r of lane l sits at tile row row(r), column l % kT.
+template <int CP>
+struct Tile {
+    static constexpr int kT = CP > 16 ? 32 : 16;
+    static constexpr int kK = kT == 32 ? 2 : 4;      // contraction indices per step
+    static constexpr int kSteps = CP / kK;
+    static constexpr int kV = kT == 32 ? 16 : 4;     // values per lane
+    // values whose row lies below CP (rows grow with r for the 32-wide tile)
+    static constexpr int kVr = kT == 32 ? (CP / 2 < 16 ? CP / 2 : 16) : 4;
+    __device__ static int row(int r, int lane) {
+        return kT == 32 ? (r >> 2) * 8 + ((lane >> 5) << 2) + (r & 3) : ((lane >> 4) << 2) + r;
+    }
+};
 
 // Product of the LEFT node at slot sl and the RIGHT node at slot sr into slot sp, in the
-// form kRole.  Output blocks are 16 x 16 (v_mfma_f32_16x16x4f32): one block for CP <= 16
-// (member 0 only), four for CP > 16 shared by two waves -- by block rows when the result is
-// normalised per row (LEFT, NONE) and by block columns when per column (RIGHT), so each
-// wave holds whole rows (or columns) of what it normalises.
+// form kRole (one wave).
 template <int CP, int kRole>
-__device__ __forceinline__ void prod_log(const LogLayout& ly, int sl, int sr, int sp, int m) {
-    constexpr bool kTwo = CP > 16;
-    constexpr bool kColSplit = kTwo && kRole == kRight;
-    constexpr int kSteps = CP / 4;
+__device__ __forceinline__ void prod_log(const LogLayout<CP>& ly, int sl, int sr, int sp) {
+    using Ly = LogLayout<CP>;
+    using Tl = Tile<CP>;
+    constexpr int kT = Tl::kT, kLd = Ly::kLd;
+    constexpr bool kTrans = kRole == kLeft;   // compute P^T: lanes own rows of P
     const int C = ly.C;
-    const int Lc = ly.core(sl), Lro = ly.ro(sl);
-    const int Rc = ly.core(sr), Rco = ly.co(sr);
-    const int Pc = ly.core(sp), Pro = ly.ro(sp), Pco = ly.co(sp);
-    const int lane = threadIdx.x % kWave, l16 = lane & 15, kq = lane >> 4;
-    const int rb0 = kTwo ? (kColSplit ? 0 : 16 * m) : 0, cb0 = kColSplit ? 16 * m : 0;
-    const int rb1 = kColSplit ? 16 : rb0, cb1 = kColSplit ? cb0 : 16;
-    const int ia0 = rb0 + l16, ia1 = rb1 + l16, jb0 = cb0 + l16, jb1 = cb1 + l16;
-    // row / column base offsets (clamped into the matrix; masked below)
-    const int arow0 = Lc + min(ia0, C - 1) * C, arow1 = Lc + min(ia1, C - 1) * C;
-    const int bcol0 = Rc + min(jb0, C - 1), bcol1 = Rc + min(jb1, C - 1);
-    float av[kSteps], bv[kSteps], cv[kSteps];
+    const int lane = threadIdx.x % kWave, own = lane % kT, grp = lane / kT;
+    const int oc = min(own, C - 1);
+    const int Lc = Ly::core(sl), Rc = Ly::core(sr), Pc = Ly::core(sp);
+    // offsets of the values' own lines, read before the products so they overlap them:
+    // LEFT: co_R of each value's column, RIGHT: ro_L of each value's row
+    const int offBase = kRole == kLeft ? Ly::co(sr) : Ly::ro(sl);
+    const float mOff = kRole == kNone ? 0.f
+        : safe_shift(wave_max_fast(lane < C ? (float)Dd(offBase + 2 * min(lane, C - 1)) : -INFINITY));
+    float oh[Tl::kVr];
+    if constexpr (kRole != kNone) {
 #pragma unroll
-    for (int st = 0; st < kSteps; ++st) {
-        const int kc = min(4 * st + kq, C - 1);
-        av[st] = F(arow0 + kc);
-        bv[st] = F(bcol0 + kc * C);
-        if (kTwo) cv[st] = kColSplit ? F(arow1 + kc) : F(bcol1 + kc * C);
+        for (int r = 0; r < Tl::kVr; ++r)
+            oh[r] = (float)(Dd(offBase + 2 * min(Tl::row(r, lane), CP - 1)) - (double)mOff);
     }
-    f4v acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-    const bool a0ok = ia0 < C, b0ok = jb0 < C, c1ok = kColSplit ? ia1 < C : jb1 < C;
+    // operand values: L[own][k] and R[k][own], k = kK * st + grp
+    float lv[Tl::kSteps], rv[Tl::kSteps];
 #pragma unroll
-    for (int st = 0; st < kSteps; ++st) {
-        const bool kv = 4 * st + kq < C;
-        const float a0 = (kv && a0ok) ? fexp(av[st]) : 0.f;
-        const float b0 = (kv && b0ok) ? fexp(bv[st]) : 0.f;
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b0, acc0, 0, 0, 0);
-        if (kTwo) {
-            const float c = (kv && c1ok) ? fexp(cv[st]) : 0.f;
-            if (kColSplit) acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(c, b0, acc1, 0, 0, 0);
-            else acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, c, acc1, 0, 0, 0);
-        }
+    for (int st = 0; st < Tl::kSteps; ++st) {
+        const int k = Tl::kK * st + grp;
+        lv[st] = F(Lc + oc * kLd + k);
+        rv[st] = F(Rc + k * kLd + oc);
     }
-    // log S; lane-held entries: block X rows rbX + 4 kq + r, column cbX + l16
-    constexpr int kB = kTwo ? 2 : 1;
-    float ls[kB][4];
-    bool need = false;
+    typedef float accv __attribute__((ext_vector_type(Tl::kV)));
+    accv acc = {};
 #pragma unroll
-    for (int x = 0; x < kB; ++x)
+    for (int st = 0; st < Tl::kSteps; ++st) {
+        const float el = fexp(lv[st]), er = fexp(rv[st]);
+        if constexpr (kT == 32)
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(kTrans ? er : el, kTrans ? el : er, acc, 0, 0, 0);
+        else
+            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(kTrans ? er : el, kTrans ? el : er, acc, 0, 0, 0);
+    }
+    // log S; the padded part of the tile copies valid entries, so every value is tested
+    float x[Tl::kVr];
+    float smin = INFINITY;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const float S = x ? acc1[r] : acc0[r];
-            const int row = (x ? rb1 : rb0) + 4 * kq + r, col = x ? jb1 : jb0;
-            ls[x][r] = flog(S);
-            need |= row < C && col < C && !(S >= kUnderflow);
-        }
-    if (need) {   // some entry underflowed (or is padding): exact recomputation
+    for (int r = 0; r < Tl::kVr; ++r) {
+        x[r] = flog(acc[r]);
+        smin = fminf(smin, acc[r]);
+    }
+    if (__builtin_amdgcn_ballot_w64(!(smin >= kUnderflow))) {
+        // exact recomputation of underflowed entries: LSE_b core_L[a][b] + core_R[b][c]
 #pragma unroll
-        for (int x = 0; x < kB; ++x)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int row = (x ? rb1 : rb0) + 4 * kq + r, col = x ? jb1 : jb0;
-                const float S = x ? acc1[r] : acc0[r];
-                if (!(S >= kUnderflow) && row < C && col < C) {
-                    float q = -INFINITY;
-                    for (int k = 0; k < C; ++k) q = fmaxf(q, F(Lc + row * C + k) + F(Rc + k * C + col));
-                    float v = -INFINITY;
-                    if (q != -INFINITY) {
-                        float s = 0.f;
-                        for (int k = 0; k < C; ++k) s += fexp(F(Lc + row * C + k) + F(Rc + k * C + col) - q);
-                        v = q + flog(s);
-                    }
-                    ls[x][r] = v;
+        for (int r = 0; r < Tl::kVr; ++r) {
+            if (!(acc[r] >= kUnderflow)) {
+                const int other = min(Tl::row(r, lane), C - 1);
+                const int a = kTrans ? oc : other, c = kTrans ? other : oc;
+                float q = -INFINITY;
+                for (int k = 0; k < C; ++k) q = fmaxf(q, F(Lc + a * kLd + k) + F(Rc + k * kLd + c));
+                float v = -INFINITY;
+                if (q != -INFINITY) {
+                    float s = 0.f;
+                    for (int k = 0; k < C; ++k) s += fexp(F(Lc + a * kLd + k) + F(Rc + k * kLd + c) - q);
+                    v = q + flog(s);
                 }
+                x[r] = v;
             }
+        }
     }
-    const int lc = min(lane, C - 1);
-    if constexpr (kRole == kLeft) {
-        // P[a][c] = ro_L[a] + co_R[c] + log S: fold co_R (shifted) in, then shift each row to max 0
-        const float mco = safe_shift(wave_max_fast(lane < C ? (float)Dd(Rco + 2 * lc) : -INFINITY));
-        float coh[kB];
-        coh[0] = (float)(Dd(Rco + 2 * min(jb0, C - 1)) - (double)mco);
-        if (kTwo) coh[kB - 1] = (float)(Dd(Rco + 2 * min(jb1, C - 1)) - (double)mco);
+    const bool rowsOk = kT == 32 || Tl::row(0, lane) < CP;   // 16-wide tile, CP = 8
+    if constexpr (kRole == kNone) {
+        // the root: P = log S (offsets copied), no normalisation
+        if (own < CP && rowsOk) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int row = rb0 + 4 * kq + r;
-            float x0 = b0ok ? ls[0][r] + coh[0] : -INFINITY;
-            float x1 = (kTwo && jb1 < C) ? ls[kB - 1][r] + coh[kB - 1] : -INFINITY;
-            float mx = fmaxf(x0, x1);
-            mx = fmaxf(mx, dpp_f(mx, 0xB1));
-            mx = fmaxf(mx, dpp_f(mx, 0x4E));
-            mx = fmaxf(mx, dpp_f(mx, 0x141));
-            mx = fmaxf(mx, dpp_f(mx, 0x140));
-            const float sh = safe_shift(mx);
-            if (row < C) {
-                if (b0ok) F(Pc + row * C + jb0) = x0 - sh;
-                if (kTwo && jb1 < C) F(Pc + row * C + jb1) = x1 - sh;
-                if (l16 == 0) Dd(Pro + 2 * row) = Dd(Lro + 2 * row) + (double)mco + (double)sh;
-            }
+            for (int r = 0; r < Tl::kVr; ++r) F(Pc + Tl::row(r, lane) * kLd + own) = x[r];
         }
-        if (m == 0 && lane < C) Dd(Pco + 2 * lane) = 0.0;
-    } else if constexpr (kRole == kRight) {
-        // fold ro_L (shifted) in, then shift each column to max 0
-        const float mro = safe_shift(wave_max_fast(lane < C ? (float)Dd(Lro + 2 * lc) : -INFINITY));
-        float xs[kB][4];
-        float mx = -INFINITY;
-#pragma unroll
-        for (int x = 0; x < kB; ++x)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int row = (x ? rb1 : rb0) + 4 * kq + r;
-                const float roh = (float)(Dd(Lro + 2 * min(row, C - 1)) - (double)mro);
-                xs[x][r] = row < C ? ls[x][r] + roh : -INFINITY;
-                mx = fmaxf(mx, xs[x][r]);
-            }
-        mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-        const float sh = safe_shift(mx);
-        if (b0ok) {
-#pragma unroll
-            for (int x = 0; x < kB; ++x)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int row = (x ? rb1 : rb0) + 4 * kq + r;
-                    if (row < C) F(Pc + row * C + jb0) = xs[x][r] - sh;
-                }
-            if (kq == 0) Dd(Pco + 2 * jb0) = Dd(Rco + 2 * jb0) + (double)mro + (double)sh;
+        if (lane < CP) {
+            Dd(Ly::ro(sp) + 2 * lane) = Dd(Ly::ro(sl) + 2 * lane);
+            Dd(Ly::co(sp) + 2 * lane) = Dd(Ly::co(sr) + 2 * lane);
         }
-        if (m == 0 && lane < C) Dd(Pro + 2 * lane) = 0.0;
     } else {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int row = rb0 + 4 * kq + r;
-            if (row < C) {
-                if (b0ok) F(Pc + row * C + jb0) = ls[0][r];
-                if (kTwo && jb1 < C) F(Pc + row * C + jb1) = ls[kB - 1][r];
-            }
-        }
-        if (m == 0 && lane < C) {
-            Dd(Pro + 2 * lane) = Dd(Lro + 2 * lane);
-            Dd(Pco + 2 * lane) = Dd(Rco + 2 * lane);
-        }
-    }
-}
-
-// Put a staged leaf (raw potentials in slot t, ro = co = 0) into the form of its role.
-template <int CP>
-__device__ void normalise_leaf(int C, int slot, int role, int slotF, int coreF) {
-    const int lane = threadIdx.x % kWave;
-    const int c0 = slot * slotF, ro = c0 + coreF, co = ro + 2 * C;
-    const int x = min(lane, C - 1);
-    if (role == kNone) {
-        if (lane < C) {
-            Dd(ro + 2 * lane) = 0.0;
-            Dd(co + 2 * lane) = 0.0;
-        }
-        wave_sync();
-        return;
-    }
-    // LEFT: lane x owns row x; RIGHT: lane x owns column x.  Loads are unconditional
-    // (indices clamped into the matrix) so they issue back to back.
-    const int base = role == kLeft ? c0 + x * C : c0 + x;
-    const int stride = role == kLeft ? 1 : C;
-    float v[CP];
-#pragma unroll
-    for (int j = 0; j < CP; ++j) v[j] = F(base + min(j, C - 1) * stride);
-    float m = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < CP; ++j) m = fmaxf(m, v[j]);   // entries past C repeat entry C-1
-    const float sh = safe_shift(m);
-    if (lane < C) {
-#pragma unroll
-        for (int j = 0; j < CP; ++j)
-            if (j < C) F(base + j * stride) = v[j] - sh;
-        Dd((role == kLeft ? ro : co) + 2 * lane) = (double)sh;
-        Dd((role == kLeft ? co : ro) + 2 * lane) = 0.0;
-    }
-    wave_sync();
-}
-
-// One wave, C <= CP <= 32, node N[a][b] = ro[a] + co[b] + core[a][b] at LDS offsets
-// (Nc, Nro; co follows ro).  kRowSide == false: y[j] = LSE_i x[i] + N[i][j] (y = x (x) N);
-// kRowSide == true: y[i] = LSE_j N[i][j] + x[j] (y = N (x) x).  y is shifted to max 0.
-template <int CP, bool kRowSide>
-__device__ void wave_vec_log(int C, int x, int Nc, int Nro, int y, int scr) {
-    const int lane = threadIdx.x % kWave;
-    // x on the left pairs with ro and the result picks up co; on the right the reverse
-    const int inOff = kRowSide ? 2 * C : 0, outOff = kRowSide ? 0 : 2 * C;
-    double w = -INFINITY;
-    if (lane < C) w = (double)F(x + lane) + Dd(Nro + inOff + 2 * lane);
-    const double ws = (double)safe_shift(wave_max_fast((float)w));
-    if (lane < C) F(scr + lane) = (w == -INFINITY) ? -INFINITY : (float)(w - ws);
-    wave_sync();
-    double z = -INFINITY;
-    {
-        const int lc = min(lane, C - 1);
-        float e[CP];
-#pragma unroll
-        for (int t = 0; t < CP; ++t) {
-            const int tc = min(t, C - 1);
-            e[t] = F(scr + tc) + (kRowSide ? F(Nc + lc * C + tc) : F(Nc + tc * C + lc));
-        }
+        // fold the shifted offsets of the other index in, then shift the lane's line to max 0
         float m = -INFINITY;
 #pragma unroll
-        for (int t = 0; t < CP; ++t) {
-            e[t] = t < C ? e[t] : -INFINITY;
-            m = fmaxf(m, e[t]);
+        for (int r = 0; r < Tl::kVr; ++r) {
+            x[r] += oh[r];
+            m = fmaxf(m, x[r]);
         }
-        if (m != -INFINITY && lane < C) {
-            float s = 0.f;
+        if constexpr (kT == 32) {
+            m = xor32_max(m);
+        } else {
+            m = fmaxf(m, __shfl_xor(m, 16, kWave));
+            m = fmaxf(m, __shfl_xor(m, 32, kWave));
+        }
+        // lines past C become -inf (shift by +inf): the padding invariant
+        const float sh = own < C ? safe_shift(m) : INFINITY;
+        if (own < CP && rowsOk) {
 #pragma unroll
-            for (int t = 0; t < CP; ++t) s += fexp(e[t] - m);
-            z = Dd(Nro + outOff + 2 * lane) + (double)(m + flog(s));
+            for (int r = 0; r < Tl::kVr; ++r) {
+                const int o = Tl::row(r, lane);
+                F(Pc + (kTrans ? own * kLd + o : o * kLd + own)) = x[r] - sh;
+            }
+        }
+        if (lane < CP) {
+            // the lane's line offset picks up the other side's max and the shift; the other
+            // offset is 0 (padding -inf)
+            const int keep = kTrans ? Ly::ro(sl) : Ly::co(sr);
+            const int mine = kTrans ? Ly::ro(sp) : Ly::co(sp);
+            const int zero = kTrans ? Ly::co(sp) : Ly::ro(sp);
+            Dd(mine + 2 * lane) = lane < C ? Dd(keep + 2 * lane) + (double)mOff + (double)sh : -INFINITY;
+            Dd(zero + 2 * lane) = lane < C ? 0.0 : -INFINITY;
         }
     }
+}
+
+// Leaves straight from global memory into the form of their roles: one thread per line
+// (row of a LEFT or NONE leaf, column of a RIGHT leaf), which it shifts to max 0 (not the
+// NONE leaf of a one-edge sequence) and whose shift it records as ro (LEFT) or co (RIGHT);
+// the other offset is 0.  Lines C..CP-1 and entries C..CP-1 of a line are -inf, so a leaf's
+// whole padding is -inf.
+template <int CP>
+__device__ void load_leaves(const LogLayout<CP>& ly, const float* gleaf, int E) {
+    using Ly = LogLayout<CP>;
+    constexpr int kLd = Ly::kLd;
+    const int C = ly.C, CC = C * C;
+    for (int i = threadIdx.x; i < E * CP; i += kSmallThreads) {
+        const int t = i / CP, r = i - t * CP;
+        const int role = role_of(E, 0, t);
+        const bool col = role == kRight, pad = r >= C;
+        const int rc = min(r, C - 1);
+        const float* line = gleaf + (size_t)t * CC + (col ? rc : rc * C);
+        const int stride = col ? C : 1;
+        float v[CP];
+#pragma unroll
+        for (int j = 0; j < CP; ++j) v[j] = line[min(j, C - 1) * stride];
+        float m = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < CP; ++j) {
+            v[j] = (j < C && !pad) ? v[j] : -INFINITY;
+            m = fmaxf(m, v[j]);
+        }
+        const float sh = role == kNone ? 0.f : safe_shift(m);
+        const int base = Ly::core(t) + (col ? r : r * kLd);
+        const int step = col ? kLd : 1;
+#pragma unroll
+        for (int j = 0; j < CP; ++j) F(base + j * step) = v[j] - sh;
+        const int ro = Ly::ro(t), co = Ly::co(t);
+        Dd((col ? co : ro) + 2 * r) = pad ? -INFINITY : (double)sh;
+        Dd((col ? ro : co) + 2 * r) = pad ? -INFINITY : 0.0;
+    }
+}
+
+// One wave: outside-vector product with the node at `slot` (N[i][j] = ro[i] + co[j] +
+// core[i][j]).  kRowSide == false: y[j] = LSE_i x[i] + N[i][j] (y = x (x) N);
+// kRowSide == true: y[i] = LSE_j N[i][j] + x[j] (y = N (x) x).  y is shifted to max 0 and
+// its padding is -inf.  Lane l computes output l % 32 over half l / 32 of the index.
+template <int CP, bool kRowSide>
+__device__ void vec_log(const LogLayout<CP>& ly, int x, int slot, int y, int scr) {
+    using Ly = LogLayout<CP>;
+    constexpr int kLd = Ly::kLd, kHalf = CP / 2;
+    const int C = ly.C;
+    const int lane = threadIdx.x % kWave, o = lane & 31, h = lane >> 5;
+    const int Nc = Ly::core(slot);
+    // x on the left pairs with ro and the result picks up co; on the right the reverse
+    const int inOff = kRowSide ? Ly::co(slot) : Ly::ro(slot);
+    const int outOff = kRowSide ? Ly::ro(slot) : Ly::co(slot);
+    const int li = min(lane, CP - 1);
+    const double w = lane < CP ? (double)F(x + li) + Dd(inOff + 2 * li) : -INFINITY;
+    const double ws = (double)safe_shift(wave_max_fast((float)w));
+    if (lane < CP) F(scr + lane) = (float)(w - ws);
+    wave_sync();
+    const int oc = min(o, C - 1);
+    float e[kHalf];
+#pragma unroll
+    for (int q = 0; q < kHalf; ++q) {
+        const int t = h * kHalf + q;
+        e[q] = F(scr + t) + (kRowSide ? F(Nc + oc * kLd + t) : F(Nc + t * kLd + oc));
+    }
+    float m = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < kHalf; ++q) m = fmaxf(m, e[q]);
+    m = safe_shift(xor32_max(m));
+    float s = 0.f;
+#pragma unroll
+    for (int q = 0; q < kHalf; ++q) s += fexp(e[q] - m);
+    s = xor32_sum(s);
+    const double z = (o < C && s > 0.f) ? Dd(outOff + 2 * oc) + (double)(m + flog(s)) : -INFINITY;
     const double zs = (double)safe_shift(wave_max_fast((float)z));
-    if (lane < C) F(y + lane) = (z == -INFINITY) ? -INFINITY : (float)(z - zs);
+    if (h == 0 && o < CP) F(y + o) = (float)(z - zs);
     wave_sync();
 }
 
@@ -395,10 +432,12 @@ struct SmallLogArgs {
 
 template <int CP>
 __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int64_t b) {
+    using Ly = LogLayout<CP>;
+    constexpr int kLd = Ly::kLd;
     const int C = a.C;
     const int64_t E = a.N - 1;
     const int Eb = (int)(clamp_len(a.lengths, b, a.N) - 1);
-    const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int w = uni(threadIdx.x / kWave), lane = threadIdx.x % kWave;
     const int CC = C * C;
     const float* gleaf = a.pot + (size_t)b * E * CC;
     if (a.marg) {  // padding edges are exactly zero
@@ -412,50 +451,34 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
     }
     __shared__ Tree T;
     if (threadIdx.x == 0) T.init(Eb);
-    LogLayout ly;
+    Ly ly;
     ly.init(C, Eb);
-    // ---- stage the valid edges into slots 0..Eb-1 (8 loads in flight per thread)
-    {
-        const int n = Eb * CC;
-        for (int base = 0; base < n; base += 8 * kSmallThreads) {
-            float v[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = gleaf[min(base + u * kSmallThreads + (int)threadIdx.x, n - 1)];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const int idx = base + u * kSmallThreads + threadIdx.x;
-                if (idx < n) {
-                    const int t = idx / CC;
-                    F(t * ly.slotF + idx - t * CC) = v[u];
-                }
-            }
-        }
-    }
+    // ---- leaves (global -> LDS, normalised) and the node table
+    load_leaves<CP>(ly, gleaf, Eb);
+    build_node_table(Eb, (int)small_tree_nodes(Eb), ly.info);
     __syncthreads();
-    for (int t = w; t < Eb; t += kSmallWaves)
-        normalise_leaf<CP>(C, t, node_role(T, 0, t), ly.slotF, ly.coreF);
-    __syncthreads();
-    // ---- up-sweep: one wave per product (two for CP > 16)
-    constexpr int kPer = CP > 16 ? 2 : 1;
+    // ---- up-sweep: one wave per product
     for (int l = 1; l <= T.D; ++l) {
-        const int np = T.products(l);
-        for (int task = w; task < np * kPer; task += kSmallWaves) {
-            const int k = task / kPer, m = task % kPer;
-            const int sl = log_slot(T, l - 1, 2 * k), sr = log_slot(T, l - 1, 2 * k + 1);
-            const int sp = T.E + T.pbase[l] + k, role = node_role(T, l, k);
-            if (role == kLeft) prod_log<CP, kLeft>(ly, sl, sr, sp, m);
-            else if (role == kRight) prod_log<CP, kRight>(ly, sl, sr, sp, m);
-            else prod_log<CP, kNone>(ly, sl, sr, sp, m);
+        const int np = uni(T.products(l));
+        const int vb0 = uni(T.vbase[l - 1]), vb1 = uni(T.vbase[l]);
+        for (int k = w; k < np; k += kSmallWaves) {
+            const int sl = uni(H(ly.info + vb0 + 2 * k)) & kSlotMask;
+            const int sr = uni(H(ly.info + vb0 + 2 * k + 1)) & kSlotMask;
+            const int ip = uni(H(ly.info + vb1 + k));
+            const int sp = ip & kSlotMask, role = ip >> 14;
+            if (role == kLeft) prod_log<CP, kLeft>(ly, sl, sr, sp);
+            else if (role == kRight) prod_log<CP, kRight>(ly, sl, sr, sp);
+            else prod_log<CP, kNone>(ly, sl, sr, sp);
             wave_sync();
         }
         __syncthreads();
     }
-    const int rslot = log_slot(T, T.D, 0);
-    auto U = [&](int l, int k) { return ly.vecs + (T.vbase[l] + k) * 2 * C; };
+    const int rslot = uni(H(ly.info + T.vbase[T.D])) & kSlotMask;
+    auto U = [&](int l, int k) { return ly.vecs + (T.vbase[l] + k) * 2 * CP; };
     // ---- root: log Z = LSE_{a,c} ro[a] + co[c] + core[a][c]   (last wave, overlapping
     // the first outside level, which does not need it)
     if (a.logZ && w == kSmallWaves - 1) {
-        const int rc = ly.core(rslot), rr = ly.ro(rslot), rcc = ly.co(rslot);
+        const int rc = Ly::core(rslot), rr = Ly::ro(rslot), rcc = Ly::co(rslot);
         const int lc = min(lane, C - 1);
         const double rs = (double)safe_shift(wave_max_fast(lane < C ? (float)Dd(rr + 2 * lc) : -INFINITY));
         const double cs = (double)safe_shift(wave_max_fast(lane < C ? (float)Dd(rcc + 2 * lc) : -INFINITY));
@@ -466,7 +489,7 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
 #pragma unroll
         for (int q = 0; q < kRows; ++q) {
             const int ic = min(i0 + 2 * q, C - 1);
-            x[q] = F(rc + ic * C + jc) + (float)(Dd(rr + 2 * ic) - rs) + cj;
+            x[q] = F(rc + ic * kLd + jc) + (float)(Dd(rr + 2 * ic) - rs) + cj;
         }
         float m = -INFINITY;
 #pragma unroll
@@ -485,53 +508,52 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
             a.logZ[b] = (m == -INFINITY) ? -INFINITY : (float)(rs + cs + (double)(m + flog(s)));
     }
     if (!a.marg) return;
-    // ---- outside sweep: u, v of every node (root: zeros)
-    if (w < kSmallWaves - 1 || !a.logZ)
-        for (int idx = lane; idx < 2 * C; idx += kWave)
-            if (w == 0) F(U(T.D, 0) + idx) = 0.f;
+    // ---- outside sweep: u, v of every node (root: zeros, padding -inf)
+    if (w == 0)
+        for (int idx = lane; idx < 2 * CP; idx += kWave)
+            F(U(T.D, 0) + idx) = (idx % CP) < C ? 0.f : -INFINITY;
     __syncthreads();
-    const int scr = ly.vecs + T.nodes * 2 * C + w * 64;
+    const int scr = ly.scr + w * 64;
     for (int l = T.D; l >= 1; --l) {
-        const int nn = T.n[l];
+        const int nn = uni(T.n[l]), nprev = uni(T.n[l - 1]), vb0 = uni(T.vbase[l - 1]);
+        const int ub = uni(U(l, 0)), ub0 = uni(U(l - 1, 0));
         for (int task = w; task < 3 * nn; task += kSmallWaves) {
-            const int k = task / 3, which = task % 3;
-            const bool right = 2 * k + 1 < T.n[l - 1];
-            const int uN = U(l, k), vN = uN + C;
+            const int k = task / 3, which = task - 3 * k;
+            const bool right = 2 * k + 1 < nprev;
+            const int uN = ub + k * 2 * CP, vN = uN + CP;
+            const int uL = ub0 + 2 * k * 2 * CP, uR = uL + 2 * CP;
             if (which == 0) {
-                if (lane < C) {
-                    F(U(l - 1, 2 * k) + lane) = F(uN + lane);
-                    if (right) F(U(l - 1, 2 * k + 1) + C + lane) = F(vN + lane);
-                    else F(U(l - 1, 2 * k) + C + lane) = F(vN + lane);
+                if (lane < CP) {
+                    F(uL + lane) = F(uN + lane);
+                    if (right) F(uR + CP + lane) = F(vN + lane);
+                    else F(uL + CP + lane) = F(vN + lane);
                 }
             } else if (which == 1 && right) {   // u_R = u_N (x) L
-                const int sl = log_slot(T, l - 1, 2 * k);
-                wave_vec_log<CP, false>(C, uN, ly.core(sl), ly.ro(sl), U(l - 1, 2 * k + 1), scr);
+                const int sl = uni(H(ly.info + vb0 + 2 * k)) & kSlotMask;
+                vec_log<CP, false>(ly, uN, sl, uR, scr);
             } else if (which == 2 && right) {   // v_L = R (x) v_N
-                const int sr = log_slot(T, l - 1, 2 * k + 1);
-                wave_vec_log<CP, true>(C, vN, ly.core(sr), ly.ro(sr), U(l - 1, 2 * k) + C, scr);
+                const int sr = uni(H(ly.info + vb0 + 2 * k + 1)) & kSlotMask;
+                vec_log<CP, true>(ly, vN, sr, uL + CP, scr);
             }
         }
         __syncthreads();
     }
-    // ---- marginals with a per-edge normaliser n_t; the raw edge is re-read from global
-    // memory (L2).  Lane -> column j = lane & 31 and rows (lane >> 5) + 2q.
+    // ---- marginals with a per-edge normaliser n_t, from the leaves kept in LDS:
+    // l[i][j] = ro[i] + co[j] + core[i][j].  Lane -> column j = lane & 31 and rows
+    // (lane >> 5) + 2q.
     constexpr int kRows = CP / 2;
     const int j = lane & 31, i0 = lane >> 5, jc = min(j, C - 1);
     for (int t = w; t < Eb; t += kSmallWaves) {
-        const int al = U(0, t), be = al + C;
-        const float* leaf = gleaf + (size_t)t * CC;
-        const float bj = F(be + jc);
+        const int al = U(0, t), be = al + CP;
+        const int lc = Ly::core(t), lro = Ly::ro(t), lco = Ly::co(t);
+        const float bj = F(be + jc) + (float)Dd(lco + 2 * jc);
         float x[kRows];
-#pragma unroll
-        for (int q = 0; q < kRows; ++q) {
-            const int i = i0 + 2 * q, ic = min(i, C - 1);
-            x[q] = leaf[ic * C + jc];
-        }
         float m = -INFINITY;
 #pragma unroll
         for (int q = 0; q < kRows; ++q) {
             const int i = i0 + 2 * q, ic = min(i, C - 1);
-            x[q] = (i < C && j < C) ? F(al + ic) + x[q] + bj : -INFINITY;
+            const float v = F(al + ic) + (float)Dd(lro + 2 * ic) + F(lc + ic * kLd + jc) + bj;
+            x[q] = (i < C && j < C) ? v : -INFINITY;
             m = fmaxf(m, x[q]);
         }
         m = wave_max_fast(m);
@@ -788,9 +810,10 @@ __global__ __launch_bounds__(kSmallThreads) void k_small_both(SmallLogArgs la, S
 // uses a prefix of each region, so the offsets computed in the kernels stay inside.
 size_t small_log_lds_bytes(int64_t E, int64_t C) {
     if (E < 1) return 0;
-    const int64_t slotF = ((C * C + 3) & ~3) + 4 * C;
-    const int64_t floats = (2 * E - 1) * slotF + small_tree_nodes(E) * 2 * C + kSmallWaves * 64;
-    return sizeof(float) * (size_t)floats;
+    const int64_t CP = C <= 8 ? 8 : C <= 16 ? 16 : C <= 24 ? 24 : 32;   // as the launcher
+    const int64_t coreF = (CP * (CP + 1) + 1) & ~1, slotF = coreF + 4 * CP;
+    const int64_t floats = (2 * E - 1) * slotF + small_tree_nodes(E) * 2 * CP + kSmallWaves * 64;
+    return sizeof(float) * (size_t)floats + 2 * (size_t)small_tree_nodes(E);   // + node table
 }
 
 size_t small_max_lds_bytes(int64_t E, int64_t C) {
