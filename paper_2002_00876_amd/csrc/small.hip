@@ -81,33 +81,6 @@ struct Tree {
     }
 };
 
-// coalesced copy of a sequence's valid edges into LDS, several loads in flight per thread
-__device__ __forceinline__ void stage_leaves(const float* src, int dst, int n) {
-    const int tid = threadIdx.x, nt = blockDim.x;
-    if ((((uintptr_t)src) & 15) == 0 && (n & 3) == 0 && (dst & 3) == 0) {
-        const float4* s4 = (const float4*)src;
-        float4* d4 = reinterpret_cast<float4*>(ts_small_lds + dst);
-        const int n4 = n / 4;
-        for (int base = 0; base < n4; base += 4 * nt) {
-            float4 v[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) v[u] = s4[min(base + u * nt + tid, n4 - 1)];
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-                if (base + u * nt + tid < n4) d4[base + u * nt + tid] = v[u];
-        }
-    } else {
-        for (int base = 0; base < n; base += 8 * nt) {
-            float v[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = src[min(base + u * nt + tid, n - 1)];
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-                if (base + u * nt + tid < n) F(dst + base + u * nt + tid) = v[u];
-        }
-    }
-}
-
 // ================================================================== log semiring
 // Every node is kept in the form its consumer needs, so a product needs only exp + MFMA:
 //   LEFT operand  (left child of a product):  P[a][b] = ro[a] + core[a][b], max_b core[a][b] = 0
@@ -158,31 +131,33 @@ __device__ __forceinline__ int role_of(int E, int l, int k) {
     return kNone;
 }
 
-// slot of node (l, k): leaves are slots 0..E-1, products E + (products of levels < l) + k;
-// a node without a right child is its left child
-__device__ __forceinline__ int slot_of(int E, int l, int k) {
-    while (l > 0) {
-        if (k < lvl_n(E, l - 1) / 2) {
-            int base = E;
-            for (int q = 1; q < l; ++q) base += lvl_n(E, q - 1) / 2;
-            return base + k;
-        }
-        --l;
-        k *= 2;
-    }
-    return k;
-}
-
 // The node table: one 16-bit entry per node in level-major order (node (l, k) at
-// vbase[l] + k) holding its slot (bits 0..13) and role (bits 14..15).
+// vbase[l] + k) holding its slot (bits 0..13) and role (bits 14..15).  Leaves are slots
+// 0..E-1; the products of level l follow those of the levels below (slots from
+// pbase[l] = E + sum_{q<l} n[q-1] / 2); a node without a right child is its left child.
+// One pass per node with running sums, register arithmetic only.
 constexpr int kSlotMask = 0x3fff;
 
 __device__ void build_node_table(int E, int nodes, int info) {
     for (int i = threadIdx.x; i < nodes; i += kSmallThreads) {
-        int l = 0, vb = 0;
-        while (i >= vb + lvl_n(E, l)) vb += lvl_n(E, l++);
+        int l = 0, vb = 0, n = E, nprev = 0, pb = E;   // pb = pbase[l] once l >= 1
+        while (i >= vb + n) {
+            if (l >= 1) pb += nprev / 2;
+            vb += n;
+            nprev = n;
+            n = (n + 1) / 2;
+            ++l;
+        }
         const int k = i - vb;
-        H(info + i) = (unsigned short)(slot_of(E, l, k) | (role_of(E, l, k) << 14));
+        // follow the left-child chain down to a product or a leaf
+        int ll = l, kk = k;
+        while (ll > 0 && kk >= lvl_n(E, ll - 1) / 2) {
+            --ll;
+            kk *= 2;
+            if (ll > 0) pb -= lvl_n(E, ll - 1) / 2;
+        }
+        const int slot = ll == 0 ? kk : pb + kk;
+        H(info + i) = (unsigned short)(slot | (role_of(E, l, k) << 14));
     }
 }
 
@@ -576,10 +551,11 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
 // ================================================================== max semiring
 // LDS layout (float offsets): leaves fp32 [E][C][C] | product slots fp64 [E-1][C][C] |
 // last leaf again in fp64 [C][C] | forward scores fp64 [nodes][C] | last scores fp64 [C] |
-// backpointers u8 [E][C].  Above level 1 the only leaf that can still be an operand is the
-// last one (through nodes whose right half is padding), so levels >= 2 read fp64 only.
+// node table (16-bit slots, as for the log semiring) | backpointers u8 [E][C].  Above
+// level 1 the only leaf that can still be an operand is the last one (through nodes whose
+// right half is padding), so levels >= 2 read fp64 only.
 struct MaxLayout {
-    int C, CC, leaves, slots, lastc, vecs, dlast, bp;
+    int C, CC, leaves, slots, lastc, vecs, dlast, info, bp;
     __device__ void init(int c, int E, int nodes) {
         C = c;
         CC = c * c;
@@ -588,11 +564,24 @@ struct MaxLayout {
         lastc = slots + (E - 1) * CC * 2;
         vecs = lastc + CC * 2;
         dlast = vecs + nodes * c * 2;
-        bp = dlast + 2 * c;
+        info = 2 * (dlast + 2 * c);             // in halves
+        bp = align4(dlast + 2 * c + (nodes + 1) / 2);
+    }
+    // fp64 node of a level >= 1 node-table slot: a product slot or the last leaf
+    __device__ int node64(int slot, int E) const {
+        return slot < E ? lastc : slots + (slot - E) * CC * 2;
     }
 };
 
-// element idx of a node: a leaf in fp32 or a product slot in fp64
+// quotient x / d for 0 <= x < 2^22 and 1 <= d, with inv = 1.0f / d (float estimate, then
+// corrected, so it is exact)
+__device__ __forceinline__ int fdiv(int x, int d, float inv) {
+    int q = (int)((float)x * inv);
+    q -= q * d > x;
+    q += (q + 1) * d <= x;
+    return q;
+}
+
 template <bool kLeaf>
 __device__ __forceinline__ double mx(int base, int idx) {
     if constexpr (kLeaf) return (double)F(base + idx);
@@ -600,48 +589,63 @@ __device__ __forceinline__ double mx(int base, int idx) {
 }
 
 // All products of level l, P = L (x) R in (max, +), float64, by the whole workgroup: every
-// thread owns MR x MC output entries of one product (register-tiled loop over the inner
-// index).  kLeaves: the operands are leaves (level 1, fp32); otherwise fp64 slots.
+// thread owns MR x MC output entries of one product (consecutive threads take consecutive
+// column tiles, so reads of R are contiguous across lanes and reads of L shared).  The
+// inner index q runs in batches of kB with every read of a batch issued together, then the
+// remainder; entries past C read neighbouring data and are not stored.  kLeaves: level 1
+// (fp32 leaves).
 template <int MR, int MC, bool kLeaves>
-__device__ void block_prod_max(const MaxLayout& ly, const Tree& T, int l) {
+__device__ void block_prod_max(const MaxLayout& ly, int E, int np, int vb0, int pbase) {
+    constexpr int kS = kLeaves ? 1 : 2;   // floats per element
+    constexpr int kB = MR * MC >= 8 ? 4 : 8;
     const int C = ly.C, CC = ly.CC;
     const int TR = (C + MR - 1) / MR, TC = (C + MC - 1) / MC, tpp = TR * TC;
-    const int total = T.products(l) * tpp;
+    const float invTpp = 1.f / (float)tpp, invTc = 1.f / (float)TC;
+    const int total = np * tpp;
     for (int tile = threadIdx.x; tile < total; tile += kSmallThreads) {
-        const int k = tile / tpp, rem = tile - k * tpp, tr = rem / TC, tc = rem - tr * TC;
-        const int hl = T.handle(l - 1, 2 * k), hr = T.handle(l - 1, 2 * k + 1);
-        int lb, rb;
-        if constexpr (kLeaves) {
-            lb = ly.leaves + (-hl - 1) * CC;
-            rb = ly.leaves + (-hr - 1) * CC;
-        } else {
-            lb = hl < 0 ? ly.lastc : ly.slots + hl * CC * 2;
-            rb = hr < 0 ? ly.lastc : ly.slots + hr * CC * 2;
-        }
+        const int k = fdiv(tile, tpp, invTpp), rem = tile - k * tpp;
+        const int tr = fdiv(rem, TC, invTc), tc = rem - tr * TC;
+        const int sl = H(ly.info + vb0 + 2 * k) & kSlotMask, sr = H(ly.info + vb0 + 2 * k + 1) & kSlotMask;
+        const int lb = kLeaves ? ly.leaves + sl * CC : ly.node64(sl, E);
+        const int rb = kLeaves ? ly.leaves + sr * CC : ly.node64(sr, E);
         const int r0 = tr * MR, c0 = tc * MC;
-        int ra[MR], cb[MC];
-#pragma unroll
-        for (int i = 0; i < MR; ++i) ra[i] = min(r0 + i, C - 1) * C;
-#pragma unroll
-        for (int j = 0; j < MC; ++j) cb[j] = min(c0 + j, C - 1);
+        int lp = lb + kS * r0 * C;   // L[r0][q]: + kS * (i * C + q)
+        int rp = rb + kS * c0;       // R[q][c0]: + kS * (q * C + j)
         double acc[MR][MC];
 #pragma unroll
         for (int i = 0; i < MR; ++i)
 #pragma unroll
             for (int j = 0; j < MC; ++j) acc[i][j] = -INFINITY;
-#pragma unroll 2
-        for (int q = 0; q < C; ++q) {
-            double av[MR], bv[MC];
+        int q = 0;
+        for (; q + kB <= C; q += kB) {
+            double av[kB][MR], bv[kB][MC];
 #pragma unroll
-            for (int i = 0; i < MR; ++i) av[i] = mx<kLeaves>(lb, ra[i] + q);
+            for (int u = 0; u < kB; ++u) {
 #pragma unroll
-            for (int j = 0; j < MC; ++j) bv[j] = mx<kLeaves>(rb, q * C + cb[j]);
+                for (int i = 0; i < MR; ++i) av[u][i] = mx<kLeaves>(lp, i * C + u);
 #pragma unroll
-            for (int i = 0; i < MR; ++i)
+                for (int j = 0; j < MC; ++j) bv[u][j] = mx<kLeaves>(rp + kS * u * C, j);
+            }
 #pragma unroll
-                for (int j = 0; j < MC; ++j) acc[i][j] = fmax(acc[i][j], av[i] + bv[j]);
+            for (int u = 0; u < kB; ++u)
+#pragma unroll
+                for (int i = 0; i < MR; ++i)
+#pragma unroll
+                    for (int j = 0; j < MC; ++j) acc[i][j] = fmax(acc[i][j], av[u][i] + bv[u][j]);
+            lp += kS * kB;
+            rp += kS * kB * C;
         }
-        const int Pb = ly.slots + (T.pbase[l] + k) * CC * 2;
+        for (; q < C; ++q) {
+#pragma unroll
+            for (int i = 0; i < MR; ++i) {
+                const double av = mx<kLeaves>(lp, i * C);
+#pragma unroll
+                for (int j = 0; j < MC; ++j) acc[i][j] = fmax(acc[i][j], av + mx<kLeaves>(rp, j));
+            }
+            lp += kS;
+            rp += kS * C;
+        }
+        const int Pb = ly.slots + (pbase + k) * CC * 2;
 #pragma unroll
         for (int i = 0; i < MR; ++i)
 #pragma unroll
@@ -650,32 +654,43 @@ __device__ void block_prod_max(const MaxLayout& ly, const Tree& T, int l) {
     }
 }
 
-// the smallest register tile that still gives every thread at most one tile
+// the smallest register tile that still gives every thread at most one tile (2 x 4 at
+// most: larger levels loop)
 template <bool kLeaves>
-__device__ void level_prod_max(const MaxLayout& ly, const Tree& T, int l) {
-    const int np = T.products(l), C = ly.C;
+__device__ void level_prod_max(const MaxLayout& ly, int E, int np, int vb0, int pbase) {
+    const int C = ly.C;
     auto tiles = [&](int mr, int mc) { return np * ((C + mr - 1) / mr) * ((C + mc - 1) / mc); };
-    if (tiles(1, 1) <= kSmallThreads) block_prod_max<1, 1, kLeaves>(ly, T, l);
-    else if (tiles(1, 2) <= kSmallThreads) block_prod_max<1, 2, kLeaves>(ly, T, l);
-    else if (tiles(2, 2) <= kSmallThreads) block_prod_max<2, 2, kLeaves>(ly, T, l);
-    else if (tiles(2, 4) <= kSmallThreads) block_prod_max<2, 4, kLeaves>(ly, T, l);
-    else block_prod_max<4, 4, kLeaves>(ly, T, l);
+    if (tiles(1, 1) <= kSmallThreads) block_prod_max<1, 1, kLeaves>(ly, E, np, vb0, pbase);
+    else if (tiles(1, 2) <= kSmallThreads) block_prod_max<1, 2, kLeaves>(ly, E, np, vb0, pbase);
+    else if (tiles(2, 2) <= kSmallThreads) block_prod_max<2, 2, kLeaves>(ly, E, np, vb0, pbase);
+    else block_prod_max<2, 4, kLeaves>(ly, E, np, vb0, pbase);
 }
 
+__device__ __forceinline__ double xor32_max_d(double x) {
+    const uint64_t u = __double_as_longlong(x);
+    const auto lo = __builtin_amdgcn_permlane32_swap((unsigned)u, (unsigned)u, false, false);
+    const auto hi = __builtin_amdgcn_permlane32_swap((unsigned)(u >> 32), (unsigned)(u >> 32), false, false);
+    const double a = __longlong_as_double((long long)(((uint64_t)hi[0] << 32) | lo[0]));
+    const double b = __longlong_as_double((long long)(((uint64_t)hi[1] << 32) | lo[1]));
+    return fmax(a, b);
+}
+
+// One wave: y[j] = max_i x[i] + N[i][j] (fp64).  Lane l
+// computes column l % 32 over half l / 32 of i; the halves meet through a cross-half max.
+// Past C the index repeats C - 1, which leaves a max unchanged.
 template <int CP, bool kLeaf>
 __device__ void wave_vec_max(int C, int x, int Nb, int y) {
-    const int lane = threadIdx.x % kWave;
-    const int j = min(lane, C - 1);
-    double v[CP];
-#pragma unroll
-    for (int i = 0; i < CP; ++i) {
-        const int ic = min(i, C - 1);
-        v[i] = Dd(x + 2 * ic) + mx<kLeaf>(Nb, ic * C + j);   // past C: repeats entry C-1
-    }
+    constexpr int kHalf = CP / 2;
+    const int lane = threadIdx.x % kWave, o = lane & 31, h = lane >> 5;
+    const int j = min(o, C - 1);
     double m = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < CP; ++i) m = fmax(m, v[i]);
-    if (lane < C) Dd(y + 2 * lane) = m;
+    for (int q = 0; q < kHalf; ++q) {
+        const int ic = min(h * kHalf + q, C - 1);
+        m = fmax(m, Dd(x + 2 * ic) + mx<kLeaf>(Nb, ic * C + j));
+    }
+    m = xor32_max_d(m);
+    if (h == 0 && o < C) Dd(y + 2 * o) = m;
     wave_sync();
 }
 
@@ -693,7 +708,7 @@ __device__ __forceinline__ void small_max_body(const SmallMaxArgs& a, const int6
     const int C = a.C;
     const int64_t E = a.N - 1;
     const int L = (int)clamp_len(a.lengths, b, a.N), Eb = L - 1;
-    const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int w = uni(threadIdx.x / kWave), lane = threadIdx.x % kWave;
     const int CC = C * C;
     int32_t* path = a.path + (size_t)b * a.N;
     for (int64_t n = L + threadIdx.x; n < a.N; n += kSmallThreads) path[n] = -1;
@@ -703,65 +718,90 @@ __device__ __forceinline__ void small_max_body(const SmallMaxArgs& a, const int6
     }
     __shared__ Tree T;
     if (threadIdx.x == 0) T.init(Eb);
-    stage_leaves(a.pot + (size_t)b * E * CC, 0, Eb * CC);
-    __syncthreads();
+    const int nodes = (int)small_tree_nodes(Eb);
     MaxLayout ly;
-    ly.init(C, Eb, T.nodes);
-    auto base = [&](int h) { return h < 0 ? ly.leaves + (-h - 1) * CC : ly.slots + h * CC * 2; };
+    ly.init(C, Eb, nodes);
+    // ---- leaves into LDS (16 loads in flight per thread); the node table is built while
+    // the first batch is in flight
+    {
+        const float* gleaf = a.pot + (size_t)b * E * CC;
+        const int n = Eb * CC;
+        for (int base = 0; base < n; base += 16 * kSmallThreads) {
+            float v[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) v[u] = gleaf[min(base + u * kSmallThreads + (int)threadIdx.x, n - 1)];
+            if (base == 0) build_node_table(Eb, nodes, ly.info);
+#pragma unroll
+            for (int u = 0; u < 16; ++u)
+                if (base + u * kSmallThreads + (int)threadIdx.x < n) F(base + u * kSmallThreads + threadIdx.x) = v[u];
+        }
+    }
+    __syncthreads();
     // the last leaf in fp64 for levels >= 2 (read only after the level-1 barrier)
     for (int i = threadIdx.x; i < CC; i += kSmallThreads)
         Dd(ly.lastc + 2 * i) = (double)F(ly.leaves + (Eb - 1) * CC + i);
     // ---- up-sweep: all threads share each level's products
     for (int l = 1; l <= T.D; ++l) {
-        if (l == 1) level_prod_max<true>(ly, T, l);
-        else level_prod_max<false>(ly, T, l);
+        const int np = uni(T.products(l)), vb0 = uni(T.vbase[l - 1]), pb = uni(T.pbase[l]);
+        if (l == 1) level_prod_max<true>(ly, Eb, np, vb0, pb);
+        else level_prod_max<false>(ly, Eb, np, vb0, pb);
         __syncthreads();
     }
-    // ---- forward scores: u_L = u_N, u_R = u_N (x) L
+    // ---- forward scores: u_L = u_N, u_R = u_N (x) L   (root: zeros)
     auto U = [&](int l, int k) { return ly.vecs + (T.vbase[l] + k) * 2 * C; };
     for (int i = threadIdx.x; i < C; i += kSmallThreads) Dd(U(T.D, 0) + 2 * i) = 0.0;
     __syncthreads();
     for (int l = T.D; l >= 1; --l) {
-        const int nn = T.n[l];
+        const int nn = uni(T.n[l]), nprev = uni(T.n[l - 1]), vb0 = uni(T.vbase[l - 1]);
+        const int ub = uni(U(l, 0)), ub0 = uni(U(l - 1, 0));
         for (int task = w; task < 2 * nn; task += kSmallWaves) {
-            const int k = task / 2, which = task % 2;
-            const int uN = U(l, k);
+            const int k = task >> 1, which = task & 1;
+            const int uN = ub + k * 2 * C, uL = ub0 + 2 * k * 2 * C;
             if (which == 0) {
-                if (lane < C) Dd(U(l - 1, 2 * k) + 2 * lane) = Dd(uN + 2 * lane);
-            } else if (2 * k + 1 < T.n[l - 1]) {
-                const int hl = T.handle(l - 1, 2 * k);
-                if (hl < 0) wave_vec_max<CP, true>(C, uN, base(hl), U(l - 1, 2 * k + 1));
-                else wave_vec_max<CP, false>(C, uN, base(hl), U(l - 1, 2 * k + 1));
+                if (lane < C) Dd(uL + 2 * lane) = Dd(uN + 2 * lane);
+            } else if (2 * k + 1 < nprev) {
+                const int sl = uni(H(ly.info + vb0 + 2 * k)) & kSlotMask;
+                if (l == 1) wave_vec_max<CP, true>(C, uN, ly.leaves + sl * CC, uL + 2 * C);
+                else wave_vec_max<CP, false>(C, uN, ly.node64(sl, Eb), uL + 2 * C);
             }
         }
         __syncthreads();
     }
-    // ---- backpointers: bp[t][j] = lowest argmax_i delta_t[i] + l[t][i][j]
+    // ---- backpointers bp[t][j] = lowest argmax_i delta_t[i] + l[t][i][j]: one (t, j) per
+    // lane pair (l, l ^ 32), each lane scanning half of i; the lower half wins ties
     uint8_t* bp = reinterpret_cast<uint8_t*>(ts_small_lds + ly.bp);
-    for (int t = w; t < Eb; t += kSmallWaves) {
-        const int d = U(0, t), leaf = ly.leaves + t * CC;
-        const int j = min(lane, C - 1);
-        double v[CP];
+    {
+        constexpr int kHalf = CP / 2;
+        const int h = lane >> 5;
+        const float invC = 1.f / (float)C;
+        for (int p = w * 32 + (lane & 31); p < ((Eb * C + 31) & ~31); p += kSmallWaves * 32) {
+            const int pc = min(p, Eb * C - 1);
+            const int t = fdiv(pc, C, invC), j = pc - t * C;
+            const int d = U(0, t), leaf = ly.leaves + t * CC;
+            double best = -INFINITY;
+            int arg = h * kHalf;
 #pragma unroll
-        for (int i = 0; i < CP; ++i) {
-            const int ic = min(i, C - 1);
-            v[i] = Dd(d + 2 * ic) + (double)F(leaf + ic * C + j);
-        }
-        double best = v[0];
-        int arg = 0;
-#pragma unroll
-        for (int i = 1; i < CP; ++i) {
-            const bool better = i < C && v[i] > best;   // strict: the lowest index wins ties
-            best = better ? v[i] : best;
-            arg = better ? i : arg;
-        }
-        if (lane < C) {
-            bp[t * C + lane] = (uint8_t)arg;
-            if (t == Eb - 1) Dd(ly.dlast + 2 * lane) = best;
+            for (int q = 0; q < kHalf; ++q) {
+                const int i = h * kHalf + q, ic = min(i, C - 1);
+                const double v = Dd(d + 2 * ic) + (double)F(leaf + ic * C + j);
+                const bool better = i < C && v > best;   // strict: the lowest index wins ties
+                best = better ? v : best;
+                arg = better ? i : arg;
+            }
+            // partner half: the upper half takes over only when strictly better
+            const double ob = xor32_max_d(best);   // max of both halves
+            const bool upperWins = h == 0 && ob > best;
+            const int oarg = __shfl_xor(arg, 32, kWave);
+            if (h == 0 && p < Eb * C) {
+                bp[t * C + j] = (uint8_t)(upperWins ? oarg : arg);
+                if (t == Eb - 1) Dd(ly.dlast + 2 * j) = ob;
+            }
         }
     }
     __syncthreads();
-    // ---- last label (lowest argmax), score, backtrace
+    // ---- last label (lowest argmax), score, backtrace.  Wave 0 keeps 32 edges of
+    // backpointers at a time in registers (lane j holds column j, four edges per register)
+    // and follows the path with readlane.
     if (w == 0) {
         double best = lane < C ? Dd(ly.dlast + 2 * lane) : -INFINITY;
         int arg = lane < C ? lane : 0x7fffffff;
@@ -771,14 +811,38 @@ __device__ __forceinline__ void small_max_body(const SmallMaxArgs& a, const int6
             const int oi = __shfl_xor(arg, o, kWave);
             if (ov > best || (ov == best && oi < arg)) { best = ov; arg = oi; }
         }
+        int z = uni(arg < C ? arg : 0);
         if (lane == 0) {
-            int z = arg < C ? arg : 0;
             a.score[b] = (float)best;
             path[Eb] = z;
-            for (int t = Eb - 1; t >= 0; --t) {
-                z = bp[t * C + z];
-                path[t] = z;
+        }
+        const int jc = min(lane, C - 1);
+        for (int t1 = Eb; t1 > 0; t1 -= 32) {          // edges [t1 - 32, t1)
+            const int t0 = max(t1 - 32, 0);
+            unsigned pk[8];
+#pragma unroll
+            for (int g = 0; g < 8; ++g) {
+                unsigned v = 0;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int t = t0 + 4 * g + e;
+                    v |= (unsigned)bp[min(t, Eb - 1) * C + jc] << (8 * e);
+                }
+                pk[g] = v;
             }
+            int zs = 0;   // lane t - t0 records z_t
+#pragma unroll
+            for (int g = 7; g >= 0; --g) {
+#pragma unroll
+                for (int e = 3; e >= 0; --e) {
+                    const int t = t0 + 4 * g + e;
+                    if (t < t1) {
+                        z = (__builtin_amdgcn_readlane(pk[g], z) >> (8 * e)) & 0xff;
+                        zs = lane == 4 * g + e ? z : zs;
+                    }
+                }
+            }
+            if (lane < t1 - t0) path[t0 + lane] = zs;
         }
     }
 }
@@ -818,8 +882,9 @@ size_t small_log_lds_bytes(int64_t E, int64_t C) {
 
 size_t small_max_lds_bytes(int64_t E, int64_t C) {
     if (E < 1) return 0;
-    const int64_t CC = C * C;
-    const int64_t floats = (E * CC + 3) + (E - 1) * CC * 2 + CC * 2 + small_tree_nodes(E) * C * 2 + 2 * C;
+    const int64_t CC = C * C, nodes = small_tree_nodes(E);
+    const int64_t floats = (E * CC + 3) + (E - 1) * CC * 2 + CC * 2 + nodes * C * 2 + 2 * C +
+                           (nodes + 1) / 2 + 3;   // + node table, alignment of bp
     return sizeof(float) * (size_t)floats + (size_t)(E * C);
 }
 
