@@ -137,6 +137,25 @@ __device__ __forceinline__ Lse block_lse(Lse a, float* red) {
 __device__ __forceinline__ float safe_shift(float m) { return m == -INFINITY ? 0.f : m; }
 __device__ __forceinline__ double safe_shift_d(double m) { return m == -INFINITY ? 0.0 : m; }
 
+// Online log-sum-exp folded K values at a time: value = m + log(s), m = -inf while empty.
+// One exp per value plus one per chunk (the rescale of the running sum).
+template <int K>
+__device__ __forceinline__ void lse_fold(float& m, float& s, const float (&x)[K]) {
+    float cm = x[0];
+#pragma unroll
+    for (int k = 1; k < K; ++k) cm = fmaxf(cm, x[k]);
+    const float nm = fmaxf(m, cm);
+    const float sh = safe_shift(nm);
+    float t = 0.f;
+#pragma unroll
+    for (int k = 0; k < K; ++k) t += fexp(x[k] - sh);
+    s = s * fexp(m - sh) + t;
+    m = nm;
+}
+__device__ __forceinline__ float lse_val(float m, float s) {
+    return m == -INFINITY ? -INFINITY : m + flog(s);
+}
+
 // Blocks are dispatched round-robin over the 8 XCDs (block i -> XCD i % 8).  Renumber so
 // that logically consecutive blocks (the tiles of one node) share an XCD and its L2.
 // `nblocks` must be a multiple of 8.

@@ -14,6 +14,8 @@
 //
 // All LDS data is addressed as integer offsets into the one dynamic LDS array, so every
 // access compiles to a ds_read/ds_write.
+#include <type_traits>
+
 #include "device.h"
 #include "internal.h"
 #include "small.h"
@@ -29,7 +31,9 @@ constexpr int kSmallWaves = kSmallThreads / kWave;
 constexpr float kUnderflow = 0x1p-80f;
 
 __device__ __forceinline__ float& F(int off) { return ts_small_lds[off]; }
+// doubles sit at even float offsets
 __device__ __forceinline__ double& Dd(int off_floats) {
+    __builtin_assume((off_floats & 1) == 0);
     return reinterpret_cast<double*>(ts_small_lds)[off_floats >> 1];
 }
 __device__ __forceinline__ unsigned short& H(int off_halves) {
@@ -52,33 +56,7 @@ struct Tree {
     int pbase[kSmallMaxLevels + 1];  // first product slot of each level
     int vbase[kSmallMaxLevels + 1];  // first vector index of each level
     int nodes;                       // sum of n over all levels
-    __device__ void init(int e) {
-        E = e;
-        D = 0;
-        n[0] = e;
-        pbase[0] = 0;
-        vbase[0] = 0;
-        int slots = 0, vec = e;
-        while (n[D] > 1) {
-            ++D;
-            n[D] = (n[D - 1] + 1) / 2;
-            pbase[D] = slots;
-            vbase[D] = vec;
-            slots += n[D - 1] / 2;
-            vec += n[D];
-        }
-        nodes = vec;
-    }
     __device__ int products(int l) const { return n[l - 1] / 2; }
-    // >= 0: product slot; < 0: leaf -(h+1)
-    __device__ int handle(int l, int k) const {
-        while (l > 0) {
-            if (k < products(l)) return pbase[l] + k;
-            --l;
-            k *= 2;
-        }
-        return -(k + 1);
-    }
 };
 
 // ================================================================== log semiring
@@ -139,7 +117,10 @@ __device__ __forceinline__ int role_of(int E, int l, int k) {
 constexpr int kSlotMask = 0x3fff;
 
 __device__ void build_node_table(int E, int nodes, int info) {
-    for (int i = threadIdx.x; i < nodes; i += kSmallThreads) {
+    // node i goes to lane i / 16 of wave i % 16: a few lanes of every wave, not one wave
+    for (int base = 0; base < nodes; base += kSmallThreads) {
+        const int i = base + (int)(threadIdx.x % kWave) * kSmallWaves + (int)(threadIdx.x / kWave);
+        if (i >= nodes) continue;
         int l = 0, vb = 0, n = E, nprev = 0, pb = E;   // pb = pbase[l] once l >= 1
         while (i >= vb + n) {
             if (l >= 1) pb += nprev / 2;
@@ -160,6 +141,47 @@ __device__ void build_node_table(int E, int nodes, int info) {
         H(info + i) = (unsigned short)(slot | (role_of(E, l, k) << 14));
     }
 }
+
+// Tree of E >= 1 leaves set up by one wave (lane l fills level l), instead of one thread
+// walking the levels
+__device__ void tree_init_wave(Tree& T, int E) {
+    const int l = threadIdx.x % kWave;
+    if (l <= kSmallMaxLevels) {
+        int vb = 0, pb = 0;
+        for (int q = 0; q < l; ++q) {
+            vb += lvl_n(E, q);
+            if (q >= 1) pb += lvl_n(E, q - 1) / 2;
+        }
+        T.n[l] = lvl_n(E, l);
+        T.vbase[l] = vb;
+        T.pbase[l] = pb;
+    }
+    if (l == 0) {
+        T.E = E;
+        T.D = E <= 1 ? 0 : 32 - __clz(E - 1);
+        T.nodes = (int)small_tree_nodes(E);
+    }
+}
+
+// Flat, coalesced copy of a sequence's first `n` potentials (all N-1 edges: the loads go
+// out before the length is known) into registers; kPer loads per thread.
+template <int kPer>
+struct LeafBatch {
+    float v[kPer];
+    __device__ void load(const float* src, int base, int n) {
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) v[u] = src[min(base + u * kSmallThreads + (int)threadIdx.x, n - 1)];
+    }
+    // store elements [base, min(n, base + kPer * threads)) to LDS at dst
+    __device__ void store(int dst, int base, int n) const {
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int idx = base + u * kSmallThreads + threadIdx.x;
+            if (idx < n) F(dst + idx) = v[u];
+        }
+    }
+};
+constexpr int kLeafBatch = 16;
 
 template <int CP>
 struct LogLayout {
@@ -319,13 +341,13 @@ __device__ __forceinline__ void prod_log(const LogLayout<CP>& ly, int sl, int sr
     }
 }
 
-// Leaves straight from global memory into the form of their roles: one thread per line
-// (row of a LEFT or NONE leaf, column of a RIGHT leaf), which it shifts to max 0 (not the
-// NONE leaf of a one-edge sequence) and whose shift it records as ro (LEFT) or co (RIGHT);
-// the other offset is 0.  Lines C..CP-1 and entries C..CP-1 of a line are -inf, so a leaf's
-// whole padding is -inf.
+// Staged leaves (raw, flat at LDS offset raw) into the form of their roles: one thread per
+// line (row of a LEFT or NONE leaf, column of a RIGHT leaf), which it shifts to max 0 (not
+// the NONE leaf of a one-edge sequence) and whose shift it records as ro (LEFT) or co
+// (RIGHT); the other offset is 0.  Lines C..CP-1 and entries C..CP-1 of a line are -inf,
+// so a leaf's whole padding is -inf.
 template <int CP>
-__device__ void load_leaves(const LogLayout<CP>& ly, const float* gleaf, int E) {
+__device__ void normalise_leaves(const LogLayout<CP>& ly, int raw, int E) {
     using Ly = LogLayout<CP>;
     constexpr int kLd = Ly::kLd;
     const int C = ly.C, CC = C * C;
@@ -334,11 +356,11 @@ __device__ void load_leaves(const LogLayout<CP>& ly, const float* gleaf, int E) 
         const int role = role_of(E, 0, t);
         const bool col = role == kRight, pad = r >= C;
         const int rc = min(r, C - 1);
-        const float* line = gleaf + (size_t)t * CC + (col ? rc : rc * C);
+        const int line = raw + t * CC + (col ? rc : rc * C);
         const int stride = col ? C : 1;
         float v[CP];
 #pragma unroll
-        for (int j = 0; j < CP; ++j) v[j] = line[min(j, C - 1) * stride];
+        for (int j = 0; j < CP; ++j) v[j] = F(line + min(j, C - 1) * stride);
         float m = -INFINITY;
 #pragma unroll
         for (int j = 0; j < CP; ++j) {
@@ -411,26 +433,42 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
     constexpr int kLd = Ly::kLd;
     const int C = a.C;
     const int64_t E = a.N - 1;
-    const int Eb = (int)(clamp_len(a.lengths, b, a.N) - 1);
-    const int w = uni(threadIdx.x / kWave), lane = threadIdx.x % kWave;
     const int CC = C * C;
     const float* gleaf = a.pot + (size_t)b * E * CC;
-    if (a.marg) {  // padding edges are exactly zero
+    // the first loads of the potentials go out before the length is known
+    LeafBatch<kLeafBatch> lb;
+    lb.load(gleaf, 0, (int)E * CC);
+    const int Eb = (int)(clamp_len(a.lengths, b, a.N) - 1);
+    const int w = uni(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+    // padding edges are exactly zero (written last: these stores would otherwise hold up
+    // the first loads, which wait for all earlier memory operations)
+    auto zero_padding = [&]() {
+        if (!a.marg) return;
         float* mz = a.marg + ((size_t)b * E + Eb) * CC;
         const size_t nz = (size_t)(E - Eb) * CC;
         for (size_t idx = threadIdx.x; idx < nz; idx += kSmallThreads) mz[idx] = 0.f;
-    }
+    };
     if (Eb == 0) {
         if (a.logZ && threadIdx.x == 0) a.logZ[b] = logf((float)C);
+        zero_padding();
         return;
     }
     __shared__ Tree T;
-    if (threadIdx.x == 0) T.init(Eb);
     Ly ly;
     ly.init(C, Eb);
-    // ---- leaves (global -> LDS, normalised) and the node table
-    load_leaves<CP>(ly, gleaf, Eb);
-    build_node_table(Eb, (int)small_tree_nodes(Eb), ly.info);
+    const int nodes = (int)small_tree_nodes(Eb);
+    // ---- tree, node table and raw leaves (staged in the product-slot region, which the
+    // normalised leaves do not touch), then the leaves in the forms of their roles
+    if (w == kSmallWaves - 1) tree_init_wave(T, Eb);
+    build_node_table(Eb, nodes, ly.info);
+    const int raw = Ly::core(Eb), n = Eb * CC;
+    lb.store(raw, 0, n);
+    for (int base = kLeafBatch * kSmallThreads; base < n; base += kLeafBatch * kSmallThreads) {
+        lb.load(gleaf, base, n);
+        lb.store(raw, base, n);
+    }
+    __syncthreads();
+    normalise_leaves<CP>(ly, raw, Eb);
     __syncthreads();
     // ---- up-sweep: one wave per product
     for (int l = 1; l <= T.D; ++l) {
@@ -546,6 +584,7 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
             if (i < C && j < C) out[i * C + j] = (n == -INFINITY) ? 0.f : fexp(x[q] - n);
         }
     }
+    zero_padding();
 }
 
 // ================================================================== max semiring
@@ -596,35 +635,41 @@ __device__ __forceinline__ double mx(int base, int idx) {
 // (fp32 leaves).
 template <int MR, int MC, bool kLeaves>
 __device__ void block_prod_max(const MaxLayout& ly, int E, int np, int vb0, int pbase) {
-    constexpr int kS = kLeaves ? 1 : 2;   // floats per element
-    constexpr int kB = MR * MC >= 8 ? 4 : 8;
+    using T = typename std::conditional<kLeaves, float, double>::type;
+    constexpr int kB = MR * MC >= 8 ? 2 : 4;   // q per batch
     const int C = ly.C, CC = ly.CC;
     const int TR = (C + MR - 1) / MR, TC = (C + MC - 1) / MC, tpp = TR * TC;
     const float invTpp = 1.f / (float)tpp, invTc = 1.f / (float)TC;
     const int total = np * tpp;
+    const T* const nodes = reinterpret_cast<const T*>(ts_small_lds);   // element index
+    double* const prod = reinterpret_cast<double*>(ts_small_lds) + ly.slots / 2;
     for (int tile = threadIdx.x; tile < total; tile += kSmallThreads) {
         const int k = fdiv(tile, tpp, invTpp), rem = tile - k * tpp;
         const int tr = fdiv(rem, TC, invTc), tc = rem - tr * TC;
         const int sl = H(ly.info + vb0 + 2 * k) & kSlotMask, sr = H(ly.info + vb0 + 2 * k + 1) & kSlotMask;
-        const int lb = kLeaves ? ly.leaves + sl * CC : ly.node64(sl, E);
-        const int rb = kLeaves ? ly.leaves + sr * CC : ly.node64(sr, E);
+        // element offsets of the operands (leaves: floats; fp64 nodes: doubles)
+        const int lb = kLeaves ? ly.leaves + sl * CC : ly.node64(sl, E) / 2;
+        const int rb = kLeaves ? ly.leaves + sr * CC : ly.node64(sr, E) / 2;
         const int r0 = tr * MR, c0 = tc * MC;
-        int lp = lb + kS * r0 * C;   // L[r0][q]: + kS * (i * C + q)
-        int rp = rb + kS * c0;       // R[q][c0]: + kS * (q * C + j)
+        const T* lp = nodes + lb + r0 * C;   // L[r0 + i][q] = lp[i * C + q]
+        const T* rp = nodes + rb + c0;       // R[q][c0 + j] = rp[q * C + j]
         double acc[MR][MC];
 #pragma unroll
         for (int i = 0; i < MR; ++i)
 #pragma unroll
             for (int j = 0; j < MC; ++j) acc[i][j] = -INFINITY;
         int q = 0;
+        // unrolled by two so that a batch's reads can be issued while the previous one computes
+#pragma unroll 2
         for (; q + kB <= C; q += kB) {
             double av[kB][MR], bv[kB][MC];
 #pragma unroll
             for (int u = 0; u < kB; ++u) {
 #pragma unroll
-                for (int i = 0; i < MR; ++i) av[u][i] = mx<kLeaves>(lp, i * C + u);
+                for (int i = 0; i < MR; ++i) av[u][i] = (double)lp[i * C + u];
+                const T* ru = rp + u * C;
 #pragma unroll
-                for (int j = 0; j < MC; ++j) bv[u][j] = mx<kLeaves>(rp + kS * u * C, j);
+                for (int j = 0; j < MC; ++j) bv[u][j] = (double)ru[j];
             }
 #pragma unroll
             for (int u = 0; u < kB; ++u)
@@ -632,25 +677,25 @@ __device__ void block_prod_max(const MaxLayout& ly, int E, int np, int vb0, int 
                 for (int i = 0; i < MR; ++i)
 #pragma unroll
                     for (int j = 0; j < MC; ++j) acc[i][j] = fmax(acc[i][j], av[u][i] + bv[u][j]);
-            lp += kS * kB;
-            rp += kS * kB * C;
+            lp += kB;
+            rp += kB * C;
         }
         for (; q < C; ++q) {
 #pragma unroll
             for (int i = 0; i < MR; ++i) {
-                const double av = mx<kLeaves>(lp, i * C);
+                const double av = (double)lp[i * C];
 #pragma unroll
-                for (int j = 0; j < MC; ++j) acc[i][j] = fmax(acc[i][j], av + mx<kLeaves>(rp, j));
+                for (int j = 0; j < MC; ++j) acc[i][j] = fmax(acc[i][j], av + (double)rp[j]);
             }
-            lp += kS;
-            rp += kS * C;
+            lp += 1;
+            rp += C;
         }
-        const int Pb = ly.slots + (pbase + k) * CC * 2;
+        double* out = prod + (pbase + k) * CC;
 #pragma unroll
         for (int i = 0; i < MR; ++i)
 #pragma unroll
             for (int j = 0; j < MC; ++j)
-                if (r0 + i < C && c0 + j < C) Dd(Pb + 2 * ((r0 + i) * C + c0 + j)) = acc[i][j];
+                if (r0 + i < C && c0 + j < C) out[(r0 + i) * C + c0 + j] = acc[i][j];
     }
 }
 
@@ -707,33 +752,36 @@ template <int CP>
 __device__ __forceinline__ void small_max_body(const SmallMaxArgs& a, const int64_t b) {
     const int C = a.C;
     const int64_t E = a.N - 1;
+    const int CC = C * C;
+    const float* gleaf = a.pot + (size_t)b * E * CC;
+    // the first loads of the potentials go out before the length is known
+    LeafBatch<kLeafBatch> lb;
+    lb.load(gleaf, 0, (int)E * CC);
     const int L = (int)clamp_len(a.lengths, b, a.N), Eb = L - 1;
     const int w = uni(threadIdx.x / kWave), lane = threadIdx.x % kWave;
-    const int CC = C * C;
     int32_t* path = a.path + (size_t)b * a.N;
-    for (int64_t n = L + threadIdx.x; n < a.N; n += kSmallThreads) path[n] = -1;
+    // past the length the path is -1 (written last, as the marginals' padding)
+    auto pad_path = [&]() {
+        for (int64_t n = L + threadIdx.x; n < a.N; n += kSmallThreads) path[n] = -1;
+    };
     if (Eb == 0) {
         if (threadIdx.x == 0) { path[0] = 0; a.score[b] = 0.f; }
+        pad_path();
         return;
     }
     __shared__ Tree T;
-    if (threadIdx.x == 0) T.init(Eb);
     const int nodes = (int)small_tree_nodes(Eb);
     MaxLayout ly;
     ly.init(C, Eb, nodes);
-    // ---- leaves into LDS (16 loads in flight per thread); the node table is built while
-    // the first batch is in flight
+    // ---- tree, node table and leaves (fp32, flat)
+    if (w == kSmallWaves - 1) tree_init_wave(T, Eb);
+    build_node_table(Eb, nodes, ly.info);
     {
-        const float* gleaf = a.pot + (size_t)b * E * CC;
         const int n = Eb * CC;
-        for (int base = 0; base < n; base += 16 * kSmallThreads) {
-            float v[16];
-#pragma unroll
-            for (int u = 0; u < 16; ++u) v[u] = gleaf[min(base + u * kSmallThreads + (int)threadIdx.x, n - 1)];
-            if (base == 0) build_node_table(Eb, nodes, ly.info);
-#pragma unroll
-            for (int u = 0; u < 16; ++u)
-                if (base + u * kSmallThreads + (int)threadIdx.x < n) F(base + u * kSmallThreads + threadIdx.x) = v[u];
+        lb.store(ly.leaves, 0, n);
+        for (int base = kLeafBatch * kSmallThreads; base < n; base += kLeafBatch * kSmallThreads) {
+            lb.load(gleaf, base, n);
+            lb.store(ly.leaves, base, n);
         }
     }
     __syncthreads();
@@ -845,6 +893,7 @@ __device__ __forceinline__ void small_max_body(const SmallMaxArgs& a, const int6
             if (lane < t1 - t0) path[t0 + lane] = zs;
         }
     }
+    pad_path();
 }
 
 template <int CP>

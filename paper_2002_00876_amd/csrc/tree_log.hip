@@ -347,6 +347,119 @@ __global__ __launch_bounds__(256) void k_root_log(RootArgs a) {
 // message into its first edge, v the backward message out of its last edge:
 //   u_L = u_N,  v_L = R (x) v_N,  u_R = u_N (x) L,  v_R = v_N
 // (an absent right child leaves v_L = v_N).  Vectors are stored shifted to max 0.
+//
+// The two vector products of a node read one C x C matrix each, so a level is a stream
+// over its child matrices: a workgroup of 512 threads takes one node, its first 256
+// threads the column pass (u_R, one thread per column j, loads coalesced across j) and the
+// other 256 the row pass (v_L, one thread per row i, 16-byte loads along the row).
+constexpr int kVecThreads = 512;
+constexpr int kHalfThreads = kVecThreads / 2;
+
+// LSE_i (w[i] + M[i][j]) for one column j (w in LDS, M row-major in global memory), eight
+// loads in flight per step
+__device__ __forceinline__ float col_lse(const float* __restrict__ M, int C, const float* w, int j) {
+    float m = -INFINITY, s = 0.f;
+    int i = 0;
+    for (; i + 8 <= C; i += 8) {
+        float x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] = M[(size_t)(i + u) * C + j];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] += w[i + u];
+        lse_fold<8>(m, s, x);
+    }
+    for (; i < C; ++i) {
+        float x[1] = {M[(size_t)i * C + j] + w[i]};
+        lse_fold<1>(m, s, x);
+    }
+    return lse_val(m, s);
+}
+
+// LSE_j (M[i][j] + w[j]) for one row i; kVec: 16-byte loads (C % 4 == 0)
+template <bool kVec>
+__device__ __forceinline__ float row_lse(const float* __restrict__ M, int C, const float* w, int i) {
+    const float* row = M + (size_t)i * C;
+    float m = -INFINITY, s = 0.f;
+    int j = 0;
+    if constexpr (kVec) {
+        const float4* r4 = reinterpret_cast<const float4*>(row);
+        for (; j + 16 <= C; j += 16) {
+            float4 v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) v[u] = r4[j / 4 + u];
+            float x[16];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                x[4 * u + 0] = v[u].x + w[j + 4 * u + 0];
+                x[4 * u + 1] = v[u].y + w[j + 4 * u + 1];
+                x[4 * u + 2] = v[u].z + w[j + 4 * u + 2];
+                x[4 * u + 3] = v[u].w + w[j + 4 * u + 3];
+            }
+            lse_fold<16>(m, s, x);
+        }
+    }
+    for (; j + 8 <= C; j += 8) {
+        float x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] = row[j + u] + w[j + u];
+        lse_fold<8>(m, s, x);
+    }
+    for (; j < C; ++j) {
+        float x[1] = {row[j] + w[j]};
+        lse_fold<1>(m, s, x);
+    }
+    return lse_val(m, s);
+}
+
+// Max of a double over the calling thread's half of the workgroup (each half gets its own
+// result); red holds one double per wave.  Both halves call it together (it contains
+// workgroup barriers).
+__device__ __forceinline__ double half_max_d(double x, double* red) {
+    x = wave_max_d(x);
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) red[w] = x;
+    __syncthreads();
+    const int w0 = threadIdx.x < kHalfThreads ? 0 : kHalfThreads / kWave;
+    double r = red[w0];
+#pragma unroll
+    for (int i = 1; i < kHalfThreads / kWave; ++i) r = fmax(r, red[w0 + i]);
+    __syncthreads();
+    return r;
+}
+
+// One outside-vector product per half-workgroup, both halves in step:
+//   half 0: y[j] = co[j] + LSE_i (x[i] + ro[i] + core[i][j])     (x (x) N, column pass)
+//   half 1: y[i] = ro[i] + LSE_j (core[i][j] + co[j] + x[j])     (N (x) x, row pass)
+// x, w and y are this half's LDS vectors; the result shifted to max 0 goes to y and, when
+// yraw is given, unshifted (as float) to yraw.  ro/co may be null (leaves).  Either half may
+// be idle (active == false) but still joins the barriers.
+template <bool kVec>
+__device__ void half_vec(bool active, const float* core, const double* ro, const double* co,
+                         int C, const float* x, float* w, float* y, double* red, float* yraw) {
+    const bool rowPass = threadIdx.x >= kHalfThreads;
+    const int t = threadIdx.x - (rowPass ? kHalfThreads : 0);
+    const double* inOff = rowPass ? co : ro;
+    const double* outOff = rowPass ? ro : co;
+    // w = x + inOff, shifted to max 0 (float64 for the offsets)
+    double wm = -INFINITY;
+    if (active)
+        for (int i = t; i < C; i += kHalfThreads) wm = fmax(wm, (double)x[i] + (inOff ? inOff[i] : 0.0));
+    const double ws = safe_shift_d(half_max_d(wm, red));
+    if (active)
+        for (int i = t; i < C; i += kHalfThreads)
+            w[i] = (float)((double)x[i] + (inOff ? inOff[i] : 0.0) - ws);
+    __syncthreads();
+    double z = -INFINITY;
+    if (active && t < C) {
+        const float l = rowPass ? row_lse<kVec>(core, C, w, t) : col_lse(core, C, w, t);
+        z = (l == -INFINITY) ? -INFINITY : (outOff ? outOff[t] : 0.0) + ws + (double)l;
+        if (yraw) yraw[t] = (float)z;
+    }
+    const double zs = safe_shift_d(half_max_d(z, red));
+    if (active && t < C) y[t] = (z == -INFINITY) ? -INFINITY : (float)(z - zs);
+    __syncthreads();
+}
+
 struct DownArgs {
     const float* uN;       // level l vectors (nullptr at the root: zeros)
     const float* vN;
@@ -362,121 +475,53 @@ struct DownArgs {
     int level;
 };
 
-// y[j] = co[j] + LSE_i (x[i] + ro[i] + core[i][j]),  then shifted to max 0.
-// Column-parallel: thread j walks i.  x: [C] in shared memory.
-__device__ void vec_mat_log(const float* x, const float* core, const double* ro,
-                            const double* co, int64_t C, float* y, float* wsh, double* redd,
-                            float* redf) {
-    // w[i] = x[i] + ro[i], shifted (float64) so that max w = 0
-    double wm = -INFINITY;
-    for (int64_t i = threadIdx.x; i < C; i += blockDim.x)
-        wm = fmax(wm, (double)x[i] + (ro ? ro[i] : 0.0));
-    const double ws = safe_shift_d(block_max_d(wm, redd));
-    for (int64_t i = threadIdx.x; i < C; i += blockDim.x)
-        wsh[i] = (float)((double)x[i] + (ro ? ro[i] : 0.0) - ws);
-    __syncthreads();
-    double zm = -INFINITY;
-    double z = -INFINITY;
-    const int64_t j = threadIdx.x;
-    if (j < C) {
-        Lse acc = lse_empty();
-        for (int64_t i = 0; i < C; ++i) acc = lse_push(acc, wsh[i] + core[i * C + j]);
-        const float yl = lse_value(acc);
-        z = (yl == -INFINITY) ? -INFINITY : (co ? co[j] : 0.0) + (double)yl;
-        zm = z;
-    }
-    const double zs = safe_shift_d(block_max_d(zm, redd));
-    if (j < C) y[j] = (z == -INFINITY) ? -INFINITY : (float)(z - zs);
-    __syncthreads();
-    (void)redf;
-}
-
-// y[i] = ro[i] + LSE_j (core[i][j] + co[j] + x[j]), then shifted to max 0.
-// Row-parallel: one wave per row, lanes over j.
-__device__ void mat_vec_log(const float* core, const double* ro, const double* co,
-                            const float* x, int64_t C, float* y, float* wsh, float* tmp,
-                            double* redd) {
-    double wm = -INFINITY;
-    for (int64_t j = threadIdx.x; j < C; j += blockDim.x)
-        wm = fmax(wm, (double)x[j] + (co ? co[j] : 0.0));
-    const double ws = safe_shift_d(block_max_d(wm, redd));
-    for (int64_t j = threadIdx.x; j < C; j += blockDim.x)
-        wsh[j] = (float)((double)x[j] + (co ? co[j] : 0.0) - ws);
-    __syncthreads();
-    const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave, nw = blockDim.x / kWave;
-    for (int64_t i = w; i < C; i += nw) {
-        Lse acc = lse_empty();
-        for (int64_t j = lane; j < C; j += kWave) acc = lse_push(acc, core[i * C + j] + wsh[j]);
-        acc = wave_lse(acc);
-        if (lane == 0) tmp[i] = lse_value(acc);
-    }
-    __syncthreads();
-    double zm = -INFINITY, z = -INFINITY;
-    const int64_t i = threadIdx.x;
-    if (i < C) {
-        const float yl = tmp[i];
-        z = (yl == -INFINITY) ? -INFINITY : (ro ? ro[i] : 0.0) + (double)yl;
-        zm = z;
-    }
-    const double zs = safe_shift_d(block_max_d(zm, redd));
-    if (i < C) y[i] = (z == -INFINITY) ? -INFINITY : (float)(z - zs);
-    __syncthreads();
-}
-
-__global__ __launch_bounds__(256) void k_down_log(DownArgs a) {
-    __shared__ float su[kMaxLabels], sv[kMaxLabels], sy[kMaxLabels], wsh[kMaxLabels],
-        tmp[kMaxLabels];
-    __shared__ double redd[4];
-    __shared__ float redf[16];
+template <bool kVec>
+__global__ __launch_bounds__(kVecThreads) void k_down_log(DownArgs a) {
+    __shared__ float sx[2][kMaxLabels], sw[2][kMaxLabels], sy[2][kMaxLabels];
+    __shared__ double red[kVecThreads / kWave];
     const int64_t b = blockIdx.x / a.nodes, k = blockIdx.x % a.nodes;
     const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
-    const int64_t C = a.C;
+    const int C = (int)a.C;
     const int64_t span = (int64_t)1 << a.level, half = span >> 1;
     if (k * span >= Eb) return;
-    for (int64_t i = threadIdx.x; i < C; i += blockDim.x) {
-        su[i] = a.uN ? a.uN[(size_t)(b * a.nodes + k) * C + i] : 0.f;
-        sv[i] = a.vN ? a.vN[(size_t)(b * a.nodes + k) * C + i] : 0.f;
-    }
-    __syncthreads();
     const int64_t kl = 2 * k, kr = 2 * k + 1;
+    const bool right = kr * half < Eb;
+    const size_t nvec = (size_t)(b * a.nodes + k) * C;
     float* uL = a.uC + (size_t)(b * a.cnodes + kl) * C;
     float* vL = a.vC + (size_t)(b * a.cnodes + kl) * C;
-    const bool right = kr * half < Eb;
-    for (int64_t i = threadIdx.x; i < C; i += blockDim.x) uL[i] = su[i];
-    if (!right) {
-        for (int64_t i = threadIdx.x; i < C; i += blockDim.x) vL[i] = sv[i];
-        return;
-    }
     float* uR = a.uC + (size_t)(b * a.cnodes + kr) * C;
     float* vR = a.vC + (size_t)(b * a.cnodes + kr) * C;
-    for (int64_t i = threadIdx.x; i < C; i += blockDim.x) vR[i] = sv[i];
-    // u_R = u_N (x) L
-    {
-        const float* core = a.ccore + mat_off(b, kl, a.cnodes, C);
-        const double* ro = a.cro + (size_t)(b * a.cnodes + kl) * C;
-        const double* co = a.cco + (size_t)(b * a.cnodes + kl) * C;
-        vec_mat_log(su, core, ro, co, C, sy, wsh, redd, redf);
-        for (int64_t i = threadIdx.x; i < C; i += blockDim.x) uR[i] = sy[i];
-        __syncthreads();
+    // u_L = u_N; v_R = v_N (or v_L = v_N without a right child)
+    for (int i = threadIdx.x; i < C; i += kVecThreads) {
+        const float u = a.uN ? a.uN[nvec + i] : 0.f, v = a.vN ? a.vN[nvec + i] : 0.f;
+        uL[i] = u;
+        (right ? vR : vL)[i] = v;
+        sx[0][i] = u;
+        sx[1][i] = v;
     }
-    // v_L = R (x) v_N
-    {
-        const float* core = a.ccore + mat_off(b, kr, a.cnodes, C);
-        const double* ro = a.cro + (size_t)(b * a.cnodes + kr) * C;
-        const double* co = a.cco + (size_t)(b * a.cnodes + kr) * C;
-        mat_vec_log(core, ro, co, sv, C, sy, wsh, tmp, redd);
-        for (int64_t i = threadIdx.x; i < C; i += blockDim.x) vL[i] = sy[i];
-    }
+    if (!right) return;
+    __syncthreads();
+    const bool rowPass = threadIdx.x >= kHalfThreads;
+    const int64_t child = b * a.cnodes + (rowPass ? kr : kl);
+    const float* core = a.ccore + (size_t)child * C * C;
+    half_vec<kVec>(true, core, a.cro + (size_t)child * C, a.cco + (size_t)child * C, C,
+                   sx[rowPass], sw[rowPass], sy[rowPass], red, nullptr);
+    float* dst = rowPass ? vL : uR;
+    const int t = threadIdx.x - (rowPass ? kHalfThreads : 0);
+    for (int i = t; i < C; i += kHalfThreads) dst[i] = sy[rowPass][i];
 }
 
 // ---------------------------------------------------------------- marginals
-// One block per level-1 node (edges 2k and 2k+1).  With the node's outside vectors
-// (u, v): alpha_{2k} = u, beta_{2k+1} = leaf_{2k+1} (x) v, alpha_{2k+1} = u (x) leaf_{2k},
-// beta_{2k+2} = v.  Each edge's marginal uses its own normaliser
-//   n_t = LSE_{i,j} (alpha_t[i] + l[t][i][j] + beta_{t+1}[j]),
-//   mu[t][i][j] = exp(alpha_t[i] + l[t][i][j] + beta_{t+1}[j] - n_t),
-// exact because alpha_t and beta_{t+1} are the true messages up to constants and
-// log Z = const + n_t for every edge t.
+// One workgroup per level-1 node (edges 2k and 2k+1), with the node's outside vectors
+// (u, v): alpha_{2k} = u, beta_{2k+2} = v, and the two messages inside the pair come from
+// one column pass and one row pass over the two leaves, run side by side:
+//   y = u (x) leaf_{2k}   (alpha_{2k+1} = y shifted),   z = leaf_{2k+1} (x) v   (beta_{2k+1}).
+// Each edge's marginal uses its own normaliser n_t = LSE_{i,j} (alpha_t[i] + l_t[i][j] +
+// beta_{t+1}[j]), which is a vector log-sum-exp of the same products:
+//   n_{2k} = LSE_j (y[j] + beta_{2k+1}[j]),   n_{2k+1} = LSE_i (alpha_{2k+1}[i] + z[i]),
+//   mu_t[i][j] = exp(alpha_t[i] + l_t[i][j] + beta_{t+1}[j] - n_t)
+// (exact: alpha_t, beta_{t+1} are the true messages up to constants, and log Z = const +
+// n_t for every edge t).  The leaves are then streamed once more, 16 bytes per access.
 struct FormArgs {
     const float* pot;
     const float* u1;   // level-1 vectors, nullptr when level 1 is the root (D <= 1)
@@ -487,51 +532,108 @@ struct FormArgs {
     float* marg;
 };
 
-__device__ void form_edge(const float* leaf, const float* al, const float* be, int64_t C,
-                          float* out, float* red) {
-    Lse acc = lse_empty();
-    for (int64_t idx = threadIdx.x; idx < C * C; idx += blockDim.x)
-        acc = lse_push(acc, al[idx / C] + leaf[idx] + be[idx % C]);
-    acc = block_lse(acc, red);
-    const float n = lse_value(acc);
-    for (int64_t idx = threadIdx.x; idx < C * C; idx += blockDim.x)
-        out[idx] = (n == -INFINITY) ? 0.f : __expf(al[idx / C] + leaf[idx] + be[idx % C] - n);
+// mu = exp(al[i] + leaf[i][j] + be[j] - n) over one C x C edge, the whole workgroup:
+// thread t takes column group t % G (16 bytes when kVec, else one float) of rows t / G,
+// t / G + T / G, ... so that each row is read and written contiguously
+template <bool kVec>
+__device__ void write_marginal(const float* __restrict__ leaf, const float* al, const float* be,
+                               float n, int C, float* __restrict__ out) {
+    constexpr int kW = kVec ? 4 : 1;
+    const int G = C / kW, step = kVecThreads / G;
+    const int g = threadIdx.x % G, i0 = threadIdx.x / G;
+    if (i0 >= step) return;
+    const int j = g * kW;
+    float bj[kW];
+#pragma unroll
+    for (int q = 0; q < kW; ++q) bj[q] = be[j + q] - n;
+    const bool zero = n == -INFINITY;
+#pragma unroll 4
+    for (int i = i0; i < C; i += step) {
+        const float ai = al[i];
+        if constexpr (kVec) {
+            const float4 v = *reinterpret_cast<const float4*>(leaf + (size_t)i * C + j);
+            float4 r;
+            r.x = zero ? 0.f : fexp(ai + v.x + bj[0]);
+            r.y = zero ? 0.f : fexp(ai + v.y + bj[1]);
+            r.z = zero ? 0.f : fexp(ai + v.z + bj[2]);
+            r.w = zero ? 0.f : fexp(ai + v.w + bj[3]);
+            *reinterpret_cast<float4*>(out + (size_t)i * C + j) = r;
+        } else {
+            const float v = leaf[(size_t)i * C + j];
+            out[(size_t)i * C + j] = zero ? 0.f : fexp(ai + v + bj[0]);
+        }
+    }
 }
 
-__global__ __launch_bounds__(256) void k_form_log(FormArgs a) {
-    __shared__ float su[kMaxLabels], sv[kMaxLabels], aR[kMaxLabels], bL[kMaxLabels],
-        wsh[kMaxLabels], tmp[kMaxLabels];
-    __shared__ double redd[4];
-    __shared__ float red[16];
+template <bool kVec>
+__global__ __launch_bounds__(kVecThreads) void k_form_log(FormArgs a) {
+    __shared__ float su[kMaxLabels], sv[kMaxLabels], sy[2][kMaxLabels], sw[2][kMaxLabels],
+        raw[2][kMaxLabels];
+    __shared__ double red[kVecThreads / kWave];
+    __shared__ float nrm[2];
     const int64_t npairs = (a.N - 1 + 1) / 2;
     const int64_t b = blockIdx.x / npairs, k = blockIdx.x % npairs;
     const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
-    const int64_t C = a.C, E = a.N - 1;
+    const int C = (int)a.C;
+    const int64_t E = a.N - 1;
     const int64_t tL = 2 * k, tR = 2 * k + 1;
     const size_t CC = (size_t)C * C;
     // padding edges are exactly zero
     for (int64_t t = tL; t <= tR; ++t)
         if (t < E && t >= Eb) {
             float* o = a.marg + (size_t)(b * E + t) * CC;
-            for (int64_t idx = threadIdx.x; idx < (int64_t)CC; idx += blockDim.x) o[idx] = 0.f;
+            for (size_t idx = threadIdx.x; idx < CC; idx += kVecThreads) o[idx] = 0.f;
         }
     if (tL >= Eb) return;
-    for (int64_t i = threadIdx.x; i < C; i += blockDim.x) {
+    for (int i = threadIdx.x; i < C; i += kVecThreads) {
         su[i] = a.u1 ? a.u1[(size_t)(b * a.nodes1 + k) * C + i] : 0.f;
         sv[i] = a.v1 ? a.v1[(size_t)(b * a.nodes1 + k) * C + i] : 0.f;
     }
     __syncthreads();
     const float* leafL = a.pot + (size_t)(b * E + tL) * CC;
+    float* outL = a.marg + (size_t)(b * E + tL) * CC;
     const bool right = tR < Eb;
-    if (right) {
-        const float* leafR = a.pot + (size_t)(b * E + tR) * CC;
-        mat_vec_log(leafR, nullptr, nullptr, sv, C, bL, wsh, tmp, redd);   // beta_{2k+1}
-        vec_mat_log(su, leafL, nullptr, nullptr, C, aR, wsh, redd, red);   // alpha_{2k+1}
-        form_edge(leafL, su, bL, C, a.marg + (size_t)(b * E + tL) * CC, red);
-        form_edge(leafR, aR, sv, C, a.marg + (size_t)(b * E + tR) * CC, red);
-    } else {
-        form_edge(leafL, su, sv, C, a.marg + (size_t)(b * E + tL) * CC, red);
+    if (!right) {
+        // a lone edge: n = LSE_{i,j} (u[i] + l[i][j] + v[j]) = LSE_j (y[j] + v[j]), y = u (x) leaf
+        // (column pass only; the row half idles through the barriers)
+        half_vec<kVec>(threadIdx.x < kHalfThreads, leafL, nullptr, nullptr, C, su, sw[0], sy[0],
+                       red, raw[0]);
+        if (threadIdx.x < kWave) {
+            float m = -INFINITY, s = 0.f;
+            for (int j = threadIdx.x; j < C; j += kWave) {
+                float x[1] = {raw[0][j] + sv[j]};
+                lse_fold<1>(m, s, x);
+            }
+            const float mm = wave_max(m);
+            s = wave_sum(m == -INFINITY ? 0.f : s * fexp(m - safe_shift(mm)));
+            if (threadIdx.x == 0) nrm[0] = lse_val(mm, s);
+        }
+        __syncthreads();
+        write_marginal<kVec>(leafL, su, sv, nrm[0], C, outL);
+        return;
     }
+    const float* leafR = a.pot + (size_t)(b * E + tR) * CC;
+    float* outR = a.marg + (size_t)(b * E + tR) * CC;
+    // half 0: y = u (x) leaf_{2k} -> alpha_{2k+1} (sy[0]);  half 1: z = leaf_{2k+1} (x) v ->
+    // beta_{2k+1} (sy[1]); raw[] keep the unshifted log-sum-exps
+    const bool rowPass = threadIdx.x >= kHalfThreads;
+    half_vec<kVec>(true, rowPass ? leafR : leafL, nullptr, nullptr, C, rowPass ? sv : su,
+                   sw[rowPass], sy[rowPass], red, raw[rowPass]);
+    // n_{2k} = LSE_j (y[j] + beta_{2k+1}[j]) (wave 0);  n_{2k+1} = LSE_i (alpha_{2k+1}[i] + z[i]) (wave 1)
+    const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    if (w < 2) {
+        float m = -INFINITY, s = 0.f;
+        for (int j = lane; j < C; j += kWave) {
+            float x[1] = {w == 0 ? raw[0][j] + sy[1][j] : sy[0][j] + raw[1][j]};
+            lse_fold<1>(m, s, x);
+        }
+        const float mm = wave_max(m);
+        s = wave_sum(m == -INFINITY ? 0.f : s * fexp(m - safe_shift(mm)));
+        if (lane == 0) nrm[w] = lse_val(mm, s);
+    }
+    __syncthreads();
+    write_marginal<kVec>(leafL, su, sy[1], nrm[0], C, outL);
+    write_marginal<kVec>(leafR, sy[0], sv, nrm[1], C, outR);
 }
 
 template <int KP, bool VEC>
@@ -611,7 +713,10 @@ hipError_t launch_marginals_tree(const Plan& p, const float* pot, const int32_t*
         d.cnodes = p.Np >> (l - 1);
         d.uC = p.u[l - 1]; d.vC = p.v[l - 1];
         d.lengths = lengths; d.N = p.N; d.C = p.C; d.level = l;
-        hipLaunchKernelGGL(k_down_log, dim3((unsigned)(p.B * d.nodes)), dim3(256), 0, s, d);
+        if (p.C % 4 == 0)
+            hipLaunchKernelGGL(k_down_log<true>, dim3((unsigned)(p.B * d.nodes)), dim3(kVecThreads), 0, s, d);
+        else
+            hipLaunchKernelGGL(k_down_log<false>, dim3((unsigned)(p.B * d.nodes)), dim3(kVecThreads), 0, s, d);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -622,7 +727,10 @@ hipError_t launch_marginals_tree(const Plan& p, const float* pot, const int32_t*
     f.nodes1 = (p.D >= 1) ? (p.Np >> 1) : 1;
     f.lengths = lengths; f.N = p.N; f.C = p.C; f.marg = marg;
     const int64_t npairs = (p.N - 1 + 1) / 2;
-    hipLaunchKernelGGL(k_form_log, dim3((unsigned)(p.B * npairs)), dim3(256), 0, s, f);
+    if (p.C % 4 == 0)
+        hipLaunchKernelGGL(k_form_log<true>, dim3((unsigned)(p.B * npairs)), dim3(kVecThreads), 0, s, f);
+    else
+        hipLaunchKernelGGL(k_form_log<false>, dim3((unsigned)(p.B * npairs)), dim3(kVecThreads), 0, s, f);
     return hipGetLastError();
 }
 
