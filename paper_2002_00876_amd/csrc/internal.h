@@ -30,6 +30,14 @@ struct Plan {
     float* core[kMaxLevels] = {};
     double* ro[kMaxLevels] = {};
     double* co[kMaxLevels] = {};
+    // per-tile partial maxima of the rows (core + co) and columns (core + ro) of every node
+    // of levels 1..D, [nodes][C][ntile]: the exp shifts of the next level's products; and
+    // the leaves' row and column maxima [B, E, C]
+    float* pmr[kMaxLevels] = {};
+    float* pmc[kMaxLevels] = {};
+    float* lrmax = nullptr;
+    float* lcmax = nullptr;
+    int ntile = 1;              // output tiles per matrix dimension (up_tile)
     // outside vectors of the nodes of levels 1..D-1 (normalised to max 0)
     float* u[kMaxLevels] = {};
     float* v[kMaxLevels] = {};
@@ -44,6 +52,9 @@ struct Plan {
     int32_t* dec_zend = nullptr;// [B, nchunks] label at each chunk's end position
     size_t bytes = 0;
 };
+
+// Output tile edge of the log-semiring up-sweep for C labels.
+inline int up_tile(int64_t C) { return C <= 64 ? 64 : 128; }
 
 // Fills the plan; with base == nullptr only sizes are computed.  Returns false on overflow.
 bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p);

@@ -21,29 +21,11 @@ namespace tsc {
 
 namespace {
 
-constexpr int kTile = 64;        // output tile rows = cols per workgroup
-constexpr int kUpThreads = 256;  // 4 waves, each owns a 32 x 32 quadrant of the tile
+constexpr int kUpThreads = 256;  // 4 waves; each owns a (TM/2) x (TM/2) quarter of the tile
+constexpr int kSlice = 32;       // contraction indices staged per step
 constexpr float kUnderflow = 0x1p-80f;
 
 typedef float f16v __attribute__((ext_vector_type(16)));
-
-struct UpLogArgs {
-    const float* ccore;   // children (level l-1): core, or the potentials when l == 1
-    const double* cro;    // nullptr for leaves (ro = co = 0)
-    const double* cco;
-    int64_t cnodes;       // child node stride per sequence
-    float* core;          // outputs (level l)
-    double* ro;
-    double* co;
-    int64_t nodes;        // nodes per sequence at level l
-    const int32_t* lengths;
-    int64_t B, N, C;
-    int level;
-    int ntm;              // tiles per matrix dimension
-    int kp;               // C rounded up to a multiple of 8
-    int64_t nlogical;     // B * nodes * ntm * ntm
-    int64_t ngrid;        // nlogical rounded up to a multiple of 8
-};
 
 inline int64_t round8(int64_t x) { return (x + 7) / 8 * 8; }
 
@@ -51,18 +33,110 @@ __device__ __forceinline__ size_t mat_off(int64_t b, int64_t k, int64_t nodes, i
     return (size_t)(b * nodes + k) * (size_t)C * (size_t)C;
 }
 
-// One tree level: workgroup = one 64 x 64 output tile of one node.  KP is C rounded up
-// to 64, 128 or 256 (compile-time, so every staging loop unrolls into batched loads);
-// VEC selects 16-byte global loads (C % 4 == 0).
-//   LDS: As[64][KP+4]  rows a0.. of A' (k contiguous), then exp(A' - rowmax)
-//        Bs[KP][64+4]  columns c0.. of B' (k-major, as stored in HBM), then exp(B' - colmax)
-template <int KP, bool VEC>
+// Row and column maxima of the valid leaves (the exp shifts of the level-1 products):
+// lrmax[b][t][i] = max_j l[t][i][j] for a left operand (even t), lcmax[b][t][j] =
+// max_i l[t][i][j] for a right operand (odd t), and both for an unpaired last leaf (which
+// is carried up unchanged and may be consumed on either side).  Rows: one wave per row,
+// 16-byte loads along it; columns: one thread per column, loads coalesced across threads.
+struct LeafMaxArgs {
+    const float* pot;
+    const int32_t* lengths;
+    int64_t N, C;
+    float* lrmax;
+    float* lcmax;
+};
+
+template <bool kVec>
+__global__ __launch_bounds__(256) void k_leaf_max(LeafMaxArgs a) {
+    const int64_t E = a.N - 1;
+    const int64_t b = blockIdx.x / E, t = blockIdx.x % E;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    if (t >= Eb) return;
+    const bool left = (t & 1) == 0, right = (t & 1) == 1 || t + 1 == Eb;
+    const int C = (int)a.C;
+    const float* leaf = a.pot + (size_t)(b * E + t) * C * C;
+    const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
+    if (right && tid < C) {
+        float cm = -INFINITY;
+#pragma unroll 8
+        for (int i = 0; i < C; ++i) cm = fmaxf(cm, leaf[(size_t)i * C + tid]);
+        a.lcmax[(size_t)(b * E + t) * C + tid] = cm;
+    }
+    if (left) {
+        float* rmax = a.lrmax + (size_t)(b * E + t) * C;
+        for (int i = w; i < C; i += 256 / kWave) {
+            const float* row = leaf + (size_t)i * C;
+            float m = -INFINITY;
+            if (kVec) {
+                for (int j = 4 * lane; j < C; j += 4 * kWave) {
+                    const float4 v = *reinterpret_cast<const float4*>(row + j);
+                    m = fmaxf(m, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
+                }
+            } else {
+                for (int j = lane; j < C; j += kWave) m = fmaxf(m, row[j]);
+            }
+            m = wave_max(m);
+            if (lane == 0) rmax[i] = m;
+        }
+    }
+}
+
+// One tree level of the log-semiring up-sweep, P = L (x) R for every present node.
+// A workgroup computes one TM x TM output tile of one node, streaming the contraction
+// index in slices of 32 through double-buffered LDS:
+//   A''[a][b] = exp(core_L[a][b] + (co_L[b] - max co_L) - sa[a])
+//   B''[b][c] = exp(core_R[b][c] + (ro_R[b] - max ro_R) - sb[c])
+//   S = A'' B''  (fp32 MFMA 32x32x2),  core_P = log S,
+//   ro_P[a] = ro_L[a] + max co_L + sa[a],  co_P[c] = co_R[c] + max ro_R + sb[c].
+// The shifts sa (row maxima of core_L + co_L - max co_L) and sb (column maxima of core_R +
+// ro_R - max ro_R) are known before the first slice: each producer leaves partial maxima
+// of its tile's rows (pmr: max over the tile's columns of core + co) and columns (pmc: max
+// over the tile's rows of core + ro), and the leaves' maxima come from k_leaf_max.  A shift
+// only has to bound its line from above (nothing overflows) and be close to its maximum;
+// S < 2^-80 (every term underflowed) is recomputed exactly by a direct log-sum-exp.
+struct UpLogArgs {
+    const float* ccore;   // children (level l-1) core, or the potentials when l == 1
+    const double* cro;    // nullptr when l == 1 (leaves have ro = co = 0)
+    const double* cco;
+    const float* cpmr;    // children row maxima [cnodes][C][cntile] (l == 1: leaf maxima)
+    const float* cpmc;    // children column maxima [cnodes][C][cntile]
+    int64_t cnodes;       // child node stride per sequence
+    int cntile;           // partial maxima per line of a child (1 for the leaves)
+    float* core;          // outputs (level l)
+    double* ro;
+    double* co;
+    float* pmr;           // [nodes][C][ntile]
+    float* pmc;
+    int64_t nodes;        // nodes per sequence at level l
+    const int32_t* lengths;
+    int64_t B, N, C;
+    int level;
+    int ntile;            // tiles per matrix dimension
+    int64_t nlogical;     // B * nodes * ntile^2
+    int64_t ngrid;        // nlogical rounded up to a multiple of 8
+};
+
+template <int TM>
+struct UpSmem {
+    static constexpr int LDA = kSlice + 4, LDB = TM + 4, LDT = TM + 1;
+    static constexpr int kBuf = TM * LDA + kSlice * LDB;          // one A + B slice
+    static constexpr int kTileF = TM * LDT;                       // epilogue tile
+    static constexpr int kMain = (2 * kBuf > kTileF ? 2 * kBuf : kTileF);
+    // coh, roh [kMaxLabels]; sa, sb, cof, rof [TM]; red [4 doubles]
+    static constexpr int kFloats = kMain + 2 * kMaxLabels + 4 * TM + 8;
+    static constexpr size_t kBytes = sizeof(float) * kFloats;
+};
+
+template <int TM, bool VEC>
 __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
+    using Sm = UpSmem<TM>;
+    constexpr int LDA = Sm::LDA, LDB = Sm::LDB, LDT = Sm::LDT;
+    constexpr int BR = TM / 64;                 // 32 x 32 blocks per wave per dimension
+    constexpr int QW = TM / 2;                  // a wave's quarter edge
     extern __shared__ __align__(16) float smem[];
-    constexpr int LDA = KP + 4, LDB = kTile + 4;
     const int64_t lid = xcd_swizzle(blockIdx.x, a.ngrid);
     if (lid >= a.nlogical) return;
-    const int ntiles = a.ntm * a.ntm;
+    const int ntiles = a.ntile * a.ntile;
     const int tile = (int)(lid % ntiles);
     const int64_t node = lid / ntiles;
     const int64_t b = node / a.nodes, k = node % a.nodes;
@@ -70,47 +144,59 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
     const int64_t span = (int64_t)1 << a.level, half = span >> 1;
     if (k * span >= Eb) return;  // node absent: all padding
     const int C = (int)a.C;
-    const int tm = tile / a.ntm, tn = tile % a.ntm;
-    const int a0 = tm * kTile, c0 = tn * kTile;
+    const int tm = tile / a.ntile, tn = tile % a.ntile;
+    const int a0 = tm * TM, c0 = tn * TM;
     const int tid = threadIdx.x;
+    const int nt = a.ntile, cnt = a.cntile;
 
-    const float* Lc = a.ccore + mat_off(b, 2 * k, a.cnodes, C);
-    const double* Lro = a.cro ? a.cro + (size_t)(b * a.cnodes + 2 * k) * C : nullptr;
-    const double* Lco = a.cco ? a.cco + (size_t)(b * a.cnodes + 2 * k) * C : nullptr;
-    float* Pc = a.core + mat_off(b, k, a.nodes, C);
-    double* Pro = a.ro + (size_t)(b * a.nodes + k) * C;
-    double* Pco = a.co + (size_t)(b * a.nodes + k) * C;
+    const int64_t cl = b * a.cnodes + 2 * k, cr = cl + 1, pn = b * a.nodes + k;
+    const float* Lc = a.ccore + (size_t)cl * C * C;
+    float* Pc = a.core + (size_t)pn * C * C;
+    double* Pro = a.ro + (size_t)pn * C;
+    double* Pco = a.co + (size_t)pn * C;
+    float* Pmr = a.pmr + (size_t)pn * C * nt;
+    float* Pmc = a.pmc + (size_t)pn * C * nt;
 
     const bool right = (2 * k + 1) * half < Eb;
     if (!right) {
-        // the right half is padding: the node equals its left child
-#pragma unroll
-        for (int it = 0; it < kTile * kTile / kUpThreads; ++it) {
-            const int idx = tid + it * kUpThreads;
-            const int r = a0 + idx / kTile, c = c0 + idx % kTile;
-            if (r < C && c < C) Pc[r * C + c] = Lc[r * C + c];
+        // the right half is padding: the node equals its left child (tile, offsets and
+        // the partial maxima, re-tiled: a child with one partial per line keeps it in
+        // partial 0)
+        for (int idx = tid; idx < TM * TM; idx += kUpThreads) {
+            const int r = a0 + idx / TM, c = c0 + idx % TM;
+            if (r < C && c < C) Pc[(size_t)r * C + c] = Lc[(size_t)r * C + c];
         }
         if (tn == 0)
-            for (int i = tid; i < kTile; i += kUpThreads)
-                if (a0 + i < C) Pro[a0 + i] = Lro ? Lro[a0 + i] : 0.0;
+            for (int i = tid; i < TM; i += kUpThreads)
+                if (a0 + i < C) Pro[a0 + i] = a.cro ? a.cro[(size_t)cl * C + a0 + i] : 0.0;
         if (tm == 0)
-            for (int i = tid; i < kTile; i += kUpThreads)
-                if (c0 + i < C) Pco[c0 + i] = Lco ? Lco[c0 + i] : 0.0;
+            for (int i = tid; i < TM; i += kUpThreads)
+                if (c0 + i < C) Pco[c0 + i] = a.cco ? a.cco[(size_t)cl * C + c0 + i] : 0.0;
+        if (tm == 0 && tn == 0)
+            for (int i = tid; i < C * nt; i += kUpThreads) {
+                const int line = i / nt, p = i % nt;
+                const float* sr = a.cpmr + ((size_t)cl * C + line) * cnt;
+                const float* sc = a.cpmc + ((size_t)cl * C + line) * cnt;
+                Pmr[i] = p < cnt ? sr[p] : -INFINITY;
+                Pmc[i] = p < cnt ? sc[p] : -INFINITY;
+            }
         return;
     }
-    const float* Rc = a.ccore + mat_off(b, 2 * k + 1, a.cnodes, C);
-    const double* Rro = a.cro ? a.cro + (size_t)(b * a.cnodes + 2 * k + 1) * C : nullptr;
-    const double* Rco = a.cco ? a.cco + (size_t)(b * a.cnodes + 2 * k + 1) * C : nullptr;
+    const float* Rc = a.ccore + (size_t)cr * C * C;
+    const double* Lro = a.cro ? a.cro + (size_t)cl * C : nullptr;
+    const double* Lco = a.cco ? a.cco + (size_t)cl * C : nullptr;
+    const double* Rro = a.cro ? a.cro + (size_t)cr * C : nullptr;
+    const double* Rco = a.cco ? a.cco + (size_t)cr * C : nullptr;
 
-    float* As = smem;                  // [kTile][LDA]
-    float* Bs = As + kTile * LDA;      // [KP][LDB]
-    float* coh = Bs + KP * LDB;        // [KP] co_L - max co_L
-    float* roh = coh + KP;             // [KP] ro_R - max ro_R
-    float* rowm = roh + KP;            // [kTile]
-    float* colm = rowm + kTile;        // [kTile]
-    double* red = (double*)(colm + kTile);  // [4]
+    float* coh = smem + Sm::kMain;       // [kMaxLabels] co_L - max co_L
+    float* roh = coh + kMaxLabels;       // [kMaxLabels] ro_R - max ro_R
+    float* sa = roh + kMaxLabels;        // [TM] row shifts of the tile
+    float* sb = sa + TM;                 // [TM] column shifts
+    float* cof = sb + TM;                // [TM] co_P of the tile's columns (float)
+    float* rof = cof + TM;               // [TM] ro_P of the tile's rows (float)
+    double* red = reinterpret_cast<double*>(rof + TM);
 
-    // ---- column offsets of L and row offsets of R, shifted to max 0
+    // ---- offsets of the contracted index, shifted to max 0, and the tile's shifts
     double lmax = -INFINITY, rmax = -INFINITY;
     for (int i = tid; i < C; i += kUpThreads) {
         if (Lco) lmax = fmax(lmax, Lco[i]);
@@ -118,183 +204,210 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
     }
     const double coLshift = Lco ? safe_shift_d(block_max_d(lmax, red)) : 0.0;
     const double roRshift = Rro ? safe_shift_d(block_max_d(rmax, red)) : 0.0;
-    for (int i = tid; i < KP; i += kUpThreads) {
-        coh[i] = (i < C && Lco) ? (float)(Lco[i] - coLshift) : 0.f;
-        roh[i] = (i < C && Rro) ? (float)(Rro[i] - roRshift) : 0.f;
+    for (int i = tid; i < C; i += kUpThreads) {
+        coh[i] = Lco ? (float)(Lco[i] - coLshift) : 0.f;
+        roh[i] = Rro ? (float)(Rro[i] - roRshift) : 0.f;
+    }
+    for (int i = tid; i < TM; i += kUpThreads) {
+        float m = -INFINITY;
+        if (a0 + i < C) {
+            const float* p = a.cpmr + ((size_t)cl * C + a0 + i) * cnt;
+            for (int q = 0; q < cnt; ++q) m = fmaxf(m, p[q]);
+            m -= (float)coLshift;
+        }
+        sa[i] = safe_shift(m);
+        float n = -INFINITY;
+        if (c0 + i < C) {
+            const float* p = a.cpmc + ((size_t)cr * C + c0 + i) * cnt;
+            for (int q = 0; q < cnt; ++q) n = fmaxf(n, p[q]);
+            n -= (float)roRshift;
+        }
+        sb[i] = safe_shift(n);
     }
     __syncthreads();
 
-    // ---- stage A' = rows a0.. of L (+coh) and B' = columns c0.. of R (+roh); all loads of
-    // a panel are issued before any store
-    constexpr float NI = -INFINITY;
-    {
-        constexpr int GA = KP / 4, NA = kTile * GA / kUpThreads;
-        float4 v[NA];
+    // ---- staging of one slice [ks, ks + 32) of A'' (TM x 32) and B'' (32 x TM): the
+    // loads of the next slice are issued before the current slice's products
+    constexpr int GA = kSlice / 4, NA = TM * GA / kUpThreads;   // float4 groups per thread
+    constexpr int GB = TM / 4, NB = kSlice * GB / kUpThreads;
+    float4 va[NA], vb[NB];
+    auto load = [&](int ks) {
 #pragma unroll
         for (int it = 0; it < NA; ++it) {
             const int idx = tid + it * kUpThreads;
-            const int r = idx / GA, col = 4 * (idx % GA), row = a0 + r;
+            const int r = a0 + idx / GA, col = ks + 4 * (idx % GA);
+            const float* p = Lc + (size_t)min(r, C - 1) * C;
             if (VEC) {
-                v[it] = (row < C && col < C) ? *(const float4*)(Lc + (size_t)row * C + col)
-                                             : make_float4(NI, NI, NI, NI);
+                va[it] = *(const float4*)(p + min(col, C - 4));
             } else {
-                const float* p = Lc + (size_t)row * C + col;
-                v[it].x = (row < C && col + 0 < C) ? p[0] : NI;
-                v[it].y = (row < C && col + 1 < C) ? p[1] : NI;
-                v[it].z = (row < C && col + 2 < C) ? p[2] : NI;
-                v[it].w = (row < C && col + 3 < C) ? p[3] : NI;
-            }
-        }
-#pragma unroll
-        for (int it = 0; it < NA; ++it) {
-            const int idx = tid + it * kUpThreads;
-            const int r = idx / GA, col = 4 * (idx % GA);
-            float4 x = v[it];
-            x.x += coh[col]; x.y += coh[col + 1]; x.z += coh[col + 2]; x.w += coh[col + 3];
-            *(float4*)(As + r * LDA + col) = x;
-        }
-    }
-    {
-        constexpr int GB = kTile / 4, NB = KP * GB / kUpThreads;
-        float4 v[NB];
-#pragma unroll
-        for (int it = 0; it < NB; ++it) {
-            const int idx = tid + it * kUpThreads;
-            const int kk = idx / GB, cl = 4 * (idx % GB), col = c0 + cl;
-            if (VEC) {
-                v[it] = (kk < C && col < C) ? *(const float4*)(Rc + (size_t)kk * C + col)
-                                            : make_float4(NI, NI, NI, NI);
-            } else {
-                const float* p = Rc + (size_t)kk * C + col;
-                v[it].x = (kk < C && col + 0 < C) ? p[0] : NI;
-                v[it].y = (kk < C && col + 1 < C) ? p[1] : NI;
-                v[it].z = (kk < C && col + 2 < C) ? p[2] : NI;
-                v[it].w = (kk < C && col + 3 < C) ? p[3] : NI;
+                va[it].x = p[min(col + 0, C - 1)];
+                va[it].y = p[min(col + 1, C - 1)];
+                va[it].z = p[min(col + 2, C - 1)];
+                va[it].w = p[min(col + 3, C - 1)];
             }
         }
 #pragma unroll
         for (int it = 0; it < NB; ++it) {
             const int idx = tid + it * kUpThreads;
-            const int kk = idx / GB, cl = 4 * (idx % GB);
-            float4 x = v[it];
-            const float rh = roh[kk];
-            x.x += rh; x.y += rh; x.z += rh; x.w += rh;
-            *(float4*)(Bs + kk * LDB + cl) = x;
+            const int kk = ks + idx / GB, col = c0 + 4 * (idx % GB);
+            const float* p = Rc + (size_t)min(kk, C - 1) * C;
+            if (VEC) {
+                vb[it] = *(const float4*)(p + min(col, C - 4));
+            } else {
+                vb[it].x = p[min(col + 0, C - 1)];
+                vb[it].y = p[min(col + 1, C - 1)];
+                vb[it].z = p[min(col + 2, C - 1)];
+                vb[it].w = p[min(col + 3, C - 1)];
+            }
         }
-    }
-    __syncthreads();
-
-    // ---- row maxima of A' and column maxima of B' (4 neighbouring lanes per row/column)
-    {
-        const int r = tid >> 2, part = tid & 3;
-        float m1 = -INFINITY, m2 = -INFINITY;
-#pragma unroll
-        for (int g = part; g < KP / 4; g += 4) {
-            const float4 x = *(const float4*)(As + r * LDA + 4 * g);
-            m1 = fmaxf(m1, fmaxf(fmaxf(x.x, x.y), fmaxf(x.z, x.w)));
-        }
-#pragma unroll
-        for (int kk = part; kk < KP; kk += 4) m2 = fmaxf(m2, Bs[kk * LDB + r]);
-        m1 = fmaxf(m1, dpp_f(m1, 0xB1));
-        m1 = fmaxf(m1, dpp_f(m1, 0x4E));
-        m2 = fmaxf(m2, dpp_f(m2, 0xB1));
-        m2 = fmaxf(m2, dpp_f(m2, 0x4E));
-        if (part == 0) {
-            rowm[r] = m1;
-            colm[r] = m2;
-        }
-    }
-    __syncthreads();
-    {
-        constexpr int GA = KP / 4, NA = kTile * GA / kUpThreads;
+    };
+    auto store = [&](int ks, int buf) {
+        float* As = smem + buf * Sm::kBuf;
+        float* Bs = As + TM * LDA;
 #pragma unroll
         for (int it = 0; it < NA; ++it) {
             const int idx = tid + it * kUpThreads;
-            const int r = idx / GA, col = 4 * (idx % GA);
-            float4* p = (float4*)(As + r * LDA + col);
-            float4 x = *p;
-            const float s = safe_shift(rowm[r]);
-            x.x = __expf(x.x - s); x.y = __expf(x.y - s); x.z = __expf(x.z - s); x.w = __expf(x.w - s);
-            *p = x;
+            const int r = idx / GA, cl4 = 4 * (idx % GA), col = ks + cl4;
+            const bool rok = a0 + r < C;
+            const float s = sa[r];
+            float4 x;
+            x.x = (rok && col + 0 < C) ? fexp(va[it].x + coh[col + 0] - s) : 0.f;
+            x.y = (rok && col + 1 < C) ? fexp(va[it].y + coh[col + 1] - s) : 0.f;
+            x.z = (rok && col + 2 < C) ? fexp(va[it].z + coh[col + 2] - s) : 0.f;
+            x.w = (rok && col + 3 < C) ? fexp(va[it].w + coh[col + 3] - s) : 0.f;
+            *(float4*)(As + r * LDA + cl4) = x;
         }
-        constexpr int GB = kTile / 4, NB = KP * GB / kUpThreads;
 #pragma unroll
         for (int it = 0; it < NB; ++it) {
             const int idx = tid + it * kUpThreads;
-            const int kk = idx / GB, cl = 4 * (idx % GB);
-            float4* p = (float4*)(Bs + kk * LDB + cl);
-            float4 x = *p;
-            x.x = __expf(x.x - safe_shift(colm[cl]));
-            x.y = __expf(x.y - safe_shift(colm[cl + 1]));
-            x.z = __expf(x.z - safe_shift(colm[cl + 2]));
-            x.w = __expf(x.w - safe_shift(colm[cl + 3]));
-            *p = x;
+            const int kr = idx / GB, cl4 = 4 * (idx % GB), kk = ks + kr, col = c0 + cl4;
+            const bool kok = kk < C;
+            const float rh = kok ? roh[kk] : 0.f;
+            float4 x;
+            x.x = (kok && col + 0 < C) ? fexp(vb[it].x + rh - sb[cl4 + 0]) : 0.f;
+            x.y = (kok && col + 1 < C) ? fexp(vb[it].y + rh - sb[cl4 + 1]) : 0.f;
+            x.z = (kok && col + 2 < C) ? fexp(vb[it].z + rh - sb[cl4 + 2]) : 0.f;
+            x.w = (kok && col + 3 < C) ? fexp(vb[it].w + rh - sb[cl4 + 3]) : 0.f;
+            *(float4*)(Bs + kr * LDB + cl4) = x;
         }
-    }
-    __syncthreads();
+    };
 
-    // ---- S = expA * expB on the matrix cores.  Within each 8-wide k step, lanes 0-31
-    // contribute k..k+3 and lanes 32-63 k+4..k+7 (one 16-byte LDS read of A per lane);
-    // A and B use the same k assignment, so the sum over k is unchanged.
+    // ---- products: wave (wm, wn) owns rows wm*QW.., columns wn*QW.. as BR x BR blocks.
+    // Within each 8-wide k step lanes 0-31 contribute k..k+3 and lanes 32-63 k+4..k+7 (one
+    // 16-byte LDS read of A per block row); B uses the same k assignment.
     const int w = tid / kWave, lane = tid % kWave;
     const int wm = w >> 1, wn = w & 1;
-    f16v acc;
+    f16v acc[BR][BR];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-    const float* ap = As + (wm * 32 + (lane & 31)) * LDA + 4 * (lane >> 5);
-    const float* bp = Bs + (4 * (lane >> 5)) * LDB + wn * 32 + (lane & 31);
-    const int kend = (C + 7) & ~7;
-#pragma unroll 2
-    for (int kk = 0; kk < kend; kk += 8) {
-        const float4 av = *(const float4*)(ap + kk);
-        const float b0 = bp[(kk + 0) * LDB], b1 = bp[(kk + 1) * LDB];
-        const float b2 = bp[(kk + 2) * LDB], b3 = bp[(kk + 3) * LDB];
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.x, b0, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.y, b1, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.z, b2, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.w, b3, acc, 0, 0, 0);
+    for (int i = 0; i < BR; ++i)
+#pragma unroll
+        for (int j = 0; j < BR; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    const int nslices = (C + kSlice - 1) / kSlice;
+    load(0);
+    store(0, 0);
+    __syncthreads();
+    for (int s = 0; s < nslices; ++s) {
+        const int buf = s & 1;
+        if (s + 1 < nslices) load((s + 1) * kSlice);
+        const float* As = smem + buf * Sm::kBuf;
+        const float* Bs = As + TM * LDA;
+        const float* ap = As + (wm * QW + (lane & 31)) * LDA + 4 * (lane >> 5);
+        const float* bp = Bs + (4 * (lane >> 5)) * LDB + wn * QW + (lane & 31);
+#pragma unroll
+        for (int kk = 0; kk < kSlice; kk += 8) {
+            float4 av[BR];
+            float bv[BR][4];
+#pragma unroll
+            for (int i = 0; i < BR; ++i) av[i] = *(const float4*)(ap + i * 32 * LDA + kk);
+#pragma unroll
+            for (int j = 0; j < BR; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) bv[j][q] = bp[(kk + q) * LDB + j * 32];
+#pragma unroll
+            for (int i = 0; i < BR; ++i)
+#pragma unroll
+                for (int j = 0; j < BR; ++j) {
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i].x, bv[j][0], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i].y, bv[j][1], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i].z, bv[j][2], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i].w, bv[j][3], acc[i][j], 0, 0, 0);
+                }
+        }
+        if (s + 1 < nslices) store((s + 1) * kSlice, buf ^ 1);
+        __syncthreads();
     }
 
-    // ---- epilogue: core = log S (exact fallback when S underflows)
+    // ---- epilogue: core = log S into an LDS tile; entries whose S underflowed are marked
+    // and recomputed afterwards by a direct log-sum-exp (a rare, non-unrolled path)
+    float* T = smem;   // [TM][LDT], over the slice buffers (all reads are done)
+    uint64_t under = 0;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        const int row = wm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        const int col = wn * 32 + (lane & 31);
-        const int gr = a0 + row, gc = c0 + col;
-        if (gr < C && gc < C) {
-            const float S = acc[r];
-            float val;
-            if (S >= kUnderflow) {
-                val = __logf(S);
-            } else {
-                const float sa = safe_shift(rowm[row]), sb = safe_shift(colm[col]);
-                float q = -INFINITY;
-                for (int bb = 0; bb < C; ++bb) {
-                    const float x = (Lc[(size_t)gr * C + bb] + coh[bb] - sa) +
-                                    (Rc[(size_t)bb * C + gc] + roh[bb] - sb);
-                    q = fmaxf(q, x);
-                }
-                if (q == -INFINITY) {
-                    val = -INFINITY;
-                } else {
-                    float s = 0.f;
-                    for (int bb = 0; bb < C; ++bb) {
-                        const float x = (Lc[(size_t)gr * C + bb] + coh[bb] - sa) +
-                                        (Rc[(size_t)bb * C + gc] + roh[bb] - sb);
-                        s += __expf(x - q);
-                    }
-                    val = q + __logf(s);
-                }
+    for (int i = 0; i < BR; ++i)
+#pragma unroll
+        for (int j = 0; j < BR; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = wm * QW + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+                const int col = wn * QW + j * 32 + (lane & 31);
+                const float S = acc[i][j][r];
+                T[row * LDT + col] = flog(S);
+                if (!(S >= kUnderflow) && a0 + row < C && c0 + col < C)
+                    under |= 1ull << ((i * BR + j) * 16 + r);
             }
-            Pc[(size_t)gr * C + gc] = val;
+    while (under) {
+        const int bit = __builtin_ctzll(under);
+        under &= under - 1;
+        const int ij = bit >> 4, r = bit & 15, i = ij / BR, j = ij % BR;
+        const int row = wm * QW + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        const int col = wn * QW + j * 32 + (lane & 31);
+        const int gr = a0 + row, gc = c0 + col;
+        const float sr = sa[row], sc = sb[col];
+        const float* lrow = Lc + (size_t)gr * C;
+        float q = -INFINITY;
+        for (int bb = 0; bb < C; ++bb)
+            q = fmaxf(q, (lrow[bb] + coh[bb] - sr) + (Rc[(size_t)bb * C + gc] + roh[bb] - sc));
+        float val = -INFINITY;
+        if (q != -INFINITY) {
+            float sum = 0.f;
+            for (int bb = 0; bb < C; ++bb)
+                sum += fexp((lrow[bb] + coh[bb] - sr) + (Rc[(size_t)bb * C + gc] + roh[bb] - sc) - q);
+            val = q + flog(sum);
+        }
+        T[row * LDT + col] = val;
+    }
+    // the output node's offsets for the tile's rows and columns
+    for (int i = tid; i < TM; i += kUpThreads) {
+        const double ro = a0 + i < C ? (Lro ? Lro[a0 + i] : 0.0) + coLshift + sa[i] : 0.0;
+        const double co = c0 + i < C ? (Rco ? Rco[c0 + i] : 0.0) + roRshift + sb[i] : 0.0;
+        rof[i] = (float)ro;
+        cof[i] = (float)co;
+        if (tn == 0 && a0 + i < C) Pro[a0 + i] = ro;
+        if (tm == 0 && c0 + i < C) Pco[c0 + i] = co;
+    }
+    __syncthreads();
+    // partial maxima for the next level: thread t < TM row t, TM <= t < 2 TM column t - TM
+    const int nr = min(TM, C - a0), nc = min(TM, C - c0);
+    if (tid < TM) {
+        if (tid < nr) {
+            float m = -INFINITY;
+            for (int c = 0; c < nc; ++c) m = fmaxf(m, T[tid * LDT + c] + cof[c]);
+            Pmr[(size_t)(a0 + tid) * nt + tn] = m;
+        }
+    } else if (tid < 2 * TM) {
+        const int c = tid - TM;
+        if (c < nc) {
+            float m = -INFINITY;
+            for (int r = 0; r < nr; ++r) m = fmaxf(m, T[r * LDT + c] + rof[r]);
+            Pmc[(size_t)(c0 + c) * nt + tm] = m;
         }
     }
-    if (tn == 0)
-        for (int i = tid; i < kTile; i += kUpThreads)
-            if (a0 + i < C) Pro[a0 + i] = (Lro ? Lro[a0 + i] : 0.0) + coLshift + safe_shift(rowm[i]);
-    if (tm == 0)
-        for (int i = tid; i < kTile; i += kUpThreads)
-            if (c0 + i < C) Pco[c0 + i] = (Rco ? Rco[c0 + i] : 0.0) + roRshift + safe_shift(colm[i]);
+    // the tile, row by row
+    for (int idx = tid; idx < nr * TM; idx += kUpThreads) {
+        const int r = idx / TM, c = idx % TM;
+        if (c < nc) Pc[(size_t)(a0 + r) * C + c0 + c] = T[r * LDT + c];
+    }
 }
 
 // ---------------------------------------------------------------- root: log Z
@@ -636,37 +749,40 @@ __global__ __launch_bounds__(kVecThreads) void k_form_log(FormArgs a) {
     write_marginal<kVec>(leafR, sy[0], sv, nrm[1], C, outR);
 }
 
-template <int KP, bool VEC>
-hipError_t up_sweep_kp(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
-    constexpr int LDA = KP + 4, LDB = kTile + 4;
-    const size_t lds = sizeof(float) * (kTile * LDA + KP * LDB + 2 * KP + 2 * kTile) +
-                       sizeof(double) * 4;
+template <int TM, bool VEC>
+hipError_t up_sweep_tm(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
+    constexpr size_t lds = UpSmem<TM>::kBytes;
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void*)k_up_log<KP, VEC>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           160 * 1024);
+        hipError_t e = hipFuncSetAttribute((const void*)k_up_log<TM, VEC>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    const int64_t C = p.C;
-    const int ntm = (int)((C + kTile - 1) / kTile);
+    // the leaves' row and column maxima (shifts of the level-1 products)
+    LeafMaxArgs m{pot, lengths, p.N, p.C, p.lrmax, p.lcmax};
+    hipLaunchKernelGGL(k_leaf_max<VEC>, dim3((unsigned)(p.B * p.E)), dim3(256), 0, s, m);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
     for (int l = 1; l <= p.D; ++l) {
         UpLogArgs a{};
         if (l == 1) {
             a.ccore = pot; a.cro = nullptr; a.cco = nullptr; a.cnodes = p.E;
+            a.cpmr = p.lrmax; a.cpmc = p.lcmax; a.cntile = 1;
         } else {
             a.ccore = p.core[l - 1]; a.cro = p.ro[l - 1]; a.cco = p.co[l - 1];
             a.cnodes = p.Np >> (l - 1);
+            a.cpmr = p.pmr[l - 1]; a.cpmc = p.pmc[l - 1]; a.cntile = p.ntile;
         }
         a.core = p.core[l]; a.ro = p.ro[l]; a.co = p.co[l];
+        a.pmr = p.pmr[l]; a.pmc = p.pmc[l];
         a.nodes = p.Np >> l;
-        a.lengths = lengths; a.B = p.B; a.N = p.N; a.C = C; a.level = l;
-        a.ntm = ntm; a.kp = KP;
-        a.nlogical = p.B * a.nodes * ntm * ntm;
+        a.lengths = lengths; a.B = p.B; a.N = p.N; a.C = p.C; a.level = l;
+        a.ntile = p.ntile;
+        a.nlogical = p.B * a.nodes * p.ntile * p.ntile;
         a.ngrid = round8(a.nlogical);
-        hipLaunchKernelGGL((k_up_log<KP, VEC>), dim3((unsigned)a.ngrid), dim3(kUpThreads), lds, s, a);
-        hipError_t e = hipGetLastError();
+        hipLaunchKernelGGL((k_up_log<TM, VEC>), dim3((unsigned)a.ngrid), dim3(kUpThreads), lds, s, a);
+        e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -674,9 +790,9 @@ hipError_t up_sweep_kp(const Plan& p, const float* pot, const int32_t* lengths, 
 
 hipError_t up_sweep(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
     const bool vec = (p.C % 4) == 0;
-    if (p.C <= 64) return vec ? up_sweep_kp<64, true>(p, pot, lengths, s) : up_sweep_kp<64, false>(p, pot, lengths, s);
-    if (p.C <= 128) return vec ? up_sweep_kp<128, true>(p, pot, lengths, s) : up_sweep_kp<128, false>(p, pot, lengths, s);
-    return vec ? up_sweep_kp<256, true>(p, pot, lengths, s) : up_sweep_kp<256, false>(p, pot, lengths, s);
+    if (up_tile(p.C) == 64)
+        return vec ? up_sweep_tm<64, true>(p, pot, lengths, s) : up_sweep_tm<64, false>(p, pot, lengths, s);
+    return vec ? up_sweep_tm<128, true>(p, pot, lengths, s) : up_sweep_tm<128, false>(p, pot, lengths, s);
 }
 
 hipError_t root(const Plan& p, const float* pot, const int32_t* lengths, float* logZ,
