@@ -4,8 +4,10 @@
 //   log-sum-exp (log Z), outside sweep and per-edge marginals (Sec. 5.1 gradient identity);
 //   max semiring: float64 up-sweep, forward scores, backpointers and the backtrace.
 // The arithmetic is that of the multi-launch tree (tree_log.hip / tree_max.hip): node
-// matrices P[a][c] = ro[a] + co[c] + core[a][c] with an exp-shifted fp32 MFMA product,
-// and exact float64 max-plus for Viterbi.  Each product is computed by one wave.
+// matrices P[a][c] = ro[a] + co[c] + core[a][c] with an exp-shifted fp32 MFMA product
+// (one wave per product), and exact float64 max-plus for Viterbi (the whole workgroup
+// shares each level's products).  k_small_both runs both passes of a batch in one launch,
+// one workgroup per sequence and pass.
 //
 // Tree bookkeeping for a sequence with E edges: level 0 holds the E leaves (staged from
 // global memory into LDS); level l holds n_l = ceil(E / 2^l) nodes.  Node k of level l
