@@ -47,6 +47,9 @@ def load_library(path):
     for name in ("orc_viterbi", "orc_viterbi_f64"):
         getattr(lib, name).argtypes = [p, p, i64, i64, i64, p, p]
     lib.orc_marginals_seq.argtypes = [p, p, i64, i64, i64, i64, i64, i64, p, p]
+    if hasattr(lib, "orc_entropy"):
+        lib.orc_entropy.argtypes = [p, p, i64, i64, i64, p]
+        lib.orc_log_density.argtypes = [p, p, p, i64, i64, i64, p]
     lib.orc_max_threads.restype = ctypes.c_int
     return lib
 
@@ -117,6 +120,30 @@ def viterbi(pot, lengths=None, lib=None):
     fn = _load(lib).orc_viterbi_f64 if f64 else _load(lib).orc_viterbi
     _check(fn(_ptr(pot), _ptr(lengths), B, N, C, _ptr(path), _ptr(score)))
     return path, score
+
+
+def entropy(pot, lengths=None, lib=None):
+    """Entropy H[b] (float64 [B]) of each sequence's label distribution (fp32 potentials)."""
+    pot, lengths, f64, B, N, C = _prep(pot, lengths)
+    if f64:
+        raise ValueError("entropy takes fp32 potentials")
+    out = np.empty(B, np.float64)
+    _check(_load(lib).orc_entropy(_ptr(pot), _ptr(lengths), B, N, C, _ptr(out)))
+    return out
+
+
+def log_density(pot, labels, lengths=None, lib=None):
+    """log p(z_b) (float64 [B]) of label sequences labels [B, N] (int, entries past each
+    length ignored) under fp32 potentials."""
+    pot, lengths, f64, B, N, C = _prep(pot, lengths)
+    if f64:
+        raise ValueError("log_density takes fp32 potentials")
+    labels = np.ascontiguousarray(labels, dtype=np.int32)
+    if labels.shape != (B, N):
+        raise ValueError("labels must be [B, N]")
+    out = np.empty(B, np.float64)
+    _check(_load(lib).orc_log_density(_ptr(pot), _ptr(lengths), _ptr(labels), B, N, C, _ptr(out)))
+    return out
 
 
 def marginals_seq(pot, lengths, b, t0, t1):

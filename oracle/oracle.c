@@ -16,7 +16,10 @@
  *     identity), here by the classical two-pass forward-backward recursion;
  *   - the max score A*(l) = max_z sum_t l[t,z_t,z_{t+1}] and its argmax path, the
  *     (max, +) instance of the same recursion (Sec. 5.2; Table 2, "Max" semiring),
- *     with ties resolved by taking the lowest label index at every backtrace step.
+ *     with ties resolved by taking the lowest label index at every backtrace step;
+ *   - the entropy H = -sum_z p(z) log p(z) of the chain distribution (Sec. 5.1; the
+ *     quantity of Table 2's "Entropy" semiring), from the edge marginals by the chain
+ *     rule, and the log-probability log p(z) of a given label sequence (Sec. 5.1).
  *
  * Conventions (the paper leaves these open; the readings are listed in the design notes):
  *   - pot is [B, N-1, C, C] row-major: pot[((b*(N-1)+t)*C+i)*C+j] = l[b, t, i, j].
@@ -226,6 +229,82 @@ static int viterbi_impl(const float* pf, const double* pd, const int32_t* length
     return err ? ORC_ERR_MEM : ORC_OK;
 }
 
+/*
+ * Entropy of p(z) = exp(sum_t l[t,z_t,z_{t+1}] - A) for each sequence.  A chain is a
+ * Markov chain under p, so by the chain rule of entropy
+ *   H = H(z_0) + sum_{t < L-1} H(z_{t+1} | z_t),
+ *   H(z_0) = -sum_i m_0(i) log m_0(i),   m_t(i) = sum_j mu[t,i,j]  (node marginals),
+ *   H(z_{t+1} | z_t) = -sum_{i,j} mu[t,i,j] log(mu[t,i,j] / m_t(i)),   0 log 0 = 0,
+ * with mu the edge marginals above.  One token: H = log C (a free label).  A sequence with
+ * no finite path has all marginals 0 and gets H = 0.
+ */
+static int entropy_impl(const float* pf, const double* pd, const int32_t* lengths, int64_t B,
+                        int64_t N, int64_t C, double* H) {
+    int rc = check_args(pf, pd, lengths, B, N, C);
+    if (rc) return rc;
+    if (N == 1) {
+        for (int64_t b = 0; b < B; ++b) H[b] = log((double)C);
+        return ORC_OK;
+    }
+    double* logZ = malloc(sizeof(double) * B);
+    double* marg = malloc(sizeof(double) * B * (N - 1) * C * C);
+    if (!logZ || !marg) { free(logZ); free(marg); return ORC_ERR_MEM; }
+    rc = marginals_impl(pf, pd, lengths, B, N, C, logZ, marg);
+    if (rc == ORC_OK) {
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int64_t b = 0; b < B; ++b) {
+            int64_t L = lengths ? lengths[b] : N;
+            if (L == 1) { H[b] = log((double)C); continue; }
+            double h = 0.0;
+            for (int64_t t = 0; t + 1 < L; ++t) {
+                const double* mu = marg + (b * (N - 1) + t) * C * C;
+                for (int64_t i = 0; i < C; ++i) {
+                    double m = 0.0;
+                    for (int64_t j = 0; j < C; ++j) m += mu[i * C + j];
+                    if (m <= 0.0) continue;
+                    if (t == 0) h -= m * log(m);
+                    for (int64_t j = 0; j < C; ++j)
+                        if (mu[i * C + j] > 0.0) h -= mu[i * C + j] * log(mu[i * C + j] / m);
+                }
+            }
+            H[b] = h;
+        }
+    }
+    free(logZ); free(marg);
+    return rc;
+}
+
+/*
+ * log p(z) = sum_{t < L-1} l[t, z_t, z_{t+1}] - A for the label sequence labels[b, :L]
+ * (Sec. 5.1, the CRF probability of one structure); entries n >= L are ignored.  A label
+ * outside [0, C) is an argument error.
+ */
+static int log_density_impl(const float* pf, const double* pd, const int32_t* lengths,
+                            const int32_t* labels, int64_t B, int64_t N, int64_t C,
+                            double* out) {
+    int rc = check_args(pf, pd, lengths, B, N, C);
+    if (rc) return rc;
+    if (!labels) return ORC_ERR_ARG;
+    for (int64_t b = 0; b < B; ++b) {
+        int64_t L = lengths ? lengths[b] : N;
+        for (int64_t n = 0; n < L; ++n)
+            if (labels[b * N + n] < 0 || labels[b * N + n] >= C) return ORC_ERR_ARG;
+    }
+    double* logZ = malloc(sizeof(double) * B);
+    if (!logZ) return ORC_ERR_MEM;
+    rc = logpartition_impl(pf, pd, lengths, B, N, C, logZ);
+    if (rc == ORC_OK)
+        for (int64_t b = 0; b < B; ++b) {
+            int64_t L = lengths ? lengths[b] : N;
+            const int32_t* z = labels + b * N;
+            double s = 0.0;
+            for (int64_t t = 0; t + 1 < L; ++t) s += pot_at(pf, pd, N, C, b, t, z[t], z[t + 1]);
+            out[b] = s - logZ[b];
+        }
+    free(logZ);
+    return rc;
+}
+
 /* ---------------- exported entry points ---------------- */
 
 /* OpenMP threads a parallel region of the oracle may use */
@@ -243,6 +322,15 @@ int orc_marginals(const float* pot, const int32_t* lengths, int64_t B, int64_t N
 int orc_viterbi(const float* pot, const int32_t* lengths, int64_t B, int64_t N, int64_t C,
                 int32_t* path, double* score) {
     return viterbi_impl(pot, NULL, lengths, B, N, C, path, score);
+}
+
+int orc_entropy(const float* pot, const int32_t* lengths, int64_t B, int64_t N, int64_t C,
+                double* H) {
+    return entropy_impl(pot, NULL, lengths, B, N, C, H);
+}
+int orc_log_density(const float* pot, const int32_t* lengths, const int32_t* labels, int64_t B,
+                    int64_t N, int64_t C, double* out) {
+    return log_density_impl(pot, NULL, lengths, labels, B, N, C, out);
 }
 
 /* float64 potentials (used by the finite-difference pins) */

@@ -9,6 +9,8 @@ the labelled edges of Sec. 5.2) and reads every quantity off that list:
   canonical argmax = among the max-score sequences, the smallest under the key
                      (z_{L-1}, z_{L-2}, ..., z_0) -- the sequence a backtrace that
                      always takes the lowest index produces.
+  entropy          = -sum_z p(z) log p(z)
+  log p(z)         = score(z) - log Z   (brute_log_density)
 """
 import itertools
 import math
@@ -54,3 +56,39 @@ def brute(pot, lengths):
         zb = min(best, key=lambda z: tuple(reversed(z)))
         path[b, :L] = zb
     return logZ, mu, score, path
+
+
+def brute_entropy(pot, lengths):
+    """-> H [B] = -sum_z p(z) log p(z) by enumeration (0 when no sequence is finite)."""
+    pot = np.asarray(pot, dtype=np.float64)
+    B, E, C, _ = pot.shape
+    H = np.zeros(B)
+    for b in range(B):
+        seqs = enumerate_seq(pot[b], int(lengths[b]), C)
+        scores = [s for _, s in seqs]
+        m = max(scores)
+        if m == -math.inf:
+            continue
+        lz = m + math.log(sum(math.exp(s - m) for s in scores))
+        h = 0.0
+        for s in scores:
+            if s != -math.inf:
+                p = math.exp(s - lz)
+                h -= p * (s - lz)
+        H[b] = h
+    return H
+
+
+def brute_log_density(pot, lengths, labels):
+    """-> log p(z_b) [B] for the given label sequences, from the enumerated log Z."""
+    pot = np.asarray(pot, dtype=np.float64)
+    B, E, C, _ = pot.shape
+    out = np.zeros(B)
+    for b in range(B):
+        L = int(lengths[b])
+        scores = [s for _, s in enumerate_seq(pot[b], L, C)]
+        m = max(scores)
+        lz = m + math.log(sum(math.exp(s - m) for s in scores))
+        z = labels[b]
+        out[b] = sum(float(pot[b, t, z[t], z[t + 1]]) for t in range(L - 1)) - lz
+    return out
