@@ -56,12 +56,15 @@ typedef int ts_status;
 #define TS_ERR_WORKSPACE -3 /* ws_bytes below ts_chain_workspace_bytes() */
 #define TS_ERR_LENGTHS -4   /* TS_CHECK=1 and a length lies outside [1, N] */
 #define TS_ERR_HIP -5       /* a HIP runtime call or kernel launch failed */
+#define TS_ERR_LABELS -6    /* TS_CHECK=1 and a label lies outside [0, C) */
 
 /* operation codes for ts_chain_workspace_bytes */
 #define TS_OP_LOGPARTITION 0
 #define TS_OP_MARGINALS 1
 #define TS_OP_VITERBI 2
 #define TS_OP_MARGINALS_VITERBI 3
+#define TS_OP_ENTROPY 4
+#define TS_OP_LOG_DENSITY 5
 
 /* Largest supported number of labels C. */
 int ts_chain_max_labels(void);
@@ -120,6 +123,30 @@ ts_status ts_chain_marginals_viterbi(const float* pot, const int32_t* lengths, i
                                      int64_t N, int64_t C, float* logZ, float* marg,
                                      int32_t* path, float* score, void* ws, size_t ws_bytes,
                                      void* stream);
+
+/*
+ * Entropy H = -sum_z p(z) log p(z) of each sequence's label distribution (Sec. 5.1; the
+ * quantity Table 2's "Entropy" semiring computes), from the edge marginals by the chain rule
+ * of a Markov chain: H = H(z_0) + sum_t H(z_{t+1} | z_t), every term >= 0.
+ *   entropy  device float32 [B].  One token: log C.  No finite path: 0.
+ * The workspace, ts_chain_workspace_bytes(TS_OP_ENTROPY, ...), holds the marginals
+ * workspace, the marginals themselves ([B, N-1, C, C] fp32) and per-edge partial sums.
+ */
+ts_status ts_chain_entropy(const float* pot, const int32_t* lengths, int64_t B, int64_t N,
+                           int64_t C, float* entropy, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Log-probability of given label sequences (Sec. 5.1: p(z) = exp(score(z) - A)):
+ *   log p(z_b) = sum_{t < L_b - 1} l[b, t, z_b[t], z_b[t+1]] - log Z_b.
+ *   labels   device int32 [B, N]; entries n >= lengths[b] are ignored.  Labels must lie in
+ *            [0, C) (clamped on the device; TS_CHECK=1 validates them: TS_ERR_LABELS).
+ *   logp     device float32 [B].
+ * Workspace: ts_chain_workspace_bytes(TS_OP_LOG_DENSITY, ...) (the log-partition workspace
+ * and log Z).
+ */
+ts_status ts_chain_log_density(const float* pot, const int32_t* lengths, const int32_t* labels,
+                               int64_t B, int64_t N, int64_t C, float* logp, void* ws,
+                               size_t ws_bytes, void* stream);
 
 /* Message for the last non-OK status returned to the calling thread ("" if none). */
 const char* ts_last_error(void);

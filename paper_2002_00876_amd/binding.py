@@ -11,8 +11,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libtschain.so")
 
 OP_LOGPARTITION, OP_MARGINALS, OP_VITERBI, OP_MARGINALS_VITERBI = 0, 1, 2, 3
+OP_ENTROPY, OP_LOG_DENSITY = 4, 5
 STATUS = {0: "TS_OK", -1: "TS_ERR_NULL_ARG", -2: "TS_ERR_BAD_DIM", -3: "TS_ERR_WORKSPACE",
-          -4: "TS_ERR_LENGTHS", -5: "TS_ERR_HIP"}
+          -4: "TS_ERR_LENGTHS", -5: "TS_ERR_HIP", -6: "TS_ERR_LABELS"}
 
 _lib = None
 
@@ -38,8 +39,10 @@ def lib():
         L.ts_chain_marginals.argtypes = [p, p, i64, i64, i64, p, p, p, sz, p]
         L.ts_chain_viterbi.argtypes = [p, p, i64, i64, i64, p, p, p, sz, p]
         L.ts_chain_marginals_viterbi.argtypes = [p, p, i64, i64, i64, p, p, p, p, p, sz, p]
+        L.ts_chain_entropy.argtypes = [p, p, i64, i64, i64, p, p, sz, p]
+        L.ts_chain_log_density.argtypes = [p, p, p, i64, i64, i64, p, p, sz, p]
         for f in ("ts_chain_logpartition", "ts_chain_marginals", "ts_chain_viterbi",
-                  "ts_chain_marginals_viterbi"):
+                  "ts_chain_marginals_viterbi", "ts_chain_entropy", "ts_chain_log_density"):
             getattr(L, f).restype = ctypes.c_int
         L.ts_last_error.restype = ctypes.c_char_p
         _lib = L
@@ -141,3 +144,26 @@ def marginals_viterbi(pot, lengths=None, out=None, ws=None, want_logz=True):
                                             _ptr(marg) if N > 1 else None, _ptr(path),
                                             _ptr(score), _ptr(w), nb, _stream(pot.device)))
     return logz, marg, path, score
+
+
+def entropy(pot, lengths=None, out=None, ws=None):
+    """Entropy [B] (float32) of each sequence's label distribution."""
+    pot, lengths, B, N, C = _prep(pot, lengths)
+    h = out if out is not None else torch.empty(B, dtype=torch.float32, device=pot.device)
+    w, nb = _workspace(OP_ENTROPY, B, N, C, pot.device, ws)
+    _check(lib().ts_chain_entropy(_ptr(pot), _ptr(lengths), B, N, C, _ptr(h), _ptr(w), nb,
+                                  _stream(pot.device)))
+    return h
+
+
+def log_density(pot, labels, lengths=None, out=None, ws=None):
+    """log p(z) [B] (float32) of label sequences labels (int32 [B, N])."""
+    pot, lengths, B, N, C = _prep(pot, lengths)
+    if labels.device != pot.device or labels.dtype != torch.int32 or labels.shape != (B, N):
+        raise ValueError("labels must be int32 [B, N] on the same device as pot")
+    labels = labels.contiguous()
+    lp = out if out is not None else torch.empty(B, dtype=torch.float32, device=pot.device)
+    w, nb = _workspace(OP_LOG_DENSITY, B, N, C, pot.device, ws)
+    _check(lib().ts_chain_log_density(_ptr(pot), _ptr(lengths), _ptr(labels), B, N, C, _ptr(lp),
+                                      _ptr(w), nb, _stream(pot.device)))
+    return lp

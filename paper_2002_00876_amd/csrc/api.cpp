@@ -158,6 +158,51 @@ ts_status check_lengths(const int32_t* lengths, int64_t B, int64_t N, hipStream_
     return TS_OK;
 }
 
+ts_status check_labels(const int32_t* labels, const int32_t* lengths, int64_t B, int64_t N,
+                       int64_t C, hipStream_t s) {
+    const char* env = std::getenv("TS_CHECK");
+    if (!env || std::strcmp(env, "1") != 0) return TS_OK;
+    std::vector<int32_t> z((size_t)(B * N)), len((size_t)B, (int32_t)N);
+    if (hipMemcpyAsync(z.data(), labels, sizeof(int32_t) * B * N, hipMemcpyDeviceToHost, s) !=
+            hipSuccess ||
+        (lengths && hipMemcpyAsync(len.data(), lengths, sizeof(int32_t) * B,
+                                   hipMemcpyDeviceToHost, s) != hipSuccess) ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return fail(TS_ERR_HIP, "could not read labels for TS_CHECK");
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t n = 0; n < len[b] && n < N; ++n)
+            if (z[b * N + n] < 0 || z[b * N + n] >= C)
+                return fail(TS_ERR_LABELS, "labels[" + std::to_string(b) + ", " +
+                                               std::to_string(n) + "] = " +
+                                               std::to_string(z[b * N + n]) +
+                                               " is outside [0, C)");
+    return TS_OK;
+}
+
+// Workspace of the derived quantities: the plan of the call they build on, then their own
+// buffers (entropy: the marginals and per-edge partials; log density: log Z).
+struct Derived {
+    Plan base;
+    size_t extra = 0, mu = 0, part = 0, logz = 0;   // byte offsets after base.bytes
+};
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool plan_derived(int op, int64_t B, int64_t N, int64_t C, Derived* d) {
+    const int baseOp = op == TS_OP_ENTROPY ? TS_OP_MARGINALS : TS_OP_LOGPARTITION;
+    if (!make_plan(baseOp, B, N, C, nullptr, &d->base)) return false;
+    const size_t E = (size_t)(N - 1);
+    if (op == TS_OP_ENTROPY) {
+        d->mu = 0;
+        d->part = align_up(sizeof(float) * B * E * C * C);
+        d->extra = d->part + align_up(sizeof(double) * B * E);
+    } else {
+        d->logz = 0;
+        d->extra = align_up(sizeof(float) * B);
+    }
+    return true;
+}
+
 ts_status hip_status(hipError_t e) {
     if (e == hipSuccess) return TS_OK;
     return fail(TS_ERR_HIP, std::string("HIP error: ") + hipGetErrorString(e));
@@ -173,9 +218,14 @@ extern "C" {
 int ts_chain_max_labels(void) { return kMaxLabels; }
 
 size_t ts_chain_workspace_bytes(int op, int64_t B, int64_t N, int64_t C) {
-    if (op < TS_OP_LOGPARTITION || op > TS_OP_MARGINALS_VITERBI || B < 1 || N < 1 || C < 1 ||
+    if (op < TS_OP_LOGPARTITION || op > TS_OP_LOG_DENSITY || B < 1 || N < 1 || C < 1 ||
         C > kMaxLabels)
         return 0;
+    if (op == TS_OP_ENTROPY || op == TS_OP_LOG_DENSITY) {
+        Derived d;
+        if (!plan_derived(op, B, N, C, &d)) return 0;
+        return d.base.bytes + d.extra;
+    }
     Plan p, q;
     if (op == TS_OP_MARGINALS_VITERBI) {
         // the marginals plan first, then the Viterbi plan at the next 256-byte boundary
@@ -268,6 +318,58 @@ ts_status ts_chain_marginals_viterbi(const float* pot, const int32_t* lengths, i
     hipError_t e = launch_logz_tree(pm, pot, lengths, logZ, s);
     if (e == hipSuccess) e = launch_marginals_tree(pm, pot, lengths, marg, s);
     if (e == hipSuccess) e = launch_viterbi_tree(pv, pot, lengths, path, score, s);
+    return hip_status(e);
+}
+
+ts_status ts_chain_entropy(const float* pot, const int32_t* lengths, int64_t B, int64_t N,
+                           int64_t C, float* entropy, void* ws, size_t ws_bytes, void* stream) {
+    Derived d;
+    ts_status st = check_dims(pot, B, N, C, TS_OP_MARGINALS, &d.base);
+    if (st != TS_OK) return st;
+    plan_derived(TS_OP_ENTROPY, B, N, C, &d);
+    if ((st = check_ws(d.base.bytes + d.extra, ws, ws_bytes)) != TS_OK) return st;
+    if (!entropy) return fail(TS_ERR_NULL_ARG, "entropy is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = check_lengths(lengths, B, N, s)) != TS_OK) return st;
+    if (N == 1) return hip_status(launch_entropy(nullptr, lengths, B, N, C, nullptr, entropy, s));
+    char* extra = static_cast<char*>(ws) + d.base.bytes;
+    float* mu = reinterpret_cast<float*>(extra + d.mu);
+    double* part = reinterpret_cast<double*>(extra + d.part);
+    hipError_t e;
+    if (d.base.fused) {
+        e = launch_small_log(pot, lengths, B, N, C, nullptr, mu, s);
+    } else {
+        make_plan(TS_OP_MARGINALS, B, N, C, ws, &d.base);
+        e = launch_logz_tree(d.base, pot, lengths, nullptr, s);
+        if (e == hipSuccess) e = launch_marginals_tree(d.base, pot, lengths, mu, s);
+    }
+    if (e == hipSuccess) e = launch_entropy(mu, lengths, B, N, C, part, entropy, s);
+    return hip_status(e);
+}
+
+ts_status ts_chain_log_density(const float* pot, const int32_t* lengths, const int32_t* labels,
+                               int64_t B, int64_t N, int64_t C, float* logp, void* ws,
+                               size_t ws_bytes, void* stream) {
+    Derived d;
+    ts_status st = check_dims(pot, B, N, C, TS_OP_LOGPARTITION, &d.base);
+    if (st != TS_OK) return st;
+    plan_derived(TS_OP_LOG_DENSITY, B, N, C, &d);
+    if ((st = check_ws(d.base.bytes + d.extra, ws, ws_bytes)) != TS_OK) return st;
+    if (!labels || !logp) return fail(TS_ERR_NULL_ARG, "labels or logp is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = check_lengths(lengths, B, N, s)) != TS_OK) return st;
+    if ((st = check_labels(labels, lengths, B, N, C, s)) != TS_OK) return st;
+    float* logz = reinterpret_cast<float*>(static_cast<char*>(ws) + d.base.bytes + d.logz);
+    hipError_t e;
+    if (N == 1) {
+        e = launch_single_token(B, N, C, TS_OP_LOGPARTITION, logz, nullptr, nullptr, s);
+    } else if (d.base.fused) {
+        e = launch_small_log(pot, lengths, B, N, C, logz, nullptr, s);
+    } else {
+        make_plan(TS_OP_LOGPARTITION, B, N, C, ws, &d.base);
+        e = launch_logz_tree(d.base, pot, lengths, logz, s);
+    }
+    if (e == hipSuccess) e = launch_log_density(pot, lengths, labels, logz, B, N, C, logp, s);
     return hip_status(e);
 }
 

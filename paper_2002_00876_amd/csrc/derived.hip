@@ -1,0 +1,122 @@
+// derived.hip -- quantities read off the outputs of the hot path:
+//   entropy of each sequence's label distribution (the quantity of Table 2's "Entropy"
+//   semiring) from the edge marginals by the chain rule of entropy of a Markov chain:
+//     H = H(z_0) + sum_t H(z_{t+1} | z_t),   m_t(i) = sum_j mu[t,i,j],
+//     H(z_0) = -sum_i m_0(i) log m_0(i),  H(z_{t+1} | z_t) = -sum_{i,j} mu log(mu / m_t(i));
+//   log-probability of a given label sequence (Sec. 5.1): log p(z) = sum_t l[t,z_t,z_{t+1}] - A.
+// Every term of H is >= 0, so the sum has no cancellation.  Reductions run in a fixed
+// order (no atomics): per-edge partials first, then one pass per sequence.
+#include "device.h"
+#include "internal.h"
+
+namespace tsc {
+namespace {
+
+constexpr int kEntThreads = 256;
+
+// one workgroup per valid edge: part[b][t] = H(z_{t+1} | z_t) (+ H(z_0) for t = 0);
+// one wave per row i of mu_t, lanes over j
+__global__ __launch_bounds__(kEntThreads) void k_entropy_edges(const float* mu,
+                                                               const int32_t* lengths,
+                                                               int64_t N, int64_t C,
+                                                               double* part) {
+    __shared__ double red[kEntThreads / kWave];
+    const int64_t E = N - 1;
+    const int64_t b = blockIdx.x / E, t = blockIdx.x % E;
+    if (t >= clamp_len(lengths, b, N) - 1) return;
+    const int c = (int)C;
+    const float* m = mu + (size_t)(b * E + t) * c * c;
+    const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    double acc = 0.0;
+    for (int i = w; i < c; i += kEntThreads / kWave) {
+        const float* row = m + (size_t)i * c;
+        float rs = 0.f;
+        for (int j = lane; j < c; j += kWave) rs += row[j];
+        const float mi = wave_sum(rs);
+        if (mi <= 0.f) continue;
+        float h = 0.f;
+        for (int j = lane; j < c; j += kWave) {
+            const float p = row[j];
+            if (p > 0.f) h -= p * flog(p / mi);
+        }
+        h = wave_sum(h);
+        if (t == 0) h -= mi * flog(mi);
+        acc += (double)h;
+    }
+    if (lane == 0) red[w] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double s = 0.0;
+        for (int i = 0; i < kEntThreads / kWave; ++i) s += red[i];
+        part[b * E + t] = s;
+    }
+}
+
+// one thread per sequence: H = sum of its edges' partials in edge order (log C for one token)
+__global__ void k_entropy_sum(const double* part, const int32_t* lengths, int64_t B,
+                              int64_t N, int64_t C, float* H) {
+    const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= B) return;
+    const int64_t E = N - 1, Eb = clamp_len(lengths, b, N) - 1;
+    if (Eb == 0) {
+        H[b] = logf((float)C);
+        return;
+    }
+    double s = 0.0;
+    for (int64_t t = 0; t < Eb; ++t) s += part[b * E + t];
+    H[b] = (float)s;
+}
+
+// one workgroup per sequence: log p(z) = sum_{t < L-1} l[t, z_t, z_{t+1}] - log Z.  Labels
+// are clamped into [0, C) so that the gather stays in bounds (the caller promises valid
+// labels; TS_CHECK=1 validates them on the host).
+__global__ __launch_bounds__(kEntThreads) void k_log_density(const float* pot,
+                                                             const int32_t* lengths,
+                                                             const int32_t* labels,
+                                                             const float* logZ, int64_t N,
+                                                             int64_t C, float* out) {
+    __shared__ double red[kEntThreads / kWave];
+    const int64_t b = blockIdx.x, E = N - 1;
+    const int64_t Eb = clamp_len(lengths, b, N) - 1;
+    const int32_t* z = labels + b * N;
+    double s = 0.0;
+    for (int64_t t = threadIdx.x; t < Eb; t += kEntThreads) {
+        const int64_t i = min(max((int64_t)z[t], (int64_t)0), C - 1);
+        const int64_t j = min(max((int64_t)z[t + 1], (int64_t)0), C - 1);
+        s += (double)pot[((b * E + t) * C + i) * C + j];
+    }
+    s = wave_sum_d(s);
+    const int w = threadIdx.x / kWave;
+    if (threadIdx.x % kWave == 0) red[w] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double tot = 0.0;
+        for (int i = 0; i < kEntThreads / kWave; ++i) tot += red[i];
+        out[b] = (float)(tot - (double)logZ[b]);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_entropy(const float* mu, const int32_t* lengths, int64_t B, int64_t N,
+                          int64_t C, double* part, float* H, hipStream_t s) {
+    if (N > 1) {
+        hipLaunchKernelGGL(k_entropy_edges, dim3((unsigned)(B * (N - 1))), dim3(kEntThreads), 0,
+                           s, mu, lengths, N, C, part);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(k_entropy_sum, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s, part,
+                       lengths, B, N, C, H);
+    return hipGetLastError();
+}
+
+hipError_t launch_log_density(const float* pot, const int32_t* lengths, const int32_t* labels,
+                              const float* logZ, int64_t B, int64_t N, int64_t C, float* out,
+                              hipStream_t s) {
+    hipLaunchKernelGGL(k_log_density, dim3((unsigned)B), dim3(kEntThreads), 0, s, pot, lengths,
+                       labels, logZ, N, C, out);
+    return hipGetLastError();
+}
+
+}  // namespace tsc

@@ -31,6 +31,11 @@ __device__ __forceinline__ double wave_max_d(double x) {
     for (int o = 32; o > 0; o >>= 1) x = fmax(x, __shfl_xor(x, o, kWave));
     return x;
 }
+__device__ __forceinline__ double wave_sum_d(double x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, kWave);
+    return x;
+}
 
 // Hardware exp/log (v_exp_f32 / v_log_f32 are base 2).  Inputs of the callers are
 // exponents <= 0 and sums >= 2^-80, so no denormal handling is needed.

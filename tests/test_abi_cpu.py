@@ -61,7 +61,12 @@ def test_workspace_sizes(L, monkeypatch):
     # the tree over N-1 = 24 edges has levels of 16, 8, 4, 2, 1 nodes of C*C floats
     core = 32 * (16 + 8 + 4 + 2 + 1) * CW * CW * 4
     assert ws(0, 32, 25, CW) >= core
-    assert ws(4, 32, 25, CW) == 0 and ws(0, 0, 25, 20) == 0 and ws(0, 1, 25, 257) == 0
+    assert ws(6, 32, 25, CW) == 0 and ws(0, 0, 25, 20) == 0 and ws(0, 1, 25, 257) == 0
+    # entropy: the marginals workspace, the marginals themselves and per-edge partials;
+    # log density: the log-partition workspace and log Z
+    assert ws(4, 32, 25, CW) >= ws(1, 32, 25, CW) + 32 * 24 * CW * CW * 4 + 32 * 24 * 8
+    assert ws(4, 32, 25, 20) >= 32 * 24 * 20 * 20 * 4
+    assert ws(5, 32, 25, CW) >= ws(0, 32, 25, CW) + 32 * 4 and ws(5, 32, 25, 20) >= 32 * 4
     # the combined call: the marginals workspace followed by the Viterbi workspace
     assert ws(3, 32, 25, 20) == 0
     assert ws(3, 32, 25, CW) == ws(1, 32, 25, CW) + ws(2, 32, 25, CW)
@@ -76,6 +81,8 @@ def _err(L):
 
 def test_bad_dimensions_are_rejected(L):
     for B, N, C in [(0, 5, 3), (2, 0, 3), (2, 5, 0), (2, 5, 257), (-1, 5, 3)]:
+        assert L.ts_chain_entropy(FAKE, None, B, N, C, FAKE, FAKE, 1 << 30, None) == BAD_DIM
+        assert L.ts_chain_log_density(FAKE, None, FAKE, B, N, C, FAKE, FAKE, 1 << 30, None) == BAD_DIM
         assert L.ts_chain_logpartition(FAKE, None, B, N, C, FAKE, FAKE, 1 << 30, None) == BAD_DIM
         assert L.ts_chain_marginals(FAKE, None, B, N, C, FAKE, FAKE, FAKE, 1 << 30, None) == BAD_DIM
         assert L.ts_chain_viterbi(FAKE, None, B, N, C, FAKE, FAKE, FAKE, 1 << 30, None) == BAD_DIM
@@ -115,6 +122,15 @@ def test_null_pointers_are_rejected(L):
     assert mv(FAKE, None, 2, 5, CW, FAKE, FAKE, FAKE, FAKE, FAKE, need - 1, None) == WORKSPACE
     assert mv(FAKE, None, 2, 5, CW, FAKE, FAKE, FAKE, FAKE, FAKE + 16, need, None) == WORKSPACE
     assert mv(FAKE, None, 2, 5, 3, FAKE, FAKE, None, FAKE, None, 0, None) == NULL_ARG
+    need = binding.workspace_bytes(4, 2, 5, CW)
+    assert L.ts_chain_entropy(FAKE, None, 2, 5, CW, None, FAKE, need, None) == NULL_ARG
+    assert "entropy" in _err(L)
+    assert L.ts_chain_entropy(FAKE, None, 2, 5, CW, FAKE, FAKE, need - 1, None) == WORKSPACE
+    assert L.ts_chain_entropy(None, None, 2, 5, CW, FAKE, FAKE, need, None) == NULL_ARG
+    need = binding.workspace_bytes(5, 2, 5, CW)
+    assert L.ts_chain_log_density(FAKE, None, None, 2, 5, CW, FAKE, FAKE, need, None) == NULL_ARG
+    assert L.ts_chain_log_density(FAKE, None, FAKE, 2, 5, CW, None, FAKE, need, None) == NULL_ARG
+    assert L.ts_chain_log_density(FAKE, None, FAKE, 2, 5, CW, FAKE, FAKE + 16, need, None) == WORKSPACE
     # the fused path (no workspace) still rejects missing outputs
     assert L.ts_chain_marginals(FAKE, None, 2, 5, 3, FAKE, None, None, 0, None) == NULL_ARG
     assert L.ts_chain_viterbi(FAKE, None, 2, 5, 3, None, FAKE, None, 0, None) == NULL_ARG
