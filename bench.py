@@ -41,6 +41,10 @@ def parse():
                     help="bound on the oracle's CPU-baseline run (0 disables it)")
     ap.add_argument("--graph", action="store_true",
                     help="replay one captured HIP graph per step instead of calling the library")
+    ap.add_argument("--sweep", choices=["depth", "labels"], default=None,
+                    help="instead of the step: log Z by the scan against the left-to-right "
+                         "kernel over sequence lengths (depth: B=16, C=20) or label counts "
+                         "(labels: B=16, N=20); one JSON line per point")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this size (traffic-counter scale)")
     return ap.parse_args()
@@ -123,6 +127,48 @@ def calibrate_copy(mib):
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4}))
 
 
+def sweep(kind, reps=20):
+    """Time ts_chain_logpartition (the scan) against ts_chain_logpartition_sequential (the
+    left-to-right forward algorithm) on seeded N(0,1) potentials with full lengths: the
+    depth-versus-work trade-off of the parallel scan (the paper's Fig. 4a and 4c shapes)."""
+    import numpy as np
+    import torch
+
+    from paper_2002_00876_amd import binding
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    points = ([(16, n, 20) for n in (26, 51, 101, 201, 301, 401, 501)] if kind == "depth"
+              else [(16, 20, c) for c in (10, 20, 40, 60, 80, 100)])
+    for B, N, C in points:
+        rng = np.random.default_rng(1000 + N + C)
+        pot = torch.from_numpy(rng.standard_normal((B, N - 1, C, C)).astype(np.float32)).to(dev)
+        ws = binding._workspace(binding.OP_LOGPARTITION, B, N, C, dev)[0]
+        out = torch.empty(B, dtype=torch.float32, device=dev)
+
+        def timed(fn):
+            fn()
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / reps
+
+        ms_scan = timed(lambda: binding.logpartition(pot, out=out, ws=ws))
+        ms_seq = timed(lambda: binding.logpartition_sequential(pot, out=out))
+        fused = binding.workspace_bytes(binding.OP_LOGPARTITION, B, N, C) == 0
+        print(json.dumps({"sweep": kind, "B": B, "N": N, "C": C,
+                          "scan_ms": round(ms_scan, 5), "sequential_ms": round(ms_seq, 5),
+                          "scan_path": "single launch" if fused else "multi-launch tree",
+                          "scan_tokens_per_s": round(B * N / (ms_scan * 1e-3), 1),
+                          "sequential_tokens_per_s": round(B * N / (ms_seq * 1e-3), 1),
+                          "scan_speedup": round(ms_seq / ms_scan, 3)}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -135,6 +181,10 @@ def main():
 
     if args.calibrate_copy_mib:
         calibrate_copy(args.calibrate_copy_mib)
+        return
+    if args.sweep:
+        binding.lib()
+        sweep(args.sweep)
         return
     binding.lib()   # fail loudly if the HIP library is missing
     w = workloads.WORKLOADS[args.workload]

@@ -148,6 +148,16 @@ ts_status ts_chain_log_density(const float* pot, const int32_t* lengths, const i
                                int64_t B, int64_t N, int64_t C, float* logp, void* ws,
                                size_t ws_bytes, void* stream);
 
+/*
+ * Log-partition by the left-to-right forward algorithm (Sec. 5.2), the serial ordering that
+ * Fig. 4a compares the parallel scan against: L - 1 dependent vector steps of C^2 work
+ * instead of ceil(log2(L - 1)) tree levels of C^3 work per product.  Same output, layout
+ * and errors as ts_chain_logpartition; needs no workspace.  Provided to measure the
+ * depth-versus-work trade-off of the scan, not as the default path.
+ */
+ts_status ts_chain_logpartition_sequential(const float* pot, const int32_t* lengths, int64_t B,
+                                           int64_t N, int64_t C, float* logZ, void* stream);
+
 /* Message for the last non-OK status returned to the calling thread ("" if none). */
 const char* ts_last_error(void);
 

@@ -41,8 +41,10 @@ def lib():
         L.ts_chain_marginals_viterbi.argtypes = [p, p, i64, i64, i64, p, p, p, p, p, sz, p]
         L.ts_chain_entropy.argtypes = [p, p, i64, i64, i64, p, p, sz, p]
         L.ts_chain_log_density.argtypes = [p, p, p, i64, i64, i64, p, p, sz, p]
+        L.ts_chain_logpartition_sequential.argtypes = [p, p, i64, i64, i64, p, p]
         for f in ("ts_chain_logpartition", "ts_chain_marginals", "ts_chain_viterbi",
-                  "ts_chain_marginals_viterbi", "ts_chain_entropy", "ts_chain_log_density"):
+                  "ts_chain_marginals_viterbi", "ts_chain_entropy", "ts_chain_log_density",
+                  "ts_chain_logpartition_sequential"):
             getattr(L, f).restype = ctypes.c_int
         L.ts_last_error.restype = ctypes.c_char_p
         _lib = L
@@ -167,3 +169,12 @@ def log_density(pot, labels, lengths=None, out=None, ws=None):
     _check(lib().ts_chain_log_density(_ptr(pot), _ptr(lengths), _ptr(labels), B, N, C, _ptr(lp),
                                       _ptr(w), nb, _stream(pot.device)))
     return lp
+
+
+def logpartition_sequential(pot, lengths=None, out=None):
+    """log Z [B] by the left-to-right forward algorithm (the serial baseline of the scan)."""
+    pot, lengths, B, N, C = _prep(pot, lengths)
+    logz = out if out is not None else torch.empty(B, dtype=torch.float32, device=pot.device)
+    _check(lib().ts_chain_logpartition_sequential(_ptr(pot), _ptr(lengths), B, N, C, _ptr(logz),
+                                                  _stream(pot.device)))
+    return logz

@@ -373,6 +373,17 @@ ts_status ts_chain_log_density(const float* pot, const int32_t* lengths, const i
     return hip_status(e);
 }
 
+ts_status ts_chain_logpartition_sequential(const float* pot, const int32_t* lengths, int64_t B,
+                                           int64_t N, int64_t C, float* logZ, void* stream) {
+    Plan p;
+    ts_status st = check_dims(pot, B, N, C, TS_OP_LOGPARTITION, &p);
+    if (st != TS_OK) return st;
+    if (!logZ) return fail(TS_ERR_NULL_ARG, "logZ is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = check_lengths(lengths, B, N, s)) != TS_OK) return st;
+    return hip_status(launch_logz_sequential(pot, lengths, B, N, C, logZ, s));
+}
+
 const char* ts_last_error(void) { return g_err.c_str(); }
 
 }  // extern "C"

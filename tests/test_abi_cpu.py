@@ -82,6 +82,7 @@ def _err(L):
 def test_bad_dimensions_are_rejected(L):
     for B, N, C in [(0, 5, 3), (2, 0, 3), (2, 5, 0), (2, 5, 257), (-1, 5, 3)]:
         assert L.ts_chain_entropy(FAKE, None, B, N, C, FAKE, FAKE, 1 << 30, None) == BAD_DIM
+        assert L.ts_chain_logpartition_sequential(FAKE, None, B, N, C, FAKE, None) == BAD_DIM
         assert L.ts_chain_log_density(FAKE, None, FAKE, B, N, C, FAKE, FAKE, 1 << 30, None) == BAD_DIM
         assert L.ts_chain_logpartition(FAKE, None, B, N, C, FAKE, FAKE, 1 << 30, None) == BAD_DIM
         assert L.ts_chain_marginals(FAKE, None, B, N, C, FAKE, FAKE, FAKE, 1 << 30, None) == BAD_DIM
@@ -122,6 +123,8 @@ def test_null_pointers_are_rejected(L):
     assert mv(FAKE, None, 2, 5, CW, FAKE, FAKE, FAKE, FAKE, FAKE, need - 1, None) == WORKSPACE
     assert mv(FAKE, None, 2, 5, CW, FAKE, FAKE, FAKE, FAKE, FAKE + 16, need, None) == WORKSPACE
     assert mv(FAKE, None, 2, 5, 3, FAKE, FAKE, None, FAKE, None, 0, None) == NULL_ARG
+    assert L.ts_chain_logpartition_sequential(FAKE, None, 2, 5, CW, None, None) == NULL_ARG
+    assert L.ts_chain_logpartition_sequential(None, None, 2, 5, CW, FAKE, None) == NULL_ARG
     need = binding.workspace_bytes(4, 2, 5, CW)
     assert L.ts_chain_entropy(FAKE, None, 2, 5, CW, None, FAKE, need, None) == NULL_ARG
     assert "entropy" in _err(L)
