@@ -50,6 +50,7 @@ def load_library(path):
     if hasattr(lib, "orc_entropy"):
         lib.orc_entropy.argtypes = [p, p, i64, i64, i64, p]
         lib.orc_log_density.argtypes = [p, p, p, i64, i64, i64, p]
+        lib.orc_sample.argtypes = [p, p, p, i64, i64, i64, i64, p, p]
     lib.orc_max_threads.restype = ctypes.c_int
     return lib
 
@@ -144,6 +145,25 @@ def log_density(pot, labels, lengths=None, lib=None):
     out = np.empty(B, np.float64)
     _check(_load(lib).orc_log_density(_ptr(pot), _ptr(lengths), _ptr(labels), B, N, C, _ptr(out)))
     return out
+
+
+def sample(pot, uniforms, lengths=None, lib=None):
+    """Forward-filtering backward-sampling draws with the given uniforms [S, B, N] in
+    [0, 1): (paths int32 [S, B, N] with -1 past each length, margin float64 [S, B] -- the
+    closest any draw of that sequence came to picking a neighbouring label, relative to the
+    draw's total weight)."""
+    pot, lengths, f64, B, N, C = _prep(pot, lengths)
+    if f64:
+        raise ValueError("sample takes fp32 potentials")
+    uniforms = np.ascontiguousarray(uniforms, dtype=np.float32)
+    if uniforms.ndim != 3 or uniforms.shape[1:] != (B, N):
+        raise ValueError("uniforms must be [S, B, N]")
+    S = uniforms.shape[0]
+    paths = np.empty((S, B, N), np.int32)
+    margin = np.empty((S, B), np.float64)
+    _check(_load(lib).orc_sample(_ptr(pot), _ptr(lengths), _ptr(uniforms), S, B, N, C,
+                                 _ptr(paths), _ptr(margin)))
+    return paths, margin
 
 
 def marginals_seq(pot, lengths, b, t0, t1):

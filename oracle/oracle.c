@@ -19,7 +19,9 @@
  *     with ties resolved by taking the lowest label index at every backtrace step;
  *   - the entropy H = -sum_z p(z) log p(z) of the chain distribution (Sec. 5.1; the
  *     quantity of Table 2's "Entropy" semiring), from the edge marginals by the chain
- *     rule, and the log-probability log p(z) of a given label sequence (Sec. 5.1).
+ *     rule, and the log-probability log p(z) of a given label sequence (Sec. 5.1);
+ *   - samples from p(z) by forward filtering, backward sampling with caller-supplied
+ *     uniforms (Table 2's "Sample" semiring draws from the same distribution).
  *
  * Conventions (the paper leaves these open; the readings are listed in the design notes):
  *   - pot is [B, N-1, C, C] row-major: pot[((b*(N-1)+t)*C+i)*C+j] = l[b, t, i, j].
@@ -305,6 +307,79 @@ static int log_density_impl(const float* pf, const double* pd, const int32_t* le
     return rc;
 }
 
+/*
+ * Forward filtering, backward sampling (the "Sample" semiring of Table 2 draws from the
+ * same distribution): with edge marginals mu and node marginals m,
+ *   z_{L-1} ~ m_{L-1}(j) = sum_i mu[L-2, i, j],
+ *   z_t | z_{t+1} = j ~ p(z_t = i | z_{t+1} = j) = mu[t, i, j] / m_{t+1}(j),  t = L-2..0
+ * (the Markov property of the chain).  One token: z_0 uniform over the C labels.  Each
+ * draw takes the caller's uniform u in [0, 1) by inverse CDF: the smallest k whose
+ * inclusive prefix sum of the weights exceeds u * total (all-zero weights: k = 0).
+ * uniforms and paths are [S, B, N]; paths get -1 past each length.  margin[s*B + b]
+ * receives the smallest distance of u * total from an edge of the chosen bin, relative to
+ * the total, over that sequence's draws (how close the draw came to a different label).
+ */
+static int draw(const double* w, int64_t C, double u, double* margin) {
+    double tot = 0.0;
+    for (int64_t k = 0; k < C; ++k) tot += w[k];
+    if (!(tot > 0.0)) { *margin = INFINITY; return 0; }
+    const double x = u * tot;
+    double cum = 0.0;
+    for (int64_t k = 0; k < C; ++k) {
+        const double lo = cum;
+        cum += w[k];
+        if (cum > x || k == C - 1) {
+            const double d = fmin(x - lo, cum - x) / tot;
+            *margin = d;
+            return (int)k;
+        }
+    }
+    *margin = INFINITY;
+    return 0;
+}
+
+static int sample_impl(const float* pf, const int32_t* lengths, const float* uniforms,
+                       int64_t S, int64_t B, int64_t N, int64_t C, int32_t* paths,
+                       double* margin) {
+    int rc = check_args(pf, NULL, lengths, B, N, C);
+    if (rc) return rc;
+    if (!uniforms || S < 1) return ORC_ERR_ARG;
+    double* logZ = malloc(sizeof(double) * B);
+    double* marg = malloc(sizeof(double) * B * (N > 1 ? N - 1 : 1) * C * C);
+    double* w = malloc(sizeof(double) * C);
+    if (!logZ || !marg || !w) { free(logZ); free(marg); free(w); return ORC_ERR_MEM; }
+    if (N > 1) rc = marginals_impl(pf, NULL, lengths, B, N, C, logZ, marg);
+    if (rc == ORC_OK)
+        for (int64_t s = 0; s < S; ++s)
+            for (int64_t b = 0; b < B; ++b) {
+                const int64_t L = lengths ? lengths[b] : N;
+                const float* u = uniforms + (s * B + b) * N;
+                int32_t* z = paths + (s * B + b) * N;
+                double mg = INFINITY, d;
+                for (int64_t n = L; n < N; ++n) z[n] = -1;
+                if (L == 1) {
+                    for (int64_t k = 0; k < C; ++k) w[k] = 1.0;
+                } else {
+                    const double* mu = marg + (b * (N - 1) + (L - 2)) * C * C;
+                    for (int64_t j = 0; j < C; ++j) {
+                        w[j] = 0.0;
+                        for (int64_t i = 0; i < C; ++i) w[j] += mu[i * C + j];
+                    }
+                }
+                z[L - 1] = draw(w, C, (double)u[L - 1], &d);
+                mg = fmin(mg, d);
+                for (int64_t t = L - 2; t >= 0; --t) {
+                    const double* mu = marg + (b * (N - 1) + t) * C * C;
+                    for (int64_t i = 0; i < C; ++i) w[i] = mu[i * C + z[t + 1]];
+                    z[t] = draw(w, C, (double)u[t], &d);
+                    mg = fmin(mg, d);
+                }
+                if (margin) margin[s * B + b] = mg;
+            }
+    free(logZ); free(marg); free(w);
+    return rc;
+}
+
 /* ---------------- exported entry points ---------------- */
 
 /* OpenMP threads a parallel region of the oracle may use */
@@ -331,6 +406,11 @@ int orc_entropy(const float* pot, const int32_t* lengths, int64_t B, int64_t N, 
 int orc_log_density(const float* pot, const int32_t* lengths, const int32_t* labels, int64_t B,
                     int64_t N, int64_t C, double* out) {
     return log_density_impl(pot, NULL, lengths, labels, B, N, C, out);
+}
+
+int orc_sample(const float* pot, const int32_t* lengths, const float* uniforms, int64_t S,
+               int64_t B, int64_t N, int64_t C, int32_t* paths, double* margin) {
+    return sample_impl(pot, lengths, uniforms, S, B, N, C, paths, margin);
 }
 
 /* float64 potentials (used by the finite-difference pins) */
