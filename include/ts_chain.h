@@ -65,6 +65,7 @@ typedef int ts_status;
 #define TS_OP_MARGINALS_VITERBI 3
 #define TS_OP_ENTROPY 4
 #define TS_OP_LOG_DENSITY 5
+#define TS_OP_SAMPLE 6
 
 /* Largest supported number of labels C. */
 int ts_chain_max_labels(void);
@@ -147,6 +148,22 @@ ts_status ts_chain_entropy(const float* pot, const int32_t* lengths, int64_t B, 
 ts_status ts_chain_log_density(const float* pot, const int32_t* lengths, const int32_t* labels,
                                int64_t B, int64_t N, int64_t C, float* logp, void* ws,
                                size_t ws_bytes, void* stream);
+
+/*
+ * S samples per sequence from p(z) = exp(score(z) - A) (Sec. 5.1; the distribution Table 2's
+ * "Sample" semiring draws from) by forward filtering, backward sampling from the edge
+ * marginals:  z_{L-1} ~ sum_i mu[L-2, i, .],  z_t | z_{t+1} = j ~ mu[t, ., j].
+ *   uniforms device float32 [S, B, N] in [0, 1), supplied by the caller (the library draws no
+ *            random numbers): u[s, b, t] draws token t of sample s of sequence b by inverse
+ *            CDF -- the smallest label k whose inclusive prefix sum of the weights exceeds
+ *            u * (their total).  One token: uniform over the C labels.
+ *   paths    device int32 [S, B, N], -1 past each length.
+ * Workspace: ts_chain_workspace_bytes(TS_OP_SAMPLE, ...) (the marginals workspace and the
+ * marginals).  A sequence with no finite path draws label 0 everywhere.
+ */
+ts_status ts_chain_sample(const float* pot, const int32_t* lengths, const float* uniforms,
+                          int64_t S, int64_t B, int64_t N, int64_t C, int32_t* paths, void* ws,
+                          size_t ws_bytes, void* stream);
 
 /*
  * Log-partition by the left-to-right forward algorithm (Sec. 5.2), the serial ordering that

@@ -11,7 +11,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libtschain.so")
 
 OP_LOGPARTITION, OP_MARGINALS, OP_VITERBI, OP_MARGINALS_VITERBI = 0, 1, 2, 3
-OP_ENTROPY, OP_LOG_DENSITY = 4, 5
+OP_ENTROPY, OP_LOG_DENSITY, OP_SAMPLE = 4, 5, 6
 STATUS = {0: "TS_OK", -1: "TS_ERR_NULL_ARG", -2: "TS_ERR_BAD_DIM", -3: "TS_ERR_WORKSPACE",
           -4: "TS_ERR_LENGTHS", -5: "TS_ERR_HIP", -6: "TS_ERR_LABELS"}
 
@@ -42,9 +42,10 @@ def lib():
         L.ts_chain_entropy.argtypes = [p, p, i64, i64, i64, p, p, sz, p]
         L.ts_chain_log_density.argtypes = [p, p, p, i64, i64, i64, p, p, sz, p]
         L.ts_chain_logpartition_sequential.argtypes = [p, p, i64, i64, i64, p, p]
+        L.ts_chain_sample.argtypes = [p, p, p, i64, i64, i64, i64, p, p, sz, p]
         for f in ("ts_chain_logpartition", "ts_chain_marginals", "ts_chain_viterbi",
                   "ts_chain_marginals_viterbi", "ts_chain_entropy", "ts_chain_log_density",
-                  "ts_chain_logpartition_sequential"):
+                  "ts_chain_logpartition_sequential", "ts_chain_sample"):
             getattr(L, f).restype = ctypes.c_int
         L.ts_last_error.restype = ctypes.c_char_p
         _lib = L
@@ -178,3 +179,20 @@ def logpartition_sequential(pot, lengths=None, out=None):
     _check(lib().ts_chain_logpartition_sequential(_ptr(pot), _ptr(lengths), B, N, C, _ptr(logz),
                                                   _stream(pot.device)))
     return logz
+
+
+def sample(pot, uniforms, lengths=None, out=None, ws=None):
+    """Forward-filtering backward-sampling draws: paths int32 [S, B, N] (-1 past each
+    length) from caller-supplied uniforms float32 [S, B, N] in [0, 1)."""
+    pot, lengths, B, N, C = _prep(pot, lengths)
+    if (uniforms.device != pot.device or uniforms.dtype != torch.float32 or uniforms.dim() != 3
+            or tuple(uniforms.shape[1:]) != (B, N)):
+        raise ValueError("uniforms must be float32 [S, B, N] on the same device as pot")
+    uniforms = uniforms.contiguous()
+    S = uniforms.shape[0]
+    paths = out if out is not None else torch.empty((S, B, N), dtype=torch.int32,
+                                                    device=pot.device)
+    w, nb = _workspace(OP_SAMPLE, B, N, C, pot.device, ws)
+    _check(lib().ts_chain_sample(_ptr(pot), _ptr(lengths), _ptr(uniforms), S, B, N, C,
+                                 _ptr(paths), _ptr(w), nb, _stream(pot.device)))
+    return paths

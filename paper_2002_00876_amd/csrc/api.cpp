@@ -189,13 +189,13 @@ struct Derived {
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 bool plan_derived(int op, int64_t B, int64_t N, int64_t C, Derived* d) {
-    const int baseOp = op == TS_OP_ENTROPY ? TS_OP_MARGINALS : TS_OP_LOGPARTITION;
+    const int baseOp = op == TS_OP_LOG_DENSITY ? TS_OP_LOGPARTITION : TS_OP_MARGINALS;
     if (!make_plan(baseOp, B, N, C, nullptr, &d->base)) return false;
     const size_t E = (size_t)(N - 1);
-    if (op == TS_OP_ENTROPY) {
+    if (op == TS_OP_ENTROPY || op == TS_OP_SAMPLE) {
         d->mu = 0;
         d->part = align_up(sizeof(float) * B * E * C * C);
-        d->extra = d->part + align_up(sizeof(double) * B * E);
+        d->extra = d->part + (op == TS_OP_ENTROPY ? align_up(sizeof(double) * B * E) : 0);
     } else {
         d->logz = 0;
         d->extra = align_up(sizeof(float) * B);
@@ -218,10 +218,10 @@ extern "C" {
 int ts_chain_max_labels(void) { return kMaxLabels; }
 
 size_t ts_chain_workspace_bytes(int op, int64_t B, int64_t N, int64_t C) {
-    if (op < TS_OP_LOGPARTITION || op > TS_OP_LOG_DENSITY || B < 1 || N < 1 || C < 1 ||
+    if (op < TS_OP_LOGPARTITION || op > TS_OP_SAMPLE || B < 1 || N < 1 || C < 1 ||
         C > kMaxLabels)
         return 0;
-    if (op == TS_OP_ENTROPY || op == TS_OP_LOG_DENSITY) {
+    if (op >= TS_OP_ENTROPY) {
         Derived d;
         if (!plan_derived(op, B, N, C, &d)) return 0;
         return d.base.bytes + d.extra;
@@ -370,6 +370,38 @@ ts_status ts_chain_log_density(const float* pot, const int32_t* lengths, const i
         e = launch_logz_tree(d.base, pot, lengths, logz, s);
     }
     if (e == hipSuccess) e = launch_log_density(pot, lengths, labels, logz, B, N, C, logp, s);
+    return hip_status(e);
+}
+
+ts_status ts_chain_sample(const float* pot, const int32_t* lengths, const float* uniforms,
+                          int64_t S, int64_t B, int64_t N, int64_t C, int32_t* paths, void* ws,
+                          size_t ws_bytes, void* stream) {
+    Derived d;
+    ts_status st = check_dims(pot, B, N, C, TS_OP_MARGINALS, &d.base);
+    if (st != TS_OK) return st;
+    if (S < 1) return fail(TS_ERR_BAD_DIM, "S must be >= 1");
+    int64_t sbn;
+    if (!mul_ok(S, B, &sbn) || sbn > ((int64_t)1 << 32) || !mul_ok(sbn, N, &sbn) ||
+        sbn > ((int64_t)1 << 40))
+        return fail(TS_ERR_BAD_DIM, "S * B * N overflows the supported range");
+    plan_derived(TS_OP_SAMPLE, B, N, C, &d);
+    if ((st = check_ws(d.base.bytes + d.extra, ws, ws_bytes)) != TS_OK) return st;
+    if (!uniforms || !paths) return fail(TS_ERR_NULL_ARG, "uniforms or paths is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = check_lengths(lengths, B, N, s)) != TS_OK) return st;
+    float* mu = N > 1 ? reinterpret_cast<float*>(static_cast<char*>(ws) + d.base.bytes + d.mu)
+                      : nullptr;
+    hipError_t e = hipSuccess;
+    if (N > 1) {
+        if (d.base.fused) {
+            e = launch_small_log(pot, lengths, B, N, C, nullptr, mu, s);
+        } else {
+            make_plan(TS_OP_MARGINALS, B, N, C, ws, &d.base);
+            e = launch_logz_tree(d.base, pot, lengths, nullptr, s);
+            if (e == hipSuccess) e = launch_marginals_tree(d.base, pot, lengths, mu, s);
+        }
+    }
+    if (e == hipSuccess) e = launch_sample(mu, lengths, uniforms, S, B, N, C, paths, s);
     return hip_status(e);
 }
 

@@ -3,7 +3,11 @@
 //   semiring) from the edge marginals by the chain rule of entropy of a Markov chain:
 //     H = H(z_0) + sum_t H(z_{t+1} | z_t),   m_t(i) = sum_j mu[t,i,j],
 //     H(z_0) = -sum_i m_0(i) log m_0(i),  H(z_{t+1} | z_t) = -sum_{i,j} mu log(mu / m_t(i));
-//   log-probability of a given label sequence (Sec. 5.1): log p(z) = sum_t l[t,z_t,z_{t+1}] - A.
+//   log-probability of a given label sequence (Sec. 5.1): log p(z) = sum_t l[t,z_t,z_{t+1}] - A;
+//   samples by forward filtering, backward sampling (the distribution of Table 2's "Sample"
+//   semiring) from the edge marginals: z_{L-1} ~ sum_i mu[L-2,i,.], then
+//   z_t | z_{t+1} = j ~ mu[t,.,j] (the Markov property), each draw by inverse CDF with a
+//   caller-supplied uniform: the smallest k whose inclusive prefix sum exceeds u * total.
 // Every term of H is >= 0, so the sum has no cancellation.  Reductions run in a fixed
 // order (no atomics): per-edge partials first, then one pass per sequence.
 #include "device.h"
@@ -96,7 +100,99 @@ __global__ __launch_bounds__(kEntThreads) void k_log_density(const float* pot,
     }
 }
 
+// Inverse-CDF draw over the c weights w[k * stride] by one wave: lane l holds labels l,
+// l + 64, ... (kMaxLabels / 64 chunks in registers).  The total is the scan's own final
+// prefix, so u < 1 always lands inside it; a label of weight 0 is never taken (the prefix
+// test also asks w > 0), and if rounding leaves no positive label past u * total the last
+// positive label is taken.  All weights 0: label 0.
+constexpr int kChunks = kMaxLabels / kWave;
+
+__device__ int draw_wave(const float* w, int stride, int c, float u, int lane) {
+    float p[kChunks], wk[kChunks];
+    float carry = 0.f;
+#pragma unroll
+    for (int q = 0; q < kChunks; ++q) {
+        const int k = q * kWave + lane;
+        if (q * kWave >= c) {   // wave-uniform: chunks past c hold nothing
+            wk[q] = 0.f;
+            p[q] = carry;
+            continue;
+        }
+        wk[q] = k < c ? w[(size_t)k * stride] : 0.f;
+        float x = wk[q];
+#pragma unroll
+        for (int d = 1; d < kWave; d <<= 1) {
+            const float o = __shfl_up(x, d, kWave);
+            if (lane >= d) x += o;
+        }
+        p[q] = x + carry;
+        carry = __shfl(p[q], kWave - 1, kWave);
+    }
+    const float tot = carry;
+    if (!(tot > 0.f)) return 0;
+    const float x = u * tot;
+    int last = 0;
+#pragma unroll
+    for (int q = 0; q < kChunks; ++q) {
+        const uint64_t hit = __ballot(wk[q] > 0.f && p[q] > x);
+        if (hit) return q * kWave + __builtin_ctzll(hit);
+        const uint64_t pos = __ballot(wk[q] > 0.f);
+        if (pos) last = q * kWave + 63 - __builtin_clzll(pos);
+    }
+    return last;
+}
+
+constexpr int kSampleWaves = 4;
+
+__global__ __launch_bounds__(kSampleWaves * kWave) void k_sample(const float* mu,
+                                                                 const int32_t* lengths,
+                                                                 const float* uniforms,
+                                                                 int64_t S, int64_t B,
+                                                                 int64_t N, int64_t C,
+                                                                 int32_t* paths) {
+    __shared__ float colsum[kSampleWaves][kMaxLabels];
+    const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int64_t sb = (int64_t)blockIdx.x * kSampleWaves + w;
+    if (sb >= S * B) return;
+    const int64_t b = sb % B, E = N - 1;
+    const int64_t L = clamp_len(lengths, b, N);
+    const int c = (int)C;
+    const float* u = uniforms + sb * N;
+    int32_t* z = paths + sb * N;
+    for (int64_t n = L + lane; n < N; n += kWave) z[n] = -1;
+    // the last token: column sums of the last edge's marginal (uniform for one token)
+    float* cs = colsum[w];
+    for (int j = lane; j < c; j += kWave) {
+        float s = 1.f;
+        if (L > 1) {
+            const float* last = mu + (size_t)(b * E + (L - 2)) * c * c;
+            s = 0.f;
+            for (int i = 0; i < c; ++i) s += last[(size_t)i * c + j];
+        }
+        cs[j] = s;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    int zn = draw_wave(cs, 1, c, u[L - 1], lane);
+    if (lane == 0) z[L - 1] = zn;
+    for (int64_t t = L - 2; t >= 0; --t) {
+        const float* col = mu + (size_t)(b * E + t) * c * c + zn;   // mu[t][.][z_{t+1}]
+        zn = draw_wave(col, c, c, u[t], lane);
+        if (lane == 0) z[t] = zn;
+    }
+}
+
 }  // namespace
+
+hipError_t launch_sample(const float* mu, const int32_t* lengths, const float* uniforms,
+                         int64_t S, int64_t B, int64_t N, int64_t C, int32_t* paths,
+                         hipStream_t s) {
+    const int64_t waves = S * B;
+    hipLaunchKernelGGL(k_sample, dim3((unsigned)((waves + kSampleWaves - 1) / kSampleWaves)),
+                       dim3(kSampleWaves * kWave), 0, s, mu, lengths, uniforms, S, B, N, C, paths);
+    return hipGetLastError();
+}
 
 hipError_t launch_entropy(const float* mu, const int32_t* lengths, int64_t B, int64_t N,
                           int64_t C, double* part, float* H, hipStream_t s) {

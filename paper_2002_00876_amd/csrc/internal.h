@@ -71,6 +71,10 @@ hipError_t launch_single_token(int64_t B, int64_t N, int64_t C, int op, float* l
 // entropy from marginals mu [B, N-1, C, C]; part is [B, N-1] doubles (unused when N == 1)
 hipError_t launch_entropy(const float* mu, const int32_t* lengths, int64_t B, int64_t N,
                           int64_t C, double* part, float* H, hipStream_t s);
+// FFBS draws from marginals mu [B, N-1, C, C] with uniforms [S, B, N] into paths [S, B, N]
+hipError_t launch_sample(const float* mu, const int32_t* lengths, const float* uniforms,
+                         int64_t S, int64_t B, int64_t N, int64_t C, int32_t* paths,
+                         hipStream_t s);
 hipError_t launch_logz_sequential(const float* pot, const int32_t* lengths, int64_t B,
                                   int64_t N, int64_t C, float* logZ, hipStream_t s);
 hipError_t launch_log_density(const float* pot, const int32_t* lengths, const int32_t* labels,

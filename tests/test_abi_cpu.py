@@ -61,7 +61,8 @@ def test_workspace_sizes(L, monkeypatch):
     # the tree over N-1 = 24 edges has levels of 16, 8, 4, 2, 1 nodes of C*C floats
     core = 32 * (16 + 8 + 4 + 2 + 1) * CW * CW * 4
     assert ws(0, 32, 25, CW) >= core
-    assert ws(6, 32, 25, CW) == 0 and ws(0, 0, 25, 20) == 0 and ws(0, 1, 25, 257) == 0
+    assert ws(7, 32, 25, CW) == 0 and ws(0, 0, 25, 20) == 0 and ws(0, 1, 25, 257) == 0
+    assert ws(6, 32, 25, CW) >= ws(1, 32, 25, CW) + 32 * 24 * CW * CW * 4
     # entropy: the marginals workspace, the marginals themselves and per-edge partials;
     # log density: the log-partition workspace and log Z
     assert ws(4, 32, 25, CW) >= ws(1, 32, 25, CW) + 32 * 24 * CW * CW * 4 + 32 * 24 * 8
@@ -83,6 +84,7 @@ def test_bad_dimensions_are_rejected(L):
     for B, N, C in [(0, 5, 3), (2, 0, 3), (2, 5, 0), (2, 5, 257), (-1, 5, 3)]:
         assert L.ts_chain_entropy(FAKE, None, B, N, C, FAKE, FAKE, 1 << 30, None) == BAD_DIM
         assert L.ts_chain_logpartition_sequential(FAKE, None, B, N, C, FAKE, None) == BAD_DIM
+        assert L.ts_chain_sample(FAKE, None, FAKE, 1, B, N, C, FAKE, FAKE, 1 << 30, None) == BAD_DIM
         assert L.ts_chain_log_density(FAKE, None, FAKE, B, N, C, FAKE, FAKE, 1 << 30, None) == BAD_DIM
         assert L.ts_chain_logpartition(FAKE, None, B, N, C, FAKE, FAKE, 1 << 30, None) == BAD_DIM
         assert L.ts_chain_marginals(FAKE, None, B, N, C, FAKE, FAKE, FAKE, 1 << 30, None) == BAD_DIM
@@ -124,6 +126,11 @@ def test_null_pointers_are_rejected(L):
     assert mv(FAKE, None, 2, 5, CW, FAKE, FAKE, FAKE, FAKE, FAKE + 16, need, None) == WORKSPACE
     assert mv(FAKE, None, 2, 5, 3, FAKE, FAKE, None, FAKE, None, 0, None) == NULL_ARG
     assert L.ts_chain_logpartition_sequential(FAKE, None, 2, 5, CW, None, None) == NULL_ARG
+    need = binding.workspace_bytes(6, 2, 5, CW)
+    assert L.ts_chain_sample(FAKE, None, FAKE, 0, 2, 5, CW, FAKE, FAKE, need, None) == BAD_DIM
+    assert L.ts_chain_sample(FAKE, None, None, 3, 2, 5, CW, FAKE, FAKE, need, None) == NULL_ARG
+    assert L.ts_chain_sample(FAKE, None, FAKE, 3, 2, 5, CW, None, FAKE, need, None) == NULL_ARG
+    assert L.ts_chain_sample(FAKE, None, FAKE, 3, 2, 5, CW, FAKE, FAKE, need - 1, None) == WORKSPACE
     assert L.ts_chain_logpartition_sequential(None, None, 2, 5, CW, FAKE, None) == NULL_ARG
     need = binding.workspace_bytes(4, 2, 5, CW)
     assert L.ts_chain_entropy(FAKE, None, 2, 5, CW, None, FAKE, need, None) == NULL_ARG
