@@ -45,6 +45,12 @@ def parse():
                     help="instead of the step: log Z by the scan against the left-to-right "
                          "kernel over sequence lengths (depth: B=16, C=20) or label counts "
                          "(labels: B=16, N=20); one JSON line per point")
+    ap.add_argument("--ops", action="store_true",
+                    help="instead of the step: time each entry point separately on the "
+                         "workload (log Z by the scan and left to right, marginals, entropy, "
+                         "log-density, sampling); one JSON line per entry point")
+    ap.add_argument("--samples", type=int, default=64,
+                    help="samples per sequence for the sampling entry point under --ops")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this size (traffic-counter scale)")
     return ap.parse_args()
@@ -169,6 +175,71 @@ def sweep(kind, reps=20):
                           "scan_speedup": round(ms_seq / ms_scan, 3)}), flush=True)
 
 
+def ops(w, samples, reps=50):
+    """Time each entry point separately on one workload: the hot path's calls and the
+    quantities read off their outputs (entropy, log-density of the Viterbi labels, samples).
+    ms is the mean of back-to-back calls by HIP events on the library's stream; extra_ms is
+    the time over the call the entry point builds on."""
+    import numpy as np
+    import torch
+
+    from paper_2002_00876_amd import binding, workloads
+
+    pot_h, lens_h = workloads.generate(w)
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    pot = torch.from_numpy(pot_h).to(dev)
+    lens = torch.from_numpy(lens_h).to(dev)
+    B, E, C, _ = pot.shape
+    N = E + 1
+    path, _ = binding.viterbi(pot, lens)
+    labels = torch.where(path >= 0, path, torch.zeros_like(path)).contiguous()
+    u = torch.from_numpy(np.random.default_rng(7).random((samples, B, N), dtype=np.float32))
+    u = u.to(dev)
+    wss = {op: binding._workspace(op, B, N, C, dev)[0] for op in range(7)}
+    logz = torch.empty(B, dtype=torch.float32, device=dev)
+    marg = torch.empty_like(pot)
+    h = torch.empty(B, dtype=torch.float32, device=dev)
+    lp = torch.empty(B, dtype=torch.float32, device=dev)
+    paths = torch.empty((samples, B, N), dtype=torch.int32, device=dev)
+    calls = {
+        "logpartition": (lambda: binding.logpartition(pot, lens, out=logz,
+                                                      ws=wss[binding.OP_LOGPARTITION]), None),
+        "logpartition_sequential": (lambda: binding.logpartition_sequential(pot, lens, out=logz),
+                                    None),
+        "marginals": (lambda: binding.marginals(pot, lens, out=(logz, marg),
+                                                ws=wss[binding.OP_MARGINALS]), None),
+        "entropy": (lambda: binding.entropy(pot, lens, out=h, ws=wss[binding.OP_ENTROPY]),
+                    "marginals"),
+        "log_density": (lambda: binding.log_density(pot, labels, lens, out=lp,
+                                                    ws=wss[binding.OP_LOG_DENSITY]),
+                        "logpartition"),
+        "sample": (lambda: binding.sample(pot, u, lens, out=paths, ws=wss[binding.OP_SAMPLE]),
+                   "marginals"),
+    }
+    ms = {}
+    for name, (fn, base) in calls.items():
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms[name] = e0.elapsed_time(e1) / reps
+        tokens = B * N * (samples if name == "sample" else 1)
+        line = {"op": name, "workload": f"{w.name}: B={B} N={N} C={C}", "ms": round(ms[name], 5),
+                "tokens_per_s": round(tokens / (ms[name] * 1e-3), 1)}
+        if name == "sample":
+            line["samples_per_sequence"] = samples
+        if base is not None:
+            line["extra_ms"] = round(ms[name] - ms[base], 5)
+        print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -188,6 +259,9 @@ def main():
         return
     binding.lib()   # fail loudly if the HIP library is missing
     w = workloads.WORKLOADS[args.workload]
+    if args.ops:
+        ops(w, args.samples)
+        return
     pot_h, lens_h = workloads.generate(w)
     dev = torch.device("cuda:0")
     pot = torch.from_numpy(pot_h).to(dev)

@@ -18,8 +18,14 @@ namespace {
 
 constexpr int kEntThreads = 256;
 
-// one workgroup per valid edge: part[b][t] = H(z_{t+1} | z_t) (+ H(z_0) for t = 0);
-// one wave per row i of mu_t, lanes over j
+// one workgroup per valid edge: part[b][t] = H(z_{t+1} | z_t) (+ H(z_0) for t = 0).  Each
+// wave takes kGroup rows of mu_t at a time, lanes over j (kPer = ceil(C / 64) values of a
+// row per lane): all the group's loads are issued before any reduction, so a wave keeps
+// kGroup * kPer coalesced row loads in flight.  Per row:
+//   m = sum_j p,   m * H(row / m) = -sum_j p (log p - log m).
+constexpr int kGroup = 8;
+
+template <int kPer>
 __global__ __launch_bounds__(kEntThreads) void k_entropy_edges(const float* mu,
                                                                const int32_t* lengths,
                                                                int64_t N, int64_t C,
@@ -32,20 +38,32 @@ __global__ __launch_bounds__(kEntThreads) void k_entropy_edges(const float* mu,
     const float* m = mu + (size_t)(b * E + t) * c * c;
     const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     double acc = 0.0;
-    for (int i = w; i < c; i += kEntThreads / kWave) {
-        const float* row = m + (size_t)i * c;
-        float rs = 0.f;
-        for (int j = lane; j < c; j += kWave) rs += row[j];
-        const float mi = wave_sum(rs);
-        if (mi <= 0.f) continue;
+    for (int i0 = w * kGroup; i0 < c; i0 += (kEntThreads / kWave) * kGroup) {
+        float v[kGroup][kPer];
+#pragma unroll
+        for (int g = 0; g < kGroup; ++g)
+#pragma unroll
+            for (int q = 0; q < kPer; ++q) {
+                const int i = i0 + g, j = q * kWave + lane;
+                v[g][q] = (i < c && j < c) ? m[(size_t)i * c + j] : 0.f;
+            }
         float h = 0.f;
-        for (int j = lane; j < c; j += kWave) {
-            const float p = row[j];
-            if (p > 0.f) h -= p * flog(p / mi);
+#pragma unroll
+        for (int g = 0; g < kGroup; ++g) {
+            float rs = 0.f;
+#pragma unroll
+            for (int q = 0; q < kPer; ++q) rs += v[g][q];
+            const float mi = wave_sum(rs);
+            if (!(mi > 0.f)) continue;   // wave-uniform
+            const float lm = flog(mi);
+            float hg = 0.f;
+#pragma unroll
+            for (int q = 0; q < kPer; ++q)
+                if (v[g][q] > 0.f) hg -= v[g][q] * (flog(v[g][q]) - lm);
+            if (t == 0 && lane == 0) hg -= mi * lm;
+            h += hg;
         }
-        h = wave_sum(h);
-        if (t == 0) h -= mi * flog(mi);
-        acc += (double)h;
+        acc += (double)wave_sum(h);
     }
     if (lane == 0) red[w] = acc;
     __syncthreads();
@@ -56,19 +74,28 @@ __global__ __launch_bounds__(kEntThreads) void k_entropy_edges(const float* mu,
     }
 }
 
-// one thread per sequence: H = sum of its edges' partials in edge order (log C for one token)
-__global__ void k_entropy_sum(const double* part, const int32_t* lengths, int64_t B,
-                              int64_t N, int64_t C, float* H) {
-    const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (b >= B) return;
-    const int64_t E = N - 1, Eb = clamp_len(lengths, b, N) - 1;
+// one workgroup per sequence: H = the sum of its edges' partials (log C for one token), in
+// a fixed order -- thread k sums edges k, k + 256, ..., then waves and lanes combine in a
+// fixed tree -- so the result does not depend on scheduling
+__global__ __launch_bounds__(kEntThreads) void k_entropy_sum(const double* part,
+                                                             const int32_t* lengths,
+                                                             int64_t N, int64_t C, float* H) {
+    __shared__ double red[kEntThreads / kWave];
+    const int64_t b = blockIdx.x, E = N - 1, Eb = clamp_len(lengths, b, N) - 1;
     if (Eb == 0) {
-        H[b] = logf((float)C);
+        if (threadIdx.x == 0) H[b] = logf((float)C);
         return;
     }
     double s = 0.0;
-    for (int64_t t = 0; t < Eb; ++t) s += part[b * E + t];
-    H[b] = (float)s;
+    for (int64_t t = threadIdx.x; t < Eb; t += kEntThreads) s += part[b * E + t];
+    s = wave_sum_d(s);
+    if (threadIdx.x % kWave == 0) red[threadIdx.x / kWave] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double tot = 0.0;
+        for (int i = 0; i < kEntThreads / kWave; ++i) tot += red[i];
+        H[b] = (float)tot;
+    }
 }
 
 // one workgroup per sequence: log p(z) = sum_{t < L-1} l[t, z_t, z_{t+1}] - log Z.  Labels
@@ -197,13 +224,18 @@ hipError_t launch_sample(const float* mu, const int32_t* lengths, const float* u
 hipError_t launch_entropy(const float* mu, const int32_t* lengths, int64_t B, int64_t N,
                           int64_t C, double* part, float* H, hipStream_t s) {
     if (N > 1) {
-        hipLaunchKernelGGL(k_entropy_edges, dim3((unsigned)(B * (N - 1))), dim3(kEntThreads), 0,
-                           s, mu, lengths, N, C, part);
+        const dim3 g((unsigned)(B * (N - 1))), blk(kEntThreads);
+        if (C <= kWave)
+            hipLaunchKernelGGL(k_entropy_edges<1>, g, blk, 0, s, mu, lengths, N, C, part);
+        else if (C <= 2 * kWave)
+            hipLaunchKernelGGL(k_entropy_edges<2>, g, blk, 0, s, mu, lengths, N, C, part);
+        else
+            hipLaunchKernelGGL(k_entropy_edges<4>, g, blk, 0, s, mu, lengths, N, C, part);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(k_entropy_sum, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s, part,
-                       lengths, B, N, C, H);
+    hipLaunchKernelGGL(k_entropy_sum, dim3((unsigned)B), dim3(kEntThreads), 0, s, part, lengths,
+                       N, C, H);
     return hipGetLastError();
 }
 
