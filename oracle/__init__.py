@@ -1,4 +1,4 @@
-"""Float64 CPU oracle for batched linear-chain CRF inference.
+"""Float64 CPU oracle for batched linear-chain (and semi-Markov) CRF inference.
 
 TEST INFRASTRUCTURE ONLY: the slow, plain checker the HIP path is compared against.
 Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
@@ -51,6 +51,10 @@ def load_library(path):
         lib.orc_entropy.argtypes = [p, p, i64, i64, i64, p]
         lib.orc_log_density.argtypes = [p, p, p, i64, i64, i64, p]
         lib.orc_sample.argtypes = [p, p, p, i64, i64, i64, i64, p, p]
+    if hasattr(lib, "orc_semi_marginals"):
+        for name in ("orc_semi_marginals", "orc_semi_marginals_f64"):
+            getattr(lib, name).argtypes = [p, p, i64, i64, i64, i64, p, p]
+        lib.orc_semi_viterbi.argtypes = [p, p, i64, i64, i64, i64, p, p, p]
     lib.orc_max_threads.restype = ctypes.c_int
     return lib
 
@@ -181,3 +185,54 @@ def marginals_seq(pot, lengths, b, t0, t1):
 def max_threads():
     """OpenMP threads available to the oracle's parallel loops."""
     return _load().orc_max_threads()
+
+
+def _prep_semi(sp, lengths):
+    sp = np.asarray(sp)
+    if sp.ndim != 5 or sp.shape[3] != sp.shape[4]:
+        raise ValueError("semi-Markov potentials must be [B, N-1, K, C, C]")
+    f64 = sp.dtype == np.float64
+    sp = np.ascontiguousarray(sp, dtype=np.float64 if f64 else np.float32)
+    B, E, K, C, _ = sp.shape
+    if lengths is not None:
+        lengths = np.ascontiguousarray(lengths, dtype=np.int32)
+        if lengths.shape != (B,):
+            raise ValueError("lengths must be [B]")
+    return sp, lengths, f64, B, E + 1, K, C
+
+
+def semi_marginals(sp, lengths=None, lib=None):
+    """Semi-Markov CRF: (log Z [B], segment marginals [B, N-1, K, C, C]) in float64, for
+    segment potentials sp [B, N-1, K, C, C]: sp[b, t, k-1, i, j] scores a segment of length
+    k starting at step t with label j after a segment labelled i."""
+    sp, lengths, f64, B, N, K, C = _prep_semi(sp, lengths)
+    logz = np.empty(B, np.float64)
+    marg = np.empty((B, N - 1, K, C, C), np.float64)
+    fn = _load(lib).orc_semi_marginals_f64 if f64 else _load(lib).orc_semi_marginals
+    _check(fn(_ptr(sp), _ptr(lengths), B, N, K, C, _ptr(logz), _ptr(marg)))
+    return logz, marg
+
+
+def semi_logpartition(sp, lengths=None, lib=None):
+    """Semi-Markov CRF log Z [B] (float64)."""
+    sp, lengths, f64, B, N, K, C = _prep_semi(sp, lengths)
+    logz = np.empty(B, np.float64)
+    fn = _load(lib).orc_semi_marginals_f64 if f64 else _load(lib).orc_semi_marginals
+    _check(fn(_ptr(sp), _ptr(lengths), B, N, K, C, _ptr(logz), None))
+    return logz
+
+
+def semi_viterbi(sp, lengths=None, lib=None):
+    """Semi-Markov CRF best segmentation: (path int32 [B, N] -- path[0] the free initial
+    label, path[t+1] the label of the segment covering step t; seglen int32 [B, N-1] -- the
+    length of the segment starting at step t, else 0; both -1 past each sequence; score
+    float64 [B])."""
+    sp, lengths, f64, B, N, K, C = _prep_semi(sp, lengths)
+    if f64:
+        raise ValueError("semi_viterbi takes fp32 potentials")
+    path = np.empty((B, N), np.int32)
+    seglen = np.empty((B, N - 1), np.int32)
+    score = np.empty(B, np.float64)
+    _check(_load(lib).orc_semi_viterbi(_ptr(sp), _ptr(lengths), B, N, K, C, _ptr(path),
+                                       _ptr(seglen), _ptr(score)))
+    return path, seglen, score

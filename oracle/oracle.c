@@ -21,7 +21,9 @@
  *     quantity of Table 2's "Entropy" semiring), from the edge marginals by the chain
  *     rule, and the log-probability log p(z) of a given label sequence (Sec. 5.1);
  *   - samples from p(z) by forward filtering, backward sampling with caller-supplied
- *     uniforms (Table 2's "Sample" semiring draws from the same distribution).
+ *     uniforms (Table 2's "Sample" semiring draws from the same distribution);
+ *   - the semi-Markov CRF of Table 1 (segment labels, parts N K C^2): log Z, segment
+ *     marginals and the best segmentation by the segmental forward-backward recursion.
  *
  * Conventions (the paper leaves these open; the readings are listed in the design notes):
  *   - pot is [B, N-1, C, C] row-major: pot[((b*(N-1)+t)*C+i)*C+j] = l[b, t, i, j].
@@ -380,6 +382,150 @@ static int sample_impl(const float* pf, const int32_t* lengths, const float* uni
     return rc;
 }
 
+/*
+ * Semi-Markov CRF (Table 1, "Semi-Markov": segment labels, parts N K C^2, segmental
+ * forward-backward).  A sequence of L tokens has E = L-1 steps t = 0..E-1 (the chain's
+ * edges).  A segmentation covers the steps with consecutive segments of lengths 1..K;
+ * segment m spans steps [s_m, s_m + k_m) and carries label y_m, and y_0 is a free initial
+ * label (the chain's z_0).  Its score is sum_m sp[s_m, k_m - 1, y_{m-1}, y_m] with
+ * sp [B, N-1, K, C, C].  With K = 1 this is the linear chain exactly.
+ *   alpha_0(i) = 0,  alpha_e(j) = LSE over k <= min(K, e), i of alpha_{e-k}(i) + sp[e-k, k-1, i, j],
+ *   A = LSE_j alpha_E(j)  (E = 0: log C),
+ *   beta_E(j) = 0,   beta_e(i) = LSE over k <= min(K, E-e), j of sp[e, k-1, i, j] + beta_{e+k}(j),
+ *   mu[e, k-1, i, j] = exp(alpha_e(i) + sp[e, k-1, i, j] + beta_{e+k}(j) - A)  (dA/dsp, Sec.
+ *   5.1), and 0 where e + k > E.
+ * Viterbi: V the same recursion in (max, +); the last label is the lowest j maximising
+ * V_E(j); going back from a segment end e with label j it takes, among the (k, i) with
+ * V_{e-k}(i) + sp[e-k, k-1, i, j] = V_e(j), the smallest k and then the lowest i.
+ * Outputs path[n] for n < L: path[0] = y_0 and path[t+1] = the label of the segment that
+ * covers step t; seglen[t] = k where a segment of length k starts at step t, else 0; both
+ * -1 past the sequence.
+ */
+static inline double sp_at(const float* pf, const double* pd, int64_t N, int64_t K, int64_t C,
+                           int64_t b, int64_t t, int64_t k, int64_t i, int64_t j) {
+    int64_t idx = (((b * (N - 1) + t) * K + k) * C + i) * C + j;
+    return pd ? pd[idx] : (double)pf[idx];
+}
+
+/* alpha [E+1, C] and beta [E+1, C] of one sequence with E steps; tmp [K*C].  Returns A. */
+static double semi_fwd_bwd(const float* pf, const double* pd, int64_t N, int64_t K, int64_t C,
+                           int64_t b, int64_t E, double* alpha, double* beta, double* tmp) {
+    for (int64_t i = 0; i < C; ++i) alpha[i] = 0.0;
+    for (int64_t e = 1; e <= E; ++e)
+        for (int64_t j = 0; j < C; ++j) {
+            int64_t n = 0;
+            for (int64_t k = 1; k <= K && k <= e; ++k)
+                for (int64_t i = 0; i < C; ++i)
+                    tmp[n++] = alpha[(e - k) * C + i] + sp_at(pf, pd, N, K, C, b, e - k, k - 1, i, j);
+            alpha[e * C + j] = lse(tmp, n);
+        }
+    for (int64_t j = 0; j < C; ++j) beta[E * C + j] = 0.0;
+    for (int64_t e = E - 1; e >= 0; --e)
+        for (int64_t i = 0; i < C; ++i) {
+            int64_t n = 0;
+            for (int64_t k = 1; k <= K && e + k <= E; ++k)
+                for (int64_t j = 0; j < C; ++j)
+                    tmp[n++] = sp_at(pf, pd, N, K, C, b, e, k - 1, i, j) + beta[(e + k) * C + j];
+            beta[e * C + i] = lse(tmp, n);
+        }
+    return E == 0 ? log((double)C) : lse(alpha + E * C, C);
+}
+
+static int semi_marginals_impl(const float* pf, const double* pd, const int32_t* lengths,
+                               int64_t B, int64_t N, int64_t K, int64_t C, double* logZ,
+                               double* marg) {
+    int rc = check_args(pf, pd, lengths, B, N, C);
+    if (rc || K < 1) return rc ? rc : ORC_ERR_ARG;
+    int err = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        const int64_t E = (lengths ? lengths[b] : N) - 1;
+        double* alpha = malloc(sizeof(double) * (E + 1) * C);
+        double* beta = malloc(sizeof(double) * (E + 1) * C);
+        double* tmp = malloc(sizeof(double) * K * C);
+        if (!alpha || !beta || !tmp) {
+#pragma omp atomic write
+            err = 1;
+            free(alpha); free(beta); free(tmp);
+            continue;
+        }
+        const double A = semi_fwd_bwd(pf, pd, N, K, C, b, E, alpha, beta, tmp);
+        logZ[b] = A;
+        if (marg)
+            for (int64_t e = 0; e < N - 1; ++e)
+                for (int64_t k = 1; k <= K; ++k)
+                    for (int64_t i = 0; i < C; ++i)
+                        for (int64_t j = 0; j < C; ++j) {
+                            double v = 0.0;
+                            if (e + k <= E && A != -INFINITY)
+                                v = exp(alpha[e * C + i] + sp_at(pf, pd, N, K, C, b, e, k - 1, i, j)
+                                        + beta[(e + k) * C + j] - A);
+                            marg[((((b * (N - 1) + e) * K) + k - 1) * C + i) * C + j] = v;
+                        }
+        free(alpha); free(beta); free(tmp);
+    }
+    return err ? ORC_ERR_MEM : ORC_OK;
+}
+
+static int semi_viterbi_impl(const float* pf, const double* pd, const int32_t* lengths,
+                             int64_t B, int64_t N, int64_t K, int64_t C, int32_t* path,
+                             int32_t* seglen, double* score) {
+    int rc = check_args(pf, pd, lengths, B, N, C);
+    if (rc || K < 1) return rc ? rc : ORC_ERR_ARG;
+    int err = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        const int64_t E = (lengths ? lengths[b] : N) - 1;
+        double* V = malloc(sizeof(double) * (E + 1) * C);
+        if (!V) {
+#pragma omp atomic write
+            err = 1;
+            continue;
+        }
+        for (int64_t i = 0; i < C; ++i) V[i] = 0.0;
+        for (int64_t e = 1; e <= E; ++e)
+            for (int64_t j = 0; j < C; ++j) {
+                double best = -INFINITY;
+                for (int64_t k = 1; k <= K && k <= e; ++k)
+                    for (int64_t i = 0; i < C; ++i) {
+                        double v = V[(e - k) * C + i] + sp_at(pf, pd, N, K, C, b, e - k, k - 1, i, j);
+                        if (v > best) best = v;
+                    }
+                V[e * C + j] = best;
+            }
+        int32_t j = 0;
+        for (int64_t c = 1; c < C; ++c)
+            if (V[E * C + c] > V[E * C + j]) j = (int32_t)c;
+        score[b] = V[E * C + j];
+        int32_t* p = path + b * N;
+        int32_t* g = seglen + b * (N - 1);
+        for (int64_t n = E + 1; n < N; ++n) p[n] = -1;
+        for (int64_t t = 0; t < N - 1; ++t) g[t] = t < E ? 0 : -1;
+        /* walk back over the segments: the smallest k, then the lowest i, that attains V */
+        int64_t e = E;
+        while (e > 0) {
+            int64_t kb = 1;
+            int32_t ib = 0;
+            int found = 0;
+            for (int64_t k = 1; k <= K && k <= e && !found; ++k)
+                for (int64_t i = 0; i < C && !found; ++i)
+                    if (V[(e - k) * C + i] + sp_at(pf, pd, N, K, C, b, e - k, k - 1, i, j) ==
+                        V[e * C + j]) {
+                        kb = k;
+                        ib = (int32_t)i;
+                        found = 1;
+                    }
+            for (int64_t t = e - kb; t < e; ++t) p[t + 1] = j;
+            g[e - kb] = (int32_t)kb;
+            j = ib;
+            e -= kb;
+        }
+        p[0] = j;
+        free(V);
+    }
+    return err ? ORC_ERR_MEM : ORC_OK;
+}
+
 /* ---------------- exported entry points ---------------- */
 
 /* OpenMP threads a parallel region of the oracle may use */
@@ -454,4 +600,18 @@ int orc_marginals_seq(const float* pot, const int32_t* lengths, int64_t B, int64
     }
     free(alpha); free(beta); free(tmp);
     return ORC_OK;
+}
+
+/* semi-Markov CRF: sp [B, N-1, K, C, C] (fp32 widened exactly, or float64) */
+int orc_semi_marginals(const float* sp, const int32_t* lengths, int64_t B, int64_t N, int64_t K,
+                       int64_t C, double* logZ, double* marg) {
+    return semi_marginals_impl(sp, NULL, lengths, B, N, K, C, logZ, marg);
+}
+int orc_semi_marginals_f64(const double* sp, const int32_t* lengths, int64_t B, int64_t N,
+                           int64_t K, int64_t C, double* logZ, double* marg) {
+    return semi_marginals_impl(NULL, sp, lengths, B, N, K, C, logZ, marg);
+}
+int orc_semi_viterbi(const float* sp, const int32_t* lengths, int64_t B, int64_t N, int64_t K,
+                     int64_t C, int32_t* path, int32_t* seglen, double* score) {
+    return semi_viterbi_impl(sp, NULL, lengths, B, N, K, C, path, seglen, score);
 }

@@ -92,3 +92,76 @@ def brute_log_density(pot, lengths, labels):
         z = labels[b]
         out[b] = sum(float(pot[b, t, z[t], z[t + 1]]) for t in range(L - 1)) - lz
     return out
+
+
+def compositions(E, K):
+    """All ordered tuples of segment lengths in 1..K that sum to E."""
+    if E == 0:
+        yield ()
+        return
+    for k in range(1, min(K, E) + 1):
+        for rest in compositions(E - k, K):
+            yield (k,) + rest
+
+
+def enumerate_segmentations(sp_b, E, K, C):
+    """All labelled segmentations of E steps for one sequence, sp_b [N-1, K, C, C]: a list
+    of (starts, lengths, labels y_0..y_m, score) with score = sum_m sp[s_m, k_m-1, y_{m-1}, y_m]
+    (Table 1's semi-Markov parts: a segment's potential depends on its start, its length,
+    its label and the previous segment's label; y_0 is a free initial label)."""
+    out = []
+    for ks in compositions(E, K):
+        starts = [sum(ks[:m]) for m in range(len(ks))]
+        for ys in itertools.product(range(C), repeat=len(ks) + 1):
+            s = 0.0
+            for m, (t, k) in enumerate(zip(starts, ks)):
+                s += float(sp_b[t, k - 1, ys[m], ys[m + 1]])
+            out.append((starts, ks, ys, s))
+    return out
+
+
+def brute_semi(sp, lengths):
+    """Semi-Markov CRF by enumeration -> logZ [B], mu [B, N-1, K, C, C], score [B],
+    path [B, N], seglen [B, N-1].  The canonical argmax is the max-score segmentation that
+    is smallest under the key (y_m, k_m, y_{m-1}, k_{m-1}, ..., k_1, y_0): the one a
+    backtrace produces that always takes the last label lowest, then the shortest last
+    segment, then the lowest previous label."""
+    sp = np.asarray(sp, dtype=np.float64)
+    B, E1, K, C, _ = sp.shape
+    N = E1 + 1
+    logZ = np.zeros(B)
+    mu = np.zeros((B, E1, K, C, C))
+    score = np.zeros(B)
+    path = np.full((B, N), -1, np.int32)
+    seglen = np.full((B, E1), -1, np.int32)
+    for b in range(B):
+        E = int(lengths[b]) - 1
+        segs = enumerate_segmentations(sp[b], E, K, C)
+        scores = [s for *_, s in segs]
+        m = max(scores)
+        if E == 0:
+            logZ[b] = math.log(C)
+        elif m == -math.inf:
+            logZ[b] = -math.inf
+        else:
+            logZ[b] = m + math.log(sum(math.exp(s - m) for s in scores))
+            for starts, ks, ys, s in segs:
+                p = math.exp(s - logZ[b])
+                for mm, (t, k) in enumerate(zip(starts, ks)):
+                    mu[b, t, k - 1, ys[mm], ys[mm + 1]] += p
+        score[b] = m
+
+        def key(seg):
+            starts, ks, ys, _ = seg
+            out = []
+            for mm in range(len(ks), 0, -1):
+                out += [ys[mm], ks[mm - 1]]
+            return tuple(out + [ys[0]])
+
+        starts, ks, ys, _ = min((g for g in segs if g[3] == m), key=key)
+        path[b, 0] = ys[0]
+        seglen[b, :E] = 0
+        for mm, (t, k) in enumerate(zip(starts, ks)):
+            path[b, t + 1:t + k + 1] = ys[mm + 1]
+            seglen[b, t] = k
+    return logZ, mu, score, path, seglen
