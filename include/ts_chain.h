@@ -176,6 +176,47 @@ ts_status ts_chain_logpartition_sequential(const float* pot, const int32_t* leng
                                            int64_t N, int64_t C, float* logZ, void* stream);
 
 /* Message for the last non-OK status returned to the calling thread ("" if none). */
+/*
+ * Semi-Markov CRF (Table 1, "Semi-Markov": segment labels, parts N K C^2; Sec. 6a carries
+ * the parallel scan over to it).  A sequence of L tokens has L-1 steps (the chain's edges),
+ * covered by consecutive segments of lengths 1..K, each with a label; the first segment
+ * follows a free initial label.
+ *   sp       device float32 [B, N-1, K, C, C]: sp[(((b*(N-1) + t)*K + k-1)*C + i)*C + j]
+ *            scores a segment of length k that starts at step t with label j after a
+ *            segment labelled i.  Entries with t + k > L-1 are never used.
+ *   K        maximum segment length, K >= 1 and K * C <= ts_chain_max_labels().
+ *   lengths, B, N, C, ws, stream as above; ws is sized by ts_semimarkov_workspace_bytes.
+ * The call runs the linear-chain scan over K*C expanded states (the label of the segment
+ * in progress and the steps it has left), whose edges it builds in the workspace.
+ * With K = 1 every result equals the linear chain's on sp[:, :, 0].
+ */
+size_t ts_semimarkov_workspace_bytes(int op /* TS_OP_LOGPARTITION, _MARGINALS or _VITERBI */,
+                                     int64_t B, int64_t N, int64_t K, int64_t C);
+
+/* log Z [B] (float32); one token gives log C.  Segmental forward algorithm. */
+ts_status ts_semimarkov_logpartition(const float* sp, const int32_t* lengths, int64_t B,
+                                     int64_t N, int64_t K, int64_t C, float* logZ, void* ws,
+                                     size_t ws_bytes, void* stream);
+
+/* Segment marginals marg [B, N-1, K, C, C] = dA/dsp (Sec. 5.1): the probability that a
+ * segment of length k starts at step t with label j after label i; 0 for padding and for
+ * segments that would overrun the sequence.  logZ [B] is optional (NULL skips it). */
+ts_status ts_semimarkov_marginals(const float* sp, const int32_t* lengths, int64_t B,
+                                  int64_t N, int64_t K, int64_t C, float* logZ, float* marg,
+                                  void* ws, size_t ws_bytes, void* stream);
+
+/* Best segmentation (Table 2 "Max" semiring):
+ *   path   int32 [B, N]: path[b, 0] is the initial label, path[b, t+1] the label of the
+ *          segment covering step t; -1 past the sequence;
+ *   seglen int32 [B, N-1]: k where a segment of length k starts at step t, else 0; -1 past
+ *          the last step (may be NULL when N == 1);
+ *   score  float32 [B]: its score, accumulated in float64.
+ * Ties: the lowest last label, then at every segment end (going back) the shortest segment,
+ * then the lowest previous label. */
+ts_status ts_semimarkov_viterbi(const float* sp, const int32_t* lengths, int64_t B, int64_t N,
+                                int64_t K, int64_t C, int32_t* path, int32_t* seglen,
+                                float* score, void* ws, size_t ws_bytes, void* stream);
+
 const char* ts_last_error(void);
 
 #ifdef __cplusplus

@@ -43,9 +43,16 @@ def lib():
         L.ts_chain_log_density.argtypes = [p, p, p, i64, i64, i64, p, p, sz, p]
         L.ts_chain_logpartition_sequential.argtypes = [p, p, i64, i64, i64, p, p]
         L.ts_chain_sample.argtypes = [p, p, p, i64, i64, i64, i64, p, p, sz, p]
+        L.ts_semimarkov_workspace_bytes.argtypes = [ctypes.c_int, i64, i64, i64, i64]
+        L.ts_semimarkov_workspace_bytes.restype = sz
+        L.ts_semimarkov_logpartition.argtypes = [p, p, i64, i64, i64, i64, p, p, sz, p]
+        L.ts_semimarkov_marginals.argtypes = [p, p, i64, i64, i64, i64, p, p, p, sz, p]
+        L.ts_semimarkov_viterbi.argtypes = [p, p, i64, i64, i64, i64, p, p, p, p, sz, p]
         for f in ("ts_chain_logpartition", "ts_chain_marginals", "ts_chain_viterbi",
                   "ts_chain_marginals_viterbi", "ts_chain_entropy", "ts_chain_log_density",
-                  "ts_chain_logpartition_sequential", "ts_chain_sample"):
+                  "ts_chain_logpartition_sequential", "ts_chain_sample",
+                  "ts_semimarkov_logpartition", "ts_semimarkov_marginals",
+                  "ts_semimarkov_viterbi"):
             getattr(L, f).restype = ctypes.c_int
         L.ts_last_error.restype = ctypes.c_char_p
         _lib = L
@@ -196,3 +203,75 @@ def sample(pot, uniforms, lengths=None, out=None, ws=None):
     _check(lib().ts_chain_sample(_ptr(pot), _ptr(lengths), _ptr(uniforms), S, B, N, C,
                                  _ptr(paths), _ptr(w), nb, _stream(pot.device)))
     return paths
+
+
+# ---- semi-Markov CRF: segment potentials sp [B, N-1, K, C, C] ----
+
+def _prep_semi(sp, lengths):
+    if not sp.is_cuda:
+        raise ValueError("sp must be a device tensor")
+    if sp.dtype != torch.float32 or sp.dim() != 5 or sp.shape[3] != sp.shape[4]:
+        raise ValueError("sp must be float32 [B, N-1, K, C, C]")
+    sp = sp.contiguous()
+    B, E, K, C, _ = sp.shape
+    if lengths is not None:
+        if lengths.device != sp.device or lengths.dtype != torch.int32 or lengths.shape != (B,):
+            raise ValueError("lengths must be int32 [B] on the same device as sp")
+        lengths = lengths.contiguous()
+    return sp, lengths, B, E + 1, K, C
+
+
+def semi_workspace_bytes(op, B, N, K, C):
+    return lib().ts_semimarkov_workspace_bytes(op, B, N, K, C)
+
+
+def _semi_workspace(op, B, N, K, C, device, ws=None):
+    if ws is not None:
+        return ws, ws.numel() * ws.element_size()
+    need = semi_workspace_bytes(op, B, N, K, C)
+    if need == 0:
+        return None, 0
+    return torch.empty(need, dtype=torch.uint8, device=device), need
+
+
+def semi_logpartition(sp, lengths=None, out=None, ws=None):
+    """Semi-Markov log Z [B] (float32)."""
+    sp, lengths, B, N, K, C = _prep_semi(sp, lengths)
+    logz = out if out is not None else torch.empty(B, dtype=torch.float32, device=sp.device)
+    w, nb = _semi_workspace(OP_LOGPARTITION, B, N, K, C, sp.device, ws)
+    _check(lib().ts_semimarkov_logpartition(_ptr(sp), _ptr(lengths), B, N, K, C, _ptr(logz),
+                                            _ptr(w), nb, _stream(sp.device)))
+    return logz
+
+
+def semi_marginals(sp, lengths=None, out=None, ws=None, want_logz=True):
+    """Semi-Markov (log Z [B] or None, segment marginals [B, N-1, K, C, C]), float32."""
+    sp, lengths, B, N, K, C = _prep_semi(sp, lengths)
+    if out is not None:
+        logz, marg = out
+    else:
+        logz = torch.empty(B, dtype=torch.float32, device=sp.device) if want_logz else None
+        marg = torch.empty_like(sp)
+    w, nb = _semi_workspace(OP_MARGINALS, B, N, K, C, sp.device, ws)
+    _check(lib().ts_semimarkov_marginals(_ptr(sp), _ptr(lengths), B, N, K, C, _ptr(logz),
+                                         _ptr(marg) if N > 1 else None, _ptr(w), nb,
+                                         _stream(sp.device)))
+    return logz, marg
+
+
+def semi_viterbi(sp, lengths=None, out=None, ws=None):
+    """Semi-Markov best segmentation: (path int32 [B, N], seglen int32 [B, N-1],
+    score float32 [B])."""
+    sp, lengths, B, N, K, C = _prep_semi(sp, lengths)
+    if out is not None:
+        path, seglen, score = out
+    else:
+        dev = sp.device
+        path = torch.empty((B, N), dtype=torch.int32, device=dev)
+        seglen = torch.empty((B, N - 1), dtype=torch.int32, device=dev)
+        score = torch.empty(B, dtype=torch.float32, device=dev)
+    w, nb = _semi_workspace(OP_VITERBI, B, N, K, C, sp.device, ws)
+    _check(lib().ts_semimarkov_viterbi(_ptr(sp), _ptr(lengths), B, N, K, C, _ptr(path),
+                                       _ptr(seglen) if N > 1 else None, _ptr(score), _ptr(w),
+                                       nb, _stream(sp.device)))
+    return path, seglen, score

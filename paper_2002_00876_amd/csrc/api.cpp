@@ -208,6 +208,38 @@ ts_status hip_status(hipError_t e) {
     return fail(TS_ERR_HIP, std::string("HIP error: ") + hipGetErrorString(e));
 }
 
+// Workspace of a semi-Markov call: the expanded edges [B, N-1, KC, KC], the expanded
+// marginals (marginals) or path [B, N] (Viterbi), then the chain plan over KC labels.
+struct SemiPlan {
+    int64_t KC = 0;
+    size_t xpot = 0, xout = 0, chain = 0, total = 0;
+    Plan base;
+};
+
+// Sizes only; returns the reason when the dimensions are out of range, else nullptr.
+const char* plan_semi(int op, int64_t B, int64_t N, int64_t K, int64_t C, SemiPlan* q) {
+    if (B < 1 || N < 1 || K < 1 || C < 1) return "B, N, K and C must all be >= 1";
+    if (K > kMaxLabels || K * C > kMaxLabels) return "K * C exceeds ts_chain_max_labels()";
+    q->KC = K * C;
+    if (N == 1) return nullptr;   // one token per sequence: no edges, no workspace
+    if (!make_plan(op, B, N, q->KC, nullptr, &q->base))
+        return "problem size overflows the supported range";
+    const size_t x = align_up(sizeof(float) * B * (N - 1) * q->KC * q->KC);
+    q->xpot = 0;
+    q->xout = x;
+    q->chain = x + (op == TS_OP_MARGINALS ? x
+                    : op == TS_OP_VITERBI ? align_up(sizeof(int32_t) * B * N) : 0);
+    q->total = q->chain + q->base.bytes;
+    return nullptr;
+}
+
+ts_status check_semi(const float* sp, int op, int64_t B, int64_t N, int64_t K, int64_t C,
+                     void* ws, size_t ws_bytes, SemiPlan* q) {
+    if (const char* why = plan_semi(op, B, N, K, C, q)) return fail(TS_ERR_BAD_DIM, why);
+    if (N > 1 && !sp) return fail(TS_ERR_NULL_ARG, "sp is NULL");
+    return check_ws(q->total, ws, ws_bytes);
+}
+
 }  // namespace
 }  // namespace tsc
 
@@ -414,6 +446,79 @@ ts_status ts_chain_logpartition_sequential(const float* pot, const int32_t* leng
     hipStream_t s = static_cast<hipStream_t>(stream);
     if ((st = check_lengths(lengths, B, N, s)) != TS_OK) return st;
     return hip_status(launch_logz_sequential(pot, lengths, B, N, C, logZ, s));
+}
+
+size_t ts_semimarkov_workspace_bytes(int op, int64_t B, int64_t N, int64_t K, int64_t C) {
+    if (op < TS_OP_LOGPARTITION || op > TS_OP_VITERBI) return 0;
+    SemiPlan q;
+    return plan_semi(op, B, N, K, C, &q) ? 0 : q.total;
+}
+
+ts_status ts_semimarkov_logpartition(const float* sp, const int32_t* lengths, int64_t B,
+                                     int64_t N, int64_t K, int64_t C, float* logZ, void* ws,
+                                     size_t ws_bytes, void* stream) {
+    SemiPlan q;
+    ts_status st = check_semi(sp, TS_OP_LOGPARTITION, B, N, K, C, ws, ws_bytes, &q);
+    if (st != TS_OK) return st;
+    if (!logZ) return fail(TS_ERR_NULL_ARG, "logZ is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = check_lengths(lengths, B, N, s)) != TS_OK) return st;
+    if (N == 1) return hip_status(launch_single_token(B, N, C, TS_OP_LOGPARTITION, logZ,
+                                                      nullptr, nullptr, s));
+    char* w = static_cast<char*>(ws);
+    float* xp = reinterpret_cast<float*>(w + q.xpot);
+    if ((st = hip_status(launch_semi_expand(sp, lengths, B, N, K, C, xp, s))) != TS_OK) return st;
+    st = ts_chain_logpartition(xp, lengths, B, N, q.KC, logZ, q.base.bytes ? w + q.chain : nullptr,
+                               q.base.bytes, stream);
+    if (st != TS_OK) return st;
+    return hip_status(launch_semi_single(lengths, B, N, C, logZ, s));
+}
+
+ts_status ts_semimarkov_marginals(const float* sp, const int32_t* lengths, int64_t B,
+                                  int64_t N, int64_t K, int64_t C, float* logZ, float* marg,
+                                  void* ws, size_t ws_bytes, void* stream) {
+    SemiPlan q;
+    ts_status st = check_semi(sp, TS_OP_MARGINALS, B, N, K, C, ws, ws_bytes, &q);
+    if (st != TS_OK) return st;
+    if (N > 1 && !marg) return fail(TS_ERR_NULL_ARG, "marg is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = check_lengths(lengths, B, N, s)) != TS_OK) return st;
+    if (N == 1) {
+        if (!logZ) return TS_OK;
+        return hip_status(launch_single_token(B, N, C, TS_OP_LOGPARTITION, logZ, nullptr,
+                                              nullptr, s));
+    }
+    char* w = static_cast<char*>(ws);
+    float* xp = reinterpret_cast<float*>(w + q.xpot);
+    float* xm = reinterpret_cast<float*>(w + q.xout);
+    if ((st = hip_status(launch_semi_expand(sp, lengths, B, N, K, C, xp, s))) != TS_OK) return st;
+    st = ts_chain_marginals(xp, lengths, B, N, q.KC, logZ, xm,
+                            q.base.bytes ? w + q.chain : nullptr, q.base.bytes, stream);
+    if (st != TS_OK) return st;
+    if ((st = hip_status(launch_semi_gather(xm, B, N, K, C, marg, s))) != TS_OK) return st;
+    return logZ ? hip_status(launch_semi_single(lengths, B, N, C, logZ, s)) : TS_OK;
+}
+
+ts_status ts_semimarkov_viterbi(const float* sp, const int32_t* lengths, int64_t B, int64_t N,
+                                int64_t K, int64_t C, int32_t* path, int32_t* seglen,
+                                float* score, void* ws, size_t ws_bytes, void* stream) {
+    SemiPlan q;
+    ts_status st = check_semi(sp, TS_OP_VITERBI, B, N, K, C, ws, ws_bytes, &q);
+    if (st != TS_OK) return st;
+    if (!path || !score || (N > 1 && !seglen))
+        return fail(TS_ERR_NULL_ARG, "path, seglen or score is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = check_lengths(lengths, B, N, s)) != TS_OK) return st;
+    if (N == 1)
+        return hip_status(launch_single_token(B, N, C, TS_OP_VITERBI, nullptr, path, score, s));
+    char* w = static_cast<char*>(ws);
+    float* xp = reinterpret_cast<float*>(w + q.xpot);
+    int32_t* xs = reinterpret_cast<int32_t*>(w + q.xout);
+    if ((st = hip_status(launch_semi_expand(sp, lengths, B, N, K, C, xp, s))) != TS_OK) return st;
+    st = ts_chain_viterbi(xp, lengths, B, N, q.KC, xs, score, q.base.bytes ? w + q.chain : nullptr,
+                          q.base.bytes, stream);
+    if (st != TS_OK) return st;
+    return hip_status(launch_semi_decode(xs, lengths, B, N, C, path, seglen, s));
 }
 
 const char* ts_last_error(void) { return g_err.c_str(); }

@@ -75,6 +75,17 @@ hipError_t launch_entropy(const float* mu, const int32_t* lengths, int64_t B, in
 hipError_t launch_sample(const float* mu, const int32_t* lengths, const float* uniforms,
                          int64_t S, int64_t B, int64_t N, int64_t C, int32_t* paths,
                          hipStream_t s);
+// semi-Markov CRF: expand segment potentials [B, N-1, K, C, C] into chain edges over K*C
+// states [B, N-1, KC, KC]; gather the segment marginals back; fix one-token log Z; decode
+// the expanded Viterbi path into labels [B, N] and segment lengths [B, N-1]
+hipError_t launch_semi_expand(const float* sp, const int32_t* lengths, int64_t B, int64_t N,
+                              int64_t K, int64_t C, float* xp, hipStream_t s);
+hipError_t launch_semi_gather(const float* xm, int64_t B, int64_t N, int64_t K, int64_t C,
+                              float* marg, hipStream_t s);
+hipError_t launch_semi_single(const int32_t* lengths, int64_t B, int64_t N, int64_t C,
+                              float* logZ, hipStream_t s);
+hipError_t launch_semi_decode(const int32_t* xs, const int32_t* lengths, int64_t B, int64_t N,
+                              int64_t C, int32_t* path, int32_t* seglen, hipStream_t s);
 hipError_t launch_logz_sequential(const float* pot, const int32_t* lengths, int64_t B,
                                   int64_t N, int64_t C, float* logZ, hipStream_t s);
 hipError_t launch_log_density(const float* pot, const int32_t* lengths, const int32_t* labels,

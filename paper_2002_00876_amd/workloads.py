@@ -133,3 +133,39 @@ def random_case(seed, B, N, C, kind="normal", sigma=1.0, lengths="random", int_r
     else:
         lens = np.asarray(lengths)
     return pot, lens.astype(np.int32)
+
+
+# Semi-Markov CRF: segment potentials sp [B, N-1, K, C, C] (Table 1's timing shape for the
+# semi-Markov row: batch 32, N=25, C=20, K=5).  Same recipe: potentials first, one sequence
+# at a time (rng.standard_normal((N-1, K, C, C))), scaled by sigma in float64 and cast to
+# float32 once, then lengths.
+SEMI_WORKLOADS = {
+    "semi": dict(B=32, N=25, K=5, C=20, seed=6, len_range=(13, 25)),
+    "semi_long": dict(B=8, N=1024, K=8, C=32, seed=7, len_range=(512, 1024)),
+}
+
+
+def semi_case(seed, B, N, K, C, sigma=1.0, len_range=None, kind="normal", int_range=1,
+              neg_inf_frac=0.0):
+    """Seeded semi-Markov segment potentials [B, N-1, K, C, C] (float32) and lengths [B].
+    kind "int" draws integers in [-int_range, int_range] (exact ties); len_range None gives
+    lengths uniform in [1, N]."""
+    rng = np.random.default_rng(seed)
+    shape = (N - 1, K, C, C)
+    if kind == "normal":
+        sp = np.stack([rng.standard_normal(shape) * sigma for _ in range(B)])
+    elif kind == "int":
+        sp = np.stack([rng.integers(-int_range, int_range, endpoint=True, size=shape)
+                       for _ in range(B)]).astype(np.float64)
+    else:
+        raise ValueError(kind)
+    if neg_inf_frac > 0:
+        sp[rng.random(sp.shape) < neg_inf_frac] = -np.inf
+    lo, hi = len_range if len_range is not None else (1, N)
+    lengths = rng.integers(lo, hi, endpoint=True, size=B).astype(np.int32)
+    return sp.astype(np.float32), lengths
+
+
+def generate_semi(name):
+    w = SEMI_WORKLOADS[name]
+    return semi_case(w["seed"], w["B"], w["N"], w["K"], w["C"], len_range=w["len_range"])

@@ -155,3 +155,49 @@ def test_small_or_misaligned_workspace_is_rejected(L):
         assert "workspace too small" in _err(L)
         assert f(FAKE, None, 4, 9, CW, *args, FAKE + 16, need, None) == WORKSPACE
         assert "aligned" in _err(L)
+
+
+def test_semimarkov_workspace_sizes(L):
+    sw = binding.semi_workspace_bytes
+    # expanded edges [B, N-1, KC, KC] come first, then the chain plan over K*C labels
+    B, N, K, C = 32, 25, 5, 20
+    x = B * (N - 1) * (K * C) ** 2 * 4
+    assert sw(0, B, N, K, C) >= x + binding.workspace_bytes(0, B, N, K * C)
+    assert sw(1, B, N, K, C) >= 2 * x + binding.workspace_bytes(1, B, N, K * C)
+    assert sw(2, B, N, K, C) >= x + B * N * 4 + binding.workspace_bytes(2, B, N, K * C)
+    assert all(sw(op, B, N, K, C) % 256 == 0 for op in (0, 1, 2))
+    # small expanded label sets keep the chain on its single-launch path
+    assert sw(0, B, N, 2, 8) == B * (N - 1) * 16 * 16 * 4
+    assert sw(0, 4, 1, 5, 20) == 0                    # one token: no edges
+    assert sw(3, B, N, K, C) == 0 and sw(0, B, N, 0, C) == 0
+    assert sw(0, B, N, 13, 20) == 0                   # K * C = 260 > 256
+
+
+def test_semimarkov_bad_arguments_are_rejected(L):
+    for B, N, K, C in [(0, 5, 2, 3), (2, 0, 2, 3), (2, 5, 0, 3), (2, 5, 2, 0), (2, 5, 13, 20)]:
+        assert L.ts_semimarkov_logpartition(FAKE, None, B, N, K, C, FAKE, FAKE, 1 << 30,
+                                            None) == BAD_DIM
+        assert L.ts_semimarkov_marginals(FAKE, None, B, N, K, C, FAKE, FAKE, FAKE, 1 << 30,
+                                         None) == BAD_DIM
+        assert L.ts_semimarkov_viterbi(FAKE, None, B, N, K, C, FAKE, FAKE, FAKE, FAKE, 1 << 30,
+                                       None) == BAD_DIM
+    B, N, K, C = 2, 5, 3, 20
+    need = binding.semi_workspace_bytes(0, B, N, K, C)
+    assert L.ts_semimarkov_logpartition(None, None, B, N, K, C, FAKE, FAKE, need, None) == NULL_ARG
+    assert "sp" in _err(L)
+    assert L.ts_semimarkov_logpartition(FAKE, None, B, N, K, C, None, FAKE, need, None) == NULL_ARG
+    assert L.ts_semimarkov_logpartition(FAKE, None, B, N, K, C, FAKE, FAKE, need - 1,
+                                        None) == WORKSPACE
+    assert L.ts_semimarkov_logpartition(FAKE, None, B, N, K, C, FAKE, FAKE + 16, need,
+                                        None) == WORKSPACE
+    need = binding.semi_workspace_bytes(1, B, N, K, C)
+    assert L.ts_semimarkov_marginals(FAKE, None, B, N, K, C, FAKE, None, FAKE, need,
+                                     None) == NULL_ARG
+    assert L.ts_semimarkov_marginals(FAKE, None, B, N, K, C, FAKE, FAKE, None, need,
+                                     None) == NULL_ARG
+    need = binding.semi_workspace_bytes(2, B, N, K, C)
+    vit = L.ts_semimarkov_viterbi
+    assert vit(FAKE, None, B, N, K, C, None, FAKE, FAKE, FAKE, need, None) == NULL_ARG
+    assert vit(FAKE, None, B, N, K, C, FAKE, None, FAKE, FAKE, need, None) == NULL_ARG
+    assert vit(FAKE, None, B, N, K, C, FAKE, FAKE, None, FAKE, need, None) == NULL_ARG
+    assert vit(FAKE, None, B, N, K, C, FAKE, FAKE, FAKE, FAKE, need - 1, None) == WORKSPACE
