@@ -49,6 +49,10 @@ def parse():
                     help="instead of the step: time each entry point separately on the "
                          "workload (log Z by the scan and left to right, marginals, entropy, "
                          "log-density, sampling); one JSON line per entry point")
+    ap.add_argument("--semi", choices=["semi", "semi_long"], default=None,
+                    help="instead of the step: the semi-Markov CRF on a seeded workload "
+                         "(semi: B=32 N=25 K=5 C=20, the paper's Table 1 shape; semi_long: "
+                         "B=8 N=1024 K=8 C=32); one JSON line")
     ap.add_argument("--samples", type=int, default=64,
                     help="samples per sequence for the sampling entry point under --ops")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -240,6 +244,67 @@ def ops(w, samples, reps=50):
         print(json.dumps(line), flush=True)
 
 
+def semi(name, steps, warmup):
+    """Semi-Markov CRF: log Z + segment marginals and the best segmentation per step (the
+    chain scan over K*C expanded states), HIP-event timed like the chain step."""
+    import torch
+
+    from paper_2002_00876_amd import binding, workloads
+
+    sp_h, lens_h = workloads.generate_semi(name)
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    sp = torch.from_numpy(sp_h).to(dev)
+    lens = torch.from_numpy(lens_h).to(dev)
+    B, E, K, C, _ = sp.shape
+    N = E + 1
+    logz = torch.empty(B, dtype=torch.float32, device=dev)
+    marg = torch.empty_like(sp)
+    path = torch.empty((B, N), dtype=torch.int32, device=dev)
+    seglen = torch.empty((B, N - 1), dtype=torch.int32, device=dev)
+    score = torch.empty(B, dtype=torch.float32, device=dev)
+    ws_m = binding._semi_workspace(binding.OP_MARGINALS, B, N, K, C, dev)[0]
+    ws_v = binding._semi_workspace(binding.OP_VITERBI, B, N, K, C, dev)[0]
+
+    def marg_call():
+        binding.semi_marginals(sp, lens, out=(logz, marg), ws=ws_m)
+
+    def vit_call():
+        binding.semi_viterbi(sp, lens, out=(path, seglen, score), ws=ws_v)
+
+    def step():
+        marg_call()
+        vit_call()
+
+    def timed(fn, n):
+        for _ in range(max(warmup, 1)):
+            fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(n):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    ms_step = timed(step, steps)
+    ms_marg = timed(marg_call, steps)
+    ms_vit = timed(vit_call, steps)
+    fused = binding.workspace_bytes(binding.OP_MARGINALS, B, N, K * C) == 0
+    print(json.dumps({
+        "metric": "semi-Markov tokens/sec (log Z + segment marginals + best segmentation)",
+        "value": round(B * N / (ms_step * 1e-3), 1), "unit": "tokens/s",
+        "ms_per_step": round(ms_step, 5), "steps": steps, "warmup": warmup,
+        "config": {"workload": f"{name}: B={B} N={N} K={K} C={C}", "expanded_labels": K * C,
+                   "chain_path": "fused single launch" if fused else "multi-launch tree"},
+        "breakdown": {"marginals_ms": round(ms_marg, 5), "viterbi_ms": round(ms_vit, 5)},
+        "paper_context": {"tokens_per_s": 87e3,
+                          "note": "Table 1 semi-Markov, K80, B=32 N=25 C=20 K=5; log Z only"},
+    }), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -258,6 +323,9 @@ def main():
         sweep(args.sweep)
         return
     binding.lib()   # fail loudly if the HIP library is missing
+    if args.semi:
+        semi(args.semi, args.steps, args.warmup)
+        return
     w = workloads.WORKLOADS[args.workload]
     if args.ops:
         ops(w, args.samples)

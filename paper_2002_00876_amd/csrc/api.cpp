@@ -45,7 +45,7 @@ bool mul_ok(int64_t a, int64_t b, int64_t* out) {
 
 }  // namespace
 
-bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p) {
+bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, bool masks) {
     *p = Plan{};
     p->B = B; p->N = N; p->C = C; p->E = N - 1; p->op = op;
     int64_t cc, bcc;
@@ -79,6 +79,12 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p) {
         }
         p->lrmax = bump.take<float>((size_t)B * p->E * C);
         p->lcmax = bump.take<float>((size_t)B * p->E * C);
+        p->bw = (int)((C + 63) / 64);
+        for (int l = 0; masks && l < D; ++l) {
+            const size_t n = l == 0 ? (size_t)B * p->E : (size_t)B * (size_t)(Np >> l);
+            p->rbits[l] = bump.take<uint64_t>(n * C * p->bw);
+            p->cbits[l] = bump.take<uint64_t>(n * C * p->bw);
+        }
         if (op == TS_OP_MARGINALS)
             for (int l = 1; l < D; ++l) {
                 const size_t n = (size_t)B * (size_t)(Np >> l);
@@ -222,7 +228,7 @@ const char* plan_semi(int op, int64_t B, int64_t N, int64_t K, int64_t C, SemiPl
     if (K > kMaxLabels || K * C > kMaxLabels) return "K * C exceeds ts_chain_max_labels()";
     q->KC = K * C;
     if (N == 1) return nullptr;   // one token per sequence: no edges, no workspace
-    if (!make_plan(op, B, N, q->KC, nullptr, &q->base))
+    if (!make_plan(op, B, N, q->KC, nullptr, &q->base, /*masks=*/true))
         return "problem size overflows the supported range";
     const size_t x = align_up(sizeof(float) * B * (N - 1) * q->KC * q->KC);
     q->xpot = 0;
@@ -467,11 +473,17 @@ ts_status ts_semimarkov_logpartition(const float* sp, const int32_t* lengths, in
                                                       nullptr, nullptr, s));
     char* w = static_cast<char*>(ws);
     float* xp = reinterpret_cast<float*>(w + q.xpot);
-    if ((st = hip_status(launch_semi_expand(sp, lengths, B, N, K, C, xp, s))) != TS_OK) return st;
-    st = ts_chain_logpartition(xp, lengths, B, N, q.KC, logZ, q.base.bytes ? w + q.chain : nullptr,
-                               q.base.bytes, stream);
-    if (st != TS_OK) return st;
-    return hip_status(launch_semi_single(lengths, B, N, C, logZ, s));
+    hipError_t e = launch_semi_expand(sp, lengths, B, N, K, C, xp, s);
+    if (e == hipSuccess) {
+        if (q.base.fused) {
+            e = launch_small_log(xp, lengths, B, N, q.KC, logZ, nullptr, s);
+        } else {
+            make_plan(TS_OP_LOGPARTITION, B, N, q.KC, w + q.chain, &q.base, true);
+            e = launch_logz_tree(q.base, xp, lengths, logZ, s);
+        }
+    }
+    if (e == hipSuccess) e = launch_semi_single(lengths, B, N, C, logZ, s);
+    return hip_status(e);
 }
 
 ts_status ts_semimarkov_marginals(const float* sp, const int32_t* lengths, int64_t B,
@@ -491,12 +503,19 @@ ts_status ts_semimarkov_marginals(const float* sp, const int32_t* lengths, int64
     char* w = static_cast<char*>(ws);
     float* xp = reinterpret_cast<float*>(w + q.xpot);
     float* xm = reinterpret_cast<float*>(w + q.xout);
-    if ((st = hip_status(launch_semi_expand(sp, lengths, B, N, K, C, xp, s))) != TS_OK) return st;
-    st = ts_chain_marginals(xp, lengths, B, N, q.KC, logZ, xm,
-                            q.base.bytes ? w + q.chain : nullptr, q.base.bytes, stream);
-    if (st != TS_OK) return st;
-    if ((st = hip_status(launch_semi_gather(xm, B, N, K, C, marg, s))) != TS_OK) return st;
-    return logZ ? hip_status(launch_semi_single(lengths, B, N, C, logZ, s)) : TS_OK;
+    hipError_t e = launch_semi_expand(sp, lengths, B, N, K, C, xp, s);
+    if (e == hipSuccess) {
+        if (q.base.fused) {
+            e = launch_small_log(xp, lengths, B, N, q.KC, logZ, xm, s);
+        } else {
+            make_plan(TS_OP_MARGINALS, B, N, q.KC, w + q.chain, &q.base, true);
+            e = launch_logz_tree(q.base, xp, lengths, logZ, s);
+            if (e == hipSuccess) e = launch_marginals_tree(q.base, xp, lengths, xm, s);
+        }
+    }
+    if (e == hipSuccess) e = launch_semi_gather(xm, B, N, K, C, marg, s);
+    if (e == hipSuccess && logZ) e = launch_semi_single(lengths, B, N, C, logZ, s);
+    return hip_status(e);
 }
 
 ts_status ts_semimarkov_viterbi(const float* sp, const int32_t* lengths, int64_t B, int64_t N,
@@ -514,11 +533,17 @@ ts_status ts_semimarkov_viterbi(const float* sp, const int32_t* lengths, int64_t
     char* w = static_cast<char*>(ws);
     float* xp = reinterpret_cast<float*>(w + q.xpot);
     int32_t* xs = reinterpret_cast<int32_t*>(w + q.xout);
-    if ((st = hip_status(launch_semi_expand(sp, lengths, B, N, K, C, xp, s))) != TS_OK) return st;
-    st = ts_chain_viterbi(xp, lengths, B, N, q.KC, xs, score, q.base.bytes ? w + q.chain : nullptr,
-                          q.base.bytes, stream);
-    if (st != TS_OK) return st;
-    return hip_status(launch_semi_decode(xs, lengths, B, N, C, path, seglen, s));
+    hipError_t e = launch_semi_expand(sp, lengths, B, N, K, C, xp, s);
+    if (e == hipSuccess) {
+        if (q.base.fused) {
+            e = launch_small_max(xp, lengths, B, N, q.KC, xs, score, s);
+        } else {
+            make_plan(TS_OP_VITERBI, B, N, q.KC, w + q.chain, &q.base, true);
+            e = launch_viterbi_tree(q.base, xp, lengths, xs, score, s);
+        }
+    }
+    if (e == hipSuccess) e = launch_semi_decode(xs, lengths, B, N, C, path, seglen, s);
+    return hip_status(e);
 }
 
 const char* ts_last_error(void) { return g_err.c_str(); }

@@ -37,6 +37,14 @@ struct Plan {
     float* pmc[kMaxLevels] = {};
     float* lrmax = nullptr;
     float* lcmax = nullptr;
+    // finiteness bitmasks (only with masks; nullptr otherwise) of every node consumed by a
+    // product (levels 0..D-1; level 0 is the leaves [B, E]): rbits [nodes][C][bw] has bit c of row a set iff entry (a, c) is
+    // finite, cbits [nodes][C][bw] bit a of column c.  An entry of L (x) R is -inf exactly
+    // when row a of L and column c of R share no finite index, which spares the exact
+    // fallback of the exp-shifted product for structural zeros.
+    uint64_t* rbits[kMaxLevels] = {};
+    uint64_t* cbits[kMaxLevels] = {};
+    int bw = 1;                 // 64-bit words per line: ceil(C / 64)
     int ntile = 1;              // output tiles per matrix dimension (up_tile)
     // outside vectors of the nodes of levels 1..D-1 (normalised to max 0)
     float* u[kMaxLevels] = {};
@@ -57,7 +65,10 @@ struct Plan {
 inline int up_tile(int64_t C) { return C <= 64 ? 64 : 128; }
 
 // Fills the plan; with base == nullptr only sizes are computed.  Returns false on overflow.
-bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p);
+// masks: keep finiteness bitmasks of the log-semiring nodes (inputs with many structural
+// -inf entries, such as the semi-Markov expansion).
+bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p,
+               bool masks = false);
 
 // ---- launchers (return the first HIP error, hipSuccess otherwise) ----
 hipError_t launch_logz_tree(const Plan& p, const float* pot, const int32_t* lengths,

@@ -44,9 +44,12 @@ struct LeafMaxArgs {
     int64_t N, C;
     float* lrmax;
     float* lcmax;
+    uint64_t* rbits;   // [B, E, C, bw] finiteness of the left leaves' rows
+    uint64_t* cbits;   // [B, E, C, bw] finiteness of the right leaves' columns
+    int bw;
 };
 
-template <bool kVec>
+template <bool kVec, bool kBits>
 __global__ __launch_bounds__(256) void k_leaf_max(LeafMaxArgs a) {
     const int64_t E = a.N - 1;
     const int64_t b = blockIdx.x / E, t = blockIdx.x % E;
@@ -61,6 +64,21 @@ __global__ __launch_bounds__(256) void k_leaf_max(LeafMaxArgs a) {
 #pragma unroll 8
         for (int i = 0; i < C; ++i) cm = fmaxf(cm, leaf[(size_t)i * C + tid]);
         a.lcmax[(size_t)(b * E + t) * C + tid] = cm;
+        if (kBits && a.cbits) {
+            bool hole = false;   // a -inf entry in the column
+            for (int i = 0; i < C; ++i) hole |= leaf[(size_t)i * C + tid] == -INFINITY;
+            uint64_t* cb = a.cbits + ((size_t)(b * E + t) * C + tid) * a.bw;
+            for (int q = 0; q < a.bw; ++q) {
+                const int i1 = min(C, 64 * q + 64);
+                uint64_t bits = i1 - 64 * q == 64 ? ~0ull : (1ull << (i1 - 64 * q)) - 1;
+                if (hole) {
+                    bits = 0;
+                    for (int i = 64 * q; i < i1; ++i)
+                        bits |= (uint64_t)(leaf[(size_t)i * C + tid] > -INFINITY) << (i - 64 * q);
+                }
+                cb[q] = bits;
+            }
+        }
     }
     if (left) {
         float* rmax = a.lrmax + (size_t)(b * E + t) * C;
@@ -77,6 +95,16 @@ __global__ __launch_bounds__(256) void k_leaf_max(LeafMaxArgs a) {
             }
             m = wave_max(m);
             if (lane == 0) rmax[i] = m;
+            if (!kBits || !a.rbits) continue;   // (no products: one edge per sequence)
+            bool h = false;
+            for (int j = lane; j < C; j += kWave) h |= row[j] == -INFINITY;
+            const bool hole = __ballot(h) != 0;   // wave-uniform
+            uint64_t* rb = a.rbits + ((size_t)(b * E + t) * C + i) * a.bw;
+            for (int q = 0; q < a.bw; ++q) {
+                const int j = 64 * q + lane;
+                const uint64_t bits = __ballot(j < C && (!hole || row[min(j, C - 1)] > -INFINITY));
+                if (lane == q) rb[q] = bits;
+            }
         }
     }
 }
@@ -102,6 +130,11 @@ struct UpLogArgs {
     const float* cpmc;    // children column maxima [cnodes][C][cntile]
     int64_t cnodes;       // child node stride per sequence
     int cntile;           // partial maxima per line of a child (1 for the leaves)
+    const uint64_t* crbits;   // children's row / column finiteness bitmasks
+    const uint64_t* ccbits;
+    uint64_t* rbits;      // the outputs' bitmasks (nullptr at the root level)
+    uint64_t* cbits;
+    int bw;               // words per bitmask line
     float* core;          // outputs (level l)
     double* ro;
     double* co;
@@ -127,7 +160,7 @@ struct UpSmem {
     static constexpr size_t kBytes = sizeof(float) * kFloats;
 };
 
-template <int TM, bool VEC>
+template <int TM, bool VEC, bool kBits>
 __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
     using Sm = UpSmem<TM>;
     constexpr int LDA = Sm::LDA, LDB = Sm::LDB, LDT = Sm::LDT;
@@ -179,6 +212,11 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
                 const float* sc = a.cpmc + ((size_t)cl * C + line) * cnt;
                 Pmr[i] = p < cnt ? sr[p] : -INFINITY;
                 Pmc[i] = p < cnt ? sc[p] : -INFINITY;
+            }
+        if (kBits && tm == 0 && tn == 0 && a.rbits)
+            for (int i = tid; i < C * a.bw; i += kUpThreads) {
+                a.rbits[(size_t)pn * C * a.bw + i] = a.crbits[(size_t)cl * C * a.bw + i];
+                a.cbits[(size_t)pn * C * a.bw + i] = a.ccbits[(size_t)cl * C * a.bw + i];
             }
         return;
     }
@@ -356,6 +394,7 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
                 if (!(S >= kUnderflow) && a0 + row < C && c0 + col < C)
                     under |= 1ull << ((i * BR + j) * 16 + r);
             }
+    const int under_seen = under != 0;
     while (under) {
         const int bit = __builtin_ctzll(under);
         under &= under - 1;
@@ -363,6 +402,17 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
         const int row = wm * QW + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
         const int col = wn * QW + j * 32 + (lane & 31);
         const int gr = a0 + row, gc = c0 + col;
+        if (kBits) {
+            // no finite index shared by row gr of L and column gc of R: exactly -inf
+            const uint64_t* lb = a.crbits + ((size_t)cl * C + gr) * a.bw;
+            const uint64_t* rb = a.ccbits + ((size_t)cr * C + gc) * a.bw;
+            uint64_t shared = 0;
+            for (int q = 0; q < a.bw; ++q) shared |= lb[q] & rb[q];
+            if (!shared) {
+                T[row * LDT + col] = -INFINITY;
+                continue;
+            }
+        }
         const float sr = sa[row], sc = sb[col];
         const float* lrow = Lc + (size_t)gr * C;
         float q = -INFINITY;
@@ -377,6 +427,7 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
         }
         T[row * LDT + col] = val;
     }
+    const bool any_under = kBits && __syncthreads_or(under_seen);
     // the output node's offsets for the tile's rows and columns
     for (int i = tid; i < TM; i += kUpThreads) {
         const double ro = a0 + i < C ? (Lro ? Lro[a0 + i] : 0.0) + coLshift + sa[i] : 0.0;
@@ -401,6 +452,30 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
             float m = -INFINITY;
             for (int r = 0; r < nr; ++r) m = fmaxf(m, T[r * LDT + c] + rof[r]);
             Pmc[(size_t)(c0 + c) * nt + tm] = m;
+        }
+    }
+    // the finiteness bitmasks of the tile's rows (the words of its columns) and columns.
+    // Only entries recomputed by the fallback can be -inf: without any, every bit is set.
+    if (kBits && a.rbits) {
+        constexpr int kWords = TM / 64;
+        auto prefix = [](int n) { return n >= 64 ? ~0ull : n <= 0 ? 0ull : (1ull << n) - 1; };
+        const bool isrow = tid < TM;
+        const int line = isrow ? tid : tid - TM, nl = isrow ? nr : nc, len = isrow ? nc : nr;
+        if (tid < 2 * TM && line < nl) {
+            uint64_t bits[kWords];
+#pragma unroll
+            for (int q = 0; q < kWords; ++q) bits[q] = any_under ? 0ull : prefix(len - 64 * q);
+            if (any_under)
+                for (int e = 0; e < len; ++e) {
+                    const float v = isrow ? T[line * LDT + e] : T[e * LDT + line];
+                    bits[e >> 6] |= (uint64_t)(v > -INFINITY) << (e & 63);
+                }
+            uint64_t* out = isrow ? a.rbits + ((size_t)pn * C + a0 + line) * a.bw + c0 / 64
+                                  : a.cbits + ((size_t)pn * C + c0 + line) * a.bw + a0 / 64;
+            const int w0 = (isrow ? c0 : a0) / 64;
+#pragma unroll
+            for (int q = 0; q < kWords; ++q)
+                if (w0 + q < a.bw) out[q] = bits[q];
         }
     }
     // the tile, row by row
@@ -749,19 +824,19 @@ __global__ __launch_bounds__(kVecThreads) void k_form_log(FormArgs a) {
     write_marginal<kVec>(leafR, sy[0], sv, nrm[1], C, outR);
 }
 
-template <int TM, bool VEC>
+template <int TM, bool VEC, bool kBits>
 hipError_t up_sweep_tm(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
     constexpr size_t lds = UpSmem<TM>::kBytes;
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void*)k_up_log<TM, VEC>,
+        hipError_t e = hipFuncSetAttribute((const void*)k_up_log<TM, VEC, kBits>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
     // the leaves' row and column maxima (shifts of the level-1 products)
-    LeafMaxArgs m{pot, lengths, p.N, p.C, p.lrmax, p.lcmax};
-    hipLaunchKernelGGL(k_leaf_max<VEC>, dim3((unsigned)(p.B * p.E)), dim3(256), 0, s, m);
+    LeafMaxArgs m{pot, lengths, p.N, p.C, p.lrmax, p.lcmax, p.rbits[0], p.cbits[0], p.bw};
+    hipLaunchKernelGGL((k_leaf_max<VEC, kBits>), dim3((unsigned)(p.B * p.E)), dim3(256), 0, s, m);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     for (int l = 1; l <= p.D; ++l) {
@@ -776,23 +851,35 @@ hipError_t up_sweep_tm(const Plan& p, const float* pot, const int32_t* lengths, 
         }
         a.core = p.core[l]; a.ro = p.ro[l]; a.co = p.co[l];
         a.pmr = p.pmr[l]; a.pmc = p.pmc[l];
+        a.crbits = p.rbits[l - 1]; a.ccbits = p.cbits[l - 1];
+        a.rbits = l < p.D ? p.rbits[l] : nullptr;
+        a.cbits = l < p.D ? p.cbits[l] : nullptr;
+        a.bw = p.bw;
         a.nodes = p.Np >> l;
         a.lengths = lengths; a.B = p.B; a.N = p.N; a.C = p.C; a.level = l;
         a.ntile = p.ntile;
         a.nlogical = p.B * a.nodes * p.ntile * p.ntile;
         a.ngrid = round8(a.nlogical);
-        hipLaunchKernelGGL((k_up_log<TM, VEC>), dim3((unsigned)a.ngrid), dim3(kUpThreads), lds, s, a);
+        hipLaunchKernelGGL((k_up_log<TM, VEC, kBits>), dim3((unsigned)a.ngrid), dim3(kUpThreads), lds, s, a);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
 }
 
-hipError_t up_sweep(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
+template <bool kBits>
+hipError_t up_sweep_bits(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
     const bool vec = (p.C % 4) == 0;
     if (up_tile(p.C) == 64)
-        return vec ? up_sweep_tm<64, true>(p, pot, lengths, s) : up_sweep_tm<64, false>(p, pot, lengths, s);
-    return vec ? up_sweep_tm<128, true>(p, pot, lengths, s) : up_sweep_tm<128, false>(p, pot, lengths, s);
+        return vec ? up_sweep_tm<64, true, kBits>(p, pot, lengths, s)
+                   : up_sweep_tm<64, false, kBits>(p, pot, lengths, s);
+    return vec ? up_sweep_tm<128, true, kBits>(p, pot, lengths, s)
+               : up_sweep_tm<128, false, kBits>(p, pot, lengths, s);
+}
+
+hipError_t up_sweep(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
+    return p.rbits[0] ? up_sweep_bits<true>(p, pot, lengths, s)
+                      : up_sweep_bits<false>(p, pot, lengths, s);
 }
 
 hipError_t root(const Plan& p, const float* pot, const int32_t* lengths, float* logZ,
