@@ -21,8 +21,8 @@ namespace tsc {
 
 namespace {
 
-constexpr int kMT = 64;    // output tile
-constexpr int kMK = 32;    // k slice
+constexpr int kMT = 64;    // output tile edge
+constexpr int kMK = 32;    // k slice of the narrow kernel
 constexpr int kMThreads = 256;
 
 struct UpMaxArgs {
@@ -43,9 +43,12 @@ __device__ __forceinline__ double child_at(const UpMaxArgs& a, int64_t b, int64_
     return a.cnode ? a.cnode[off] : (double)a.leaves[off];
 }
 
-__global__ __launch_bounds__(kMThreads) void k_up_max(UpMaxArgs a) {
-    __shared__ double As[kMK][kMT];   // As[k][row]
-    __shared__ double Bs[kMK][kMT];   // Bs[k][col]
+// One tree level of the max-plus up-sweep for C <= 64: a 64 x 64 output tile per workgroup of
+// 256 threads with 4 x 4 float64 outputs each (small register footprint, many waves).
+__global__ __launch_bounds__(kMThreads) void k_up_max_narrow(UpMaxArgs a) {
+    __shared__ __align__(16) double As[kMK][kMT + 2];   // As[k][row]; the padding spreads
+                                                        // the transposing stores over banks
+    __shared__ __align__(16) double Bs[kMK][kMT];       // Bs[k][col]
     const int64_t lid = xcd_swizzle(blockIdx.x, a.ngrid);
     if (lid >= a.nlogical) return;
     const int ntiles = a.ntm * a.ntm;
@@ -108,6 +111,112 @@ __global__ __launch_bounds__(kMThreads) void k_up_max(UpMaxArgs a) {
             const int64_t r = a0 + ty * 4 + i, c = c0 + tx * 4 + j;
             if (r < C && c < C) P[r * C + c] = acc[i][j];
         }
+}
+
+// One tree level of the max-plus up-sweep, P[a][c] = max_b L[a][b] + R[b][c], for one TM x TM
+// output tile per workgroup of (TM/8)^2 threads, each holding an 8 x 8 block of float64
+// accumulators (64 add + 64 max per 16 operand reads from LDS).  The contraction index runs
+// in slices of KS: A is staged transposed, As[k][row] (rows padded to TM + 2 doubles, which
+// keeps the 16-byte operand reads aligned and spreads the transposing stores over the
+// banks), B as is, Bs[k][col]; the next slice's global loads are in flight while the current
+// one is used.
+template <int TM, int KS>
+__global__ __launch_bounds__((TM / 8) * (TM / 8)) void k_up_max(UpMaxArgs a) {
+    constexpr int TPD = TM / 8, NT = TPD * TPD, LDA = TM + 2;
+    constexpr int NA = TM * KS / NT;   // staged values per thread and operand
+    __shared__ __align__(16) double As[KS * LDA];
+    __shared__ __align__(16) double Bs[KS * TM];
+    const int64_t lid = xcd_swizzle(blockIdx.x, a.ngrid);
+    if (lid >= a.nlogical) return;
+    const int ntiles = a.ntm * a.ntm;
+    const int tile = (int)(lid % ntiles);
+    const int64_t node = lid / ntiles;
+    const int64_t b = node / a.nodes, k = node % a.nodes;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    const int64_t span = (int64_t)1 << a.level, half = span >> 1;
+    if (k * span >= Eb) return;
+    const int C = (int)a.C;
+    const int tm = tile / a.ntm, tn = tile % a.ntm;
+    const int a0 = tm * TM, c0 = tn * TM;
+    const int tid = threadIdx.x;
+    double* P = a.node + (size_t)(b * a.nodes + k) * C * C;
+    const bool right = (2 * k + 1) * half < Eb;
+    if (!right) {
+        for (int idx = tid; idx < TM * TM; idx += NT) {
+            const int r = a0 + idx / TM, c = c0 + idx % TM;
+            if (r < C && c < C) P[(size_t)r * C + c] = child_at(a, b, 2 * k, r, c);
+        }
+        return;
+    }
+    const size_t lbase = (size_t)(b * a.cnodes + 2 * k) * C * C;
+    const size_t rbase = lbase + (size_t)C * C;
+    auto at = [&](size_t off) { return a.cnode ? a.cnode[off] : (double)a.leaves[off]; };
+    double ra[NA], rb[NA];
+    // staging of slice [k0, k0 + KS): thread value v of A is (row idx / KS, k idx % KS) with
+    // idx = tid + v * NT (consecutive threads read consecutive k), of B (k idx / TM, col idx % TM)
+    auto load = [&](int k0) {
+#pragma unroll
+        for (int v = 0; v < NA; ++v) {
+            const int idx = tid + v * NT;
+            const int r = a0 + idx / KS, kk = k0 + idx % KS;
+            ra[v] = (r < C && kk < C) ? at(lbase + (size_t)r * C + kk) : -INFINITY;
+            const int kr = k0 + idx / TM, c = c0 + idx % TM;
+            rb[v] = (kr < C && c < C) ? at(rbase + (size_t)kr * C + c) : -INFINITY;
+        }
+    };
+    auto store = [&]() {
+#pragma unroll
+        for (int v = 0; v < NA; ++v) {
+            const int idx = tid + v * NT;
+            As[(idx % KS) * LDA + idx / KS] = ra[v];
+            Bs[idx] = rb[v];
+        }
+    };
+    const int ty = tid / TPD, tx = tid % TPD;
+    double acc[8][8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[i][j] = -INFINITY;
+    const int nslices = (C + KS - 1) / KS;
+    load(0);
+    store();
+    __syncthreads();
+    for (int s = 0; s < nslices; ++s) {
+        if (s + 1 < nslices) load((s + 1) * KS);
+#pragma unroll 2
+        for (int kk = 0; kk < KS; ++kk) {
+            double av[8], bv[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                av[i] = As[kk * LDA + ty * 8 + i];
+                bv[i] = Bs[kk * TM + tx * 8 + i];
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                double t[8];   // eight independent sums, then eight independent maxima
+#pragma unroll
+                for (int j = 0; j < 8; ++j) t[j] = av[i] + bv[j];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) acc[i][j] = fmax(acc[i][j], t[j]);
+            }
+        }
+        if (s + 1 < nslices) {
+            __syncthreads();
+            store();
+            __syncthreads();
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int r = a0 + ty * 8 + i;
+        if (r >= C) continue;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int c = c0 + tx * 8 + j;
+            if (c < C) P[(size_t)r * C + c] = acc[i][j];
+        }
+    }
 }
 
 // ---- forward scores down the tree: u_L = u_N, u_R = u_N (x) L
@@ -324,7 +433,8 @@ inline int64_t round8(int64_t x) { return (x + 7) / 8 * 8; }
 hipError_t launch_viterbi_tree(const Plan& p, const float* pot, const int32_t* lengths,
                                int32_t* path, float* score, hipStream_t s) {
     const int64_t C = p.C;
-    const int ntm = (int)((C + kMT - 1) / kMT);
+    const int tmax = C <= kMT ? kMT : 2 * kMT;   // the narrow kernel below, 128-wide above
+    const int ntm = (int)((C + tmax - 1) / tmax);
     for (int l = 1; l <= p.D; ++l) {
         UpMaxArgs a{};
         a.leaves = (l == 1) ? pot : nullptr;
@@ -335,7 +445,10 @@ hipError_t launch_viterbi_tree(const Plan& p, const float* pot, const int32_t* l
         a.lengths = lengths; a.B = p.B; a.N = p.N; a.C = C; a.level = l; a.ntm = ntm;
         a.nlogical = p.B * a.nodes * ntm * ntm;
         a.ngrid = round8(a.nlogical);
-        hipLaunchKernelGGL(k_up_max, dim3((unsigned)a.ngrid), dim3(kMThreads), 0, s, a);
+        if (tmax == kMT)
+            hipLaunchKernelGGL(k_up_max_narrow, dim3((unsigned)a.ngrid), dim3(kMThreads), 0, s, a);
+        else
+            hipLaunchKernelGGL((k_up_max<2 * kMT, 16>), dim3((unsigned)a.ngrid), dim3(256), 0, s, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
