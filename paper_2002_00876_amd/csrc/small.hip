@@ -491,7 +491,10 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
     const int rslot = uni(H(ly.info + T.vbase[T.D])) & kSlotMask;
     auto U = [&](int l, int k) { return ly.vecs + (T.vbase[l] + k) * 2 * CP; };
     // ---- root: log Z = LSE_{a,c} ro[a] + co[c] + core[a][c]   (last wave, overlapping
-    // the first outside level, which does not need it)
+    // the first outside level, which does not need it).  The value stays in a register
+    // until the end: a global store before a barrier would hold the barrier up until it
+    // completes.
+    float lz = 0.f;
     if (a.logZ && w == kSmallWaves - 1) {
         const int rc = Ly::core(rslot), rr = Ly::ro(rslot), rcc = Ly::co(rslot);
         const int lc = min(lane, C - 1);
@@ -519,10 +522,15 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
             for (int q = 0; q < kRows; ++q) s += fexp(x[q] - m);
         }
         s = wave_sum_fast(s);
-        if (lane == 0)
-            a.logZ[b] = (m == -INFINITY) ? -INFINITY : (float)(rs + cs + (double)(m + flog(s)));
+        lz = (m == -INFINITY) ? -INFINITY : (float)(rs + cs + (double)(m + flog(s)));
     }
-    if (!a.marg) return;
+    auto store_logz = [&]() {
+        if (a.logZ && w == kSmallWaves - 1 && lane == 0) a.logZ[b] = lz;
+    };
+    if (!a.marg) {
+        store_logz();
+        return;
+    }
     // ---- outside sweep: u, v of every node (root: zeros, padding -inf)
     if (w == 0)
         for (int idx = lane; idx < 2 * CP; idx += kWave)
@@ -586,6 +594,7 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
             if (i < C && j < C) out[i * C + j] = (n == -INFINITY) ? 0.f : fexp(x[q] - n);
         }
     }
+    store_logz();
     zero_padding();
 }
 
