@@ -421,7 +421,9 @@ def main():
     t_mfma = alg["marg_flops"] / MFMA_F32_PEAK
     t_f64 = alg["vit_ops"] / VALU_F64_OPS_PEAK
     sec = ms_call * 1e-3
-    if t_mem >= t_mfma + t_f64:
+    # the binding resource is the one with the longest time at its peak: on the single-launch
+    # path the log-semiring and the max-plus workgroups run side by side on different CUs
+    if t_mem >= max(t_mfma, t_f64):
         achieved = alg["step_bytes"] / sec / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK / 1e9,
                 "unit": "GB/s", "frac": round(achieved / (HBM_PEAK / 1e9), 5)}
@@ -437,7 +439,7 @@ def main():
     roof["kernel"] = dom
     roof["kernel_ms"] = round(ms_call, 5)
     roof["algorithmic_bytes"] = alg["step_bytes"]
-    roof["roofline_ms"] = round(max(t_mem, t_mfma + t_f64) * 1e3, 6)
+    roof["roofline_ms"] = round(max(t_mem, t_mfma, t_f64) * 1e3, 6)
 
     out = {
         "metric": "tokens/sec for linear-chain logZ+marginals (B,N,C); % of HBM/compute roofline",
