@@ -23,7 +23,8 @@
  *            unless the environment variable TS_CHECK=1 is set, in which case the call
  *            copies the lengths to the host synchronously and returns TS_ERR_LENGTHS.
  *   B, N, C  batch size, maximum number of tokens, number of labels:
- *            B >= 1, N >= 1, 1 <= C <= ts_chain_max_labels().
+ *            B >= 1, N >= 1, 1 <= C <= ts_chain_max_labels(), B * N <= 2^29 (one launch
+ *            grid covers every edge); larger problems return TS_ERR_BAD_DIM.
  *   ws       device workspace of at least ts_chain_workspace_bytes(op, B, N, C) bytes,
  *            aligned to 256 bytes (any hipMalloc / PyTorch CUDA allocation is).  May be
  *            NULL when that size is 0.  Its contents on entry are ignored.

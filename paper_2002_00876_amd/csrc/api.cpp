@@ -23,6 +23,7 @@ ts_status fail(ts_status code, const std::string& msg) {
 }
 
 constexpr size_t kAlign = 256;
+constexpr int64_t kMaxGridItems = (int64_t)1 << 29;   // B * N bound: grids stay below 2^31
 
 struct Bump {
     char* base;
@@ -53,6 +54,9 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, boo
     if (!mul_ok(C, C, &cc) || !mul_ok(B, cc, &bcc) || !mul_ok(bcc, 2 * (N + 1), &cc) ||
         !mul_ok(cc, 8, &cc) || cc > ((int64_t)1 << 60))
         return false;
+    // launch grids reach B * (N-1) * 4 workgroups (one per edge, or per tile of a tree
+    // node); keep that within one launch's grid
+    if (!mul_ok(B, N, &cc) || cc > kMaxGridItems) return false;
     if (N == 1) return true;  // no edges: no workspace
     // small label sets: one fused launch per call, tree kept in LDS, no workspace.
     // TS_PATH=tree forces the multi-launch tree (used by the tests to cover both paths).
@@ -225,7 +229,11 @@ struct SemiPlan {
 // Sizes only; returns the reason when the dimensions are out of range, else nullptr.
 const char* plan_semi(int op, int64_t B, int64_t N, int64_t K, int64_t C, SemiPlan* q) {
     if (B < 1 || N < 1 || K < 1 || C < 1) return "B, N, K and C must all be >= 1";
-    if (K > kMaxLabels || K * C > kMaxLabels) return "K * C exceeds ts_chain_max_labels()";
+    if (K > kMaxLabels || C > kMaxLabels || K * C > kMaxLabels)
+        return "K * C exceeds ts_chain_max_labels()";
+    int64_t bn;
+    if (!mul_ok(B, N, &bn) || bn > kMaxGridItems)
+        return "problem size overflows the supported range";
     q->KC = K * C;
     if (N == 1) return nullptr;   // one token per sequence: no edges, no workspace
     if (!make_plan(op, B, N, q->KC, nullptr, &q->base, /*masks=*/true))

@@ -97,6 +97,14 @@ def test_bad_dimensions_are_rejected(L):
 def test_size_overflow_is_rejected(L):
     assert L.ts_chain_logpartition(FAKE, None, 1 << 40, 1 << 20, 256, FAKE, FAKE, 1, None) == BAD_DIM
     assert "overflow" in _err(L)
+    # B * N beyond what one launch grid covers, even with tiny label sets
+    assert L.ts_chain_logpartition(FAKE, None, 1 << 20, 1 << 10, 2, FAKE, FAKE, 1 << 40, None) == BAD_DIM
+    assert L.ts_chain_workspace_bytes(0, 1 << 20, 1 << 10, 2) == 0
+    assert L.ts_semimarkov_logpartition(FAKE, None, 1 << 20, 1 << 10, 1, 2, FAKE, FAKE, 1 << 40,
+                                        None) == BAD_DIM
+    # a huge label count with K = 1 is rejected before K * C is formed
+    assert L.ts_semimarkov_logpartition(FAKE, None, 2, 5, 1, 1 << 62, FAKE, FAKE, 1 << 40,
+                                        None) == BAD_DIM
 
 
 def test_null_pointers_are_rejected(L):
