@@ -119,9 +119,14 @@ __device__ __forceinline__ int role_of(int E, int l, int k) {
 constexpr int kSlotMask = 0x3fff;
 
 __device__ void build_node_table(int E, int nodes, int info) {
-    // node i goes to lane i / 16 of wave i % 16: a few lanes of every wave, not one wave
-    for (int base = 0; base < nodes; base += kSmallThreads) {
-        const int i = base + (int)(threadIdx.x % kWave) * kSmallWaves + (int)(threadIdx.x / kWave);
+    // A table of at most 64 nodes is built in one pass by one wave (the one before the wave
+    // that sets up the tree): every wave that runs this code issues all of its instructions,
+    // whatever few lanes are active.  Larger tables: node i goes to lane i / 16 of wave i % 16.
+    const bool one = nodes <= kWave;
+    const int wave = (int)(threadIdx.x / kWave), lane = (int)(threadIdx.x % kWave);
+    if (one && wave != kSmallWaves - 2) return;
+    for (int base = 0; base < nodes; base += one ? kWave : kSmallThreads) {
+        const int i = one ? base + lane : base + lane * kSmallWaves + wave;
         if (i >= nodes) continue;
         int l = 0, vb = 0, n = E, nprev = 0, pb = E;   // pb = pbase[l] once l >= 1
         while (i >= vb + n) {
