@@ -111,6 +111,73 @@ __device__ __forceinline__ int role_of(int E, int l, int k) {
     return kNone;
 }
 
+// The node tables of every tree of up to kTableEdges leaves, computed at compile time (the
+// same walk as build_node_table below): a short sequence copies its row instead of
+// computing it.
+constexpr int kTableEdges = 64;
+
+constexpr int ce_lvl_n(int E, int l) { return ((E - 1) >> l) + 1; }
+
+constexpr int ce_nodes(int E) {
+    int total = E, n = E;
+    while (n > 1) { n = (n + 1) / 2; total += n; }
+    return total;
+}
+
+constexpr int ce_role(int E, int l, int k) {
+    while ((E - 1) >> l) {
+        if (k & 1) return kRight;
+        if (k + 1 < ce_lvl_n(E, l)) return kLeft;
+        ++l;
+        k >>= 1;
+    }
+    return kNone;
+}
+
+constexpr unsigned short ce_entry(int E, int i) {
+    int l = 0, vb = 0, n = E, nprev = 0, pb = E;
+    while (i >= vb + n) {
+        if (l >= 1) pb += nprev / 2;
+        vb += n;
+        nprev = n;
+        n = (n + 1) / 2;
+        ++l;
+    }
+    const int k = i - vb;
+    int ll = l, kk = k;
+    while (ll > 0 && kk >= ce_lvl_n(E, ll - 1) / 2) {
+        --ll;
+        kk *= 2;
+        if (ll > 0) pb -= ce_lvl_n(E, ll - 1) / 2;
+    }
+    const int slot = ll == 0 ? kk : pb + kk;
+    return (unsigned short)(slot | (ce_role(E, l, k) << 14));
+}
+
+constexpr int ce_total() {
+    int t = 0;
+    for (int E = 1; E <= kTableEdges; ++E) t += ce_nodes(E);
+    return t;
+}
+
+struct NodeTables {
+    int off[kTableEdges + 1];
+    unsigned short entry[ce_total()];
+};
+
+constexpr NodeTables ce_tables() {
+    NodeTables t{};
+    int o = 0;
+    for (int E = 1; E <= kTableEdges; ++E) {
+        t.off[E] = o;
+        for (int i = 0; i < ce_nodes(E); ++i) t.entry[o + i] = ce_entry(E, i);
+        o += ce_nodes(E);
+    }
+    return t;
+}
+
+__constant__ NodeTables kNodeTables = ce_tables();
+
 // The node table: one 16-bit entry per node in level-major order (node (l, k) at
 // vbase[l] + k) holding its slot (bits 0..13) and role (bits 14..15).  Leaves are slots
 // 0..E-1; the products of level l follow those of the levels below (slots from
@@ -122,8 +189,13 @@ __device__ void build_node_table(int E, int nodes, int info) {
     // A table of at most 64 nodes is built in one pass by one wave (the one before the wave
     // that sets up the tree): every wave that runs this code issues all of its instructions,
     // whatever few lanes are active.  Larger tables: node i goes to lane i / 16 of wave i % 16.
-    const bool one = nodes <= kWave;
     const int wave = (int)(threadIdx.x / kWave), lane = (int)(threadIdx.x % kWave);
+    if (E <= kTableEdges) {   // precomputed: one wave copies the row
+        if (wave != kSmallWaves - 2) return;
+        for (int i = lane; i < nodes; i += kWave) H(info + i) = kNodeTables.entry[kNodeTables.off[E] + i];
+        return;
+    }
+    const bool one = nodes <= kWave;
     if (one && wave != kSmallWaves - 2) return;
     for (int base = 0; base < nodes; base += one ? kWave : kSmallThreads) {
         const int i = one ? base + lane : base + lane * kSmallWaves + wave;
@@ -152,16 +224,21 @@ __device__ void build_node_table(int E, int nodes, int info) {
 // Tree of E >= 1 leaves set up by one wave (lane l fills level l), instead of one thread
 // walking the levels
 __device__ void tree_init_wave(Tree& T, int E) {
+    // lane l <= kSmallMaxLevels holds level l; vbase and pbase are prefix sums over the lanes
     const int l = threadIdx.x % kWave;
+    const int n = l <= kSmallMaxLevels ? lvl_n(E, l) : 0;
+    int sn = n, sp = n / 2;   // n[l] / 2 = products of level l + 1
+#pragma unroll
+    for (int d = 1; d <= kSmallMaxLevels; d <<= 1) {
+        const int on = __shfl_up(sn, d, kWave), op = __shfl_up(sp, d, kWave);
+        sn += l >= d ? on : 0;
+        sp += l >= d ? op : 0;
+    }
+    const int sp2 = __shfl_up(sp, 2, kWave);   // products of levels 1..l-1
     if (l <= kSmallMaxLevels) {
-        int vb = 0, pb = 0;
-        for (int q = 0; q < l; ++q) {
-            vb += lvl_n(E, q);
-            if (q >= 1) pb += lvl_n(E, q - 1) / 2;
-        }
-        T.n[l] = lvl_n(E, l);
-        T.vbase[l] = vb;
-        T.pbase[l] = pb;
+        T.n[l] = n;
+        T.vbase[l] = sn - n;
+        T.pbase[l] = l >= 2 ? sp2 : 0;
     }
     if (l == 0) {
         T.E = E;
