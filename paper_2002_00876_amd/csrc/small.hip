@@ -622,21 +622,25 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
     for (int l = T.D; l >= 1; --l) {
         const int nn = uni(T.n[l]), nprev = uni(T.n[l - 1]), vb0 = uni(T.vbase[l - 1]);
         const int ub = uni(U(l, 0)), ub0 = uni(U(l - 1, 0));
-        for (int task = w; task < 3 * nn; task += kSmallWaves) {
-            const int k = task / 3, which = task - 3 * k;
+        // two tasks per node, the copies folded into them: u_L = u_N with u_R = u_N (x) L
+        // (or v_L = v_N without a right child), and v_R = v_N with v_L = R (x) v_N
+        for (int task = w; task < 2 * nn; task += kSmallWaves) {
+            const int k = task >> 1, which = task & 1;
             const bool right = 2 * k + 1 < nprev;
             const int uN = ub + k * 2 * CP, vN = uN + CP;
             const int uL = ub0 + 2 * k * 2 * CP, uR = uL + 2 * CP;
             if (which == 0) {
                 if (lane < CP) {
                     F(uL + lane) = F(uN + lane);
-                    if (right) F(uR + CP + lane) = F(vN + lane);
-                    else F(uL + CP + lane) = F(vN + lane);
+                    if (!right) F(uL + CP + lane) = F(vN + lane);
                 }
-            } else if (which == 1 && right) {   // u_R = u_N (x) L
-                const int sl = uni(H(ly.info + vb0 + 2 * k)) & kSlotMask;
-                vec_log<CP, false>(ly, uN, sl, uR, scr);
-            } else if (which == 2 && right) {   // v_L = R (x) v_N
+                if (right) {   // u_R = u_N (x) L
+                    const int sl = uni(H(ly.info + vb0 + 2 * k)) & kSlotMask;
+                    vec_log<CP, false>(ly, uN, sl, uR, scr);
+                }
+            } else if (right) {
+                if (lane < CP) F(uR + CP + lane) = F(vN + lane);
+                // v_L = R (x) v_N
                 const int sr = uni(H(ly.info + vb0 + 2 * k + 1)) & kSlotMask;
                 vec_log<CP, true>(ly, vN, sr, uL + CP, scr);
             }
@@ -895,12 +899,11 @@ __device__ __forceinline__ void small_max_body(const SmallMaxArgs& a, const int6
     for (int l = T.D; l >= 1; --l) {
         const int nn = uni(T.n[l]), nprev = uni(T.n[l - 1]), vb0 = uni(T.vbase[l - 1]);
         const int ub = uni(U(l, 0)), ub0 = uni(U(l - 1, 0));
-        for (int task = w; task < 2 * nn; task += kSmallWaves) {
-            const int k = task >> 1, which = task & 1;
+        // one task per node: u_L = u_N, and u_R = u_N (x) L when there is a right child
+        for (int k = w; k < nn; k += kSmallWaves) {
             const int uN = ub + k * 2 * C, uL = ub0 + 2 * k * 2 * C;
-            if (which == 0) {
-                if (lane < C) Dd(uL + 2 * lane) = Dd(uN + 2 * lane);
-            } else if (2 * k + 1 < nprev) {
+            if (lane < C) Dd(uL + 2 * lane) = Dd(uN + 2 * lane);
+            if (2 * k + 1 < nprev) {
                 const int sl = uni(H(ly.info + vb0 + 2 * k)) & kSlotMask;
                 if (l == 1) wave_vec_max<CP, true>(C, uN, ly.leaves + sl * CC, uL + 2 * C);
                 else wave_vec_max<CP, false>(C, uN, ly.node64(sl, Eb), uL + 2 * C);
