@@ -465,9 +465,10 @@ __device__ void normalise_leaves(const LogLayout<CP>& ly, int raw, int E) {
 // One wave: outside-vector product with the node at `slot` (N[i][j] = ro[i] + co[j] +
 // core[i][j]).  kRowSide == false: y[j] = LSE_i x[i] + N[i][j] (y = x (x) N);
 // kRowSide == true: y[i] = LSE_j N[i][j] + x[j] (y = N (x) x).  y is shifted to max 0 and
-// its padding is -inf.  Lane l computes output l % 32 over half l / 32 of the index.
+// its padding is -inf; the total shift (of the input and of the output) is returned.  Lane l
+// computes output l % 32 over half l / 32 of the index.
 template <int CP, bool kRowSide>
-__device__ void vec_log(const LogLayout<CP>& ly, int x, int slot, int y, int scr) {
+__device__ double vec_log(const LogLayout<CP>& ly, int x, int slot, int y, int scr) {
     using Ly = LogLayout<CP>;
     constexpr int kLd = Ly::kLd, kHalf = CP / 2;
     const int C = ly.C;
@@ -500,6 +501,7 @@ __device__ void vec_log(const LogLayout<CP>& ly, int x, int slot, int y, int scr
     const double zs = (double)safe_shift(wave_max_fast((float)z));
     if (h == 0 && o < CP) F(y + o) = (float)(z - zs);
     wave_sync();
+    return ws + zs;   // y as stored plus this is the exact x (x) N
 }
 
 struct SmallLogArgs {
@@ -554,8 +556,9 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
     __syncthreads();
     normalise_leaves<CP>(ly, raw, Eb);
     __syncthreads();
-    // ---- up-sweep: one wave per product
-    for (int l = 1; l <= T.D; ++l) {
+    // ---- up-sweep: one wave per product, below the root: the root's matrix is never needed
+    // (log Z comes from its children's outside vectors)
+    for (int l = 1; l < T.D; ++l) {
         const int np = uni(T.products(l));
         const int vb0 = uni(T.vbase[l - 1]), vb1 = uni(T.vbase[l]);
         for (int k = w; k < np; k += kSmallWaves) {
@@ -570,50 +573,55 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
         }
         __syncthreads();
     }
-    const int rslot = uni(H(ly.info + T.vbase[T.D])) & kSlotMask;
     auto U = [&](int l, int k) { return ly.vecs + (T.vbase[l] + k) * 2 * CP; };
-    // ---- root: log Z = LSE_{a,c} ro[a] + co[c] + core[a][c]   (last wave, overlapping
-    // the first outside level, which does not need it).  The value stays in a register
-    // until the end: a global store before a barrier would hold the barrier up until it
-    // completes.
+    // log Z stays in a register of the last wave until the end: a global store before a
+    // barrier would hold the barrier up until it completes
     float lz = 0.f;
-    if (a.logZ && w == kSmallWaves - 1) {
-        const int rc = Ly::core(rslot), rr = Ly::ro(rslot), rcc = Ly::co(rslot);
-        const int lc = min(lane, C - 1);
-        const double rs = (double)safe_shift(wave_max_fast(lane < C ? (float)Dd(rr + 2 * lc) : -INFINITY));
-        const double cs = (double)safe_shift(wave_max_fast(lane < C ? (float)Dd(rcc + 2 * lc) : -INFINITY));
-        constexpr int kRows = CP / 2;
-        const int j = lane & 31, i0 = lane >> 5, jc = min(j, C - 1);
-        const float cj = (float)(Dd(rcc + 2 * jc) - cs);
-        float x[kRows];
-#pragma unroll
-        for (int q = 0; q < kRows; ++q) {
-            const int ic = min(i0 + 2 * q, C - 1);
-            x[q] = F(rc + ic * kLd + jc) + (float)(Dd(rr + 2 * ic) - rs) + cj;
-        }
-        float m = -INFINITY;
-#pragma unroll
-        for (int q = 0; q < kRows; ++q) {
-            x[q] = (i0 + 2 * q < C && j < C) ? x[q] : -INFINITY;
-            m = fmaxf(m, x[q]);
-        }
-        m = wave_max_fast(m);
-        float s = 0.f;
-        if (m != -INFINITY) {
-#pragma unroll
-            for (int q = 0; q < kRows; ++q) s += fexp(x[q] - m);
-        }
-        s = wave_sum_fast(s);
-        lz = (m == -INFINITY) ? -INFINITY : (float)(rs + cs + (double)(m + flog(s)));
-    }
     auto store_logz = [&]() {
         if (a.logZ && w == kSmallWaves - 1 && lane == 0) a.logZ[b] = lz;
     };
-    if (!a.marg) {
-        store_logz();
-        return;
+    if (T.D == 0) {
+        // one edge: log Z = LSE_{a,c} of the leaf itself
+        if (a.logZ && w == kSmallWaves - 1) {
+            const int rslot = uni(H(ly.info + T.vbase[0])) & kSlotMask;
+            const int rc = Ly::core(rslot), rr = Ly::ro(rslot), rcc = Ly::co(rslot);
+            const int lc = min(lane, C - 1);
+            const double rs = (double)safe_shift(wave_max_fast(lane < C ? (float)Dd(rr + 2 * lc) : -INFINITY));
+            const double cs = (double)safe_shift(wave_max_fast(lane < C ? (float)Dd(rcc + 2 * lc) : -INFINITY));
+            constexpr int kRows = CP / 2;
+            const int j = lane & 31, i0 = lane >> 5, jc = min(j, C - 1);
+            const float cj = (float)(Dd(rcc + 2 * jc) - cs);
+            float x[kRows];
+#pragma unroll
+            for (int q = 0; q < kRows; ++q) {
+                const int ic = min(i0 + 2 * q, C - 1);
+                x[q] = F(rc + ic * kLd + jc) + (float)(Dd(rr + 2 * ic) - rs) + cj;
+            }
+            float m = -INFINITY;
+#pragma unroll
+            for (int q = 0; q < kRows; ++q) {
+                x[q] = (i0 + 2 * q < C && j < C) ? x[q] : -INFINITY;
+                m = fmaxf(m, x[q]);
+            }
+            m = wave_max_fast(m);
+            float s = 0.f;
+            if (m != -INFINITY) {
+#pragma unroll
+                for (int q = 0; q < kRows; ++q) s += fexp(x[q] - m);
+            }
+            s = wave_sum_fast(s);
+            lz = (m == -INFINITY) ? -INFINITY : (float)(rs + cs + (double)(m + flog(s)));
+        }
+        if (!a.marg) {
+            store_logz();
+            return;
+        }
     }
-    // ---- outside sweep: u, v of every node (root: zeros, padding -inf)
+    // ---- outside sweep: u, v of every node (root: zeros, padding -inf).  With the root's
+    // children L and R, log Z = LSE_{a,c} (L (x) R)[a][c] = LSE_b u_R[b] + v_L[b], where
+    // u_R = 0 (x) L and v_L = R (x) 0 are the first level's outside vectors; their shifts
+    // are kept in rootShift.
+    __shared__ double rootShift[2];
     if (w == 0)
         for (int idx = lane; idx < 2 * CP; idx += kWave)
             F(U(T.D, 0) + idx) = (idx % CP) < C ? 0.f : -INFINITY;
@@ -636,16 +644,32 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
                 }
                 if (right) {   // u_R = u_N (x) L
                     const int sl = uni(H(ly.info + vb0 + 2 * k)) & kSlotMask;
-                    vec_log<CP, false>(ly, uN, sl, uR, scr);
+                    const double zs = vec_log<CP, false>(ly, uN, sl, uR, scr);
+                    if (l == T.D && lane == 0) rootShift[0] = zs;
                 }
             } else if (right) {
                 if (lane < CP) F(uR + CP + lane) = F(vN + lane);
                 // v_L = R (x) v_N
                 const int sr = uni(H(ly.info + vb0 + 2 * k + 1)) & kSlotMask;
-                vec_log<CP, true>(ly, vN, sr, uL + CP, scr);
+                const double zs = vec_log<CP, true>(ly, vN, sr, uL + CP, scr);
+                if (l == T.D && lane == 0) rootShift[1] = zs;
             }
         }
         __syncthreads();
+        if (l == T.D) {
+            if (a.logZ && w == kSmallWaves - 1) {
+                const int uR = U(T.D - 1, 1), vL = U(T.D - 1, 0) + CP;
+                const float xb = lane < C ? F(uR + lane) + F(vL + lane) : -INFINITY;
+                const float m = wave_max_fast(xb);
+                const float s = wave_sum_fast(m == -INFINITY ? 0.f : fexp(xb - m));
+                lz = (m == -INFINITY) ? -INFINITY
+                                      : (float)(rootShift[0] + rootShift[1] + (double)(m + flog(s)));
+            }
+            if (!a.marg) {   // log Z only
+                store_logz();
+                return;
+            }
+        }
     }
     // ---- marginals with a per-edge normaliser n_t, from the leaves kept in LDS:
     // l[i][j] = ro[i] + co[j] + core[i][j].  Lane -> column j = lane & 31 and rows
@@ -885,8 +909,9 @@ __device__ __forceinline__ void small_max_body(const SmallMaxArgs& a, const int6
     // the last leaf in fp64 for levels >= 2 (read only after the level-1 barrier)
     for (int i = threadIdx.x; i < CC; i += kSmallThreads)
         Dd(ly.lastc + 2 * i) = (double)F(ly.leaves + (Eb - 1) * CC + i);
-    // ---- up-sweep: all threads share each level's products
-    for (int l = 1; l <= T.D; ++l) {
+    // ---- up-sweep: all threads share each level's products, below the root (the forward
+    // scores start from the root with zeros and only use its children's matrices)
+    for (int l = 1; l < T.D; ++l) {
         const int np = uni(T.products(l)), vb0 = uni(T.vbase[l - 1]), pb = uni(T.pbase[l]);
         if (l == 1) level_prod_max<true>(ly, Eb, np, vb0, pb);
         else level_prod_max<false>(ly, Eb, np, vb0, pb);
