@@ -96,7 +96,7 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, boo
                 p->v[l] = bump.take<float>(n * C);
             }
     } else {
-        for (int l = 1; l <= D; ++l) {
+        for (int l = 1; l < D; ++l) {   // the root's matrix is never formed
             const size_t n = (size_t)B * (size_t)(Np >> l);
             p->mnode[l] = bump.take<double>(n * C * C);
         }

@@ -49,7 +49,8 @@ struct Plan {
     // outside vectors of the nodes of levels 1..D-1 (normalised to max 0)
     float* u[kMaxLevels] = {};
     float* v[kMaxLevels] = {};
-    // max semiring (float64 nodes, levels 1..D) and forward vectors (levels 1..D-1)
+    // max semiring (float64 nodes, levels 1..D-1: the root matrix is never needed) and forward
+    // vectors (levels 1..D-1)
     double* mnode[kMaxLevels] = {};
     double* mu[kMaxLevels] = {};
     uint8_t* bp = nullptr;      // [B, E, C] backpointers

@@ -7,7 +7,7 @@
 // the tree's forward scores delta_t equal the sequential recursion's bit for bit and
 // every argmax decision (and tie) is the same whatever the association order.
 //
-//   up-sweep:   P[a][c] = max_b L[a][b] + R[b][c]              (nodes of levels 1..D)
+//   up-sweep:   P[a][c] = max_b L[a][b] + R[b][c]              (nodes of levels 1..D-1)
 //   down-sweep: u_L = u_N, u_R = u_N (x) L                     (forward scores only)
 //   leaves:     delta_t = u at edge t; bp_t[j] = lowest argmax_i delta_t[i] + l[t][i][j];
 //               the last edge also gives z_{L-1} = lowest argmax_j delta_{L-1}[j] and the score
@@ -435,7 +435,9 @@ hipError_t launch_viterbi_tree(const Plan& p, const float* pot, const int32_t* l
     const int64_t C = p.C;
     const int tmax = C <= kMT ? kMT : 2 * kMT;   // the narrow kernel below, 128-wide above
     const int ntm = (int)((C + tmax - 1) / tmax);
-    for (int l = 1; l <= p.D; ++l) {
+    // levels below the root: the forward scores start from the root with zeros and only
+    // read its children's matrices
+    for (int l = 1; l < p.D; ++l) {
         UpMaxArgs a{};
         a.leaves = (l == 1) ? pot : nullptr;
         a.cnode = (l == 1) ? nullptr : p.mnode[l - 1];
