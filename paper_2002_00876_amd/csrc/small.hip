@@ -672,37 +672,54 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
         }
     }
     // ---- marginals with a per-edge normaliser n_t, from the leaves kept in LDS:
-    // l[i][j] = ro[i] + co[j] + core[i][j].  Lane -> column j = lane & 31 and rows
-    // (lane >> 5) + 2q.
-    constexpr int kRows = CP / 2;
-    const int j = lane & 31, i0 = lane >> 5, jc = min(j, C - 1);
+    // l[i][j] = ro[i] + co[j] + core[i][j].  One wave per edge; lane l holds the entries
+    // v = l + 64 q of the row-major C x C edge (every lane busy, contiguous stores).  The
+    // edge's row terms alpha(i) + ro(i) and column terms beta(j) + co(j) go to the wave's
+    // scratch first; mu = exp(x - m) / s with m the maximum and s the sum.
+    constexpr int kF = (CP * CP + kWave - 1) / kWave;
+    const int di = kWave / C, dj = kWave - di * C;          // the step of 64 entries
+    const int i0 = lane / C, j0 = lane - i0 * C;
     for (int t = w; t < Eb; t += kSmallWaves) {
         const int al = U(0, t), be = al + CP;
         const int lc = Ly::core(t), lro = Ly::ro(t), lco = Ly::co(t);
-        const float bj = F(be + jc) + (float)Dd(lco + 2 * jc);
-        float x[kRows];
+        if (lane < C) {
+            F(scr + lane) = F(al + lane) + (float)Dd(lro + 2 * lane);
+            F(scr + 32 + lane) = F(be + lane) + (float)Dd(lco + 2 * lane);
+        }
+        wave_sync();
+        float x[kF];
         float m = -INFINITY;
+        int i = i0, jj = j0;
 #pragma unroll
-        for (int q = 0; q < kRows; ++q) {
-            const int i = i0 + 2 * q, ic = min(i, C - 1);
-            const float v = F(al + ic) + (float)Dd(lro + 2 * ic) + F(lc + ic * kLd + jc) + bj;
-            x[q] = (i < C && j < C) ? v : -INFINITY;
+        for (int q = 0; q < kF; ++q) {
+            const int ic = min(i, C - 1);
+            const float v = F(scr + ic) + F(scr + 32 + jj) + F(lc + ic * kLd + jj);
+            x[q] = lane + kWave * q < CC ? v : -INFINITY;
             m = fmaxf(m, x[q]);
+            jj += dj;
+            i += di;
+            const bool wrap = jj >= C;
+            jj -= wrap ? C : 0;
+            i += wrap ? 1 : 0;
         }
         m = wave_max_fast(m);
         float s = 0.f;
         if (m != -INFINITY) {
 #pragma unroll
-            for (int q = 0; q < kRows; ++q) s += fexp(x[q] - m);
+            for (int q = 0; q < kF; ++q) {
+                x[q] = fexp(x[q] - m);
+                s += x[q];
+            }
         }
         s = wave_sum_fast(s);
-        const float n = (m == -INFINITY) ? -INFINITY : m + flog(s);
+        const float inv = m == -INFINITY ? 0.f : 1.f / s;
         float* out = a.marg + ((size_t)b * E + t) * CC;
 #pragma unroll
-        for (int q = 0; q < kRows; ++q) {
-            const int i = i0 + 2 * q;
-            if (i < C && j < C) out[i * C + j] = (n == -INFINITY) ? 0.f : fexp(x[q] - n);
+        for (int q = 0; q < kF; ++q) {
+            const int v = lane + kWave * q;
+            if (v < CC) out[v] = m == -INFINITY ? 0.f : x[q] * inv;
         }
+        wave_sync();   // the scratch is rewritten for the wave's next edge
     }
     store_logz();
     zero_padding();
