@@ -765,23 +765,42 @@ __device__ __forceinline__ double mx(int base, int idx) {
     else return Dd(base + 2 * idx);
 }
 
-// All products of level l, P = L (x) R in (max, +), float64, by the whole workgroup: every
-// thread owns MR x MC output entries of one product (consecutive threads take consecutive
-// column tiles, so reads of R are contiguous across lanes and reads of L shared).  The
-// inner index q runs in batches of kB with every read of a batch issued together, then the
-// remainder; entries past C read neighbouring data and are not stored.  kLeaves: level 1
+// x of lane l ^ kXor within its quad of lanes (DPP quad permutation), float64
+template <int kXor>
+__device__ __forceinline__ double quad_xor_d(double x) {
+    constexpr int kCtrl = kXor == 1 ? 0xB1 : 0x4E;   // quad_perm [1,0,3,2] / [2,3,0,1]
+    const uint64_t u = __double_as_longlong(x);
+    const int lo = (int)(unsigned)u, hi = (int)(unsigned)(u >> 32);
+    const unsigned rlo = (unsigned)__builtin_amdgcn_update_dpp(lo, lo, kCtrl, 0xF, 0xF, false);
+    const unsigned rhi = (unsigned)__builtin_amdgcn_update_dpp(hi, hi, kCtrl, 0xF, 0xF, false);
+    return __longlong_as_double((long long)(((uint64_t)rhi << 32) | rlo));
+}
+
+// All products of level l, P = L (x) R in (max, +), float64, by the whole workgroup.  The
+// outputs of a product are cut into MR x MC tiles and each tile goes to a group of kS
+// consecutive lanes (kS = 2 or 4, inside one DPP quad): lane s of the group takes the
+// contraction indices q = s, s + kS, ... (clamped to C - 1: a repeated index leaves a max
+// unchanged), and the group's partial maxima are then combined by DPP.  A max is exact in
+// any order, so splitting q changes no bit of the result; it cuts the chain of dependent
+// maxima and lets larger register tiles (fewer LDS reads per pair) keep enough lanes busy.
+// Entries past C are computed from neighbouring data and not stored.  kLeaves: level 1
 // (fp32 leaves).
-template <int MR, int MC, bool kLeaves>
+template <int MR, int MC, int kS, bool kLeaves>
 __device__ void block_prod_max(const MaxLayout& ly, int E, int np, int vb0, int pbase) {
     using T = typename std::conditional<kLeaves, float, double>::type;
-    constexpr int kB = MR * MC >= 8 ? 2 : 4;   // q per batch
+    static_assert(kS == 2 || kS == 4, "the q split runs inside a DPP quad");
+    static_assert((MR * MC) % kS == 0, "every lane of a group stores the same count");
+    constexpr int kPer = MR * MC / kS;   // entries stored per lane
     const int C = ly.C, CC = ly.CC;
     const int TR = (C + MR - 1) / MR, TC = (C + MC - 1) / MC, tpp = TR * TC;
     const float invTpp = 1.f / (float)tpp, invTc = 1.f / (float)TC;
-    const int total = np * tpp;
+    const int nq = (C + kS - 1) / kS;
+    const int total = np * tpp * kS;   // lanes; a multiple of kS, and so is every stride
+    const int s = (int)(threadIdx.x % kS);
     const T* const nodes = reinterpret_cast<const T*>(ts_small_lds);   // element index
     double* const prod = reinterpret_cast<double*>(ts_small_lds) + ly.slots / 2;
-    for (int tile = threadIdx.x; tile < total; tile += kSmallThreads) {
+    for (int g = threadIdx.x; g < total; g += kSmallThreads) {
+        const int tile = g / kS;
         const int k = fdiv(tile, tpp, invTpp), rem = tile - k * tpp;
         const int tr = fdiv(rem, TC, invTc), tc = rem - tr * TC;
         const int sl = H(ly.info + vb0 + 2 * k) & kSlotMask, sr = H(ly.info + vb0 + 2 * k + 1) & kSlotMask;
@@ -789,64 +808,65 @@ __device__ void block_prod_max(const MaxLayout& ly, int E, int np, int vb0, int 
         const int lb = kLeaves ? ly.leaves + sl * CC : ly.node64(sl, E) / 2;
         const int rb = kLeaves ? ly.leaves + sr * CC : ly.node64(sr, E) / 2;
         const int r0 = tr * MR, c0 = tc * MC;
-        const T* lp = nodes + lb + r0 * C;   // L[r0 + i][q] = lp[i * C + q]
+        // rows past C repeat row C - 1 (MR - 1 rows could otherwise run past the operand);
+        // columns past C read at most MC - 1 entries beyond it, which stay inside the layout
+        int lrow[MR];
+#pragma unroll
+        for (int i = 0; i < MR; ++i) lrow[i] = lb + min(r0 + i, C - 1) * C;
         const T* rp = nodes + rb + c0;       // R[q][c0 + j] = rp[q * C + j]
-        double acc[MR][MC];
+        double acc[MR * MC];
 #pragma unroll
-        for (int i = 0; i < MR; ++i)
+        for (int e = 0; e < MR * MC; ++e) acc[e] = -INFINITY;
+        auto step = [&](int q) {
+            double av[MR], bv[MC];
 #pragma unroll
-            for (int j = 0; j < MC; ++j) acc[i][j] = -INFINITY;
-        int q = 0;
-        // unrolled by two so that a batch's reads can be issued while the previous one computes
-#pragma unroll 2
-        for (; q + kB <= C; q += kB) {
-            double av[kB][MR], bv[kB][MC];
+            for (int i = 0; i < MR; ++i) av[i] = (double)nodes[lrow[i] + q];
 #pragma unroll
-            for (int u = 0; u < kB; ++u) {
+            for (int j = 0; j < MC; ++j) bv[j] = (double)rp[q * C + j];
 #pragma unroll
-                for (int i = 0; i < MR; ++i) av[u][i] = (double)lp[i * C + u];
-                const T* ru = rp + u * C;
+            for (int i = 0; i < MR; ++i)
 #pragma unroll
-                for (int j = 0; j < MC; ++j) bv[u][j] = (double)ru[j];
-            }
-#pragma unroll
-            for (int u = 0; u < kB; ++u)
-#pragma unroll
-                for (int i = 0; i < MR; ++i)
-#pragma unroll
-                    for (int j = 0; j < MC; ++j) acc[i][j] = fmax(acc[i][j], av[u][i] + bv[u][j]);
-            lp += kB;
-            rp += kB * C;
+                for (int j = 0; j < MC; ++j) acc[i * MC + j] = fmax(acc[i * MC + j], av[i] + bv[j]);
+        };
+        int i = 0;
+        for (; i + 2 <= nq; i += 2) {   // two indices per trip: their reads go out together
+            step(min(s + kS * i, C - 1));
+            step(min(s + kS * (i + 1), C - 1));
         }
-        for (; q < C; ++q) {
+        if (i < nq) step(min(s + kS * i, C - 1));
 #pragma unroll
-            for (int i = 0; i < MR; ++i) {
-                const double av = (double)lp[i * C];
+        for (int e = 0; e < MR * MC; ++e) acc[e] = fmax(acc[e], quad_xor_d<1>(acc[e]));
+        if constexpr (kS == 4) {
 #pragma unroll
-                for (int j = 0; j < MC; ++j) acc[i][j] = fmax(acc[i][j], av + (double)rp[j]);
-            }
-            lp += 1;
-            rp += C;
+            for (int e = 0; e < MR * MC; ++e) acc[e] = fmax(acc[e], quad_xor_d<2>(acc[e]));
         }
+        // lane s stores the entries e = m * kS + s of the tile
         double* out = prod + (pbase + k) * CC;
 #pragma unroll
-        for (int i = 0; i < MR; ++i)
+        for (int m = 0; m < kPer; ++m) {
+            double v = acc[m * kS];
 #pragma unroll
-            for (int j = 0; j < MC; ++j)
-                if (r0 + i < C && c0 + j < C) out[(r0 + i) * C + c0 + j] = acc[i][j];
+            for (int u = 1; u < kS; ++u) v = s == u ? acc[m * kS + u] : v;
+            const int e = m * kS + s, r = r0 + e / MC, c = c0 + e % MC;
+            if (r < C && c < C) out[r * C + c] = v;
+        }
     }
 }
 
-// the smallest register tile that still gives every thread at most one tile (2 x 4 at
-// most: larger levels loop)
+// Tile shape and q split of a level: the largest tiles (fewest LDS reads per pair) that still
+// give at least six waves of lanes, at most one tile per lane; the widest level splits q in
+// two only.
 template <bool kLeaves>
 __device__ void level_prod_max(const MaxLayout& ly, int E, int np, int vb0, int pbase) {
     const int C = ly.C;
-    auto tiles = [&](int mr, int mc) { return np * ((C + mr - 1) / mr) * ((C + mc - 1) / mc); };
-    if (tiles(1, 1) <= kSmallThreads) block_prod_max<1, 1, kLeaves>(ly, E, np, vb0, pbase);
-    else if (tiles(1, 2) <= kSmallThreads) block_prod_max<1, 2, kLeaves>(ly, E, np, vb0, pbase);
-    else if (tiles(2, 2) <= kSmallThreads) block_prod_max<2, 2, kLeaves>(ly, E, np, vb0, pbase);
-    else block_prod_max<2, 4, kLeaves>(ly, E, np, vb0, pbase);
+    auto lanes = [&](int mr, int mc, int ks) {
+        return np * ((C + mr - 1) / mr) * ((C + mc - 1) / mc) * ks;
+    };
+    constexpr int kEnough = 6 * kWave;
+    if (lanes(4, 4, 4) > kSmallThreads) block_prod_max<4, 4, 2, kLeaves>(ly, E, np, vb0, pbase);
+    else if (lanes(4, 4, 4) >= kEnough) block_prod_max<4, 4, 4, kLeaves>(ly, E, np, vb0, pbase);
+    else if (lanes(2, 4, 4) >= kEnough) block_prod_max<2, 4, 4, kLeaves>(ly, E, np, vb0, pbase);
+    else block_prod_max<2, 2, 4, kLeaves>(ly, E, np, vb0, pbase);
 }
 
 __device__ __forceinline__ double xor32_max_d(double x) {
