@@ -161,12 +161,17 @@ __device__ __forceinline__ float lse_val(float m, float s) {
     return m == -INFINITY ? -INFINITY : m + flog(s);
 }
 
-// Blocks are dispatched round-robin over the 8 XCDs (block i -> XCD i % 8).  Renumber so
-// that logically consecutive blocks (the tiles of one node) share an XCD and its L2.
-// `nblocks` must be a multiple of 8.
-__device__ __forceinline__ int64_t xcd_swizzle(int64_t bid, int64_t nblocks) {
-    const int64_t per = nblocks >> 3;
-    return (bid & 7) * per + (bid >> 3);
+// Blocks are dispatched round-robin over the 8 XCDs (block i -> XCD i % 8).  Logical block
+// lid = node * ntiles + tile: the tiles of one node go to one XCD, one after another (they
+// share operand strips in that XCD's L2), and consecutive nodes go to consecutive XCDs, so
+// the work stays spread over all eight when only a prefix of each sequence's nodes is
+// present (variable lengths).  The grid must hold node_grid(nodes, ntiles) blocks; blocks
+// past the last node get lid >= nodes * ntiles.
+__device__ __forceinline__ int64_t xcd_node_swizzle(int64_t bid, int ntiles) {
+    const int64_t x = bid & 7, j = bid >> 3;
+    const int64_t ng = j / ntiles, tile = j - ng * ntiles;
+    return (ng * 8 + x) * ntiles + tile;
 }
+inline int64_t node_grid(int64_t nodes, int ntiles) { return (nodes + 7) / 8 * 8 * ntiles; }
 
 }  // namespace tsc

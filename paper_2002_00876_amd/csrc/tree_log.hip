@@ -27,7 +27,6 @@ constexpr float kUnderflow = 0x1p-80f;
 
 typedef float f16v __attribute__((ext_vector_type(16)));
 
-inline int64_t round8(int64_t x) { return (x + 7) / 8 * 8; }
 
 __device__ __forceinline__ size_t mat_off(int64_t b, int64_t k, int64_t nodes, int64_t C) {
     return (size_t)(b * nodes + k) * (size_t)C * (size_t)C;
@@ -146,7 +145,7 @@ struct UpLogArgs {
     int level;
     int ntile;            // tiles per matrix dimension
     int64_t nlogical;     // B * nodes * ntile^2
-    int64_t ngrid;        // nlogical rounded up to a multiple of 8
+    int64_t ngrid;        // node_grid(B * nodes, ntile^2)
 };
 
 template <int TM>
@@ -167,9 +166,9 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
     constexpr int BR = TM / 64;                 // 32 x 32 blocks per wave per dimension
     constexpr int QW = TM / 2;                  // a wave's quarter edge
     extern __shared__ __align__(16) float smem[];
-    const int64_t lid = xcd_swizzle(blockIdx.x, a.ngrid);
-    if (lid >= a.nlogical) return;
     const int ntiles = a.ntile * a.ntile;
+    const int64_t lid = xcd_node_swizzle(blockIdx.x, ntiles);
+    if (lid >= a.nlogical) return;
     const int tile = (int)(lid % ntiles);
     const int64_t node = lid / ntiles;
     const int64_t b = node / a.nodes, k = node % a.nodes;
@@ -859,7 +858,7 @@ hipError_t up_sweep_tm(const Plan& p, const float* pot, const int32_t* lengths, 
         a.lengths = lengths; a.B = p.B; a.N = p.N; a.C = p.C; a.level = l;
         a.ntile = p.ntile;
         a.nlogical = p.B * a.nodes * p.ntile * p.ntile;
-        a.ngrid = round8(a.nlogical);
+        a.ngrid = node_grid(p.B * a.nodes, p.ntile * p.ntile);
         hipLaunchKernelGGL((k_up_log<TM, VEC, kBits>), dim3((unsigned)a.ngrid), dim3(kUpThreads), lds, s, a);
         e = hipGetLastError();
         if (e != hipSuccess) return e;

@@ -49,9 +49,9 @@ __global__ __launch_bounds__(kMThreads) void k_up_max_narrow(UpMaxArgs a) {
     __shared__ __align__(16) double As[kMK][kMT + 2];   // As[k][row]; the padding spreads
                                                         // the transposing stores over banks
     __shared__ __align__(16) double Bs[kMK][kMT];       // Bs[k][col]
-    const int64_t lid = xcd_swizzle(blockIdx.x, a.ngrid);
-    if (lid >= a.nlogical) return;
     const int ntiles = a.ntm * a.ntm;
+    const int64_t lid = xcd_node_swizzle(blockIdx.x, ntiles);
+    if (lid >= a.nlogical) return;
     const int tile = (int)(lid % ntiles);
     const int64_t node = lid / ntiles;
     const int64_t b = node / a.nodes, k = node % a.nodes;
@@ -126,9 +126,9 @@ __global__ __launch_bounds__((TM / 8) * (TM / 8)) void k_up_max(UpMaxArgs a) {
     constexpr int NA = TM * KS / NT;   // staged values per thread and operand
     __shared__ __align__(16) double As[KS * LDA];
     __shared__ __align__(16) double Bs[KS * TM];
-    const int64_t lid = xcd_swizzle(blockIdx.x, a.ngrid);
-    if (lid >= a.nlogical) return;
     const int ntiles = a.ntm * a.ntm;
+    const int64_t lid = xcd_node_swizzle(blockIdx.x, ntiles);
+    if (lid >= a.nlogical) return;
     const int tile = (int)(lid % ntiles);
     const int64_t node = lid / ntiles;
     const int64_t b = node / a.nodes, k = node % a.nodes;
@@ -426,7 +426,6 @@ __global__ __launch_bounds__(64) void k_dec_emit(DecArgs a) {
     }
 }
 
-inline int64_t round8(int64_t x) { return (x + 7) / 8 * 8; }
 
 }  // namespace
 
@@ -446,7 +445,7 @@ hipError_t launch_viterbi_tree(const Plan& p, const float* pot, const int32_t* l
         a.nodes = p.Np >> l;
         a.lengths = lengths; a.B = p.B; a.N = p.N; a.C = C; a.level = l; a.ntm = ntm;
         a.nlogical = p.B * a.nodes * ntm * ntm;
-        a.ngrid = round8(a.nlogical);
+        a.ngrid = node_grid(p.B * a.nodes, ntm * ntm);
         if (tmax == kMT)
             hipLaunchKernelGGL(k_up_max_narrow, dim3((unsigned)a.ngrid), dim3(kMThreads), 0, s, a);
         else
