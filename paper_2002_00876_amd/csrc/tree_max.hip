@@ -14,6 +14,8 @@
 //   decode:     z_t = bp_t[z_{t+1}] by chunks: each chunk maps its end label to its start
 //               label for every possible end label; one short serial walk over chunks;
 //               each chunk then emits its labels.
+#include <type_traits>
+
 #include "device.h"
 #include "internal.h"
 
@@ -24,6 +26,7 @@ namespace {
 constexpr int kMT = 64;    // output tile edge
 constexpr int kMK = 32;    // k slice of the narrow kernel
 constexpr int kMThreads = 256;
+constexpr int64_t kFewTiles = 512;   // two 128-wide tiles per compute unit
 
 struct UpMaxArgs {
     const float* leaves;    // level 1 reads the potentials
@@ -37,14 +40,19 @@ struct UpMaxArgs {
     int64_t nlogical, ngrid;
 };
 
+// child entry (r, c) of child k of sequence b: a potential (kLeaf, level 1) or a float64 node
+template <bool kLeaf>
 __device__ __forceinline__ double child_at(const UpMaxArgs& a, int64_t b, int64_t k, int64_t r,
                                            int64_t c) {
     const size_t off = (size_t)(b * a.cnodes + k) * a.C * a.C + (size_t)(r * a.C + c);
-    return a.cnode ? a.cnode[off] : (double)a.leaves[off];
+    if constexpr (kLeaf) return (double)a.leaves[off];
+    else return a.cnode[off];
 }
 
-// One tree level of the max-plus up-sweep for C <= 64: a 64 x 64 output tile per workgroup of
-// 256 threads with 4 x 4 float64 outputs each (small register footprint, many waves).
+// One tree level of the max-plus up-sweep in 64 x 64 output tiles (C <= 64, and the levels
+// of larger C with few products): one tile per workgroup of 256 threads with 4 x 4 float64
+// outputs each (small register footprint, many waves).  kLeaf: level 1 (fp32 potentials).
+template <bool kLeaf>
 __global__ __launch_bounds__(kMThreads) void k_up_max_narrow(UpMaxArgs a) {
     __shared__ __align__(16) double As[kMK][kMT + 2];   // As[k][row]; the padding spreads
                                                         // the transposing stores over banks
@@ -67,7 +75,7 @@ __global__ __launch_bounds__(kMThreads) void k_up_max_narrow(UpMaxArgs a) {
     if (!right) {
         for (int idx = tid; idx < kMT * kMT; idx += kMThreads) {
             const int64_t r = a0 + idx / kMT, c = c0 + idx % kMT;
-            if (r < C && c < C) P[r * C + c] = child_at(a, b, 2 * k, r, c);
+            if (r < C && c < C) P[r * C + c] = child_at<kLeaf>(a, b, 2 * k, r, c);
         }
         return;
     }
@@ -77,16 +85,25 @@ __global__ __launch_bounds__(kMThreads) void k_up_max_narrow(UpMaxArgs a) {
     for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = -INFINITY;
+    constexpr int kPer = kMT * kMK / kMThreads;   // staged values per thread and operand
     for (int64_t k0 = 0; k0 < C; k0 += kMK) {
-        for (int idx = tid; idx < kMT * kMK; idx += kMThreads) {
+        // every load of the slice is issued before the first is used
+        double va[kPer], vb[kPer];
+#pragma unroll
+        for (int v = 0; v < kPer; ++v) {
+            const int idx = tid + v * kMThreads;
             const int r = idx / kMK, kk = idx % kMK;
             const int64_t row = a0 + r, kg = k0 + kk;
-            As[kk][r] = (row < C && kg < C) ? child_at(a, b, 2 * k, row, kg) : -INFINITY;
+            va[v] = (row < C && kg < C) ? child_at<kLeaf>(a, b, 2 * k, row, kg) : -INFINITY;
+            const int kb = idx / kMT, cc = idx % kMT;
+            const int64_t col = c0 + cc, kgb = k0 + kb;
+            vb[v] = (col < C && kgb < C) ? child_at<kLeaf>(a, b, 2 * k + 1, kgb, col) : -INFINITY;
         }
-        for (int idx = tid; idx < kMT * kMK; idx += kMThreads) {
-            const int kk = idx / kMT, cc = idx % kMT;
-            const int64_t col = c0 + cc, kg = k0 + kk;
-            Bs[kk][cc] = (col < C && kg < C) ? child_at(a, b, 2 * k + 1, kg, col) : -INFINITY;
+#pragma unroll
+        for (int v = 0; v < kPer; ++v) {
+            const int idx = tid + v * kMThreads;
+            As[idx % kMK][idx / kMK] = va[v];
+            Bs[idx / kMT][idx % kMT] = vb[v];
         }
         __syncthreads();
 #pragma unroll 4
@@ -119,8 +136,8 @@ __global__ __launch_bounds__(kMThreads) void k_up_max_narrow(UpMaxArgs a) {
 // in slices of KS: A is staged transposed, As[k][row] (rows padded to TM + 2 doubles, which
 // keeps the 16-byte operand reads aligned and spreads the transposing stores over the
 // banks), B as is, Bs[k][col]; the next slice's global loads are in flight while the current
-// one is used.
-template <int TM, int KS>
+// one is used (kLeaf: level 1, whose fp32 potentials are widened when they are staged).
+template <int TM, int KS, bool kLeaf>
 __global__ __launch_bounds__((TM / 8) * (TM / 8)) void k_up_max(UpMaxArgs a) {
     constexpr int TPD = TM / 8, NT = TPD * TPD, LDA = TM + 2;
     constexpr int NA = TM * KS / NT;   // staged values per thread and operand
@@ -144,14 +161,15 @@ __global__ __launch_bounds__((TM / 8) * (TM / 8)) void k_up_max(UpMaxArgs a) {
     if (!right) {
         for (int idx = tid; idx < TM * TM; idx += NT) {
             const int r = a0 + idx / TM, c = c0 + idx % TM;
-            if (r < C && c < C) P[(size_t)r * C + c] = child_at(a, b, 2 * k, r, c);
+            if (r < C && c < C) P[(size_t)r * C + c] = child_at<kLeaf>(a, b, 2 * k, r, c);
         }
         return;
     }
     const size_t lbase = (size_t)(b * a.cnodes + 2 * k) * C * C;
     const size_t rbase = lbase + (size_t)C * C;
-    auto at = [&](size_t off) { return a.cnode ? a.cnode[off] : (double)a.leaves[off]; };
-    double ra[NA], rb[NA];
+    using T = typename std::conditional<kLeaf, float, double>::type;
+    const T* src = kLeaf ? (const T*)a.leaves : (const T*)a.cnode;
+    T ra[NA], rb[NA];   // raw values: the widening waits until they are stored
     // staging of slice [k0, k0 + KS): thread value v of A is (row idx / KS, k idx % KS) with
     // idx = tid + v * NT (consecutive threads read consecutive k), of B (k idx / TM, col idx % TM)
     auto load = [&](int k0) {
@@ -159,17 +177,17 @@ __global__ __launch_bounds__((TM / 8) * (TM / 8)) void k_up_max(UpMaxArgs a) {
         for (int v = 0; v < NA; ++v) {
             const int idx = tid + v * NT;
             const int r = a0 + idx / KS, kk = k0 + idx % KS;
-            ra[v] = (r < C && kk < C) ? at(lbase + (size_t)r * C + kk) : -INFINITY;
+            ra[v] = (r < C && kk < C) ? src[lbase + (size_t)r * C + kk] : (T)-INFINITY;
             const int kr = k0 + idx / TM, c = c0 + idx % TM;
-            rb[v] = (kr < C && c < C) ? at(rbase + (size_t)kr * C + c) : -INFINITY;
+            rb[v] = (kr < C && c < C) ? src[rbase + (size_t)kr * C + c] : (T)-INFINITY;
         }
     };
     auto store = [&]() {
 #pragma unroll
         for (int v = 0; v < NA; ++v) {
             const int idx = tid + v * NT;
-            As[(idx % KS) * LDA + idx / KS] = ra[v];
-            Bs[idx] = rb[v];
+            As[(idx % KS) * LDA + idx / KS] = (double)ra[v];
+            Bs[idx] = (double)rb[v];
         }
     };
     const int ty = tid / TPD, tx = tid % TPD;
@@ -432,11 +450,16 @@ __global__ __launch_bounds__(64) void k_dec_emit(DecArgs a) {
 hipError_t launch_viterbi_tree(const Plan& p, const float* pot, const int32_t* lengths,
                                int32_t* path, float* score, hipStream_t s) {
     const int64_t C = p.C;
-    const int tmax = C <= kMT ? kMT : 2 * kMT;   // the narrow kernel below, 128-wide above
-    const int ntm = (int)((C + tmax - 1) / tmax);
     // levels below the root: the forward scores start from the root with zeros and only
     // read its children's matrices
     for (int l = 1; l < p.D; ++l) {
+        // 128-wide tiles above C = 64, unless a level has too few of them to give every
+        // compute unit a workgroup: then the narrow kernel's 64-wide tiles (a quarter of the
+        // work each, so four times the workgroups and a quarter of the latency)
+        const int64_t wide = (C + 2 * kMT - 1) / (2 * kMT);
+        const bool narrow = C <= kMT || p.B * (p.Np >> l) * wide * wide < kFewTiles;
+        const int tmax = narrow ? kMT : 2 * kMT;
+        const int ntm = (int)((C + tmax - 1) / tmax);
         UpMaxArgs a{};
         a.leaves = (l == 1) ? pot : nullptr;
         a.cnode = (l == 1) ? nullptr : p.mnode[l - 1];
@@ -446,10 +469,14 @@ hipError_t launch_viterbi_tree(const Plan& p, const float* pot, const int32_t* l
         a.lengths = lengths; a.B = p.B; a.N = p.N; a.C = C; a.level = l; a.ntm = ntm;
         a.nlogical = p.B * a.nodes * ntm * ntm;
         a.ngrid = node_grid(p.B * a.nodes, ntm * ntm);
-        if (tmax == kMT)
-            hipLaunchKernelGGL(k_up_max_narrow, dim3((unsigned)a.ngrid), dim3(kMThreads), 0, s, a);
+        if (narrow && l == 1)
+            hipLaunchKernelGGL(k_up_max_narrow<true>, dim3((unsigned)a.ngrid), dim3(kMThreads), 0, s, a);
+        else if (narrow)
+            hipLaunchKernelGGL(k_up_max_narrow<false>, dim3((unsigned)a.ngrid), dim3(kMThreads), 0, s, a);
+        else if (l == 1)
+            hipLaunchKernelGGL((k_up_max<2 * kMT, 16, true>), dim3((unsigned)a.ngrid), dim3(256), 0, s, a);
         else
-            hipLaunchKernelGGL((k_up_max<2 * kMT, 16>), dim3((unsigned)a.ngrid), dim3(256), 0, s, a);
+            hipLaunchKernelGGL((k_up_max<2 * kMT, 16, false>), dim3((unsigned)a.ngrid), dim3(256), 0, s, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
