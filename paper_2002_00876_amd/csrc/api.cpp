@@ -72,14 +72,15 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, boo
     p->Np = Np; p->D = D;
     Bump bump{static_cast<char*>(base)};
     if (op == TS_OP_LOGPARTITION || op == TS_OP_MARGINALS) {
-        p->ntile = (int)((C + up_tile(C) - 1) / up_tile(C));
         for (int l = 1; l <= D; ++l) {
             const size_t n = (size_t)B * (size_t)(Np >> l);
+            const int tm = up_tile(C, (int64_t)n);
+            p->ntile[l] = (int)((C + tm - 1) / tm);
             p->core[l] = bump.take<float>(n * C * C);
             p->ro[l] = bump.take<double>(n * C);
             p->co[l] = bump.take<double>(n * C);
-            p->pmr[l] = bump.take<float>(n * C * p->ntile);
-            p->pmc[l] = bump.take<float>(n * C * p->ntile);
+            p->pmr[l] = bump.take<float>(n * C * p->ntile[l]);
+            p->pmc[l] = bump.take<float>(n * C * p->ntile[l]);
         }
         p->lrmax = bump.take<float>((size_t)B * p->E * C);
         p->lcmax = bump.take<float>((size_t)B * p->E * C);

@@ -31,7 +31,7 @@ struct Plan {
     double* ro[kMaxLevels] = {};
     double* co[kMaxLevels] = {};
     // per-tile partial maxima of the rows (core + co) and columns (core + ro) of every node
-    // of levels 1..D, [nodes][C][ntile]: the exp shifts of the next level's products; and
+    // of levels 1..D, [nodes][C][ntile[l]]: the exp shifts of the next level's products; and
     // the leaves' row and column maxima [B, E, C]
     float* pmr[kMaxLevels] = {};
     float* pmc[kMaxLevels] = {};
@@ -45,7 +45,7 @@ struct Plan {
     uint64_t* rbits[kMaxLevels] = {};
     uint64_t* cbits[kMaxLevels] = {};
     int bw = 1;                 // 64-bit words per line: ceil(C / 64)
-    int ntile = 1;              // output tiles per matrix dimension (up_tile)
+    int ntile[kMaxLevels] = {}; // output tiles per matrix dimension of each level (up_tile)
     // outside vectors of the nodes of levels 1..D-1 (normalised to max 0)
     float* u[kMaxLevels] = {};
     float* v[kMaxLevels] = {};
@@ -62,8 +62,15 @@ struct Plan {
     size_t bytes = 0;
 };
 
-// Output tile edge of the log-semiring up-sweep for C labels.
-inline int up_tile(int64_t C) { return C <= 64 ? 64 : 128; }
+// Output tile edge of a level of the log-semiring up-sweep with `nodes` nodes (all
+// sequences) of C labels: 64 for C <= 64; 128 above, unless the level has too few 128-wide
+// tiles to give every compute unit two of them: then 64 (four times the workgroups, each
+// with a quarter of the work and of the latency).
+inline int up_tile(int64_t C, int64_t nodes) {
+    if (C <= 64) return 64;
+    const int64_t t = (C + 127) / 128;
+    return nodes * t * t < 512 ? 64 : 128;
+}
 
 // Fills the plan; with base == nullptr only sizes are computed.  Returns false on overflow.
 // masks: keep finiteness bitmasks of the log-semiring nodes (inputs with many structural

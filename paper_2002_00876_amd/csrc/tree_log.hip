@@ -192,8 +192,7 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
     const bool right = (2 * k + 1) * half < Eb;
     if (!right) {
         // the right half is padding: the node equals its left child (tile, offsets and
-        // the partial maxima, re-tiled: a child with one partial per line keeps it in
-        // partial 0)
+        // the partial maxima, re-tiled)
         for (int idx = tid; idx < TM * TM; idx += kUpThreads) {
             const int r = a0 + idx / TM, c = c0 + idx % TM;
             if (r < C && c < C) Pc[(size_t)r * C + c] = Lc[(size_t)r * C + c];
@@ -206,11 +205,18 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
                 if (c0 + i < C) Pco[c0 + i] = a.cco ? a.cco[(size_t)cl * C + c0 + i] : 0.0;
         if (tm == 0 && tn == 0)
             for (int i = tid; i < C * nt; i += kUpThreads) {
+                // only the maximum over a line's partials is ever read: partial 0 takes it
                 const int line = i / nt, p = i % nt;
                 const float* sr = a.cpmr + ((size_t)cl * C + line) * cnt;
                 const float* sc = a.cpmc + ((size_t)cl * C + line) * cnt;
-                Pmr[i] = p < cnt ? sr[p] : -INFINITY;
-                Pmc[i] = p < cnt ? sc[p] : -INFINITY;
+                float mr = -INFINITY, mc = -INFINITY;
+                if (p == 0)
+                    for (int q = 0; q < cnt; ++q) {
+                        mr = fmaxf(mr, sr[q]);
+                        mc = fmaxf(mc, sc[q]);
+                    }
+                Pmr[i] = mr;
+                Pmc[i] = mc;
             }
         if (kBits && tm == 0 && tn == 0 && a.rbits)
             for (int i = tid; i < C * a.bw; i += kUpThreads) {
@@ -824,19 +830,27 @@ __global__ __launch_bounds__(kVecThreads) void k_form_log(FormArgs a) {
 }
 
 template <int TM, bool VEC, bool kBits>
-hipError_t up_sweep_tm(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
-    constexpr size_t lds = UpSmem<TM>::kBytes;
+hipError_t allow_up_lds() {
     static bool attr_set = false;
     if (!attr_set) {
         hipError_t e = hipFuncSetAttribute((const void*)k_up_log<TM, VEC, kBits>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)UpSmem<TM>::kBytes);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
+    return hipSuccess;
+}
+
+template <bool VEC, bool kBits>
+hipError_t up_sweep_vec(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
+    hipError_t e = allow_up_lds<64, VEC, kBits>();
+    if (e == hipSuccess && p.C > 64) e = allow_up_lds<128, VEC, kBits>();
+    if (e != hipSuccess) return e;
     // the leaves' row and column maxima (shifts of the level-1 products)
     LeafMaxArgs m{pot, lengths, p.N, p.C, p.lrmax, p.lcmax, p.rbits[0], p.cbits[0], p.bw};
     hipLaunchKernelGGL((k_leaf_max<VEC, kBits>), dim3((unsigned)(p.B * p.E)), dim3(256), 0, s, m);
-    hipError_t e = hipGetLastError();
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
     for (int l = 1; l <= p.D; ++l) {
         UpLogArgs a{};
@@ -846,7 +860,7 @@ hipError_t up_sweep_tm(const Plan& p, const float* pot, const int32_t* lengths, 
         } else {
             a.ccore = p.core[l - 1]; a.cro = p.ro[l - 1]; a.cco = p.co[l - 1];
             a.cnodes = p.Np >> (l - 1);
-            a.cpmr = p.pmr[l - 1]; a.cpmc = p.pmc[l - 1]; a.cntile = p.ntile;
+            a.cpmr = p.pmr[l - 1]; a.cpmc = p.pmc[l - 1]; a.cntile = p.ntile[l - 1];
         }
         a.core = p.core[l]; a.ro = p.ro[l]; a.co = p.co[l];
         a.pmr = p.pmr[l]; a.pmc = p.pmc[l];
@@ -856,10 +870,16 @@ hipError_t up_sweep_tm(const Plan& p, const float* pot, const int32_t* lengths, 
         a.bw = p.bw;
         a.nodes = p.Np >> l;
         a.lengths = lengths; a.B = p.B; a.N = p.N; a.C = p.C; a.level = l;
-        a.ntile = p.ntile;
-        a.nlogical = p.B * a.nodes * p.ntile * p.ntile;
-        a.ngrid = node_grid(p.B * a.nodes, p.ntile * p.ntile);
-        hipLaunchKernelGGL((k_up_log<TM, VEC, kBits>), dim3((unsigned)a.ngrid), dim3(kUpThreads), lds, s, a);
+        const int nt = p.ntile[l];
+        a.ntile = nt;
+        a.nlogical = p.B * a.nodes * nt * nt;
+        a.ngrid = node_grid(p.B * a.nodes, nt * nt);
+        if (up_tile(p.C, p.B * a.nodes) == 64)
+            hipLaunchKernelGGL((k_up_log<64, VEC, kBits>), dim3((unsigned)a.ngrid), dim3(kUpThreads),
+                               UpSmem<64>::kBytes, s, a);
+        else
+            hipLaunchKernelGGL((k_up_log<128, VEC, kBits>), dim3((unsigned)a.ngrid), dim3(kUpThreads),
+                               UpSmem<128>::kBytes, s, a);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -868,12 +888,8 @@ hipError_t up_sweep_tm(const Plan& p, const float* pot, const int32_t* lengths, 
 
 template <bool kBits>
 hipError_t up_sweep_bits(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
-    const bool vec = (p.C % 4) == 0;
-    if (up_tile(p.C) == 64)
-        return vec ? up_sweep_tm<64, true, kBits>(p, pot, lengths, s)
-                   : up_sweep_tm<64, false, kBits>(p, pot, lengths, s);
-    return vec ? up_sweep_tm<128, true, kBits>(p, pot, lengths, s)
-               : up_sweep_tm<128, false, kBits>(p, pot, lengths, s);
+    return (p.C % 4) == 0 ? up_sweep_vec<true, kBits>(p, pot, lengths, s)
+                          : up_sweep_vec<false, kBits>(p, pot, lengths, s);
 }
 
 hipError_t up_sweep(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
