@@ -430,35 +430,56 @@ __device__ __forceinline__ void prod_log(const LogLayout<CP>& ly, int sl, int sr
 // the NONE leaf of a one-edge sequence) and whose shift it records as ro (LEFT) or co
 // (RIGHT); the other offset is 0.  Lines C..CP-1 and entries C..CP-1 of a line are -inf,
 // so a leaf's whole padding is -inf.
-template <int CP>
-__device__ void normalise_leaves(const LogLayout<CP>& ly, int raw, int E) {
+//
+// Leaves normalised by rows (the even ones but a last leaf without a sibling) take the
+// first half of the workgroup, leaves normalised by columns (the odd ones and that last
+// leaf) the second half, so every wave runs one of the two forms with its strides known at
+// compile time.
+template <int CP, bool kCols>
+__device__ __forceinline__ void normalise_line(const LogLayout<CP>& ly, int raw, int E, int t,
+                                               int r) {
     using Ly = LogLayout<CP>;
     constexpr int kLd = Ly::kLd;
     const int C = ly.C, CC = C * C;
-    for (int i = threadIdx.x; i < E * CP; i += kSmallThreads) {
-        const int t = i / CP, r = i - t * CP;
-        const int role = role_of(E, 0, t);
-        const bool col = role == kRight, pad = r >= C;
-        const int rc = min(r, C - 1);
-        const int line = raw + t * CC + (col ? rc : rc * C);
-        const int stride = col ? C : 1;
-        float v[CP];
+    const bool pad = r >= C;
+    const int rc = min(r, C - 1);
+    // entries past C repeat entry C - 1: the maximum is unchanged, and their stores are
+    // overwritten with -inf below (no per-entry masks)
+    float v[CP];
+    const int line = raw + t * CC + (kCols ? rc : rc * C);
 #pragma unroll
-        for (int j = 0; j < CP; ++j) v[j] = F(line + min(j, C - 1) * stride);
-        float m = -INFINITY;
+    for (int q = 0; q < CP; ++q) v[q] = F(line + min(q, C - 1) * (kCols ? C : 1));
+    float m = v[0];
 #pragma unroll
-        for (int j = 0; j < CP; ++j) {
-            v[j] = (j < C && !pad) ? v[j] : -INFINITY;
-            m = fmaxf(m, v[j]);
+    for (int q = 1; q < CP; ++q) m = fmaxf(m, v[q]);
+    const bool none = !kCols && E == 1;   // the root of a one-edge tree keeps its values
+    const float sh = none ? 0.f : safe_shift(m);
+    constexpr int kStep = kCols ? kLd : 1;
+    const int base = Ly::core(t) + (kCols ? r : r * kLd);
+#pragma unroll
+    for (int q = 0; q < CP; ++q) F(base + q * kStep) = pad ? -INFINITY : v[q] - sh;
+    for (int q = C; q < CP; ++q) F(base + q * kStep) = -INFINITY;
+    const int ro = Ly::ro(t), co = Ly::co(t);
+    Dd((kCols ? co : ro) + 2 * r) = pad ? -INFINITY : (double)sh;
+    Dd((kCols ? ro : co) + 2 * r) = pad ? -INFINITY : 0.0;
+}
+
+template <int CP>
+__device__ void normalise_leaves(const LogLayout<CP>& ly, int raw, int E) {
+    constexpr int kHalf = kSmallThreads / 2;
+    const int nCols = E / 2 + ((E & 1) && E > 1 ? 1 : 0);   // odd leaves + a lone last leaf
+    const int nRows = E - nCols;
+    const int tid = (int)threadIdx.x;
+    if (tid < kHalf) {
+        for (int i = tid; i < nRows * CP; i += kHalf) {
+            const int q = i / CP;
+            normalise_line<CP, false>(ly, raw, E, 2 * q, i - q * CP);
         }
-        const float sh = role == kNone ? 0.f : safe_shift(m);
-        const int base = Ly::core(t) + (col ? r : r * kLd);
-        const int step = col ? kLd : 1;
-#pragma unroll
-        for (int j = 0; j < CP; ++j) F(base + j * step) = v[j] - sh;
-        const int ro = Ly::ro(t), co = Ly::co(t);
-        Dd((col ? co : ro) + 2 * r) = pad ? -INFINITY : (double)sh;
-        Dd((col ? ro : co) + 2 * r) = pad ? -INFINITY : 0.0;
+    } else {
+        for (int i = tid - kHalf; i < nCols * CP; i += kHalf) {
+            const int q = i / CP;
+            normalise_line<CP, true>(ly, raw, E, min(2 * q + 1, E - 1), i - q * CP);
+        }
     }
 }
 
