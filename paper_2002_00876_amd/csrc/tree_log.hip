@@ -154,8 +154,8 @@ struct UpSmem {
     static constexpr int kBuf = TM * LDA + kSlice * LDB;          // one A + B slice
     static constexpr int kTileF = TM * LDT;                       // epilogue tile
     static constexpr int kMain = (2 * kBuf > kTileF ? 2 * kBuf : kTileF);
-    // coh, roh [kMaxLabels]; sa, sb, cof, rof [TM]; red [4 doubles]
-    static constexpr int kFloats = kMain + 2 * kMaxLabels + 4 * TM + 8;
+    // coh, roh [kMaxLabels]; sa, sb, cof, rof [TM]; red [2 doubles per wave]
+    static constexpr int kFloats = kMain + 2 * kMaxLabels + 4 * TM + 4 * (kUpThreads / kWave);
     static constexpr size_t kBytes = sizeof(float) * kFloats;
 };
 
@@ -239,36 +239,6 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
     float* rof = cof + TM;               // [TM] ro_P of the tile's rows (float)
     double* red = reinterpret_cast<double*>(rof + TM);
 
-    // ---- offsets of the contracted index, shifted to max 0, and the tile's shifts
-    double lmax = -INFINITY, rmax = -INFINITY;
-    for (int i = tid; i < C; i += kUpThreads) {
-        if (Lco) lmax = fmax(lmax, Lco[i]);
-        if (Rro) rmax = fmax(rmax, Rro[i]);
-    }
-    const double coLshift = Lco ? safe_shift_d(block_max_d(lmax, red)) : 0.0;
-    const double roRshift = Rro ? safe_shift_d(block_max_d(rmax, red)) : 0.0;
-    for (int i = tid; i < C; i += kUpThreads) {
-        coh[i] = Lco ? (float)(Lco[i] - coLshift) : 0.f;
-        roh[i] = Rro ? (float)(Rro[i] - roRshift) : 0.f;
-    }
-    for (int i = tid; i < TM; i += kUpThreads) {
-        float m = -INFINITY;
-        if (a0 + i < C) {
-            const float* p = a.cpmr + ((size_t)cl * C + a0 + i) * cnt;
-            for (int q = 0; q < cnt; ++q) m = fmaxf(m, p[q]);
-            m -= (float)coLshift;
-        }
-        sa[i] = safe_shift(m);
-        float n = -INFINITY;
-        if (c0 + i < C) {
-            const float* p = a.cpmc + ((size_t)cr * C + c0 + i) * cnt;
-            for (int q = 0; q < cnt; ++q) n = fmaxf(n, p[q]);
-            n -= (float)roRshift;
-        }
-        sb[i] = safe_shift(n);
-    }
-    __syncthreads();
-
     // ---- staging of one slice [ks, ks + 32) of A'' (TM x 32) and B'' (32 x TM): the
     // loads of the next slice are issued before the current slice's products
     constexpr int GA = kSlice / 4, NA = TM * GA / kUpThreads;   // float4 groups per thread
@@ -335,6 +305,50 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
         }
     };
 
+    // ---- offsets of the contracted index, shifted to max 0, and the tile's shifts.  Every
+    // global read of this part goes out at once, together with the first slice (whose
+    // exponentials are the first use of the shifts): one memory round trip before the loop.
+    load(0);
+    static_assert(kMaxLabels <= kUpThreads, "one offset of the contracted index per thread");
+    const double lco = (Lco && tid < C) ? Lco[tid] : -INFINITY;
+    const double rro = (Rro && tid < C) ? Rro[tid] : -INFINITY;
+    float pa = -INFINITY, pb = -INFINITY;   // maxima of the partials of row a0 + tid, column c0 + tid
+    if (tid < TM && a0 + tid < C) {
+        const float* p = a.cpmr + ((size_t)cl * C + a0 + tid) * cnt;
+        for (int q = 0; q < cnt; ++q) pa = fmaxf(pa, p[q]);
+    }
+    if (tid < TM && c0 + tid < C) {
+        const float* p = a.cpmc + ((size_t)cr * C + c0 + tid) * cnt;
+        for (int q = 0; q < cnt; ++q) pb = fmaxf(pb, p[q]);
+    }
+    // both maxima in one block reduction
+    {
+        const double lw = wave_max_d(lco), rw = wave_max_d(rro);
+        const int w = tid / kWave;
+        if ((tid & (kWave - 1)) == 0) {
+            red[2 * w] = lw;
+            red[2 * w + 1] = rw;
+        }
+    }
+    __syncthreads();
+    double lmax = red[0], rmax = red[1];
+#pragma unroll
+    for (int w = 1; w < kUpThreads / kWave; ++w) {
+        lmax = fmax(lmax, red[2 * w]);
+        rmax = fmax(rmax, red[2 * w + 1]);
+    }
+    const double coLshift = Lco ? safe_shift_d(lmax) : 0.0;
+    const double roRshift = Rro ? safe_shift_d(rmax) : 0.0;
+    if (tid < C) {
+        coh[tid] = Lco ? (float)(lco - coLshift) : 0.f;
+        roh[tid] = Rro ? (float)(rro - roRshift) : 0.f;
+    }
+    if (tid < TM) {
+        sa[tid] = safe_shift(a0 + tid < C ? pa - (float)coLshift : -INFINITY);
+        sb[tid] = safe_shift(c0 + tid < C ? pb - (float)roRshift : -INFINITY);
+    }
+    __syncthreads();
+
     // ---- products: wave (wm, wn) owns rows wm*QW.., columns wn*QW.. as BR x BR blocks.
     // Within each 8-wide k step lanes 0-31 contribute k..k+3 and lanes 32-63 k+4..k+7 (one
     // 16-byte LDS read of A per block row); B uses the same k assignment.
@@ -348,8 +362,7 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
     const int nslices = (C + kSlice - 1) / kSlice;
-    load(0);
-    store(0, 0);
+    store(0, 0);   // (slice 0 was loaded before the shifts)
     __syncthreads();
     for (int s = 0; s < nslices; ++s) {
         const int buf = s & 1;
