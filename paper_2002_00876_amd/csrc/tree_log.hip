@@ -274,11 +274,14 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
             }
         }
     };
-    auto store = [&](int ks, int buf) {
+    // the staged groups of one part: parts p of P take the A groups [p NA / P, (p+1) NA / P)
+    // and the B groups likewise, so the exponentials of a slice can be spread over the
+    // product steps of the previous one
+    auto store_part = [&](int ks, int buf, int part, int nparts) {
         float* As = smem + buf * Sm::kBuf;
         float* Bs = As + TM * LDA;
 #pragma unroll
-        for (int it = 0; it < NA; ++it) {
+        for (int it = part * NA / nparts; it < (part + 1) * NA / nparts; ++it) {
             const int idx = tid + it * kUpThreads;
             const int r = idx / GA, cl4 = 4 * (idx % GA), col = ks + cl4;
             const bool rok = a0 + r < C;
@@ -291,7 +294,7 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
             *(float4*)(As + r * LDA + cl4) = x;
         }
 #pragma unroll
-        for (int it = 0; it < NB; ++it) {
+        for (int it = part * NB / nparts; it < (part + 1) * NB / nparts; ++it) {
             const int idx = tid + it * kUpThreads;
             const int kr = idx / GB, cl4 = 4 * (idx % GB), kk = ks + kr, col = c0 + cl4;
             const bool kok = kk < C;
@@ -304,6 +307,7 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
             *(float4*)(Bs + kr * LDB + cl4) = x;
         }
     };
+    auto store = [&](int ks, int buf) { store_part(ks, buf, 0, 1); };
 
     // ---- offsets of the contracted index, shifted to max 0, and the tile's shifts.  Every
     // global read of this part goes out at once, together with the first slice (whose
@@ -373,6 +377,10 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
         const float* bp = Bs + (4 * (lane >> 5)) * LDB + wn * QW + (lane & 31);
 #pragma unroll
         for (int kk = 0; kk < kSlice; kk += 8) {
+            // the second half of the slice's steps carries the next slice's exponentials
+            // (its loads have had the first half to arrive); they issue while the products run
+            if (kk >= kSlice / 2 && s + 1 < nslices)
+                store_part((s + 1) * kSlice, buf ^ 1, (kk - kSlice / 2) / 8, kSlice / 16);
             float4 av[BR];
             float bv[BR][4];
 #pragma unroll
@@ -391,7 +399,6 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i].w, bv[j][3], acc[i][j], 0, 0, 0);
                 }
         }
-        if (s + 1 < nslices) store((s + 1) * kSlice, buf ^ 1);
         __syncthreads();
     }
 
@@ -458,18 +465,27 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
     __syncthreads();
     // partial maxima for the next level: thread t < TM row t, TM <= t < 2 TM column t - TM
     const int nr = min(TM, C - a0), nc = min(TM, C - c0);
+    // (four running maxima per line: a short dependency chain)
     if (tid < TM) {
         if (tid < nr) {
-            float m = -INFINITY;
-            for (int c = 0; c < nc; ++c) m = fmaxf(m, T[tid * LDT + c] + cof[c]);
-            Pmr[(size_t)(a0 + tid) * nt + tn] = m;
+            float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+            int c = 0;
+            for (; c + 4 <= nc; c += 4)
+#pragma unroll
+                for (int u = 0; u < 4; ++u) m[u] = fmaxf(m[u], T[tid * LDT + c + u] + cof[c + u]);
+            for (; c < nc; ++c) m[0] = fmaxf(m[0], T[tid * LDT + c] + cof[c]);
+            Pmr[(size_t)(a0 + tid) * nt + tn] = fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3]));
         }
     } else if (tid < 2 * TM) {
         const int c = tid - TM;
         if (c < nc) {
-            float m = -INFINITY;
-            for (int r = 0; r < nr; ++r) m = fmaxf(m, T[r * LDT + c] + rof[r]);
-            Pmc[(size_t)(c0 + c) * nt + tm] = m;
+            float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+            int r = 0;
+            for (; r + 4 <= nr; r += 4)
+#pragma unroll
+                for (int u = 0; u < 4; ++u) m[u] = fmaxf(m[u], T[(r + u) * LDT + c] + rof[r + u]);
+            for (; r < nr; ++r) m[0] = fmaxf(m[0], T[r * LDT + c] + rof[r]);
+            Pmc[(size_t)(c0 + c) * nt + tm] = fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3]));
         }
     }
     // the finiteness bitmasks of the tile's rows (the words of its columns) and columns.
@@ -496,10 +512,23 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
                 if (w0 + q < a.bw) out[q] = bits[q];
         }
     }
-    // the tile, row by row
-    for (int idx = tid; idx < nr * TM; idx += kUpThreads) {
-        const int r = idx / TM, c = idx % TM;
-        if (c < nc) Pc[(size_t)(a0 + r) * C + c0 + c] = T[r * LDT + c];
+    // the tile, row by row (16-byte stores when C is a multiple of 4: tiles then start and
+    // end on multiples of 4 columns)
+    if (VEC) {
+        constexpr int kQ = TM / 4;
+        const int nc4 = nc / 4;
+        for (int idx = tid; idx < nr * kQ; idx += kUpThreads) {
+            const int r = idx / kQ, c4 = idx % kQ;
+            if (c4 < nc4) {
+                const float* t = T + r * LDT + 4 * c4;
+                *(float4*)(Pc + (size_t)(a0 + r) * C + c0 + 4 * c4) = make_float4(t[0], t[1], t[2], t[3]);
+            }
+        }
+    } else {
+        for (int idx = tid; idx < nr * TM; idx += kUpThreads) {
+            const int r = idx / TM, c = idx % TM;
+            if (c < nc) Pc[(size_t)(a0 + r) * C + c0 + c] = T[r * LDT + c];
+        }
     }
 }
 
