@@ -225,14 +225,27 @@ __global__ __launch_bounds__((TM / 8) * (TM / 8)) void k_up_max(UpMaxArgs a) {
             __syncthreads();
         }
     }
+    // a lane's eight columns of a row are contiguous: 16-byte stores when they all lie inside
+    // the matrix and start on a 16-byte boundary (even C), single stores at the edges
+    const int cb = c0 + tx * 8;
+    const bool wide = cb + 8 <= C && (C % 2) == 0;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         const int r = a0 + ty * 8 + i;
         if (r >= C) continue;
+        double* row = P + (size_t)r * C + cb;
+        if (wide) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int c = c0 + tx * 8 + j;
-            if (c < C) P[(size_t)r * C + c] = acc[i][j];
+            for (int j = 0; j < 8; j += 2) {
+                double2 v;
+                v.x = acc[i][j];
+                v.y = acc[i][j + 1];
+                *(double2*)(row + j) = v;
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (cb + j < C) row[j] = acc[i][j];
         }
     }
 }
