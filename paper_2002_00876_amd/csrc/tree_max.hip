@@ -121,13 +121,28 @@ __global__ __launch_bounds__(kMThreads) void k_up_max_narrow(UpMaxArgs a) {
         }
         __syncthreads();
     }
+    // 16-byte stores of a lane's four columns when they lie inside the matrix (even C)
+    const int64_t cb = c0 + tx * 4;
+    const bool wide = cb + 4 <= C && (C % 2) == 0;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i) {
+        const int64_t r = a0 + ty * 4 + i;
+        if (r >= C) continue;
+        double* row = P + r * C + cb;
+        if (wide) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t r = a0 + ty * 4 + i, c = c0 + tx * 4 + j;
-            if (r < C && c < C) P[r * C + c] = acc[i][j];
+            for (int j = 0; j < 4; j += 2) {
+                double2 v;
+                v.x = acc[i][j];
+                v.y = acc[i][j + 1];
+                *(double2*)(row + j) = v;
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (cb + j < C) row[j] = acc[i][j];
         }
+    }
 }
 
 // One tree level of the max-plus up-sweep, P[a][c] = max_b L[a][b] + R[b][c], for one TM x TM
