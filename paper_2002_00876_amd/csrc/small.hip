@@ -642,57 +642,7 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
     // children L and R, log Z = LSE_{a,c} (L (x) R)[a][c] = LSE_b u_R[b] + v_L[b], where
     // u_R = 0 (x) L and v_L = R (x) 0 are the first level's outside vectors; their shifts
     // are kept in rootShift.
-    __shared__ double rootShift[2];
-    if (w == 0)
-        for (int idx = lane; idx < 2 * CP; idx += kWave)
-            F(U(T.D, 0) + idx) = (idx % CP) < C ? 0.f : -INFINITY;
-    __syncthreads();
-    const int scr = ly.scr + w * 64;
-    for (int l = T.D; l >= 1; --l) {
-        const int nn = uni(T.n[l]), nprev = uni(T.n[l - 1]), vb0 = uni(T.vbase[l - 1]);
-        const int ub = uni(U(l, 0)), ub0 = uni(U(l - 1, 0));
-        // two tasks per node, the copies folded into them: u_L = u_N with u_R = u_N (x) L
-        // (or v_L = v_N without a right child), and v_R = v_N with v_L = R (x) v_N
-        for (int task = w; task < 2 * nn; task += kSmallWaves) {
-            const int k = task >> 1, which = task & 1;
-            const bool right = 2 * k + 1 < nprev;
-            const int uN = ub + k * 2 * CP, vN = uN + CP;
-            const int uL = ub0 + 2 * k * 2 * CP, uR = uL + 2 * CP;
-            if (which == 0) {
-                if (lane < CP) {
-                    F(uL + lane) = F(uN + lane);
-                    if (!right) F(uL + CP + lane) = F(vN + lane);
-                }
-                if (right) {   // u_R = u_N (x) L
-                    const int sl = uni(H(ly.info + vb0 + 2 * k)) & kSlotMask;
-                    const double zs = vec_log<CP, false>(ly, uN, sl, uR, scr);
-                    if (l == T.D && lane == 0) rootShift[0] = zs;
-                }
-            } else if (right) {
-                if (lane < CP) F(uR + CP + lane) = F(vN + lane);
-                // v_L = R (x) v_N
-                const int sr = uni(H(ly.info + vb0 + 2 * k + 1)) & kSlotMask;
-                const double zs = vec_log<CP, true>(ly, vN, sr, uL + CP, scr);
-                if (l == T.D && lane == 0) rootShift[1] = zs;
-            }
-        }
-        __syncthreads();
-        if (l == T.D) {
-            if (a.logZ && w == kSmallWaves - 1) {
-                const int uR = U(T.D - 1, 1), vL = U(T.D - 1, 0) + CP;
-                const float xb = lane < C ? F(uR + lane) + F(vL + lane) : -INFINITY;
-                const float m = wave_max_fast(xb);
-                const float s = wave_sum_fast(m == -INFINITY ? 0.f : fexp(xb - m));
-                lz = (m == -INFINITY) ? -INFINITY
-                                      : (float)(rootShift[0] + rootShift[1] + (double)(m + flog(s)));
-            }
-            if (!a.marg) {   // log Z only
-                store_logz();
-                return;
-            }
-        }
-    }
-    // ---- marginals with a per-edge normaliser n_t, from the leaves kept in LDS:
+    // ---- marginals of edge t with a per-edge normaliser n_t, from the leaves kept in LDS:
     // l[i][j] = ro[i] + co[j] + core[i][j].  One wave per edge; lane l holds the entries
     // v = l + 64 q of the row-major C x C edge (every lane busy, contiguous stores).  The
     // edge's row terms alpha(i) + ro(i) and column terms beta(j) + co(j) go to the wave's
@@ -700,8 +650,9 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
     constexpr int kF = (CP * CP + kWave - 1) / kWave;
     const int di = kWave / C, dj = kWave - di * C;          // the step of 64 entries
     const int i0 = lane / C, j0 = lane - i0 * C;
-    for (int t = w; t < Eb; t += kSmallWaves) {
-        const int al = U(0, t), be = al + CP;
+    const int scr = ly.scr + w * 64;
+    // alpha_t at LDS offset al, beta_{t+1} at be
+    auto form_edge = [&](int t, int al, int be) {
         const int lc = Ly::core(t), lro = Ly::ro(t), lco = Ly::co(t);
         if (lane < C) {
             F(scr + lane) = F(al + lane) + (float)Dd(lro + 2 * lane);
@@ -741,7 +692,67 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
             if (v < CC) out[v] = m == -INFINITY ? 0.f : x[q] * inv;
         }
         wave_sync();   // the scratch is rewritten for the wave's next edge
+    };
+
+    __shared__ double rootShift[2];
+    if (w == 0)
+        for (int idx = lane; idx < 2 * CP; idx += kWave)
+            F(U(T.D, 0) + idx) = (idx % CP) < C ? 0.f : -INFINITY;
+    __syncthreads();
+    for (int l = T.D; l >= 1; --l) {
+        const int nn = uni(T.n[l]), nprev = uni(T.n[l - 1]), vb0 = uni(T.vbase[l - 1]);
+        const int ub = uni(U(l, 0)), ub0 = uni(U(l - 1, 0));
+        // two tasks per node, the copies folded into them: u_L = u_N with u_R = u_N (x) L
+        // (or v_L = v_N without a right child), and v_R = v_N with v_L = R (x) v_N.  On the
+        // leaf level (a leaf t holds alpha_t and beta_{t+1}) each task goes on to the
+        // marginals of the edge whose vectors it has just completed, reading the copied one
+        // from the parent, so the copies are not needed there.
+        const bool leaves = l == 1, form = leaves && a.marg;
+        for (int task = w; task < 2 * nn; task += kSmallWaves) {
+            const int k = task >> 1, which = task & 1;
+            const bool right = 2 * k + 1 < nprev;
+            const int uN = ub + k * 2 * CP, vN = uN + CP;
+            const int uL = ub0 + 2 * k * 2 * CP, uR = uL + 2 * CP;
+            if (which == 0) {
+                if (!leaves && lane < CP) {
+                    F(uL + lane) = F(uN + lane);
+                    if (!right) F(uL + CP + lane) = F(vN + lane);
+                }
+                if (right) {   // u_R = u_N (x) L
+                    const int sl = uni(H(ly.info + vb0 + 2 * k)) & kSlotMask;
+                    const double zs = vec_log<CP, false>(ly, uN, sl, uR, scr);
+                    if (l == T.D && lane == 0) rootShift[0] = zs;
+                    if (form) form_edge(2 * k + 1, uR, vN);
+                } else if (form) {
+                    form_edge(2 * k, uN, vN);
+                }
+            } else if (right) {
+                if (!leaves && lane < CP) F(uR + CP + lane) = F(vN + lane);
+                // v_L = R (x) v_N
+                const int sr = uni(H(ly.info + vb0 + 2 * k + 1)) & kSlotMask;
+                const double zs = vec_log<CP, true>(ly, vN, sr, uL + CP, scr);
+                if (l == T.D && lane == 0) rootShift[1] = zs;
+                if (form) form_edge(2 * k, uN, uL + CP);
+            }
+        }
+        __syncthreads();
+        if (l == T.D) {
+            if (a.logZ && w == kSmallWaves - 1) {
+                const int uR = U(T.D - 1, 1), vL = U(T.D - 1, 0) + CP;
+                const float xb = lane < C ? F(uR + lane) + F(vL + lane) : -INFINITY;
+                const float m = wave_max_fast(xb);
+                const float s = wave_sum_fast(m == -INFINITY ? 0.f : fexp(xb - m));
+                lz = (m == -INFINITY) ? -INFINITY
+                                      : (float)(rootShift[0] + rootShift[1] + (double)(m + flog(s)));
+            }
+            if (!a.marg) {   // log Z only
+                store_logz();
+                return;
+            }
+        }
     }
+    // a single edge (no tree levels): its vectors are the root's zeros
+    if (T.D == 0 && w == 0) form_edge(0, U(0, 0), U(0, 0) + CP);
     store_logz();
     zero_padding();
 }
