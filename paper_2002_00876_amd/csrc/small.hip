@@ -760,7 +760,8 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
 // ================================================================== max semiring
 // LDS layout (float offsets): leaves fp32 [E][C][C] | product slots fp64 [E-1][C][C] |
 // last leaf again in fp64 [C][C] | forward scores fp64 [nodes][C] | last scores fp64 [C] |
-// node table (16-bit slots, as for the log semiring) | backpointers u8 [E][C].  Above
+// node table (16-bit slots, as for the log semiring) | backpointers u8 [C][E rounded up to
+// 4] (column-major: the backtrace reads four edges of a column at once).  Above
 // level 1 the only leaf that can still be an operand is the last one (through nodes whose
 // right half is padding), so levels >= 2 read fp64 only.
 struct MaxLayout {
@@ -929,6 +930,37 @@ __device__ void wave_vec_max(int C, int x, int Nb, int y) {
     wave_sync();
 }
 
+// One wave, one edge (fp32 leaf at Nb) after forward scores x (fp64): bp[j * ep] = the lowest
+// i maximising x[i] + l[i][j] (the backpointer of column j; the column-major layout puts
+// a column's edges next to each other), and the maximum itself into y when y >= 0 (the next
+// edge's forward scores) and into dl when dl >= 0 (the last edge's scores).  Lane l takes
+// column l % 32 over half l / 32 of i; the upper half wins only when strictly better.
+template <int CP>
+__device__ void wave_edge_argmax(int C, int x, int Nb, uint8_t* bp, int ep, int y, int dl) {
+    constexpr int kHalf = CP / 2;
+    const int lane = threadIdx.x % kWave, o = lane & 31, h = lane >> 5;
+    const int j = min(o, C - 1);
+    double best = -INFINITY;
+    int arg = h * kHalf;
+#pragma unroll
+    for (int q = 0; q < kHalf; ++q) {
+        const int i = h * kHalf + q, ic = min(i, C - 1);
+        const double v = Dd(x + 2 * ic) + (double)F(Nb + ic * C + j);
+        const bool better = i < C && v > best;   // strict: the lowest index wins ties
+        best = better ? v : best;
+        arg = better ? i : arg;
+    }
+    const double ob = xor32_max_d(best);   // max of both halves
+    const bool upperWins = h == 0 && ob > best;
+    const int oarg = __shfl_xor(arg, 32, kWave);
+    if (h == 0 && o < C) {
+        bp[o * ep] = (uint8_t)(upperWins ? oarg : arg);
+        if (y >= 0) Dd(y + 2 * o) = ob;
+        if (dl >= 0) Dd(dl + 2 * o) = ob;
+    }
+    wave_sync();
+}
+
 struct SmallMaxArgs {
     const float* pot;
     const int32_t* lengths;
@@ -990,53 +1022,39 @@ __device__ __forceinline__ void small_max_body(const SmallMaxArgs& a, const int6
     auto U = [&](int l, int k) { return ly.vecs + (T.vbase[l] + k) * 2 * C; };
     for (int i = threadIdx.x; i < C; i += kSmallThreads) Dd(U(T.D, 0) + 2 * i) = 0.0;
     __syncthreads();
+    // backpointers, column-major with ep (edges rounded up to 4) bytes per column
+    uint8_t* bp = reinterpret_cast<uint8_t*>(ts_small_lds + ly.bp);
+    const int ep = (Eb + 3) & ~3;
     for (int l = T.D; l >= 1; --l) {
         const int nn = uni(T.n[l]), nprev = uni(T.n[l - 1]), vb0 = uni(T.vbase[l - 1]);
         const int ub = uni(U(l, 0)), ub0 = uni(U(l - 1, 0));
-        // one task per node: u_L = u_N, and u_R = u_N (x) L when there is a right child
+        // one task per node: u_L = u_N, and u_R = u_N (x) L when there is a right child.  On
+        // the leaf level the same maximisation gives the left edge's backpointers, and the
+        // right edge's follow from u_R; u_L is read from the parent there (no copy).
         for (int k = w; k < nn; k += kSmallWaves) {
             const int uN = ub + k * 2 * C, uL = ub0 + 2 * k * 2 * C;
+            const bool right = 2 * k + 1 < nprev;
+            if (l == 1) {
+                const int t = 2 * k;
+                wave_edge_argmax<CP>(C, uN, ly.leaves + t * CC, bp + t, ep, right ? uL + 2 * C : -1,
+                                     t == Eb - 1 ? ly.dlast : -1);
+                if (right)
+                    wave_edge_argmax<CP>(C, uL + 2 * C, ly.leaves + (t + 1) * CC, bp + t + 1, ep, -1,
+                                         t + 1 == Eb - 1 ? ly.dlast : -1);
+                continue;
+            }
             if (lane < C) Dd(uL + 2 * lane) = Dd(uN + 2 * lane);
-            if (2 * k + 1 < nprev) {
+            if (right) {
                 const int sl = uni(H(ly.info + vb0 + 2 * k)) & kSlotMask;
-                if (l == 1) wave_vec_max<CP, true>(C, uN, ly.leaves + sl * CC, uL + 2 * C);
-                else wave_vec_max<CP, false>(C, uN, ly.node64(sl, Eb), uL + 2 * C);
+                wave_vec_max<CP, false>(C, uN, ly.node64(sl, Eb), uL + 2 * C);
             }
         }
         __syncthreads();
     }
-    // ---- backpointers bp[t][j] = lowest argmax_i delta_t[i] + l[t][i][j]: one (t, j) per
-    // lane pair (l, l ^ 32), each lane scanning half of i; the lower half wins ties
-    uint8_t* bp = reinterpret_cast<uint8_t*>(ts_small_lds + ly.bp);
-    {
-        constexpr int kHalf = CP / 2;
-        const int h = lane >> 5;
-        const float invC = 1.f / (float)C;
-        for (int p = w * 32 + (lane & 31); p < ((Eb * C + 31) & ~31); p += kSmallWaves * 32) {
-            const int pc = min(p, Eb * C - 1);
-            const int t = fdiv(pc, C, invC), j = pc - t * C;
-            const int d = U(0, t), leaf = ly.leaves + t * CC;
-            double best = -INFINITY;
-            int arg = h * kHalf;
-#pragma unroll
-            for (int q = 0; q < kHalf; ++q) {
-                const int i = h * kHalf + q, ic = min(i, C - 1);
-                const double v = Dd(d + 2 * ic) + (double)F(leaf + ic * C + j);
-                const bool better = i < C && v > best;   // strict: the lowest index wins ties
-                best = better ? v : best;
-                arg = better ? i : arg;
-            }
-            // partner half: the upper half takes over only when strictly better
-            const double ob = xor32_max_d(best);   // max of both halves
-            const bool upperWins = h == 0 && ob > best;
-            const int oarg = __shfl_xor(arg, 32, kWave);
-            if (h == 0 && p < Eb * C) {
-                bp[t * C + j] = (uint8_t)(upperWins ? oarg : arg);
-                if (t == Eb - 1) Dd(ly.dlast + 2 * j) = ob;
-            }
-        }
+    if (T.D == 0) {   // one edge: its forward scores are the root's zeros
+        if (w == 0) wave_edge_argmax<CP>(C, U(0, 0), ly.leaves, bp, ep, -1, ly.dlast);
+        __syncthreads();
     }
-    __syncthreads();
     // ---- last label (lowest argmax), score, backtrace.  Wave 0 keeps 32 edges of
     // backpointers at a time in registers (lane j holds column j, four edges per register)
     // and follows the path with readlane.
@@ -1055,19 +1073,13 @@ __device__ __forceinline__ void small_max_body(const SmallMaxArgs& a, const int6
             path[Eb] = z;
         }
         const int jc = min(lane, C - 1);
-        for (int t1 = Eb; t1 > 0; t1 -= 32) {          // edges [t1 - 32, t1)
-            const int t0 = max(t1 - 32, 0);
+        for (int c = (Eb - 1) >> 5; c >= 0; --c) {       // edges [32 c, min(32 c + 32, Eb))
+            const int t0 = 32 * c, t1 = min(t0 + 32, Eb);
+            // four edges of column jc per 32-bit read (the bytes past Eb are never used)
             unsigned pk[8];
 #pragma unroll
-            for (int g = 0; g < 8; ++g) {
-                unsigned v = 0;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int t = t0 + 4 * g + e;
-                    v |= (unsigned)bp[min(t, Eb - 1) * C + jc] << (8 * e);
-                }
-                pk[g] = v;
-            }
+            for (int g = 0; g < 8; ++g)
+                pk[g] = t0 + 4 * g < Eb ? *reinterpret_cast<const unsigned*>(bp + jc * ep + t0 + 4 * g) : 0u;
             int zs = 0;   // lane t - t0 records z_t
 #pragma unroll
             for (int g = 7; g >= 0; --g) {
@@ -1124,7 +1136,7 @@ size_t small_max_lds_bytes(int64_t E, int64_t C) {
     const int64_t CC = C * C, nodes = small_tree_nodes(E);
     const int64_t floats = (E * CC + 3) + (E - 1) * CC * 2 + CC * 2 + nodes * C * 2 + 2 * C +
                            (nodes + 1) / 2 + 3;   // + node table, alignment of bp
-    return sizeof(float) * (size_t)floats + (size_t)(E * C);
+    return sizeof(float) * (size_t)floats + (size_t)(((E + 3) & ~3) * C);
 }
 
 bool small_path_fits(int64_t N, int64_t C) {
