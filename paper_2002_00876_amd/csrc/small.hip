@@ -304,8 +304,10 @@ struct Tile {
     static constexpr int kK = kT == 32 ? 2 : 4;      // contraction indices per step
     static constexpr int kSteps = CP / kK;
     static constexpr int kV = kT == 32 ? 16 : 4;     // values per lane
-    // values whose row lies below CP (rows grow with r for the 32-wide tile)
-    static constexpr int kVr = kT == 32 ? (CP / 2 < 16 ? CP / 2 : 16) : 4;
+    // values that hold a row below CP in at least one half of the wave (rows grow with r
+    // for the 32-wide tile; rows at or past CP are computed from clamped operands and not
+    // stored)
+    static constexpr int kVr = kT == 32 ? ((CP + 7) / 8) * 4 : 4;
     __device__ static int row(int r, int lane) {
         return kT == 32 ? (r >> 2) * 8 + ((lane >> 5) << 2) + (r & 3) : ((lane >> 4) << 2) + r;
     }
@@ -384,7 +386,8 @@ __device__ __forceinline__ void prod_log(const LogLayout<CP>& ly, int sl, int sr
         // the root: P = log S (offsets copied), no normalisation
         if (own < CP && rowsOk) {
 #pragma unroll
-            for (int r = 0; r < Tl::kVr; ++r) F(Pc + Tl::row(r, lane) * kLd + own) = x[r];
+            for (int r = 0; r < Tl::kVr; ++r)
+                if (Tl::row(r, lane) < CP) F(Pc + Tl::row(r, lane) * kLd + own) = x[r];
         }
         if (lane < CP) {
             Dd(Ly::ro(sp) + 2 * lane) = Dd(Ly::ro(sl) + 2 * lane);
@@ -410,7 +413,7 @@ __device__ __forceinline__ void prod_log(const LogLayout<CP>& ly, int sl, int sr
 #pragma unroll
             for (int r = 0; r < Tl::kVr; ++r) {
                 const int o = Tl::row(r, lane);
-                F(Pc + (kTrans ? own * kLd + o : o * kLd + own)) = x[r] - sh;
+                if (o < CP) F(Pc + (kTrans ? own * kLd + o : o * kLd + own)) = x[r] - sh;
             }
         }
         if (lane < CP) {
@@ -1125,7 +1128,7 @@ __global__ __launch_bounds__(kSmallThreads) void k_small_both(SmallLogArgs la, S
 // uses a prefix of each region, so the offsets computed in the kernels stay inside.
 size_t small_log_lds_bytes(int64_t E, int64_t C) {
     if (E < 1) return 0;
-    const int64_t CP = C <= 8 ? 8 : C <= 16 ? 16 : C <= 24 ? 24 : 32;   // as the launcher
+    const int64_t CP = C <= 8 ? 8 : C <= 16 ? 16 : C <= 20 ? 20 : C <= 24 ? 24 : 32;   // as the launcher
     const int64_t coreF = (CP * (CP + 1) + 1) & ~1, slotF = coreF + 4 * CP;
     const int64_t floats = (2 * E - 1) * slotF + small_tree_nodes(E) * 2 * CP + kSmallWaves * 64;
     return sizeof(float) * (size_t)floats + 2 * (size_t)small_tree_nodes(E);   // + node table
@@ -1200,6 +1203,7 @@ hipError_t launch_small_log(const float* pot, const int32_t* lengths, int64_t B,
     const size_t lds = small_log_lds_bytes(N - 1, C);
     if (C <= 8) return small_log_cp<8>(a, B, lds, s);
     if (C <= 16) return small_log_cp<16>(a, B, lds, s);
+    if (C <= 20) return small_log_cp<20>(a, B, lds, s);
     if (C <= 24) return small_log_cp<24>(a, B, lds, s);
     return small_log_cp<32>(a, B, lds, s);
 }
@@ -1210,6 +1214,7 @@ hipError_t launch_small_max(const float* pot, const int32_t* lengths, int64_t B,
     const size_t lds = small_max_lds_bytes(N - 1, C);
     if (C <= 8) return small_max_cp<8>(a, B, lds, s);
     if (C <= 16) return small_max_cp<16>(a, B, lds, s);
+    if (C <= 20) return small_max_cp<20>(a, B, lds, s);
     if (C <= 24) return small_max_cp<24>(a, B, lds, s);
     return small_max_cp<32>(a, B, lds, s);
 }
@@ -1222,6 +1227,7 @@ hipError_t launch_small_both(const float* pot, const int32_t* lengths, int64_t B
     const size_t lds = std::max(small_log_lds_bytes(N - 1, C), small_max_lds_bytes(N - 1, C));
     if (C <= 8) return small_both_cp<8>(la, ma, B, lds, s);
     if (C <= 16) return small_both_cp<16>(la, ma, B, lds, s);
+    if (C <= 20) return small_both_cp<20>(la, ma, B, lds, s);
     if (C <= 24) return small_both_cp<24>(la, ma, B, lds, s);
     return small_both_cp<32>(la, ma, B, lds, s);
 }

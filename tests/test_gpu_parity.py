@@ -31,6 +31,8 @@ SHAPES = [  # (B, N, C): several tiles, ragged tails, odd label counts
     (3, 2, 5), (4, 3, 3), (5, 9, 20), (3, 17, 33), (2, 33, 64), (2, 24, 65),
     (2, 30, 128), (2, 12, 129), (1, 9, 256), (2, 7, 200), (3, 100, 16), (2, 257, 8),
     (4, 64, 1), (2, 5, 2), (3, 40, 31), (2, 18, 96),
+    # every label padding of the single-launch kernels (C padded to 8, 16, 20, 24 or 32)
+    (3, 13, 17), (2, 21, 19), (3, 11, 23), (2, 15, 24), (2, 9, 12), (3, 6, 28),
 ]
 
 
