@@ -67,7 +67,9 @@ struct Tree {
 //   RIGHT operand (right child of a product): P[b][c] = co[c] + core[b][c], max_b core[b][c] = 0
 //   NONE (the root): P[a][c] = ro[a] + co[c] + core[a][c]
 // (an absent right child makes a node equal to its left child, so a node takes the role
-// of its first ancestor that is consumed; the root is consumed by the log-sum-exp).
+// of its first ancestor that is consumed).  The root's matrix is never formed: log Z comes
+// from its children's outside vectors, so every product is a LEFT or a RIGHT node; only
+// the single leaf of a one-edge sequence is a NONE node.
 // For P = L (x) R with L in LEFT and R in RIGHT form:
 //   S[a][c] = sum_b exp(core_L[a][b]) exp(core_R[b][c])     (fp32 MFMA, every factor <= 1)
 //   P[a][c] = ro_L[a] + co_R[c] + log S[a][c]
@@ -76,7 +78,7 @@ struct Tree {
 //
 // One wave computes a whole product as one MFMA tile (32 x 32 for CP > 16, 16 x 16
 // otherwise).  The tile's output layout gives each lane one column and a set of rows, so
-// a product that is normalised per column (RIGHT, and the root) is computed as P and one
+// a product that is normalised per column (RIGHT) is computed as P and one
 // normalised per row (LEFT) as its transpose P^T = R^T L^T: either way the lane owns the
 // line it normalises, and the reduction is over its own values plus the lanes holding the
 // same column.
@@ -317,6 +319,7 @@ struct Tile {
 // form kRole (one wave).
 template <int CP, int kRole>
 __device__ __forceinline__ void prod_log(const LogLayout<CP>& ly, int sl, int sr, int sp) {
+    static_assert(kRole == kLeft || kRole == kRight, "products below the root only");
     using Ly = LogLayout<CP>;
     using Tl = Tile<CP>;
     constexpr int kT = Tl::kT, kLd = Ly::kLd;
@@ -328,14 +331,12 @@ __device__ __forceinline__ void prod_log(const LogLayout<CP>& ly, int sl, int sr
     // offsets of the values' own lines, read before the products so they overlap them:
     // LEFT: co_R of each value's column, RIGHT: ro_L of each value's row
     const int offBase = kRole == kLeft ? Ly::co(sr) : Ly::ro(sl);
-    const float mOff = kRole == kNone ? 0.f
-        : safe_shift(wave_max_fast(lane < C ? (float)Dd(offBase + 2 * min(lane, C - 1)) : -INFINITY));
+    const float mOff =
+        safe_shift(wave_max_fast(lane < C ? (float)Dd(offBase + 2 * min(lane, C - 1)) : -INFINITY));
     float oh[Tl::kVr];
-    if constexpr (kRole != kNone) {
 #pragma unroll
-        for (int r = 0; r < Tl::kVr; ++r)
-            oh[r] = (float)(Dd(offBase + 2 * min(Tl::row(r, lane), CP - 1)) - (double)mOff);
-    }
+    for (int r = 0; r < Tl::kVr; ++r)
+        oh[r] = (float)(Dd(offBase + 2 * min(Tl::row(r, lane), CP - 1)) - (double)mOff);
     // operand values: L[own][k] and R[k][own], k = kK * st + grp
     float lv[Tl::kSteps], rv[Tl::kSteps];
 #pragma unroll
@@ -382,18 +383,7 @@ __device__ __forceinline__ void prod_log(const LogLayout<CP>& ly, int sl, int sr
         }
     }
     const bool rowsOk = kT == 32 || Tl::row(0, lane) < CP;   // 16-wide tile, CP = 8
-    if constexpr (kRole == kNone) {
-        // the root: P = log S (offsets copied), no normalisation
-        if (own < CP && rowsOk) {
-#pragma unroll
-            for (int r = 0; r < Tl::kVr; ++r)
-                if (Tl::row(r, lane) < CP) F(Pc + Tl::row(r, lane) * kLd + own) = x[r];
-        }
-        if (lane < CP) {
-            Dd(Ly::ro(sp) + 2 * lane) = Dd(Ly::ro(sl) + 2 * lane);
-            Dd(Ly::co(sp) + 2 * lane) = Dd(Ly::co(sr) + 2 * lane);
-        }
-    } else {
+    {
         // fold the shifted offsets of the other index in, then shift the lane's line to max 0
         float m = -INFINITY;
 #pragma unroll
@@ -590,9 +580,9 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
             const int sr = uni(H(ly.info + vb0 + 2 * k + 1)) & kSlotMask;
             const int ip = uni(H(ly.info + vb1 + k));
             const int sp = ip & kSlotMask, role = ip >> 14;
+            // below the root every node is consumed as a left or a right operand
             if (role == kLeft) prod_log<CP, kLeft>(ly, sl, sr, sp);
-            else if (role == kRight) prod_log<CP, kRight>(ly, sl, sr, sp);
-            else prod_log<CP, kNone>(ly, sl, sr, sp);
+            else prod_log<CP, kRight>(ly, sl, sr, sp);
             wave_sync();
         }
         __syncthreads();
