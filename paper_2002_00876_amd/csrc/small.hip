@@ -315,6 +315,18 @@ struct Tile {
     }
 };
 
+// LSE_k row[k] + col[k * stride] over k < C, by a direct max-shifted sum: the exact value of
+// a product entry whose exp-shifted terms all underflowed.  A rare path, kept out of line so
+// that the products' code stays small.
+__device__ __noinline__ float exact_entry(int row, int col, int stride, int C) {
+    float q = -INFINITY;
+    for (int k = 0; k < C; ++k) q = fmaxf(q, F(row + k) + F(col + k * stride));
+    if (q == -INFINITY) return -INFINITY;
+    float s = 0.f;
+    for (int k = 0; k < C; ++k) s += fexp(F(row + k) + F(col + k * stride) - q);
+    return q + flog(s);
+}
+
 // Product of the LEFT node at slot sl and the RIGHT node at slot sr into slot sp, in the
 // form kRole (one wave).
 template <int CP, int kRole>
@@ -370,15 +382,7 @@ __device__ __forceinline__ void prod_log(const LogLayout<CP>& ly, int sl, int sr
             if (!(acc[r] >= kUnderflow)) {
                 const int other = min(Tl::row(r, lane), C - 1);
                 const int a = kTrans ? oc : other, c = kTrans ? other : oc;
-                float q = -INFINITY;
-                for (int k = 0; k < C; ++k) q = fmaxf(q, F(Lc + a * kLd + k) + F(Rc + k * kLd + c));
-                float v = -INFINITY;
-                if (q != -INFINITY) {
-                    float s = 0.f;
-                    for (int k = 0; k < C; ++k) s += fexp(F(Lc + a * kLd + k) + F(Rc + k * kLd + c) - q);
-                    v = q + flog(s);
-                }
-                x[r] = v;
+                x[r] = exact_entry(Lc + a * kLd, Rc + c, kLd, C);
             }
         }
     }

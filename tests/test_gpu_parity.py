@@ -63,10 +63,12 @@ def test_neg_inf_rows_and_columns_large_c():
     check_all(pot, lens, "neg-inf rows/cols")
 
 
-def test_wide_dynamic_range_uses_exact_fallback():
-    # sigma 40: exp-shifted products underflow and must be recomputed exactly
-    pot, lens = W.random_case(79, 3, 20, 48, sigma=40.0, lengths=[20, 11, 2])
-    check_all(pot, lens, "sigma=40")
+@pytest.mark.parametrize("C", [48, 20, 13])
+def test_wide_dynamic_range_uses_exact_fallback(C):
+    # sigma 40: exp-shifted products underflow and must be recomputed exactly (C = 20 and 13
+    # take the single-launch kernels by default, C = 48 the multi-launch tree)
+    pot, lens = W.random_case(79 + C, 3, 20, C, sigma=40.0, lengths=[20, 11, 2])
+    check_all(pot, lens, f"sigma=40 C={C}")
 
 
 def test_large_common_offset():
