@@ -31,8 +31,9 @@
  *   stream   the hipStream_t to enqueue on (NULL = the default stream).
  *
  * Ownership and synchronisation: every pointer is owned by the caller.  The library
- * allocates nothing, keeps no pointer after returning, and only enqueues kernels on
- * `stream`; results are ready once that stream is synchronised.  Calls with distinct
+ * allocates no memory, keeps no pointer after returning, and enqueues its kernels on
+ * `stream` (ts_chain_marginals_viterbi may fork part of its work onto a side stream and
+ * joins it back, see there); results are ready once that stream is synchronised.  Calls with distinct
  * workspaces may run concurrently on different streams.  Results are bitwise
  * reproducible for identical inputs (no floating-point atomics).
  *
@@ -117,9 +118,13 @@ ts_status ts_chain_viterbi(const float* pot, const int32_t* lengths, int64_t B, 
  * ts_chain_marginals (logZ nullable, marg) and of ts_chain_viterbi (path, score), with the
  * same meaning, layout and values.  For label sets small enough for the single-launch path
  * both passes run in one launch (one workgroup per sequence and pass, side by side);
- * otherwise the two kernel sequences run one after the other on `stream`.  The workspace
- * is ts_chain_workspace_bytes(TS_OP_MARGINALS_VITERBI, ...): the marginals workspace
- * followed by the Viterbi workspace.  Errors as for the two separate calls.
+ * otherwise the Viterbi kernel sequence runs on a side stream of the library's (one per
+ * device, default priority, created by the first such call and kept until the process
+ * ends), forked from `stream` and joined back into it with events, while the marginals
+ * sequence runs on `stream`: the call stays ordered on `stream` as any other, and can be
+ * captured into a HIP graph.  The workspace is
+ * ts_chain_workspace_bytes(TS_OP_MARGINALS_VITERBI, ...): the marginals workspace followed
+ * by the Viterbi workspace.  Errors as for the two separate calls.
  */
 ts_status ts_chain_marginals_viterbi(const float* pot, const int32_t* lengths, int64_t B,
                                      int64_t N, int64_t C, float* logZ, float* marg,

@@ -5,6 +5,7 @@
 
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -20,6 +21,42 @@ thread_local std::string g_err;
 ts_status fail(ts_status code, const std::string& msg) {
     g_err = msg;
     return code;
+}
+
+// Side stream of the combined marginals + Viterbi call on the multi-launch tree: one per
+// device (default priority, created on first use and kept until the process ends), with an
+// event for the fork from the caller's stream and one for the join back into it.  A record
+// and the wait on it are made under one lock, so concurrent callers cannot interleave them
+// (a wait takes the event's latest record).
+constexpr int kMaxDevices = 64;
+struct Side {
+    hipStream_t stream = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+};
+std::mutex g_side_mu;
+Side g_side[kMaxDevices];
+
+hipError_t side_of_current_device(Side** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_side_mu);
+    Side& sd = g_side[dev];
+    if (!sd.stream) {
+        if ((e = hipEventCreateWithFlags(&sd.fork, hipEventDisableTiming)) != hipSuccess) return e;
+        if ((e = hipEventCreateWithFlags(&sd.join, hipEventDisableTiming)) != hipSuccess) return e;
+        if ((e = hipStreamCreateWithFlags(&sd.stream, hipStreamNonBlocking)) != hipSuccess) return e;
+    }
+    *out = &sd;
+    return hipSuccess;
+}
+
+// `to` waits for everything enqueued on `from` so far
+hipError_t link(hipEvent_t ev, hipStream_t from, hipStream_t to) {
+    std::lock_guard<std::mutex> lock(g_side_mu);
+    hipError_t e = hipEventRecord(ev, from);
+    return e == hipSuccess ? hipStreamWaitEvent(to, ev, 0) : e;
 }
 
 constexpr size_t kAlign = 256;
@@ -362,9 +399,17 @@ ts_status ts_chain_marginals_viterbi(const float* pot, const int32_t* lengths, i
     }
     if (pm.fused && pv.fused)
         return hip_status(launch_small_both(pot, lengths, B, N, C, logZ, marg, path, score, s));
-    hipError_t e = launch_logz_tree(pm, pot, lengths, logZ, s);
+    // the two tree sequences share only read-only inputs and write disjoint outputs and
+    // workspace halves: the Viterbi one runs on the side stream, forked from `stream` and
+    // joined back into it, so the levels of one fill the compute units the other's small
+    // levels leave idle
+    Side* side = nullptr;
+    hipError_t e = side_of_current_device(&side);
+    if (e == hipSuccess) e = link(side->fork, s, side->stream);
+    if (e == hipSuccess) e = launch_viterbi_tree(pv, pot, lengths, path, score, side->stream);
+    if (e == hipSuccess) e = launch_logz_tree(pm, pot, lengths, logZ, s);
     if (e == hipSuccess) e = launch_marginals_tree(pm, pot, lengths, marg, s);
-    if (e == hipSuccess) e = launch_viterbi_tree(pv, pot, lengths, path, score, s);
+    if (e == hipSuccess) e = link(side->join, side->stream, s);
     return hip_status(e);
 }
 

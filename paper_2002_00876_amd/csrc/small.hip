@@ -789,12 +789,6 @@ __device__ __forceinline__ int fdiv(int x, int d, float inv) {
     return q;
 }
 
-template <bool kLeaf>
-__device__ __forceinline__ double mx(int base, int idx) {
-    if constexpr (kLeaf) return (double)F(base + idx);
-    else return Dd(base + 2 * idx);
-}
-
 // x of lane l ^ kXor within its quad of lanes (DPP quad permutation), float64
 template <int kXor>
 __device__ __forceinline__ double quad_xor_d(double x) {
@@ -908,10 +902,10 @@ __device__ __forceinline__ double xor32_max_d(double x) {
     return fmax(a, b);
 }
 
-// One wave: y[j] = max_i x[i] + N[i][j] (fp64).  Lane l
-// computes column l % 32 over half l / 32 of i; the halves meet through a cross-half max.
-// Past C the index repeats C - 1, which leaves a max unchanged.
-template <int CP, bool kLeaf>
+// One wave: y[j] = max_i x[i] + N[i][j] with N a float64 node at Nb.  Lane l computes
+// column l % 32 over half l / 32 of i; the halves meet through a cross-half max.  Past C the
+// index repeats C - 1, which leaves a max unchanged.
+template <int CP>
 __device__ void wave_vec_max(int C, int x, int Nb, int y) {
     constexpr int kHalf = CP / 2;
     const int lane = threadIdx.x % kWave, o = lane & 31, h = lane >> 5;
@@ -920,7 +914,7 @@ __device__ void wave_vec_max(int C, int x, int Nb, int y) {
 #pragma unroll
     for (int q = 0; q < kHalf; ++q) {
         const int ic = min(h * kHalf + q, C - 1);
-        m = fmax(m, Dd(x + 2 * ic) + mx<kLeaf>(Nb, ic * C + j));
+        m = fmax(m, Dd(x + 2 * ic) + Dd(Nb + 2 * (ic * C + j)));
     }
     m = xor32_max_d(m);
     if (h == 0 && o < C) Dd(y + 2 * o) = m;
@@ -1043,7 +1037,7 @@ __device__ __forceinline__ void small_max_body(const SmallMaxArgs& a, const int6
             if (lane < C) Dd(uL + 2 * lane) = Dd(uN + 2 * lane);
             if (right) {
                 const int sl = uni(H(ly.info + vb0 + 2 * k)) & kSlotMask;
-                wave_vec_max<CP, false>(C, uN, ly.node64(sl, Eb), uL + 2 * C);
+                wave_vec_max<CP>(C, uN, ly.node64(sl, Eb), uL + 2 * C);
             }
         }
         __syncthreads();

@@ -80,3 +80,52 @@ def test_graph_replay_matches_eager(case, monkeypatch):
         binding.viterbi(other, other_len, ws=ws_v)
         torch.cuda.synchronize()
     say(f"graph replay case {case}: 4 replays bitwise equal to eager")
+
+
+@pytest.mark.parametrize("case", ["paper", "tree_c40"])
+def test_graph_replay_of_the_combined_call(case, monkeypatch):
+    """The combined call captured as it stands: on the multi-launch tree it forks its Viterbi
+    half onto the library's side stream and joins it back, which the capture must follow."""
+    import torch
+    from paper_2002_00876_amd import binding
+    if case == "paper":
+        pot_h, lens_h = W.generate("paper")
+    else:
+        monkeypatch.setenv("TS_PATH", "tree")
+        pot_h, lens_h = W.random_case(13, 3, 37, 40)
+    say(f"combined-call graph case {case}: shape {pot_h.shape}")
+    dev = torch.device("cuda:0")
+    pot = torch.from_numpy(pot_h).to(dev)
+    lens = torch.from_numpy(lens_h).to(dev)
+    B, E, C, _ = pot.shape
+    N = E + 1
+    ws = binding._workspace(binding.OP_MARGINALS_VITERBI, B, N, C, dev)[0]
+    ref = _outputs(dev, B, N, C)
+    binding.marginals_viterbi(pot, lens, out=ref, ws=ws)
+    torch.cuda.synchronize()
+    ref = [t.cpu() for t in ref]
+
+    out = _outputs(dev, B, N, C)
+    cap = torch.cuda.Stream(device=dev)
+    graph = torch.cuda.CUDAGraph()
+    cap.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(graph, stream=cap):
+            binding.marginals_viterbi(pot, lens, out=out, ws=ws)
+    torch.cuda.current_stream(dev).wait_stream(cap)
+    torch.cuda.synchronize()
+
+    other_h, other_l = W.random_case(14, B, N, C)
+    other = torch.from_numpy(other_h).to(dev)
+    other_len = torch.from_numpy(other_l).to(dev)
+    for rep in range(4):
+        for t in out:
+            t.fill_(-7)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for got, want, name in zip(out, ref, ("logZ", "marginals", "path", "score")):
+            assert torch.equal(got.cpu(), want), f"replay {rep}: {name} differs from eager"
+        binding.marginals_viterbi(other, other_len, ws=ws)   # eager work on the same workspace
+        torch.cuda.synchronize()
+    say(f"combined-call graph case {case}: 4 replays bitwise equal to eager")
