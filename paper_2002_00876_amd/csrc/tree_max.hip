@@ -86,26 +86,38 @@ __global__ __launch_bounds__(kMThreads) void k_up_max_narrow(UpMaxArgs a) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = -INFINITY;
     constexpr int kPer = kMT * kMK / kMThreads;   // staged values per thread and operand
-    for (int64_t k0 = 0; k0 < C; k0 += kMK) {
-        // every load of the slice is issued before the first is used
-        double va[kPer], vb[kPer];
+    using T = typename std::conditional<kLeaf, float, double>::type;
+    const T* src = kLeaf ? (const T*)a.leaves : (const T*)a.cnode;
+    const size_t lbase = (size_t)(b * a.cnodes + 2 * k) * C * C, rbase = lbase + (size_t)C * C;
+    // the next slice's loads are in flight while the current slice is used (raw values:
+    // the widening of fp32 leaves waits until they are stored)
+    T va[kPer], vb[kPer];
+    auto load = [&](int64_t k0) {
 #pragma unroll
         for (int v = 0; v < kPer; ++v) {
             const int idx = tid + v * kMThreads;
             const int r = idx / kMK, kk = idx % kMK;
             const int64_t row = a0 + r, kg = k0 + kk;
-            va[v] = (row < C && kg < C) ? child_at<kLeaf>(a, b, 2 * k, row, kg) : -INFINITY;
+            va[v] = (row < C && kg < C) ? src[lbase + (size_t)row * C + kg] : (T)-INFINITY;
             const int kb = idx / kMT, cc = idx % kMT;
             const int64_t col = c0 + cc, kgb = k0 + kb;
-            vb[v] = (col < C && kgb < C) ? child_at<kLeaf>(a, b, 2 * k + 1, kgb, col) : -INFINITY;
+            vb[v] = (col < C && kgb < C) ? src[rbase + (size_t)kgb * C + col] : (T)-INFINITY;
         }
+    };
+    auto store = [&]() {
 #pragma unroll
         for (int v = 0; v < kPer; ++v) {
             const int idx = tid + v * kMThreads;
-            As[idx % kMK][idx / kMK] = va[v];
-            Bs[idx / kMT][idx % kMT] = vb[v];
+            As[idx % kMK][idx / kMK] = (double)va[v];
+            Bs[idx / kMT][idx % kMT] = (double)vb[v];
         }
-        __syncthreads();
+    };
+    load(0);
+    store();
+    __syncthreads();
+    for (int64_t k0 = 0; k0 < C; k0 += kMK) {
+        const bool more = k0 + kMK < C;
+        if (more) load(k0 + kMK);
 #pragma unroll 4
         for (int kk = 0; kk < kMK; ++kk) {
             double av[4], bv[4];
@@ -119,7 +131,11 @@ __global__ __launch_bounds__(kMThreads) void k_up_max_narrow(UpMaxArgs a) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) acc[i][j] = fmax(acc[i][j], av[i] + bv[j]);
         }
-        __syncthreads();
+        if (more) {
+            __syncthreads();
+            store();
+            __syncthreads();
+        }
     }
     // 16-byte stores of a lane's four columns when they lie inside the matrix (even C)
     const int64_t cb = c0 + tx * 4;
