@@ -44,9 +44,17 @@ hipError_t side_of_current_device(Side** out) {
     std::lock_guard<std::mutex> lock(g_side_mu);
     Side& sd = g_side[dev];
     if (!sd.stream) {
-        if ((e = hipEventCreateWithFlags(&sd.fork, hipEventDisableTiming)) != hipSuccess) return e;
-        if ((e = hipEventCreateWithFlags(&sd.join, hipEventDisableTiming)) != hipSuccess) return e;
-        if ((e = hipStreamCreateWithFlags(&sd.stream, hipStreamNonBlocking)) != hipSuccess) return e;
+        // all three or none: a failed creation releases what was made and is retried later
+        Side made;
+        e = hipEventCreateWithFlags(&made.fork, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&made.join, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipStreamCreateWithFlags(&made.stream, hipStreamNonBlocking);
+        if (e != hipSuccess) {
+            if (made.fork) (void)hipEventDestroy(made.fork);
+            if (made.join) (void)hipEventDestroy(made.join);
+            return e;
+        }
+        sd = made;
     }
     *out = &sd;
     return hipSuccess;
