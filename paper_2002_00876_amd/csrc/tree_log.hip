@@ -767,6 +767,165 @@ struct FormArgs {
     float* marg;
 };
 
+// The same per-pair computation with each leaf read from memory once (C <= 128, C % 4 == 0):
+// the workgroup keeps both leaves in registers, in the layout write_marginal uses (thread t
+// holds columns 4 (t % G) .. +3 of rows t / G + q * step, q < kR), and forms
+//   y = u (x) leaf_{2k}: partial column log-sum-exps over the thread's rows, merged in LDS
+//   over the `step` threads of a column group;
+//   z = leaf_{2k+1} (x) v: partial row log-sum-exps over the thread's 4 columns, merged in
+//   LDS over the G threads of a row;
+// then the normalisers and the marginals from the registers (the second read of each leaf
+// in k_form_log is gone: one read and one write per edge, the algorithmic traffic).
+constexpr int kRegMaxLabels = 128;
+
+// (m, s) += (m2, s2) for log-sum-exp states value = m + log s (m = -inf: empty)
+__device__ __forceinline__ void lse_merge_into(float& m, float& s, float m2, float s2) {
+    if (m2 == -INFINITY) return;
+    if (m == -INFINITY) { m = m2; s = s2; return; }
+    const float nm = fmaxf(m, m2);
+    s = s * fexp(m - nm) + s2 * fexp(m2 - nm);
+    m = nm;
+}
+
+template <int kR>
+__global__ __launch_bounds__(kVecThreads) void k_form_reg(FormArgs a) {
+    // column partials [step][C] (step * C <= 4 kVecThreads) and row partials [C][G]
+    constexpr int kMaxC = kR == 2 ? 64 : kRegMaxLabels;   // kR = 2 serves C <= 64
+    constexpr int kColParts = 4 * kVecThreads, kRowParts = kMaxC * kMaxC / 4;
+    __shared__ float su[kRegMaxLabels], sv[kRegMaxLabels], ya[kRegMaxLabels], zb[kRegMaxLabels],
+        yraw[kRegMaxLabels], zraw[kRegMaxLabels];
+    __shared__ float pm[kColParts], ps[kColParts], qm[kRowParts], qs[kRowParts];
+    __shared__ float nrm[2], mx[2];
+    const int64_t npairs = (a.N - 1 + 1) / 2;
+    const int64_t b = blockIdx.x / npairs, k = blockIdx.x % npairs;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    const int C = (int)a.C;
+    const int64_t E = a.N - 1;
+    const int64_t tL = 2 * k, tR = 2 * k + 1;
+    const size_t CC = (size_t)C * C;
+    const int tid = threadIdx.x;
+    for (int64_t t = tL; t <= tR; ++t)
+        if (t < E && t >= Eb) {
+            float* o = a.marg + (size_t)(b * E + t) * CC;
+            for (size_t idx = tid; idx < CC; idx += kVecThreads) o[idx] = 0.f;
+        }
+    if (tL >= Eb) return;
+    const bool right = tR < Eb;
+    const int G = C / 4, step = kVecThreads / G;
+    const int g = tid % G, i0 = tid / G, j = 4 * g;
+    const bool act = i0 < step;
+    // both leaves into registers first (every load in flight together)
+    const float* leafL = a.pot + (size_t)(b * E + tL) * CC;
+    const float* leafR = a.pot + (size_t)(b * E + tR) * CC;
+    float4 lv[kR], rv[kR];
+#pragma unroll
+    for (int q = 0; q < kR; ++q) {
+        const int i = i0 + q * step;
+        const bool ok = act && i < C;
+        lv[q] = ok ? *reinterpret_cast<const float4*>(leafL + (size_t)i * C + j) : make_float4(0.f, 0.f, 0.f, 0.f);
+        rv[q] = ok && right ? *reinterpret_cast<const float4*>(leafR + (size_t)i * C + j)
+                            : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    for (int i = tid; i < C; i += kVecThreads) {
+        su[i] = a.u1 ? a.u1[(size_t)(b * a.nodes1 + k) * C + i] : 0.f;
+        sv[i] = a.v1 ? a.v1[(size_t)(b * a.nodes1 + k) * C + i] : 0.f;
+    }
+    __syncthreads();
+    // partial log-sum-exps: columns j..j+3 of leaf_{2k} over the thread's rows (with u), and
+    // each of the thread's rows of leaf_{2k+1} over its 4 columns (with v)
+    if (act) {
+        const float v0 = sv[j], v1 = sv[j + 1], v2 = sv[j + 2], v3 = sv[j + 3];
+        float xc[4][kR];   // u[i] + l_{2k}[i][j + c] of the thread's rows (-inf past C)
+#pragma unroll
+        for (int q = 0; q < kR; ++q) {
+            const int i = i0 + q * step;
+            const bool ok = i < C;
+            const float ui = ok ? su[i] : -INFINITY;
+            xc[0][q] = ui + lv[q].x;
+            xc[1][q] = ui + lv[q].y;
+            xc[2][q] = ui + lv[q].z;
+            xc[3][q] = ui + lv[q].w;
+            if (right && ok) {
+                const float r[4] = {rv[q].x + v0, rv[q].y + v1, rv[q].z + v2, rv[q].w + v3};
+                const float m = fmaxf(fmaxf(r[0], r[1]), fmaxf(r[2], r[3]));
+                float sr = 0.f;
+                if (m != -INFINITY) {
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) sr += fexp(r[c] - m);
+                }
+                qm[i * G + g] = m;
+                qs[i * G + g] = sr;
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            float m = -INFINITY, sm = 0.f;
+            lse_fold<kR>(m, sm, xc[c]);
+            pm[i0 * C + j + c] = m;
+            ps[i0 * C + j + c] = sm;
+        }
+    }
+    __syncthreads();
+    // merged: yraw[j] = LSE_i u[i] + l_{2k}[i][j],  zraw[i] = LSE_j l_{2k+1}[i][j] + v[j]
+    if (tid < C) {
+        float m = -INFINITY, sm = 0.f;
+        for (int r = 0; r < step; ++r) lse_merge_into(m, sm, pm[r * C + tid], ps[r * C + tid]);
+        yraw[tid] = lse_val(m, sm);
+    } else if (right && tid >= kVecThreads / 2 && tid - kVecThreads / 2 < C) {
+        const int i = tid - kVecThreads / 2;
+        float m = -INFINITY, sm = 0.f;
+        for (int r = 0; r < G; ++r) lse_merge_into(m, sm, qm[i * G + r], qs[i * G + r]);
+        zraw[i] = lse_val(m, sm);
+    }
+    __syncthreads();
+    // the messages shifted to max 0 (wave 0: alpha_{2k+1} from y, wave 1: beta_{2k+1} from z)
+    const int w = tid / kWave, lane = tid % kWave;
+    if (w < 2 && (w == 0 || right)) {
+        const float* src = w == 0 ? yraw : zraw;
+        float m = -INFINITY;
+        for (int i = lane; i < C; i += kWave) m = fmaxf(m, src[i]);
+        m = safe_shift(wave_max(m));
+        float* dst = w == 0 ? ya : zb;
+        for (int i = lane; i < C; i += kWave) dst[i] = src[i] - m;
+        if (lane == 0) mx[w] = m;
+    }
+    __syncthreads();
+    // normalisers: n_{2k} = LSE_j yraw[j] + beta_{2k+1}[j] (or + v[j] without a right edge),
+    // n_{2k+1} = LSE_i alpha_{2k+1}[i] + zraw[i]
+    if (w < 2 && (w == 0 || right)) {
+        float m = -INFINITY, sm = 0.f;
+        for (int i = lane; i < C; i += kWave) {
+            float x[1] = {w == 0 ? yraw[i] + (right ? zb[i] : sv[i]) : ya[i] + zraw[i]};
+            lse_fold<1>(m, sm, x);
+        }
+        const float mm = wave_max(m);
+        sm = wave_sum(m == -INFINITY ? 0.f : sm * fexp(m - safe_shift(mm)));
+        if (lane == 0) nrm[w] = lse_val(mm, sm);
+    }
+    __syncthreads();
+    if (!act) return;
+    // the marginals from the registers
+    auto write = [&](const float4* lvq, const float* al, const float* be, float n, float* out) {
+        const bool zero = n == -INFINITY;
+        const float b0 = be[j] - n, b1 = be[j + 1] - n, b2 = be[j + 2] - n, b3 = be[j + 3] - n;
+#pragma unroll
+        for (int q = 0; q < kR; ++q) {
+            const int i = i0 + q * step;
+            if (i < C) {
+                const float ai = al[i];
+                float4 r;
+                r.x = zero ? 0.f : fexp(ai + lvq[q].x + b0);
+                r.y = zero ? 0.f : fexp(ai + lvq[q].y + b1);
+                r.z = zero ? 0.f : fexp(ai + lvq[q].z + b2);
+                r.w = zero ? 0.f : fexp(ai + lvq[q].w + b3);
+                *reinterpret_cast<float4*>(out + (size_t)i * C + j) = r;
+            }
+        }
+    };
+    write(lv, su, right ? zb : sv, nrm[0], a.marg + (size_t)(b * E + tL) * CC);
+    if (right) write(rv, ya, sv, nrm[1], a.marg + (size_t)(b * E + tR) * CC);
+}
+
 // mu = exp(al[i] + leaf[i][j] + be[j] - n) over one C x C edge, the whole workgroup:
 // thread t takes column group t % G (16 bytes when kVec, else one float) of rows t / G,
 // t / G + T / G, ... so that each row is read and written contiguously
@@ -987,10 +1146,16 @@ hipError_t launch_marginals_tree(const Plan& p, const float* pot, const int32_t*
     f.nodes1 = (p.D >= 1) ? (p.Np >> 1) : 1;
     f.lengths = lengths; f.N = p.N; f.C = p.C; f.marg = marg;
     const int64_t npairs = (p.N - 1 + 1) / 2;
-    if (p.C % 4 == 0)
-        hipLaunchKernelGGL(k_form_log<true>, dim3((unsigned)(p.B * npairs)), dim3(kVecThreads), 0, s, f);
+    const dim3 grid((unsigned)(p.B * npairs));
+    // both leaves of a pair held in registers when they fit: one read of each edge
+    if (p.C % 4 == 0 && p.C <= 64)
+        hipLaunchKernelGGL(k_form_reg<2>, grid, dim3(kVecThreads), 0, s, f);
+    else if (p.C % 4 == 0 && p.C <= kRegMaxLabels)
+        hipLaunchKernelGGL(k_form_reg<8>, grid, dim3(kVecThreads), 0, s, f);
+    else if (p.C % 4 == 0)
+        hipLaunchKernelGGL(k_form_log<true>, grid, dim3(kVecThreads), 0, s, f);
     else
-        hipLaunchKernelGGL(k_form_log<false>, dim3((unsigned)(p.B * npairs)), dim3(kVecThreads), 0, s, f);
+        hipLaunchKernelGGL(k_form_log<false>, grid, dim3(kVecThreads), 0, s, f);
     return hipGetLastError();
 }
 
