@@ -329,22 +329,45 @@ struct BpArgs {
 };
 
 // For edge t with forward scores d (shared, [C]): bp[t][j] = lowest argmax_i d[i] + l[t][i][j]
-// and, into dn[j] (shared, may be nullptr), the max itself.
-__device__ void backpointers(const float* leaf, const double* d, int64_t C, uint8_t* bp,
-                             double* dn) {
-    const int64_t j = threadIdx.x;
+// and, into dn[j] (shared, may be nullptr), the max itself.  kS consecutive threads share a
+// column (kS * C <= 256 threads): part s scans rows s, s + kS, ... in ascending order, four
+// rows' loads issued together, keeping the first maximum; the parts then meet through lane
+// exchanges, the lower index winning ties (all -inf gives row 0, as a serial scan would).
+template <int kS>
+__device__ void backpointers(const float* leaf, const double* d, int C, uint8_t* bp, double* dn) {
+    const int t = (int)threadIdx.x, j = t / kS, s = t % kS;
+    double best = -INFINITY;
+    int arg = s;
     if (j < C) {
-        double best = d[0] + (double)leaf[j];
-        int arg = 0;
-        for (int64_t i = 1; i < C; ++i) {
-            const double v = d[i] + (double)leaf[i * C + j];
-            if (v > best) { best = v; arg = (int)i; }
+        int i = s;
+        for (; i + 3 * kS < C; i += 4 * kS) {
+            float l[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) l[u] = leaf[(size_t)(i + u * kS) * C + j];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const double v = d[i + u * kS] + (double)l[u];
+                if (v > best) { best = v; arg = i + u * kS; }
+            }
         }
+        for (; i < C; i += kS) {
+            const double v = d[i] + (double)leaf[(size_t)i * C + j];
+            if (v > best) { best = v; arg = i; }
+        }
+    }
+#pragma unroll
+    for (int o = 1; o < kS; o <<= 1) {
+        const double ov = __shfl_xor(best, o, kWave);
+        const int oi = __shfl_xor(arg, o, kWave);
+        if (ov > best || (ov == best && oi < arg)) { best = ov; arg = oi; }
+    }
+    if (j < C && s == 0) {
         bp[j] = (uint8_t)arg;
         if (dn) dn[j] = best;
     }
 }
 
+template <int kS>
 __global__ __launch_bounds__(256) void k_bp_max(BpArgs a) {
     __shared__ double su[kMaxLabels], sr[kMaxLabels], sl[kMaxLabels];
     __shared__ double rv[4];
@@ -365,12 +388,12 @@ __global__ __launch_bounds__(256) void k_bp_max(BpArgs a) {
     const float* leafL = a.pot + (size_t)(b * E + tL) * C * C;
     const bool right = tR < Eb;
     // edge tL: delta_{tL} = u; its max gives delta_{tL+1} = delta_{tR}
-    backpointers(leafL, su, C, a.bp + (size_t)(b * E + tL) * C, sr);
+    backpointers<kS>(leafL, su, (int)C, a.bp + (size_t)(b * E + tL) * C, sr);
     __syncthreads();
     const double* dlast = sr;
     if (right) {
         const float* leafR = a.pot + (size_t)(b * E + tR) * C * C;
-        backpointers(leafR, sr, C, a.bp + (size_t)(b * E + tR) * C, sl);
+        backpointers<kS>(leafR, sr, (int)C, a.bp + (size_t)(b * E + tR) * C, sl);
         __syncthreads();
         dlast = sl;
     }
@@ -543,7 +566,11 @@ hipError_t launch_viterbi_tree(const Plan& p, const float* pot, const int32_t* l
     bpa.lengths = lengths; bpa.N = p.N; bpa.C = C; bpa.bp = p.bp; bpa.zlast = p.zlast;
     bpa.score = score;
     const int64_t npairs = (p.N - 1 + 1) / 2;
-    hipLaunchKernelGGL(k_bp_max, dim3((unsigned)(p.B * npairs)), dim3(256), 0, s, bpa);
+    // as many threads per column as 256 threads allow, up to four
+    const dim3 bgrid((unsigned)(p.B * npairs));
+    if (C <= 64) hipLaunchKernelGGL(k_bp_max<4>, bgrid, dim3(256), 0, s, bpa);
+    else if (C <= 128) hipLaunchKernelGGL(k_bp_max<2>, bgrid, dim3(256), 0, s, bpa);
+    else hipLaunchKernelGGL(k_bp_max<1>, bgrid, dim3(256), 0, s, bpa);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
 
