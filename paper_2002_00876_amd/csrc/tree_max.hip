@@ -293,6 +293,7 @@ struct DownMaxArgs {
     int level;
 };
 
+template <int kS>
 __global__ __launch_bounds__(256) void k_down_max(DownMaxArgs a) {
     __shared__ double su[kMaxLabels];
     const int64_t b = blockIdx.x / a.nodes, k = blockIdx.x % a.nodes;
@@ -308,12 +309,24 @@ __global__ __launch_bounds__(256) void k_down_max(DownMaxArgs a) {
     if ((2 * k + 1) * half >= Eb) return;
     const double* L = a.cnode + (size_t)(b * a.cnodes + 2 * k) * C * C;
     double* uR = a.uC + (size_t)(b * a.cnodes + 2 * k + 1) * C;
-    const int64_t j = threadIdx.x;
+    // kS consecutive threads per column, each over every kS-th row (four loads in flight),
+    // then a max across them (exact in any order)
+    const int t = (int)threadIdx.x, j = t / kS, s = t % kS;
+    double m = -INFINITY;
     if (j < C) {
-        double m = -INFINITY;
-        for (int64_t i = 0; i < C; ++i) m = fmax(m, su[i] + L[i * C + j]);
-        uR[j] = m;
+        int i = s;
+        for (; i + 3 * kS < C; i += 4 * kS) {
+            double l[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) l[u] = L[(size_t)(i + u * kS) * C + j];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) m = fmax(m, su[i + u * kS] + l[u]);
+        }
+        for (; i < C; i += kS) m = fmax(m, su[i] + L[(size_t)i * C + j]);
     }
+#pragma unroll
+    for (int o = 1; o < kS; o <<= 1) m = fmax(m, __shfl_xor(m, o, kWave));
+    if (j < C && s == 0) uR[j] = m;
 }
 
 // ---- leaves: backpointers, last label and score
@@ -555,7 +568,10 @@ hipError_t launch_viterbi_tree(const Plan& p, const float* pot, const int32_t* l
         d.cnodes = p.Np >> (l - 1);
         d.uC = p.mu[l - 1];
         d.lengths = lengths; d.N = p.N; d.C = C; d.level = l;
-        hipLaunchKernelGGL(k_down_max, dim3((unsigned)(p.B * d.nodes)), dim3(256), 0, s, d);
+        const dim3 dgrid((unsigned)(p.B * d.nodes));
+        if (C <= 64) hipLaunchKernelGGL(k_down_max<4>, dgrid, dim3(256), 0, s, d);
+        else if (C <= 128) hipLaunchKernelGGL(k_down_max<2>, dgrid, dim3(256), 0, s, d);
+        else hipLaunchKernelGGL(k_down_max<1>, dgrid, dim3(256), 0, s, d);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
