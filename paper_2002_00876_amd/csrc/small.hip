@@ -574,6 +574,13 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
     __syncthreads();
     normalise_leaves<CP>(ly, raw, Eb);
     __syncthreads();
+    // the root's outside vectors (zeros, padding -inf; the root is the last node), written
+    // once the raw leaves (which can reach into the vectors' region) are consumed and read
+    // after the next barrier
+    if (w == kSmallWaves - 1)
+        for (int idx = lane; idx < 2 * CP; idx += kWave)
+            F(ly.vecs + (nodes - 1) * 2 * CP + idx) = (idx % CP) < C ? 0.f : -INFINITY;
+    if (T.D < 2) __syncthreads();   // no level of the up-sweep (and no barrier) follows
     // ---- up-sweep: one wave per product, below the root: the root's matrix is never needed
     // (log Z comes from its children's outside vectors)
     for (int l = 1; l < T.D; ++l) {
@@ -692,10 +699,6 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
     };
 
     __shared__ double rootShift[2];
-    if (w == 0)
-        for (int idx = lane; idx < 2 * CP; idx += kWave)
-            F(U(T.D, 0) + idx) = (idx % CP) < C ? 0.f : -INFINITY;
-    __syncthreads();
     for (int l = T.D; l >= 1; --l) {
         const int nn = uni(T.n[l]), nprev = uni(T.n[l - 1]), vb0 = uni(T.vbase[l - 1]);
         const int ub = uni(U(l, 0)), ub0 = uni(U(l - 1, 0));
@@ -758,7 +761,8 @@ __device__ __forceinline__ void small_log_body(const SmallLogArgs& a, const int6
 // LDS layout (float offsets): leaves fp32 [E][C][C] | product slots fp64 [E-1][C][C] |
 // last leaf again in fp64 [C][C] | forward scores fp64 [nodes][C] | last scores fp64 [C] |
 // node table (16-bit slots, as for the log semiring) | backpointers u8 [C][E rounded up to
-// 4] (column-major: the backtrace reads four edges of a column at once).  Above
+// 32] (column-major: the backtrace reads 32 edges of a column at once; the padding edges
+// map every label to itself, so the backtrace runs through whole chunks of 32).  Above
 // level 1 the only leaf that can still be an operand is the last one (through nodes whose
 // right half is padding), so levels >= 2 read fp64 only.
 struct MaxLayout {
@@ -789,15 +793,38 @@ __device__ __forceinline__ int fdiv(int x, int d, float inv) {
     return q;
 }
 
-// x of lane l ^ kXor within its quad of lanes (DPP quad permutation), float64
-template <int kXor>
-__device__ __forceinline__ double quad_xor_d(double x) {
-    constexpr int kCtrl = kXor == 1 ? 0xB1 : 0x4E;   // quad_perm [1,0,3,2] / [2,3,0,1]
+// DPP permutation kCtrl of a float64 (both halves moved alike)
+template <int kCtrl>
+__device__ __forceinline__ double dpp_d(double x) {
     const uint64_t u = __double_as_longlong(x);
     const int lo = (int)(unsigned)u, hi = (int)(unsigned)(u >> 32);
     const unsigned rlo = (unsigned)__builtin_amdgcn_update_dpp(lo, lo, kCtrl, 0xF, 0xF, false);
     const unsigned rhi = (unsigned)__builtin_amdgcn_update_dpp(hi, hi, kCtrl, 0xF, 0xF, false);
     return __longlong_as_double((long long)(((uint64_t)rhi << 32) | rlo));
+}
+
+// x of lane l ^ kXor within its quad of lanes (DPP quad_perm [1,0,3,2] / [2,3,0,1]), float64
+template <int kXor>
+__device__ __forceinline__ double quad_xor_d(double x) {
+    return dpp_d<kXor == 1 ? 0xB1 : 0x4E>(x);
+}
+
+__device__ __forceinline__ double readlane_d(double x, int lane) {
+    const uint64_t u = __double_as_longlong(x);
+    const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)u, lane);
+    const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(u >> 32), lane);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// Maximum of a float64 over the wave (uniform result): DPP inside each row of 16 lanes
+// (quad swaps, then the mirrors within 8 and within 16), readlane across the rows.  A max is
+// exact, so the order of the steps does not matter.
+__device__ __forceinline__ double wave_max_dpp_d(double x) {
+    x = fmax(x, dpp_d<0xB1>(x));
+    x = fmax(x, dpp_d<0x4E>(x));
+    x = fmax(x, dpp_d<0x141>(x));
+    x = fmax(x, dpp_d<0x140>(x));
+    return fmax(fmax(readlane_d(x, 0), readlane_d(x, 16)), fmax(readlane_d(x, 32), readlane_d(x, 48)));
 }
 
 // All products of level l, P = L (x) R in (max, +), float64, by the whole workgroup.  The
@@ -808,14 +835,15 @@ __device__ __forceinline__ double quad_xor_d(double x) {
 // any order, so splitting q changes no bit of the result; it cuts the chain of dependent
 // maxima and lets larger register tiles (fewer LDS reads per pair) keep enough lanes busy.
 // Entries past C are computed from neighbouring data and not stored.  kLeaves: level 1
-// (fp32 leaves).
-template <int MR, int MC, int kS, bool kLeaves>
+// (fp32 leaves).  kC > 0: C == kC known at compile time (strides fold into the LDS offsets
+// and the index loop unrolls); 0: C at run time.
+template <int MR, int MC, int kS, bool kLeaves, int kC>
 __device__ void block_prod_max(const MaxLayout& ly, int E, int np, int vb0, int pbase) {
     using T = typename std::conditional<kLeaves, float, double>::type;
     static_assert(kS == 2 || kS == 4, "the q split runs inside a DPP quad");
     static_assert((MR * MC) % kS == 0, "every lane of a group stores the same count");
     constexpr int kPer = MR * MC / kS;   // entries stored per lane
-    const int C = ly.C, CC = ly.CC;
+    const int C = kC > 0 ? kC : ly.C, CC = C * C;
     const int TR = (C + MR - 1) / MR, TC = (C + MC - 1) / MC, tpp = TR * TC;
     const float invTpp = 1.f / (float)tpp, invTc = 1.f / (float)TC;
     const int nq = (C + kS - 1) / kS;
@@ -852,12 +880,17 @@ __device__ void block_prod_max(const MaxLayout& ly, int E, int np, int vb0, int 
 #pragma unroll
                 for (int j = 0; j < MC; ++j) acc[i * MC + j] = fmax(acc[i * MC + j], av[i] + bv[j]);
         };
-        int i = 0;
-        for (; i + 2 <= nq; i += 2) {   // two indices per trip: their reads go out together
-            step(min(s + kS * i, C - 1));
-            step(min(s + kS * (i + 1), C - 1));
+        if constexpr (kC > 0) {
+#pragma unroll 2
+            for (int i = 0; i < nq; ++i) step(min(s + kS * i, C - 1));
+        } else {
+            int i = 0;
+            for (; i + 2 <= nq; i += 2) {   // two indices per trip: their reads go out together
+                step(min(s + kS * i, C - 1));
+                step(min(s + kS * (i + 1), C - 1));
+            }
+            if (i < nq) step(min(s + kS * i, C - 1));
         }
-        if (i < nq) step(min(s + kS * i, C - 1));
 #pragma unroll
         for (int e = 0; e < MR * MC; ++e) acc[e] = fmax(acc[e], quad_xor_d<1>(acc[e]));
         if constexpr (kS == 4) {
@@ -880,17 +913,24 @@ __device__ void block_prod_max(const MaxLayout& ly, int E, int np, int vb0, int 
 // Tile shape and q split of a level: the largest tiles (fewest LDS reads per pair) that still
 // give at least six waves of lanes, at most one tile per lane; the widest level splits q in
 // two only.
-template <bool kLeaves>
-__device__ void level_prod_max(const MaxLayout& ly, int E, int np, int vb0, int pbase) {
+template <bool kLeaves, int kC>
+__device__ void level_prod_max_c(const MaxLayout& ly, int E, int np, int vb0, int pbase) {
     const int C = ly.C;
     auto lanes = [&](int mr, int mc, int ks) {
         return np * ((C + mr - 1) / mr) * ((C + mc - 1) / mc) * ks;
     };
     constexpr int kEnough = 6 * kWave;
-    if (lanes(4, 4, 4) > kSmallThreads) block_prod_max<4, 4, 2, kLeaves>(ly, E, np, vb0, pbase);
-    else if (lanes(4, 4, 4) >= kEnough) block_prod_max<4, 4, 4, kLeaves>(ly, E, np, vb0, pbase);
-    else if (lanes(2, 4, 4) >= kEnough) block_prod_max<2, 4, 4, kLeaves>(ly, E, np, vb0, pbase);
-    else block_prod_max<2, 2, 4, kLeaves>(ly, E, np, vb0, pbase);
+    if (lanes(4, 4, 4) > kSmallThreads) block_prod_max<4, 4, 2, kLeaves, kC>(ly, E, np, vb0, pbase);
+    else if (lanes(4, 4, 4) >= kEnough) block_prod_max<4, 4, 4, kLeaves, kC>(ly, E, np, vb0, pbase);
+    else if (lanes(2, 4, 4) >= kEnough) block_prod_max<2, 4, 4, kLeaves, kC>(ly, E, np, vb0, pbase);
+    else block_prod_max<2, 2, 4, kLeaves, kC>(ly, E, np, vb0, pbase);
+}
+
+// C equal to the padded size CP takes the compile-time variant
+template <bool kLeaves, int CP>
+__device__ void level_prod_max(const MaxLayout& ly, int E, int np, int vb0, int pbase) {
+    if (ly.C == CP) level_prod_max_c<kLeaves, CP>(ly, E, np, vb0, pbase);
+    else level_prod_max_c<kLeaves, 0>(ly, E, np, vb0, pbase);
 }
 
 __device__ __forceinline__ double xor32_max_d(double x) {
@@ -997,6 +1037,14 @@ __device__ __forceinline__ void small_max_body(const SmallMaxArgs& a, const int6
             lb.store(ly.leaves, base, n);
         }
     }
+    // the root's forward scores (zeros; the root is the last node): nothing else writes the
+    // score vectors before the forward sweep
+    if (w == 0 && lane < C) Dd(ly.vecs + (nodes - 1) * 2 * C + 2 * lane) = 0.0;
+    // padding edges [Eb, ep) of the backpointers: z_t = z_{t+1}
+    if ((int)threadIdx.x < C) {
+        uint8_t* col = reinterpret_cast<uint8_t*>(ts_small_lds + ly.bp) + threadIdx.x * ((Eb + 31) & ~31);
+        for (int t = Eb; t < ((Eb + 31) & ~31); ++t) col[t] = (uint8_t)threadIdx.x;
+    }
     __syncthreads();
     // the last leaf in fp64 for levels >= 2 (read only after the level-1 barrier)
     for (int i = threadIdx.x; i < CC; i += kSmallThreads)
@@ -1005,17 +1053,16 @@ __device__ __forceinline__ void small_max_body(const SmallMaxArgs& a, const int6
     // scores start from the root with zeros and only use its children's matrices)
     for (int l = 1; l < T.D; ++l) {
         const int np = uni(T.products(l)), vb0 = uni(T.vbase[l - 1]), pb = uni(T.pbase[l]);
-        if (l == 1) level_prod_max<true>(ly, Eb, np, vb0, pb);
-        else level_prod_max<false>(ly, Eb, np, vb0, pb);
+        if (l == 1) level_prod_max<true, CP>(ly, Eb, np, vb0, pb);
+        else level_prod_max<false, CP>(ly, Eb, np, vb0, pb);
         __syncthreads();
     }
-    // ---- forward scores: u_L = u_N, u_R = u_N (x) L   (root: zeros)
+    // ---- forward scores: u_L = u_N, u_R = u_N (x) L   (root: zeros, set with the leaves)
     auto U = [&](int l, int k) { return ly.vecs + (T.vbase[l] + k) * 2 * C; };
-    for (int i = threadIdx.x; i < C; i += kSmallThreads) Dd(U(T.D, 0) + 2 * i) = 0.0;
-    __syncthreads();
-    // backpointers, column-major with ep (edges rounded up to 4) bytes per column
+    // backpointers, column-major with ep (edges rounded up to 32) bytes per column; the
+    // padding edges were set to the identity with the leaves
     uint8_t* bp = reinterpret_cast<uint8_t*>(ts_small_lds + ly.bp);
-    const int ep = (Eb + 3) & ~3;
+    const int ep = (Eb + 31) & ~31;
     for (int l = T.D; l >= 1; --l) {
         const int nn = uni(T.n[l]), nprev = uni(T.n[l - 1]), vb0 = uni(T.vbase[l - 1]);
         const int ub = uni(U(l, 0)), ub0 = uni(U(l - 1, 0));
@@ -1046,44 +1093,35 @@ __device__ __forceinline__ void small_max_body(const SmallMaxArgs& a, const int6
         if (w == 0) wave_edge_argmax<CP>(C, U(0, 0), ly.leaves, bp, ep, -1, ly.dlast);
         __syncthreads();
     }
-    // ---- last label (lowest argmax), score, backtrace.  Wave 0 keeps 32 edges of
-    // backpointers at a time in registers (lane j holds column j, four edges per register)
-    // and follows the path with readlane.
+    // ---- last label (lowest argmax: the first lane holding the maximum), score, backtrace.
+    // Wave 0 keeps 32 edges of backpointers at a time in registers (lane j holds column j,
+    // four edges per register) and follows the path with readlane; the padding edges past
+    // Eb leave the label unchanged.
     if (w == 0) {
-        double best = lane < C ? Dd(ly.dlast + 2 * lane) : -INFINITY;
-        int arg = lane < C ? lane : 0x7fffffff;
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-            const double ov = __shfl_xor(best, o, kWave);
-            const int oi = __shfl_xor(arg, o, kWave);
-            if (ov > best || (ov == best && oi < arg)) { best = ov; arg = oi; }
-        }
-        int z = uni(arg < C ? arg : 0);
+        const double v = lane < C ? Dd(ly.dlast + 2 * lane) : -INFINITY;
+        const double best = wave_max_dpp_d(v);
+        const uint64_t hit = __builtin_amdgcn_ballot_w64(lane < C && v == best);
+        int z = hit ? uni((int)__builtin_ctzll(hit)) : 0;
         if (lane == 0) {
             a.score[b] = (float)best;
             path[Eb] = z;
         }
         const int jc = min(lane, C - 1);
-        for (int c = (Eb - 1) >> 5; c >= 0; --c) {       // edges [32 c, min(32 c + 32, Eb))
-            const int t0 = 32 * c, t1 = min(t0 + 32, Eb);
-            // four edges of column jc per 32-bit read (the bytes past Eb are never used)
+        for (int c = (Eb - 1) >> 5; c >= 0; --c) {       // edges [32 c, 32 c + 32)
+            const int t0 = 32 * c;
             unsigned pk[8];
 #pragma unroll
-            for (int g = 0; g < 8; ++g)
-                pk[g] = t0 + 4 * g < Eb ? *reinterpret_cast<const unsigned*>(bp + jc * ep + t0 + 4 * g) : 0u;
+            for (int g = 0; g < 8; ++g) pk[g] = *reinterpret_cast<const unsigned*>(bp + jc * ep + t0 + 4 * g);
             int zs = 0;   // lane t - t0 records z_t
 #pragma unroll
             for (int g = 7; g >= 0; --g) {
 #pragma unroll
                 for (int e = 3; e >= 0; --e) {
-                    const int t = t0 + 4 * g + e;
-                    if (t < t1) {
-                        z = (__builtin_amdgcn_readlane(pk[g], z) >> (8 * e)) & 0xff;
-                        zs = lane == 4 * g + e ? z : zs;
-                    }
+                    z = (__builtin_amdgcn_readlane(pk[g], z) >> (8 * e)) & 0xff;
+                    zs = lane == 4 * g + e ? z : zs;
                 }
             }
-            if (lane < t1 - t0) path[t0 + lane] = zs;
+            if (lane < min(32, Eb - t0)) path[t0 + lane] = zs;
         }
     }
     pad_path();
@@ -1127,7 +1165,7 @@ size_t small_max_lds_bytes(int64_t E, int64_t C) {
     const int64_t CC = C * C, nodes = small_tree_nodes(E);
     const int64_t floats = (E * CC + 3) + (E - 1) * CC * 2 + CC * 2 + nodes * C * 2 + 2 * C +
                            (nodes + 1) / 2 + 3;   // + node table, alignment of bp
-    return sizeof(float) * (size_t)floats + (size_t)(((E + 3) & ~3) * C);
+    return sizeof(float) * (size_t)floats + (size_t)(((E + 31) & ~31) * C);
 }
 
 bool small_path_fits(int64_t N, int64_t C) {
