@@ -33,6 +33,9 @@ SHAPES = [  # (B, N, C): several tiles, ragged tails, odd label counts
     (4, 64, 1), (2, 5, 2), (3, 40, 31), (2, 18, 96),
     # every label padding of the single-launch kernels (C padded to 8, 16, 20, 24 or 32)
     (3, 13, 17), (2, 21, 19), (3, 11, 23), (2, 15, 24), (2, 9, 12), (3, 6, 28),
+    # single-launch backtraces over several chunks of 32 edges: a last chunk of one edge, a
+    # whole chunk, padded and unpadded multi-chunk sequences
+    (3, 34, 7), (2, 33, 5), (3, 98, 8), (2, 161, 6),
 ]
 
 
@@ -43,7 +46,8 @@ def test_random_shapes(B, N, C):
     check_all(pot, lens, f"random B={B} N={N} C={C}")
 
 
-@pytest.mark.parametrize("B,N,C,r", [(4, 30, 5, 1), (3, 20, 20, 1), (2, 17, 64, 2), (2, 9, 130, 1)])
+@pytest.mark.parametrize("B,N,C,r", [(4, 30, 5, 1), (3, 20, 20, 1), (2, 17, 64, 2), (2, 9, 130, 1),
+                                     (3, 70, 4, 1)])
 def test_integer_ties(B, N, C, r):
     pot, lens = W.random_case(2000 + C, B, N, C, kind="int", int_range=r, lengths="random")
     check_all(pot, lens, f"ties B={B} N={N} C={C}")
