@@ -35,8 +35,12 @@ __device__ __forceinline__ size_t mat_off(int64_t b, int64_t k, int64_t nodes, i
 // Row and column maxima of the valid leaves (the exp shifts of the level-1 products):
 // lrmax[b][t][i] = max_j l[t][i][j] for a left operand (even t), lcmax[b][t][j] =
 // max_i l[t][i][j] for a right operand (odd t), and both for an unpaired last leaf (which
-// is carried up unchanged and may be consumed on either side).  Rows: one wave per row,
-// 16-byte loads along it; columns: one thread per column, loads coalesced across threads.
+// is carried up unchanged and may be consumed on either side).  Without finiteness masks
+// and with C <= 128: rows (C = 64 or 128) take C / 4 lanes of 16-byte loads and a DPP
+// maximum each, so a wave covers 4 or 2 rows per pass; columns take one thread per column
+// and part of the rows (256 / C parts, combined through LDS).  Otherwise one wave per row
+// (16-byte loads along it) and one thread per column over all rows.  Column loads are
+// coalesced across threads.
 struct LeafMaxArgs {
     const float* pot;
     const int32_t* lengths;
@@ -58,7 +62,23 @@ __global__ __launch_bounds__(256) void k_leaf_max(LeafMaxArgs a) {
     const int C = (int)a.C;
     const float* leaf = a.pot + (size_t)(b * E + t) * C * C;
     const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
-    if (right && tid < C) {
+    const bool masks = kBits && (a.cbits || a.rbits);
+    const bool split = !masks && C <= 128;
+    if (right && split) {
+        __shared__ float part[256];
+        const int P = 256 / C, p = tid / C, c = tid - p * C;   // C <= 128: P >= 2
+        float cm = -INFINITY;
+        if (p < P) {
+#pragma unroll 8
+            for (int i = p; i < C; i += P) cm = fmaxf(cm, leaf[(size_t)i * C + c]);
+        }
+        part[tid] = cm;
+        __syncthreads();
+        if (tid < C) {
+            for (int q = 1; q < P; ++q) cm = fmaxf(cm, part[q * C + tid]);
+            a.lcmax[(size_t)(b * E + t) * C + tid] = cm;
+        }
+    } else if (right && tid < C) {
         float cm = -INFINITY;
 #pragma unroll 8
         for (int i = 0; i < C; ++i) cm = fmaxf(cm, leaf[(size_t)i * C + tid]);
@@ -79,7 +99,22 @@ __global__ __launch_bounds__(256) void k_leaf_max(LeafMaxArgs a) {
             }
         }
     }
-    if (left) {
+    if (left && kVec && split && (C == 64 || C == 128)) {
+        float* rmax = a.lrmax + (size_t)(b * E + t) * C;
+        const int lpr = C >> 2, rpw = kWave / lpr;   // lanes per row (16 or 32), rows per pass
+        const int sub = lane / lpr, col = 4 * (lane - sub * lpr);
+        for (int i0 = w * rpw; i0 < C; i0 += (256 / kWave) * rpw) {
+            const int i = i0 + sub;
+            const float4 v = *reinterpret_cast<const float4*>(leaf + (size_t)i * C + col);
+            float m = fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w));
+            m = fmaxf(m, dpp_f(m, 0xB1));    // within each row of 16 lanes
+            m = fmaxf(m, dpp_f(m, 0x4E));
+            m = fmaxf(m, dpp_f(m, 0x141));
+            m = fmaxf(m, dpp_f(m, 0x140));
+            if (lpr == 32) m = fmaxf(m, __shfl_xor(m, 16, kWave));
+            if (lane - sub * lpr == 0) rmax[i] = m;
+        }
+    } else if (left) {
         float* rmax = a.lrmax + (size_t)(b * E + t) * C;
         for (int i = w; i < C; i += 256 / kWave) {
             const float* row = leaf + (size_t)i * C;
