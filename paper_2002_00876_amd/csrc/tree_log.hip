@@ -702,10 +702,14 @@ __device__ __forceinline__ double half_max_d(double x, double* red) {
 //   half 1: y[i] = ro[i] + LSE_j (core[i][j] + co[j] + x[j])     (N (x) x, row pass)
 // x, w and y are this half's LDS vectors; the result shifted to max 0 goes to y and, when
 // yraw is given, unshifted (as float) to yraw.  ro/co may be null (leaves).  Either half may
-// be idle (active == false) but still joins the barriers.
+// be idle (active == false) but still joins the barriers.  With C = 32 or 64 (16-byte loads)
+// every thread of the half works: the C lines are cut into P = 256 / C parts (rows
+// i = p, p + P, ... of a column; a contiguous chunk of a row), whose partial log-sum-exps are
+// merged through LDS.  (At C = 128, two parts per line were slower than one.)
 template <bool kVec>
 __device__ void half_vec(bool active, const float* core, const double* ro, const double* co,
                          int C, const float* x, float* w, float* y, double* red, float* yraw) {
+    __shared__ float pm[kVecThreads], ps[kVecThreads];
     const bool rowPass = threadIdx.x >= kHalfThreads;
     const int t = threadIdx.x - (rowPass ? kHalfThreads : 0);
     const double* inOff = rowPass ? co : ro;
@@ -720,8 +724,47 @@ __device__ void half_vec(bool active, const float* core, const double* ro, const
             w[i] = (float)((double)x[i] + (inOff ? inOff[i] : 0.0) - ws);
     __syncthreads();
     double z = -INFINITY;
+    float l = -INFINITY;
+    if (kVec && (C == 32 || C == 64)) {
+        const int P = kHalfThreads / C, p = t / C, c = t - p * C, nr = C / P;   // nr % 4 == 0
+        float m = -INFINITY, sum = 0.f;
+        if (active) {
+            if (rowPass) {   // row c, columns [p nr, p nr + nr)
+                const float4* r4 = reinterpret_cast<const float4*>(core + (size_t)c * C + p * nr);
+                for (int q = 0; q < nr / 4; ++q) {
+                    const float4 v = r4[q];
+                    const int j = p * nr + 4 * q;
+                    const float xs[4] = {v.x + w[j], v.y + w[j + 1], v.z + w[j + 2], v.w + w[j + 3]};
+                    lse_fold<4>(m, sum, xs);
+                }
+            } else {         // column c, rows p, p + P, ...
+                for (int k = 0; k < nr; k += 4) {
+                    float xs[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int i = p + P * (k + u);
+                        xs[u] = core[(size_t)i * C + c] + w[i];
+                    }
+                    lse_fold<4>(m, sum, xs);
+                }
+            }
+        }
+        pm[threadIdx.x] = m;
+        ps[threadIdx.x] = sum;
+        __syncthreads();
+        if (active && t < C) {
+            const int base = rowPass ? kHalfThreads : 0;
+            float mm = -INFINITY;
+            for (int q = 0; q < P; ++q) mm = fmaxf(mm, pm[base + q * C + t]);
+            const float sh = safe_shift(mm);
+            float ss = 0.f;
+            for (int q = 0; q < P; ++q) ss += ps[base + q * C + t] * fexp(pm[base + q * C + t] - sh);
+            l = lse_val(mm, ss);
+        }
+    } else if (active && t < C) {
+        l = rowPass ? row_lse<kVec>(core, C, w, t) : col_lse(core, C, w, t);
+    }
     if (active && t < C) {
-        const float l = rowPass ? row_lse<kVec>(core, C, w, t) : col_lse(core, C, w, t);
         z = (l == -INFINITY) ? -INFINITY : (outOff ? outOff[t] : 0.0) + ws + (double)l;
         if (yraw) yraw[t] = (float)z;
     }
