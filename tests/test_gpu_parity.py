@@ -36,6 +36,8 @@ SHAPES = [  # (B, N, C): several tiles, ragged tails, odd label counts
     # single-launch backtraces over several chunks of 32 edges: a last chunk of one edge, a
     # whole chunk, padded and unpadded multi-chunk sequences
     (3, 34, 7), (2, 33, 5), (3, 98, 8), (2, 161, 6),
+    # the multi-launch outside sweep with each line split over 8 thread parts (32 labels)
+    (2, 40, 32),
 ]
 
 
