@@ -1,15 +1,16 @@
 """Benchmark: tokens/s of batched linear-chain CRF inference on one MI355X.
 
-One step is one pass of the whole hot path over one batch: ts_chain_marginals (log Z and
-edge marginals: tree up-sweep, root, outside sweep, per-edge marginals) and
-ts_chain_viterbi (max-plus tree, backpointers, backtrace).  Both calls only read the
-potentials, so the step is one call of ts_chain_marginals_viterbi, which on the
-single-launch path runs both passes in one launch, side by side (--graph replays a captured
-HIP graph of that call instead).  Inputs, outputs and workspaces are resident in HBM before
-the timed region.  Prints one JSON line.
+One timed step is one call of ts_chain_marginals over one batch: log Z and the edge
+marginals (tree up-sweep, root, outside sweep, per-edge marginals), the quantity the
+metric names.  The Viterbi call (max-plus tree, backpointers, backtrace) and the combined
+call ts_chain_marginals_viterbi (the whole hot path: both trees, the Viterbi one on a side
+stream) are timed too and reported in `breakdown`.  --step selects another call as the
+timed step; --graph replays a captured HIP graph of it.  Inputs, outputs and workspaces are
+resident in HBM before the timed region.  Prints one JSON line.
 
-Default workload: the paper-shaped batch (B=32, N=25, C=20, N(0,1) potentials, lengths
-uniform in [13, 25]).  --workload selects another of the five seeded workloads.
+Default workload: the HMM-style batch (B=16, N=1024, C=256; potentials log_softmax_j(T) +
+emissions, full lengths), the largest of the five seeded workloads.  --workload selects
+another (paper: B=32 N=25 C=20, the paper's Table 1 linear-chain shape).
 """
 import argparse
 import json
@@ -33,10 +34,16 @@ PAPER_CONTEXT_TOKENS_PER_S = 390e3   # Table 1, K80, batch 32, N=25, C=20 (conte
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="paper",
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="hmm",
                     choices=["tiny", "paper", "mid", "hmm", "long"])
+    ap.add_argument("--step", default="marginals", choices=["marginals", "viterbi", "both"],
+                    help="the call one timed step makes (default: ts_chain_marginals, the "
+                         "metric's log Z + marginals)")
+    ap.add_argument("--only", action="store_true",
+                    help="time the step only and print a short line (for profiler runs: no "
+                         "other calls, no CPU baseline)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="bound on the oracle's CPU-baseline run (0 disables it)")
     ap.add_argument("--graph", action="store_true",
@@ -107,23 +114,6 @@ def code_hash(path):
         if line:
             lines.append(line)
     return hashlib.sha256("\n".join(lines).encode()).hexdigest()
-
-
-def cpu_baseline(pot, lens, seconds):
-    import oracle
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        oracle.marginals(pot, lens)
-        oracle.viterbi(pot, lens)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
-    B, E = pot.shape[0], pot.shape[1]
-    return {"value": B * (E + 1) * reps / el, "unit": "tokens/s",
-            "cores": min(oracle.max_threads(), B), "kind": "oracle",
-            "sample": f"the full batch, oracle marginals + Viterbi repeated {reps}x "
-                      f"({el:.1f} s, float64, OpenMP over sequences)"}
 
 
 def calibrate_copy(mib):
@@ -305,6 +295,45 @@ def semi(name, steps, warmup):
     }), flush=True)
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline_streamed(pot, lens, seconds):
+    """The oracle's log Z + marginals (float64 forward-backward of every sequence, then
+    the marginals of every edge, formed range by range into one reusable buffer so the
+    float64 tensor is never held whole), repeated until `seconds` have passed."""
+    import numpy as np
+
+    import oracle
+    B, E, C, _ = pot.shape
+    chunk = max(1, (1 << 22) // (C * C))
+    buf = np.empty((chunk, C, C), np.float64)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        msg = oracle.Messages(pot, lens)
+        for b in range(B):
+            Eb = int(lens[b]) - 1
+            for e0 in range(0, Eb, chunk):
+                msg.edge_marginals(b, e0, min(Eb, e0 + chunk), out=buf[:min(Eb, e0 + chunk) - e0])
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return {"value": B * (E + 1) * reps / el, "unit": "tokens/s",
+            "cores": oracle.max_threads(), "kind": "oracle",
+            "cpu_model": cpu_model(),
+            "sample": f"the full batch: oracle log Z + marginals (float64 forward-backward, "
+                      f"OpenMP over sequences; marginals of every valid edge, OpenMP over "
+                      f"edges), {reps} pass(es) in {el:.1f} s"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -351,16 +380,16 @@ def main():
     def vit_call():
         binding.viterbi(pot, lens, out=(path, score), ws=ws_v)
 
-    def step():
-        # the whole path in one call: one launch on the single-launch path, where the
-        # marginals and the Viterbi workgroups run side by side
+    def both_call():
+        # the whole hot path in one call: on the single-launch path one launch, where the
+        # marginals and the Viterbi workgroups run side by side; on the multi-launch tree
+        # the Viterbi sequence runs on a side stream beside the marginals sequence
         binding.marginals_viterbi(pot, lens, out=(logz, marg, path, score), ws=ws_mv)
 
+    step = {"marginals": marg_call, "viterbi": vit_call, "both": both_call}[args.step]
     # warm up first: the first call of each entry point sets the kernels' LDS limits
     for _ in range(max(args.warmup, 1)):
         step()
-    marg_call()
-    vit_call()
     torch.cuda.synchronize()
 
     run = step
@@ -388,11 +417,16 @@ def main():
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
     ms_step = total_ms / args.steps
+    if args.only:
+        print(json.dumps({"step": args.step, "workload": w.name, "steps": args.steps,
+                          "ms_per_step": round(ms_step, 5)}), flush=True)
+        return
 
     # per-call durations: each entry point issued n times back to back on the stream its
-    # kernels run on, bracketed by two HIP events; on the single-launch path one call is one
-    # kernel, so this is that kernel's average duration (launch gaps included)
+    # kernels run on, bracketed by two HIP events
     def per_call(fn, n):
+        for _ in range(2):
+            fn()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
@@ -403,43 +437,58 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / n
 
-    n_calls = max(10, min(args.steps, 200))
-    ms_marg = per_call(marg_call, n_calls)
+    n_calls = max(5, min(args.steps, 200))
+    ms_marg = ms_step if args.step == "marginals" and not args.graph else per_call(marg_call, n_calls)
     ms_vit = per_call(vit_call, n_calls)
+    ms_both = per_call(both_call, n_calls)
 
     alg = algorithmic(pot_h, lens_h)
     tokens = B * N
     value = tokens / (ms_step * 1e-3)
 
-    # the roofline of the step's dominant kernel.  On the single-launch path the step is one
-    # kernel (k_small_both), timed back to back; on the multi-launch tree the whole call is
-    # timed and the bound is the sum of its kernels' bounds.
-    fused = binding.workspace_bytes(binding.OP_MARGINALS_VITERBI, B, N, C) == 0
-    ms_call = per_call(step, n_calls)
-    dom = "k_small_both" if fused else "ts_chain_marginals_viterbi (multi-launch)"
-    t_mem = alg["step_bytes"] / HBM_PEAK
-    t_mfma = alg["marg_flops"] / MFMA_F32_PEAK
-    t_f64 = alg["vit_ops"] / VALU_F64_OPS_PEAK
-    sec = ms_call * 1e-3
-    # the binding resource is the one with the longest time at its peak: on the single-launch
-    # path the log-semiring and the max-plus workgroups run side by side on different CUs
-    if t_mem >= max(t_mfma, t_f64):
-        achieved = alg["step_bytes"] / sec / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK / 1e9,
-                "unit": "GB/s", "frac": round(achieved / (HBM_PEAK / 1e9), 5)}
-    elif t_mfma >= t_f64:
-        achieved = alg["marg_flops"] / sec / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": MFMA_F32_PEAK / 1e12,
-                "unit": "TFLOP/s", "frac": round(achieved / (MFMA_F32_PEAK / 1e12), 5)}
-    else:
-        achieved = alg["vit_ops"] / sec / 1e12
-        roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": VALU_F64_OPS_PEAK / 1e12,
-                "unit": "TFLOP/s", "frac": round(achieved / (VALU_F64_OPS_PEAK / 1e12), 5)}
-    roof["traffic"] = measured_traffic(dom, w.name) if fused else None
-    roof["kernel"] = dom
-    roof["kernel_ms"] = round(ms_call, 5)
-    roof["algorithmic_bytes"] = alg["step_bytes"]
-    roof["roofline_ms"] = round(max(t_mem, t_mfma, t_f64) * 1e3, 6)
+    # Roofline of the timed call.  On the single-launch path the marginals call is one
+    # kernel (k_small_log); on the multi-launch tree it is a sequence of kernels whose bound
+    # is the call's algorithmic work: read the valid edges and write all marginals (HBM),
+    # and 2 C^3 flop per tree product on the fp32 matrix cores (MFMA).  The binding resource
+    # is the one with the longer time at its peak.
+    fused = binding.workspace_bytes(binding.OP_MARGINALS, B, N, C) == 0
+
+    def roofline(kind, sec):
+        if kind == "marginals":
+            t_mem, t_cmp = alg["marg_bytes"] / HBM_PEAK, alg["marg_flops"] / MFMA_F32_PEAK
+            if t_mem >= t_cmp:
+                a = alg["marg_bytes"] / sec / 1e9
+                r = {"bound": "hbm", "achieved": round(a, 2), "peak": HBM_PEAK / 1e9,
+                     "unit": "GB/s", "frac": round(a / (HBM_PEAK / 1e9), 5)}
+            else:
+                a = alg["marg_flops"] / sec / 1e12
+                r = {"bound": "mfma", "achieved": round(a, 3), "peak": MFMA_F32_PEAK / 1e12,
+                     "unit": "TFLOP/s", "frac": round(a / (MFMA_F32_PEAK / 1e12), 5)}
+            r["algorithmic_bytes"] = alg["marg_bytes"]
+            r["algorithmic_flops"] = alg["marg_flops"]
+        else:
+            t_mem, t_cmp = alg["vit_bytes"] / HBM_PEAK, alg["vit_ops"] / VALU_F64_OPS_PEAK
+            if t_mem >= t_cmp:
+                a = alg["vit_bytes"] / sec / 1e9
+                r = {"bound": "hbm", "achieved": round(a, 2), "peak": HBM_PEAK / 1e9,
+                     "unit": "GB/s", "frac": round(a / (HBM_PEAK / 1e9), 5)}
+            else:
+                a = alg["vit_ops"] / sec / 1e12
+                r = {"bound": "alu", "achieved": round(a, 3), "peak": VALU_F64_OPS_PEAK / 1e12,
+                     "unit": "T fp64 add/max per s", "frac": round(a / (VALU_F64_OPS_PEAK / 1e12), 5)}
+            r["algorithmic_bytes"] = alg["vit_bytes"]
+            r["algorithmic_fp64_ops"] = alg["vit_ops"]
+        r["roofline_ms"] = round(max(t_mem, t_cmp) * 1e3, 6)
+        return r
+
+    roof = roofline("marginals", ms_marg * 1e-3)
+    dom = "k_small_log" if fused else "ts_chain_marginals"
+    roof["traffic"] = measured_traffic(dom, w.name)
+    roof["kernel"] = dom if fused else (
+        "ts_chain_marginals (the call's kernel sequence: k_leaf_max, k_up_log per level, "
+        "k_root_log, k_down_log per level, k_form_*)")
+    roof["kernel_ms"] = round(ms_marg, 5)
+    roof_v = roofline("viterbi", ms_vit * 1e-3)
 
     out = {
         "metric": "tokens/sec for linear-chain logZ+marginals (B,N,C); % of HBM/compute roofline",
@@ -456,13 +505,18 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{w.name}: B={B} N={N} C={C}", "B": B, "N": N, "C": C,
                    "lengths": "uniform" if w.len_range else "fixed",
-                   "step": "ts_chain_marginals_viterbi (log Z, marginals, Viterbi path and score)"
-                           + (", replayed as a HIP graph" if args.graph else ""),
+                   "step": {"marginals": "ts_chain_marginals (log Z and edge marginals)",
+                            "viterbi": "ts_chain_viterbi (path and score)",
+                            "both": "ts_chain_marginals_viterbi (log Z, marginals, Viterbi)"}[
+                                args.step] + (", replayed as a HIP graph" if args.graph else ""),
                    "path": "fused single launch per call" if fused else "multi-launch tree"},
         "breakdown": {"marginals_ms": round(ms_marg, 5), "viterbi_ms": round(ms_vit, 5),
-                      "separate_calls_ms": round(ms_marg + ms_vit, 5),
+                      "marginals_viterbi_ms": round(ms_both, 5),
                       "marginals_tokens_per_s": round(tokens / (ms_marg * 1e-3), 1),
-                      "valid_tokens_per_s": round(float(lens_h.sum()) / (ms_step * 1e-3), 1)},
+                      "viterbi_tokens_per_s": round(tokens / (ms_vit * 1e-3), 1),
+                      "whole_path_tokens_per_s": round(tokens / (ms_both * 1e-3), 1),
+                      "valid_tokens_per_s": round(float(lens_h.sum()) / (ms_step * 1e-3), 1),
+                      "viterbi_roofline": roof_v},
         "dtype_note": "log semiring in fp32 (fp32 MFMA, float64 row/column offsets); "
                       "Viterbi max-plus in float64",
         "paper_context": {"tokens_per_s": PAPER_CONTEXT_TOKENS_PER_S,
@@ -470,7 +524,7 @@ def main():
         "roofline": roof,
     }
     if args.cpu_seconds > 0:
-        out["cpu_baseline"] = cpu_baseline(pot_h, lens_h, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline_streamed(pot_h, lens_h, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 

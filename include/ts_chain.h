@@ -17,18 +17,24 @@
  *            values and -inf (the semiring zero) are allowed; +inf and NaN are not.
  *            May be NULL only when N == 1 (no edges).
  *   lengths  device pointer, int32 [B]: number of tokens of each sequence,
- *            1 <= lengths[b] <= N.  Edges t >= lengths[b]-1 are padding: they are never
- *            read and act as the identity.  NULL means every length is N.  Values are not
+ *            1 <= lengths[b] <= N.  Edges t >= lengths[b]-1 are padding: they act as the
+ *            identity and their values never affect any result (the multi-launch tree
+ *            never reads them; the single-launch kernels for small label sets load whole
+ *            sequences and discard them).  NULL means every length is N.  Values are not
  *            read on the host: out-of-range values are clamped to [1, N] by the kernels,
  *            unless the environment variable TS_CHECK=1 is set, in which case the call
  *            copies the lengths to the host synchronously and returns TS_ERR_LENGTHS.
  *   B, N, C  batch size, maximum number of tokens, number of labels:
  *            B >= 1, N >= 1, 1 <= C <= ts_chain_max_labels(), B * N <= 2^29 (one launch
- *            grid covers every edge); larger problems return TS_ERR_BAD_DIM.
+ *            grid covers every edge); larger problems return TS_ERR_BAD_DIM.  The Viterbi
+ *            calls also keep their backtrace tables in 64 KiB of LDS: with K the largest
+ *            power of two <= 65536 / C, N - 1 <= K * floor(65536 / C) edges (C = 256:
+ *            N <= 65537; C = 128: N <= 262145), else TS_ERR_BAD_DIM.
  *   ws       device workspace of at least ts_chain_workspace_bytes(op, B, N, C) bytes,
  *            aligned to 256 bytes (any hipMalloc / PyTorch CUDA allocation is).  May be
  *            NULL when that size is 0.  Its contents on entry are ignored.
- *   stream   the hipStream_t to enqueue on (NULL = the default stream).
+ *   stream   the hipStream_t to enqueue on (NULL = the default stream), passed as void* so
+ *            that this header needs no HIP header.
  *
  * Ownership and synchronisation: every pointer is owned by the caller.  The library
  * allocates no memory, keeps no pointer after returning, and enqueues its kernels on
@@ -181,7 +187,6 @@ ts_status ts_chain_sample(const float* pot, const int32_t* lengths, const float*
 ts_status ts_chain_logpartition_sequential(const float* pot, const int32_t* lengths, int64_t B,
                                            int64_t N, int64_t C, float* logZ, void* stream);
 
-/* Message for the last non-OK status returned to the calling thread ("" if none). */
 /*
  * Semi-Markov CRF (Table 1, "Semi-Markov": segment labels, parts N K C^2; Sec. 6a carries
  * the parallel scan over to it).  A sequence of L tokens has L-1 steps (the chain's edges),
@@ -223,6 +228,7 @@ ts_status ts_semimarkov_viterbi(const float* sp, const int32_t* lengths, int64_t
                                 int64_t K, int64_t C, int32_t* path, int32_t* seglen,
                                 float* score, void* ws, size_t ws_bytes, void* stream);
 
+/* Message for the last non-OK status returned to the calling thread ("" if none). */
 const char* ts_last_error(void);
 
 #ifdef __cplusplus

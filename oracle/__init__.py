@@ -47,6 +47,9 @@ def load_library(path):
     for name in ("orc_viterbi", "orc_viterbi_f64"):
         getattr(lib, name).argtypes = [p, p, i64, i64, i64, p, p]
     lib.orc_marginals_seq.argtypes = [p, p, i64, i64, i64, i64, i64, i64, p, p]
+    if hasattr(lib, "orc_messages"):
+        lib.orc_messages.argtypes = [p, p, i64, i64, i64, p, p, p]
+        lib.orc_edge_marginals.argtypes = [p, p, i64, i64, i64, p, p, p, i64, i64, i64, p]
     if hasattr(lib, "orc_entropy"):
         lib.orc_entropy.argtypes = [p, p, i64, i64, i64, p]
         lib.orc_log_density.argtypes = [p, p, p, i64, i64, i64, p]
@@ -180,6 +183,35 @@ def marginals_seq(pot, lengths, b, t0, t1):
     _check(_load().orc_marginals_seq(_ptr(pot), _ptr(lengths), B, N, C, b, t0, t1, _ptr(out),
                                      ctypes.addressof(logz)))
     return out, logz.value
+
+
+class Messages:
+    """Forward and backward log-messages of every sequence (one pass of the recursions),
+    from which the marginals of any range of edges can be formed in bounded memory."""
+
+    def __init__(self, pot, lengths=None, lib=None):
+        pot, lengths, f64, B, N, C = _prep(pot, lengths)
+        if f64:
+            raise ValueError("Messages takes fp32 potentials")
+        self._lib = _load(lib)
+        self.pot, self.lengths, self.B, self.N, self.C = pot, lengths, B, N, C
+        self.alpha = np.empty((B, N, C), np.float64)
+        self.beta = np.empty((B, N, C), np.float64)
+        self.logz = np.empty(B, np.float64)
+        _check(self._lib.orc_messages(_ptr(pot), _ptr(lengths), B, N, C, _ptr(self.alpha),
+                                      _ptr(self.beta), _ptr(self.logz)))
+
+    def edge_marginals(self, b, t0, t1, out=None):
+        """Marginals of edges [t0, t1) of sequence b, float64 [(t1-t0), C, C] (0 for
+        padding edges); bitwise equal to the same slice of marginals()."""
+        C = self.C
+        if out is None:
+            out = np.empty((t1 - t0, C, C), np.float64)
+        assert out.dtype == np.float64 and out.flags.c_contiguous and out.shape == (t1 - t0, C, C)
+        _check(self._lib.orc_edge_marginals(_ptr(self.pot), _ptr(self.lengths), self.B, self.N,
+                                            C, _ptr(self.alpha), _ptr(self.beta),
+                                            _ptr(self.logz), b, t0, t1, _ptr(out)))
+        return out
 
 
 def max_threads():

@@ -602,6 +602,55 @@ int orc_marginals_seq(const float* pot, const int32_t* lengths, int64_t B, int64
     return ORC_OK;
 }
 
+/*
+ * Streamed marginals, for sizes where the float64 tensor [B, N-1, C, C] is too large to
+ * hold at once.  orc_messages runs the forward and backward recursions of every sequence
+ * once (the same fwd_bwd_seq as orc_marginals): alpha and beta are [B, N, C] (rows at or
+ * past a sequence's length are left unwritten), logZ is [B].  orc_edge_marginals then
+ * forms the marginals of edges t0 <= t < t1 of sequence b from them with the same
+ * edge_marginal as orc_marginals, so the two agree bitwise; out is [(t1-t0), C, C] and
+ * edges at or past the sequence's last edge are 0.
+ */
+int orc_messages(const float* pot, const int32_t* lengths, int64_t B, int64_t N, int64_t C,
+                 double* alpha, double* beta, double* logZ) {
+    int rc = check_args(pot, NULL, lengths, B, N, C);
+    if (rc) return rc;
+    if (!alpha || !beta || !logZ) return ORC_ERR_ARG;
+    int err = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        int64_t L = lengths ? lengths[b] : N;
+        double* tmp = malloc(sizeof(double) * C);
+        if (!tmp) {
+#pragma omp atomic write
+            err = 1;
+        } else {
+            logZ[b] = fwd_bwd_seq(pot, NULL, N, C, b, L, alpha + b * N * C, beta + b * N * C, tmp);
+        }
+        free(tmp);
+    }
+    return err ? ORC_ERR_MEM : ORC_OK;
+}
+
+int orc_edge_marginals(const float* pot, const int32_t* lengths, int64_t B, int64_t N,
+                       int64_t C, const double* alpha, const double* beta, const double* logZ,
+                       int64_t b, int64_t t0, int64_t t1, double* out) {
+    if (!pot || !alpha || !beta || !logZ || !out || b < 0 || b >= B || t0 < 0 || t1 < t0 ||
+        t1 > N - 1 || C < 1)
+        return ORC_ERR_ARG;
+    int64_t L = lengths ? lengths[b] : N;
+    if (L < 1 || L > N) return ORC_ERR_ARG;
+#pragma omp parallel for schedule(static)
+    for (int64_t t = t0; t < t1; ++t) {
+        double* o = out + (t - t0) * C * C;
+        if (t + 1 < L)
+            edge_marginal(pot, NULL, N, C, b, t, alpha + b * N * C, beta + b * N * C, logZ[b], o);
+        else
+            memset(o, 0, sizeof(double) * C * C);
+    }
+    return ORC_OK;
+}
+
 /* semi-Markov CRF: sp [B, N-1, K, C, C] (fp32 widened exactly, or float64) */
 int orc_semi_marginals(const float* sp, const int32_t* lengths, int64_t B, int64_t N, int64_t K,
                        int64_t C, double* logZ, double* marg) {

@@ -1,7 +1,10 @@
-"""Build the HIP library libtschain.so in-tree with hipcc for gfx950."""
+"""Build the HIP library libtschain.so in-tree with hipcc for gfx950: every source is
+compiled to an object of its own (in parallel), then the objects are linked."""
 import glob
 import os
 import subprocess
+import tempfile
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
@@ -9,7 +12,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libtschain.so")
 
 HIPCC_FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     # hand-written code must not be turned into packed fp32 VALU ops
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # NaN inputs are undefined (infinities are honoured): lets fmax map to one v_max
@@ -22,18 +25,31 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip"))) + [os.path.join(CSRC, "api.cpp")]
 
 
+def _run(cmd):
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError("hipcc failed:\n" + " ".join(cmd) + "\n" + res.stdout + res.stderr)
+    return res.stdout + res.stderr
+
+
 def build(verbose=False):
     """Compile every HIP source and the C-ABI layer into libtschain.so (always rebuilds)."""
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    tmp = LIB + ".tmp"
-    cmd = [hipcc, *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-I", CSRC,
-           *sources(), "-o", tmp]
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        raise RuntimeError("hipcc failed:\n" + res.stdout + res.stderr)
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
+    jobs = max(1, min(len(sources()), int(os.environ.get("MAX_JOBS", os.cpu_count() or 1))))
+    with tempfile.TemporaryDirectory(prefix="tschain-build-") as tmpdir:
+        objs, cmds = [], []
+        for src in sources():
+            obj = os.path.join(tmpdir, os.path.basename(src) + ".o")
+            objs.append(obj)
+            cmds.append([hipcc, *HIPCC_FLAGS, *inc, "-c", src, "-o", obj])
+        with ThreadPoolExecutor(jobs) as pool:
+            logs = list(pool.map(_run, cmds))
+        tmp = LIB + ".tmp"
+        logs.append(_run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]))
     if verbose:
         noise = "packed-fp32-ops"
-        msg = "\n".join(l for l in (res.stdout + res.stderr).splitlines() if noise not in l)
+        msg = "\n".join(l for l in "\n".join(logs).splitlines() if noise not in l)
         if msg.strip():
             print(msg)
     os.replace(tmp, LIB)

@@ -388,7 +388,10 @@ ts_status ts_chain_marginals_viterbi(const float* pot, const int32_t* lengths, i
     Plan pm, pv;
     ts_status st = check_dims(pot, B, N, C, TS_OP_MARGINALS, &pm);
     if (st != TS_OK) return st;
-    make_plan(TS_OP_VITERBI, B, N, C, nullptr, &pv);
+    // the Viterbi plan can fail where the marginals plan does not (its decode tables must
+    // fit in LDS): report that before anything is launched, as ts_chain_viterbi does
+    if (!make_plan(TS_OP_VITERBI, B, N, C, nullptr, &pv))
+        return fail(TS_ERR_BAD_DIM, "problem size overflows the supported range");
     // the marginals plan first, then the Viterbi plan (both sizes are multiples of 256)
     if ((st = check_ws(pm.bytes + pv.bytes, ws, ws_bytes)) != TS_OK) return st;
     if (N > 1 && !marg) return fail(TS_ERR_NULL_ARG, "marg is NULL");

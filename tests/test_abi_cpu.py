@@ -209,3 +209,21 @@ def test_semimarkov_bad_arguments_are_rejected(L):
     assert vit(FAKE, None, B, N, K, C, FAKE, None, FAKE, FAKE, need, None) == NULL_ARG
     assert vit(FAKE, None, B, N, K, C, FAKE, FAKE, None, FAKE, need, None) == NULL_ARG
     assert vit(FAKE, None, B, N, K, C, FAKE, FAKE, FAKE, FAKE, need - 1, None) == WORKSPACE
+
+
+def test_viterbi_decode_length_limit_is_rejected(L):
+    # the backtrace tables must fit in LDS: with C = 256 at most 65536 edges per sequence.
+    # The marginals plan alone accepts this size; the combined call must still refuse it
+    # (before any device call) as ts_chain_viterbi does.
+    B, N, C = 1, 70000, 256
+    assert binding.workspace_bytes(1, B, N, C) > 0
+    assert binding.workspace_bytes(2, B, N, C) == 0
+    assert binding.workspace_bytes(3, B, N, C) == 0
+    big = 1 << 40
+    assert L.ts_chain_viterbi(FAKE, None, B, N, C, FAKE, FAKE, FAKE, big, None) == BAD_DIM
+    assert L.ts_chain_marginals_viterbi(FAKE, None, B, N, C, FAKE, FAKE, FAKE, FAKE, FAKE, big,
+                                        None) == BAD_DIM
+    assert "overflow" in _err(L) or "range" in _err(L)
+    # the largest accepted length at C = 256 (65536 edges)
+    assert binding.workspace_bytes(2, 1, 65537, C) > 0
+    assert binding.workspace_bytes(2, 1, 65538, C) == 0

@@ -2,11 +2,13 @@
 the same caller uniforms, on both paths (single launch and multi-launch tree).
 
 The draws are integers decided by floating point: the GPU takes them from fp32 marginals
-(within ~1e-6 relative of the oracle's) by an fp32 inverse CDF, the oracle from fp64
-ones.  The two can differ only where u * total falls within that error of a bin edge: so
-every sequence whose GPU path differs from the oracle's must have an oracle draw margin
-(distance of u * total from the nearest bin edge, relative to the total) below
-MARGIN_TOL, and such sequences must be rare.  Every drawn transition must have a finite
+by an fp32 inverse CDF, the oracle from fp64 ones.  The two can differ only where u * total
+falls within the GPU's error of a bin edge.  That error, relative to the total, is bounded
+by the fp32 prefix sum of at most C <= 256 non-negative weights (C * 2^-24 <= 1.5e-5) plus
+the weights' own relative error (the marginals' ~1e-6), so MARGIN_TOL = 2e-5: every
+sequence whose GPU path differs from the oracle's must have an oracle draw margin (distance
+of u * total from the nearest bin edge, relative to the total) below it, and such
+sequences must be rare.  Every drawn transition must have a finite
 potential, and closed forms (uniform potentials give floor(u * C)) hold exactly.
 """
 import numpy as np
@@ -18,7 +20,7 @@ from paper_2002_00876_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
 
-MARGIN_TOL = 1e-3
+MARGIN_TOL = 2e-5
 MAX_DIFF_FRAC = 0.02
 
 
@@ -72,7 +74,8 @@ def _check_parity(pot, lens, u, tag):
         assert worst < MARGIN_TOL, (
             f"{diff.sum()} sequences differ; one has oracle margin {worst:.2e}")
     assert diff.mean() <= MAX_DIFF_FRAC, f"{diff.mean():.3f} of the sequences differ"
-    say(f"  {diff.sum()} of {diff.size} sampled sequences differ (all at bin edges)")
+    say(f"  {diff.sum()} of {diff.size} sampled sequences differ (all at bin edges; worst "
+        f"oracle margin {margin[diff].max(initial=0.0):.2e})")
     return z
 
 

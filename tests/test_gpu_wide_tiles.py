@@ -1,0 +1,32 @@
+"""Parity of the multi-launch tree on shapes whose lower levels take the 128-wide output
+tiles of the log-semiring product (a level uses them when it has at least 512 such tiles),
+every marginal compared element by element: dense rows (C a multiple of 4, 16-byte loads)
+and odd label counts (scalar loads), ragged lengths and exact integer ties."""
+import numpy as np
+import pytest
+
+from gpu_util import check_all
+from paper_2002_00876_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+CASES = [
+    # (B, N, C, lengths): level 1 has B * 128 nodes, i.e. >= 512 tiles of 128 x 128
+    (4, 257, 128, [257, 200, 131, 64]),
+    (2, 129, 256, [129, 77]),
+    (2, 257, 256, [257, 190]),
+    (2, 257, 130, [257, 101]),    # two tiles per dimension, the second one ragged
+    (3, 300, 192, [300, 299, 150]),
+]
+
+
+@pytest.mark.parametrize("B,N,C,lens", CASES)
+def test_wide_tiles_normal(B, N, C, lens):
+    pot, lens = W.random_case(3000 + N + C, B, N, C, sigma=1.5, lengths=lens)
+    check_all(pot, lens, f"wide tiles B={B} N={N} C={C}")
+
+
+@pytest.mark.parametrize("B,N,C,lens", [CASES[0], CASES[3]])
+def test_wide_tiles_integer_ties(B, N, C, lens):
+    pot, lens = W.random_case(4000 + N + C, B, N, C, kind="int", int_range=1, lengths=lens)
+    check_all(pot, lens, f"wide tiles, ties B={B} N={N} C={C}")

@@ -262,6 +262,23 @@ def test_marginals_seq_matches_full():
         np.testing.assert_array_equal(part, m[b, 2:11])
 
 
+@pytest.mark.parametrize("B,N,C,lens", [(3, 12, 4, [12, 7, 1]), (2, 40, 9, [40, 2]),
+                                        (4, 17, 1, None)])
+def test_streamed_messages_match_full(B, N, C, lens):
+    # the streamed entry points (messages once, then any range of edges) inherit every pin
+    # of orc_marginals: they must reproduce its output bitwise, padding included
+    pot, lens = W.random_case(10 + N, B, N, C, lengths=lens if lens is not None else "full")
+    z, m = oracle.marginals(pot, lens)
+    msg = oracle.Messages(pot, lens)
+    np.testing.assert_array_equal(msg.logz, z)
+    for b in range(B):
+        for t0, t1 in ((0, N - 1), (0, 1), (N // 3, N - 1), (N - 2, N - 1)):
+            if 0 <= t0 <= t1 <= N - 1:
+                np.testing.assert_array_equal(msg.edge_marginals(b, t0, t1), m[b, t0:t1])
+    with pytest.raises(ValueError):
+        msg.edge_marginals(0, 0, N)          # past the last edge of the batch
+
+
 def test_oracle_rejects_bad_lengths():
     pot = np.zeros((2, 3, 2, 2), np.float32)
     with pytest.raises(ValueError):
