@@ -567,6 +567,352 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
     }
 }
 
+// The same product for full tiles (C a multiple of TM, no finiteness masks), scheduled for
+// the matrix cores: the raw potentials of slice s + 2 are loaded during slice s (two
+// register sets, so a load has a whole slice to arrive); the exponentials of slice s + 1
+// are spread over the four 8-wide k groups of slice s, between their products; and each
+// group's LDS operands are read before the previous group's products are issued.  No
+// per-entry masks are needed: every row, column and contracted index of a tile is valid.
+// An operand is exp2(fma(x, log2 e, o log2 e) - s log2 e), the thread's shifts scaled once.
+template <int TM>
+struct UpFullSmem {
+    static constexpr int LDA = kSlice + 4, LDB = TM + 4, LDT = TM + 1;
+    static constexpr int kBuf = TM * LDA + kSlice * LDB;
+    static constexpr int kTileF = TM * LDT;
+    static constexpr int kMain = (2 * kBuf > kTileF ? 2 * kBuf : kTileF);
+    // coh, roh, and both scaled by log2 e [kMaxLabels]; sa, sb, cof, rof [TM]; red [2 doubles
+    // per wave]
+    static constexpr int kFloats = kMain + 4 * kMaxLabels + 4 * TM + 4 * (kUpThreads / kWave);
+    static constexpr size_t kBytes = sizeof(float) * kFloats;
+};
+
+template <int TM>
+__global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
+    using Sm = UpFullSmem<TM>;
+    constexpr int LDA = Sm::LDA, LDB = Sm::LDB, LDT = Sm::LDT;
+    constexpr int BR = TM / 64;                 // 32 x 32 blocks per wave per dimension
+    constexpr int QW = TM / 2;                  // a wave's quarter edge
+    constexpr float kL2E = 1.4426950408889634f;
+    extern __shared__ __align__(16) float smem[];
+    const int ntiles = a.ntile * a.ntile;
+    const int64_t lid = xcd_node_swizzle(blockIdx.x, ntiles);
+    if (lid >= a.nlogical) return;
+    const int tile = (int)(lid % ntiles);
+    const int64_t node = lid / ntiles;
+    const int64_t b = node / a.nodes, k = node % a.nodes;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    const int64_t span = (int64_t)1 << a.level, half = span >> 1;
+    if (k * span >= Eb) return;  // node absent: all padding
+    const int C = (int)a.C;
+    const int tm = tile / a.ntile, tn = tile % a.ntile;
+    const int a0 = tm * TM, c0 = tn * TM;
+    const int tid = threadIdx.x;
+    const int nt = a.ntile, cnt = a.cntile;
+
+    const int64_t cl = b * a.cnodes + 2 * k, cr = cl + 1, pn = b * a.nodes + k;
+    const float* Lc = a.ccore + (size_t)cl * C * C;
+    float* Pc = a.core + (size_t)pn * C * C;
+    double* Pro = a.ro + (size_t)pn * C;
+    double* Pco = a.co + (size_t)pn * C;
+    float* Pmr = a.pmr + (size_t)pn * C * nt;
+    float* Pmc = a.pmc + (size_t)pn * C * nt;
+
+    if (!((2 * k + 1) * half < Eb)) {
+        // the right half is padding: the node equals its left child (tile, offsets and the
+        // maximum of each line's partials, kept in partial 0)
+        constexpr int kQ = TM / 4;
+        for (int idx = tid; idx < TM * kQ; idx += kUpThreads) {
+            const int r = a0 + idx / kQ, c = c0 + 4 * (idx % kQ);
+            *(float4*)(Pc + (size_t)r * C + c) = *(const float4*)(Lc + (size_t)r * C + c);
+        }
+        if (tn == 0)
+            for (int i = tid; i < TM; i += kUpThreads)
+                Pro[a0 + i] = a.cro ? a.cro[(size_t)cl * C + a0 + i] : 0.0;
+        if (tm == 0)
+            for (int i = tid; i < TM; i += kUpThreads)
+                Pco[c0 + i] = a.cco ? a.cco[(size_t)cl * C + c0 + i] : 0.0;
+        if (tm == 0 && tn == 0)
+            for (int i = tid; i < C * nt; i += kUpThreads) {
+                const int line = i / nt, p = i % nt;
+                const float* sr = a.cpmr + ((size_t)cl * C + line) * cnt;
+                const float* sc = a.cpmc + ((size_t)cl * C + line) * cnt;
+                float mr = -INFINITY, mc = -INFINITY;
+                if (p == 0)
+                    for (int q = 0; q < cnt; ++q) {
+                        mr = fmaxf(mr, sr[q]);
+                        mc = fmaxf(mc, sc[q]);
+                    }
+                Pmr[i] = mr;
+                Pmc[i] = mc;
+            }
+        return;
+    }
+    const float* Rc = a.ccore + (size_t)cr * C * C;
+    const double* Lro = a.cro ? a.cro + (size_t)cl * C : nullptr;
+    const double* Lco = a.cco ? a.cco + (size_t)cl * C : nullptr;
+    const double* Rro = a.cro ? a.cro + (size_t)cr * C : nullptr;
+    const double* Rco = a.cco ? a.cco + (size_t)cr * C : nullptr;
+
+    float* coh = smem + Sm::kMain;       // [kMaxLabels] co_L - max co_L
+    float* roh = coh + kMaxLabels;       // [kMaxLabels] ro_R - max ro_R
+    float* cohs = roh + kMaxLabels;      // [kMaxLabels] coh log2 e
+    float* rohs = cohs + kMaxLabels;     // [kMaxLabels] roh log2 e
+    float* sa = rohs + kMaxLabels;       // [TM] row shifts of the tile
+    float* sb = sa + TM;                 // [TM] column shifts
+    float* cof = sb + TM;                // [TM] co_P of the tile's columns (float)
+    float* rof = cof + TM;               // [TM] ro_P of the tile's rows (float)
+    double* red = reinterpret_cast<double*>(rof + TM);
+
+    // ---- per-thread staging assignment (fixed over the slices):
+    //   A'' (TM x 32): rows ar + 32 it (it < NA), contracted indices ak .. ak + 3;
+    //   B'' (32 x TM): contracted rows bk .. bk + NB - 1, columns bc .. bc + 3
+    constexpr int GA = kSlice / 4, NA = TM * GA / kUpThreads;
+    constexpr int GB = TM / 4, NB = kSlice * GB / kUpThreads;
+    static_assert(NB == 4 || NB == 2, "contracted rows of a thread: one or half a float4");
+    const int ar = tid / GA, ak = 4 * (tid % GA);
+    const int bk = NB * (tid / GB), bc = 4 * (tid % GB);
+    const float* Lrow = Lc + (size_t)(a0 + ar) * C + ak;
+    const float* Rrow = Rc + (size_t)bk * C + c0 + bc;
+    float4 ra[2][NA], rb[2][NB];
+    auto gload = [&](float4 (&xa)[NA], float4 (&xb)[NB], int ks) {
+#pragma unroll
+        for (int it = 0; it < NA; ++it) xa[it] = *(const float4*)(Lrow + (size_t)(32 * it) * C + ks);
+#pragma unroll
+        for (int it = 0; it < NB; ++it) xb[it] = *(const float4*)(Rrow + (size_t)(ks + it) * C);
+    };
+    float sas[NA], sbs[4];
+    // the offsets of the staged contracted indices (A: ak..ak+3, B: bk..bk+NB-1), scaled by
+    // log2 e, read from LDS once per slice
+    auto offsets = [&](float (&oa)[4], float (&ob)[4], int ks) {
+        const float4 x = *(const float4*)(cohs + ks + ak);
+        oa[0] = x.x; oa[1] = x.y; oa[2] = x.z; oa[3] = x.w;
+        if constexpr (NB == 4) {
+            const float4 y = *(const float4*)(rohs + ks + bk);
+            ob[0] = y.x; ob[1] = y.y; ob[2] = y.z; ob[3] = y.w;
+        } else {
+            const float2 y = *(const float2*)(rohs + ks + bk);
+            ob[0] = y.x; ob[1] = y.y; ob[2] = ob[3] = 0.f;
+        }
+    };
+    // exponentials of staged part `part` of `nparts` (A groups, then B groups) into buffer buf
+    auto stage = [&](const float4 (&xa)[NA], const float4 (&xb)[NB], const float (&oa)[4],
+                     const float (&ob)[4], int buf, int part, int nparts) {
+        float* As = smem + buf * Sm::kBuf;
+        float* Bs = As + TM * LDA;
+#pragma unroll
+        for (int it = NA * part / nparts; it < NA * (part + 1) / nparts; ++it) {
+            float4 x;
+            x.x = __builtin_amdgcn_exp2f(fmaf(xa[it].x, kL2E, oa[0]) - sas[it]);
+            x.y = __builtin_amdgcn_exp2f(fmaf(xa[it].y, kL2E, oa[1]) - sas[it]);
+            x.z = __builtin_amdgcn_exp2f(fmaf(xa[it].z, kL2E, oa[2]) - sas[it]);
+            x.w = __builtin_amdgcn_exp2f(fmaf(xa[it].w, kL2E, oa[3]) - sas[it]);
+            *(float4*)(As + (ar + 32 * it) * LDA + ak) = x;
+        }
+#pragma unroll
+        for (int it = NB * part / nparts; it < NB * (part + 1) / nparts; ++it) {
+            float4 x;
+            x.x = __builtin_amdgcn_exp2f(fmaf(xb[it].x, kL2E, ob[it]) - sbs[0]);
+            x.y = __builtin_amdgcn_exp2f(fmaf(xb[it].y, kL2E, ob[it]) - sbs[1]);
+            x.z = __builtin_amdgcn_exp2f(fmaf(xb[it].z, kL2E, ob[it]) - sbs[2]);
+            x.w = __builtin_amdgcn_exp2f(fmaf(xb[it].w, kL2E, ob[it]) - sbs[3]);
+            *(float4*)(Bs + (bk + it) * LDB + bc) = x;
+        }
+    };
+
+    // ---- the first two slices' loads and every global read of the set-up go out at once
+    const int nslices = C / kSlice;   // even: C is a multiple of 64
+    gload(ra[0], rb[0], 0);
+    gload(ra[1], rb[1], kSlice);
+    static_assert(kMaxLabels <= kUpThreads, "one offset of the contracted index per thread");
+    const double lco = (Lco && tid < C) ? Lco[tid] : -INFINITY;
+    const double rro = (Rro && tid < C) ? Rro[tid] : -INFINITY;
+    float pa = -INFINITY, pb = -INFINITY;
+    if (tid < TM) {
+        const float* p = a.cpmr + ((size_t)cl * C + a0 + tid) * cnt;
+        for (int q = 0; q < cnt; ++q) pa = fmaxf(pa, p[q]);
+        const float* r = a.cpmc + ((size_t)cr * C + c0 + tid) * cnt;
+        for (int q = 0; q < cnt; ++q) pb = fmaxf(pb, r[q]);
+    }
+    {
+        const double lw = wave_max_d(lco), rw = wave_max_d(rro);
+        const int w = tid / kWave;
+        if ((tid & (kWave - 1)) == 0) {
+            red[2 * w] = lw;
+            red[2 * w + 1] = rw;
+        }
+    }
+    __syncthreads();
+    double lmax = red[0], rmax = red[1];
+#pragma unroll
+    for (int w = 1; w < kUpThreads / kWave; ++w) {
+        lmax = fmax(lmax, red[2 * w]);
+        rmax = fmax(rmax, red[2 * w + 1]);
+    }
+    const double coLshift = Lco ? safe_shift_d(lmax) : 0.0;
+    const double roRshift = Rro ? safe_shift_d(rmax) : 0.0;
+    if (tid < C) {
+        const float ch = Lco ? (float)(lco - coLshift) : 0.f;
+        const float rh = Rro ? (float)(rro - roRshift) : 0.f;
+        coh[tid] = ch;
+        roh[tid] = rh;
+        cohs[tid] = ch * kL2E;
+        rohs[tid] = rh * kL2E;
+    }
+    if (tid < TM) {
+        sa[tid] = safe_shift(pa - (float)coLshift);
+        sb[tid] = safe_shift(pb - (float)roRshift);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int it = 0; it < NA; ++it) sas[it] = sa[ar + 32 * it] * kL2E;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) sbs[q] = sb[bc + q] * kL2E;
+    {
+        float oa[4], ob[4];
+        offsets(oa, ob, 0);
+        stage(ra[0], rb[0], oa, ob, 0, 0, 1);
+    }
+    __syncthreads();
+
+    // ---- products: wave (wm, wn) owns rows wm*QW.., columns wn*QW.. as BR x BR blocks.
+    // Within each 8-wide k group lanes 0-31 contribute k..k+3 and lanes 32-63 k+4..k+7 (one
+    // 16-byte LDS read of A per block row, four reads of B per block column).
+    const int w = tid / kWave, lane = tid % kWave;
+    const int wm = w >> 1, wn = w & 1;
+    f16v acc[BR][BR];
+#pragma unroll
+    for (int i = 0; i < BR; ++i)
+#pragma unroll
+        for (int j = 0; j < BR; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    const int aoff = (wm * QW + (lane & 31)) * LDA + 4 * (lane >> 5);
+    const int boff = TM * LDA + (4 * (lane >> 5)) * LDB + wn * QW + (lane & 31);
+    float4 av[2][BR];
+    float bv[2][BR][4];
+    auto lds_ops = [&](float4 (&xa)[BR], float (&xb)[BR][4], int buf, int kk) {
+        const float* base = smem + buf * Sm::kBuf;
+#pragma unroll
+        for (int i = 0; i < BR; ++i) xa[i] = *(const float4*)(base + aoff + i * 32 * LDA + kk);
+#pragma unroll
+        for (int j = 0; j < BR; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) xb[j][q] = base[boff + (kk + q) * LDB + j * 32];
+    };
+    auto mfma_group = [&](const float4 (&xa)[BR], const float (&xb)[BR][4]) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int i = 0; i < BR; ++i)
+#pragma unroll
+                for (int j = 0; j < BR; ++j) {
+                    const float ax = q == 0 ? xa[i].x : q == 1 ? xa[i].y : q == 2 ? xa[i].z : xa[i].w;
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ax, xb[j][q], acc[i][j], 0, 0, 0);
+                }
+    };
+    // one slice: products of buffer `cur` while slice s + 1 (raw set xa1/xb1) is staged into
+    // the other buffer and slice s + 2 is loaded into the set just consumed (xa0/xb0).  After
+    // the last slice the staging works on stale registers into a buffer nobody reads (no
+    // branch, so the products and the staging form one block the scheduler can interleave).
+    auto slice = [&](int s, int cur, float4 (&xa0)[NA], float4 (&xb0)[NB], float4 (&xa1)[NA],
+                     float4 (&xb1)[NB]) {
+        if (s + 2 < nslices) gload(xa0, xb0, (s + 2) * kSlice);
+        float oa[4], ob[4];
+        offsets(oa, ob, min(s + 1, nslices - 1) * kSlice);
+        lds_ops(av[0], bv[0], cur, 0);
+#pragma unroll
+        for (int g = 0; g < kSlice / 8; ++g) {
+            if (g + 1 < kSlice / 8) lds_ops(av[(g + 1) & 1], bv[(g + 1) & 1], cur, 8 * (g + 1));
+            stage(xa1, xb1, oa, ob, cur ^ 1, g, kSlice / 8);
+            mfma_group(av[g & 1], bv[g & 1]);
+            // one product, then two VALU instructions (the staging), and the operand reads
+            // of the next group and the staging's stores spread over the products
+#pragma unroll
+            for (int i = 0; i < 4 * BR * BR; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+                if (i % 2 == 0) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                if (i % 8 == 7) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+            }
+        }
+        __syncthreads();
+    };
+    for (int s = 0; s < nslices; s += 2) {
+        slice(s, 0, ra[0], rb[0], ra[1], rb[1]);
+        slice(s + 1, 1, ra[1], rb[1], ra[0], rb[0]);
+    }
+
+    // ---- epilogue: core = log S into an LDS tile; entries whose S underflowed are
+    // recomputed afterwards by a direct log-sum-exp (a rare, non-unrolled path)
+    float* T = smem;   // [TM][LDT], over the slice buffers (all reads are done)
+    uint64_t under = 0;
+#pragma unroll
+    for (int i = 0; i < BR; ++i)
+#pragma unroll
+        for (int j = 0; j < BR; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = wm * QW + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+                const int col = wn * QW + j * 32 + (lane & 31);
+                const float S = acc[i][j][r];
+                T[row * LDT + col] = flog(S);
+                if (!(S >= kUnderflow)) under |= 1ull << ((i * BR + j) * 16 + r);
+            }
+    while (under) {
+        const int bit = __builtin_ctzll(under);
+        under &= under - 1;
+        const int ij = bit >> 4, r = bit & 15, i = ij / BR, j = ij % BR;
+        const int row = wm * QW + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        const int col = wn * QW + j * 32 + (lane & 31);
+        const int gr = a0 + row, gc = c0 + col;
+        const float sr = sa[row], sc = sb[col];
+        const float* lrow = Lc + (size_t)gr * C;
+        float q = -INFINITY;
+        for (int bb = 0; bb < C; ++bb)
+            q = fmaxf(q, (lrow[bb] + coh[bb] - sr) + (Rc[(size_t)bb * C + gc] + roh[bb] - sc));
+        float val = -INFINITY;
+        if (q != -INFINITY) {
+            float sum = 0.f;
+            for (int bb = 0; bb < C; ++bb)
+                sum += fexp((lrow[bb] + coh[bb] - sr) + (Rc[(size_t)bb * C + gc] + roh[bb] - sc) - q);
+            val = q + flog(sum);
+        }
+        T[row * LDT + col] = val;
+    }
+    // the output node's offsets for the tile's rows and columns
+    for (int i = tid; i < TM; i += kUpThreads) {
+        const double ro = (Lro ? Lro[a0 + i] : 0.0) + coLshift + sa[i];
+        const double co = (Rco ? Rco[c0 + i] : 0.0) + roRshift + sb[i];
+        rof[i] = (float)ro;
+        cof[i] = (float)co;
+        if (tn == 0) Pro[a0 + i] = ro;
+        if (tm == 0) Pco[c0 + i] = co;
+    }
+    __syncthreads();
+    // partial maxima for the next level: thread t < TM row t, TM <= t < 2 TM column t - TM
+    if (tid < TM) {
+        float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+        for (int c = 0; c < TM; c += 4)
+#pragma unroll
+            for (int u = 0; u < 4; ++u) m[u] = fmaxf(m[u], T[tid * LDT + c + u] + cof[c + u]);
+        Pmr[(size_t)(a0 + tid) * nt + tn] = fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3]));
+    } else if (tid < 2 * TM) {
+        const int c = tid - TM;
+        float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+        for (int r = 0; r < TM; r += 4)
+#pragma unroll
+            for (int u = 0; u < 4; ++u) m[u] = fmaxf(m[u], T[(r + u) * LDT + c] + rof[r + u]);
+        Pmc[(size_t)(c0 + c) * nt + tm] = fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3]));
+    }
+    // the tile, row by row, 16 bytes per store
+    constexpr int kQ = TM / 4;
+    for (int idx = tid; idx < TM * kQ; idx += kUpThreads) {
+        const int r = idx / kQ, c4 = idx % kQ;
+        const float* t = T + r * LDT + 4 * c4;
+        *(float4*)(Pc + (size_t)(a0 + r) * C + c0 + 4 * c4) = make_float4(t[0], t[1], t[2], t[3]);
+    }
+}
+
 // ---------------------------------------------------------------- root: log Z
 struct RootArgs {
     const float* core;   // level D core, or the potentials when D == 0
@@ -1121,10 +1467,27 @@ hipError_t allow_up_lds() {
     return hipSuccess;
 }
 
+template <int TM>
+hipError_t allow_up_full_lds() {
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute((const void*)k_up_log_full<TM>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)UpFullSmem<TM>::kBytes);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    return hipSuccess;
+}
+
 template <bool VEC, bool kBits>
 hipError_t up_sweep_vec(const Plan& p, const float* pot, const int32_t* lengths, hipStream_t s) {
     hipError_t e = allow_up_lds<64, VEC, kBits>();
     if (e == hipSuccess && p.C > 64) e = allow_up_lds<128, VEC, kBits>();
+    // full tiles (every tile edge divides C; dense chains): the scheduled kernel
+    const bool full64 = !kBits && p.C % 64 == 0, full128 = !kBits && p.C % 128 == 0;
+    if (e == hipSuccess && full64) e = allow_up_full_lds<64>();
+    if (e == hipSuccess && full128) e = allow_up_full_lds<128>();
     if (e != hipSuccess) return e;
     // the leaves' row and column maxima (shifts of the level-1 products)
     LeafMaxArgs m{pot, lengths, p.N, p.C, p.lrmax, p.lcmax, p.rbits[0], p.cbits[0], p.bw};
@@ -1153,7 +1516,14 @@ hipError_t up_sweep_vec(const Plan& p, const float* pot, const int32_t* lengths,
         a.ntile = nt;
         a.nlogical = p.B * a.nodes * nt * nt;
         a.ngrid = node_grid(p.B * a.nodes, nt * nt);
-        if (up_tile(p.C, p.B * a.nodes) == 64)
+        const int tm = up_tile(p.C, p.B * a.nodes);
+        if (tm == 64 && full64)
+            hipLaunchKernelGGL((k_up_log_full<64>), dim3((unsigned)a.ngrid), dim3(kUpThreads),
+                               UpFullSmem<64>::kBytes, s, a);
+        else if (tm == 128 && full128)
+            hipLaunchKernelGGL((k_up_log_full<128>), dim3((unsigned)a.ngrid), dim3(kUpThreads),
+                               UpFullSmem<128>::kBytes, s, a);
+        else if (tm == 64)
             hipLaunchKernelGGL((k_up_log<64, VEC, kBits>), dim3((unsigned)a.ngrid), dim3(kUpThreads),
                                UpSmem<64>::kBytes, s, a);
         else
