@@ -228,6 +228,25 @@ ts_status ts_semimarkov_viterbi(const float* sp, const int32_t* lengths, int64_t
                                 int64_t K, int64_t C, int32_t* path, int32_t* seglen,
                                 float* score, void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * ts_chain_marginals without a workspace argument, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation.  Arguments, outputs, layout and errors are those of ts_chain_marginals without
+ * ws / ws_bytes; the kernels and the results are the same.  The call allocates nothing: its
+ * scratch is one array of ts_chain_noalloc_scratch_bytes() bytes (64 MiB) per GPU inside the
+ * library, held from the first call on that GPU until the process ends.  A problem whose
+ * ts_chain_workspace_bytes(TS_OP_MARGINALS, B, N, C) exceeds it returns TS_ERR_BAD_DIM
+ * before any device call (the single-launch path for small label sets needs no scratch).
+ * Every call on one GPU shares that GPU's array, which keeps the last call's contents (the
+ * kernels need none of it cleared): calls that overlap on one GPU, from different streams
+ * or threads, race on it and must be serialised by the caller.  TS_CHECK=1 copies the
+ * lengths synchronously, which graph capture does not allow.
+ */
+size_t ts_chain_noalloc_scratch_bytes(void);
+ts_status ts_chain_marginals_noalloc(const float* pot, const int32_t* lengths, int64_t B,
+                                     int64_t N, int64_t C, float* logZ, float* marg,
+                                     void* stream);
+
 /* Message for the last non-OK status returned to the calling thread ("" if none). */
 const char* ts_last_error(void);
 

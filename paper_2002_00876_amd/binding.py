@@ -39,6 +39,8 @@ def lib():
         L.ts_chain_marginals.argtypes = [p, p, i64, i64, i64, p, p, p, sz, p]
         L.ts_chain_viterbi.argtypes = [p, p, i64, i64, i64, p, p, p, sz, p]
         L.ts_chain_marginals_viterbi.argtypes = [p, p, i64, i64, i64, p, p, p, p, p, sz, p]
+        L.ts_chain_marginals_noalloc.argtypes = [p, p, i64, i64, i64, p, p, p]
+        L.ts_chain_noalloc_scratch_bytes.restype = sz
         L.ts_chain_entropy.argtypes = [p, p, i64, i64, i64, p, p, sz, p]
         L.ts_chain_log_density.argtypes = [p, p, p, i64, i64, i64, p, p, sz, p]
         L.ts_chain_logpartition_sequential.argtypes = [p, p, i64, i64, i64, p, p]
@@ -49,6 +51,7 @@ def lib():
         L.ts_semimarkov_marginals.argtypes = [p, p, i64, i64, i64, i64, p, p, p, sz, p]
         L.ts_semimarkov_viterbi.argtypes = [p, p, i64, i64, i64, i64, p, p, p, p, sz, p]
         for f in ("ts_chain_logpartition", "ts_chain_marginals", "ts_chain_viterbi",
+                  "ts_chain_marginals_noalloc",
                   "ts_chain_marginals_viterbi", "ts_chain_entropy", "ts_chain_log_density",
                   "ts_chain_logpartition_sequential", "ts_chain_sample",
                   "ts_semimarkov_logpartition", "ts_semimarkov_marginals",
@@ -121,6 +124,26 @@ def marginals(pot, lengths=None, out=None, ws=None, want_logz=True):
     _check(lib().ts_chain_marginals(_ptr(pot), _ptr(lengths), B, N, C, _ptr(logz),
                                     _ptr(marg) if N > 1 else None, _ptr(w), nb,
                                     _stream(pot.device)))
+    return logz, marg
+
+
+def noalloc_scratch_bytes():
+    """Bytes of the per-GPU scratch array of the allocation-free marginals call."""
+    return lib().ts_chain_noalloc_scratch_bytes()
+
+
+def marginals_noalloc(pot, lengths=None, out=None, want_logz=True):
+    """marginals() through ts_chain_marginals_noalloc: no workspace; the library's per-GPU
+    scratch array is used instead (calls on one GPU must not overlap)."""
+    pot, lengths, B, N, C = _prep(pot, lengths)
+    if out is not None:
+        logz, marg = out
+    else:
+        logz = torch.empty(B, dtype=torch.float32, device=pot.device) if want_logz else None
+        marg = torch.empty_like(pot)
+    _check(lib().ts_chain_marginals_noalloc(_ptr(pot), _ptr(lengths), B, N, C, _ptr(logz),
+                                            _ptr(marg) if N > 1 else None,
+                                            _stream(pot.device)))
     return logz, marg
 
 

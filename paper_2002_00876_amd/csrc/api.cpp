@@ -91,6 +91,8 @@ bool mul_ok(int64_t a, int64_t b, int64_t* out) {
 
 }  // namespace
 
+int report_error(int code, const char* msg) { return fail(code, msg); }
+
 bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, bool masks) {
     *p = Plan{};
     p->B = B; p->N = N; p->C = C; p->E = N - 1; p->op = op;

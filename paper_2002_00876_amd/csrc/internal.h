@@ -72,6 +72,9 @@ inline int up_tile(int64_t C, int64_t nodes) {
     return nodes * t * t < 512 ? 64 : 128;
 }
 
+// Records `msg` as the calling thread's last error (ts_last_error) and returns `code`.
+int report_error(int code, const char* msg);
+
 // Fills the plan; with base == nullptr only sizes are computed.  Returns false on overflow.
 // masks: keep finiteness bitmasks of the log-semiring nodes (inputs with many structural
 // -inf entries, such as the semi-Markov expansion).

@@ -227,3 +227,16 @@ def test_viterbi_decode_length_limit_is_rejected(L):
     # the largest accepted length at C = 256 (65536 edges)
     assert binding.workspace_bytes(2, 1, 65537, C) > 0
     assert binding.workspace_bytes(2, 1, 65538, C) == 0
+
+
+def test_noalloc_entry_point_rejects_oversized_problems(L):
+    # the allocation-free marginals call checks the workspace it would need against its
+    # fixed per-GPU scratch before any device call
+    cap = L.ts_chain_noalloc_scratch_bytes()
+    assert cap == 64 << 20
+    B, N, C = 4, 400, 128
+    assert binding.workspace_bytes(1, B, N, C) > cap
+    assert L.ts_chain_marginals_noalloc(FAKE, None, B, N, C, FAKE, FAKE, None) == BAD_DIM
+    assert "scratch" in _err(L)
+    # the call's own argument checks still apply
+    assert L.ts_chain_marginals_noalloc(FAKE, None, 0, 5, 3, FAKE, FAKE, None) == BAD_DIM
