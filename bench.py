@@ -48,10 +48,11 @@ def parse():
                     help="bound on the oracle's CPU-baseline run (0 disables it)")
     ap.add_argument("--graph", action="store_true",
                     help="replay one captured HIP graph per step instead of calling the library")
-    ap.add_argument("--sweep", choices=["depth", "labels"], default=None,
+    ap.add_argument("--sweep", choices=["depth", "labels", "large"], default=None,
                     help="instead of the step: log Z by the scan against the left-to-right "
-                         "kernel over sequence lengths (depth: B=16, C=20) or label counts "
-                         "(labels: B=16, N=20); one JSON line per point")
+                         "kernel over sequence lengths (depth: B=16, C=20), label counts "
+                         "(labels: B=16, N=20) or long sequences of many labels (large: B=4, "
+                         "C=128 and 256, N=512..8192); one JSON line per point")
     ap.add_argument("--ops", action="store_true",
                     help="instead of the step: time each entry point separately on the "
                          "workload (log Z by the scan and left to right, marginals, entropy, "
@@ -130,7 +131,8 @@ def calibrate_copy(mib):
 def sweep(kind, reps=20):
     """Time ts_chain_logpartition (the scan) against ts_chain_logpartition_sequential (the
     left-to-right forward algorithm) on seeded N(0,1) potentials with full lengths: the
-    depth-versus-work trade-off of the parallel scan (the paper's Fig. 4a and 4c shapes)."""
+    depth-versus-work trade-off of the parallel scan (the paper's Fig. 4a and 4c shapes, and
+    long sequences of 128 and 256 labels, where the tree does C times the serial work)."""
     import numpy as np
     import torch
 
@@ -138,11 +140,23 @@ def sweep(kind, reps=20):
 
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
-    points = ([(16, n, 20) for n in (26, 51, 101, 201, 301, 401, 501)] if kind == "depth"
-              else [(16, 20, c) for c in (10, 20, 40, 60, 80, 100)])
+    if kind == "depth":
+        points = [(16, n, 20) for n in (26, 51, 101, 201, 301, 401, 501)]
+    elif kind == "labels":
+        points = [(16, 20, c) for c in (10, 20, 40, 60, 80, 100)]
+    else:
+        points = ([(4, n, c) for c in (128, 256) for n in (512, 1024, 2048, 4096, 8192)]
+                  + [(16, 1024, 256)])
+        reps = 3
     for B, N, C in points:
-        rng = np.random.default_rng(1000 + N + C)
-        pot = torch.from_numpy(rng.standard_normal((B, N - 1, C, C)).astype(np.float32)).to(dev)
+        if kind == "large":
+            # drawn on the device (gigabytes of potentials; no oracle takes part)
+            g = torch.Generator(device=dev)
+            g.manual_seed(1000 + N + C)
+            pot = torch.randn((B, N - 1, C, C), generator=g, device=dev, dtype=torch.float32)
+        else:
+            rng = np.random.default_rng(1000 + N + C)
+            pot = torch.from_numpy(rng.standard_normal((B, N - 1, C, C)).astype(np.float32)).to(dev)
         ws = binding._workspace(binding.OP_LOGPARTITION, B, N, C, dev)[0]
         out = torch.empty(B, dtype=torch.float32, device=dev)
 
@@ -161,7 +175,10 @@ def sweep(kind, reps=20):
         ms_scan = timed(lambda: binding.logpartition(pot, out=out, ws=ws))
         ms_seq = timed(lambda: binding.logpartition_sequential(pot, out=out))
         fused = binding.workspace_bytes(binding.OP_LOGPARTITION, B, N, C) == 0
+        tree_flop = 2 * B * max(N - 2, 0) * C ** 3           # tree products: 2 C^3 flop each
+        serial_flop = 2 * B * (N - 1) * C ** 2              # left to right: 2 C^2 per step
         print(json.dumps({"sweep": kind, "B": B, "N": N, "C": C,
+                          "tree_flop": tree_flop, "serial_flop": serial_flop,
                           "scan_ms": round(ms_scan, 5), "sequential_ms": round(ms_seq, 5),
                           "scan_path": "single launch" if fused else "multi-launch tree",
                           "scan_tokens_per_s": round(B * N / (ms_scan * 1e-3), 1),

@@ -845,7 +845,7 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
     // ---- epilogue: core = log S into an LDS tile; entries whose S underflowed are
     // recomputed afterwards by a direct log-sum-exp (a rare, non-unrolled path)
     float* T = smem;   // [TM][LDT], over the slice buffers (all reads are done)
-    uint64_t under = 0;
+    float smin = INFINITY;   // the lane's smallest sum: one compare per entry on the hot path
 #pragma unroll
     for (int i = 0; i < BR; ++i)
 #pragma unroll
@@ -856,8 +856,19 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
                 const int col = wn * QW + j * 32 + (lane & 31);
                 const float S = acc[i][j][r];
                 T[row * LDT + col] = flog(S);
-                if (!(S >= kUnderflow)) under |= 1ull << ((i * BR + j) * 16 + r);
+                smin = fminf(smin, S);
             }
+    uint64_t under = 0;
+    if (!(smin >= kUnderflow)) {
+        // rare: which entries underflowed
+#pragma unroll
+        for (int i = 0; i < BR; ++i)
+#pragma unroll
+            for (int j = 0; j < BR; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    if (!(acc[i][j][r] >= kUnderflow)) under |= 1ull << ((i * BR + j) * 16 + r);
+    }
     while (under) {
         const int bit = __builtin_ctzll(under);
         under &= under - 1;
