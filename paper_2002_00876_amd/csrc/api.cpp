@@ -119,7 +119,9 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, boo
     p->Np = Np; p->D = D;
     Bump bump{static_cast<char*>(base)};
     if (op == TS_OP_LOGPARTITION || op == TS_OP_MARGINALS) {
-        for (int l = 1; l <= D; ++l) {
+        p->chunk = chunk_path(C, masks);
+        p->lc = p->chunk ? (D < kChunkLog ? D : kChunkLog) : 0;
+        for (int l = p->chunk ? (p->lc > 0 ? p->lc : D + 1) : 1; l <= D; ++l) {
             const size_t n = (size_t)B * (size_t)(Np >> l);
             const int tm = up_tile(C, (int64_t)n);
             p->ntile[l] = (int)((C + tm - 1) / tm);
@@ -129,8 +131,10 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, boo
             p->pmr[l] = bump.take<float>(n * C * p->ntile[l]);
             p->pmc[l] = bump.take<float>(n * C * p->ntile[l]);
         }
-        p->lrmax = bump.take<float>((size_t)B * p->E * C);
-        p->lcmax = bump.take<float>((size_t)B * p->E * C);
+        if (!p->chunk) {
+            p->lrmax = bump.take<float>((size_t)B * p->E * C);
+            p->lcmax = bump.take<float>((size_t)B * p->E * C);
+        }
         p->bw = (int)((C + 63) / 64);
         for (int l = 0; masks && l < D; ++l) {
             const size_t n = l == 0 ? (size_t)B * p->E : (size_t)B * (size_t)(Np >> l);
@@ -138,7 +142,7 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, boo
             p->cbits[l] = bump.take<uint64_t>(n * C * p->bw);
         }
         if (op == TS_OP_MARGINALS)
-            for (int l = 1; l < D; ++l) {
+            for (int l = p->chunk ? p->lc : 1; l < D; ++l) {
                 const size_t n = (size_t)B * (size_t)(Np >> l);
                 p->u[l] = bump.take<float>(n * C);
                 p->v[l] = bump.take<float>(n * C);
@@ -284,7 +288,9 @@ const char* plan_semi(int op, int64_t B, int64_t N, int64_t K, int64_t C, SemiPl
         return "problem size overflows the supported range";
     q->KC = K * C;
     if (N == 1) return nullptr;   // one token per sequence: no edges, no workspace
-    if (!make_plan(op, B, N, q->KC, nullptr, &q->base, /*masks=*/true))
+    // finiteness masks only where the expansion has structural zeros (K > 1); with K = 1 the
+    // expanded chain is the chain itself and takes the same kernels
+    if (!make_plan(op, B, N, q->KC, nullptr, &q->base, /*masks=*/K > 1))
         return "problem size overflows the supported range";
     const size_t x = align_up(sizeof(float) * B * (N - 1) * q->KC * q->KC);
     q->xpot = 0;
@@ -545,7 +551,7 @@ ts_status ts_semimarkov_logpartition(const float* sp, const int32_t* lengths, in
         if (q.base.fused) {
             e = launch_small_log(xp, lengths, B, N, q.KC, logZ, nullptr, s);
         } else {
-            make_plan(TS_OP_LOGPARTITION, B, N, q.KC, w + q.chain, &q.base, true);
+            make_plan(TS_OP_LOGPARTITION, B, N, q.KC, w + q.chain, &q.base, K > 1);
             e = launch_logz_tree(q.base, xp, lengths, logZ, s);
         }
     }
@@ -575,7 +581,7 @@ ts_status ts_semimarkov_marginals(const float* sp, const int32_t* lengths, int64
         if (q.base.fused) {
             e = launch_small_log(xp, lengths, B, N, q.KC, logZ, xm, s);
         } else {
-            make_plan(TS_OP_MARGINALS, B, N, q.KC, w + q.chain, &q.base, true);
+            make_plan(TS_OP_MARGINALS, B, N, q.KC, w + q.chain, &q.base, K > 1);
             e = launch_logz_tree(q.base, xp, lengths, logZ, s);
             if (e == hipSuccess) e = launch_marginals_tree(q.base, xp, lengths, xm, s);
         }
@@ -605,7 +611,7 @@ ts_status ts_semimarkov_viterbi(const float* sp, const int32_t* lengths, int64_t
         if (q.base.fused) {
             e = launch_small_max(xp, lengths, B, N, q.KC, xs, score, s);
         } else {
-            make_plan(TS_OP_VITERBI, B, N, q.KC, w + q.chain, &q.base, true);
+            make_plan(TS_OP_VITERBI, B, N, q.KC, w + q.chain, &q.base, K > 1);
             e = launch_viterbi_tree(q.base, xp, lengths, xs, score, s);
         }
     }

@@ -26,6 +26,11 @@ struct Plan {
     int D = 0;
     int op = 0;
     bool fused = false;   // single-launch path of small.hip (no workspace)
+    // log semiring for C <= 64 without masks: the levels below lc are folded per chunk of
+    // 2^lc edges by chunk.hip (k_chunk_up writes the level-lc nodes, k_chunk_form the
+    // marginals from the level-lc outside vectors); levels 1..lc-1 are never formed
+    bool chunk = false;
+    int lc = 0;
     // log semiring, levels 1..D (index by level)
     float* core[kMaxLevels] = {};
     double* ro[kMaxLevels] = {};
@@ -62,6 +67,11 @@ struct Plan {
     size_t bytes = 0;
 };
 
+constexpr int kChunkLog = 4;   // chunks of at most 16 edges
+
+// Whether the log-semiring tree of C labels takes the chunk kernels (C <= 64, no masks).
+bool chunk_path(int64_t C, bool masks);
+
 // Output tile edge of a level of the log-semiring up-sweep with `nodes` nodes (all
 // sequences) of C labels: 64 for C <= 64; 128 above, unless the level has too few 128-wide
 // tiles to give every compute unit two of them: then 64 (four times the workgroups, each
@@ -88,6 +98,10 @@ hipError_t launch_marginals_tree(const Plan& p, const float* pot, const int32_t*
                                  float* marg, hipStream_t s);
 hipError_t launch_viterbi_tree(const Plan& p, const float* pot, const int32_t* lengths,
                                int32_t* path, float* score, hipStream_t s);
+hipError_t launch_chunk_up(const Plan& p, const float* pot, const int32_t* lengths,
+                           hipStream_t s);
+hipError_t launch_chunk_form(const Plan& p, const float* pot, const int32_t* lengths,
+                             float* marg, hipStream_t s);
 hipError_t launch_single_token(int64_t B, int64_t N, int64_t C, int op, float* logZ,
                                int32_t* path, float* score, hipStream_t s);
 // entropy from marginals mu [B, N-1, C, C]; part is [B, N-1] doubles (unused when N == 1)

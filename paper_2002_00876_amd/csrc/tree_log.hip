@@ -1500,12 +1500,17 @@ hipError_t up_sweep_vec(const Plan& p, const float* pot, const int32_t* lengths,
     if (e == hipSuccess && full64) e = allow_up_full_lds<64>();
     if (e == hipSuccess && full128) e = allow_up_full_lds<128>();
     if (e != hipSuccess) return e;
-    // the leaves' row and column maxima (shifts of the level-1 products)
-    LeafMaxArgs m{pot, lengths, p.N, p.C, p.lrmax, p.lcmax, p.rbits[0], p.cbits[0], p.bw};
-    hipLaunchKernelGGL((k_leaf_max<VEC, kBits>), dim3((unsigned)(p.B * p.E)), dim3(256), 0, s, m);
-    e = hipGetLastError();
+    if (p.chunk) {
+        // the chunk kernel forms the level-lc nodes from the leaves directly
+        if (p.lc > 0) e = launch_chunk_up(p, pot, lengths, s);
+    } else {
+        // the leaves' row and column maxima (shifts of the level-1 products)
+        LeafMaxArgs m{pot, lengths, p.N, p.C, p.lrmax, p.lcmax, p.rbits[0], p.cbits[0], p.bw};
+        hipLaunchKernelGGL((k_leaf_max<VEC, kBits>), dim3((unsigned)(p.B * p.E)), dim3(256), 0, s, m);
+        e = hipGetLastError();
+    }
     if (e != hipSuccess) return e;
-    for (int l = 1; l <= p.D; ++l) {
+    for (int l = p.chunk ? p.lc + 1 : 1; l <= p.D; ++l) {
         UpLogArgs a{};
         if (l == 1) {
             a.ccore = pot; a.cro = nullptr; a.cco = nullptr; a.cnodes = p.E;
@@ -1582,7 +1587,8 @@ hipError_t launch_logz_tree(const Plan& p, const float* pot, const int32_t* leng
 hipError_t launch_marginals_tree(const Plan& p, const float* pot, const int32_t* lengths,
                                  float* marg, hipStream_t s) {
     // (the up-sweep has been enqueued by the caller)
-    for (int l = p.D; l >= 2; --l) {
+    const int lowest = p.chunk ? p.lc + 1 : 2;   // the last level whose children get vectors
+    for (int l = p.D; l >= lowest; --l) {
         DownArgs d{};
         d.uN = (l == p.D) ? nullptr : p.u[l];
         d.vN = (l == p.D) ? nullptr : p.v[l];
@@ -1598,6 +1604,7 @@ hipError_t launch_marginals_tree(const Plan& p, const float* pot, const int32_t*
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
+    if (p.chunk) return launch_chunk_form(p, pot, lengths, marg, s);
     FormArgs f{};
     f.pot = pot;
     f.u1 = (p.D >= 2) ? p.u[1] : nullptr;
