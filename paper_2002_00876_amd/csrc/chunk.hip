@@ -10,7 +10,7 @@
 // formed.  A product is the exp-shifted GEMM of the tree kernels (Sec. 6c's operation),
 //   S[a][c] = sum_k exp(P[a][k] + coh[k] - sa[a]) exp(l[k][c] - sb[c]),
 //   core = log S,  ro' = ro + max co + sa,  co' = sb,
-// on the fp32 matrix cores, one 32 x 32 block per wave; S < 2^-80 is recomputed exactly.
+// on the fp32 matrix cores, a 16-row strip per wave; S < 2^-80 is recomputed exactly.
 //
 // Marginals (k_chunk_form): given the outside vectors of the chunk's node (u, the forward
 // message into its first edge, and v, the backward message out of its last edge), the
@@ -39,7 +39,7 @@ namespace tsc {
 namespace {
 
 constexpr int kCP = 64;              // labels padded to 64
-constexpr int kCT = 256;             // threads: 4 waves, one 32 x 32 output block each
+constexpr int kCT = 256;             // threads: 4 waves
 constexpr int kLD = kCP + 4;         // LDS row stride: 16-byte rows, conflict-free b128 reads
 constexpr float kChunkUnderflow = 0x1p-80f;
 
@@ -66,28 +66,6 @@ __device__ __forceinline__ void load_mat(const float* __restrict__ M, int C, flo
 
 __device__ __forceinline__ float f4get(const float4& v, int q) {
     return q == 0 ? v.x : q == 1 ? v.y : q == 2 ? v.z : v.w;
-}
-
-// (m, s) += (m2, s2) for log-sum-exp states value = m + log s (m = -inf: empty)
-__device__ __forceinline__ void lse_acc(float& m, float& s, float m2, float s2) {
-    if (m2 == -INFINITY) return;
-    if (m == -INFINITY) { m = m2; s = s2; return; }
-    const float nm = fmaxf(m, m2);
-    s = s * fexp(m - nm) + s2 * fexp(m2 - nm);
-    m = nm;
-}
-
-// log-sum-exp state of four values
-__device__ __forceinline__ void lse4(float v0, float v1, float v2, float v3, float& m, float& s) {
-    m = fmaxf(fmaxf(v0, v1), fmaxf(v2, v3));
-    s = m == -INFINITY ? 0.f
-                       : fexp(v0 - m) + fexp(v1 - m) + fexp(v2 - m) + fexp(v3 - m);
-}
-
-// merge of the states held by lanes lane and lane ^ o
-__device__ __forceinline__ void lse_xor(float& m, float& s, int o) {
-    const float m2 = __shfl_xor(m, o, kWave), s2 = __shfl_xor(s, o, kWave);
-    lse_acc(m, s, m2, s2);
 }
 
 // log-sum-exp over the 64 lanes of a wave (every lane gets the result)
@@ -139,14 +117,28 @@ __device__ __forceinline__ void col_partials(const float4 (&x)[4], float (*red)[
     if (lane < 16) *(float4*)&red[w][4 * lane] = make_float4(m4[0], m4[1], m4[2], m4[3]);
 }
 
+// max over the 16 lanes of a DPP row (quad swaps, then the mirrors within 8 and 16)
+__device__ __forceinline__ float row16_max(float x) {
+    x = fmaxf(x, dpp_f(x, 0xB1));
+    x = fmaxf(x, dpp_f(x, 0x4E));
+    x = fmaxf(x, dpp_f(x, 0x141));
+    return fmaxf(x, dpp_f(x, 0x140));
+}
+
+// Products as 16-row strips: wave w owns rows 16 w .. 16 w + 15 of every product and all 64
+// columns (four 16 x 16 blocks of v_mfma_f32_16x16x4f32), so each row of P is read,
+// exponentiated and rewritten by one wave only, and the next product's row shifts come out
+// of the epilogue with in-wave reductions.  Lanes 16 g .. 16 g + 15 contribute the indices
+// k + 4 g .. k + 4 g + 3 of each 16-wide step (one 16-byte read of P and of each block of
+// the transposed right operand).
 template <bool kVec>
 __global__ __launch_bounds__(kCT, 4) void k_chunk_up(ChunkUpArgs a) {
     __shared__ __align__(16) float P[kCP * kLD];       // the running product's core
     __shared__ __align__(16) float Bt[kCP * kLD];      // right operand, transposed: Bt[c][k]
     __shared__ __align__(16) float red[4][kCP];         // per-wave partial column maxima
-    __shared__ __align__(16) float sa[kCP], sb[kCP], cop[kCP];
+    __shared__ __align__(16) float sbuf[2][kCP];        // column shifts (= co) of the products
+    __shared__ __align__(16) float sa[kCP];             // row shifts of the next product
     __shared__ double rop[kCP];
-    __shared__ float cmaxp[1];
     const int64_t b = blockIdx.x / a.nodes, q = blockIdx.x % a.nodes;
     const int64_t E = a.N - 1, Eb = clamp_len(a.lengths, b, a.N) - 1;
     const int64_t S = (int64_t)1 << a.lc, t0 = q * S;
@@ -154,9 +146,12 @@ __global__ __launch_bounds__(kCT, 4) void k_chunk_up(ChunkUpArgs a) {
     const int64_t t1 = min(t0 + S, Eb);
     const int C = (int)a.C, tid = threadIdx.x, lane = tid & (kWave - 1), w = tid >> 6;
     const int rg = tid >> 4, c4 = tid & 15;
+    const int lr = lane & 15, lg = lane >> 4;      // strip row / column within a block; group
+    const int arow = 16 * w + lr;                  // the row this lane feeds to the products
     const size_t CC = (size_t)C * C;
     const float* leaves = a.pot + (size_t)(b * E) * CC;
     const size_t pn = (size_t)(b * a.nodes + q);
+    constexpr float kL2E = 1.4426950408889634f;
 
     // P = leaf t0 (ro = co = 0); the next leaf into registers and its column partials
     float4 x[4];
@@ -165,22 +160,31 @@ __global__ __launch_bounds__(kCT, 4) void k_chunk_up(ChunkUpArgs a) {
     for (int i = 0; i < 4; ++i) *(float4*)(P + (rg + 16 * i) * kLD + 4 * c4) = x[i];
     if (tid < kCP) {
         rop[tid] = 0.0;
-        cop[tid] = 0.f;
+        sbuf[1][tid] = 0.f;
     }
-    if (tid == 0) cmaxp[0] = 0.f;
     if (t0 + 1 < t1) {
         load_mat<kVec>(leaves + (size_t)(t0 + 1) * CC, C, x);
         col_partials(x, red);
     }
     __syncthreads();
+    {
+        // row shifts of the first product: lane group lg scans columns 16 lg .. 16 lg + 15
+        float m = -INFINITY;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const float4 p4 = *(const float4*)(P + arow * kLD + 16 * lg + 4 * u);
+            m = fmaxf(m, fmaxf(fmaxf(p4.x, p4.y), fmaxf(p4.z, p4.w)));
+        }
+        m = max_x32(max_x16(m));
+        if (lg == 0) sa[arow] = safe_shift(m);
+    }
 
-    const int wm = w >> 1, wn = w & 1;
-    const int arow = wm * 32 + (lane & 31), kofs = 4 * (lane >> 5);
-    constexpr float kL2E = 1.4426950408889634f;
-    for (int64_t t = t0 + 1; t < t1; ++t) {
-        const float cm = cmaxp[0];
-        // -- A: column shifts from the four waves' partials and the right operand, transposed,
-        // into Bt; row shifts of P (a quad of lanes per row); the next leaf's loads
+    const int np = (int)(t1 - t0 - 1);
+    for (int p = 0; p < np; ++p) {
+        const int64_t t = t0 + 1 + p;
+        const int cur = p & 1, prv = cur ^ 1;
+        // -- A: column shifts of leaf t from the four waves' partials and the right operand,
+        // transposed, into Bt; the next leaf's loads
         {
             float sq[4];
             const float4 r0 = *(const float4*)&red[0][4 * c4], r1 = *(const float4*)&red[1][4 * c4];
@@ -189,111 +193,109 @@ __global__ __launch_bounds__(kCT, 4) void k_chunk_up(ChunkUpArgs a) {
             for (int qq = 0; qq < 4; ++qq)
                 sq[qq] = safe_shift(fmaxf(fmaxf(f4get(r0, qq), f4get(r1, qq)),
                                           fmaxf(f4get(r2, qq), f4get(r3, qq))));
-            if (rg == 0) *(float4*)&sb[4 * c4] = make_float4(sq[0], sq[1], sq[2], sq[3]);
+            if (rg == 0) *(float4*)&sbuf[cur][4 * c4] = make_float4(sq[0], sq[1], sq[2], sq[3]);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int qq = 0; qq < 4; ++qq)
                     Bt[(4 * c4 + qq) * kLD + rg + 16 * i] = fexp(f4get(x[i], qq) - sq[qq]);
         }
-        {
-            const int ar = tid >> 2, kp = 16 * (tid & 3);
-            float m = -INFINITY;
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const float4 p4 = *(const float4*)(P + ar * kLD + kp + 4 * u);
-                const float4 o4 = *(const float4*)(cop + kp + 4 * u);
-                m = fmaxf(m, fmaxf(fmaxf(p4.x + (o4.x - cm), p4.y + (o4.y - cm)),
-                                   fmaxf(p4.z + (o4.z - cm), p4.w + (o4.w - cm))));
-            }
-            m = quad_max(m);
-            if ((tid & 3) == 0) sa[ar] = safe_shift(m);
-        }
         if (t + 1 < t1) load_mat<kVec>(leaves + (size_t)(t + 1) * CC, C, x);
         __syncthreads();
-        // -- B: S = A'' B'' for the wave's 32 x 32 block; the left operand is exponentiated
-        // from P as it is read: A''[a][k] = exp2(fma(P + co - max co, log2 e, -sa log2 e)).
-        // Lanes 0-31 contribute k..k+3 of each 8-wide k step, lanes 32-63 k+4..k+7.
-        f16v acc;
+        // -- B: S = A'' B'' for the wave's strip; A''[a][k] = exp2(fma(P + co - max co,
+        // log2 e, -sa log2 e)) formed as P is read
+        const float cm = safe_shift(wave_max_fast(lane < C ? sbuf[prv][lane] : -INFINITY));
+        const float sar = sa[arow];
+        typedef float f4v __attribute__((ext_vector_type(4)));
+        f4v acc[4];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+        for (int n = 0; n < 4; ++n) acc[n] = (f4v){0.f, 0.f, 0.f, 0.f};
         {
-            const float nsa = -sa[arow] * kL2E;
-            const float* ap = P + arow * kLD + kofs;
-            const float* op = cop + kofs;
-            const float* bp = Bt + (wn * 32 + (lane & 31)) * kLD + kofs;
+            const float nsa = -sar * kL2E;
+            const float* ap = P + arow * kLD + 4 * lg;
+            const float* op = sbuf[prv] + 4 * lg;
+            const float* bp = Bt + lr * kLD + 4 * lg;
 #pragma unroll
-            for (int kk = 0; kk < kCP; kk += 8) {
+            for (int kk = 0; kk < kCP; kk += 16) {
                 const float4 p4 = *(const float4*)(ap + kk), o4 = *(const float4*)(op + kk);
-                const float4 bv = *(const float4*)(bp + kk);
+                float4 bv[4];
+#pragma unroll
+                for (int n = 0; n < 4; ++n) bv[n] = *(const float4*)(bp + 16 * n * kLD + kk);
                 const float a0 = __builtin_amdgcn_exp2f(fmaf(p4.x + (o4.x - cm), kL2E, nsa));
                 const float a1 = __builtin_amdgcn_exp2f(fmaf(p4.y + (o4.y - cm), kL2E, nsa));
                 const float a2 = __builtin_amdgcn_exp2f(fmaf(p4.z + (o4.z - cm), kL2E, nsa));
                 const float a3 = __builtin_amdgcn_exp2f(fmaf(p4.w + (o4.w - cm), kL2E, nsa));
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, bv.x, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, bv.y, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a2, bv.z, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a3, bv.w, acc, 0, 0, 0);
-            }
-        }
-        float smin = INFINITY;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int row = wm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-            const int col = wn * 32 + (lane & 31);
-            if (row < C && col < C) smin = fminf(smin, acc[r]);
-        }
-        // (also the barrier after every wave's reads of P and Bt)
-        const bool any_under = __syncthreads_or(!(smin >= kChunkUnderflow));
-        // -- C: the product's core log S into P; entries whose terms all underflowed are
-        // recomputed exactly (a rare path: all reads of P before any write)
-        float val[16];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int row = wm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-            const int col = wn * 32 + (lane & 31);
-            val[r] = (row < C && col < C) ? flog(acc[r]) : -INFINITY;
-        }
-        if (any_under) {
-#pragma unroll 1
-            for (int r = 0; r < 16; ++r) {
-                const int row = wm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-                const int col = wn * 32 + (lane & 31);
-                if (row >= C || col >= C || acc[r] >= kChunkUnderflow) continue;
-                const float* lcol = leaves + (size_t)t * CC + col;
-                const float sr = sa[row], sc = sb[col];
-                float mq = -INFINITY;
-                for (int k = 0; k < C; ++k)
-                    mq = fmaxf(mq, (P[row * kLD + k] + (cop[k] - cm) - sr) + (lcol[(size_t)k * C] - sc));
-                float v = -INFINITY;
-                if (mq != -INFINITY) {
-                    float sum = 0.f;
-                    for (int k = 0; k < C; ++k)
-                        sum += fexp((P[row * kLD + k] + (cop[k] - cm) - sr) + (lcol[(size_t)k * C] - sc) - mq);
-                    v = mq + flog(sum);
+                for (int n = 0; n < 4; ++n) {
+                    acc[n] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, bv[n].x, acc[n], 0, 0, 0);
+                    acc[n] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, bv[n].y, acc[n], 0, 0, 0);
+                    acc[n] = __builtin_amdgcn_mfma_f32_16x16x4f32(a2, bv[n].z, acc[n], 0, 0, 0);
+                    acc[n] = __builtin_amdgcn_mfma_f32_16x16x4f32(a3, bv[n].w, acc[n], 0, 0, 0);
                 }
-                val[r] = v;
             }
-            __syncthreads();
         }
+        // -- C: the product's core log S (entry (16 w + 4 lg + r, 16 n + lr) of acc[n][r]);
+        // entries whose terms all underflowed are recomputed exactly from P before it is
+        // overwritten (a rare path); then the wave's rows of P, ro and the next row shifts
+        float val[4][4], smin = INFINITY;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int row = wm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-            const int col = wn * 32 + (lane & 31);
-            P[row * kLD + col] = val[r];
+        for (int n = 0; n < 4; ++n)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = 16 * w + 4 * lg + r, col = 16 * n + lr;
+                const bool ok = row < C && col < C;
+                val[n][r] = ok ? flog(acc[n][r]) : -INFINITY;
+                if (ok) smin = fminf(smin, acc[n][r]);
+            }
+        if (__builtin_amdgcn_ballot_w64(!(smin >= kChunkUnderflow))) {
+#pragma unroll 1
+            for (int n = 0; n < 4; ++n)
+#pragma unroll 1
+                for (int r = 0; r < 4; ++r) {
+                    const int row = 16 * w + 4 * lg + r, col = 16 * n + lr;
+                    if (row >= C || col >= C || acc[n][r] >= kChunkUnderflow) continue;
+                    const float* lcol = leaves + (size_t)t * CC + col;
+                    const float sr = sa[row], sc = sbuf[cur][col];
+                    float mq = -INFINITY;
+                    for (int k = 0; k < C; ++k)
+                        mq = fmaxf(mq, (P[row * kLD + k] + (sbuf[prv][k] - cm) - sr) +
+                                           (lcol[(size_t)k * C] - sc));
+                    float v = -INFINITY;
+                    if (mq != -INFINITY) {
+                        float sum = 0.f;
+                        for (int k = 0; k < C; ++k)
+                            sum += fexp((P[row * kLD + k] + (sbuf[prv][k] - cm) - sr) +
+                                        (lcol[(size_t)k * C] - sc) - mq);
+                        v = mq + flog(sum);
+                    }
+                    val[n][r] = v;
+                }
         }
-        if (tid < kCP) {   // wave 0 only: its reads of cmaxp and cop precede its updates
-            rop[tid] = tid < C ? rop[tid] + (double)cm + (double)sa[tid] : 0.0;
-            const float sbt = tid < C ? sb[tid] : -INFINITY;
-            const float ncm = safe_shift(wave_max_fast(sbt));
-            cop[tid] = tid < C ? sbt : 0.f;
-            if (tid == 0) cmaxp[0] = ncm;
+        const float cmn = safe_shift(wave_max_fast(lane < C ? sbuf[cur][lane] : -INFINITY));
+        float sbc[4];
+#pragma unroll
+        for (int n = 0; n < 4; ++n) sbc[n] = sbuf[cur][16 * n + lr];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int row = 16 * w + 4 * lg + r;
+            float m = -INFINITY;
+#pragma unroll
+            for (int n = 0; n < 4; ++n) {
+                P[row * kLD + 16 * n + lr] = val[n][r];
+                m = fmaxf(m, val[n][r] + sbc[n]);
+            }
+            m = row16_max(m);
+            if (lr == 0) {
+                if (row < C) rop[row] += (double)cm + (double)sa[row];
+                sa[row] = safe_shift(m - cmn);
+            }
         }
         if (t + 1 < t1) col_partials(x, red);
         __syncthreads();
     }
 
     // ---- the node: core, offsets and the partial maxima of its rows and columns
+    const float* cop = sbuf[(np - 1) & 1];   // co of the last product (zeros for one edge)
     float* Pc = a.core + pn * CC;
     for (int idx = tid; idx < kCP * kCP; idx += kCT) {
         const int r = idx >> 6, c = idx & (kCP - 1);
@@ -336,24 +338,23 @@ struct ChunkFormArgs {
 
 constexpr int kMaxChunk = 1 << kChunkLog;
 
-// merges of log-sum-exp states across lanes: DPP within rows of 16 lanes, lane swaps across
-// rows; the merge is symmetric, so both lanes of a pair hold the same state afterwards
-__device__ __forceinline__ void lse_dpp(float& m, float& s, int ctrl) {
-    lse_acc(m, s, dpp_f(m, ctrl), dpp_f(s, ctrl));
+// Reductions across lanes: max first, then one exponential per value and a sum (so a
+// log-sum-exp over lanes costs one exponential per value).  Sums over lanes l and l ^ 16 /
+// l ^ 32 by lane swaps; over the 16 lanes of a DPP row by quad swaps and the mirrors within
+// 8 and 16.
+__device__ __forceinline__ float sum_x16(float x) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
-__device__ __forceinline__ void lse_x16(float& m, float& s) {
-    const auto rm = __builtin_amdgcn_permlane16_swap(__float_as_uint(m), __float_as_uint(m), false, false);
-    const auto rs = __builtin_amdgcn_permlane16_swap(__float_as_uint(s), __float_as_uint(s), false, false);
-    m = __uint_as_float(rm[0]);
-    s = __uint_as_float(rs[0]);
-    lse_acc(m, s, __uint_as_float(rm[1]), __uint_as_float(rs[1]));
+__device__ __forceinline__ float sum_x32(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
-__device__ __forceinline__ void lse_x32(float& m, float& s) {
-    const auto rm = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
-    const auto rs = __builtin_amdgcn_permlane32_swap(__float_as_uint(s), __float_as_uint(s), false, false);
-    m = __uint_as_float(rm[0]);
-    s = __uint_as_float(rs[0]);
-    lse_acc(m, s, __uint_as_float(rm[1]), __uint_as_float(rs[1]));
+__device__ __forceinline__ float row16_sum(float x) {
+    x += dpp_f(x, 0xB1);
+    x += dpp_f(x, 0x4E);
+    x += dpp_f(x, 0x141);
+    return x + dpp_f(x, 0x140);
 }
 
 // Every wave turns the four waves' partial states (m, s) of the 64 lines into the shifted
@@ -361,10 +362,12 @@ __device__ __forceinline__ void lse_x32(float& m, float& s) {
 __device__ __forceinline__ float shifted_from_partials(const float (*pm)[kCP], const float (*ps)[kCP],
                                                        int C, float* h_out) {
     const int c = threadIdx.x & (kWave - 1);
-    float m = pm[0][c], s = ps[0][c];
-    lse_acc(m, s, pm[1][c], ps[1][c]);
-    lse_acc(m, s, pm[2][c], ps[2][c]);
-    lse_acc(m, s, pm[3][c], ps[3][c]);
+    const float m0 = pm[0][c], m1 = pm[1][c], m2 = pm[2][c], m3 = pm[3][c];
+    float m = fmaxf(fmaxf(m0, m1), fmaxf(m2, m3));
+    float s = 0.f;
+    if (m != -INFINITY)
+        s = ps[0][c] * fexp(m0 - m) + ps[1][c] * fexp(m1 - m) + ps[2][c] * fexp(m2 - m) +
+            ps[3][c] * fexp(m3 - m);
     if (c >= C) m = -INFINITY;
     const float h = safe_shift(wave_max_fast(m));
     *h_out = h;
@@ -412,13 +415,16 @@ __global__ __launch_bounds__(kCT) void k_chunk_form(ChunkFormArgs a) {
     for (int64_t t = t0; t < t1; ++t) {
         const int k = (int)(t - t0), par = k & 1;
         if (t + 1 < t1) load_mat<kVec>(leaves + (size_t)(t + 1) * CC, C, xn);
+        // the wave's state (m, s) of each of the thread's columns over the wave's 16 rows
         float mq[4], sq[4];
 #pragma unroll
         for (int qq = 0; qq < 4; ++qq) {
-            lse4(ar[0] + f4get(x[0], qq), ar[1] + f4get(x[1], qq), ar[2] + f4get(x[2], qq),
-                 ar[3] + f4get(x[3], qq), mq[qq], sq[qq]);
-            lse_x16(mq[qq], sq[qq]);
-            lse_x32(mq[qq], sq[qq]);
+            const float v0 = ar[0] + f4get(x[0], qq), v1 = ar[1] + f4get(x[1], qq);
+            const float v2 = ar[2] + f4get(x[2], qq), v3 = ar[3] + f4get(x[3], qq);
+            const float m = max_x32(max_x16(fmaxf(fmaxf(v0, v1), fmaxf(v2, v3))));
+            const float sh = safe_shift(m);
+            mq[qq] = m;
+            sq[qq] = sum_x32(sum_x16(fexp(v0 - sh) + fexp(v1 - sh) + fexp(v2 - sh) + fexp(v3 - sh)));
         }
         if (lane < 16) {
             *(float4*)&pm[par][w][4 * lane] = make_float4(mq[0], mq[1], mq[2], mq[3]);
@@ -475,12 +481,12 @@ __global__ __launch_bounds__(kCT) void k_chunk_form(ChunkFormArgs a) {
                     if (4 * c4 + 3 < C) p[3] = mu.w;
                 }
             }
-            // row state over this thread's four columns, merged over the row's 16 lanes
-            lse4(x[i].x + bq[0], x[i].y + bq[1], x[i].z + bq[2], x[i].w + bq[3], zm[i], zs[i]);
-            lse_dpp(zm[i], zs[i], 0xB1);
-            lse_dpp(zm[i], zs[i], 0x4E);
-            lse_dpp(zm[i], zs[i], 0x141);
-            lse_dpp(zm[i], zs[i], 0x140);
+            // row state over the row's 64 columns (the 16 lanes of the row group)
+            const float v0 = x[i].x + bq[0], v1 = x[i].y + bq[1], v2 = x[i].z + bq[2],
+                        v3 = x[i].w + bq[3];
+            zm[i] = row16_max(fmaxf(fmaxf(v0, v1), fmaxf(v2, v3)));
+            const float sh = safe_shift(zm[i]);
+            zs[i] = row16_sum(fexp(v0 - sh) + fexp(v1 - sh) + fexp(v2 - sh) + fexp(v3 - sh));
         }
         // lane c4 == 0 of row group rg holds rows rg + 16 i: wave w covers rows 4w .. 4w+3
         // (+ 16 i); stored as pm[par][i][r] so that every wave reads four partials per row
