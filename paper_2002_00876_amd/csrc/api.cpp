@@ -120,8 +120,26 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, boo
     Bump bump{static_cast<char*>(base)};
     if (op == TS_OP_LOGPARTITION || op == TS_OP_MARGINALS) {
         p->chunk = chunk_path(C, masks);
-        p->lc = p->chunk ? (D < kChunkLog ? D : kChunkLog) : 0;
-        for (int l = p->chunk ? (p->lc > 0 ? p->lc : D + 1) : 1; l <= D; ++l) {
+        if (p->chunk) {
+            // the chunk nodes (level lc; the leaves themselves when lc == 0) and, for the
+            // marginals, their outside vectors
+            const int lc = D < kChunkLog ? D : kChunkLog;
+            const size_t n = (size_t)B * (size_t)(Np >> lc);
+            p->lc = lc;
+            if (lc > 0) {
+                p->core[lc] = bump.take<float>(n * C * C);
+                p->ro[lc] = bump.take<double>(n * C);
+                p->co[lc] = bump.take<double>(n * C);
+            }
+            if (op == TS_OP_MARGINALS) {
+                const size_t nv = lc > 0 ? n : (size_t)B * p->E;
+                p->u[lc] = bump.take<float>(nv * C);
+                p->v[lc] = bump.take<float>(nv * C);
+            }
+            p->bytes = (bump.off + kAlign - 1) / kAlign * kAlign;
+            return true;
+        }
+        for (int l = 1; l <= D; ++l) {
             const size_t n = (size_t)B * (size_t)(Np >> l);
             const int tm = up_tile(C, (int64_t)n);
             p->ntile[l] = (int)((C + tm - 1) / tm);
@@ -131,10 +149,8 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, boo
             p->pmr[l] = bump.take<float>(n * C * p->ntile[l]);
             p->pmc[l] = bump.take<float>(n * C * p->ntile[l]);
         }
-        if (!p->chunk) {
-            p->lrmax = bump.take<float>((size_t)B * p->E * C);
-            p->lcmax = bump.take<float>((size_t)B * p->E * C);
-        }
+        p->lrmax = bump.take<float>((size_t)B * p->E * C);
+        p->lcmax = bump.take<float>((size_t)B * p->E * C);
         p->bw = (int)((C + 63) / 64);
         for (int l = 0; masks && l < D; ++l) {
             const size_t n = l == 0 ? (size_t)B * p->E : (size_t)B * (size_t)(Np >> l);
@@ -142,7 +158,7 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, boo
             p->cbits[l] = bump.take<uint64_t>(n * C * p->bw);
         }
         if (op == TS_OP_MARGINALS)
-            for (int l = p->chunk ? p->lc : 1; l < D; ++l) {
+            for (int l = 1; l < D; ++l) {
                 const size_t n = (size_t)B * (size_t)(Np >> l);
                 p->u[l] = bump.take<float>(n * C);
                 p->v[l] = bump.take<float>(n * C);

@@ -1,6 +1,8 @@
-// chunk.hip -- the lowest levels of the log-semiring tree for label sets of at most 64
-// (padded to 64), one workgroup per chunk of S = 2^lc consecutive edges of a sequence
-// (lc = the plan's chunk level, at most kChunkLog).
+// chunk.hip -- log Z and the marginals for label sets of at most 64 (padded to 64) in
+// chunks of S = 2^lc consecutive edges of a sequence (lc = the plan's chunk level, at most
+// kChunkLog): the chunk products (k_chunk_up, one workgroup per chunk), the forward and
+// backward recursions over each sequence's chunk products (k_chunk_scan), and the
+// messages and marginals inside each chunk from its boundary vectors (k_chunk_form).
 //
 // Up (k_chunk_up): the workgroup folds the chunk's valid edges into their product
 //   P = l_{t0} (x) l_{t0+1} (x) ... (x) l_{t1-1}
@@ -11,6 +13,8 @@
 //   S[a][c] = sum_k exp(P[a][k] + coh[k] - sa[a]) exp(l[k][c] - sb[c]),
 //   core = log S,  ro' = ro + max co + sa,  co' = sb,
 // on the fp32 matrix cores, a 16-row strip per wave; S < 2^-80 is recomputed exactly.
+//
+// Across chunks (k_chunk_scan): see the kernel.
 //
 // Marginals (k_chunk_form): given the outside vectors of the chunk's node (u, the forward
 // message into its first edge, and v, the backward message out of its last edge), the
@@ -82,18 +86,11 @@ struct ChunkUpArgs {
     int64_t N, C;
     int lc;              // chunk level: a chunk is 2^lc edges
     int64_t nodes;       // nodes per sequence at level lc
-    float* core;         // level-lc nodes (one output tile per line: partial maxima [nodes][C][1])
+    float* core;         // level-lc nodes
     double* ro;
     double* co;
-    float* pmr;
-    float* pmc;
 };
 
-// max over the four lanes of a quad (DPP quad permutations)
-__device__ __forceinline__ float quad_max(float x) {
-    x = fmaxf(x, dpp_f(x, 0xB1));
-    return fmaxf(x, dpp_f(x, 0x4E));
-}
 // value of lanes l and l ^ 16 / l ^ 32 combined by max (one lane swap each)
 __device__ __forceinline__ float max_x16(float x) {
     const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -125,6 +122,17 @@ __device__ __forceinline__ float row16_max(float x) {
     return fmaxf(x, dpp_f(x, 0x140));
 }
 
+// LDS of the exact path
+struct ExactSmem {
+    float P[kCP * kLD];       // the running product's core
+    float Bt[kCP * kLD];      // right operand, transposed: Bt[c][k]
+    float red[4][kCP];        // per-wave partial column maxima
+    float sbuf[2][kCP];       // column shifts (= co) of the products
+    float sa[kCP];            // row shifts of the next product
+    double rop[kCP];
+};
+
+// ---- the exact path: every product in the log domain
 // Products as 16-row strips: wave w owns rows 16 w .. 16 w + 15 of every product and all 64
 // columns (four 16 x 16 blocks of v_mfma_f32_16x16x4f32), so each row of P is read,
 // exponentiated and rewritten by one wave only, and the next product's row shifts come out
@@ -132,25 +140,21 @@ __device__ __forceinline__ float row16_max(float x) {
 // k + 4 g .. k + 4 g + 3 of each 16-wide step (one 16-byte read of P and of each block of
 // the transposed right operand).
 template <bool kVec>
-__global__ __launch_bounds__(kCT, 4) void k_chunk_up(ChunkUpArgs a) {
-    __shared__ __align__(16) float P[kCP * kLD];       // the running product's core
-    __shared__ __align__(16) float Bt[kCP * kLD];      // right operand, transposed: Bt[c][k]
-    __shared__ __align__(16) float red[4][kCP];         // per-wave partial column maxima
-    __shared__ __align__(16) float sbuf[2][kCP];        // column shifts (= co) of the products
-    __shared__ __align__(16) float sa[kCP];             // row shifts of the next product
-    __shared__ double rop[kCP];
-    const int64_t b = blockIdx.x / a.nodes, q = blockIdx.x % a.nodes;
-    const int64_t E = a.N - 1, Eb = clamp_len(a.lengths, b, a.N) - 1;
-    const int64_t S = (int64_t)1 << a.lc, t0 = q * S;
-    if (t0 >= Eb) return;   // node absent: all padding
-    const int64_t t1 = min(t0 + S, Eb);
+__device__ void chunk_up_exact(const ChunkUpArgs& a, int64_t b, int64_t t0, int64_t t1,
+                               size_t pn, ExactSmem& sm) {
+    float* P = sm.P;
+    float* Bt = sm.Bt;
+    float (*red)[kCP] = sm.red;
+    float (*sbuf)[kCP] = sm.sbuf;
+    float* sa = sm.sa;
+    double* rop = sm.rop;
+    const int64_t E = a.N - 1;
     const int C = (int)a.C, tid = threadIdx.x, lane = tid & (kWave - 1), w = tid >> 6;
     const int rg = tid >> 4, c4 = tid & 15;
     const int lr = lane & 15, lg = lane >> 4;      // strip row / column within a block; group
     const int arow = 16 * w + lr;                  // the row this lane feeds to the products
     const size_t CC = (size_t)C * C;
     const float* leaves = a.pot + (size_t)(b * E) * CC;
-    const size_t pn = (size_t)(b * a.nodes + q);
     constexpr float kL2E = 1.4426950408889634f;
 
     // P = leaf t0 (ro = co = 0); the next leaf into registers and its column partials
@@ -294,7 +298,7 @@ __global__ __launch_bounds__(kCT, 4) void k_chunk_up(ChunkUpArgs a) {
         __syncthreads();
     }
 
-    // ---- the node: core, offsets and the partial maxima of its rows and columns
+    // ---- the node: core and offsets
     const float* cop = sbuf[(np - 1) & 1];   // co of the last product (zeros for one edge)
     float* Pc = a.core + pn * CC;
     for (int idx = tid; idx < kCP * kCP; idx += kCT) {
@@ -305,24 +309,239 @@ __global__ __launch_bounds__(kCT, 4) void k_chunk_up(ChunkUpArgs a) {
         a.ro[pn * C + tid] = rop[tid];
         a.co[pn * C + tid] = (double)cop[tid];
     }
-    {
-        // rows and columns: a quad of lanes per line, sixteen entries each
-        const int line = tid >> 2, part = 16 * (tid & 3);
-        float mr = -INFINITY, mc = -INFINITY;
-        for (int u = 0; u < 16; ++u) {
-            const int k = part + u;
-            if (k < C) {
-                mr = fmaxf(mr, P[line * kLD + k] + cop[k]);
-                mc = fmaxf(mc, P[k * kLD + line] + (float)rop[k]);
-            }
-        }
-        mr = quad_max(mr);
-        mc = quad_max(mc);
-        if ((tid & 3) == 0 && line < C) {
-            a.pmr[pn * C + line] = mr;
-            a.pmc[pn * C + line] = mc;
+}
+
+// ---- the fast path: the running product in the linear domain, in the accumulators
+// P_p = P_{p-1} (x) l_p is kept as P[a][c] = ro[a] + log S[a][c] + co[c] with S in fp32
+// linear form, every row of S scaled to a maximum in [1/2, 1) by a power of two (exact; ro
+// counts the powers), and co = CO + cb (CO a float64 scalar, cb <= 0).  Then
+//   S_p = S_{p-1} B_p,   B_p[k][c] = exp(cb_{p-1}[k] + l_p[k][c] - s_p[c]),
+//   s_p[c] = max_k (cb_{p-1}[k] + l_p[k][c]),   CO_p = CO_{p-1} + max s_p,  cb_p = s_p - max s_p,
+// so the chain itself needs neither exp nor log: B_p depends on the leaves only and is
+// prepared one product ahead, while the product runs on the matrix cores.  The product is
+// formed transposed, T_p = B_p^T T_{p-1} with T = S^T: wave w owns the columns a = 16 w ..
+// 16 w + 15 of T, and the accumulators of v_mfma_f32_16x16x4f32 (lane l: T[16 m + 4 (l / 16)
+// + r][16 w + l % 16]) are exactly the right operand of the next product, so T never leaves
+// the registers.  T_{-1} = I.  The result equals the exact path's up to rounding as long as
+// every entry of every S_p (rows of S_{p-1} at most 1, columns of B_p at most 1) is at least
+// 2^-80: then nothing below fp32's normal range ever enters a sum that matters.  Otherwise
+// the path reports failure and the chunk is redone by the exact path.
+struct LinSmem {
+    float bt[2][kCP * kCP];   // B of two products, transposed (bt[c][k]), 16-byte groups swizzled
+    float red[2][4][kCP];     // per-wave partial column maxima of two leaves
+};
+
+// dword offset of element (c, 4 kg .. 4 kg + 3) of a transposed operand: the 16-byte groups of
+// a row are permuted by c, so that both the writes (lanes: 16 consecutive 4-column groups) and
+// the reads (lanes: 16 consecutive rows c) touch 16 distinct 16-byte bank groups
+__device__ __forceinline__ int bt_off(int c, int kg) { return c * kCP + 4 * (kg ^ ((c ^ (c >> 2)) & 15)); }
+
+// thread t: rows 4 (t >> 4) + i, columns 4 (t & 15) .. + 3 (past C: -inf)
+template <bool kVec>
+__device__ __forceinline__ void load_rows4(const float* __restrict__ M, int C, float4 (&x)[4]) {
+    const int r0 = 4 * (threadIdx.x >> 4), c = 4 * (threadIdx.x & 15);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int r = r0 + i;
+        const float* p = M + (size_t)r * C + c;
+        if constexpr (kVec) {
+            x[i] = (r < C && c < C) ? *(const float4*)p
+                                    : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+        } else {
+            x[i].x = (r < C && c + 0 < C) ? p[0] : -INFINITY;
+            x[i].y = (r < C && c + 1 < C) ? p[1] : -INFINITY;
+            x[i].z = (r < C && c + 2 < C) ? p[2] : -INFINITY;
+            x[i].w = (r < C && c + 3 < C) ? p[3] : -INFINITY;
         }
     }
+}
+
+template <bool kVec>
+__device__ bool chunk_up_linear(const ChunkUpArgs& a, int64_t b, int64_t t0, int64_t t1,
+                                size_t pn, LinSmem& sm, int (&flag)[2]) {
+    typedef float f4v __attribute__((ext_vector_type(4)));
+    const int64_t E = a.N - 1;
+    const int C = (int)a.C, tid = threadIdx.x, lane = tid & (kWave - 1), w = tid >> 6;
+    const int rg = tid >> 4, c4 = tid & 15;        // leaf layout: rows 4 rg + i, columns 4 c4 + q
+    const int lr = lane & 15, g = lane >> 4;       // product layout
+    const int ac = 16 * w + lr;                    // the column of T (row of S) of this lane
+    const size_t CC = (size_t)C * C;
+    const float* leaves = a.pot + (size_t)(b * E) * CC;
+    const int np = (int)(t1 - t0);
+
+    float4 lf[4];          // a leaf on its way from memory
+    float v[4][4];         // cb[k] + l[k][c] of the next leaf to prepare
+    float cbr[4];          // cb at the thread's rows 4 rg + i (of the last prepared leaf)
+    float cbc[4];          // cb at the thread's columns 4 c4 + q
+    double CO = 0.0;
+
+    auto make_v = [&]() {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            v[i][0] = cbr[i] + lf[i].x;
+            v[i][1] = cbr[i] + lf[i].y;
+            v[i][2] = cbr[i] + lf[i].z;
+            v[i][3] = cbr[i] + lf[i].w;
+        }
+    };
+    // the wave's column maxima of v (its 16 rows) into red[par][w]
+    auto partials = [&](int par) {
+        float m4[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            m4[q] = max_x32(max_x16(fmaxf(fmaxf(v[0][q], v[1][q]), fmaxf(v[2][q], v[3][q]))));
+        if (lane < 16) *(float4*)&sm.red[par][w][4 * c4] = make_float4(m4[0], m4[1], m4[2], m4[3]);
+    };
+    // B of the leaf whose v is in registers (column maxima from red[par]) into bt[buf]; cb of
+    // that leaf at the thread's rows and columns; CO
+    auto prep = [&](int par, int buf) {
+        float sc[4], sr[4];
+        {
+            const float4 r0 = *(const float4*)&sm.red[par][0][4 * c4], r1 = *(const float4*)&sm.red[par][1][4 * c4];
+            const float4 r2 = *(const float4*)&sm.red[par][2][4 * c4], r3 = *(const float4*)&sm.red[par][3][4 * c4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                sc[q] = fmaxf(fmaxf(f4get(r0, q), f4get(r1, q)), fmaxf(f4get(r2, q), f4get(r3, q)));
+        }
+        {
+            const float4 r0 = *(const float4*)&sm.red[par][0][4 * rg], r1 = *(const float4*)&sm.red[par][1][4 * rg];
+            const float4 r2 = *(const float4*)&sm.red[par][2][4 * rg], r3 = *(const float4*)&sm.red[par][3][4 * rg];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                sr[i] = fmaxf(fmaxf(f4get(r0, i), f4get(r1, i)), fmaxf(f4get(r2, i), f4get(r3, i)));
+        }
+        // max over all columns: the sixteen lanes of a DPP row hold every column once
+        const float M = safe_shift(row16_max(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]))));
+        float* bt = sm.bt[buf];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float sh = safe_shift(sc[q]);
+            *(float4*)(bt + bt_off(4 * c4 + q, rg)) =
+                make_float4(fexp(v[0][q] - sh), fexp(v[1][q] - sh), fexp(v[2][q] - sh), fexp(v[3][q] - sh));
+            cbc[q] = sc[q] - M;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) cbr[i] = sr[i] - M;
+        CO += (double)M;
+    };
+
+    // prologue: B_0 (cb_{-1} = 0) and the column maxima of leaf 1
+    load_rows4<kVec>(leaves + (size_t)t0 * CC, C, lf);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) cbr[i] = 0.f;
+    make_v();
+    partials(0);
+    if (np > 1) load_rows4<kVec>(leaves + (size_t)(t0 + 1) * CC, C, lf);
+    __syncthreads();
+    prep(0, 0);
+    if (np > 1) {
+        make_v();
+        partials(1);
+        if (np > 2) load_rows4<kVec>(leaves + (size_t)(t0 + 2) * CC, C, lf);
+    }
+    __syncthreads();
+
+    f4v T[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) T[m][r] = (16 * m + 4 * g + r == ac) ? 1.f : 0.f;
+    int esum = 0;
+    const int xb = 64 * lr + 4 * (g ^ lr ^ (lr >> 2));
+    const int cl = ac < C ? C - 4 * g : 0;   // entry (16 m + 4 g + r, ac) is real iff 16 m + r < cl
+
+    for (int p = 0; p < np; ++p) {
+        const int cur = p & 1;
+        // leaf p + 1's B into the other buffer (the product below reads this one)
+        if (p + 1 < np) prep((p + 1) & 1, cur ^ 1);
+        // T_p = B_p^T T_{p-1}: k-step 16 mp + 4 g + j of this lane is T[mp][j] on the right and
+        // bt[16 mb + lr][16 mp + 4 g + j] on the left
+        // (bt_off(16 mb + lr, 4 mp + g) = 1024 mb + (xb ^ 16 (mp ^ mb)), xb = 64 lr + 4 (g ^ lr ^ lr / 4))
+        const float* bt = sm.bt[cur];
+        f4v U[4];
+#pragma unroll
+        for (int m = 0; m < 4; ++m) U[m] = (f4v){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int mp = 0; mp < 4; ++mp)
+#pragma unroll
+            for (int mb = 0; mb < 4; ++mb) {
+                const float4 av = *(const float4*)(bt + 1024 * mb + (xb ^ (16 * (mp ^ mb))));
+                U[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, T[mp][0], U[mb], 0, 0, 0);
+                U[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, T[mp][1], U[mb], 0, 0, 0);
+                U[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, T[mp][2], U[mb], 0, 0, 0);
+                U[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, T[mp][3], U[mb], 0, 0, 0);
+            }
+        // leaf p + 2's column maxima (its load was issued a product ago), leaf p + 3's load
+        if (p + 2 < np) {
+            make_v();
+            partials(p & 1);
+            if (p + 3 < np) load_rows4<kVec>(leaves + (size_t)(t0 + p + 3) * CC, C, lf);
+        }
+        // scale column ac of T (row ac of S) by the power of two that brings its maximum into
+        // [1/2, 1); any real entry below 2^-80 sends the chunk to the exact path
+        float mx = 0.f, mn = INFINITY;
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                mx = fmaxf(mx, U[m][r]);
+                if (16 * m + r < cl) mn = fminf(mn, U[m][r]);
+            }
+        mx = max_x32(max_x16(mx));
+        if (__builtin_amdgcn_ballot_w64(!(mn >= kChunkUnderflow)) && lane == 0) flag[cur] = 1;
+        const int e = mx > 0.f ? ((__float_as_int(mx) >> 23) & 0xff) - 126 : 0;
+        const float sc = __int_as_float((127 - e) << 23);
+#pragma unroll
+        for (int m = 0; m < 4; ++m) T[m] = U[m] * sc;
+        esum += e;
+        __syncthreads();
+        if (flag[cur]) return false;   // (a flag is written only before the barrier of its parity)
+    }
+
+    // the node: core = log S (lane: row ac, columns 16 m + 4 g + r), ro, co
+    if (ac < C) {
+        float* row = a.core + pn * CC + (size_t)ac * C;
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const int c0 = 16 * m + 4 * g;
+            if constexpr (kVec) {
+                if (c0 < C)
+                    *(float4*)(row + c0) = make_float4(flog(T[m][0]), flog(T[m][1]), flog(T[m][2]), flog(T[m][3]));
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (c0 + r < C) row[c0 + r] = flog(T[m][r]);
+            }
+        }
+        if (g == 0) a.ro[pn * C + ac] = (double)esum * 0.6931471805599453;
+    }
+    if (rg == 0) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (4 * c4 + q < C) a.co[pn * C + 4 * c4 + q] = CO + (double)cbc[q];
+    }
+    return true;
+}
+
+union ChunkUpSmem {
+    ExactSmem exact;
+    LinSmem lin;
+};
+
+template <bool kVec>
+__global__ __launch_bounds__(kCT, 4) void k_chunk_up(ChunkUpArgs a) {
+    __shared__ ChunkUpSmem sm;
+    __shared__ int flag[2];
+    const int64_t b = blockIdx.x / a.nodes, q = blockIdx.x % a.nodes;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    const int64_t S = (int64_t)1 << a.lc, t0 = q * S;
+    if (t0 >= Eb) return;   // node absent: all padding
+    const int64_t t1 = min(t0 + S, Eb);
+    const size_t pn = (size_t)(b * a.nodes + q);
+    if (threadIdx.x < 2) flag[threadIdx.x] = 0;
+    __syncthreads();
+    if (!chunk_up_linear<kVec>(a, b, t0, t1, pn, sm.lin, flag))
+        chunk_up_exact<kVec>(a, b, t0, t1, pn, sm.exact);
 }
 
 struct ChunkFormArgs {
@@ -512,6 +731,159 @@ __global__ __launch_bounds__(kCT) void k_chunk_form(ChunkFormArgs a) {
     }
 }
 
+
+// ---------------------------------------------------------------- across the chunks
+// The chunk nodes M_0, ..., M_{K-1} of a sequence (K = ceil(E_b / S), M_q = ro + core + co
+// the product of the edges of chunk q) form a shorter chain with the same log partition and
+// the same messages at the chunk boundaries.  One workgroup per sequence runs its forward
+// recursion and another its backward recursion (Sec. 5's dynamic program, over chunks):
+//   u_0 = 0,      u_{q+1}[j] = LSE_i (u_q[i] + M_q[i][j]),        log Z = LSE_j u_K[j],
+//   v_{K-1} = 0,  v_{q-1}[i] = LSE_j (M_q[i][j] + v_q[j]),
+// the outside vectors of the chunk nodes (u_q the forward message into chunk q's first edge,
+// v_q the backward message out of its last edge), each stored shifted to max 0 while the
+// shifts are summed in float64 for log Z.  The matrices are independent of the vectors, so
+// they are loaded kScanAhead steps ahead of their use and each step costs one barrier.
+struct ChunkScanArgs {
+    const float* core;    // [B * nodes][C][C]: the chunk nodes, or the potentials when lc == 0
+    const double* ro;     // [B * nodes][C] (nullptr: zeros, lc == 0)
+    const double* co;
+    int64_t nodes;        // node stride per sequence
+    const int32_t* lengths;
+    int64_t N, C;
+    int lc;
+    float* logZ;          // [B] or nullptr
+    float* u;             // [B * nodes][C] or nullptr
+    float* v;             // [B * nodes][C] or nullptr (no backward workgroups)
+};
+
+constexpr int kScanAhead = 4;
+
+template <bool kVec>
+__global__ __launch_bounds__(kCT) void k_chunk_scan(ChunkScanArgs a) {
+    __shared__ __align__(16) float pm[2][4][kCP], ps[2][4][kCP];
+    const bool fwd = blockIdx.x < gridDim.x / (a.v ? 2 : 1) || !a.v;
+    const int64_t B = a.v ? gridDim.x / 2 : gridDim.x;
+    const int64_t b = fwd ? blockIdx.x : blockIdx.x - B;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    const int C = (int)a.C, tid = threadIdx.x, lane = tid & (kWave - 1), w = tid >> 6;
+    const int rg = tid >> 4, c4 = tid & 15;
+    if (Eb <= 0) {
+        if (fwd && tid == 0 && a.logZ) a.logZ[b] = logf((float)C);
+        return;
+    }
+    const int64_t S = (int64_t)1 << a.lc, K = (Eb + S - 1) / S;
+    const size_t CC = (size_t)C * C, base = (size_t)b * a.nodes;
+    const bool lv = lane < C;
+    // the matrices of the next kScanAhead steps in registers (step k uses slot k % kScanAhead)
+    float4 x[kScanAhead][4];
+    double rr[kScanAhead], cr[kScanAhead];
+    auto fetch = [&](int slot, int64_t step) {
+        const int64_t q = fwd ? step : K - 1 - step;
+        if (step >= (fwd ? K : K - 1)) return;
+        load_mat<kVec>(a.core + (base + q) * CC, C, x[slot]);
+        rr[slot] = (a.ro && lv) ? a.ro[(base + q) * C + lane] : 0.0;
+        cr[slot] = (a.co && lv) ? a.co[(base + q) * C + lane] : 0.0;
+    };
+#pragma unroll
+    for (int s = 0; s < kScanAhead; ++s) fetch(s, s);
+    float cur = lv ? 0.f : -INFINITY;   // lane c: entry c of u_q (forward) or v_q (backward)
+    double acc = 0.0;
+    if (w == 0 && lv) {
+        if (fwd && a.u) a.u[base * C + lane] = cur;
+        if (!fwd) a.v[(base + K - 1) * C + lane] = cur;
+    }
+    const int64_t steps = fwd ? K : K - 1;
+    for (int64_t k0 = 0; k0 < steps; k0 += kScanAhead) {
+#pragma unroll
+        for (int s = 0; s < kScanAhead; ++s) {
+            const int64_t k = k0 + s;
+            if (k >= steps) break;
+            const int par = (int)(k & 1);
+            float4 m4[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) m4[i] = x[s][i];
+            const double ro = rr[s], co = cr[s];
+            fetch(s, k + kScanAhead);
+            if (fwd) {
+                // w[i] = u[i] + ro[i], shifted; column states over the thread's four rows
+                const double wd = lv ? (double)cur + ro : -INFINITY;
+                const float W = safe_shift(wave_max_fast((float)wd));
+                const float wf = lv ? (float)(wd - (double)W) : -INFINITY;
+                float ar[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) ar[i] = __shfl(wf, rg + 16 * i, kWave);
+                float mq[4], sq[4];
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq) {
+                    const float v0 = ar[0] + f4get(m4[0], qq), v1 = ar[1] + f4get(m4[1], qq);
+                    const float v2 = ar[2] + f4get(m4[2], qq), v3 = ar[3] + f4get(m4[3], qq);
+                    const float m = max_x32(max_x16(fmaxf(fmaxf(v0, v1), fmaxf(v2, v3))));
+                    const float sh = safe_shift(m);
+                    mq[qq] = m;
+                    sq[qq] = sum_x32(sum_x16(fexp(v0 - sh) + fexp(v1 - sh) + fexp(v2 - sh) +
+                                             fexp(v3 - sh)));
+                }
+                if (lane < 16) {
+                    *(float4*)&pm[par][w][4 * lane] = make_float4(mq[0], mq[1], mq[2], mq[3]);
+                    *(float4*)&ps[par][w][4 * lane] = make_float4(sq[0], sq[1], sq[2], sq[3]);
+                }
+                __syncthreads();
+                // column `lane`: merge the four waves' states, add co, shift to max 0
+                const float n0 = pm[par][0][lane], n1 = pm[par][1][lane];
+                const float n2 = pm[par][2][lane], n3 = pm[par][3][lane];
+                const float m = fmaxf(fmaxf(n0, n1), fmaxf(n2, n3));
+                double z = -INFINITY;
+                if (lv && m != -INFINITY) {
+                    const float s = ps[par][0][lane] * fexp(n0 - m) + ps[par][1][lane] * fexp(n1 - m) +
+                                    ps[par][2][lane] * fexp(n2 - m) + ps[par][3][lane] * fexp(n3 - m);
+                    z = co + (double)m + (double)flog(s);
+                }
+                const float Z = safe_shift(wave_max_fast((float)z));
+                cur = (float)(z - (double)Z);
+                acc += (double)W + (double)Z;
+                if (a.u && w == 0 && lv && k + 1 < K) a.u[(base + k + 1) * C + lane] = cur;
+            } else {
+                // w[j] = co[j] + v[j], shifted; row states over the 16 lanes of a row group
+                const double wd = lv ? co + (double)cur : -INFINITY;
+                const float W = safe_shift(wave_max_fast((float)wd));
+                const float wf = lv ? (float)(wd - (double)W) : -INFINITY;
+                float bq[4];
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq) bq[qq] = __shfl(wf, 4 * c4 + qq, kWave);
+                float zm[4], zs[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float v0 = m4[i].x + bq[0], v1 = m4[i].y + bq[1], v2 = m4[i].z + bq[2],
+                                v3 = m4[i].w + bq[3];
+                    zm[i] = row16_max(fmaxf(fmaxf(v0, v1), fmaxf(v2, v3)));
+                    const float sh = safe_shift(zm[i]);
+                    zs[i] = row16_sum(fexp(v0 - sh) + fexp(v1 - sh) + fexp(v2 - sh) + fexp(v3 - sh));
+                }
+                if (c4 == 0) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        pm[par][i][rg + 16 * i] = zm[i];
+                        ps[par][i][rg + 16 * i] = zs[i];
+                    }
+                }
+                __syncthreads();
+                // row `lane` has one state, in slot lane / 16
+                const float m = pm[par][lane >> 4][lane];
+                double z = -INFINITY;
+                if (lv && m != -INFINITY) z = ro + (double)m + (double)flog(ps[par][lane >> 4][lane]);
+                const float Z = safe_shift(wave_max_fast((float)z));
+                cur = (float)(z - (double)Z);
+                const int64_t q = K - 1 - k;   // node q gave v_{q-1}
+                if (w == 0 && lv) a.v[(base + q - 1) * C + lane] = cur;
+            }
+        }
+    }
+    if (fwd && a.logZ) {
+        const float l = wave_lse64(cur);
+        if (tid == 0) a.logZ[b] = l == -INFINITY ? -INFINITY : (float)(acc + (double)l);
+    }
+}
+
 }  // namespace
 
 bool chunk_path(int64_t C, bool masks) { return !masks && C <= kCP; }
@@ -523,12 +895,32 @@ hipError_t launch_chunk_up(const Plan& p, const float* pot, const int32_t* lengt
     a.lc = p.lc;
     a.nodes = p.Np >> p.lc;
     a.core = p.core[p.lc]; a.ro = p.ro[p.lc]; a.co = p.co[p.lc];
-    a.pmr = p.pmr[p.lc]; a.pmc = p.pmc[p.lc];
     const dim3 grid((unsigned)(p.B * a.nodes));
     if (p.C % 4 == 0)
         hipLaunchKernelGGL(k_chunk_up<true>, grid, dim3(kCT), 0, s, a);
     else
         hipLaunchKernelGGL(k_chunk_up<false>, grid, dim3(kCT), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_chunk_scan(const Plan& p, const float* pot, const int32_t* lengths,
+                             float* logZ, hipStream_t s) {
+    ChunkScanArgs a{};
+    if (p.lc > 0) {
+        a.core = p.core[p.lc]; a.ro = p.ro[p.lc]; a.co = p.co[p.lc];
+        a.nodes = p.Np >> p.lc;
+    } else {
+        a.core = pot; a.ro = nullptr; a.co = nullptr;   // one edge per chunk: the leaves
+        a.nodes = p.E;
+    }
+    a.lengths = lengths; a.N = p.N; a.C = p.C; a.lc = p.lc;
+    a.logZ = logZ; a.u = p.u[p.lc]; a.v = p.v[p.lc];
+    if (!a.logZ && !a.u) return hipSuccess;
+    const dim3 grid((unsigned)(a.v ? 2 * p.B : p.B));
+    if (p.C % 4 == 0)
+        hipLaunchKernelGGL(k_chunk_scan<true>, grid, dim3(kCT), 0, s, a);
+    else
+        hipLaunchKernelGGL(k_chunk_scan<false>, grid, dim3(kCT), 0, s, a);
     return hipGetLastError();
 }
 
@@ -538,8 +930,8 @@ hipError_t launch_chunk_form(const Plan& p, const float* pot, const int32_t* len
     a.pot = pot; a.lengths = lengths; a.N = p.N; a.C = p.C;
     a.lc = p.lc;
     a.nodes = p.Np >> p.lc;
-    a.u = p.lc < p.D ? p.u[p.lc] : nullptr;
-    a.v = p.lc < p.D ? p.v[p.lc] : nullptr;
+    a.u = p.u[p.lc];
+    a.v = p.v[p.lc];
     a.marg = marg;
     const dim3 grid((unsigned)(p.B * a.nodes));
     if (p.C % 4 == 0)

@@ -26,9 +26,10 @@ struct Plan {
     int D = 0;
     int op = 0;
     bool fused = false;   // single-launch path of small.hip (no workspace)
-    // log semiring for C <= 64 without masks: the levels below lc are folded per chunk of
-    // 2^lc edges by chunk.hip (k_chunk_up writes the level-lc nodes, k_chunk_form the
-    // marginals from the level-lc outside vectors); levels 1..lc-1 are never formed
+    // log semiring for C <= 64 without masks (chunk.hip): k_chunk_up folds every chunk of
+    // 2^lc edges into its level-lc node, k_chunk_scan runs the forward and backward
+    // recursions over a sequence's chunk nodes (log Z and the chunks' outside vectors
+    // u[lc], v[lc]) and k_chunk_form the marginals inside each chunk; no other level is formed
     bool chunk = false;
     int lc = 0;
     // log semiring, levels 1..D (index by level)
@@ -100,6 +101,7 @@ hipError_t launch_viterbi_tree(const Plan& p, const float* pot, const int32_t* l
                                int32_t* path, float* score, hipStream_t s);
 hipError_t launch_chunk_up(const Plan& p, const float* pot, const int32_t* lengths,
                            hipStream_t s);
+hipError_t launch_chunk_scan(const Plan&, const float*, const int32_t*, float*, hipStream_t);
 hipError_t launch_chunk_form(const Plan& p, const float* pot, const int32_t* lengths,
                              float* marg, hipStream_t s);
 hipError_t launch_single_token(int64_t B, int64_t N, int64_t C, int op, float* logZ,

@@ -1500,17 +1500,12 @@ hipError_t up_sweep_vec(const Plan& p, const float* pot, const int32_t* lengths,
     if (e == hipSuccess && full64) e = allow_up_full_lds<64>();
     if (e == hipSuccess && full128) e = allow_up_full_lds<128>();
     if (e != hipSuccess) return e;
-    if (p.chunk) {
-        // the chunk kernel forms the level-lc nodes from the leaves directly
-        if (p.lc > 0) e = launch_chunk_up(p, pot, lengths, s);
-    } else {
-        // the leaves' row and column maxima (shifts of the level-1 products)
-        LeafMaxArgs m{pot, lengths, p.N, p.C, p.lrmax, p.lcmax, p.rbits[0], p.cbits[0], p.bw};
-        hipLaunchKernelGGL((k_leaf_max<VEC, kBits>), dim3((unsigned)(p.B * p.E)), dim3(256), 0, s, m);
-        e = hipGetLastError();
-    }
+    // the leaves' row and column maxima (shifts of the level-1 products)
+    LeafMaxArgs m{pot, lengths, p.N, p.C, p.lrmax, p.lcmax, p.rbits[0], p.cbits[0], p.bw};
+    hipLaunchKernelGGL((k_leaf_max<VEC, kBits>), dim3((unsigned)(p.B * p.E)), dim3(256), 0, s, m);
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
-    for (int l = p.chunk ? p.lc + 1 : 1; l <= p.D; ++l) {
+    for (int l = 1; l <= p.D; ++l) {
         UpLogArgs a{};
         if (l == 1) {
             a.ccore = pot; a.cro = nullptr; a.cco = nullptr; a.cnodes = p.E;
@@ -1579,6 +1574,12 @@ hipError_t root(const Plan& p, const float* pot, const int32_t* lengths, float* 
 
 hipError_t launch_logz_tree(const Plan& p, const float* pot, const int32_t* lengths,
                             float* logZ, hipStream_t s) {
+    if (p.chunk) {
+        // chunk nodes from the leaves, then the recursions over the chunks (log Z and, for
+        // the marginals, the chunks' outside vectors)
+        hipError_t e = p.lc > 0 ? launch_chunk_up(p, pot, lengths, s) : hipSuccess;
+        return e == hipSuccess ? launch_chunk_scan(p, pot, lengths, logZ, s) : e;
+    }
     hipError_t e = up_sweep(p, pot, lengths, s);
     if (e != hipSuccess || !logZ) return e;
     return root(p, pot, lengths, logZ, s);
@@ -1587,8 +1588,8 @@ hipError_t launch_logz_tree(const Plan& p, const float* pot, const int32_t* leng
 hipError_t launch_marginals_tree(const Plan& p, const float* pot, const int32_t* lengths,
                                  float* marg, hipStream_t s) {
     // (the up-sweep has been enqueued by the caller)
-    const int lowest = p.chunk ? p.lc + 1 : 2;   // the last level whose children get vectors
-    for (int l = p.D; l >= lowest; --l) {
+    if (p.chunk) return launch_chunk_form(p, pot, lengths, marg, s);
+    for (int l = p.D; l >= 2; --l) {
         DownArgs d{};
         d.uN = (l == p.D) ? nullptr : p.u[l];
         d.vN = (l == p.D) ? nullptr : p.v[l];
@@ -1604,7 +1605,6 @@ hipError_t launch_marginals_tree(const Plan& p, const float* pot, const int32_t*
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    if (p.chunk) return launch_chunk_form(p, pot, lengths, marg, s);
     FormArgs f{};
     f.pot = pot;
     f.u1 = (p.D >= 2) ? p.u[1] : nullptr;

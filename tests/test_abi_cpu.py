@@ -59,10 +59,10 @@ def test_workspace_sizes(L, monkeypatch):
     # marginals need the log-partition buffers plus the outside vectors
     assert ws(1, 32, 25, CW) > ws(0, 32, 25, CW)
     # the tree over N-1 = 24 edges has levels of 16, 8, 4, 2, 1 nodes of C*C floats; with
-    # at most 64 labels the chunk kernels fold chunks of 16 edges, so only the levels from
-    # the chunk level up (2 + 1 nodes) are stored
-    assert ws(0, 32, 25, CW) >= 32 * (2 + 1) * CW * CW * 4
-    assert ws(0, 32, 25, CW) < 32 * (4 + 2 + 1) * CW * CW * 4
+    # at most 64 labels the chunk kernels fold chunks of 16 edges and run the recursions
+    # over the chunk products, so only the chunk level (2 nodes) is stored
+    assert ws(0, 32, 25, CW) >= 32 * 2 * CW * CW * 4
+    assert ws(0, 32, 25, CW) < 32 * (2 + 1) * CW * CW * 4
     # above 64 labels every level is stored
     assert ws(0, 32, 25, 65) >= 32 * (16 + 8 + 4 + 2 + 1) * 65 * 65 * 4
     assert ws(7, 32, 25, CW) == 0 and ws(0, 0, 25, 20) == 0 and ws(0, 1, 25, 257) == 0
@@ -77,7 +77,7 @@ def test_workspace_sizes(L, monkeypatch):
     assert ws(3, 32, 25, CW) == ws(1, 32, 25, CW) + ws(2, 32, 25, CW)
     # TS_PATH=tree forces the multi-launch tree (with its chunk kernels) for small C too
     monkeypatch.setenv("TS_PATH", "tree")
-    assert ws(0, 32, 25, 20) >= 32 * (2 + 1) * 20 * 20 * 4
+    assert ws(0, 32, 25, 20) >= 32 * 2 * 20 * 20 * 4
 
 
 def _err(L):
