@@ -130,6 +130,7 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, boo
                 p->core[lc] = bump.take<float>(n * C * C);
                 p->ro[lc] = bump.take<double>(n * C);
                 p->co[lc] = bump.take<double>(n * C);
+                p->clin = bump.take<int32_t>(n);
             }
             if (op == TS_OP_MARGINALS) {
                 const size_t nv = lc > 0 ? n : (size_t)B * p->E;

@@ -29,8 +29,11 @@
 // Vectors are kept shifted: alpha_{t+1} = y_t - h_t with h_t the largest of the columns'
 // maxima, each entry formed as (m - h_t) + log s from its log-sum-exp state (m, s), so no
 // message ever passes through a large unshifted value; then n_t - h_t = LSE_j (alpha_{t+1}[j]
-// + beta_{t+1}[j]) and mu_t[i][j] = exp((l_t[i][j] - h_t) + alpha_t[i] + beta_{t+1}[j] -
-// (n_t - h_t)), the two large terms cancelling first.  The same for beta_t.
+// + beta_{t+1}[j]) and, with w_t[i][j] = (l_t[i][j] - h_t) + beta_{t+1}[j] (the two large
+// terms cancelling first) and z_i = max_j w_t[i][j],
+//   mu_t[i][j] = exp(w_t[i][j] - z_i) exp(z_i + alpha_t[i] - (n_t - h_t)),
+// where the first factor is also the term of row i's log-sum-exp state that gives beta_t[i]:
+// one exponential per entry for both.  The same shifting for beta_t.
 //
 // Layout of a 64 x 64 matrix in registers (loads and the leaf's uses): thread t holds rows
 // (t >> 4) + 16 i, i < 4, and columns 4 (t & 15) .. + 3 as four float4; rows and columns
@@ -89,6 +92,7 @@ struct ChunkUpArgs {
     float* core;         // level-lc nodes
     double* ro;
     double* co;
+    int32_t* lin;        // per node: 1 when core holds S itself (linear path), 0 for log S
 };
 
 // value of lanes l and l ^ 16 / l ^ 32 combined by max (one lane swap each)
@@ -301,6 +305,7 @@ __device__ void chunk_up_exact(const ChunkUpArgs& a, int64_t b, int64_t t0, int6
     // ---- the node: core and offsets
     const float* cop = sbuf[(np - 1) & 1];   // co of the last product (zeros for one edge)
     float* Pc = a.core + pn * CC;
+    if (tid == 0) a.lin[pn] = 0;
     for (int idx = tid; idx < kCP * kCP; idx += kCT) {
         const int r = idx >> 6, c = idx & (kCP - 1);
         if (r < C && c < C) Pc[(size_t)r * C + c] = P[r * kLD + c];
@@ -498,19 +503,20 @@ __device__ bool chunk_up_linear(const ChunkUpArgs& a, int64_t b, int64_t t0, int
         if (flag[cur]) return false;   // (a flag is written only before the barrier of its parity)
     }
 
-    // the node: core = log S (lane: row ac, columns 16 m + 4 g + r), ro, co
+    // the node in linear form: S itself (lane: row ac, columns 16 m + 4 g + r; every real
+    // entry in [2^-87, 1)), ro, co
+    if (tid == 0) a.lin[pn] = 1;
     if (ac < C) {
         float* row = a.core + pn * CC + (size_t)ac * C;
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
             const int c0 = 16 * m + 4 * g;
             if constexpr (kVec) {
-                if (c0 < C)
-                    *(float4*)(row + c0) = make_float4(flog(T[m][0]), flog(T[m][1]), flog(T[m][2]), flog(T[m][3]));
+                if (c0 < C) *(float4*)(row + c0) = make_float4(T[m][0], T[m][1], T[m][2], T[m][3]);
             } else {
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
-                    if (c0 + r < C) row[c0 + r] = flog(T[m][r]);
+                    if (c0 + r < C) row[c0 + r] = T[m][r];
             }
         }
         if (g == 0) a.ro[pn * C + ac] = (double)esum * 0.6931471805599453;
@@ -665,7 +671,7 @@ __global__ __launch_bounds__(kCT) void k_chunk_form(ChunkFormArgs a) {
     __syncthreads();   // al and hs complete
 
     // ---- right to left: the marginals of edge t from registers, then
-    // beta_t[r] = (m_r - h) + log s_r, the row states of l_t[r][c] + beta_{t+1}[c]
+    // beta_t[r] = (m_r - hb) + log s_r from the row states (m_r, s_r) of w_t[r][.]
     float bcur = lane < C ? (a.v ? a.v[nv + lane] : 0.f) : -INFINITY;   // lane c: beta_{t+1}[c]
     load_mat<kVec>(leaves + (size_t)(t1 - 1) * CC, C, x);
     for (int64_t t = t1 - 1; t >= t0; --t) {
@@ -683,12 +689,17 @@ __global__ __launch_bounds__(kCT) void k_chunk_form(ChunkFormArgs a) {
         for (int i = 0; i < 4; ++i) {
             const int r = rg + 16 * i;
             const float ai = al[k][r];
-            float4 mu;
-            mu.x = fexp((x[i].x - h) + ai + bq[0] - n);
-            mu.y = fexp((x[i].y - h) + ai + bq[1] - n);
-            mu.z = fexp((x[i].z - h) + ai + bq[2] - n);
-            mu.w = fexp((x[i].w - h) + ai + bq[3] - n);
-            if (n == -INFINITY) mu = make_float4(0.f, 0.f, 0.f, 0.f);
+            // row state of (l_t[r][c] - h) + beta_{t+1}[c] over the row's 64 columns (the 16
+            // lanes of the row group); its exponentials serve the marginals as well:
+            // mu[r][c] = exp(v_c - sh) * exp(sh + alpha_t[r] - (n_t - h)) <= 1
+            const float v0 = (x[i].x - h) + bq[0], v1 = (x[i].y - h) + bq[1],
+                        v2 = (x[i].z - h) + bq[2], v3 = (x[i].w - h) + bq[3];
+            zm[i] = row16_max(fmaxf(fmaxf(v0, v1), fmaxf(v2, v3)));
+            const float sh = safe_shift(zm[i]);
+            const float e0 = fexp(v0 - sh), e1 = fexp(v1 - sh), e2 = fexp(v2 - sh), e3 = fexp(v3 - sh);
+            zs[i] = row16_sum((e0 + e1) + (e2 + e3));
+            const float f = n == -INFINITY ? 0.f : fexp((sh + ai) - n);
+            const float4 mu = make_float4(e0 * f, e1 * f, e2 * f, e3 * f);
             if (r < C) {
                 float* p = o + (size_t)r * C + 4 * c4;
                 if constexpr (kVec) {
@@ -700,12 +711,6 @@ __global__ __launch_bounds__(kCT) void k_chunk_form(ChunkFormArgs a) {
                     if (4 * c4 + 3 < C) p[3] = mu.w;
                 }
             }
-            // row state over the row's 64 columns (the 16 lanes of the row group)
-            const float v0 = x[i].x + bq[0], v1 = x[i].y + bq[1], v2 = x[i].z + bq[2],
-                        v3 = x[i].w + bq[3];
-            zm[i] = row16_max(fmaxf(fmaxf(v0, v1), fmaxf(v2, v3)));
-            const float sh = safe_shift(zm[i]);
-            zs[i] = row16_sum(fexp(v0 - sh) + fexp(v1 - sh) + fexp(v2 - sh) + fexp(v3 - sh));
         }
         // lane c4 == 0 of row group rg holds rows rg + 16 i: wave w covers rows 4w .. 4w+3
         // (+ 16 i); stored as pm[par][i][r] so that every wave reads four partials per row
@@ -747,6 +752,7 @@ struct ChunkScanArgs {
     const float* core;    // [B * nodes][C][C]: the chunk nodes, or the potentials when lc == 0
     const double* ro;     // [B * nodes][C] (nullptr: zeros, lc == 0)
     const double* co;
+    const int32_t* lin;   // per node: core holds S (1) or log S (0); nullptr: log S
     int64_t nodes;        // node stride per sequence
     const int32_t* lengths;
     int64_t N, C;
@@ -777,9 +783,11 @@ __global__ __launch_bounds__(kCT) void k_chunk_scan(ChunkScanArgs a) {
     // the matrices of the next kScanAhead steps in registers (step k uses slot k % kScanAhead)
     float4 x[kScanAhead][4];
     double rr[kScanAhead], cr[kScanAhead];
+    int lf[kScanAhead];
     auto fetch = [&](int slot, int64_t step) {
         const int64_t q = fwd ? step : K - 1 - step;
         if (step >= (fwd ? K : K - 1)) return;
+        lf[slot] = a.lin ? a.lin[base + q] : 0;
         load_mat<kVec>(a.core + (base + q) * CC, C, x[slot]);
         rr[slot] = (a.ro && lv) ? a.ro[(base + q) * C + lane] : 0.0;
         cr[slot] = (a.co && lv) ? a.co[(base + q) * C + lane] : 0.0;
@@ -803,9 +811,55 @@ __global__ __launch_bounds__(kCT) void k_chunk_scan(ChunkScanArgs a) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) m4[i] = x[s][i];
             const double ro = rr[s], co = cr[s];
+            const bool lin = lf[s] != 0;
             fetch(s, k + kScanAhead);
-            if (fwd) {
-                // w[i] = u[i] + ro[i], shifted; column states over the thread's four rows
+            if (lin) {
+                // linear node (every real entry of S in [2^-87, 1), padding read as -inf -> 0):
+                // the weights exp(w - W) times S, summed; one exponential per lane
+                const double wd = lv ? (fwd ? (double)cur + ro : co + (double)cur) : -INFINITY;
+                const float W = safe_shift(wave_max_fast((float)wd));
+                const float ew = lv ? fexp((float)(wd - (double)W)) : 0.f;
+                float y;
+                if (fwd) {
+                    float er[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) er[i] = __shfl(ew, rg + 16 * i, kWave);
+                    float yq[4];
+#pragma unroll
+                    for (int qq = 0; qq < 4; ++qq)
+                        yq[qq] = sum_x32(sum_x16(er[0] * fmaxf(f4get(m4[0], qq), 0.f) + er[1] * fmaxf(f4get(m4[1], qq), 0.f) +
+                                                 er[2] * fmaxf(f4get(m4[2], qq), 0.f) + er[3] * fmaxf(f4get(m4[3], qq), 0.f)));
+                    if (lane < 16) *(float4*)&ps[par][w][4 * lane] = make_float4(yq[0], yq[1], yq[2], yq[3]);
+                    __syncthreads();
+                    y = (ps[par][0][lane] + ps[par][1][lane]) + (ps[par][2][lane] + ps[par][3][lane]);
+                } else {
+                    float bq[4];
+#pragma unroll
+                    for (int qq = 0; qq < 4; ++qq) bq[qq] = __shfl(ew, 4 * c4 + qq, kWave);
+                    float zs[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        zs[i] = row16_sum(fmaxf(m4[i].x, 0.f) * bq[0] + fmaxf(m4[i].y, 0.f) * bq[1] +
+                                          fmaxf(m4[i].z, 0.f) * bq[2] + fmaxf(m4[i].w, 0.f) * bq[3]);
+                    if (c4 == 0) {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) ps[par][i][rg + 16 * i] = zs[i];
+                    }
+                    __syncthreads();
+                    y = ps[par][lane >> 4][lane];
+                }
+                const double z = (lv && y > 0.f) ? (fwd ? co : ro) + (double)flog(y) : -INFINITY;
+                const float Z = safe_shift(wave_max_fast((float)z));
+                cur = (float)(z - (double)Z);
+                if (fwd) {
+                    acc += (double)W + (double)Z;
+                    if (a.u && w == 0 && lv && k + 1 < K) a.u[(base + k + 1) * C + lane] = cur;
+                } else {
+                    const int64_t q = K - 1 - k;
+                    if (w == 0 && lv) a.v[(base + q - 1) * C + lane] = cur;
+                }
+            } else if (fwd) {
+                // log node: w[i] = u[i] + ro[i], shifted; column states over the thread's four rows
                 const double wd = lv ? (double)cur + ro : -INFINITY;
                 const float W = safe_shift(wave_max_fast((float)wd));
                 const float wf = lv ? (float)(wd - (double)W) : -INFINITY;
@@ -843,7 +897,7 @@ __global__ __launch_bounds__(kCT) void k_chunk_scan(ChunkScanArgs a) {
                 acc += (double)W + (double)Z;
                 if (a.u && w == 0 && lv && k + 1 < K) a.u[(base + k + 1) * C + lane] = cur;
             } else {
-                // w[j] = co[j] + v[j], shifted; row states over the 16 lanes of a row group
+                // log node: w[j] = co[j] + v[j], shifted; row states over the 16 lanes of a row group
                 const double wd = lv ? co + (double)cur : -INFINITY;
                 const float W = safe_shift(wave_max_fast((float)wd));
                 const float wf = lv ? (float)(wd - (double)W) : -INFINITY;
@@ -894,7 +948,7 @@ hipError_t launch_chunk_up(const Plan& p, const float* pot, const int32_t* lengt
     a.pot = pot; a.lengths = lengths; a.N = p.N; a.C = p.C;
     a.lc = p.lc;
     a.nodes = p.Np >> p.lc;
-    a.core = p.core[p.lc]; a.ro = p.ro[p.lc]; a.co = p.co[p.lc];
+    a.core = p.core[p.lc]; a.ro = p.ro[p.lc]; a.co = p.co[p.lc]; a.lin = p.clin;
     const dim3 grid((unsigned)(p.B * a.nodes));
     if (p.C % 4 == 0)
         hipLaunchKernelGGL(k_chunk_up<true>, grid, dim3(kCT), 0, s, a);
@@ -907,7 +961,7 @@ hipError_t launch_chunk_scan(const Plan& p, const float* pot, const int32_t* len
                              float* logZ, hipStream_t s) {
     ChunkScanArgs a{};
     if (p.lc > 0) {
-        a.core = p.core[p.lc]; a.ro = p.ro[p.lc]; a.co = p.co[p.lc];
+        a.core = p.core[p.lc]; a.ro = p.ro[p.lc]; a.co = p.co[p.lc]; a.lin = p.clin;
         a.nodes = p.Np >> p.lc;
     } else {
         a.core = pot; a.ro = nullptr; a.co = nullptr;   // one edge per chunk: the leaves

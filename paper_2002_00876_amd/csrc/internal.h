@@ -32,6 +32,7 @@ struct Plan {
     // u[lc], v[lc]) and k_chunk_form the marginals inside each chunk; no other level is formed
     bool chunk = false;
     int lc = 0;
+    int32_t* clin = nullptr;   // per chunk node: its core holds S (1) or log S (0)
     // log semiring, levels 1..D (index by level)
     float* core[kMaxLevels] = {};
     double* ro[kMaxLevels] = {};
