@@ -52,14 +52,16 @@ constexpr float kChunkUnderflow = 0x1p-80f;
 
 typedef float f16v __attribute__((ext_vector_type(16)));
 
-template <bool kVec>
+template <bool kVec, bool kFull = false>
 __device__ __forceinline__ void load_mat(const float* __restrict__ M, int C, float4 (&x)[4]) {
     const int rg = threadIdx.x >> 4, c = 4 * (threadIdx.x & 15);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int r = rg + 16 * i;
         const float* p = M + (size_t)r * C + c;
-        if constexpr (kVec) {
+        if constexpr (kFull) {
+            x[i] = *(const float4*)p;
+        } else if constexpr (kVec) {
             x[i] = (r < C && c < C) ? *(const float4*)p
                                     : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
         } else {
@@ -327,10 +329,10 @@ __device__ void chunk_up_exact(const ChunkUpArgs& a, int64_t b, int64_t t0, int6
 // formed transposed, T_p = B_p^T T_{p-1} with T = S^T: wave w owns the columns a = 16 w ..
 // 16 w + 15 of T, and the accumulators of v_mfma_f32_16x16x4f32 (lane l: T[16 m + 4 (l / 16)
 // + r][16 w + l % 16]) are exactly the right operand of the next product, so T never leaves
-// the registers.  T_{-1} = I.  The result equals the exact path's up to rounding as long as
-// every entry of every S_p (rows of S_{p-1} at most 1, columns of B_p at most 1) is at least
-// 2^-80: then nothing below fp32's normal range ever enters a sum that matters.  Otherwise
-// the path reports failure and the chunk is redone by the exact path.
+// the registers (T_0 = B_0^T is read from LDS).  The result equals the exact path's up to
+// rounding as long as every entry of every S_p (rows of S_{p-1} at most 1, columns of B_p at
+// most 1) is at least 2^-80: then nothing below fp32's normal range ever enters a sum that
+// matters.  Otherwise the path reports failure and the chunk is redone by the exact path.
 struct LinSmem {
     float bt[2][kCP * kCP];   // B of two products, transposed (bt[c][k]), 16-byte groups swizzled
     float red[2][4][kCP];     // per-wave partial column maxima of two leaves
@@ -342,14 +344,16 @@ struct LinSmem {
 __device__ __forceinline__ int bt_off(int c, int kg) { return c * kCP + 4 * (kg ^ ((c ^ (c >> 2)) & 15)); }
 
 // thread t: rows 4 (t >> 4) + i, columns 4 (t & 15) .. + 3 (past C: -inf)
-template <bool kVec>
+template <bool kVec, bool kFull>
 __device__ __forceinline__ void load_rows4(const float* __restrict__ M, int C, float4 (&x)[4]) {
     const int r0 = 4 * (threadIdx.x >> 4), c = 4 * (threadIdx.x & 15);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int r = r0 + i;
         const float* p = M + (size_t)r * C + c;
-        if constexpr (kVec) {
+        if constexpr (kFull) {
+            x[i] = *(const float4*)p;
+        } else if constexpr (kVec) {
             x[i] = (r < C && c < C) ? *(const float4*)p
                                     : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
         } else {
@@ -361,7 +365,7 @@ __device__ __forceinline__ void load_rows4(const float* __restrict__ M, int C, f
     }
 }
 
-template <bool kVec>
+template <bool kVec, bool kFull>
 __device__ bool chunk_up_linear(const ChunkUpArgs& a, int64_t b, int64_t t0, int64_t t1,
                                 size_t pn, LinSmem& sm, int (&flag)[2]) {
     typedef float f4v __attribute__((ext_vector_type(4)));
@@ -380,13 +384,16 @@ __device__ bool chunk_up_linear(const ChunkUpArgs& a, int64_t b, int64_t t0, int
     float cbc[4];          // cb at the thread's columns 4 c4 + q
     double CO = 0.0;
 
+    // (the leaf work runs in log2 units: v, cb and CO below are natural-log values times
+    // log2 e, so that every entry of B is one exp2)
+    constexpr float kL2E = 1.4426950408889634f;
     auto make_v = [&]() {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            v[i][0] = cbr[i] + lf[i].x;
-            v[i][1] = cbr[i] + lf[i].y;
-            v[i][2] = cbr[i] + lf[i].z;
-            v[i][3] = cbr[i] + lf[i].w;
+            v[i][0] = fmaf(lf[i].x, kL2E, cbr[i]);
+            v[i][1] = fmaf(lf[i].y, kL2E, cbr[i]);
+            v[i][2] = fmaf(lf[i].z, kL2E, cbr[i]);
+            v[i][3] = fmaf(lf[i].w, kL2E, cbr[i]);
         }
     };
     // the wave's column maxima of v (its 16 rows) into red[par][w]
@@ -422,7 +429,8 @@ __device__ bool chunk_up_linear(const ChunkUpArgs& a, int64_t b, int64_t t0, int
         for (int q = 0; q < 4; ++q) {
             const float sh = safe_shift(sc[q]);
             *(float4*)(bt + bt_off(4 * c4 + q, rg)) =
-                make_float4(fexp(v[0][q] - sh), fexp(v[1][q] - sh), fexp(v[2][q] - sh), fexp(v[3][q] - sh));
+                make_float4(__builtin_amdgcn_exp2f(v[0][q] - sh), __builtin_amdgcn_exp2f(v[1][q] - sh),
+                            __builtin_amdgcn_exp2f(v[2][q] - sh), __builtin_amdgcn_exp2f(v[3][q] - sh));
             cbc[q] = sc[q] - M;
         }
 #pragma unroll
@@ -431,26 +439,22 @@ __device__ bool chunk_up_linear(const ChunkUpArgs& a, int64_t b, int64_t t0, int
     };
 
     // prologue: B_0 (cb_{-1} = 0) and the column maxima of leaf 1
-    load_rows4<kVec>(leaves + (size_t)t0 * CC, C, lf);
+    load_rows4<kVec, kFull>(leaves + (size_t)t0 * CC, C, lf);
 #pragma unroll
     for (int i = 0; i < 4; ++i) cbr[i] = 0.f;
     make_v();
     partials(0);
-    if (np > 1) load_rows4<kVec>(leaves + (size_t)(t0 + 1) * CC, C, lf);
+    if (np > 1) load_rows4<kVec, kFull>(leaves + (size_t)(t0 + 1) * CC, C, lf);
     __syncthreads();
     prep(0, 0);
     if (np > 1) {
         make_v();
         partials(1);
-        if (np > 2) load_rows4<kVec>(leaves + (size_t)(t0 + 2) * CC, C, lf);
+        if (np > 2) load_rows4<kVec, kFull>(leaves + (size_t)(t0 + 2) * CC, C, lf);
     }
     __syncthreads();
 
     f4v T[4];
-#pragma unroll
-    for (int m = 0; m < 4; ++m)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) T[m][r] = (16 * m + 4 * g + r == ac) ? 1.f : 0.f;
     int esum = 0;
     const int xb = 64 * lr + 4 * (g ^ lr ^ (lr >> 2));
     const int cl = ac < C ? C - 4 * g : 0;   // entry (16 m + 4 g + r, ac) is real iff 16 m + r < cl
@@ -464,23 +468,48 @@ __device__ bool chunk_up_linear(const ChunkUpArgs& a, int64_t b, int64_t t0, int
         // (bt_off(16 mb + lr, 4 mp + g) = 1024 mb + (xb ^ 16 (mp ^ mb)), xb = 64 lr + 4 (g ^ lr ^ lr / 4))
         const float* bt = sm.bt[cur];
         f4v U[4];
+        if (p == 0) {
+            // T_0 = B_0^T, read from the transposed buffer (entry (c, k = ac))
 #pragma unroll
-        for (int m = 0; m < 4; ++m) U[m] = (f4v){0.f, 0.f, 0.f, 0.f};
+            for (int m = 0; m < 4; ++m)
 #pragma unroll
-        for (int mp = 0; mp < 4; ++mp)
+                for (int r = 0; r < 4; ++r) U[m][r] = bt[bt_off(16 * m + 4 * g + r, ac >> 2) + (ac & 3)];
+        } else {
 #pragma unroll
-            for (int mb = 0; mb < 4; ++mb) {
-                const float4 av = *(const float4*)(bt + 1024 * mb + (xb ^ (16 * (mp ^ mb))));
-                U[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, T[mp][0], U[mb], 0, 0, 0);
-                U[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, T[mp][1], U[mb], 0, 0, 0);
-                U[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, T[mp][2], U[mb], 0, 0, 0);
-                U[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, T[mp][3], U[mb], 0, 0, 0);
+            for (int m = 0; m < 4; ++m) U[m] = (f4v){0.f, 0.f, 0.f, 0.f};
+            // (each left operand is read one step ahead of its four products; the products form
+            // a scheduling region of their own with that order imposed)
+            __builtin_amdgcn_sched_barrier(0);
+            float4 av[2];
+            av[0] = *(const float4*)(bt + xb);
+#pragma unroll
+            for (int st = 0; st < 16; ++st) {
+                const int mp = st >> 2, mb = st & 3;
+                if (st + 1 < 16) {
+                    const int mp1 = (st + 1) >> 2, mb1 = (st + 1) & 3;
+                    av[(st + 1) & 1] = *(const float4*)(bt + 1024 * mb1 + (xb ^ (16 * (mp1 ^ mb1))));
+                }
+                const float4 a4 = av[st & 1];
+                U[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.x, T[mp][0], U[mb], 0, 0, 0);
+                U[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.y, T[mp][1], U[mb], 0, 0, 0);
+                U[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.z, T[mp][2], U[mb], 0, 0, 0);
+                U[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.w, T[mp][3], U[mb], 0, 0, 0);
             }
+            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+#pragma unroll
+            for (int st = 1; st < 15; ++st) {
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
         // leaf p + 2's column maxima (its load was issued a product ago), leaf p + 3's load
         if (p + 2 < np) {
             make_v();
             partials(p & 1);
-            if (p + 3 < np) load_rows4<kVec>(leaves + (size_t)(t0 + p + 3) * CC, C, lf);
+            if (p + 3 < np) load_rows4<kVec, kFull>(leaves + (size_t)(t0 + p + 3) * CC, C, lf);
         }
         // scale column ac of T (row ac of S) by the power of two that brings its maximum into
         // [1/2, 1); any real entry below 2^-80 sends the chunk to the exact path
@@ -490,7 +519,7 @@ __device__ bool chunk_up_linear(const ChunkUpArgs& a, int64_t b, int64_t t0, int
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 mx = fmaxf(mx, U[m][r]);
-                if (16 * m + r < cl) mn = fminf(mn, U[m][r]);
+                if (kFull || 16 * m + r < cl) mn = fminf(mn, U[m][r]);
             }
         mx = max_x32(max_x16(mx));
         if (__builtin_amdgcn_ballot_w64(!(mn >= kChunkUnderflow)) && lane == 0) flag[cur] = 1;
@@ -524,7 +553,7 @@ __device__ bool chunk_up_linear(const ChunkUpArgs& a, int64_t b, int64_t t0, int
     if (rg == 0) {
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-            if (4 * c4 + q < C) a.co[pn * C + 4 * c4 + q] = CO + (double)cbc[q];
+            if (4 * c4 + q < C) a.co[pn * C + 4 * c4 + q] = (CO + (double)cbc[q]) * 0.6931471805599453;
     }
     return true;
 }
@@ -534,7 +563,7 @@ union ChunkUpSmem {
     LinSmem lin;
 };
 
-template <bool kVec>
+template <bool kVec, bool kFull>
 __global__ __launch_bounds__(kCT, 4) void k_chunk_up(ChunkUpArgs a) {
     __shared__ ChunkUpSmem sm;
     __shared__ int flag[2];
@@ -546,7 +575,7 @@ __global__ __launch_bounds__(kCT, 4) void k_chunk_up(ChunkUpArgs a) {
     const size_t pn = (size_t)(b * a.nodes + q);
     if (threadIdx.x < 2) flag[threadIdx.x] = 0;
     __syncthreads();
-    if (!chunk_up_linear<kVec>(a, b, t0, t1, pn, sm.lin, flag))
+    if (!chunk_up_linear<kVec, kFull>(a, b, t0, t1, pn, sm.lin, flag))
         chunk_up_exact<kVec>(a, b, t0, t1, pn, sm.exact);
 }
 
@@ -599,7 +628,7 @@ __device__ __forceinline__ float shifted_from_partials(const float (*pm)[kCP], c
     return m == -INFINITY ? -INFINITY : (m - h) + flog(s);
 }
 
-template <bool kVec>
+template <bool kVec, bool kFull>
 __global__ __launch_bounds__(kCT) void k_chunk_form(ChunkFormArgs a) {
     __shared__ __align__(16) float al[kMaxChunk + 1][kCP];   // alpha_t, shifted (t - t0)
     __shared__ float hs[kMaxChunk];                          // h_t: the shift of alpha_{t+1}
@@ -634,12 +663,12 @@ __global__ __launch_bounds__(kCT) void k_chunk_form(ChunkFormArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) ar[i] = __shfl(acur, rg + 16 * i, kWave);
     float4 x[4], xn[4];
-    load_mat<kVec>(leaves + (size_t)t0 * CC, C, x);
+    load_mat<kVec, kFull>(leaves + (size_t)t0 * CC, C, x);
 
     // ---- left to right: y_t[c] = LSE_r (alpha_t[r] + l_t[r][c]); alpha_{t+1} = y_t - h_t
     for (int64_t t = t0; t < t1; ++t) {
         const int k = (int)(t - t0), par = k & 1;
-        if (t + 1 < t1) load_mat<kVec>(leaves + (size_t)(t + 1) * CC, C, xn);
+        if (t + 1 < t1) load_mat<kVec, kFull>(leaves + (size_t)(t + 1) * CC, C, xn);
         // the wave's state (m, s) of each of the thread's columns over the wave's 16 rows
         float mq[4], sq[4];
 #pragma unroll
@@ -673,10 +702,10 @@ __global__ __launch_bounds__(kCT) void k_chunk_form(ChunkFormArgs a) {
     // ---- right to left: the marginals of edge t from registers, then
     // beta_t[r] = (m_r - hb) + log s_r from the row states (m_r, s_r) of w_t[r][.]
     float bcur = lane < C ? (a.v ? a.v[nv + lane] : 0.f) : -INFINITY;   // lane c: beta_{t+1}[c]
-    load_mat<kVec>(leaves + (size_t)(t1 - 1) * CC, C, x);
+    load_mat<kVec, kFull>(leaves + (size_t)(t1 - 1) * CC, C, x);
     for (int64_t t = t1 - 1; t >= t0; --t) {
         const int k = (int)(t - t0), par = k & 1;
-        if (t > t0) load_mat<kVec>(leaves + (size_t)(t - 1) * CC, C, xn);
+        if (t > t0) load_mat<kVec, kFull>(leaves + (size_t)(t - 1) * CC, C, xn);
         // the edge's normaliser less h_t (lane c holds column c)
         const float n = wave_lse64(lane < C ? al[k + 1][lane] + bcur : -INFINITY);
         const float h = hs[k];
@@ -700,10 +729,10 @@ __global__ __launch_bounds__(kCT) void k_chunk_form(ChunkFormArgs a) {
             zs[i] = row16_sum((e0 + e1) + (e2 + e3));
             const float f = n == -INFINITY ? 0.f : fexp((sh + ai) - n);
             const float4 mu = make_float4(e0 * f, e1 * f, e2 * f, e3 * f);
-            if (r < C) {
+            if (kFull || r < C) {
                 float* p = o + (size_t)r * C + 4 * c4;
                 if constexpr (kVec) {
-                    if (4 * c4 < C) *(float4*)p = mu;
+                    if (kFull || 4 * c4 < C) *(float4*)p = mu;
                 } else {
                     if (4 * c4 + 0 < C) p[0] = mu.x;
                     if (4 * c4 + 1 < C) p[1] = mu.y;
@@ -950,10 +979,12 @@ hipError_t launch_chunk_up(const Plan& p, const float* pot, const int32_t* lengt
     a.nodes = p.Np >> p.lc;
     a.core = p.core[p.lc]; a.ro = p.ro[p.lc]; a.co = p.co[p.lc]; a.lin = p.clin;
     const dim3 grid((unsigned)(p.B * a.nodes));
-    if (p.C % 4 == 0)
-        hipLaunchKernelGGL(k_chunk_up<true>, grid, dim3(kCT), 0, s, a);
+    if (p.C == kCP)
+        hipLaunchKernelGGL((k_chunk_up<true, true>), grid, dim3(kCT), 0, s, a);
+    else if (p.C % 4 == 0)
+        hipLaunchKernelGGL((k_chunk_up<true, false>), grid, dim3(kCT), 0, s, a);
     else
-        hipLaunchKernelGGL(k_chunk_up<false>, grid, dim3(kCT), 0, s, a);
+        hipLaunchKernelGGL((k_chunk_up<false, false>), grid, dim3(kCT), 0, s, a);
     return hipGetLastError();
 }
 
@@ -988,10 +1019,12 @@ hipError_t launch_chunk_form(const Plan& p, const float* pot, const int32_t* len
     a.v = p.v[p.lc];
     a.marg = marg;
     const dim3 grid((unsigned)(p.B * a.nodes));
-    if (p.C % 4 == 0)
-        hipLaunchKernelGGL(k_chunk_form<true>, grid, dim3(kCT), 0, s, a);
+    if (p.C == kCP)
+        hipLaunchKernelGGL((k_chunk_form<true, true>), grid, dim3(kCT), 0, s, a);
+    else if (p.C % 4 == 0)
+        hipLaunchKernelGGL((k_chunk_form<true, false>), grid, dim3(kCT), 0, s, a);
     else
-        hipLaunchKernelGGL(k_chunk_form<false>, grid, dim3(kCT), 0, s, a);
+        hipLaunchKernelGGL((k_chunk_form<false, false>), grid, dim3(kCT), 0, s, a);
     return hipGetLastError();
 }
 
