@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdlib>
+#include <cmath>
 #include <cstring>
 #include <mutex>
 #include <string>
@@ -123,7 +124,18 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, boo
         if (p->chunk) {
             // the chunk nodes (level lc; the leaves themselves when lc == 0) and, for the
             // marginals, their outside vectors
-            const int lc = D < kChunkLog ? D : kChunkLog;
+            // chunks of S = 2^lc edges.  For log Z alone the critical path is about S - 1
+            // chunk products and E / S steps of the recursion over chunks; with their
+            // measured costs (about 2 : 1.1) its minimum lies near S = sqrt(0.55 E).  The
+            // marginals keep the longest chunks: every chunk boundary passes the messages
+            // through float storage, and fewer boundaries keep wide-range inputs within
+            // the marginals' absolute tolerance.
+            int lc = D < kChunkLog ? D : kChunkLog;
+            if (op == TS_OP_LOGPARTITION && D > 0) {
+                const double sopt = std::sqrt(0.55 * (double)p->E);
+                const int l2 = (int)std::lround(std::log2(sopt > 2.0 ? sopt : 2.0));
+                lc = l2 < lc ? l2 : lc;
+            }
             const size_t n = (size_t)B * (size_t)(Np >> lc);
             p->lc = lc;
             if (lc > 0) {

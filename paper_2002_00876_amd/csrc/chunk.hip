@@ -774,8 +774,8 @@ __global__ __launch_bounds__(kCT) void k_chunk_form(ChunkFormArgs a) {
 //   u_0 = 0,      u_{q+1}[j] = LSE_i (u_q[i] + M_q[i][j]),        log Z = LSE_j u_K[j],
 //   v_{K-1} = 0,  v_{q-1}[i] = LSE_j (M_q[i][j] + v_q[j]),
 // the outside vectors of the chunk nodes (u_q the forward message into chunk q's first edge,
-// v_q the backward message out of its last edge), each stored shifted to max 0 while the
-// shifts are summed in float64 for log Z.  The matrices are independent of the vectors, so
+// v_q the backward message out of its last edge), carried in float64 shifted to max 0 and
+// stored as float; the shifts are summed in float64 for log Z.  The matrices are independent of the vectors, so
 // they are loaded kScanAhead steps ahead of their use and each step costs one barrier.
 struct ChunkScanArgs {
     const float* core;    // [B * nodes][C][C]: the chunk nodes, or the potentials when lc == 0
@@ -823,11 +823,12 @@ __global__ __launch_bounds__(kCT) void k_chunk_scan(ChunkScanArgs a) {
     };
 #pragma unroll
     for (int s = 0; s < kScanAhead; ++s) fetch(s, s);
-    float cur = lv ? 0.f : -INFINITY;   // lane c: entry c of u_q (forward) or v_q (backward)
+    double cur = lv ? 0.0 : -INFINITY;  // lane c: entry c of u_q (forward) or v_q (backward),
+                                        // shifted to max 0 (float64: see the log steps)
     double acc = 0.0;
     if (w == 0 && lv) {
-        if (fwd && a.u) a.u[base * C + lane] = cur;
-        if (!fwd) a.v[(base + K - 1) * C + lane] = cur;
+        if (fwd && a.u) a.u[base * C + lane] = 0.f;
+        if (!fwd) a.v[(base + K - 1) * C + lane] = 0.f;
     }
     const int64_t steps = fwd ? K : K - 1;
     for (int64_t k0 = 0; k0 < steps; k0 += kScanAhead) {
@@ -845,7 +846,7 @@ __global__ __launch_bounds__(kCT) void k_chunk_scan(ChunkScanArgs a) {
             if (lin) {
                 // linear node (every real entry of S in [2^-87, 1), padding read as -inf -> 0):
                 // the weights exp(w - W) times S, summed; one exponential per lane
-                const double wd = lv ? (fwd ? (double)cur + ro : co + (double)cur) : -INFINITY;
+                const double wd = lv ? (fwd ? cur + ro : co + cur) : -INFINITY;
                 const float W = safe_shift(wave_max_fast((float)wd));
                 const float ew = lv ? fexp((float)(wd - (double)W)) : 0.f;
                 float y;
@@ -879,27 +880,31 @@ __global__ __launch_bounds__(kCT) void k_chunk_scan(ChunkScanArgs a) {
                 }
                 const double z = (lv && y > 0.f) ? (fwd ? co : ro) + (double)flog(y) : -INFINITY;
                 const float Z = safe_shift(wave_max_fast((float)z));
-                cur = (float)(z - (double)Z);
+                cur = z - (double)Z;
                 if (fwd) {
                     acc += (double)W + (double)Z;
-                    if (a.u && w == 0 && lv && k + 1 < K) a.u[(base + k + 1) * C + lane] = cur;
+                    if (a.u && w == 0 && lv && k + 1 < K) a.u[(base + k + 1) * C + lane] = (float)cur;
                 } else {
                     const int64_t q = K - 1 - k;
-                    if (w == 0 && lv) a.v[(base + q - 1) * C + lane] = cur;
+                    if (w == 0 && lv) a.v[(base + q - 1) * C + lane] = (float)cur;
                 }
             } else if (fwd) {
-                // log node: w[i] = u[i] + ro[i], shifted; column states over the thread's four rows
-                const double wd = lv ? (double)cur + ro : -INFINITY;
+                // log node: w[i] = u[i] + ro[i], shifted; column states over the thread's four
+                // rows.  A term w[i] + core[i][j] that matters can add two large values of
+                // opposite sign (far-apart offsets): it is formed in float64 and rounded once.
+                const double wd = lv ? cur + ro : -INFINITY;
                 const float W = safe_shift(wave_max_fast((float)wd));
-                const float wf = lv ? (float)(wd - (double)W) : -INFINITY;
-                float ar[4];
+                const double wdel = lv ? wd - (double)W : -INFINITY;
+                double ar[4];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) ar[i] = __shfl(wf, rg + 16 * i, kWave);
+                for (int i = 0; i < 4; ++i) ar[i] = __shfl(wdel, rg + 16 * i, kWave);
                 float mq[4], sq[4];
 #pragma unroll
                 for (int qq = 0; qq < 4; ++qq) {
-                    const float v0 = ar[0] + f4get(m4[0], qq), v1 = ar[1] + f4get(m4[1], qq);
-                    const float v2 = ar[2] + f4get(m4[2], qq), v3 = ar[3] + f4get(m4[3], qq);
+                    const float v0 = (float)(ar[0] + (double)f4get(m4[0], qq));
+                    const float v1 = (float)(ar[1] + (double)f4get(m4[1], qq));
+                    const float v2 = (float)(ar[2] + (double)f4get(m4[2], qq));
+                    const float v3 = (float)(ar[3] + (double)f4get(m4[3], qq));
                     const float m = max_x32(max_x16(fmaxf(fmaxf(v0, v1), fmaxf(v2, v3))));
                     const float sh = safe_shift(m);
                     mq[qq] = m;
@@ -922,22 +927,23 @@ __global__ __launch_bounds__(kCT) void k_chunk_scan(ChunkScanArgs a) {
                     z = co + (double)m + (double)flog(s);
                 }
                 const float Z = safe_shift(wave_max_fast((float)z));
-                cur = (float)(z - (double)Z);
+                cur = z - (double)Z;
                 acc += (double)W + (double)Z;
-                if (a.u && w == 0 && lv && k + 1 < K) a.u[(base + k + 1) * C + lane] = cur;
+                if (a.u && w == 0 && lv && k + 1 < K) a.u[(base + k + 1) * C + lane] = (float)cur;
             } else {
-                // log node: w[j] = co[j] + v[j], shifted; row states over the 16 lanes of a row group
-                const double wd = lv ? co + (double)cur : -INFINITY;
+                // log node: w[j] = co[j] + v[j], shifted; row states over the 16 lanes of a
+                // row group (terms formed in float64, as above)
+                const double wd = lv ? co + cur : -INFINITY;
                 const float W = safe_shift(wave_max_fast((float)wd));
-                const float wf = lv ? (float)(wd - (double)W) : -INFINITY;
-                float bq[4];
+                const double wdel = lv ? wd - (double)W : -INFINITY;
+                double bq[4];
 #pragma unroll
-                for (int qq = 0; qq < 4; ++qq) bq[qq] = __shfl(wf, 4 * c4 + qq, kWave);
+                for (int qq = 0; qq < 4; ++qq) bq[qq] = __shfl(wdel, 4 * c4 + qq, kWave);
                 float zm[4], zs[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const float v0 = m4[i].x + bq[0], v1 = m4[i].y + bq[1], v2 = m4[i].z + bq[2],
-                                v3 = m4[i].w + bq[3];
+                    const float v0 = (float)((double)m4[i].x + bq[0]), v1 = (float)((double)m4[i].y + bq[1]);
+                    const float v2 = (float)((double)m4[i].z + bq[2]), v3 = (float)((double)m4[i].w + bq[3]);
                     zm[i] = row16_max(fmaxf(fmaxf(v0, v1), fmaxf(v2, v3)));
                     const float sh = safe_shift(zm[i]);
                     zs[i] = row16_sum(fexp(v0 - sh) + fexp(v1 - sh) + fexp(v2 - sh) + fexp(v3 - sh));
@@ -955,14 +961,14 @@ __global__ __launch_bounds__(kCT) void k_chunk_scan(ChunkScanArgs a) {
                 double z = -INFINITY;
                 if (lv && m != -INFINITY) z = ro + (double)m + (double)flog(ps[par][lane >> 4][lane]);
                 const float Z = safe_shift(wave_max_fast((float)z));
-                cur = (float)(z - (double)Z);
+                cur = z - (double)Z;
                 const int64_t q = K - 1 - k;   // node q gave v_{q-1}
-                if (w == 0 && lv) a.v[(base + q - 1) * C + lane] = cur;
+                if (w == 0 && lv) a.v[(base + q - 1) * C + lane] = (float)cur;
             }
         }
     }
     if (fwd && a.logZ) {
-        const float l = wave_lse64(cur);
+        const float l = wave_lse64((float)cur);
         if (tid == 0) a.logZ[b] = l == -INFINITY ? -INFINITY : (float)(acc + (double)l);
     }
 }

@@ -56,13 +56,18 @@ def test_workspace_sizes(L, monkeypatch):
         assert ws(op, 32, 25, CW) % 256 == 0
         assert ws(op, 64, 25, CW) > ws(op, 32, 25, CW)
         assert ws(op, 32, 50, CW) > ws(op, 32, 25, CW)
-    # marginals need the log-partition buffers plus the outside vectors
-    assert ws(1, 32, 25, CW) > ws(0, 32, 25, CW)
+    # marginals need the chunk nodes plus the outside vectors
+    assert ws(1, 4, 513, CW) > ws(0, 4, 513, CW)
     # the tree over N-1 = 24 edges has levels of 16, 8, 4, 2, 1 nodes of C*C floats; with
-    # at most 64 labels the chunk kernels fold chunks of 16 edges and run the recursions
-    # over the chunk products, so only the chunk level (2 nodes) is stored
-    assert ws(0, 32, 25, CW) >= 32 * 2 * CW * CW * 4
-    assert ws(0, 32, 25, CW) < 32 * (2 + 1) * CW * CW * 4
+    # at most 64 labels the chunk kernels fold chunks of 2^lc edges and run the recursions
+    # over the chunk products, so only the chunk level is stored: for log Z lc follows the
+    # length (4 edges for 24: 32 / 4 = 8 nodes), the marginals keep 16 edges (2 nodes)
+    assert ws(0, 32, 25, CW) >= 32 * 8 * CW * CW * 4
+    assert ws(0, 32, 25, CW) < 32 * (8 + 1) * CW * CW * 4
+    assert 32 * 2 * CW * CW * 4 <= ws(1, 32, 25, CW) < 32 * 3 * CW * CW * 4
+    # longer sequences take chunks of at most 16 edges: N - 1 = 512 edges, 32 chunk nodes
+    node = CW * CW * 4 + 2 * CW * 8          # core and the float64 row and column offsets
+    assert 4 * 32 * node <= ws(0, 4, 513, CW) < 4 * 32 * node + 4096
     # above 64 labels every level is stored
     assert ws(0, 32, 25, 65) >= 32 * (16 + 8 + 4 + 2 + 1) * 65 * 65 * 4
     assert ws(7, 32, 25, CW) == 0 and ws(0, 0, 25, 20) == 0 and ws(0, 1, 25, 257) == 0
