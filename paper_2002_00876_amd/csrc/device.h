@@ -40,6 +40,19 @@ __device__ __forceinline__ double wave_sum_d(double x) {
 // Hardware exp/log (v_exp_f32 / v_log_f32 are base 2).  Inputs of the callers are
 // exponents <= 0 and sums >= 2^-80, so no denormal handling is needed.
 __device__ __forceinline__ float fexp(float x) { return __builtin_amdgcn_exp2f(x * 1.4426950408889634f); }
+
+// Raw buffer access to `n` floats at `base` (a workgroup-uniform pointer): loads take a
+// per-lane 32-bit byte offset and a uniform byte offset held in a scalar register; an
+// access past the n floats reads 0.  The descriptor's third word is the gfx9 raw-buffer
+// format (no stride, no swizzle).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float* base, int n) {
+    return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, 4 * n, 0x00020000);
+}
+__device__ __forceinline__ float4 buffer_load4(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff) {
+    typedef int v4i __attribute__((ext_vector_type(4)));
+    const v4i x = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    return make_float4(__int_as_float(x.x), __int_as_float(x.y), __int_as_float(x.z), __int_as_float(x.w));
+}
 __device__ __forceinline__ float flog(float x) { return __builtin_amdgcn_logf(x) * 0.6931471805599453f; }
 
 // Full-wave reductions with DPP inside each row of 16 lanes and readlane across the four

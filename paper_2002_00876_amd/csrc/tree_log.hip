@@ -671,14 +671,22 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
     static_assert(NB == 4 || NB == 2, "contracted rows of a thread: one or half a float4");
     const int ar = tid / GA, ak = 4 * (tid % GA);
     const int bk = NB * (tid / GB), bc = 4 * (tid % GB);
-    const float* Lrow = Lc + (size_t)(a0 + ar) * C + ak;
-    const float* Rrow = Rc + (size_t)bk * C + c0 + bc;
+    // loads: raw buffer loads over each child matrix (C * C floats), a fixed 32-bit byte
+    // offset per thread and register and the slice's offset in a scalar register, so that
+    // no address arithmetic is repeated per slice
+    const __amdgpu_buffer_rsrc_t rsL = make_rsrc(Lc, C * C);
+    const __amdgpu_buffer_rsrc_t rsR = make_rsrc(Rc, C * C);
+    unsigned offa[NA], offb[NB];
+#pragma unroll
+    for (int it = 0; it < NA; ++it) offa[it] = 4u * (unsigned)((a0 + ar + 32 * it) * C + ak);
+#pragma unroll
+    for (int it = 0; it < NB; ++it) offb[it] = 4u * (unsigned)((bk + it) * C + c0 + bc);
     float4 ra[2][NA], rb[2][NB];
     auto gload = [&](float4 (&xa)[NA], float4 (&xb)[NB], int ks) {
 #pragma unroll
-        for (int it = 0; it < NA; ++it) xa[it] = *(const float4*)(Lrow + (size_t)(32 * it) * C + ks);
+        for (int it = 0; it < NA; ++it) xa[it] = buffer_load4(rsL, offa[it], 4 * ks);
 #pragma unroll
-        for (int it = 0; it < NB; ++it) xb[it] = *(const float4*)(Rrow + (size_t)(ks + it) * C);
+        for (int it = 0; it < NB; ++it) xb[it] = buffer_load4(rsR, offb[it], 4 * ks * C);
     };
     float sas[NA], sbs[4];
     // the offsets of the staged contracted indices (A: ak..ak+3, B: bk..bk+NB-1), scaled by
