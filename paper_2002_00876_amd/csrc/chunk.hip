@@ -662,7 +662,7 @@ __global__ __launch_bounds__(kCT) void k_chunk_form(ChunkFormArgs a) {
     float ar[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) ar[i] = __shfl(acur, rg + 16 * i, kWave);
-    float4 x[4], xn[4];
+    float4 x[4], xn[4], xs[4], xs2[4];
     load_mat<kVec, kFull>(leaves + (size_t)t0 * CC, C, x);
 
     // ---- left to right: y_t[c] = LSE_r (alpha_t[r] + l_t[r][c]); alpha_{t+1} = y_t - h_t
@@ -694,18 +694,38 @@ __global__ __launch_bounds__(kCT) void k_chunk_form(ChunkFormArgs a) {
         // this thread's rows of alpha_{t+1}: rows rg + 16 i live in lanes rg + 16 i of the wave
 #pragma unroll
         for (int i = 0; i < 4; ++i) ar[i] = __shfl(anext, rg + 16 * i, kWave);
+        // the chunk's last three edges stay in registers for the right-to-left pass
+        if (t + 1 < t1) {
+            if (t + 2 == t1) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) x[i] = xn[i];
+                for (int i = 0; i < 4; ++i) xs[i] = x[i];
+            }
+            if (t + 3 == t1) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) xs2[i] = x[i];
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) x[i] = xn[i];
+        }
     }
     __syncthreads();   // al and hs complete
 
     // ---- right to left: the marginals of edge t from registers, then
     // beta_t[r] = (m_r - hb) + log s_r from the row states (m_r, s_r) of w_t[r][.]
     float bcur = lane < C ? (a.v ? a.v[nv + lane] : 0.f) : -INFINITY;   // lane c: beta_{t+1}[c]
-    load_mat<kVec, kFull>(leaves + (size_t)(t1 - 1) * CC, C, x);
-    for (int64_t t = t1 - 1; t >= t0; --t) {
+    for (int64_t t = t1 - 1; t >= t0; --t) {    // (x holds edge t1 - 1, xs t1 - 2, xs2 t1 - 3)
         const int k = (int)(t - t0), par = k & 1;
-        if (t > t0) load_mat<kVec, kFull>(leaves + (size_t)(t - 1) * CC, C, xn);
+        if (t > t0) {
+            if (t + 1 == t1) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) xn[i] = xs[i];
+            } else if (t + 2 == t1) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) xn[i] = xs2[i];
+            } else {
+                load_mat<kVec, kFull>(leaves + (size_t)(t - 1) * CC, C, xn);
+            }
+        }
         // the edge's normaliser less h_t (lane c holds column c)
         const float n = wave_lse64(lane < C ? al[k + 1][lane] + bcur : -INFINITY);
         const float h = hs[k];
