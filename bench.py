@@ -180,7 +180,8 @@ def sweep(kind, reps=20):
         print(json.dumps({"sweep": kind, "B": B, "N": N, "C": C,
                           "tree_flop": tree_flop, "serial_flop": serial_flop,
                           "scan_ms": round(ms_scan, 5), "sequential_ms": round(ms_seq, 5),
-                          "scan_path": "single launch" if fused else "multi-launch tree",
+                          "scan_path": ("single launch" if fused else "chunks" if C <= 64
+                                        else "multi-launch tree"),
                           "scan_tokens_per_s": round(B * N / (ms_scan * 1e-3), 1),
                           "sequential_tokens_per_s": round(B * N / (ms_seq * 1e-3), 1),
                           "scan_speedup": round(ms_seq / ms_scan, 3)}), flush=True)
@@ -501,9 +502,14 @@ def main():
     roof = roofline("marginals", ms_marg * 1e-3)
     dom = "k_small_log" if fused else "ts_chain_marginals"
     roof["traffic"] = measured_traffic(dom, w.name)
-    roof["kernel"] = dom if fused else (
-        "ts_chain_marginals (the call's kernel sequence: k_leaf_max, k_up_log per level, "
-        "k_root_log, k_down_log per level, k_form_*)")
+    if fused:
+        roof["kernel"] = dom
+    elif C <= 64:
+        roof["kernel"] = ("ts_chain_marginals (the call's kernel sequence: k_chunk_up, "
+                          "k_chunk_scan, k_chunk_form)")
+    else:
+        roof["kernel"] = ("ts_chain_marginals (the call's kernel sequence: k_leaf_max, "
+                          "k_up_log per level, k_root_log, k_down_log per level, k_form_*)")
     roof["kernel_ms"] = round(ms_marg, 5)
     roof_v = roofline("viterbi", ms_vit * 1e-3)
 
@@ -526,7 +532,9 @@ def main():
                             "viterbi": "ts_chain_viterbi (path and score)",
                             "both": "ts_chain_marginals_viterbi (log Z, marginals, Viterbi)"}[
                                 args.step] + (", replayed as a HIP graph" if args.graph else ""),
-                   "path": "fused single launch per call" if fused else "multi-launch tree"},
+                   "path": ("fused single launch per call" if fused else
+                            "chunks: three launches per call" if C <= 64 else
+                            "multi-launch tree")},
         "breakdown": {"marginals_ms": round(ms_marg, 5), "viterbi_ms": round(ms_vit, 5),
                       "marginals_viterbi_ms": round(ms_both, 5),
                       "marginals_tokens_per_s": round(tokens / (ms_marg * 1e-3), 1),
