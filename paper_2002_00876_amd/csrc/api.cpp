@@ -154,7 +154,7 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, boo
         }
         for (int l = 1; l <= D; ++l) {
             const size_t n = (size_t)B * (size_t)(Np >> l);
-            const int tm = up_tile(C, (int64_t)n);
+            const int tm = up_tile(C, (int64_t)n, masks);
             p->ntile[l] = (int)((C + tm - 1) / tm);
             p->core[l] = bump.take<float>(n * C * C);
             p->ro[l] = bump.take<double>(n * C);

@@ -53,6 +53,9 @@ __device__ __forceinline__ float4 buffer_load4(__amdgpu_buffer_rsrc_t r, unsigne
     const v4i x = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
     return make_float4(__int_as_float(x.x), __int_as_float(x.y), __int_as_float(x.z), __int_as_float(x.w));
 }
+__device__ __forceinline__ float buffer_load1(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff) {
+    return __int_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
 __device__ __forceinline__ float flog(float x) { return __builtin_amdgcn_logf(x) * 0.6931471805599453f; }
 
 // Full-wave reductions with DPP inside each row of 16 lanes and readlane across the four

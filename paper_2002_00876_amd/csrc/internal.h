@@ -75,10 +75,18 @@ constexpr int kChunkLog = 4;   // chunks of at most 16 edges
 bool chunk_path(int64_t C, bool masks);
 
 // Output tile edge of a level of the log-semiring up-sweep with `nodes` nodes (all
-// sequences) of C labels: 64 for C <= 64; 128 above, unless the level has too few 128-wide
+// sequences) of C labels.  32 (the latency-bound kernel, no finiteness masks) while the
+// level has at most kSmallTiles such tiles -- about 4 per compute unit: there each
+// workgroup's chain of memory round trips and barriers, not the chip's throughput, sets
+// the time; otherwise 64 for C <= 64, and 128 above unless the level has too few 128-wide
 // tiles to give every compute unit two of them: then 64 (four times the workgroups, each
 // with a quarter of the work and of the latency).
-inline int up_tile(int64_t C, int64_t nodes) {
+constexpr int64_t kSmallTiles = 1024;
+inline int up_tile(int64_t C, int64_t nodes, bool masks) {
+    if (!masks) {
+        const int64_t t = (C + 31) / 32;
+        if (nodes * t * t <= kSmallTiles) return 32;
+    }
     if (C <= 64) return 64;
     const int64_t t = (C + 127) / 128;
     return nodes * t * t < 512 ? 64 : 128;

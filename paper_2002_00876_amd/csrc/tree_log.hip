@@ -7,13 +7,16 @@
 //
 // Node representation (levels >= 1): P[a][c] = ro[a] + co[c] + core[a][c], ro/co in
 // float64, core in float32.  The product P = L (x) R is evaluated as an exp-shifted
-// dense GEMM on the fp32 matrix cores:
+// dense GEMM on the matrix cores (fp32 MFMA; for 128-wide full tiles, bf16 MFMA over a
+// three-part bf16 split of each float32 operand, which keeps float32 precision):
 //   A'[a][b] = core_L[a][b] + (co_L[b] - max co_L),   B'[b][c] = core_R[b][c] + (ro_R[b] - max ro_R)
 //   rA[a] = max_b A'[a][b],  cB[c] = max_b B'[b][c]
-//   S[a][c] = sum_b exp(A'[a][b] - rA[a]) * exp(B'[b][c] - cB[c])          (MFMA, fp32)
+//   S[a][c] = sum_b exp(A'[a][b] - rA[a]) * exp(B'[b][c] - cB[c])          (MFMA)
 //   core_P = log S,  ro_P[a] = ro_L[a] + max co_L + rA[a],  co_P[c] = co_R[c] + max ro_R + cB[c]
 // Every exponent is <= 0, so nothing overflows; S < 2^-80 (all terms underflowing) is
 // recomputed exactly by a direct max-shifted log-sum-exp over b.
+#include <type_traits>
+
 #include "device.h"
 #include "internal.h"
 
@@ -23,6 +26,7 @@ namespace {
 
 constexpr int kUpThreads = 256;  // 4 waves; each owns a (TM/2) x (TM/2) quarter of the tile
 constexpr int kSlice = 32;       // contraction indices staged per step
+constexpr bool kUpBf16 = true;   // 128-wide full tiles: products from bf16 parts (see k_up_log_full)
 constexpr float kUnderflow = 0x1p-80f;
 
 typedef float f16v __attribute__((ext_vector_type(16)));
@@ -141,6 +145,78 @@ __global__ __launch_bounds__(256) void k_leaf_max(LeafMaxArgs a) {
             }
         }
     }
+}
+
+// The same maxima for C <= 128 without finiteness masks, one leaf per workgroup with every
+// load in flight at once: the leaf goes to LDS (row stride C + 1, conflict-free for rows and
+// columns alike), then thread t < C reduces row t and thread 128 + t column t.  (Looping
+// over a leaf's rows or columns with a few loads in flight leaves a small launch -- a few
+// sequences of short chains -- bound by memory latency, not bandwidth.)
+constexpr int kLeafLdsMaxLabels = 128;
+constexpr int kLeafLdsThreads = 256;
+
+template <bool kVec>
+__global__ __launch_bounds__(kLeafLdsThreads) void k_leaf_max_lds(LeafMaxArgs a) {
+    extern __shared__ float T[];   // [C][C + 1]
+    const int64_t E = a.N - 1;
+    const int64_t b = blockIdx.x / E, t = blockIdx.x % E;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    if (t >= Eb) return;
+    const bool left = (t & 1) == 0, right = (t & 1) == 1 || t + 1 == Eb;
+    const int C = (int)a.C, CC = C * C, LD = C + 1, tid = threadIdx.x;
+    const float* leaf = a.pot + (size_t)(b * E + t) * CC;
+    if constexpr (kVec) {
+        // C % 4 == 0: a float4 never straddles two rows
+        constexpr int kQ = kLeafLdsMaxLabels * kLeafLdsMaxLabels / 4 / kLeafLdsThreads;
+        const int C4 = CC / 4;
+        float4 v[kQ];
+#pragma unroll
+        for (int q = 0; q < kQ; ++q) {
+            const int i4 = tid + q * kLeafLdsThreads;
+            if (i4 < C4) v[q] = reinterpret_cast<const float4*>(leaf)[i4];
+        }
+#pragma unroll
+        for (int q = 0; q < kQ; ++q) {
+            const int i4 = tid + q * kLeafLdsThreads;
+            if (i4 < C4) {
+                const int r = (4 * i4) / C, c = 4 * i4 - r * C;
+                float* d = T + r * LD + c;
+                d[0] = v[q].x;
+                d[1] = v[q].y;
+                d[2] = v[q].z;
+                d[3] = v[q].w;
+            }
+        }
+    } else {
+        constexpr int kQ = kLeafLdsMaxLabels * kLeafLdsMaxLabels / kLeafLdsThreads;
+        float v[kQ];
+#pragma unroll
+        for (int q = 0; q < kQ; ++q) {
+            const int i = tid + q * kLeafLdsThreads;
+            if (i < CC) v[q] = leaf[i];
+        }
+#pragma unroll
+        for (int q = 0; q < kQ; ++q) {
+            const int i = tid + q * kLeafLdsThreads;
+            if (i < CC) {
+                const int r = i / C;
+                T[r * LD + i - r * C] = v[q];
+            }
+        }
+    }
+    __syncthreads();
+    // four running maxima per line: a short dependency chain
+    const bool isrow = tid < kLeafLdsMaxLabels;
+    const int line = isrow ? tid : tid - kLeafLdsMaxLabels;
+    if (line >= C || !(isrow ? left : right)) return;
+    const int base = isrow ? line * LD : line, stride = isrow ? 1 : LD;
+    float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    int e = 0;
+    for (; e + 4 <= C; e += 4)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) m[u] = fmaxf(m[u], T[base + (e + u) * stride]);
+    for (; e < C; ++e) m[0] = fmaxf(m[0], T[base + e * stride]);
+    (isrow ? a.lrmax : a.lcmax)[(size_t)(b * E + t) * C + line] = fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3]));
 }
 
 // One tree level of the log-semiring up-sweep, P = L (x) R for every present node.
@@ -567,6 +643,261 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
     }
 }
 
+// The same product for levels with few output tiles, where latency, not throughput, bounds
+// the launch (the upper levels, and every level of a short batch): 32 x 32 output tiles, the
+// contraction split over the four waves (wave w takes slices w, w + 4, ... of 32 indices),
+// each operand exponentiated in registers straight from memory (lane l holds row / column
+// l % 32 at 16 consecutive contraction indices, the same indices for A and B, so the MFMA
+// sums over all of them without LDS staging), and the four partial tiles summed through
+// LDS.  Every global read goes out before the sequence length is known (no address depends
+// on it: an absent child is read from an in-bounds node and never used), so the workgroup
+// waits for memory once before its products.  Same outputs as k_up_log (core, ro, co, the
+// partial maxima per 32-wide tile); no finiteness masks.
+constexpr int kSmTM = 32;
+constexpr int kSmSlicesPerWave = (kMaxLabels / kSlice + 3) / 4;
+
+template <bool VEC>
+__global__ __launch_bounds__(kUpThreads) void k_up_log_small(UpLogArgs a) {
+    constexpr int TM = kSmTM, LDP = TM + 1, NQ = kSmSlicesPerWave;
+    static_assert(kUpThreads == 4 * kWave && TM == 32, "four waves, 32 x 32 tiles");
+    __shared__ float part[4][TM * LDP];   // the waves' partial tiles; part[0] then holds log S
+    __shared__ float coh[kMaxLabels], roh[kMaxLabels];
+    __shared__ float sa[TM], sb[TM], rof[TM], cof[TM];
+    __shared__ double red[2 * (kUpThreads / kWave)];
+    const int ntiles = a.ntile * a.ntile;
+    const int64_t lid = xcd_node_swizzle(blockIdx.x, ntiles);
+    if (lid >= a.nlogical) return;
+    const int tile = (int)(lid % ntiles);
+    const int64_t node = lid / ntiles;
+    const int64_t b = node / a.nodes, k = node % a.nodes;
+    const int C = (int)a.C, nt = a.ntile, cnt = a.cntile;
+    const int tm = tile / nt, tn = tile % nt;
+    const int a0 = tm * TM, c0 = tn * TM;
+    const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
+    const int r = lane & 31, h = lane >> 5;
+
+    // children, clamped into the sequence's node range (the node or its right child may be
+    // absent; that is known only once the length has arrived)
+    const int64_t cl = b * a.cnodes + min(2 * k, a.cnodes - 1);
+    const int64_t cr = b * a.cnodes + min(2 * k + 1, a.cnodes - 1);
+    const float* Lc = a.ccore + (size_t)cl * C * C;
+    const float* Rc = a.ccore + (size_t)cr * C * C;
+    const double* Lro = a.cro ? a.cro + (size_t)cl * C : nullptr;
+    const double* Lco = a.cco ? a.cco + (size_t)cl * C : nullptr;
+    const double* Rro = a.cro ? a.cro + (size_t)cr * C : nullptr;
+    const double* Rco = a.cco ? a.cco + (size_t)cr * C : nullptr;
+
+    // ---- every global read at once: the wave's slices of A (row a0 + r) and B (column c0 + r),
+    // the contracted offsets, the output lines' offsets and the children's partial maxima
+    const int nslices = (C + kSlice - 1) / kSlice;
+    const int ga = min(a0 + r, C - 1), gc = min(c0 + r, C - 1);
+    float xa[NQ][16], xb[NQ][16];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+        const int kb = (w + 4 * q) * kSlice + 16 * h;   // this lane's 16 contraction indices
+        if (w + 4 * q < nslices) {
+            const float* pa = Lc + (size_t)ga * C;
+            if (VEC) {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const float4 v = *(const float4*)(pa + min(kb + 4 * u, C - 4));
+                    xa[q][4 * u + 0] = v.x;
+                    xa[q][4 * u + 1] = v.y;
+                    xa[q][4 * u + 2] = v.z;
+                    xa[q][4 * u + 3] = v.w;
+                }
+            } else {
+#pragma unroll
+                for (int u = 0; u < 16; ++u) xa[q][u] = pa[min(kb + u, C - 1)];
+            }
+#pragma unroll
+            for (int u = 0; u < 16; ++u) xb[q][u] = Rc[(size_t)min(kb + u, C - 1) * C + gc];
+        }
+    }
+    static_assert(kMaxLabels <= kUpThreads, "one offset of the contracted index per thread");
+    const double lco = (Lco && tid < C) ? Lco[tid] : -INFINITY;
+    const double rro = (Rro && tid < C) ? Rro[tid] : -INFINITY;
+    // thread t < TM: row a0 + t (of L, and of the output); TM <= t < 2 TM: column c0 + t - TM
+    const bool isrow = tid < TM, iscol = tid >= TM && tid < 2 * TM;
+    const int li = isrow ? tid : tid - TM;
+    const bool lok = (isrow && a0 + li < C) || (iscol && c0 + li < C);
+    double loff = 0.0;   // ro_L of the row, co_R of the column
+    float pm = -INFINITY;
+    if (lok) {
+        loff = isrow ? (Lro ? Lro[a0 + li] : 0.0) : (Rco ? Rco[c0 + li] : 0.0);
+        const float* pp = isrow ? a.cpmr + ((size_t)cl * C + a0 + li) * cnt
+                                : a.cpmc + ((size_t)cr * C + c0 + li) * cnt;
+#pragma unroll
+        for (int q = 0; q < kMaxLabels / kSmTM; ++q)
+            if (q < cnt) pm = fmaxf(pm, pp[q]);
+    }
+
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    const int64_t span = (int64_t)1 << a.level, half = span >> 1;
+    if (k * span >= Eb) return;   // node absent: all padding
+    const int64_t pn = b * a.nodes + k;
+    float* Pc = a.core + (size_t)pn * C * C;
+    double* Pro = a.ro + (size_t)pn * C;
+    double* Pco = a.co + (size_t)pn * C;
+    float* Pmr = a.pmr + (size_t)pn * C * nt;
+    float* Pmc = a.pmc + (size_t)pn * C * nt;
+    if (!((2 * k + 1) * half < Eb)) {
+        // the right half is padding: the node equals its left child (tile, offsets and the
+        // partial maxima, re-tiled: only the maximum over a line's partials is ever read)
+        for (int idx = tid; idx < TM * TM; idx += kUpThreads) {
+            const int rr = a0 + idx / TM, cc = c0 + idx % TM;
+            if (rr < C && cc < C) Pc[(size_t)rr * C + cc] = Lc[(size_t)rr * C + cc];
+        }
+        if (tn == 0)
+            for (int i = tid; i < TM; i += kUpThreads)
+                if (a0 + i < C) Pro[a0 + i] = Lro ? Lro[a0 + i] : 0.0;
+        if (tm == 0)
+            for (int i = tid; i < TM; i += kUpThreads)
+                if (c0 + i < C) Pco[c0 + i] = Lco ? Lco[c0 + i] : 0.0;
+        if (tm == 0 && tn == 0)
+            for (int i = tid; i < C * nt; i += kUpThreads) {
+                const int line = i / nt, pq = i % nt;
+                const float* sr = a.cpmr + ((size_t)cl * C + line) * cnt;
+                const float* sc = a.cpmc + ((size_t)cl * C + line) * cnt;
+                float mr = -INFINITY, mc = -INFINITY;
+                if (pq == 0)
+                    for (int q = 0; q < cnt; ++q) {
+                        mr = fmaxf(mr, sr[q]);
+                        mc = fmaxf(mc, sc[q]);
+                    }
+                Pmr[i] = mr;
+                Pmc[i] = mc;
+            }
+        return;
+    }
+
+    // ---- shifts: max co_L and max ro_R over the contracted index (one reduction), the tile's
+    // row shifts sa (row maxima of core_L + co_L - max co_L) and column shifts sb
+    {
+        const double lw = wave_max_d(lco), rw = wave_max_d(rro);
+        if (lane == 0) {
+            red[2 * w] = lw;
+            red[2 * w + 1] = rw;
+        }
+    }
+    __syncthreads();
+    double lmax = red[0], rmax = red[1];
+#pragma unroll
+    for (int q = 1; q < kUpThreads / kWave; ++q) {
+        lmax = fmax(lmax, red[2 * q]);
+        rmax = fmax(rmax, red[2 * q + 1]);
+    }
+    const double coLshift = Lco ? safe_shift_d(lmax) : 0.0;
+    const double roRshift = Rro ? safe_shift_d(rmax) : 0.0;
+    if (tid < C) {
+        coh[tid] = Lco ? (float)(lco - coLshift) : 0.f;
+        roh[tid] = Rro ? (float)(rro - roRshift) : 0.f;
+    }
+    if (isrow) sa[li] = safe_shift(lok ? pm - (float)coLshift : -INFINITY);
+    if (iscol) sb[li] = safe_shift(lok ? pm - (float)roRshift : -INFINITY);
+    __syncthreads();
+
+    // ---- the wave's partial product over its slices
+    f16v acc;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+    {
+        const float s_a = sa[r], s_b = sb[r];
+        const bool rok = a0 + r < C, cok = c0 + r < C;
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int kb = (w + 4 * q) * kSlice + 16 * h;
+            if (w + 4 * q < nslices) {
+#pragma unroll
+                for (int u = 0; u < 16; ++u) {
+                    const int kk = kb + u;
+                    const bool kok = kk < C;
+                    const float av = (rok && kok) ? fexp(xa[q][u] + coh[kk] - s_a) : 0.f;
+                    const float bv = (cok && kok) ? fexp(xb[q][u] + roh[kk] - s_b) : 0.f;
+                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc, 0, 0, 0);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+        const int row = (q >> 2) * 8 + h * 4 + (q & 3);
+        part[w][row * LDP + r] = acc[q];
+    }
+    __syncthreads();
+
+    // ---- S = sum of the partial tiles, core = log S (an underflowed S, every term below
+    // 2^-80, is recomputed by a direct log-sum-exp: a rare, non-unrolled path)
+    const int nr = min(TM, C - a0), nc = min(TM, C - c0);
+#pragma unroll
+    for (int q = 0; q < TM * TM / kUpThreads; ++q) {
+        const int e = tid + q * kUpThreads, row = e / TM, col = e % TM, o = row * LDP + col;
+        const float S = (part[0][o] + part[1][o]) + (part[2][o] + part[3][o]);
+        float val = flog(S);
+        if (!(S >= kUnderflow) && row < nr && col < nc) {
+            const float sr = sa[row], sc = sb[col];
+            const float* lrow = Lc + (size_t)(a0 + row) * C;
+            const int gcol = c0 + col;
+            float mx = -INFINITY;
+            for (int bb = 0; bb < C; ++bb)
+                mx = fmaxf(mx, (lrow[bb] + coh[bb] - sr) + (Rc[(size_t)bb * C + gcol] + roh[bb] - sc));
+            val = -INFINITY;
+            if (mx != -INFINITY) {
+                float sum = 0.f;
+                for (int bb = 0; bb < C; ++bb)
+                    sum += fexp((lrow[bb] + coh[bb] - sr) + (Rc[(size_t)bb * C + gcol] + roh[bb] - sc) - mx);
+                val = mx + flog(sum);
+            }
+        }
+        part[0][o] = val;
+    }
+    // the output node's offsets for the tile's rows and columns
+    if (lok) {
+        const double off = isrow ? loff + coLshift + sa[li] : loff + roRshift + sb[li];
+        (isrow ? rof : cof)[li] = (float)off;
+        if (isrow && tn == 0) Pro[a0 + li] = off;
+        if (iscol && tm == 0) Pco[c0 + li] = off;
+    } else if (isrow || iscol) {
+        (isrow ? rof : cof)[li] = 0.f;
+    }
+    __syncthreads();
+
+    // ---- partial maxima for the next level: four threads per line, eight entries each
+    {
+        const bool rowp = tid < 4 * TM;
+        const int line = (rowp ? tid : tid - 4 * TM) >> 2, seg = 8 * (tid & 3);
+        const float* T = part[0];
+        float m = -INFINITY;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int e = seg + u;
+            if (rowp ? e < nc : e < nr)
+                m = fmaxf(m, rowp ? T[line * LDP + e] + cof[e] : T[e * LDP + line] + rof[e]);
+        }
+        m = fmaxf(m, __shfl_xor(m, 1, kWave));
+        m = fmaxf(m, __shfl_xor(m, 2, kWave));
+        if ((tid & 3) == 0) {
+            if (rowp && line < nr) Pmr[(size_t)(a0 + line) * nt + tn] = m;
+            if (!rowp && line < nc) Pmc[(size_t)(c0 + line) * nt + tm] = m;
+        }
+    }
+    // ---- the tile, row by row (16-byte stores when C is a multiple of 4)
+    {
+        const int row = tid / (TM / 4), c4 = 4 * (tid % (TM / 4));
+        const float* t = part[0] + row * LDP + c4;
+        if (row < nr) {
+            float* dst = Pc + (size_t)(a0 + row) * C + c0 + c4;
+            if (VEC) {
+                if (c4 < nc) *(float4*)dst = make_float4(t[0], t[1], t[2], t[3]);
+            } else {
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if (c4 + u < nc) dst[u] = t[u];
+            }
+        }
+    }
+}
+
 // The same product for full tiles (C a multiple of TM, no finiteness masks), scheduled for
 // the matrix cores: the raw potentials of slice s + 2 are loaded during slice s (two
 // register sets, so a load has a whole slice to arrive); the exponentials of slice s + 1
@@ -586,10 +917,57 @@ struct UpFullSmem {
     static constexpr size_t kBytes = sizeof(float) * kFloats;
 };
 
+// The bf16 variant (kBf) stages each exponentiated operand x as three bf16 parts
+// x = hi + mid + lo (hi = bf16(x), mid = bf16(x - hi), lo = bf16(x - hi - mid): 24 significant
+// bits, float32's own precision, and float32's exponent range), in slices of 16 contracted
+// indices, A as [row][k] and B transposed as [column][k], and sums the six products
+//   hi.hi + hi.mid + mid.hi + hi.lo + lo.hi + mid.mid
+// with the bf16 matrix instructions (32x32x16, float32 accumulation), which run 16 times the
+// float32 MFMA rate.  The three dropped products are below 2^-24 of |x y|, so a sum matches
+// the float32 product to float32 rounding.
 template <int TM>
+struct UpBfSmem {
+    static constexpr int kK = 16;                   // contracted indices per slice
+    static constexpr int LDK = kK + 8;              // bf16 per staged line (48 bytes)
+    static constexpr int kPlane = TM * LDK;         // bf16 per part plane
+    static constexpr int kBufF = 6 * kPlane / 2;    // A and B, three parts each, in floats
+    static constexpr int LDT = TM + 1;
+    static constexpr int kTileF = TM * LDT;
+    static constexpr int kMain = (2 * kBufF > kTileF ? 2 * kBufF : kTileF);
+    static constexpr int kFloats = kMain + 4 * kMaxLabels + 4 * TM + 4 * (kUpThreads / kWave);
+    static constexpr size_t kBytes = sizeof(float) * kFloats;
+};
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// x = hi + mid + lo exactly: hi is x truncated to its leading 8 significant bits (the upper
+// half of its float encoding), mid the same of the remainder r = x - hi (exact in float, at
+// most 16 significant bits), lo = r - mid (at most 8 bits, so its upper half is exact too).
+// Two elements' upper halves are packed by one byte permute.
+__device__ __forceinline__ void split_bf16x3(const float (&x)[8], bf16x8& hi, bf16x8& mid, bf16x8& lo) {
+    typedef unsigned u4v __attribute__((ext_vector_type(4)));
+    constexpr unsigned kHi = 0xffff0000u, kSel = 0x07060302u;   // upper halves of (src1, src0)
+    u4v h, m, l;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        const unsigned x0 = __float_as_uint(x[2 * p]), x1 = __float_as_uint(x[2 * p + 1]);
+        const float r0 = x[2 * p] - __uint_as_float(x0 & kHi);
+        const float r1 = x[2 * p + 1] - __uint_as_float(x1 & kHi);
+        const unsigned q0 = __float_as_uint(r0), q1 = __float_as_uint(r1);
+        const float t0 = r0 - __uint_as_float(q0 & kHi), t1 = r1 - __uint_as_float(q1 & kHi);
+        h[p] = __builtin_amdgcn_perm(x1, x0, kSel);
+        m[p] = __builtin_amdgcn_perm(q1, q0, kSel);
+        l[p] = __builtin_amdgcn_perm(__float_as_uint(t1), __float_as_uint(t0), kSel);
+    }
+    hi = __builtin_bit_cast(bf16x8, h);
+    mid = __builtin_bit_cast(bf16x8, m);
+    lo = __builtin_bit_cast(bf16x8, l);
+}
+
+template <int TM, bool kBf>
 __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
-    using Sm = UpFullSmem<TM>;
-    constexpr int LDA = Sm::LDA, LDB = Sm::LDB, LDT = Sm::LDT;
+    using Sm = std::conditional_t<kBf, UpBfSmem<TM>, UpFullSmem<TM>>;
+    constexpr int LDT = Sm::LDT;
     constexpr int BR = TM / 64;                 // 32 x 32 blocks per wave per dimension
     constexpr int QW = TM / 2;                  // a wave's quarter edge
     constexpr float kL2E = 1.4426950408889634f;
@@ -663,128 +1041,52 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
     float* rof = cof + TM;               // [TM] ro_P of the tile's rows (float)
     double* red = reinterpret_cast<double*>(rof + TM);
 
-    // ---- per-thread staging assignment (fixed over the slices):
-    //   A'' (TM x 32): rows ar + 32 it (it < NA), contracted indices ak .. ak + 3;
-    //   B'' (32 x TM): contracted rows bk .. bk + NB - 1, columns bc .. bc + 3
-    constexpr int GA = kSlice / 4, NA = TM * GA / kUpThreads;
-    constexpr int GB = TM / 4, NB = kSlice * GB / kUpThreads;
-    static_assert(NB == 4 || NB == 2, "contracted rows of a thread: one or half a float4");
-    const int ar = tid / GA, ak = 4 * (tid % GA);
-    const int bk = NB * (tid / GB), bc = 4 * (tid % GB);
-    // loads: raw buffer loads over each child matrix (C * C floats), a fixed 32-bit byte
-    // offset per thread and register and the slice's offset in a scalar register, so that
-    // no address arithmetic is repeated per slice
-    const __amdgpu_buffer_rsrc_t rsL = make_rsrc(Lc, C * C);
-    const __amdgpu_buffer_rsrc_t rsR = make_rsrc(Rc, C * C);
-    unsigned offa[NA], offb[NB];
+    // the offsets of the contracted index shifted to max 0 (coh, roh and both scaled by log2 e)
+    // and the tile's row and column shifts; every global read of it goes out at once, after
+    // the first slices' loads
+    double coLshift = 0.0, roRshift = 0.0;
+    auto shifts = [&]() {
+        static_assert(kMaxLabels <= kUpThreads, "one offset of the contracted index per thread");
+        const double lco = (Lco && tid < C) ? Lco[tid] : -INFINITY;
+        const double rro = (Rro && tid < C) ? Rro[tid] : -INFINITY;
+        float pa = -INFINITY, pb = -INFINITY;
+        if (tid < TM) {
+            const float* p = a.cpmr + ((size_t)cl * C + a0 + tid) * cnt;
+            for (int q = 0; q < cnt; ++q) pa = fmaxf(pa, p[q]);
+            const float* r = a.cpmc + ((size_t)cr * C + c0 + tid) * cnt;
+            for (int q = 0; q < cnt; ++q) pb = fmaxf(pb, r[q]);
+        }
+        {
+            const double lw = wave_max_d(lco), rw = wave_max_d(rro);
+            const int w = tid / kWave;
+            if ((tid & (kWave - 1)) == 0) {
+                red[2 * w] = lw;
+                red[2 * w + 1] = rw;
+            }
+        }
+        __syncthreads();
+        double lmax = red[0], rmax = red[1];
 #pragma unroll
-    for (int it = 0; it < NA; ++it) offa[it] = 4u * (unsigned)((a0 + ar + 32 * it) * C + ak);
-#pragma unroll
-    for (int it = 0; it < NB; ++it) offb[it] = 4u * (unsigned)((bk + it) * C + c0 + bc);
-    float4 ra[2][NA], rb[2][NB];
-    auto gload = [&](float4 (&xa)[NA], float4 (&xb)[NB], int ks) {
-#pragma unroll
-        for (int it = 0; it < NA; ++it) xa[it] = buffer_load4(rsL, offa[it], 4 * ks);
-#pragma unroll
-        for (int it = 0; it < NB; ++it) xb[it] = buffer_load4(rsR, offb[it], 4 * ks * C);
+        for (int w = 1; w < kUpThreads / kWave; ++w) {
+            lmax = fmax(lmax, red[2 * w]);
+            rmax = fmax(rmax, red[2 * w + 1]);
+        }
+        coLshift = Lco ? safe_shift_d(lmax) : 0.0;
+        roRshift = Rro ? safe_shift_d(rmax) : 0.0;
+        if (tid < C) {
+            const float ch = Lco ? (float)(lco - coLshift) : 0.f;
+            const float rh = Rro ? (float)(rro - roRshift) : 0.f;
+            coh[tid] = ch;
+            roh[tid] = rh;
+            cohs[tid] = ch * kL2E;
+            rohs[tid] = rh * kL2E;
+        }
+        if (tid < TM) {
+            sa[tid] = safe_shift(pa - (float)coLshift);
+            sb[tid] = safe_shift(pb - (float)roRshift);
+        }
+        __syncthreads();
     };
-    float sas[NA], sbs[4];
-    // the offsets of the staged contracted indices (A: ak..ak+3, B: bk..bk+NB-1), scaled by
-    // log2 e, read from LDS once per slice
-    auto offsets = [&](float (&oa)[4], float (&ob)[4], int ks) {
-        const float4 x = *(const float4*)(cohs + ks + ak);
-        oa[0] = x.x; oa[1] = x.y; oa[2] = x.z; oa[3] = x.w;
-        if constexpr (NB == 4) {
-            const float4 y = *(const float4*)(rohs + ks + bk);
-            ob[0] = y.x; ob[1] = y.y; ob[2] = y.z; ob[3] = y.w;
-        } else {
-            const float2 y = *(const float2*)(rohs + ks + bk);
-            ob[0] = y.x; ob[1] = y.y; ob[2] = ob[3] = 0.f;
-        }
-    };
-    // exponentials of staged part `part` of `nparts` (A groups, then B groups) into buffer buf
-    auto stage = [&](const float4 (&xa)[NA], const float4 (&xb)[NB], const float (&oa)[4],
-                     const float (&ob)[4], int buf, int part, int nparts) {
-        float* As = smem + buf * Sm::kBuf;
-        float* Bs = As + TM * LDA;
-#pragma unroll
-        for (int it = NA * part / nparts; it < NA * (part + 1) / nparts; ++it) {
-            float4 x;
-            x.x = __builtin_amdgcn_exp2f(fmaf(xa[it].x, kL2E, oa[0]) - sas[it]);
-            x.y = __builtin_amdgcn_exp2f(fmaf(xa[it].y, kL2E, oa[1]) - sas[it]);
-            x.z = __builtin_amdgcn_exp2f(fmaf(xa[it].z, kL2E, oa[2]) - sas[it]);
-            x.w = __builtin_amdgcn_exp2f(fmaf(xa[it].w, kL2E, oa[3]) - sas[it]);
-            *(float4*)(As + (ar + 32 * it) * LDA + ak) = x;
-        }
-#pragma unroll
-        for (int it = NB * part / nparts; it < NB * (part + 1) / nparts; ++it) {
-            float4 x;
-            x.x = __builtin_amdgcn_exp2f(fmaf(xb[it].x, kL2E, ob[it]) - sbs[0]);
-            x.y = __builtin_amdgcn_exp2f(fmaf(xb[it].y, kL2E, ob[it]) - sbs[1]);
-            x.z = __builtin_amdgcn_exp2f(fmaf(xb[it].z, kL2E, ob[it]) - sbs[2]);
-            x.w = __builtin_amdgcn_exp2f(fmaf(xb[it].w, kL2E, ob[it]) - sbs[3]);
-            *(float4*)(Bs + (bk + it) * LDB + bc) = x;
-        }
-    };
-
-    // ---- the first two slices' loads and every global read of the set-up go out at once
-    const int nslices = C / kSlice;   // even: C is a multiple of 64
-    gload(ra[0], rb[0], 0);
-    gload(ra[1], rb[1], kSlice);
-    static_assert(kMaxLabels <= kUpThreads, "one offset of the contracted index per thread");
-    const double lco = (Lco && tid < C) ? Lco[tid] : -INFINITY;
-    const double rro = (Rro && tid < C) ? Rro[tid] : -INFINITY;
-    float pa = -INFINITY, pb = -INFINITY;
-    if (tid < TM) {
-        const float* p = a.cpmr + ((size_t)cl * C + a0 + tid) * cnt;
-        for (int q = 0; q < cnt; ++q) pa = fmaxf(pa, p[q]);
-        const float* r = a.cpmc + ((size_t)cr * C + c0 + tid) * cnt;
-        for (int q = 0; q < cnt; ++q) pb = fmaxf(pb, r[q]);
-    }
-    {
-        const double lw = wave_max_d(lco), rw = wave_max_d(rro);
-        const int w = tid / kWave;
-        if ((tid & (kWave - 1)) == 0) {
-            red[2 * w] = lw;
-            red[2 * w + 1] = rw;
-        }
-    }
-    __syncthreads();
-    double lmax = red[0], rmax = red[1];
-#pragma unroll
-    for (int w = 1; w < kUpThreads / kWave; ++w) {
-        lmax = fmax(lmax, red[2 * w]);
-        rmax = fmax(rmax, red[2 * w + 1]);
-    }
-    const double coLshift = Lco ? safe_shift_d(lmax) : 0.0;
-    const double roRshift = Rro ? safe_shift_d(rmax) : 0.0;
-    if (tid < C) {
-        const float ch = Lco ? (float)(lco - coLshift) : 0.f;
-        const float rh = Rro ? (float)(rro - roRshift) : 0.f;
-        coh[tid] = ch;
-        roh[tid] = rh;
-        cohs[tid] = ch * kL2E;
-        rohs[tid] = rh * kL2E;
-    }
-    if (tid < TM) {
-        sa[tid] = safe_shift(pa - (float)coLshift);
-        sb[tid] = safe_shift(pb - (float)roRshift);
-    }
-    __syncthreads();
-#pragma unroll
-    for (int it = 0; it < NA; ++it) sas[it] = sa[ar + 32 * it] * kL2E;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) sbs[q] = sb[bc + q] * kL2E;
-    {
-        float oa[4], ob[4];
-        offsets(oa, ob, 0);
-        stage(ra[0], rb[0], oa, ob, 0, 0, 1);
-    }
-    __syncthreads();
-
-    // ---- products: wave (wm, wn) owns rows wm*QW.., columns wn*QW.. as BR x BR blocks.
-    // Within each 8-wide k group lanes 0-31 contribute k..k+3 and lanes 32-63 k+4..k+7 (one
-    // 16-byte LDS read of A per block row, four reads of B per block column).
     const int w = tid / kWave, lane = tid % kWave;
     const int wm = w >> 1, wn = w & 1;
     f16v acc[BR][BR];
@@ -794,62 +1096,290 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
         for (int j = 0; j < BR; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-    const int aoff = (wm * QW + (lane & 31)) * LDA + 4 * (lane >> 5);
-    const int boff = TM * LDA + (4 * (lane >> 5)) * LDB + wn * QW + (lane & 31);
-    float4 av[2][BR];
-    float bv[2][BR][4];
-    auto lds_ops = [&](float4 (&xa)[BR], float (&xb)[BR][4], int buf, int kk) {
-        const float* base = smem + buf * Sm::kBuf;
+    if constexpr (!kBf) {
+        constexpr int LDA = Sm::LDA, LDB = Sm::LDB;
+        // ---- per-thread staging assignment (fixed over the slices):
+        //   A'' (TM x 32): rows ar + 32 it (it < NA), contracted indices ak .. ak + 3;
+        //   B'' (32 x TM): contracted rows bk .. bk + NB - 1, columns bc .. bc + 3
+        constexpr int GA = kSlice / 4, NA = TM * GA / kUpThreads;
+        constexpr int GB = TM / 4, NB = kSlice * GB / kUpThreads;
+        static_assert(NB == 4 || NB == 2, "contracted rows of a thread: one or half a float4");
+        const int ar = tid / GA, ak = 4 * (tid % GA);
+        const int bk = NB * (tid / GB), bc = 4 * (tid % GB);
+        // loads: raw buffer loads over each child matrix (C * C floats), a fixed 32-bit byte
+        // offset per thread and register and the slice's offset in a scalar register, so that
+        // no address arithmetic is repeated per slice
+        const __amdgpu_buffer_rsrc_t rsL = make_rsrc(Lc, C * C);
+        const __amdgpu_buffer_rsrc_t rsR = make_rsrc(Rc, C * C);
+        unsigned offa[NA], offb[NB];
 #pragma unroll
-        for (int i = 0; i < BR; ++i) xa[i] = *(const float4*)(base + aoff + i * 32 * LDA + kk);
+        for (int it = 0; it < NA; ++it) offa[it] = 4u * (unsigned)((a0 + ar + 32 * it) * C + ak);
 #pragma unroll
-        for (int j = 0; j < BR; ++j)
+        for (int it = 0; it < NB; ++it) offb[it] = 4u * (unsigned)((bk + it) * C + c0 + bc);
+        float4 ra[2][NA], rb[2][NB];
+        auto gload = [&](float4 (&xa)[NA], float4 (&xb)[NB], int ks) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) xb[j][q] = base[boff + (kk + q) * LDB + j * 32];
-    };
-    auto mfma_group = [&](const float4 (&xa)[BR], const float (&xb)[BR][4]) {
+            for (int it = 0; it < NA; ++it) xa[it] = buffer_load4(rsL, offa[it], 4 * ks);
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-#pragma unroll
-            for (int i = 0; i < BR; ++i)
-#pragma unroll
-                for (int j = 0; j < BR; ++j) {
-                    const float ax = q == 0 ? xa[i].x : q == 1 ? xa[i].y : q == 2 ? xa[i].z : xa[i].w;
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ax, xb[j][q], acc[i][j], 0, 0, 0);
-                }
-    };
-    // one slice: products of buffer `cur` while slice s + 1 (raw set xa1/xb1) is staged into
-    // the other buffer and slice s + 2 is loaded into the set just consumed (xa0/xb0).  After
-    // the last slice the staging works on stale registers into a buffer nobody reads (no
-    // branch, so the products and the staging form one block the scheduler can interleave).
-    auto slice = [&](int s, int cur, float4 (&xa0)[NA], float4 (&xb0)[NB], float4 (&xa1)[NA],
-                     float4 (&xb1)[NB]) {
-        if (s + 2 < nslices) gload(xa0, xb0, (s + 2) * kSlice);
-        float oa[4], ob[4];
-        offsets(oa, ob, min(s + 1, nslices - 1) * kSlice);
-        lds_ops(av[0], bv[0], cur, 0);
-#pragma unroll
-        for (int g = 0; g < kSlice / 8; ++g) {
-            if (g + 1 < kSlice / 8) lds_ops(av[(g + 1) & 1], bv[(g + 1) & 1], cur, 8 * (g + 1));
-            stage(xa1, xb1, oa, ob, cur ^ 1, g, kSlice / 8);
-            mfma_group(av[g & 1], bv[g & 1]);
-            // one product, then two VALU instructions (the staging), and the operand reads
-            // of the next group and the staging's stores spread over the products
-#pragma unroll
-            for (int i = 0; i < 4 * BR * BR; ++i) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
-                if (i % 2 == 0) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-                if (i % 8 == 7) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+            for (int it = 0; it < NB; ++it) xb[it] = buffer_load4(rsR, offb[it], 4 * ks * C);
+        };
+        float sas[NA], sbs[4];
+        // the offsets of the staged contracted indices (A: ak..ak+3, B: bk..bk+NB-1), scaled by
+        // log2 e, read from LDS once per slice
+        auto offsets = [&](float (&oa)[4], float (&ob)[4], int ks) {
+            const float4 x = *(const float4*)(cohs + ks + ak);
+            oa[0] = x.x; oa[1] = x.y; oa[2] = x.z; oa[3] = x.w;
+            if constexpr (NB == 4) {
+                const float4 y = *(const float4*)(rohs + ks + bk);
+                ob[0] = y.x; ob[1] = y.y; ob[2] = y.z; ob[3] = y.w;
+            } else {
+                const float2 y = *(const float2*)(rohs + ks + bk);
+                ob[0] = y.x; ob[1] = y.y; ob[2] = ob[3] = 0.f;
             }
+        };
+        // exponentials of staged part `part` of `nparts` (A groups, then B groups) into buffer buf
+        auto stage = [&](const float4 (&xa)[NA], const float4 (&xb)[NB], const float (&oa)[4],
+                         const float (&ob)[4], int buf, int part, int nparts) {
+            float* As = smem + buf * Sm::kBuf;
+            float* Bs = As + TM * LDA;
+#pragma unroll
+            for (int it = NA * part / nparts; it < NA * (part + 1) / nparts; ++it) {
+                float4 x;
+                x.x = __builtin_amdgcn_exp2f(fmaf(xa[it].x, kL2E, oa[0]) - sas[it]);
+                x.y = __builtin_amdgcn_exp2f(fmaf(xa[it].y, kL2E, oa[1]) - sas[it]);
+                x.z = __builtin_amdgcn_exp2f(fmaf(xa[it].z, kL2E, oa[2]) - sas[it]);
+                x.w = __builtin_amdgcn_exp2f(fmaf(xa[it].w, kL2E, oa[3]) - sas[it]);
+                *(float4*)(As + (ar + 32 * it) * LDA + ak) = x;
+            }
+#pragma unroll
+            for (int it = NB * part / nparts; it < NB * (part + 1) / nparts; ++it) {
+                float4 x;
+                x.x = __builtin_amdgcn_exp2f(fmaf(xb[it].x, kL2E, ob[it]) - sbs[0]);
+                x.y = __builtin_amdgcn_exp2f(fmaf(xb[it].y, kL2E, ob[it]) - sbs[1]);
+                x.z = __builtin_amdgcn_exp2f(fmaf(xb[it].z, kL2E, ob[it]) - sbs[2]);
+                x.w = __builtin_amdgcn_exp2f(fmaf(xb[it].w, kL2E, ob[it]) - sbs[3]);
+                *(float4*)(Bs + (bk + it) * LDB + bc) = x;
+            }
+        };
+
+        // ---- the first two slices' loads and every global read of the set-up go out at once
+        const int nslices = C / kSlice;   // even: C is a multiple of 64
+        gload(ra[0], rb[0], 0);
+        gload(ra[1], rb[1], kSlice);
+        shifts();
+#pragma unroll
+        for (int it = 0; it < NA; ++it) sas[it] = sa[ar + 32 * it] * kL2E;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) sbs[q] = sb[bc + q] * kL2E;
+        {
+            float oa[4], ob[4];
+            offsets(oa, ob, 0);
+            stage(ra[0], rb[0], oa, ob, 0, 0, 1);
         }
         __syncthreads();
-    };
-    for (int s = 0; s < nslices; s += 2) {
-        slice(s, 0, ra[0], rb[0], ra[1], rb[1]);
-        slice(s + 1, 1, ra[1], rb[1], ra[0], rb[0]);
-    }
 
+        // ---- products: wave (wm, wn) owns rows wm*QW.., columns wn*QW.. as BR x BR blocks.
+        // Within each 8-wide k group lanes 0-31 contribute k..k+3 and lanes 32-63 k+4..k+7 (one
+        // 16-byte LDS read of A per block row, four reads of B per block column).
+        const int aoff = (wm * QW + (lane & 31)) * LDA + 4 * (lane >> 5);
+        const int boff = TM * LDA + (4 * (lane >> 5)) * LDB + wn * QW + (lane & 31);
+        float4 av[2][BR];
+        float bv[2][BR][4];
+        auto lds_ops = [&](float4 (&xa)[BR], float (&xb)[BR][4], int buf, int kk) {
+            const float* base = smem + buf * Sm::kBuf;
+#pragma unroll
+            for (int i = 0; i < BR; ++i) xa[i] = *(const float4*)(base + aoff + i * 32 * LDA + kk);
+#pragma unroll
+            for (int j = 0; j < BR; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) xb[j][q] = base[boff + (kk + q) * LDB + j * 32];
+        };
+        auto mfma_group = [&](const float4 (&xa)[BR], const float (&xb)[BR][4]) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int i = 0; i < BR; ++i)
+#pragma unroll
+                    for (int j = 0; j < BR; ++j) {
+                        const float ax = q == 0 ? xa[i].x : q == 1 ? xa[i].y : q == 2 ? xa[i].z : xa[i].w;
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ax, xb[j][q], acc[i][j], 0, 0, 0);
+                    }
+        };
+        // one slice: products of buffer `cur` while slice s + 1 (raw set xa1/xb1) is staged into
+        // the other buffer and slice s + 2 is loaded into the set just consumed (xa0/xb0).  After
+        // the last slice the staging works on stale registers into a buffer nobody reads (no
+        // branch, so the products and the staging form one block the scheduler can interleave).
+        auto slice = [&](int s, int cur, float4 (&xa0)[NA], float4 (&xb0)[NB], float4 (&xa1)[NA],
+                         float4 (&xb1)[NB]) {
+            if (s + 2 < nslices) gload(xa0, xb0, (s + 2) * kSlice);
+            float oa[4], ob[4];
+            offsets(oa, ob, min(s + 1, nslices - 1) * kSlice);
+            lds_ops(av[0], bv[0], cur, 0);
+#pragma unroll
+            for (int g = 0; g < kSlice / 8; ++g) {
+                if (g + 1 < kSlice / 8) lds_ops(av[(g + 1) & 1], bv[(g + 1) & 1], cur, 8 * (g + 1));
+                stage(xa1, xb1, oa, ob, cur ^ 1, g, kSlice / 8);
+                mfma_group(av[g & 1], bv[g & 1]);
+                // one product, then two VALU instructions (the staging), and the operand reads
+                // of the next group and the staging's stores spread over the products
+#pragma unroll
+                for (int i = 0; i < 4 * BR * BR; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+                    if (i % 2 == 0) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                    if (i % 8 == 7) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+                }
+            }
+            __syncthreads();
+        };
+        for (int s = 0; s < nslices; s += 2) {
+            slice(s, 0, ra[0], rb[0], ra[1], rb[1]);
+            slice(s + 1, 1, ra[1], rb[1], ra[0], rb[0]);
+        }
+    } else {
+        // ---- bf16 parts.  Staging: A row ar = tid / 2, contracted indices ka .. ka + 7 (two
+        // 16-byte loads); B column bcol = tid % TM, contracted indices kb .. kb + 7 (eight loads,
+        // each a row segment shared by the wave: coalesced)
+        static_assert(TM == 128, "one A line segment and one B column segment per thread");
+        constexpr int kK = Sm::kK, LDK = Sm::LDK, PL = Sm::kPlane;
+        constexpr int kBufH = 2 * Sm::kBufF;   // bf16 per slice buffer
+        __bf16* hsm = reinterpret_cast<__bf16*>(smem);
+        const int ar = tid >> 1, ka = 8 * (tid & 1);
+        const int bcol = tid & (TM - 1);
+        const int kb = __builtin_amdgcn_readfirstlane(8 * (tid / TM));   // wave-uniform
+        const __amdgpu_buffer_rsrc_t rsL = make_rsrc(Lc, C * C);
+        const __amdgpu_buffer_rsrc_t rsR = make_rsrc(Rc, C * C);
+        const unsigned offa = 4u * (unsigned)((a0 + ar) * C + ka);
+        const unsigned offb = 4u * (unsigned)(c0 + bcol);
+        float4 ra[2][2];
+        float rb[2][8];
+        auto gload = [&](float4 (&xa)[2], float (&xb)[8], int ks) {
+            xa[0] = buffer_load4(rsL, offa, 4 * ks);
+            xa[1] = buffer_load4(rsL, offa + 16u, 4 * ks);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) xb[j] = buffer_load1(rsR, offb, 4 * (ks + kb + j) * C);
+        };
+        float sas = 0.f, sbs = 0.f;
+        // staging of one slice in phases (so that the phases can go between the products of the
+        // slice before): the offset vectors of its contracted indices, the exponentials of A's
+        // (or B's) eight entries, then their parts into buffer buf
+        struct StageRegs {
+            float4 oa0, oa1, ob0, ob1;   // offsets (log2 units) of ka.., kb..
+            float x[8];                  // exponentials of the phase's side
+        };
+        auto stage_offsets = [&](StageRegs& g, int ks) {
+            g.oa0 = *(const float4*)(cohs + ks + ka);
+            g.oa1 = *(const float4*)(cohs + ks + ka + 4);
+            g.ob0 = *(const float4*)(rohs + ks + kb);
+            g.ob1 = *(const float4*)(rohs + ks + kb + 4);
+        };
+        auto stage_exp_a = [&](StageRegs& g, const float4 (&xa)[2]) {
+            g.x[0] = __builtin_amdgcn_exp2f(fmaf(xa[0].x, kL2E, g.oa0.x) - sas);
+            g.x[1] = __builtin_amdgcn_exp2f(fmaf(xa[0].y, kL2E, g.oa0.y) - sas);
+            g.x[2] = __builtin_amdgcn_exp2f(fmaf(xa[0].z, kL2E, g.oa0.z) - sas);
+            g.x[3] = __builtin_amdgcn_exp2f(fmaf(xa[0].w, kL2E, g.oa0.w) - sas);
+            g.x[4] = __builtin_amdgcn_exp2f(fmaf(xa[1].x, kL2E, g.oa1.x) - sas);
+            g.x[5] = __builtin_amdgcn_exp2f(fmaf(xa[1].y, kL2E, g.oa1.y) - sas);
+            g.x[6] = __builtin_amdgcn_exp2f(fmaf(xa[1].z, kL2E, g.oa1.z) - sas);
+            g.x[7] = __builtin_amdgcn_exp2f(fmaf(xa[1].w, kL2E, g.oa1.w) - sas);
+        };
+        auto stage_exp_b = [&](StageRegs& g, const float (&xb)[8]) {
+            g.x[0] = __builtin_amdgcn_exp2f(fmaf(xb[0], kL2E, g.ob0.x) - sbs);
+            g.x[1] = __builtin_amdgcn_exp2f(fmaf(xb[1], kL2E, g.ob0.y) - sbs);
+            g.x[2] = __builtin_amdgcn_exp2f(fmaf(xb[2], kL2E, g.ob0.z) - sbs);
+            g.x[3] = __builtin_amdgcn_exp2f(fmaf(xb[3], kL2E, g.ob0.w) - sbs);
+            g.x[4] = __builtin_amdgcn_exp2f(fmaf(xb[4], kL2E, g.ob1.x) - sbs);
+            g.x[5] = __builtin_amdgcn_exp2f(fmaf(xb[5], kL2E, g.ob1.y) - sbs);
+            g.x[6] = __builtin_amdgcn_exp2f(fmaf(xb[6], kL2E, g.ob1.z) - sbs);
+            g.x[7] = __builtin_amdgcn_exp2f(fmaf(xb[7], kL2E, g.ob1.w) - sbs);
+        };
+        // side 0: A row ar at ka; side 1: B column bcol at kb (planes 3..5)
+        auto stage_store = [&](const StageRegs& g, int side, int buf) {
+            bf16x8 h, m, l;
+            split_bf16x3(g.x, h, m, l);
+            __bf16* d = hsm + buf * kBufH + (side ? 3 * PL + bcol * LDK + kb : ar * LDK + ka);
+            *(bf16x8*)(d) = h;
+            *(bf16x8*)(d + PL) = m;
+            *(bf16x8*)(d + 2 * PL) = l;
+        };
+        auto stage = [&](const float4 (&xa)[2], const float (&xb)[8], int ks, int buf) {
+            StageRegs g;
+            stage_offsets(g, ks);
+            stage_exp_a(g, xa);
+            stage_store(g, 0, buf);
+            stage_exp_b(g, xb);
+            stage_store(g, 1, buf);
+        };
+        const int nslices = C / kK;   // even: C is a multiple of 128
+        gload(ra[0], rb[0], 0);
+        gload(ra[1], rb[1], kK);
+        shifts();
+        sas = sa[ar] * kL2E;
+        sbs = sb[bcol] * kL2E;
+        stage(ra[0], rb[0], 0, 0);
+        __syncthreads();
+
+        // ---- products: wave (wm, wn) owns rows wm*QW.., columns wn*QW.. as BR x BR blocks;
+        // lane l supplies row (column) l % 32 at contracted indices 8 (l / 32) .. + 7
+        const int li = lane & 31, lh = 8 * (lane >> 5);
+        auto operands = [&](bf16x8 (&A)[3][BR], bf16x8 (&Bv)[3][BR], int buf) {
+            const __bf16* base = hsm + buf * kBufH;
+#pragma unroll
+            for (int p = 0; p < 3; ++p) {
+#pragma unroll
+                for (int i = 0; i < BR; ++i)
+                    A[p][i] = *(const bf16x8*)(base + p * PL + (wm * QW + i * 32 + li) * LDK + lh);
+#pragma unroll
+                for (int j = 0; j < BR; ++j)
+                    Bv[p][j] = *(const bf16x8*)(base + (3 + p) * PL + (wn * QW + j * 32 + li) * LDK + lh);
+            }
+        };
+        // one slice: the products of buffer cur while slice s + 1 (raw set xa1/xb1) is staged into
+        // the other buffer and slice s + 2 is loaded into the set just consumed (xa0/xb0).  After
+        // the last slice the staging works on stale registers into a buffer nobody reads.  The
+        // six products of each block pair go out in six groups of BR x BR independent products
+        // (different accumulators); one staging phase follows each group, fenced so that the
+        // scheduler interleaves the two within the group but keeps the groups in order.
+        auto slice = [&](int s, int cur, float4 (&xa0)[2], float (&xb0)[8], float4 (&xa1)[2],
+                         float (&xb1)[8]) {
+            if (s + 2 < nslices) gload(xa0, xb0, (s + 2) * kK);
+            bf16x8 A[3][BR], Bv[3][BR];
+            operands(A, Bv, cur);
+            StageRegs g;
+            // (part of A, part of B): the smaller products first
+            constexpr int kTerms[6][2] = {{2, 0}, {0, 2}, {1, 1}, {1, 0}, {0, 1}, {0, 0}};
+            auto term = [&](int t) {
+#pragma unroll
+                for (int i = 0; i < BR; ++i)
+#pragma unroll
+                    for (int j = 0; j < BR; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            A[kTerms[t][0]][i], Bv[kTerms[t][1]][j], acc[i][j], 0, 0, 0);
+            };
+            const int ks1 = min(s + 1, nslices - 1) * kK;
+            term(0);
+            stage_offsets(g, ks1);
+            __builtin_amdgcn_sched_barrier(0);
+            term(1);
+            stage_exp_a(g, xa1);
+            __builtin_amdgcn_sched_barrier(0);
+            term(2);
+            stage_store(g, 0, cur ^ 1);
+            __builtin_amdgcn_sched_barrier(0);
+            term(3);
+            stage_exp_b(g, xb1);
+            __builtin_amdgcn_sched_barrier(0);
+            term(4);
+            stage_store(g, 1, cur ^ 1);
+            __builtin_amdgcn_sched_barrier(0);
+            term(5);
+            __syncthreads();
+        };
+        for (int s = 0; s < nslices; s += 2) {
+            slice(s, 0, ra[0], rb[0], ra[1], rb[1]);
+            slice(s + 1, 1, ra[1], rb[1], ra[0], rb[0]);
+        }
+    }
     // ---- epilogue: core = log S into an LDS tile; entries whose S underflowed are
     // recomputed afterwards by a direct log-sum-exp (a rare, non-unrolled path)
     float* T = smem;   // [TM][LDT], over the slice buffers (all reads are done)
@@ -943,35 +1473,71 @@ struct RootArgs {
     float* logZ;
 };
 
-__global__ __launch_bounds__(256) void k_root_log(RootArgs a) {
-    __shared__ float red[16];
-    __shared__ double redd[4];
+// One workgroup per sequence: log Z = LSE_{i,j} (core[i][j] + ro[i] + co[j]) of the root.
+// Latency, not bandwidth, bounds it (B workgroups): the first kRootThreads * kRootUnroll
+// entries (all of them for C <= 128) are loaded before the offsets' maxima are reduced.
+constexpr int kRootThreads = 1024, kRootUnroll = 16;
+
+__global__ __launch_bounds__(kRootThreads) void k_root_log(RootArgs a) {
+    __shared__ float red[2 * kRootThreads / kWave];
+    __shared__ double redd[2 * kRootThreads / kWave];
+    __shared__ float rof[kMaxLabels], cof[kMaxLabels];   // offsets less their maxima
     const int64_t b = blockIdx.x;
     const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
-    const int64_t C = a.C;
+    const int C = (int)a.C, CC = C * C, tid = threadIdx.x;
     if (Eb == 0) {
-        if (threadIdx.x == 0) a.logZ[b] = logf((float)C);
+        if (tid == 0) a.logZ[b] = logf((float)C);
         return;
     }
     const float* P = a.core + mat_off(b, 0, a.nodes, C);
     const double* ro = a.ro ? a.ro + (size_t)b * a.nodes * C : nullptr;
     const double* co = a.co ? a.co + (size_t)b * a.nodes * C : nullptr;
-    double rm = -INFINITY, cm = -INFINITY;
-    for (int64_t i = threadIdx.x; i < C; i += blockDim.x) {
-        if (ro) rm = fmax(rm, ro[i]);
-        if (co) cm = fmax(cm, co[i]);
+    float x[kRootUnroll];
+    auto load = [&](int base) {
+#pragma unroll
+        for (int k = 0; k < kRootUnroll; ++k) {
+            const int idx = base + k * kRootThreads;
+            x[k] = idx < CC ? P[idx] : -INFINITY;
+        }
+    };
+    load(tid);
+    const double rv = (ro && tid < C) ? ro[tid] : -INFINITY;
+    const double cv = (co && tid < C) ? co[tid] : -INFINITY;
+    // both maxima in one reduction
+    {
+        const double rw = wave_max_d(rv), cw = wave_max_d(cv);
+        if ((tid & (kWave - 1)) == 0) {
+            redd[2 * (tid / kWave)] = rw;
+            redd[2 * (tid / kWave) + 1] = cw;
+        }
     }
-    const double rs = ro ? safe_shift_d(block_max_d(rm, redd)) : 0.0;
-    const double cs = co ? safe_shift_d(block_max_d(cm, redd)) : 0.0;
+    __syncthreads();
+    double rm = redd[0], cm = redd[1];
+#pragma unroll
+    for (int w = 1; w < kRootThreads / kWave; ++w) {
+        rm = fmax(rm, redd[2 * w]);
+        cm = fmax(cm, redd[2 * w + 1]);
+    }
+    const double rs = ro ? safe_shift_d(rm) : 0.0;
+    const double cs = co ? safe_shift_d(cm) : 0.0;
+    if (tid < C) {
+        rof[tid] = ro ? (float)(rv - rs) : 0.f;
+        cof[tid] = co ? (float)(cv - cs) : 0.f;
+    }
+    __syncthreads();
     Lse acc = lse_empty();
-    for (int64_t idx = threadIdx.x; idx < C * C; idx += blockDim.x) {
-        const int64_t i = idx / C, j = idx % C;
-        float x = P[idx];
-        if (ro) x += (float)(ro[i] - rs) + (float)(co[j] - cs);
-        acc = lse_push(acc, x);
+    for (int base = tid;;) {
+#pragma unroll
+        for (int k = 0; k < kRootUnroll; ++k) {
+            const int idx = base + k * kRootThreads;
+            if (idx < CC) acc = lse_push(acc, x[k] + rof[idx / C] + cof[idx % C]);
+        }
+        base += kRootUnroll * kRootThreads;
+        if (base >= CC) break;
+        load(base);
     }
     acc = block_lse(acc, red);
-    if (threadIdx.x == 0) {
+    if (tid == 0) {
         const float l = lse_value(acc);
         a.logZ[b] = (l == -INFINITY) ? -INFINITY : (float)(rs + cs + (double)l);
     }
@@ -1486,13 +2052,27 @@ hipError_t allow_up_lds() {
     return hipSuccess;
 }
 
-template <int TM>
+template <bool VEC>
+hipError_t allow_leaf_lds() {
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute(
+            (const void*)k_leaf_max_lds<VEC>, hipFuncAttributeMaxDynamicSharedMemorySize,
+            (int)(sizeof(float) * kLeafLdsMaxLabels * (kLeafLdsMaxLabels + 1)));
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    return hipSuccess;
+}
+
+template <int TM, bool kBf>
 hipError_t allow_up_full_lds() {
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void*)k_up_log_full<TM>,
+        using Sm = std::conditional_t<kBf, UpBfSmem<TM>, UpFullSmem<TM>>;
+        hipError_t e = hipFuncSetAttribute((const void*)k_up_log_full<TM, kBf>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)UpFullSmem<TM>::kBytes);
+                                           (int)Sm::kBytes);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
@@ -1505,12 +2085,20 @@ hipError_t up_sweep_vec(const Plan& p, const float* pot, const int32_t* lengths,
     if (e == hipSuccess && p.C > 64) e = allow_up_lds<128, VEC, kBits>();
     // full tiles (every tile edge divides C; dense chains): the scheduled kernel
     const bool full64 = !kBits && p.C % 64 == 0, full128 = !kBits && p.C % 128 == 0;
-    if (e == hipSuccess && full64) e = allow_up_full_lds<64>();
-    if (e == hipSuccess && full128) e = allow_up_full_lds<128>();
+    if (e == hipSuccess && full64) e = allow_up_full_lds<64, false>();
+    if (e == hipSuccess && full128) e = allow_up_full_lds<128, kUpBf16>();
     if (e != hipSuccess) return e;
     // the leaves' row and column maxima (shifts of the level-1 products)
     LeafMaxArgs m{pot, lengths, p.N, p.C, p.lrmax, p.lcmax, p.rbits[0], p.cbits[0], p.bw};
-    hipLaunchKernelGGL((k_leaf_max<VEC, kBits>), dim3((unsigned)(p.B * p.E)), dim3(256), 0, s, m);
+    if (!kBits && p.C <= kLeafLdsMaxLabels) {
+        const size_t lds = sizeof(float) * p.C * (p.C + 1);
+        e = allow_leaf_lds<VEC>();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((k_leaf_max_lds<VEC>), dim3((unsigned)(p.B * p.E)),
+                           dim3(kLeafLdsThreads), lds, s, m);
+    } else {
+        hipLaunchKernelGGL((k_leaf_max<VEC, kBits>), dim3((unsigned)(p.B * p.E)), dim3(256), 0, s, m);
+    }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     for (int l = 1; l <= p.D; ++l) {
@@ -1535,13 +2123,15 @@ hipError_t up_sweep_vec(const Plan& p, const float* pot, const int32_t* lengths,
         a.ntile = nt;
         a.nlogical = p.B * a.nodes * nt * nt;
         a.ngrid = node_grid(p.B * a.nodes, nt * nt);
-        const int tm = up_tile(p.C, p.B * a.nodes);
-        if (tm == 64 && full64)
-            hipLaunchKernelGGL((k_up_log_full<64>), dim3((unsigned)a.ngrid), dim3(kUpThreads),
+        const int tm = up_tile(p.C, p.B * a.nodes, kBits);
+        if (tm == kSmTM)
+            hipLaunchKernelGGL((k_up_log_small<VEC>), dim3((unsigned)a.ngrid), dim3(kUpThreads), 0, s, a);
+        else if (tm == 64 && full64)
+            hipLaunchKernelGGL((k_up_log_full<64, false>), dim3((unsigned)a.ngrid), dim3(kUpThreads),
                                UpFullSmem<64>::kBytes, s, a);
         else if (tm == 128 && full128)
-            hipLaunchKernelGGL((k_up_log_full<128>), dim3((unsigned)a.ngrid), dim3(kUpThreads),
-                               UpFullSmem<128>::kBytes, s, a);
+            hipLaunchKernelGGL((k_up_log_full<128, kUpBf16>), dim3((unsigned)a.ngrid), dim3(kUpThreads),
+                               (std::conditional_t<kUpBf16, UpBfSmem<128>, UpFullSmem<128>>::kBytes), s, a);
         else if (tm == 64)
             hipLaunchKernelGGL((k_up_log<64, VEC, kBits>), dim3((unsigned)a.ngrid), dim3(kUpThreads),
                                UpSmem<64>::kBytes, s, a);
@@ -1574,7 +2164,7 @@ hipError_t root(const Plan& p, const float* pot, const int32_t* lengths, float* 
         r.core = p.core[p.D]; r.ro = p.ro[p.D]; r.co = p.co[p.D]; r.nodes = p.Np >> p.D;
     }
     r.lengths = lengths; r.N = p.N; r.C = p.C; r.logZ = logZ;
-    hipLaunchKernelGGL(k_root_log, dim3((unsigned)p.B), dim3(256), 0, s, r);
+    hipLaunchKernelGGL(k_root_log, dim3((unsigned)p.B), dim3(kRootThreads), 0, s, r);
     return hipGetLastError();
 }
 
