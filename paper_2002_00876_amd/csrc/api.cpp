@@ -164,6 +164,7 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, boo
         }
         p->lrmax = bump.take<float>((size_t)B * p->E * C);
         p->lcmax = bump.take<float>((size_t)B * p->E * C);
+        if (op == TS_OP_MARGINALS) p->wide = bump.take<int32_t>((size_t)B * p->E);
         p->bw = (int)((C + 63) / 64);
         for (int l = 0; masks && l < D; ++l) {
             const size_t n = l == 0 ? (size_t)B * p->E : (size_t)B * (size_t)(Np >> l);

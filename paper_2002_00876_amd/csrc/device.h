@@ -176,6 +176,33 @@ __device__ __forceinline__ void lse_fold(float& m, float& s, const float (&x)[K]
 __device__ __forceinline__ float lse_val(float m, float s) {
     return m == -INFINITY ? -INFINITY : m + flog(s);
 }
+// The same with float64 terms and maximum, for terms that are sums of float32 values of large
+// magnitude (raw potentials plus message entries): a term is rounded to float32 only once the
+// maximum is taken off, where it is small, so the state keeps the terms' full precision.
+template <int K>
+__device__ __forceinline__ void lse_fold_d(double& m, float& s, const double (&x)[K]) {
+    double cm = x[0];
+#pragma unroll
+    for (int k = 1; k < K; ++k) cm = fmax(cm, x[k]);
+    const double nm = fmax(m, cm);
+    const double sh = nm == -INFINITY ? 0.0 : nm;
+    float t = 0.f;
+#pragma unroll
+    for (int k = 0; k < K; ++k) t += fexp((float)(x[k] - sh));
+    s = s * fexp((float)(m - sh)) + t;
+    m = nm;
+}
+__device__ __forceinline__ double lse_val_d(double m, float s) {
+    return m == -INFINITY ? -INFINITY : m + (double)flog(s);
+}
+// either fold, by the terms' type
+template <int K, typename Tm>
+__device__ __forceinline__ void lse_fold_t(Tm& m, float& s, const Tm (&x)[K]) {
+    if constexpr (sizeof(Tm) == sizeof(double))
+        lse_fold_d<K>(m, s, x);
+    else
+        lse_fold<K>(m, s, x);
+}
 
 // Blocks are dispatched round-robin over the 8 XCDs (block i -> XCD i % 8).  Logical block
 // lid = node * ntiles + tile: the tiles of one node go to one XCD, one after another (they

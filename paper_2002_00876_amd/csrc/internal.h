@@ -44,6 +44,9 @@ struct Plan {
     float* pmc[kMaxLevels] = {};
     float* lrmax = nullptr;
     float* lcmax = nullptr;
+    // marginals: per edge, whether its potentials reach magnitude kWideMag (the edge's
+    // messages and marginal exponents are then formed in float64), [B][E]
+    int32_t* wide = nullptr;
     // finiteness bitmasks (only with masks; nullptr otherwise) of every node consumed by a
     // product (levels 0..D-1; level 0 is the leaves [B, E]): rbits [nodes][C][bw] has bit c of row a set iff entry (a, c) is
     // finite, cbits [nodes][C][bw] bit a of column c.  An entry of L (x) R is -inf exactly
@@ -70,6 +73,11 @@ struct Plan {
 };
 
 constexpr int kChunkLog = 4;   // chunks of at most 16 edges
+
+// Potentials of magnitude above this make float32 rounding of a sum such as message +
+// potential (about 2^-24 of the magnitude per operation) approach the marginals' absolute
+// tolerance; edges that reach it take the float64 formation of those sums.
+constexpr float kWideMag = 16.f;
 
 // Whether the log-semiring tree of C labels takes the chunk kernels (C <= 64, no masks).
 bool chunk_path(int64_t C, bool masks);

@@ -54,7 +54,24 @@ struct LeafMaxArgs {
     uint64_t* rbits;   // [B, E, C, bw] finiteness of the left leaves' rows
     uint64_t* cbits;   // [B, E, C, bw] finiteness of the right leaves' columns
     int bw;
+    int32_t* wide;     // [B, E] max |finite entry| > kWideMag, or nullptr
 };
+
+// Block-wide flag of the leaf's largest finite magnitude (every thread passes the maximum
+// over the entries it read; waves' maxima meet in red[], one per wave)
+__device__ __forceinline__ void leaf_wide_flag(const LeafMaxArgs& a, int64_t edge, float am, float* red) {
+    am = wave_max(am);
+    const int w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) red[w] = am;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float m = red[0];
+        for (int q = 1; q < nw; ++q) m = fmaxf(m, red[q]);
+        a.wide[edge] = m > kWideMag;
+    }
+}
+// |x| for finite x, 0 for -inf (structural zeros carry no magnitude)
+__device__ __forceinline__ float fin_abs(float x) { return x == -INFINITY ? 0.f : fabsf(x); }
 
 template <bool kVec, bool kBits>
 __global__ __launch_bounds__(256) void k_leaf_max(LeafMaxArgs a) {
@@ -68,13 +85,18 @@ __global__ __launch_bounds__(256) void k_leaf_max(LeafMaxArgs a) {
     const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
     const bool masks = kBits && (a.cbits || a.rbits);
     const bool split = !masks && C <= 128;
+    float am = 0.f;   // largest finite magnitude among the entries this thread read
     if (right && split) {
         __shared__ float part[256];
         const int P = 256 / C, p = tid / C, c = tid - p * C;   // C <= 128: P >= 2
         float cm = -INFINITY;
         if (p < P) {
 #pragma unroll 8
-            for (int i = p; i < C; i += P) cm = fmaxf(cm, leaf[(size_t)i * C + c]);
+            for (int i = p; i < C; i += P) {
+                const float x = leaf[(size_t)i * C + c];
+                cm = fmaxf(cm, x);
+                am = fmaxf(am, fin_abs(x));
+            }
         }
         part[tid] = cm;
         __syncthreads();
@@ -85,7 +107,11 @@ __global__ __launch_bounds__(256) void k_leaf_max(LeafMaxArgs a) {
     } else if (right && tid < C) {
         float cm = -INFINITY;
 #pragma unroll 8
-        for (int i = 0; i < C; ++i) cm = fmaxf(cm, leaf[(size_t)i * C + tid]);
+        for (int i = 0; i < C; ++i) {
+            const float x = leaf[(size_t)i * C + tid];
+            cm = fmaxf(cm, x);
+            am = fmaxf(am, fin_abs(x));
+        }
         a.lcmax[(size_t)(b * E + t) * C + tid] = cm;
         if (kBits && a.cbits) {
             bool hole = false;   // a -inf entry in the column
@@ -111,6 +137,7 @@ __global__ __launch_bounds__(256) void k_leaf_max(LeafMaxArgs a) {
             const int i = i0 + sub;
             const float4 v = *reinterpret_cast<const float4*>(leaf + (size_t)i * C + col);
             float m = fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w));
+            am = fmaxf(am, fmaxf(fmaxf(fin_abs(v.x), fin_abs(v.y)), fmaxf(fin_abs(v.z), fin_abs(v.w))));
             m = fmaxf(m, dpp_f(m, 0xB1));    // within each row of 16 lanes
             m = fmaxf(m, dpp_f(m, 0x4E));
             m = fmaxf(m, dpp_f(m, 0x141));
@@ -127,9 +154,13 @@ __global__ __launch_bounds__(256) void k_leaf_max(LeafMaxArgs a) {
                 for (int j = 4 * lane; j < C; j += 4 * kWave) {
                     const float4 v = *reinterpret_cast<const float4*>(row + j);
                     m = fmaxf(m, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
+                    am = fmaxf(am, fmaxf(fmaxf(fin_abs(v.x), fin_abs(v.y)), fmaxf(fin_abs(v.z), fin_abs(v.w))));
                 }
             } else {
-                for (int j = lane; j < C; j += kWave) m = fmaxf(m, row[j]);
+                for (int j = lane; j < C; j += kWave) {
+                    m = fmaxf(m, row[j]);
+                    am = fmaxf(am, fin_abs(row[j]));
+                }
             }
             m = wave_max(m);
             if (lane == 0) rmax[i] = m;
@@ -144,6 +175,10 @@ __global__ __launch_bounds__(256) void k_leaf_max(LeafMaxArgs a) {
                 if (lane == q) rb[q] = bits;
             }
         }
+    }
+    if (a.wide) {
+        __shared__ float wred[256 / kWave];
+        leaf_wide_flag(a, b * E + t, am, wred);
     }
 }
 
@@ -165,6 +200,7 @@ __global__ __launch_bounds__(kLeafLdsThreads) void k_leaf_max_lds(LeafMaxArgs a)
     const bool left = (t & 1) == 0, right = (t & 1) == 1 || t + 1 == Eb;
     const int C = (int)a.C, CC = C * C, LD = C + 1, tid = threadIdx.x;
     const float* leaf = a.pot + (size_t)(b * E + t) * CC;
+    float am = 0.f;   // largest finite magnitude among the entries this thread loaded
     if constexpr (kVec) {
         // C % 4 == 0: a float4 never straddles two rows
         constexpr int kQ = kLeafLdsMaxLabels * kLeafLdsMaxLabels / 4 / kLeafLdsThreads;
@@ -179,6 +215,8 @@ __global__ __launch_bounds__(kLeafLdsThreads) void k_leaf_max_lds(LeafMaxArgs a)
         for (int q = 0; q < kQ; ++q) {
             const int i4 = tid + q * kLeafLdsThreads;
             if (i4 < C4) {
+                am = fmaxf(am, fmaxf(fmaxf(fin_abs(v[q].x), fin_abs(v[q].y)),
+                                     fmaxf(fin_abs(v[q].z), fin_abs(v[q].w))));
                 const int r = (4 * i4) / C, c = 4 * i4 - r * C;
                 float* d = T + r * LD + c;
                 d[0] = v[q].x;
@@ -199,12 +237,17 @@ __global__ __launch_bounds__(kLeafLdsThreads) void k_leaf_max_lds(LeafMaxArgs a)
         for (int q = 0; q < kQ; ++q) {
             const int i = tid + q * kLeafLdsThreads;
             if (i < CC) {
+                am = fmaxf(am, fin_abs(v[q]));
                 const int r = i / C;
                 T[r * LD + i - r * C] = v[q];
             }
         }
     }
     __syncthreads();
+    if (a.wide) {
+        __shared__ float wred[kLeafLdsThreads / kWave];
+        leaf_wide_flag(a, b * E + t, am, wred);
+    }
     // four running maxima per line: a short dependency chain
     const bool isrow = tid < kLeafLdsMaxLabels;
     const int line = isrow ? tid : tid - kLeafLdsMaxLabels;
@@ -1612,6 +1655,51 @@ __device__ __forceinline__ float row_lse(const float* __restrict__ M, int C, con
     return lse_val(m, s);
 }
 
+// The same two passes with each term w + M formed in float64 (M raw potentials, possibly
+// large): the result keeps the terms' precision (float64 maximum plus a float32 log-sum)
+__device__ __forceinline__ double col_lse_d(const float* __restrict__ M, int C, const float* w, int j) {
+    double m = -INFINITY;
+    float s = 0.f;
+    int i = 0;
+    for (; i + 8 <= C; i += 8) {
+        double x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] = (double)M[(size_t)(i + u) * C + j];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] += (double)w[i + u];
+        lse_fold_d<8>(m, s, x);
+    }
+    for (; i < C; ++i) {
+        const double x[1] = {(double)M[(size_t)i * C + j] + (double)w[i]};
+        lse_fold_d<1>(m, s, x);
+    }
+    return lse_val_d(m, s);
+}
+
+template <bool kVec>
+__device__ __forceinline__ double row_lse_d(const float* __restrict__ M, int C, const float* w, int i) {
+    const float* row = M + (size_t)i * C;
+    double m = -INFINITY;
+    float s = 0.f;
+    int j = 0;
+    if constexpr (kVec) {
+        const float4* r4 = reinterpret_cast<const float4*>(row);
+        for (; j + 8 <= C; j += 8) {
+            const float4 v0 = r4[j / 4], v1 = r4[j / 4 + 1];
+            const double x[8] = {(double)v0.x + (double)w[j], (double)v0.y + (double)w[j + 1],
+                                 (double)v0.z + (double)w[j + 2], (double)v0.w + (double)w[j + 3],
+                                 (double)v1.x + (double)w[j + 4], (double)v1.y + (double)w[j + 5],
+                                 (double)v1.z + (double)w[j + 6], (double)v1.w + (double)w[j + 7]};
+            lse_fold_d<8>(m, s, x);
+        }
+    }
+    for (; j < C; ++j) {
+        const double x[1] = {(double)row[j] + (double)w[j]};
+        lse_fold_d<1>(m, s, x);
+    }
+    return lse_val_d(m, s);
+}
+
 // Max of a double over the calling thread's half of the workgroup (each half gets its own
 // result); red holds one double per wave.  Both halves call it together (it contains
 // workgroup barriers).
@@ -1637,9 +1725,11 @@ __device__ __forceinline__ double half_max_d(double x, double* red) {
 // every thread of the half works: the C lines are cut into P = 256 / C parts (rows
 // i = p, p + P, ... of a column; a contiguous chunk of a row), whose partial log-sum-exps are
 // merged through LDS.  (At C = 128, two parts per line were slower than one.)
-template <bool kVec>
+// kExact (leaves of large magnitude in the marginals pass): the terms formed in float64
+// (col_lse_d / row_lse_d).  yraw, when given, receives the unshifted result in float64.
+template <bool kVec, bool kExact = false>
 __device__ void half_vec(bool active, const float* core, const double* ro, const double* co,
-                         int C, const float* x, float* w, float* y, double* red, float* yraw) {
+                         int C, const float* x, float* w, float* y, double* red, double* yraw) {
     __shared__ float pm[kVecThreads], ps[kVecThreads];
     const bool rowPass = threadIdx.x >= kHalfThreads;
     const int t = threadIdx.x - (rowPass ? kHalfThreads : 0);
@@ -1655,8 +1745,8 @@ __device__ void half_vec(bool active, const float* core, const double* ro, const
             w[i] = (float)((double)x[i] + (inOff ? inOff[i] : 0.0) - ws);
     __syncthreads();
     double z = -INFINITY;
-    float l = -INFINITY;
-    if (kVec && (C == 32 || C == 64)) {
+    double l = -INFINITY;
+    if (!kExact && kVec && (C == 32 || C == 64)) {
         const int P = kHalfThreads / C, p = t / C, c = t - p * C, nr = C / P;   // nr % 4 == 0
         float m = -INFINITY, sum = 0.f;
         if (active) {
@@ -1693,11 +1783,14 @@ __device__ void half_vec(bool active, const float* core, const double* ro, const
             l = lse_val(mm, ss);
         }
     } else if (active && t < C) {
-        l = rowPass ? row_lse<kVec>(core, C, w, t) : col_lse(core, C, w, t);
+        if constexpr (kExact)
+            l = rowPass ? row_lse_d<kVec>(core, C, w, t) : col_lse_d(core, C, w, t);
+        else
+            l = rowPass ? row_lse<kVec>(core, C, w, t) : col_lse(core, C, w, t);
     }
     if (active && t < C) {
-        z = (l == -INFINITY) ? -INFINITY : (outOff ? outOff[t] : 0.0) + ws + (double)l;
-        if (yraw) yraw[t] = (float)z;
+        z = (l == -INFINITY) ? -INFINITY : (outOff ? outOff[t] : 0.0) + ws + l;
+        if (yraw) yraw[t] = z;
     }
     const double zs = safe_shift_d(half_max_d(z, red));
     if (active && t < C) y[t] = (z == -INFINITY) ? -INFINITY : (float)(z - zs);
@@ -1774,7 +1867,16 @@ struct FormArgs {
     const int32_t* lengths;
     int64_t N, C;
     float* marg;
+    const int32_t* wide;   // per edge: potentials reach kWideMag (nullptr: every edge)
 };
+
+// Whether the pair (tL, tR) of sequence b takes the float64 formation: kernels are launched
+// once per formation, and a workgroup returns at once when its pair belongs to the other.
+__device__ __forceinline__ bool pair_wide(const FormArgs& a, int64_t b, int64_t E, int64_t tL,
+                                          bool right) {
+    if (!a.wide) return true;
+    return a.wide[b * E + tL] != 0 || (right && a.wide[b * E + tL + 1] != 0);
+}
 
 // The same per-pair computation with each leaf read from memory once (C <= 128, C % 4 == 0):
 // the workgroup keeps both leaves in registers, in the layout write_marginal uses (thread t
@@ -1796,15 +1898,34 @@ __device__ __forceinline__ void lse_merge_into(float& m, float& s, float m2, flo
     m = nm;
 }
 
-template <int kR>
+// A state with a float64 maximum as a float32 state of the same value: m rounded to float,
+// the rounding folded into s (a relative change below 2^-24).  Merging such states in float
+// stays exact where it matters: maxima within a factor 2 subtract exactly, and farther ones
+// weigh in by a negligible exponential.
+__device__ __forceinline__ void lse_to_float(double m, float s, float& mf, float& sf) {
+    if (m == -INFINITY) {
+        mf = -INFINITY;
+        sf = 0.f;
+        return;
+    }
+    mf = (float)m;
+    sf = s * fexp((float)(m - (double)mf));
+}
+__device__ __forceinline__ void lse_to_float(float m, float s, float& mf, float& sf) {
+    mf = m;
+    sf = s;
+}
+
+template <int kR, bool kExact>
 __global__ __launch_bounds__(kVecThreads) void k_form_reg(FormArgs a) {
+    using Tm = std::conditional_t<kExact, double, float>;   // type of the formed terms
     // column partials [step][C] (step * C <= 4 kVecThreads) and row partials [C][G]
     constexpr int kMaxC = kR == 2 ? 64 : kRegMaxLabels;   // kR = 2 serves C <= 64
     constexpr int kColParts = 4 * kVecThreads, kRowParts = kMaxC * kMaxC / 4;
-    __shared__ float su[kRegMaxLabels], sv[kRegMaxLabels], ya[kRegMaxLabels], zb[kRegMaxLabels],
-        yraw[kRegMaxLabels], zraw[kRegMaxLabels];
+    __shared__ float su[kRegMaxLabels], sv[kRegMaxLabels], ya[kRegMaxLabels], zb[kRegMaxLabels];
+    __shared__ double yraw[kRegMaxLabels], zraw[kRegMaxLabels];
     __shared__ float pm[kColParts], ps[kColParts], qm[kRowParts], qs[kRowParts];
-    __shared__ float nrm[2], mx[2];
+    __shared__ double nrm[2];
     const int64_t npairs = (a.N - 1 + 1) / 2;
     const int64_t b = blockIdx.x / npairs, k = blockIdx.x % npairs;
     const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
@@ -1813,13 +1934,15 @@ __global__ __launch_bounds__(kVecThreads) void k_form_reg(FormArgs a) {
     const int64_t tL = 2 * k, tR = 2 * k + 1;
     const size_t CC = (size_t)C * C;
     const int tid = threadIdx.x;
-    for (int64_t t = tL; t <= tR; ++t)
-        if (t < E && t >= Eb) {
-            float* o = a.marg + (size_t)(b * E + t) * CC;
-            for (size_t idx = tid; idx < CC; idx += kVecThreads) o[idx] = 0.f;
-        }
+    if (!kExact)   // (padding edges once, by the float32 formation's launch)
+        for (int64_t t = tL; t <= tR; ++t)
+            if (t < E && t >= Eb) {
+                float* o = a.marg + (size_t)(b * E + t) * CC;
+                for (size_t idx = tid; idx < CC; idx += kVecThreads) o[idx] = 0.f;
+            }
     if (tL >= Eb) return;
     const bool right = tR < Eb;
+    if (pair_wide(a, b, E, tL, right) != kExact) return;
     const int G = C / 4, step = kVecThreads / G;
     const int g = tid % G, i0 = tid / G, j = 4 * g;
     const bool act = i0 < step;
@@ -1841,37 +1964,37 @@ __global__ __launch_bounds__(kVecThreads) void k_form_reg(FormArgs a) {
     }
     __syncthreads();
     // partial log-sum-exps: columns j..j+3 of leaf_{2k} over the thread's rows (with u), and
-    // each of the thread's rows of leaf_{2k+1} over its 4 columns (with v)
+    // each of the thread's rows of leaf_{2k+1} over its 4 columns (with v).  A term adds a raw
+    // potential to a message entry; with kExact (potentials of large magnitude) it is formed
+    // in float64 and rounded only after the maximum is taken off (here, in the normalisers
+    // and in the marginals' exponents alike), so that float32 rounding at the potentials'
+    // magnitude never enters.  (The normalisers are formed in float64 either way.)
     if (act) {
-        const float v0 = sv[j], v1 = sv[j + 1], v2 = sv[j + 2], v3 = sv[j + 3];
-        float xc[4][kR];   // u[i] + l_{2k}[i][j + c] of the thread's rows (-inf past C)
+        const Tm v0 = sv[j], v1 = sv[j + 1], v2 = sv[j + 2], v3 = sv[j + 3];
+        Tm xc[4][kR];   // u[i] + l_{2k}[i][j + c] of the thread's rows (-inf past C)
 #pragma unroll
         for (int q = 0; q < kR; ++q) {
             const int i = i0 + q * step;
             const bool ok = i < C;
-            const float ui = ok ? su[i] : -INFINITY;
-            xc[0][q] = ui + lv[q].x;
-            xc[1][q] = ui + lv[q].y;
-            xc[2][q] = ui + lv[q].z;
-            xc[3][q] = ui + lv[q].w;
+            const Tm ui = ok ? (Tm)su[i] : (Tm)-INFINITY;
+            xc[0][q] = ui + (Tm)lv[q].x;
+            xc[1][q] = ui + (Tm)lv[q].y;
+            xc[2][q] = ui + (Tm)lv[q].z;
+            xc[3][q] = ui + (Tm)lv[q].w;
             if (right && ok) {
-                const float r[4] = {rv[q].x + v0, rv[q].y + v1, rv[q].z + v2, rv[q].w + v3};
-                const float m = fmaxf(fmaxf(r[0], r[1]), fmaxf(r[2], r[3]));
+                const Tm r[4] = {(Tm)rv[q].x + v0, (Tm)rv[q].y + v1, (Tm)rv[q].z + v2, (Tm)rv[q].w + v3};
+                Tm m = -INFINITY;
                 float sr = 0.f;
-                if (m != -INFINITY) {
-#pragma unroll
-                    for (int c = 0; c < 4; ++c) sr += fexp(r[c] - m);
-                }
-                qm[i * G + g] = m;
-                qs[i * G + g] = sr;
+                lse_fold_t<4>(m, sr, r);
+                lse_to_float(m, sr, qm[i * G + g], qs[i * G + g]);
             }
         }
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            float m = -INFINITY, sm = 0.f;
-            lse_fold<kR>(m, sm, xc[c]);
-            pm[i0 * C + j + c] = m;
-            ps[i0 * C + j + c] = sm;
+            Tm m = -INFINITY;
+            float sm = 0.f;
+            lse_fold_t<kR>(m, sm, xc[c]);
+            lse_to_float(m, sm, pm[i0 * C + j + c], ps[i0 * C + j + c]);
         }
     }
     __syncthreads();
@@ -1879,54 +2002,54 @@ __global__ __launch_bounds__(kVecThreads) void k_form_reg(FormArgs a) {
     if (tid < C) {
         float m = -INFINITY, sm = 0.f;
         for (int r = 0; r < step; ++r) lse_merge_into(m, sm, pm[r * C + tid], ps[r * C + tid]);
-        yraw[tid] = lse_val(m, sm);
+        yraw[tid] = lse_val_d(m, sm);
     } else if (right && tid >= kVecThreads / 2 && tid - kVecThreads / 2 < C) {
         const int i = tid - kVecThreads / 2;
         float m = -INFINITY, sm = 0.f;
         for (int r = 0; r < G; ++r) lse_merge_into(m, sm, qm[i * G + r], qs[i * G + r]);
-        zraw[i] = lse_val(m, sm);
+        zraw[i] = lse_val_d(m, sm);
     }
     __syncthreads();
     // the messages shifted to max 0 (wave 0: alpha_{2k+1} from y, wave 1: beta_{2k+1} from z)
     const int w = tid / kWave, lane = tid % kWave;
     if (w < 2 && (w == 0 || right)) {
-        const float* src = w == 0 ? yraw : zraw;
-        float m = -INFINITY;
-        for (int i = lane; i < C; i += kWave) m = fmaxf(m, src[i]);
-        m = safe_shift(wave_max(m));
+        const double* src = w == 0 ? yraw : zraw;
+        double m = -INFINITY;
+        for (int i = lane; i < C; i += kWave) m = fmax(m, src[i]);
+        m = safe_shift_d(wave_max_d(m));
         float* dst = w == 0 ? ya : zb;
-        for (int i = lane; i < C; i += kWave) dst[i] = src[i] - m;
-        if (lane == 0) mx[w] = m;
+        for (int i = lane; i < C; i += kWave) dst[i] = (float)(src[i] - m);
     }
     __syncthreads();
     // normalisers: n_{2k} = LSE_j yraw[j] + beta_{2k+1}[j] (or + v[j] without a right edge),
     // n_{2k+1} = LSE_i alpha_{2k+1}[i] + zraw[i]
     if (w < 2 && (w == 0 || right)) {
-        float m = -INFINITY, sm = 0.f;
+        double m = -INFINITY;
+        float sm = 0.f;
         for (int i = lane; i < C; i += kWave) {
-            float x[1] = {w == 0 ? yraw[i] + (right ? zb[i] : sv[i]) : ya[i] + zraw[i]};
-            lse_fold<1>(m, sm, x);
+            const double x[1] = {w == 0 ? yraw[i] + (double)(right ? zb[i] : sv[i]) : (double)ya[i] + zraw[i]};
+            lse_fold_d<1>(m, sm, x);
         }
-        const float mm = wave_max(m);
-        sm = wave_sum(m == -INFINITY ? 0.f : sm * fexp(m - safe_shift(mm)));
-        if (lane == 0) nrm[w] = lse_val(mm, sm);
+        const double mm = wave_max_d(m);
+        sm = wave_sum(m == -INFINITY ? 0.f : sm * fexp((float)(m - safe_shift_d(mm))));
+        if (lane == 0) nrm[w] = lse_val_d(mm, sm);
     }
     __syncthreads();
     if (!act) return;
-    // the marginals from the registers
-    auto write = [&](const float4* lvq, const float* al, const float* be, float n, float* out) {
+    // the marginals from the registers (exponents formed in Tm)
+    auto write = [&](const float4* lvq, const float* al, const float* be, double n, float* out) {
         const bool zero = n == -INFINITY;
-        const float b0 = be[j] - n, b1 = be[j + 1] - n, b2 = be[j + 2] - n, b3 = be[j + 3] - n;
+        const Tm b0 = be[j], b1 = be[j + 1], b2 = be[j + 2], b3 = be[j + 3];
 #pragma unroll
         for (int q = 0; q < kR; ++q) {
             const int i = i0 + q * step;
             if (i < C) {
-                const float ai = al[i];
+                const Tm an = (Tm)((double)al[i] - n);
                 float4 r;
-                r.x = zero ? 0.f : fexp(ai + lvq[q].x + b0);
-                r.y = zero ? 0.f : fexp(ai + lvq[q].y + b1);
-                r.z = zero ? 0.f : fexp(ai + lvq[q].z + b2);
-                r.w = zero ? 0.f : fexp(ai + lvq[q].w + b3);
+                r.x = zero ? 0.f : fexp((float)(((Tm)lvq[q].x + b0) + an));
+                r.y = zero ? 0.f : fexp((float)(((Tm)lvq[q].y + b1) + an));
+                r.z = zero ? 0.f : fexp((float)(((Tm)lvq[q].z + b2) + an));
+                r.w = zero ? 0.f : fexp((float)(((Tm)lvq[q].w + b3) + an));
                 *reinterpret_cast<float4*>(out + (size_t)i * C + j) = r;
             }
         }
@@ -1938,42 +2061,44 @@ __global__ __launch_bounds__(kVecThreads) void k_form_reg(FormArgs a) {
 // mu = exp(al[i] + leaf[i][j] + be[j] - n) over one C x C edge, the whole workgroup:
 // thread t takes column group t % G (16 bytes when kVec, else one float) of rows t / G,
 // t / G + T / G, ... so that each row is read and written contiguously
-template <bool kVec>
+// (kExact: the exponent al[i] + leaf[i][j] + be[j] - n formed in float64, rounded once)
+template <bool kVec, bool kExact>
 __device__ void write_marginal(const float* __restrict__ leaf, const float* al, const float* be,
-                               float n, int C, float* __restrict__ out) {
+                               double n, int C, float* __restrict__ out) {
+    using Tm = std::conditional_t<kExact, double, float>;
     constexpr int kW = kVec ? 4 : 1;
     const int G = C / kW, step = kVecThreads / G;
     const int g = threadIdx.x % G, i0 = threadIdx.x / G;
     if (i0 >= step) return;
     const int j = g * kW;
-    float bj[kW];
+    Tm bj[kW];
 #pragma unroll
-    for (int q = 0; q < kW; ++q) bj[q] = be[j + q] - n;
+    for (int q = 0; q < kW; ++q) bj[q] = be[j + q];
     const bool zero = n == -INFINITY;
 #pragma unroll 4
     for (int i = i0; i < C; i += step) {
-        const float ai = al[i];
+        const Tm an = (Tm)((double)al[i] - n);
         if constexpr (kVec) {
             const float4 v = *reinterpret_cast<const float4*>(leaf + (size_t)i * C + j);
             float4 r;
-            r.x = zero ? 0.f : fexp(ai + v.x + bj[0]);
-            r.y = zero ? 0.f : fexp(ai + v.y + bj[1]);
-            r.z = zero ? 0.f : fexp(ai + v.z + bj[2]);
-            r.w = zero ? 0.f : fexp(ai + v.w + bj[3]);
+            r.x = zero ? 0.f : fexp((float)(((Tm)v.x + bj[0]) + an));
+            r.y = zero ? 0.f : fexp((float)(((Tm)v.y + bj[1]) + an));
+            r.z = zero ? 0.f : fexp((float)(((Tm)v.z + bj[2]) + an));
+            r.w = zero ? 0.f : fexp((float)(((Tm)v.w + bj[3]) + an));
             *reinterpret_cast<float4*>(out + (size_t)i * C + j) = r;
         } else {
             const float v = leaf[(size_t)i * C + j];
-            out[(size_t)i * C + j] = zero ? 0.f : fexp(ai + v + bj[0]);
+            out[(size_t)i * C + j] = zero ? 0.f : fexp((float)(((Tm)v + bj[0]) + an));
         }
     }
 }
 
-template <bool kVec>
+template <bool kVec, bool kExact>
 __global__ __launch_bounds__(kVecThreads) void k_form_log(FormArgs a) {
-    __shared__ float su[kMaxLabels], sv[kMaxLabels], sy[2][kMaxLabels], sw[2][kMaxLabels],
-        raw[2][kMaxLabels];
+    __shared__ float su[kMaxLabels], sv[kMaxLabels], sy[2][kMaxLabels], sw[2][kMaxLabels];
+    __shared__ double raw[2][kMaxLabels];
     __shared__ double red[kVecThreads / kWave];
-    __shared__ float nrm[2];
+    __shared__ double nrm[2];
     const int64_t npairs = (a.N - 1 + 1) / 2;
     const int64_t b = blockIdx.x / npairs, k = blockIdx.x % npairs;
     const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
@@ -1981,13 +2106,15 @@ __global__ __launch_bounds__(kVecThreads) void k_form_log(FormArgs a) {
     const int64_t E = a.N - 1;
     const int64_t tL = 2 * k, tR = 2 * k + 1;
     const size_t CC = (size_t)C * C;
-    // padding edges are exactly zero
-    for (int64_t t = tL; t <= tR; ++t)
-        if (t < E && t >= Eb) {
-            float* o = a.marg + (size_t)(b * E + t) * CC;
-            for (size_t idx = threadIdx.x; idx < CC; idx += kVecThreads) o[idx] = 0.f;
-        }
+    // padding edges are exactly zero (written by the float32 formation's launch)
+    if (!kExact)
+        for (int64_t t = tL; t <= tR; ++t)
+            if (t < E && t >= Eb) {
+                float* o = a.marg + (size_t)(b * E + t) * CC;
+                for (size_t idx = threadIdx.x; idx < CC; idx += kVecThreads) o[idx] = 0.f;
+            }
     if (tL >= Eb) return;
+    if (pair_wide(a, b, E, tL, tR < Eb) != kExact) return;
     for (int i = threadIdx.x; i < C; i += kVecThreads) {
         su[i] = a.u1 ? a.u1[(size_t)(b * a.nodes1 + k) * C + i] : 0.f;
         sv[i] = a.v1 ? a.v1[(size_t)(b * a.nodes1 + k) * C + i] : 0.f;
@@ -1999,20 +2126,21 @@ __global__ __launch_bounds__(kVecThreads) void k_form_log(FormArgs a) {
     if (!right) {
         // a lone edge: n = LSE_{i,j} (u[i] + l[i][j] + v[j]) = LSE_j (y[j] + v[j]), y = u (x) leaf
         // (column pass only; the row half idles through the barriers)
-        half_vec<kVec>(threadIdx.x < kHalfThreads, leafL, nullptr, nullptr, C, su, sw[0], sy[0],
-                       red, raw[0]);
+        half_vec<kVec, kExact>(threadIdx.x < kHalfThreads, leafL, nullptr, nullptr, C, su, sw[0],
+                               sy[0], red, raw[0]);
         if (threadIdx.x < kWave) {
-            float m = -INFINITY, s = 0.f;
+            double m = -INFINITY;
+            float s = 0.f;
             for (int j = threadIdx.x; j < C; j += kWave) {
-                float x[1] = {raw[0][j] + sv[j]};
-                lse_fold<1>(m, s, x);
+                const double x[1] = {raw[0][j] + (double)sv[j]};
+                lse_fold_d<1>(m, s, x);
             }
-            const float mm = wave_max(m);
-            s = wave_sum(m == -INFINITY ? 0.f : s * fexp(m - safe_shift(mm)));
-            if (threadIdx.x == 0) nrm[0] = lse_val(mm, s);
+            const double mm = wave_max_d(m);
+            s = wave_sum(m == -INFINITY ? 0.f : s * fexp((float)(m - safe_shift_d(mm))));
+            if (threadIdx.x == 0) nrm[0] = lse_val_d(mm, s);
         }
         __syncthreads();
-        write_marginal<kVec>(leafL, su, sv, nrm[0], C, outL);
+        write_marginal<kVec, kExact>(leafL, su, sv, nrm[0], C, outL);
         return;
     }
     const float* leafR = a.pot + (size_t)(b * E + tR) * CC;
@@ -2020,23 +2148,24 @@ __global__ __launch_bounds__(kVecThreads) void k_form_log(FormArgs a) {
     // half 0: y = u (x) leaf_{2k} -> alpha_{2k+1} (sy[0]);  half 1: z = leaf_{2k+1} (x) v ->
     // beta_{2k+1} (sy[1]); raw[] keep the unshifted log-sum-exps
     const bool rowPass = threadIdx.x >= kHalfThreads;
-    half_vec<kVec>(true, rowPass ? leafR : leafL, nullptr, nullptr, C, rowPass ? sv : su,
-                   sw[rowPass], sy[rowPass], red, raw[rowPass]);
+    half_vec<kVec, kExact>(true, rowPass ? leafR : leafL, nullptr, nullptr, C, rowPass ? sv : su,
+                           sw[rowPass], sy[rowPass], red, raw[rowPass]);
     // n_{2k} = LSE_j (y[j] + beta_{2k+1}[j]) (wave 0);  n_{2k+1} = LSE_i (alpha_{2k+1}[i] + z[i]) (wave 1)
     const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     if (w < 2) {
-        float m = -INFINITY, s = 0.f;
+        double m = -INFINITY;
+        float s = 0.f;
         for (int j = lane; j < C; j += kWave) {
-            float x[1] = {w == 0 ? raw[0][j] + sy[1][j] : sy[0][j] + raw[1][j]};
-            lse_fold<1>(m, s, x);
+            const double x[1] = {w == 0 ? raw[0][j] + (double)sy[1][j] : (double)sy[0][j] + raw[1][j]};
+            lse_fold_d<1>(m, s, x);
         }
-        const float mm = wave_max(m);
-        s = wave_sum(m == -INFINITY ? 0.f : s * fexp(m - safe_shift(mm)));
-        if (lane == 0) nrm[w] = lse_val(mm, s);
+        const double mm = wave_max_d(m);
+        s = wave_sum(m == -INFINITY ? 0.f : s * fexp((float)(m - safe_shift_d(mm))));
+        if (lane == 0) nrm[w] = lse_val_d(mm, s);
     }
     __syncthreads();
-    write_marginal<kVec>(leafL, su, sy[1], nrm[0], C, outL);
-    write_marginal<kVec>(leafR, sy[0], sv, nrm[1], C, outR);
+    write_marginal<kVec, kExact>(leafL, su, sy[1], nrm[0], C, outL);
+    write_marginal<kVec, kExact>(leafR, sy[0], sv, nrm[1], C, outR);
 }
 
 template <int TM, bool VEC, bool kBits>
@@ -2089,7 +2218,7 @@ hipError_t up_sweep_vec(const Plan& p, const float* pot, const int32_t* lengths,
     if (e == hipSuccess && full128) e = allow_up_full_lds<128, kUpBf16>();
     if (e != hipSuccess) return e;
     // the leaves' row and column maxima (shifts of the level-1 products)
-    LeafMaxArgs m{pot, lengths, p.N, p.C, p.lrmax, p.lcmax, p.rbits[0], p.cbits[0], p.bw};
+    LeafMaxArgs m{pot, lengths, p.N, p.C, p.lrmax, p.lcmax, p.rbits[0], p.cbits[0], p.bw, p.wide};
     if (!kBits && p.C <= kLeafLdsMaxLabels) {
         const size_t lds = sizeof(float) * p.C * (p.C + 1);
         e = allow_leaf_lds<VEC>();
@@ -2208,18 +2337,24 @@ hipError_t launch_marginals_tree(const Plan& p, const float* pot, const int32_t*
     f.u1 = (p.D >= 2) ? p.u[1] : nullptr;
     f.v1 = (p.D >= 2) ? p.v[1] : nullptr;
     f.nodes1 = (p.D >= 1) ? (p.Np >> 1) : 1;
-    f.lengths = lengths; f.N = p.N; f.C = p.C; f.marg = marg;
+    f.lengths = lengths; f.N = p.N; f.C = p.C; f.marg = marg; f.wide = p.wide;
     const int64_t npairs = (p.N - 1 + 1) / 2;
     const dim3 grid((unsigned)(p.B * npairs));
-    // both leaves of a pair held in registers when they fit: one read of each edge
-    if (p.C % 4 == 0 && p.C <= 64)
-        hipLaunchKernelGGL(k_form_reg<2>, grid, dim3(kVecThreads), 0, s, f);
-    else if (p.C % 4 == 0 && p.C <= kRegMaxLabels)
-        hipLaunchKernelGGL(k_form_reg<8>, grid, dim3(kVecThreads), 0, s, f);
-    else if (p.C % 4 == 0)
-        hipLaunchKernelGGL(k_form_log<true>, grid, dim3(kVecThreads), 0, s, f);
-    else
-        hipLaunchKernelGGL(k_form_log<false>, grid, dim3(kVecThreads), 0, s, f);
+    // both leaves of a pair held in registers when they fit: one read of each edge.  One
+    // launch per formation (float32 terms, float64 terms for pairs of large magnitude).
+    if (p.C % 4 == 0 && p.C <= 64) {
+        hipLaunchKernelGGL((k_form_reg<2, false>), grid, dim3(kVecThreads), 0, s, f);
+        hipLaunchKernelGGL((k_form_reg<2, true>), grid, dim3(kVecThreads), 0, s, f);
+    } else if (p.C % 4 == 0 && p.C <= kRegMaxLabels) {
+        hipLaunchKernelGGL((k_form_reg<8, false>), grid, dim3(kVecThreads), 0, s, f);
+        hipLaunchKernelGGL((k_form_reg<8, true>), grid, dim3(kVecThreads), 0, s, f);
+    } else if (p.C % 4 == 0) {
+        hipLaunchKernelGGL((k_form_log<true, false>), grid, dim3(kVecThreads), 0, s, f);
+        hipLaunchKernelGGL((k_form_log<true, true>), grid, dim3(kVecThreads), 0, s, f);
+    } else {
+        hipLaunchKernelGGL((k_form_log<false, false>), grid, dim3(kVecThreads), 0, s, f);
+        hipLaunchKernelGGL((k_form_log<false, true>), grid, dim3(kVecThreads), 0, s, f);
+    }
     return hipGetLastError();
 }
 

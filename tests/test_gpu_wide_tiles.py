@@ -1,7 +1,8 @@
 """Parity of the multi-launch tree on shapes whose lower levels take the 128-wide output
 tiles of the log-semiring product (a level uses them when it has at least 512 such tiles),
 every marginal compared element by element: dense rows (C a multiple of 4, 16-byte loads)
-and odd label counts (scalar loads), ragged lengths and exact integer ties."""
+and odd label counts (scalar loads), ragged lengths, exact integer ties and a wide dynamic
+range."""
 import numpy as np
 import pytest
 
@@ -30,3 +31,12 @@ def test_wide_tiles_normal(B, N, C, lens):
 def test_wide_tiles_integer_ties(B, N, C, lens):
     pot, lens = W.random_case(4000 + N + C, B, N, C, kind="int", int_range=1, lengths=lens)
     check_all(pot, lens, f"wide tiles, ties B={B} N={N} C={C}")
+
+
+@pytest.mark.parametrize("B,N,C,lens", [(2, 600, 128, [600, 421]), (2, 200, 256, [200, 133])])
+def test_wide_tiles_wide_dynamic_range(B, N, C, lens):
+    # sigma 40 on shapes whose lower levels take the 128-wide full tiles (products from bf16
+    # parts): those must keep float32 precision, and sums below 2^-80 take the exact
+    # recomputation
+    pot, lens = W.random_case(5000 + N + C, B, N, C, sigma=40.0, lengths=lens)
+    check_all(pot, lens, f"wide tiles, sigma=40 B={B} N={N} C={C}")
