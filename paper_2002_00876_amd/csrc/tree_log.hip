@@ -1088,10 +1088,16 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
     // and the tile's row and column shifts; every global read of it goes out at once, after
     // the first slices' loads
     double coLshift = 0.0, roRshift = 0.0;
+    double lro_t = 0.0, rco_t = 0.0;   // ro_L of row a0 + tid, co_R of column c0 + tid (tid < TM)
     auto shifts = [&]() {
         static_assert(kMaxLabels <= kUpThreads, "one offset of the contracted index per thread");
+        static_assert(TM <= kUpThreads, "one output row and column per thread");
         const double lco = (Lco && tid < C) ? Lco[tid] : -INFINITY;
         const double rro = (Rro && tid < C) ? Rro[tid] : -INFINITY;
+        if (tid < TM) {   // (for the epilogue: read now, with the rest of the set-up)
+            lro_t = Lro ? Lro[a0 + tid] : 0.0;
+            rco_t = Rco ? Rco[c0 + tid] : 0.0;
+        }
         float pa = -INFINITY, pb = -INFINITY;
         if (tid < TM) {
             const float* p = a.cpmr + ((size_t)cl * C + a0 + tid) * cnt;
@@ -1472,13 +1478,13 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
         T[row * LDT + col] = val;
     }
     // the output node's offsets for the tile's rows and columns
-    for (int i = tid; i < TM; i += kUpThreads) {
-        const double ro = (Lro ? Lro[a0 + i] : 0.0) + coLshift + sa[i];
-        const double co = (Rco ? Rco[c0 + i] : 0.0) + roRshift + sb[i];
-        rof[i] = (float)ro;
-        cof[i] = (float)co;
-        if (tn == 0) Pro[a0 + i] = ro;
-        if (tm == 0) Pco[c0 + i] = co;
+    if (tid < TM) {
+        const double ro = lro_t + coLshift + sa[tid];
+        const double co = rco_t + roRshift + sb[tid];
+        rof[tid] = (float)ro;
+        cof[tid] = (float)co;
+        if (tn == 0) Pro[a0 + tid] = ro;
+        if (tm == 0) Pco[c0 + tid] = co;
     }
     __syncthreads();
     // partial maxima for the next level: thread t < TM row t, TM <= t < 2 TM column t - TM
