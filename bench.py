@@ -24,6 +24,10 @@ if ROOT not in sys.path:
 
 HBM_PEAK = 8.0e12          # bytes/s
 MFMA_F32_PEAK = 157.3e12   # flop/s, dense fp32 matrix
+MFMA_BF16_PEAK = 2.5e15    # flop/s, dense bf16 matrix
+# The tree's 128-wide full tiles (C a multiple of 128) multiply float32 operands as three bf16
+# parts each, six bf16 products per float32 product: their float32-equivalent peak
+MFMA_BF16X6_PEAK = MFMA_BF16_PEAK / 6
 # fp64 vector: 78.6 TFLOP/s counts an FMA as two flops, i.e. 256 CUs x 4 SIMDs x 16 lanes x
 # 2.4 GHz = 39.3e12 lane-instructions/s; a max-plus pair is two of them (add, max)
 VALU_F64_OPS_PEAK = 39.3e12
@@ -467,21 +471,27 @@ def main():
     # Roofline of the timed call.  On the single-launch path the marginals call is one
     # kernel (k_small_log); on the multi-launch tree it is a sequence of kernels whose bound
     # is the call's algorithmic work: read the valid edges and write all marginals (HBM),
-    # and 2 C^3 flop per tree product on the fp32 matrix cores (MFMA).  The binding resource
-    # is the one with the longer time at its peak.
+    # and 2 C^3 flop per tree product on the matrix cores (MFMA: fp32, or for C a multiple
+    # of 128 the six-product bf16 split at 2.5 PFLOP/s / 6).  The binding resource is the
+    # one with the longer time at its peak.
     fused = binding.workspace_bytes(binding.OP_MARGINALS, B, N, C) == 0
+    bf16x6 = not fused and C > 64 and C % 128 == 0
+    cmp_peak = MFMA_BF16X6_PEAK if bf16x6 else MFMA_F32_PEAK
 
     def roofline(kind, sec):
         if kind == "marginals":
-            t_mem, t_cmp = alg["marg_bytes"] / HBM_PEAK, alg["marg_flops"] / MFMA_F32_PEAK
+            t_mem, t_cmp = alg["marg_bytes"] / HBM_PEAK, alg["marg_flops"] / cmp_peak
             if t_mem >= t_cmp:
                 a = alg["marg_bytes"] / sec / 1e9
                 r = {"bound": "hbm", "achieved": round(a, 2), "peak": HBM_PEAK / 1e9,
                      "unit": "GB/s", "frac": round(a / (HBM_PEAK / 1e9), 5)}
             else:
                 a = alg["marg_flops"] / sec / 1e12
-                r = {"bound": "mfma", "achieved": round(a, 3), "peak": MFMA_F32_PEAK / 1e12,
-                     "unit": "TFLOP/s", "frac": round(a / (MFMA_F32_PEAK / 1e12), 5)}
+                r = {"bound": "mfma", "achieved": round(a, 3), "peak": round(cmp_peak / 1e12, 2),
+                     "unit": "TFLOP/s", "frac": round(a / (cmp_peak / 1e12), 5),
+                     "peak_note": ("bf16 dense 2500 TFLOP/s / 6: six bf16 products per float32 "
+                                   "product (three-part split of each operand)" if bf16x6 else
+                                   "fp32 dense MFMA")}
             r["algorithmic_bytes"] = alg["marg_bytes"]
             r["algorithmic_flops"] = alg["marg_flops"]
         else:
@@ -542,8 +552,9 @@ def main():
                       "whole_path_tokens_per_s": round(tokens / (ms_both * 1e-3), 1),
                       "valid_tokens_per_s": round(float(lens_h.sum()) / (ms_step * 1e-3), 1),
                       "viterbi_roofline": roof_v},
-        "dtype_note": "log semiring in fp32 (fp32 MFMA, float64 row/column offsets); "
-                      "Viterbi max-plus in float64",
+        "dtype_note": "log semiring in fp32 precision (products on the bf16 matrix cores from "
+                      "three-part bf16 splits of the fp32 operands for 128-wide tiles, fp32 MFMA "
+                      "elsewhere; float64 row/column offsets); Viterbi max-plus in float64",
         "paper_context": {"tokens_per_s": PAPER_CONTEXT_TOKENS_PER_S,
                           "note": "Table 1, K80, B=32 N=25 C=20; not the same metric"},
         "roofline": roof,

@@ -53,6 +53,11 @@ __device__ __forceinline__ float4 buffer_load4(__amdgpu_buffer_rsrc_t r, unsigne
     const v4i x = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
     return make_float4(__int_as_float(x.x), __int_as_float(x.y), __int_as_float(x.z), __int_as_float(x.w));
 }
+__device__ __forceinline__ void buffer_store4(float4 v, __amdgpu_buffer_rsrc_t r, unsigned voff, int soff) {
+    typedef int v4i __attribute__((ext_vector_type(4)));
+    const v4i x = {__float_as_int(v.x), __float_as_int(v.y), __float_as_int(v.z), __float_as_int(v.w)};
+    __builtin_amdgcn_raw_buffer_store_b128(x, r, voff, soff, 0);
+}
 __device__ __forceinline__ float buffer_load1(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff) {
     return __int_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
 }

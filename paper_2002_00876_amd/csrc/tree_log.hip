@@ -2064,6 +2064,182 @@ __global__ __launch_bounds__(kVecThreads) void k_form_reg(FormArgs a) {
     if (right) write(rv, ya, sv, nrm[1], a.marg + (size_t)(b * E + tR) * CC);
 }
 
+// The per-pair computation for C = 256, where two leaves do not fit a workgroup's registers:
+// the left leaf is held in registers (1024 threads, 64 values each) and read once, the right
+// one is streamed twice (once for its row pass, once for its marginals): 1.5 reads per edge
+// instead of 2.  Thread t = 64 w + g holds columns 4g .. 4g+3 of rows w + 16 q (q < 16), so
+// each row of a leaf is one wave's contiguous 1 KiB: the row pass of the right leaf reduces
+// within a wave, the column pass of the left leaf merges the 16 waves' states through LDS.
+constexpr int kBigLabels = 256;
+constexpr int kBigThreads = 1024;
+
+// (m, s) merged over the 64 lanes of a wave; value = m + log s, m = -inf: empty
+template <typename Tm>
+__device__ __forceinline__ void wave_lse_state(Tm& m, float& s) {
+#pragma unroll
+    for (int off = kWave / 2; off >= 1; off >>= 1) {
+        const Tm m2 = __shfl_xor(m, off, kWave);
+        const float s2 = __shfl_xor(s, off, kWave);
+        const Tm nm = m > m2 ? m : m2;
+        if (nm != (Tm)-INFINITY) {
+            s = (m == (Tm)-INFINITY ? 0.f : s * fexp((float)(m - nm))) +
+                (m2 == (Tm)-INFINITY ? 0.f : s2 * fexp((float)(m2 - nm)));
+            m = nm;
+        }
+    }
+}
+
+template <bool kExact>
+__global__ __launch_bounds__(kBigThreads) void k_form_big(FormArgs a) {
+    using Tm = std::conditional_t<kExact, double, float>;   // type of the formed terms
+    constexpr int C = kBigLabels, G = C / 4, kW = kBigThreads / kWave, kR = C / kW;
+    static_assert(G == kWave && kR * kW == C, "a row is one wave's 64 float4");
+    __shared__ float su[C], sv[C], ya[C], zb[C];
+    __shared__ double yraw[C], zraw[C];
+    __shared__ float pm[kW][C], ps[kW][C];
+    __shared__ double nrm[2];
+    const int64_t npairs = (a.N - 1 + 1) / 2;
+    const int64_t b = blockIdx.x / npairs, k = blockIdx.x % npairs;
+    const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
+    const int64_t E = a.N - 1;
+    const int64_t tL = 2 * k, tR = 2 * k + 1;
+    const size_t CC = (size_t)C * C;
+    const int tid = threadIdx.x, w = tid / kWave, g = tid % kWave, j = 4 * g;
+    if (!kExact)   // (padding edges once, by the float32 formation's launch)
+        for (int64_t t = tL; t <= tR; ++t)
+            if (t < E && t >= Eb) {
+                float4* o = reinterpret_cast<float4*>(a.marg + (size_t)(b * E + t) * CC);
+                for (int idx = tid; idx < C * G; idx += kBigThreads) o[idx] = make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+    if (tL >= Eb) return;
+    const bool right = tR < Eb;
+    if (pair_wide(a, b, E, tL, right) != kExact) return;
+    // raw buffer accesses: one 32-bit offset per thread (row w, column j), the row step
+    // 16 q in a scalar offset, so that no per-row address is kept in registers
+    const __amdgpu_buffer_rsrc_t rsL = make_rsrc(a.pot + (size_t)(b * E + tL) * CC, C * C);
+    const __amdgpu_buffer_rsrc_t rsR = make_rsrc(a.pot + (size_t)(b * E + (right ? tR : tL)) * CC, C * C);
+    const unsigned voff = 4u * (unsigned)(w * C + j);
+    constexpr int kRowStep = 4 * kW * C;   // bytes between a thread's rows
+    float4 lv[kR];
+#pragma unroll
+    for (int q = 0; q < kR; ++q) lv[q] = buffer_load4(rsL, voff, kRowStep * q);
+    if (tid < C) {
+        su[tid] = a.u1 ? a.u1[(size_t)(b * a.nodes1 + k) * C + tid] : 0.f;
+        sv[tid] = a.v1 ? a.v1[(size_t)(b * a.nodes1 + k) * C + tid] : 0.f;
+    }
+    __syncthreads();
+    // column pass of the left leaf: the thread's partial log-sum-exps of u[i] + l[i][j + c]
+    // over its 16 rows, four rows at a time straight from the registers, merged below over
+    // the 16 waves
+    {
+        Tm m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+        float sc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q0 = 0; q0 < kR; q0 += 4) {
+            Tm ui[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) ui[u] = su[w + kW * (q0 + u)];
+            const Tm x0[4] = {ui[0] + (Tm)lv[q0].x, ui[1] + (Tm)lv[q0 + 1].x, ui[2] + (Tm)lv[q0 + 2].x, ui[3] + (Tm)lv[q0 + 3].x};
+            const Tm x1[4] = {ui[0] + (Tm)lv[q0].y, ui[1] + (Tm)lv[q0 + 1].y, ui[2] + (Tm)lv[q0 + 2].y, ui[3] + (Tm)lv[q0 + 3].y};
+            const Tm x2[4] = {ui[0] + (Tm)lv[q0].z, ui[1] + (Tm)lv[q0 + 1].z, ui[2] + (Tm)lv[q0 + 2].z, ui[3] + (Tm)lv[q0 + 3].z};
+            const Tm x3[4] = {ui[0] + (Tm)lv[q0].w, ui[1] + (Tm)lv[q0 + 1].w, ui[2] + (Tm)lv[q0 + 2].w, ui[3] + (Tm)lv[q0 + 3].w};
+            lse_fold_t<4>(m[0], sc[0], x0);
+            lse_fold_t<4>(m[1], sc[1], x1);
+            lse_fold_t<4>(m[2], sc[2], x2);
+            lse_fold_t<4>(m[3], sc[3], x3);
+        }
+#pragma unroll
+        for (int c = 0; c < 4; ++c) lse_to_float(m[c], sc[c], pm[w][j + c], ps[w][j + c]);
+    }
+    // row pass of the right leaf (first read): z[i] = LSE_j r[i][j] + v[j], one wave per row
+    if (right) {
+        const Tm v0 = sv[j], v1 = sv[j + 1], v2 = sv[j + 2], v3 = sv[j + 3];
+        constexpr int kChunk = 4;   // rows of a wave in flight together
+#pragma unroll
+        for (int q0 = 0; q0 < kR; q0 += kChunk) {
+            float4 rv[kChunk];
+#pragma unroll
+            for (int q = 0; q < kChunk; ++q) rv[q] = buffer_load4(rsR, voff, kRowStep * (q0 + q));
+#pragma unroll
+            for (int q = 0; q < kChunk; ++q) {
+                const Tm r[4] = {(Tm)rv[q].x + v0, (Tm)rv[q].y + v1, (Tm)rv[q].z + v2, (Tm)rv[q].w + v3};
+                Tm m = -INFINITY;
+                float sm = 0.f;
+                lse_fold_t<4>(m, sm, r);
+                wave_lse_state(m, sm);
+                if (g == 0) zraw[w + kW * (q0 + q)] = m == (Tm)-INFINITY ? -INFINITY : (double)m + (double)flog(sm);
+            }
+        }
+    }
+    __syncthreads();
+    // merged: yraw[j] = LSE_i u[i] + l_{2k}[i][j]
+    if (tid < C) {
+        float m = -INFINITY, sm = 0.f;
+#pragma unroll
+        for (int r = 0; r < kW; ++r) lse_merge_into(m, sm, pm[r][tid], ps[r][tid]);
+        yraw[tid] = lse_val_d(m, sm);
+    }
+    __syncthreads();
+    // the messages shifted to max 0 (wave 0: alpha_{2k+1} from y, wave 1: beta_{2k+1} from z)
+    if (w < 2 && (w == 0 || right)) {
+        const double* src = w == 0 ? yraw : zraw;
+        double m = -INFINITY;
+        for (int i = g; i < C; i += kWave) m = fmax(m, src[i]);
+        m = safe_shift_d(wave_max_d(m));
+        float* dst = w == 0 ? ya : zb;
+        for (int i = g; i < C; i += kWave) dst[i] = (float)(src[i] - m);
+    }
+    __syncthreads();
+    // normalisers: n_{2k} = LSE_j yraw[j] + beta_{2k+1}[j] (or + v[j] without a right edge),
+    // n_{2k+1} = LSE_i alpha_{2k+1}[i] + zraw[i]
+    if (w < 2 && (w == 0 || right)) {
+        double m = -INFINITY;
+        float sm = 0.f;
+        for (int i = g; i < C; i += kWave) {
+            const double x[1] = {w == 0 ? yraw[i] + (double)(right ? zb[i] : sv[i]) : (double)ya[i] + zraw[i]};
+            lse_fold_d<1>(m, sm, x);
+        }
+        const double mm = wave_max_d(m);
+        sm = wave_sum(m == -INFINITY ? 0.f : sm * fexp((float)(m - safe_shift_d(mm))));
+        if (g == 0) nrm[w] = lse_val_d(mm, sm);
+    }
+    __syncthreads();
+    // the marginals: the left leaf from the registers, the right one streamed again
+    auto emit = [&](const float4& x, const float* be, double n, double al) {
+        if (n == -INFINITY) return make_float4(0.f, 0.f, 0.f, 0.f);
+        const Tm an = (Tm)(al - n);
+        float4 r;
+        r.x = fexp((float)(((Tm)x.x + (Tm)be[j]) + an));
+        r.y = fexp((float)(((Tm)x.y + (Tm)be[j + 1]) + an));
+        r.z = fexp((float)(((Tm)x.z + (Tm)be[j + 2]) + an));
+        r.w = fexp((float)(((Tm)x.w + (Tm)be[j + 3]) + an));
+        return r;
+    };
+    {
+        const __amdgpu_buffer_rsrc_t rsO = make_rsrc(a.marg + (size_t)(b * E + tL) * CC, C * C);
+        const double n = nrm[0];
+        const float* be = right ? zb : sv;
+#pragma unroll
+        for (int q = 0; q < kR; ++q)
+            buffer_store4(emit(lv[q], be, n, (double)su[w + kW * q]), rsO, voff, kRowStep * q);
+    }
+    if (right) {
+        const __amdgpu_buffer_rsrc_t rsO = make_rsrc(a.marg + (size_t)(b * E + tR) * CC, C * C);
+        const double n = nrm[1];
+        constexpr int kChunk = 4;
+#pragma unroll
+        for (int q0 = 0; q0 < kR; q0 += kChunk) {
+            float4 rv[kChunk];
+#pragma unroll
+            for (int q = 0; q < kChunk; ++q) rv[q] = buffer_load4(rsR, voff, kRowStep * (q0 + q));
+#pragma unroll
+            for (int q = 0; q < kChunk; ++q)
+                buffer_store4(emit(rv[q], sv, n, (double)ya[w + kW * (q0 + q)]), rsO, voff,
+                              kRowStep * (q0 + q));
+        }
+    }
+}
+
 // mu = exp(al[i] + leaf[i][j] + be[j] - n) over one C x C edge, the whole workgroup:
 // thread t takes column group t % G (16 bytes when kVec, else one float) of rows t / G,
 // t / G + T / G, ... so that each row is read and written contiguously
@@ -2354,6 +2530,10 @@ hipError_t launch_marginals_tree(const Plan& p, const float* pot, const int32_t*
     } else if (p.C % 4 == 0 && p.C <= kRegMaxLabels) {
         hipLaunchKernelGGL((k_form_reg<8, false>), grid, dim3(kVecThreads), 0, s, f);
         hipLaunchKernelGGL((k_form_reg<8, true>), grid, dim3(kVecThreads), 0, s, f);
+    } else if (p.C == kBigLabels) {
+        // (pairs of large magnitude: the two-read kernel, whose float64 terms fit its registers)
+        hipLaunchKernelGGL((k_form_big<false>), grid, dim3(kBigThreads), 0, s, f);
+        hipLaunchKernelGGL((k_form_log<true, true>), grid, dim3(kVecThreads), 0, s, f);
     } else if (p.C % 4 == 0) {
         hipLaunchKernelGGL((k_form_log<true, false>), grid, dim3(kVecThreads), 0, s, f);
         hipLaunchKernelGGL((k_form_log<true, true>), grid, dim3(kVecThreads), 0, s, f);
