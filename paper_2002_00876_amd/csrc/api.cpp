@@ -94,6 +94,24 @@ bool mul_ok(int64_t a, int64_t b, int64_t* out) {
 
 int report_error(int code, const char* msg) { return fail(code, msg); }
 
+// The level at which log Z's up-sweep stops for the recursion over its nodes, 0 for the tree
+// to the root.  A level of few small products costs about kLevelUs (its launch and memory
+// round trips), a step of the recursion about kStepUs: with S = 2^l edges per node, levels
+// 1..l and ceil(E / S) steps against D levels and the root's log-sum-exp.
+int node_scan_level(int64_t E, int D) {
+    constexpr double kLevelUs = 12.0, kStepUs = 1.0, kScanUs = 5.0, kRootUs = 10.0;
+    double best = D * kLevelUs + kRootUs;
+    int level = 0;
+    for (int l = 1; l < D; ++l) {
+        const double t = l * kLevelUs + (double)((E + (int64_t(1) << l) - 1) >> l) * kStepUs + kScanUs;
+        if (t < best) {
+            best = t;
+            level = l;
+        }
+    }
+    return level;
+}
+
 bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, bool masks) {
     *p = Plan{};
     p->B = B; p->N = N; p->C = C; p->E = N - 1; p->op = op;
@@ -152,7 +170,10 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p, boo
             p->bytes = (bump.off + kAlign - 1) / kAlign * kAlign;
             return true;
         }
-        for (int l = 1; l <= D; ++l) {
+        if (op == TS_OP_LOGPARTITION && !masks && C <= kNodeScanMaxLabels && D >= 2)
+            p->scan_level = node_scan_level(p->E, D);
+        const int top = p->scan_level > 0 ? p->scan_level : D;   // the levels formed
+        for (int l = 1; l <= top; ++l) {
             const size_t n = (size_t)B * (size_t)(Np >> l);
             const int tm = up_tile(C, (int64_t)n, masks);
             p->ntile[l] = (int)((C + tm - 1) / tm);

@@ -32,6 +32,9 @@ struct Plan {
     // u[lc], v[lc]) and k_chunk_form the marginals inside each chunk; no other level is formed
     bool chunk = false;
     int lc = 0;
+    // log Z on the tree (C <= kNodeScanMaxLabels, no masks): the up-sweep stops at this level
+    // and k_node_scan runs the recursion over its nodes (0: the tree up to the root)
+    int scan_level = 0;
     int32_t* clin = nullptr;   // per chunk node: its core holds S (1) or log S (0)
     // log semiring, levels 1..D (index by level)
     float* core[kMaxLevels] = {};
@@ -73,6 +76,7 @@ struct Plan {
 };
 
 constexpr int kChunkLog = 4;   // chunks of at most 16 edges
+constexpr int kNodeScanMaxLabels = 128;   // the recursion over nodes keeps two nodes in LDS
 
 // Potentials of magnitude above this make float32 rounding of a sum such as message +
 // potential (about 2^-24 of the magnitude per operation) approach the marginals' absolute
@@ -112,6 +116,7 @@ bool make_plan(int op, int64_t B, int64_t N, int64_t C, void* base, Plan* p,
 // ---- launchers (return the first HIP error, hipSuccess otherwise) ----
 hipError_t launch_logz_tree(const Plan& p, const float* pot, const int32_t* lengths,
                             float* logZ, hipStream_t s);
+hipError_t launch_node_scan(const Plan& p, const int32_t* lengths, float* logZ, hipStream_t s);
 hipError_t launch_marginals_tree(const Plan& p, const float* pot, const int32_t* lengths,
                                  float* marg, hipStream_t s);
 hipError_t launch_viterbi_tree(const Plan& p, const float* pot, const int32_t* lengths,

@@ -2412,7 +2412,8 @@ hipError_t up_sweep_vec(const Plan& p, const float* pot, const int32_t* lengths,
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    for (int l = 1; l <= p.D; ++l) {
+    const int top = p.scan_level > 0 ? p.scan_level : p.D;   // the levels formed
+    for (int l = 1; l <= top; ++l) {
         UpLogArgs a{};
         if (l == 1) {
             a.ccore = pot; a.cro = nullptr; a.cco = nullptr; a.cnodes = p.E;
@@ -2491,6 +2492,7 @@ hipError_t launch_logz_tree(const Plan& p, const float* pot, const int32_t* leng
     }
     hipError_t e = up_sweep(p, pot, lengths, s);
     if (e != hipSuccess || !logZ) return e;
+    if (p.scan_level > 0) return launch_node_scan(p, lengths, logZ, s);
     return root(p, pot, lengths, logZ, s);
 }
 

@@ -68,8 +68,12 @@ def test_workspace_sizes(L, monkeypatch):
     # longer sequences take chunks of at most 16 edges: N - 1 = 512 edges, 32 chunk nodes
     node = CW * CW * 4 + 2 * CW * 8          # core and the float64 row and column offsets
     assert 4 * 32 * node <= ws(0, 4, 513, CW) < 4 * 32 * node + 4096
-    # above 64 labels every level is stored
-    assert ws(0, 32, 25, 65) >= 32 * (16 + 8 + 4 + 2 + 1) * 65 * 65 * 4
+    # above 64 labels the marginals store every level; log Z with at most 128 labels stops
+    # the up-sweep where the recursion over the level's nodes is cheaper than the levels
+    # above it (here level 1: 16 nodes), above 128 labels it forms every level
+    assert ws(1, 32, 25, 65) >= 32 * (16 + 8 + 4 + 2 + 1) * 65 * 65 * 4
+    assert 32 * 16 * 65 * 65 * 4 <= ws(0, 32, 25, 65) < 32 * (16 + 8) * 65 * 65 * 4
+    assert ws(0, 32, 25, 130) >= 32 * (16 + 8 + 4 + 2 + 1) * 130 * 130 * 4
     assert ws(7, 32, 25, CW) == 0 and ws(0, 0, 25, 20) == 0 and ws(0, 1, 25, 257) == 0
     assert ws(6, 32, 25, CW) >= ws(1, 32, 25, CW) + 32 * 24 * CW * CW * 4
     # entropy: the marginals workspace, the marginals themselves and per-edge partials;
