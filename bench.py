@@ -108,6 +108,19 @@ def measured_traffic(kernel, workload):
     return None
 
 
+def node_scan_level(E, D):
+    """The level at which log Z's up-sweep stops for the recursion over that level's nodes
+    (at most 128 labels on the tree), 0 for the tree to the root; the same cost model as the
+    workspace plan (node_scan_level in paper_2002_00876_amd/csrc/api.cpp)."""
+    level_us, step_us, scan_us, root_us = 12.0, 1.0, 5.0, 10.0
+    best, level = D * level_us + root_us, 0
+    for l in range(1, D):
+        t = l * level_us + ((E + (1 << l) - 1) >> l) * step_us + scan_us
+        if t < best:
+            best, level = t, l
+    return level
+
+
 def code_hash(path):
     """sha256 of a source file's code: comments, blank lines and indentation removed, so
     that only a change to the code itself invalidates a stored measurement."""
@@ -179,13 +192,16 @@ def sweep(kind, reps=20):
         ms_scan = timed(lambda: binding.logpartition(pot, out=out, ws=ws))
         ms_seq = timed(lambda: binding.logpartition_sequential(pot, out=out))
         fused = binding.workspace_bytes(binding.OP_LOGPARTITION, B, N, C) == 0
+        D = max(0, (N - 2).bit_length())                     # levels above the N - 1 leaves
+        lscan = node_scan_level(N - 1, D) if 64 < C <= 128 and D >= 2 else 0
+        path = ("single launch" if fused else "chunks" if C <= 64 else
+                f"tree to level {lscan}, recursion over its nodes" if lscan else "multi-launch tree")
         tree_flop = 2 * B * max(N - 2, 0) * C ** 3           # tree products: 2 C^3 flop each
         serial_flop = 2 * B * (N - 1) * C ** 2              # left to right: 2 C^2 per step
         print(json.dumps({"sweep": kind, "B": B, "N": N, "C": C,
                           "tree_flop": tree_flop, "serial_flop": serial_flop,
                           "scan_ms": round(ms_scan, 5), "sequential_ms": round(ms_seq, 5),
-                          "scan_path": ("single launch" if fused else "chunks" if C <= 64
-                                        else "multi-launch tree"),
+                          "scan_path": path,
                           "scan_tokens_per_s": round(B * N / (ms_scan * 1e-3), 1),
                           "sequential_tokens_per_s": round(B * N / (ms_seq * 1e-3), 1),
                           "scan_speedup": round(ms_seq / ms_scan, 3)}), flush=True)

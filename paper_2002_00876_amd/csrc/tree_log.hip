@@ -189,6 +189,7 @@ __global__ __launch_bounds__(256) void k_leaf_max(LeafMaxArgs a) {
 // sequences of short chains -- bound by memory latency, not bandwidth.)
 constexpr int kLeafLdsMaxLabels = 128;
 constexpr int kLeafLdsThreads = 256;
+constexpr int64_t kLeafLdsMaxEdges = 8192;   // B * (N - 1) up to which it is used
 
 template <bool kVec>
 __global__ __launch_bounds__(kLeafLdsThreads) void k_leaf_max_lds(LeafMaxArgs a) {
@@ -2401,7 +2402,9 @@ hipError_t up_sweep_vec(const Plan& p, const float* pot, const int32_t* lengths,
     if (e != hipSuccess) return e;
     // the leaves' row and column maxima (shifts of the level-1 products)
     LeafMaxArgs m{pot, lengths, p.N, p.C, p.lrmax, p.lcmax, p.rbits[0], p.cbits[0], p.bw, p.wide};
-    if (!kBits && p.C <= kLeafLdsMaxLabels) {
+    // (the LDS-staged kernel for short batches, whose few workgroups are bound by memory
+    // latency; with many edges the streaming kernel keeps more bytes in flight per CU)
+    if (!kBits && p.C <= kLeafLdsMaxLabels && p.B * p.E <= kLeafLdsMaxEdges) {
         const size_t lds = sizeof(float) * p.C * (p.C + 1);
         e = allow_leaf_lds<VEC>();
         if (e != hipSuccess) return e;
