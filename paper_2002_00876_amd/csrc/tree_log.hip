@@ -951,7 +951,7 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log_small(UpLogArgs a) {
 // An operand is exp2(fma(x, log2 e, o log2 e) - s log2 e), the thread's shifts scaled once.
 template <int TM>
 struct UpFullSmem {
-    static constexpr int LDA = kSlice + 4, LDB = TM + 4, LDT = TM + 1;
+    static constexpr int LDA = kSlice + 4, LDB = TM + 4, LDT = TM + 8;
     static constexpr int kBuf = TM * LDA + kSlice * LDB;
     static constexpr int kTileF = TM * LDT;
     static constexpr int kMain = (2 * kBuf > kTileF ? 2 * kBuf : kTileF);
@@ -975,7 +975,7 @@ struct UpBfSmem {
     static constexpr int LDK = kK + 8;              // bf16 per staged line (48 bytes)
     static constexpr int kPlane = TM * LDK;         // bf16 per part plane
     static constexpr int kBufF = 6 * kPlane / 2;    // A and B, three parts each, in floats
-    static constexpr int LDT = TM + 1;
+    static constexpr int LDT = TM + 8;
     static constexpr int kTileF = TM * LDT;
     static constexpr int kMain = (2 * kBufF > kTileF ? 2 * kBufF : kTileF);
     static constexpr int kFloats = kMain + 4 * kMaxLabels + 4 * TM + 4 * (kUpThreads / kWave);
@@ -1491,9 +1491,13 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
     // partial maxima for the next level: thread t < TM row t, TM <= t < 2 TM column t - TM
     if (tid < TM) {
         float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-        for (int c = 0; c < TM; c += 4)
-#pragma unroll
-            for (int u = 0; u < 4; ++u) m[u] = fmaxf(m[u], T[tid * LDT + c + u] + cof[c + u]);
+        for (int c = 0; c < TM; c += 4) {   // (16-byte reads: the tile's rows are 16-byte aligned)
+            const float4 v = *(const float4*)(T + tid * LDT + c), o = *(const float4*)(cof + c);
+            m[0] = fmaxf(m[0], v.x + o.x);
+            m[1] = fmaxf(m[1], v.y + o.y);
+            m[2] = fmaxf(m[2], v.z + o.z);
+            m[3] = fmaxf(m[3], v.w + o.w);
+        }
         Pmr[(size_t)(a0 + tid) * nt + tn] = fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3]));
     } else if (tid < 2 * TM) {
         const int c = tid - TM;
@@ -1507,8 +1511,7 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
     constexpr int kQ = TM / 4;
     for (int idx = tid; idx < TM * kQ; idx += kUpThreads) {
         const int r = idx / kQ, c4 = idx % kQ;
-        const float* t = T + r * LDT + 4 * c4;
-        *(float4*)(Pc + (size_t)(a0 + r) * C + c0 + 4 * c4) = make_float4(t[0], t[1], t[2], t[3]);
+        *(float4*)(Pc + (size_t)(a0 + r) * C + c0 + 4 * c4) = *(const float4*)(T + r * LDT + 4 * c4);
     }
 }
 
