@@ -303,6 +303,28 @@ struct UpLogArgs {
     int64_t ngrid;        // node_grid(B * nodes, ntile^2)
 };
 
+// The largest partial maxima of two lines (cnt >= 1 partials each at p and at r).  The first four partials of both lines are loaded before any is used
+// (indexes past cnt - 1 repeat the last partial, which leaves a maximum unchanged), so the
+// usual case (at most four tiles per line in the child level) costs one memory round trip
+// instead of one per partial.
+constexpr int kPartialsAtOnce = 4;
+__device__ __forceinline__ void partials_max2(const float* p, const float* r, int cnt, float& mp,
+                                              float& mr) {
+    float vp[kPartialsAtOnce], vr[kPartialsAtOnce];
+#pragma unroll
+    for (int q = 0; q < kPartialsAtOnce; ++q) {
+        const int i = min(q, cnt - 1);
+        vp[q] = p[i];
+        vr[q] = r[i];
+    }
+    mp = fmaxf(fmaxf(vp[0], vp[1]), fmaxf(vp[2], vp[3]));
+    mr = fmaxf(fmaxf(vr[0], vr[1]), fmaxf(vr[2], vr[3]));
+    for (int q = kPartialsAtOnce; q < cnt; ++q) {
+        mp = fmaxf(mp, p[q]);
+        mr = fmaxf(mr, r[q]);
+    }
+}
+
 template <int TM>
 struct UpSmem {
     static constexpr int LDA = kSlice + 4, LDB = TM + 4, LDT = TM + 1;
@@ -472,13 +494,11 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log(UpLogArgs a) {
     const double lco = (Lco && tid < C) ? Lco[tid] : -INFINITY;
     const double rro = (Rro && tid < C) ? Rro[tid] : -INFINITY;
     float pa = -INFINITY, pb = -INFINITY;   // maxima of the partials of row a0 + tid, column c0 + tid
-    if (tid < TM && a0 + tid < C) {
-        const float* p = a.cpmr + ((size_t)cl * C + a0 + tid) * cnt;
-        for (int q = 0; q < cnt; ++q) pa = fmaxf(pa, p[q]);
-    }
-    if (tid < TM && c0 + tid < C) {
-        const float* p = a.cpmc + ((size_t)cr * C + c0 + tid) * cnt;
-        for (int q = 0; q < cnt; ++q) pb = fmaxf(pb, p[q]);
+    if (tid < TM) {   // (lines past C read line C - 1 and are discarded)
+        partials_max2(a.cpmr + ((size_t)cl * C + min(a0 + tid, C - 1)) * cnt,
+                      a.cpmc + ((size_t)cr * C + min(c0 + tid, C - 1)) * cnt, cnt, pa, pb);
+        if (a0 + tid >= C) pa = -INFINITY;
+        if (c0 + tid >= C) pb = -INFINITY;
     }
     // both maxima in one block reduction
     {
@@ -1100,12 +1120,9 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
             rco_t = Rco ? Rco[c0 + tid] : 0.0;
         }
         float pa = -INFINITY, pb = -INFINITY;
-        if (tid < TM) {
-            const float* p = a.cpmr + ((size_t)cl * C + a0 + tid) * cnt;
-            for (int q = 0; q < cnt; ++q) pa = fmaxf(pa, p[q]);
-            const float* r = a.cpmc + ((size_t)cr * C + c0 + tid) * cnt;
-            for (int q = 0; q < cnt; ++q) pb = fmaxf(pb, r[q]);
-        }
+        if (tid < TM)
+            partials_max2(a.cpmr + ((size_t)cl * C + a0 + tid) * cnt,
+                          a.cpmc + ((size_t)cr * C + c0 + tid) * cnt, cnt, pa, pb);
         {
             const double lw = wave_max_d(lco), rw = wave_max_d(rro);
             const int w = tid / kWave;
@@ -1259,9 +1276,12 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
         // the other buffer and slice s + 2 is loaded into the set just consumed (xa0/xb0).  After
         // the last slice the staging works on stale registers into a buffer nobody reads (no
         // branch, so the products and the staging form one block the scheduler can interleave).
+        // The loads are unconditional too (the last two slices reload the last one): a load
+        // behind a branch makes the compiler wait for every outstanding load where the set
+        // loaded the slice before is used, i.e. for the load just issued, every second slice.
         auto slice = [&](int s, int cur, float4 (&xa0)[NA], float4 (&xb0)[NB], float4 (&xa1)[NA],
                          float4 (&xb1)[NB]) {
-            if (s + 2 < nslices) gload(xa0, xb0, (s + 2) * kSlice);
+            gload(xa0, xb0, min(s + 2, nslices - 1) * kSlice);
             float oa[4], ob[4];
             offsets(oa, ob, min(s + 1, nslices - 1) * kSlice);
             lds_ops(av[0], bv[0], cur, 0);
@@ -1385,14 +1405,15 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
             }
         };
         // one slice: the products of buffer cur while slice s + 1 (raw set xa1/xb1) is staged into
-        // the other buffer and slice s + 2 is loaded into the set just consumed (xa0/xb0).  After
-        // the last slice the staging works on stale registers into a buffer nobody reads.  The
-        // six products of each block pair go out in six groups of BR x BR independent products
+        // the other buffer and slice s + 2 is loaded into the set just consumed (xa0/xb0; the
+        // last two slices reload the last one, without a branch: as in the float32 variant).
+        // After the last slice the staging works on stale registers into a buffer nobody reads.
+        // The six products of each block pair go out in six groups of BR x BR independent products
         // (different accumulators); one staging phase follows each group, fenced so that the
         // scheduler interleaves the two within the group but keeps the groups in order.
         auto slice = [&](int s, int cur, float4 (&xa0)[2], float (&xb0)[8], float4 (&xa1)[2],
                          float (&xb1)[8]) {
-            if (s + 2 < nslices) gload(xa0, xb0, (s + 2) * kK);
+            gload(xa0, xb0, min(s + 2, nslices - 1) * kK);
             bf16x8 A[3][BR], Bv[3][BR];
             operands(A, Bv, cur);
             StageRegs g;
