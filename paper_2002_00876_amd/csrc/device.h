@@ -165,6 +165,14 @@ __device__ __forceinline__ double safe_shift_d(double m) { return m == -INFINITY
 
 // Online log-sum-exp folded K values at a time: value = m + log(s), m = -inf while empty.
 // One exp per value plus one per chunk (the rescale of the running sum).
+// A double that every lane of the wave holds, moved to scalar registers (the first lane's)
+__device__ __forceinline__ double uniform_d(double x) {
+    const unsigned long long u = __double_as_longlong(x);
+    const unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)u);
+    const unsigned hi = __builtin_amdgcn_readfirstlane((unsigned)(u >> 32));
+    return __longlong_as_double(((unsigned long long)hi << 32) | lo);
+}
+
 template <int K>
 __device__ __forceinline__ void lse_fold(float& m, float& s, const float (&x)[K]) {
     float cm = x[0];

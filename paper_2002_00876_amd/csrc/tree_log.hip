@@ -973,12 +973,13 @@ template <int TM>
 struct UpFullSmem {
     static constexpr int LDA = kSlice + 4, LDB = TM + 4, LDT = TM + 8;
     static constexpr int kBuf = TM * LDA + kSlice * LDB;
-    static constexpr int kTileF = TM * LDT;
+    static constexpr int kTRows = TM;               // tile rows staged at once by the epilogue
+    static constexpr int kTileF = kTRows * LDT;
     static constexpr int kMain = (2 * kBuf > kTileF ? 2 * kBuf : kTileF);
-    // coh, roh, and both scaled by log2 e [kMaxLabels]; sa, sb, cof, rof [TM]; red [2 doubles
-    // per wave]
-    static constexpr int kFloats = kMain + 4 * kMaxLabels + 4 * TM + 4 * (kUpThreads / kWave);
+    // cohs, rohs [kMaxLabels]; sa, sb, cof, rof [TM]; red [2 doubles per wave]
+    static constexpr int kFloats = kMain + 2 * kMaxLabels + 4 * TM + 4 * (kUpThreads / kWave);
     static constexpr size_t kBytes = sizeof(float) * kFloats;
+    static constexpr int kBlocksPerCU = 2;
 };
 
 // The bf16 variant (kBf) stages each exponentiated operand x as three bf16 parts
@@ -989,18 +990,28 @@ struct UpFullSmem {
 // with the bf16 matrix instructions (32x32x16, float32 accumulation), which run 16 times the
 // float32 MFMA rate.  The three dropped products are below 2^-24 of |x y|, so a sum matches
 // the float32 product to float32 rounding.
+// Its LDS fits three workgroups per CU (52 KB each): staged lines of 32 bytes without
+// padding, the two 16-byte halves of line r swapped when bit 3 of r is set (so the 16 lanes
+// of a 16-byte access, rows r .. r + 15 of one half, hit distinct banks), and an epilogue
+// that stages the tile half by half.
 template <int TM>
 struct UpBfSmem {
     static constexpr int kK = 16;                   // contracted indices per slice
-    static constexpr int LDK = kK + 8;              // bf16 per staged line (48 bytes)
+    static constexpr int LDK = kK;                  // bf16 per staged line (32 bytes)
     static constexpr int kPlane = TM * LDK;         // bf16 per part plane
     static constexpr int kBufF = 6 * kPlane / 2;    // A and B, three parts each, in floats
     static constexpr int LDT = TM + 8;
-    static constexpr int kTileF = TM * LDT;
+    static constexpr int kTRows = TM / 2;
+    static constexpr int kTileF = kTRows * LDT;
     static constexpr int kMain = (2 * kBufF > kTileF ? 2 * kBufF : kTileF);
-    static constexpr int kFloats = kMain + 4 * kMaxLabels + 4 * TM + 4 * (kUpThreads / kWave);
+    static constexpr int kFloats = kMain + 2 * kMaxLabels + 4 * TM + 4 * (kUpThreads / kWave);
     static constexpr size_t kBytes = sizeof(float) * kFloats;
+    static constexpr int kBlocksPerCU = 3;
 };
+static_assert(3 * UpBfSmem<128>::kBytes <= 160 * 1024, "three workgroups per CU");
+
+// element offset of the 16-byte half h of staged line r (LDK = 16 bf16 per line)
+__device__ __forceinline__ int bf_line_half(int r, int h) { return r * 16 + 8 * (h ^ ((r >> 3) & 1)); }
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
@@ -1029,7 +1040,9 @@ __device__ __forceinline__ void split_bf16x3(const float (&x)[8], bf16x8& hi, bf
 }
 
 template <int TM, bool kBf>
-__global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
+__global__ __launch_bounds__(kUpThreads,
+                             (kBf ? UpBfSmem<TM>::kBlocksPerCU : UpFullSmem<TM>::kBlocksPerCU))
+void k_up_log_full(UpLogArgs a) {
     using Sm = std::conditional_t<kBf, UpBfSmem<TM>, UpFullSmem<TM>>;
     constexpr int LDT = Sm::LDT;
     constexpr int BR = TM / 64;                 // 32 x 32 blocks per wave per dimension
@@ -1095,27 +1108,28 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
     const double* Rro = a.cro ? a.cro + (size_t)cr * C : nullptr;
     const double* Rco = a.cco ? a.cco + (size_t)cr * C : nullptr;
 
-    float* coh = smem + Sm::kMain;       // [kMaxLabels] co_L - max co_L
-    float* roh = coh + kMaxLabels;       // [kMaxLabels] ro_R - max ro_R
-    float* cohs = roh + kMaxLabels;      // [kMaxLabels] coh log2 e
-    float* rohs = cohs + kMaxLabels;     // [kMaxLabels] roh log2 e
+    float* cohs = smem + Sm::kMain;      // [kMaxLabels] (co_L - max co_L) log2 e
+    float* rohs = cohs + kMaxLabels;     // [kMaxLabels] (ro_R - max ro_R) log2 e
     float* sa = rohs + kMaxLabels;       // [TM] row shifts of the tile
     float* sb = sa + TM;                 // [TM] column shifts
     float* cof = sb + TM;                // [TM] co_P of the tile's columns (float)
     float* rof = cof + TM;               // [TM] ro_P of the tile's rows (float)
     double* red = reinterpret_cast<double*>(rof + TM);
 
-    // the offsets of the contracted index shifted to max 0 (coh, roh and both scaled by log2 e)
+    // the offsets of the contracted index shifted to max 0, scaled by log2 e (cohs, rohs)
     // and the tile's row and column shifts; every global read of it goes out at once, after
     // the first slices' loads
     double coLshift = 0.0, roRshift = 0.0;
-    double lro_t = 0.0, rco_t = 0.0;   // ro_L of row a0 + tid, co_R of column c0 + tid (tid < TM)
+    // ro_L of the tile's row and co_R of its column handled by this thread in the epilogue
+    // (float32 variant: read with the set-up; bf16: after the products, which hold more
+    // registers)
+    double lro_t = 0.0, rco_t = 0.0;
     auto shifts = [&]() {
         static_assert(kMaxLabels <= kUpThreads, "one offset of the contracted index per thread");
         static_assert(TM <= kUpThreads, "one output row and column per thread");
         const double lco = (Lco && tid < C) ? Lco[tid] : -INFINITY;
         const double rro = (Rro && tid < C) ? Rro[tid] : -INFINITY;
-        if (tid < TM) {   // (for the epilogue: read now, with the rest of the set-up)
+        if (!kBf && tid < TM) {
             lro_t = Lro ? Lro[a0 + tid] : 0.0;
             rco_t = Rco ? Rco[c0 + tid] : 0.0;
         }
@@ -1138,13 +1152,12 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
             lmax = fmax(lmax, red[2 * w]);
             rmax = fmax(rmax, red[2 * w + 1]);
         }
-        coLshift = Lco ? safe_shift_d(lmax) : 0.0;
-        roRshift = Rro ? safe_shift_d(rmax) : 0.0;
+        // (the same for every thread: kept in scalar registers through the products)
+        coLshift = uniform_d(Lco ? safe_shift_d(lmax) : 0.0);
+        roRshift = uniform_d(Rro ? safe_shift_d(rmax) : 0.0);
         if (tid < C) {
             const float ch = Lco ? (float)(lco - coLshift) : 0.f;
             const float rh = Rro ? (float)(rro - roRshift) : 0.f;
-            coh[tid] = ch;
-            roh[tid] = rh;
             cohs[tid] = ch * kL2E;
             rohs[tid] = rh * kL2E;
         }
@@ -1367,7 +1380,8 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
         auto stage_store = [&](const StageRegs& g, int side, int buf) {
             bf16x8 h, m, l;
             split_bf16x3(g.x, h, m, l);
-            __bf16* d = hsm + buf * kBufH + (side ? 3 * PL + bcol * LDK + kb : ar * LDK + ka);
+            __bf16* d = hsm + buf * kBufH + (side ? 3 * PL + bf_line_half(bcol, kb >> 3)
+                                                  : bf_line_half(ar, ka >> 3));
             *(bf16x8*)(d) = h;
             *(bf16x8*)(d + PL) = m;
             *(bf16x8*)(d + 2 * PL) = l;
@@ -1390,19 +1404,20 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
         __syncthreads();
 
         // ---- products: wave (wm, wn) owns rows wm*QW.., columns wn*QW.. as BR x BR blocks;
-        // lane l supplies row (column) l % 32 at contracted indices 8 (l / 32) .. + 7
-        const int li = lane & 31, lh = 8 * (lane >> 5);
-        auto operands = [&](bf16x8 (&A)[3][BR], bf16x8 (&Bv)[3][BR], int buf) {
-            const __bf16* base = hsm + buf * kBufH;
+        // lane l supplies row (column) l % 32 at contracted indices 8 (l / 32) .. + 7 (the
+        // lines' bit 3 is that of l % 32, as QW and 32 are multiples of 16)
+        const int li = lane & 31;
+        const int aoff = bf_line_half(wm * QW + li, lane >> 5), boff = bf_line_half(wn * QW + li, lane >> 5);
+        // part p of A (of B) for the wave's BR blocks
+        auto read_a = [&](bf16x8 (&A)[BR], int buf, int p) {
 #pragma unroll
-            for (int p = 0; p < 3; ++p) {
+            for (int i = 0; i < BR; ++i)
+                A[i] = *(const bf16x8*)(hsm + buf * kBufH + p * PL + aoff + i * 32 * LDK);
+        };
+        auto read_b = [&](bf16x8 (&Bv)[BR], int buf, int p) {
 #pragma unroll
-                for (int i = 0; i < BR; ++i)
-                    A[p][i] = *(const bf16x8*)(base + p * PL + (wm * QW + i * 32 + li) * LDK + lh);
-#pragma unroll
-                for (int j = 0; j < BR; ++j)
-                    Bv[p][j] = *(const bf16x8*)(base + (3 + p) * PL + (wn * QW + j * 32 + li) * LDK + lh);
-            }
+            for (int j = 0; j < BR; ++j)
+                Bv[j] = *(const bf16x8*)(hsm + buf * kBufH + (3 + p) * PL + boff + j * 32 * LDK);
         };
         // one slice: the products of buffer cur while slice s + 1 (raw set xa1/xb1) is staged into
         // the other buffer and slice s + 2 is loaded into the set just consumed (xa0/xb0; the
@@ -1414,8 +1429,13 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
         auto slice = [&](int s, int cur, float4 (&xa0)[2], float (&xb0)[8], float4 (&xa1)[2],
                          float (&xb1)[8]) {
             gload(xa0, xb0, min(s + 2, nslices - 1) * kK);
+            // the operands of the first two groups now, those of the other four during the
+            // first group (fewer registers held at once)
             bf16x8 A[3][BR], Bv[3][BR];
-            operands(A, Bv, cur);
+            read_a(A[2], cur, 2);
+            read_b(Bv[0], cur, 0);
+            read_a(A[0], cur, 0);
+            read_b(Bv[2], cur, 2);
             StageRegs g;
             // (part of A, part of B): the smaller products first
             constexpr int kTerms[6][2] = {{2, 0}, {0, 2}, {1, 1}, {1, 0}, {0, 1}, {0, 0}};
@@ -1429,6 +1449,8 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
             };
             const int ks1 = min(s + 1, nslices - 1) * kK;
             term(0);
+            read_a(A[1], cur, 1);
+            read_b(Bv[1], cur, 1);
             stage_offsets(g, ks1);
             __builtin_amdgcn_sched_barrier(0);
             term(1);
@@ -1451,89 +1473,118 @@ __global__ __launch_bounds__(kUpThreads, 2) void k_up_log_full(UpLogArgs a) {
             slice(s + 1, 1, ra[1], rb[1], ra[0], rb[0]);
         }
     }
-    // ---- epilogue: core = log S into an LDS tile; entries whose S underflowed are
-    // recomputed afterwards by a direct log-sum-exp (a rare, non-unrolled path)
-    float* T = smem;   // [TM][LDT], over the slice buffers (all reads are done)
-    float smin = INFINITY;   // the lane's smallest sum: one compare per entry on the hot path
+    // ---- epilogue: core = log S through an LDS tile of kTRows rows (the whole tile, or for
+    // the bf16 variant one half at a time: the waves whose rows it holds write it); entries
+    // whose S underflowed are recomputed by a direct log-sum-exp (a rare, non-unrolled path)
+    constexpr int kTRows = Sm::kTRows, kPasses = TM / kTRows;
+    static_assert(kPasses == 1 || kTRows == QW, "a pass holds whole wave rows");
+    float* T = smem;   // [kTRows][LDT], over the slice buffers (all reads are done)
+    // the output node's offsets for the tile's rows and columns: thread TM + t (or t for a
+    // single pass) takes row and column t, during the first pass (whose tile rows belong to
+    // the other waves) when there are two
+    const int ot = kPasses == 1 ? tid : tid - TM;
+    const bool oth = ot >= 0 && ot < TM;
+    if (kPasses != 1 && oth) {
+        lro_t = Lro ? Lro[a0 + ot] : 0.0;
+        rco_t = Rco ? Rco[c0 + ot] : 0.0;
+    }
+    auto offsets = [&]() {
+        if (oth) {
+            const double ro = lro_t + coLshift + sa[ot];
+            const double co = rco_t + roRshift + sb[ot];
+            rof[ot] = (float)ro;
+            cof[ot] = (float)co;
+            if (tn == 0) Pro[a0 + ot] = ro;
+            if (tm == 0) Pco[c0 + ot] = co;
+        }
+    };
+    static_assert(kPasses == 1 || TM == 2 * QW, "the second half's waves are threads TM ..");
+    if (kPasses == 1) offsets();
+    float cm[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};   // column maxima (TM <= tid < 2 TM)
+    for (int h = 0; h < kPasses; ++h) {
+        const int rb = h * kTRows;   // first tile row held in T
+        if (kPasses == 1 || wm == h) {
+            float smin = INFINITY;   // the lane's smallest sum: one compare per entry on the hot path
 #pragma unroll
-    for (int i = 0; i < BR; ++i)
+            for (int i = 0; i < BR; ++i)
 #pragma unroll
-        for (int j = 0; j < BR; ++j)
+                for (int j = 0; j < BR; ++j)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
+                    for (int r = 0; r < 16; ++r) {
+                        const int row = wm * QW + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+                        const int col = wn * QW + j * 32 + (lane & 31);
+                        const float S = acc[i][j][r];
+                        T[(row - rb) * LDT + col] = flog(S);
+                        smin = fminf(smin, S);
+                    }
+            uint64_t under = 0;
+            if (!(smin >= kUnderflow)) {
+                // rare: which entries underflowed
+#pragma unroll
+                for (int i = 0; i < BR; ++i)
+#pragma unroll
+                    for (int j = 0; j < BR; ++j)
+#pragma unroll
+                        for (int r = 0; r < 16; ++r)
+                            if (!(acc[i][j][r] >= kUnderflow)) under |= 1ull << ((i * BR + j) * 16 + r);
+            }
+            while (under) {
+                const int bit = __builtin_ctzll(under);
+                under &= under - 1;
+                const int ij = bit >> 4, r = bit & 15, i = ij / BR, j = ij % BR;
                 const int row = wm * QW + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
                 const int col = wn * QW + j * 32 + (lane & 31);
-                const float S = acc[i][j][r];
-                T[row * LDT + col] = flog(S);
-                smin = fminf(smin, S);
+                const int gr = a0 + row, gc = c0 + col;
+                const float sr = sa[row], sc = sb[col];
+                const float* lrow = Lc + (size_t)gr * C;
+                // one term of the sum, with the contracted index's offsets formed as the staging
+                // formed them (before the log2 e scale)
+                auto fb_term = [&](int bb) {
+                    const float ch = Lco ? (float)(Lco[bb] - coLshift) : 0.f;
+                    const float rh = Rro ? (float)(Rro[bb] - roRshift) : 0.f;
+                    return (lrow[bb] + ch - sr) + (Rc[(size_t)bb * C + gc] + rh - sc);
+                };
+                float q = -INFINITY;
+                for (int bb = 0; bb < C; ++bb) q = fmaxf(q, fb_term(bb));
+                float val = -INFINITY;
+                if (q != -INFINITY) {
+                    float sum = 0.f;
+                    for (int bb = 0; bb < C; ++bb) sum += fexp(fb_term(bb) - q);
+                    val = q + flog(sum);
+                }
+                T[(row - rb) * LDT + col] = val;
             }
-    uint64_t under = 0;
-    if (!(smin >= kUnderflow)) {
-        // rare: which entries underflowed
-#pragma unroll
-        for (int i = 0; i < BR; ++i)
-#pragma unroll
-            for (int j = 0; j < BR; ++j)
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    if (!(acc[i][j][r] >= kUnderflow)) under |= 1ull << ((i * BR + j) * 16 + r);
-    }
-    while (under) {
-        const int bit = __builtin_ctzll(under);
-        under &= under - 1;
-        const int ij = bit >> 4, r = bit & 15, i = ij / BR, j = ij % BR;
-        const int row = wm * QW + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        const int col = wn * QW + j * 32 + (lane & 31);
-        const int gr = a0 + row, gc = c0 + col;
-        const float sr = sa[row], sc = sb[col];
-        const float* lrow = Lc + (size_t)gr * C;
-        float q = -INFINITY;
-        for (int bb = 0; bb < C; ++bb)
-            q = fmaxf(q, (lrow[bb] + coh[bb] - sr) + (Rc[(size_t)bb * C + gc] + roh[bb] - sc));
-        float val = -INFINITY;
-        if (q != -INFINITY) {
-            float sum = 0.f;
-            for (int bb = 0; bb < C; ++bb)
-                sum += fexp((lrow[bb] + coh[bb] - sr) + (Rc[(size_t)bb * C + gc] + roh[bb] - sc) - q);
-            val = q + flog(sum);
         }
-        T[row * LDT + col] = val;
-    }
-    // the output node's offsets for the tile's rows and columns
-    if (tid < TM) {
-        const double ro = lro_t + coLshift + sa[tid];
-        const double co = rco_t + roRshift + sb[tid];
-        rof[tid] = (float)ro;
-        cof[tid] = (float)co;
-        if (tn == 0) Pro[a0 + tid] = ro;
-        if (tm == 0) Pco[c0 + tid] = co;
-    }
-    __syncthreads();
-    // partial maxima for the next level: thread t < TM row t, TM <= t < 2 TM column t - TM
-    if (tid < TM) {
-        float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-        for (int c = 0; c < TM; c += 4) {   // (16-byte reads: the tile's rows are 16-byte aligned)
-            const float4 v = *(const float4*)(T + tid * LDT + c), o = *(const float4*)(cof + c);
-            m[0] = fmaxf(m[0], v.x + o.x);
-            m[1] = fmaxf(m[1], v.y + o.y);
-            m[2] = fmaxf(m[2], v.z + o.z);
-            m[3] = fmaxf(m[3], v.w + o.w);
-        }
-        Pmr[(size_t)(a0 + tid) * nt + tn] = fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3]));
-    } else if (tid < 2 * TM) {
-        const int c = tid - TM;
-        float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-        for (int r = 0; r < TM; r += 4)
+        if (kPasses != 1 && h == 0) offsets();
+        __syncthreads();
+        // partial maxima for the next level: thread t < kTRows row rb + t; TM <= t < 2 TM
+        // column t - TM (over the passes)
+        if (tid < kTRows) {
+            float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+            for (int c = 0; c < TM; c += 4) {   // (16-byte reads: the tile's rows are 16-byte aligned)
+                const float4 v = *(const float4*)(T + tid * LDT + c), o = *(const float4*)(cof + c);
+                m[0] = fmaxf(m[0], v.x + o.x);
+                m[1] = fmaxf(m[1], v.y + o.y);
+                m[2] = fmaxf(m[2], v.z + o.z);
+                m[3] = fmaxf(m[3], v.w + o.w);
+            }
+            Pmr[(size_t)(a0 + rb + tid) * nt + tn] = fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3]));
+        } else if (tid >= TM && tid < 2 * TM) {
+            const int c = tid - TM;
+            for (int r = 0; r < kTRows; r += 4)
 #pragma unroll
-            for (int u = 0; u < 4; ++u) m[u] = fmaxf(m[u], T[(r + u) * LDT + c] + rof[r + u]);
-        Pmc[(size_t)(c0 + c) * nt + tm] = fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3]));
+                for (int u = 0; u < 4; ++u) cm[u] = fmaxf(cm[u], T[(r + u) * LDT + c] + rof[rb + r + u]);
+        }
+        // the rows held, 16 bytes per store
+        constexpr int kQ = TM / 4;
+        for (int idx = tid; idx < kTRows * kQ; idx += kUpThreads) {
+            const int r = idx / kQ, c4 = idx % kQ;
+            *(float4*)(Pc + (size_t)(a0 + rb + r) * C + c0 + 4 * c4) = *(const float4*)(T + r * LDT + 4 * c4);
+        }
+        if (h + 1 < kPasses) __syncthreads();
     }
-    // the tile, row by row, 16 bytes per store
-    constexpr int kQ = TM / 4;
-    for (int idx = tid; idx < TM * kQ; idx += kUpThreads) {
-        const int r = idx / kQ, c4 = idx % kQ;
-        *(float4*)(Pc + (size_t)(a0 + r) * C + c0 + 4 * c4) = *(const float4*)(T + r * LDT + 4 * c4);
-    }
+    if (tid >= TM && tid < 2 * TM)
+        Pmc[(size_t)(c0 + tid - TM) * nt + tm] = fmaxf(fmaxf(cm[0], cm[1]), fmaxf(cm[2], cm[3]));
 }
 
 // ---------------------------------------------------------------- root: log Z
