@@ -79,7 +79,10 @@ __global__ __launch_bounds__(kMThreads) void k_up_max_narrow(UpMaxArgs a) {
         }
         return;
     }
-    const int ty = tid / 16, tx = tid % 16;   // 4 x 4 outputs per thread
+    // 4 x 4 outputs per thread: rows ty * 4 .. + 3; columns in pairs, 2 tx + 32 m + {0, 1}
+    // (m = 0, 1), so that the 16 lanes of a 16-byte operand read cover 256 contiguous bytes
+    // (no bank conflicts) and a store of a pair by 16 lanes covers 256 contiguous bytes
+    const int ty = tid / 16, tx = tid % 16;
     double acc[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -122,9 +125,12 @@ __global__ __launch_bounds__(kMThreads) void k_up_max_narrow(UpMaxArgs a) {
         for (int kk = 0; kk < kMK; ++kk) {
             double av[4], bv[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                av[i] = As[kk][ty * 4 + i];
-                bv[i] = Bs[kk][tx * 4 + i];
+            for (int i = 0; i < 4; ++i) av[i] = As[kk][ty * 4 + i];
+#pragma unroll
+            for (int m = 0; m < 2; ++m) {
+                const double2 b2 = *(const double2*)&Bs[kk][32 * m + 2 * tx];
+                bv[2 * m] = b2.x;
+                bv[2 * m + 1] = b2.y;
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i)
@@ -137,37 +143,36 @@ __global__ __launch_bounds__(kMThreads) void k_up_max_narrow(UpMaxArgs a) {
             __syncthreads();
         }
     }
-    // 16-byte stores of a lane's four columns when they lie inside the matrix (even C)
-    const int64_t cb = c0 + tx * 4;
-    const bool wide = cb + 4 <= C && (C % 2) == 0;
+    // 16-byte stores of a lane's column pairs when they lie inside the matrix (even C)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int64_t r = a0 + ty * 4 + i;
         if (r >= C) continue;
-        double* row = P + r * C + cb;
-        if (wide) {
+        double* row = P + r * C;
 #pragma unroll
-            for (int j = 0; j < 4; j += 2) {
+        for (int m = 0; m < 2; ++m) {
+            const int64_t cb = c0 + 32 * m + 2 * tx;
+            if (cb + 2 <= C && (C % 2) == 0) {
                 double2 v;
-                v.x = acc[i][j];
-                v.y = acc[i][j + 1];
-                *(double2*)(row + j) = v;
+                v.x = acc[i][2 * m];
+                v.y = acc[i][2 * m + 1];
+                *(double2*)(row + cb) = v;
+            } else {
+                if (cb < C) row[cb] = acc[i][2 * m];
+                if (cb + 1 < C) row[cb + 1] = acc[i][2 * m + 1];
             }
-        } else {
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (cb + j < C) row[j] = acc[i][j];
         }
     }
 }
 
 // One tree level of the max-plus up-sweep, P[a][c] = max_b L[a][b] + R[b][c], for one TM x TM
-// output tile per workgroup of (TM/8)^2 threads, each holding an 8 x 8 block of float64
-// accumulators (64 add + 64 max per 16 operand reads from LDS).  The contraction index runs
-// in slices of KS: A is staged transposed, As[k][row] (rows padded to TM + 2 doubles, which
-// keeps the 16-byte operand reads aligned and spreads the transposing stores over the
-// banks), B as is, Bs[k][col]; the next slice's global loads are in flight while the current
-// one is used (kLeaf: level 1, whose fp32 potentials are widened when they are staged).
+// output tile per workgroup of (TM/8)^2 threads, each holding 8 x 8 float64 accumulators
+// (8 rows; 8 columns as 4 interleaved pairs; 64 add + 64 max per 16 operands read from LDS).
+// The contraction index runs in slices of KS: A is staged transposed, As[k][row] (rows padded
+// to TM + 2 doubles, which keeps the 16-byte operand reads aligned and spreads the
+// transposing stores over the banks), B as is, Bs[k][col]; the next slice's global loads are
+// in flight while the current one is used (kLeaf: level 1, whose fp32 potentials are widened
+// when they are staged).
 template <int TM, int KS, bool kLeaf>
 __global__ __launch_bounds__((TM / 8) * (TM / 8)) void k_up_max(UpMaxArgs a) {
     constexpr int TPD = TM / 8, NT = TPD * TPD, LDA = TM + 2;
@@ -221,6 +226,11 @@ __global__ __launch_bounds__((TM / 8) * (TM / 8)) void k_up_max(UpMaxArgs a) {
             Bs[idx] = (double)rb[v];
         }
     };
+    // 8 x 8 outputs per thread: rows ty * 8 .. + 7; columns in pairs, 2 tx + GW m + {0, 1}
+    // (m = 0 .. 3, GW = 2 TPD), so that the TPD lanes of a 16-byte operand read cover
+    // contiguous bytes (no bank conflicts) and so do the TPD lanes of a pair's store
+    constexpr int GW = 2 * TPD;
+    static_assert(4 * GW == TM, "four column groups of 2 TPD");
     const int ty = tid / TPD, tx = tid % TPD;
     double acc[8][8];
 #pragma unroll
@@ -237,9 +247,12 @@ __global__ __launch_bounds__((TM / 8) * (TM / 8)) void k_up_max(UpMaxArgs a) {
         for (int kk = 0; kk < KS; ++kk) {
             double av[8], bv[8];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                av[i] = As[kk * LDA + ty * 8 + i];
-                bv[i] = Bs[kk * TM + tx * 8 + i];
+            for (int i = 0; i < 8; ++i) av[i] = As[kk * LDA + ty * 8 + i];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const double2 b2 = *(const double2*)(Bs + kk * TM + GW * m + 2 * tx);
+                bv[2 * m] = b2.x;
+                bv[2 * m + 1] = b2.y;
             }
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
@@ -256,27 +269,25 @@ __global__ __launch_bounds__((TM / 8) * (TM / 8)) void k_up_max(UpMaxArgs a) {
             __syncthreads();
         }
     }
-    // a lane's eight columns of a row are contiguous: 16-byte stores when they all lie inside
-    // the matrix and start on a 16-byte boundary (even C), single stores at the edges
-    const int cb = c0 + tx * 8;
-    const bool wide = cb + 8 <= C && (C % 2) == 0;
+    // a lane's column pairs: 16-byte stores when a pair lies inside the matrix and starts on
+    // a 16-byte boundary (even C), single stores at the edges
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         const int r = a0 + ty * 8 + i;
         if (r >= C) continue;
-        double* row = P + (size_t)r * C + cb;
-        if (wide) {
+        double* row = P + (size_t)r * C;
 #pragma unroll
-            for (int j = 0; j < 8; j += 2) {
+        for (int m = 0; m < 4; ++m) {
+            const int cb = c0 + GW * m + 2 * tx;
+            if (cb + 2 <= C && (C % 2) == 0) {
                 double2 v;
-                v.x = acc[i][j];
-                v.y = acc[i][j + 1];
-                *(double2*)(row + j) = v;
+                v.x = acc[i][2 * m];
+                v.y = acc[i][2 * m + 1];
+                *(double2*)(row + cb) = v;
+            } else {
+                if (cb < C) row[cb] = acc[i][2 * m];
+                if (cb + 1 < C) row[cb + 1] = acc[i][2 * m + 1];
             }
-        } else {
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-                if (cb + j < C) row[j] = acc[i][j];
         }
     }
 }
