@@ -991,9 +991,10 @@ struct UpFullSmem {
 // float32 MFMA rate.  The three dropped products are below 2^-24 of |x y|, so a sum matches
 // the float32 product to float32 rounding.
 // Its LDS fits three workgroups per CU (52 KB each): staged lines of 32 bytes without
-// padding, the two 16-byte halves of line r swapped when bit 3 of r is set (so the 16 lanes
-// of a 16-byte access, rows r .. r + 15 of one half, hit distinct banks), and an epilogue
-// that stages the tile half by half.
+// padding, the two 16-byte halves of line r swapped when bit 2 xor bit 3 of r is set (so
+// that rows r .. r + 7 and r .. r + 15 of one half, aligned, land on distinct 16-byte bank
+// groups, whether a 16-byte access is served 8 or 16 lanes at a time), and an epilogue that
+// stages the tile half by half.
 template <int TM>
 struct UpBfSmem {
     static constexpr int kK = 16;                   // contracted indices per slice
@@ -1011,7 +1012,9 @@ struct UpBfSmem {
 static_assert(3 * UpBfSmem<128>::kBytes <= 160 * 1024, "three workgroups per CU");
 
 // element offset of the 16-byte half h of staged line r (LDK = 16 bf16 per line)
-__device__ __forceinline__ int bf_line_half(int r, int h) { return r * 16 + 8 * (h ^ ((r >> 3) & 1)); }
+__device__ __forceinline__ int bf_line_half(int r, int h) {
+    return r * 16 + 8 * (h ^ (((r >> 2) ^ (r >> 3)) & 1));
+}
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
@@ -1405,7 +1408,7 @@ void k_up_log_full(UpLogArgs a) {
 
         // ---- products: wave (wm, wn) owns rows wm*QW.., columns wn*QW.. as BR x BR blocks;
         // lane l supplies row (column) l % 32 at contracted indices 8 (l / 32) .. + 7 (the
-        // lines' bit 3 is that of l % 32, as QW and 32 are multiples of 16)
+        // lines' bits 2 and 3 are those of l % 32, as QW and 32 are multiples of 16)
         const int li = lane & 31;
         const int aoff = bf_line_half(wm * QW + li, lane >> 5), boff = bf_line_half(wn * QW + li, lane >> 5);
         // part p of A (of B) for the wave's BR blocks
@@ -1561,7 +1564,10 @@ void k_up_log_full(UpLogArgs a) {
         // column t - TM (over the passes)
         if (tid < kTRows) {
             float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-            for (int c = 0; c < TM; c += 4) {   // (16-byte reads: the tile's rows are 16-byte aligned)
+            // (16-byte reads: the tile's rows are 16-byte aligned.  Lanes t and t + 8 share a
+            // bank group; starting each lane at its own column group avoids that but made the
+            // kernel slower, the addresses no longer being immediate offsets.)
+            for (int c = 0; c < TM; c += 4) {
                 const float4 v = *(const float4*)(T + tid * LDT + c), o = *(const float4*)(cof + c);
                 m[0] = fmaxf(m[0], v.x + o.x);
                 m[1] = fmaxf(m[1], v.y + o.y);
