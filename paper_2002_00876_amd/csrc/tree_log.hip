@@ -1687,18 +1687,19 @@ __global__ __launch_bounds__(kRootThreads) void k_root_log(RootArgs a) {
 constexpr int kVecThreads = 512;
 constexpr int kHalfThreads = kVecThreads / 2;
 
-// LSE_i (w[i] + M[i][j]) for one column j (w in LDS, M row-major in global memory), eight
+// LSE_i (w[i] + M[i][j]) for one column j (w in LDS, M row-major in global memory), kU
 // loads in flight per step
+template <int kU = 8>
 __device__ __forceinline__ float col_lse(const float* __restrict__ M, int C, const float* w, int j) {
     float m = -INFINITY, s = 0.f;
     int i = 0;
-    for (; i + 8 <= C; i += 8) {
-        float x[8];
+    for (; i + kU <= C; i += kU) {
+        float x[kU];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) x[u] = M[(size_t)(i + u) * C + j];
+        for (int u = 0; u < kU; ++u) x[u] = M[(size_t)(i + u) * C + j];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) x[u] += w[i + u];
-        lse_fold<8>(m, s, x);
+        for (int u = 0; u < kU; ++u) x[u] += w[i + u];
+        lse_fold<kU>(m, s, x);
     }
     for (; i < C; ++i) {
         float x[1] = {M[(size_t)i * C + j] + w[i]};
@@ -1707,27 +1708,28 @@ __device__ __forceinline__ float col_lse(const float* __restrict__ M, int C, con
     return lse_val(m, s);
 }
 
-// LSE_j (M[i][j] + w[j]) for one row i; kVec: 16-byte loads (C % 4 == 0)
-template <bool kVec>
+// LSE_j (M[i][j] + w[j]) for one row i; kVec: 16-byte loads (C % 4 == 0), kV of them in
+// flight per step
+template <bool kVec, int kV = 4>
 __device__ __forceinline__ float row_lse(const float* __restrict__ M, int C, const float* w, int i) {
     const float* row = M + (size_t)i * C;
     float m = -INFINITY, s = 0.f;
     int j = 0;
     if constexpr (kVec) {
         const float4* r4 = reinterpret_cast<const float4*>(row);
-        for (; j + 16 <= C; j += 16) {
-            float4 v[4];
+        for (; j + 4 * kV <= C; j += 4 * kV) {
+            float4 v[kV];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) v[u] = r4[j / 4 + u];
-            float x[16];
+            for (int u = 0; u < kV; ++u) v[u] = r4[j / 4 + u];
+            float x[4 * kV];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < kV; ++u) {
                 x[4 * u + 0] = v[u].x + w[j + 4 * u + 0];
                 x[4 * u + 1] = v[u].y + w[j + 4 * u + 1];
                 x[4 * u + 2] = v[u].z + w[j + 4 * u + 2];
                 x[4 * u + 3] = v[u].w + w[j + 4 * u + 3];
             }
-            lse_fold<16>(m, s, x);
+            lse_fold<4 * kV>(m, s, x);
         }
     }
     for (; j + 8 <= C; j += 8) {
@@ -1874,7 +1876,10 @@ __device__ void half_vec(bool active, const float* core, const double* ro, const
         if constexpr (kExact)
             l = rowPass ? row_lse_d<kVec>(core, C, w, t) : col_lse_d(core, C, w, t);
         else
-            l = rowPass ? row_lse<kVec>(core, C, w, t) : col_lse(core, C, w, t);
+            // (C >= 128: 128 bytes in flight per thread, 32 loads down a column or eight
+            // 16-byte loads along a row; still two workgroups per CU)
+            l = rowPass ? (C >= 128 ? row_lse<kVec, 8>(core, C, w, t) : row_lse<kVec>(core, C, w, t))
+                        : (C >= 128 ? col_lse<32>(core, C, w, t) : col_lse(core, C, w, t));
     }
     if (active && t < C) {
         z = (l == -INFINITY) ? -INFINITY : (outOff ? outOff[t] : 0.0) + ws + l;
