@@ -6,12 +6,13 @@
 // edges, l >= 1) and this kernel finishes the sequence:
 //   v_0 = 0,  v_{q+1}[j] = LSE_i (v_q[i] + ro_q[i] + core_q[i][j]) + co_q[j],
 //   log Z = LSE_j v_K[j].
-// v is kept unshifted in float64 (it carries the running log Z); the row weights
-// v[i] + ro[i] - W (W their maximum) are formed in float64 and rounded once.  One workgroup
-// per sequence, two barriers per step: node q + 2 is loaded into registers while node q is
-// used from LDS (and node q + 1, loaded during the step before, is stored to the other LDS
-// buffer), so a load has a whole step to arrive; the next step's W is reduced together with
-// the step's result.
+// v is kept unshifted in float64 (it carries the running log Z, one entry per thread); the
+// row weights v[i] + ro[i] - W (W about their maximum) are formed in float64, rounded once
+// and stored to LDS by their row's thread, so the products read one float per row.  One
+// workgroup per sequence, three barriers per step: node q + 2 is loaded into registers while
+// node q is used from LDS (and node q + 1, loaded during the step before, is stored to the
+// other LDS buffer), so a load has a whole step to arrive; the next step's W is reduced
+// together with the step's result, then the next weights are formed.
 #include <algorithm>
 
 #include "device.h"
@@ -39,9 +40,9 @@ template <bool kVec>
 __global__ __launch_bounds__(kNsThreads) void k_node_scan_log(NodeScanArgs a) {
     extern __shared__ __align__(16) float nsm[];            // two node buffers [C][C]
     __shared__ double ros[2][kNodeScanMaxLabels];           // their ro vectors
-    __shared__ double vs[kNodeScanMaxLabels];               // v_q (unshifted, float64)
+    __shared__ float wsf[kNodeScanMaxLabels];               // row weights v_q[i] + ro_q[i] - W_q
     __shared__ float pm[kNsParts][kNodeScanMaxLabels], ps[kNsParts][kNodeScanMaxLabels];
-    __shared__ double red[2][kNsThreads / kWave];
+    __shared__ float red[2][kNsThreads / kWave];
     __shared__ float sred[kNsThreads / kWave];
     const int64_t b = blockIdx.x;
     const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
@@ -52,17 +53,18 @@ __global__ __launch_bounds__(kNsThreads) void k_node_scan_log(NodeScanArgs a) {
     }
     const int64_t S = (int64_t)1 << a.level, K = (Eb + S - 1) / S;
     const size_t base = (size_t)b * a.nodes;
-    // block maximum of a double: a barrier, then every thread reads the waves' maxima.  The
-    // two slots alternate between steps; a slot is written again only after the next step's
-    // first barrier, so one barrier per call suffices.
+    // block maximum of doubles, rounded to float (a shift: any value near the maximum
+    // serves, as it is added back exactly): a barrier, then every thread reads the waves'
+    // maxima.  The two slots alternate between steps; a slot is written again only after the
+    // next step's first barrier, so one barrier per call suffices.
     auto block_max = [&](double x, int slot) {
-        x = wave_max_d(x);
-        if (lane == 0) red[slot][w] = x;
+        const float xf = wave_max_fast((float)x);
+        if (lane == 0) red[slot][w] = xf;
         __syncthreads();
-        double m = red[slot][0];
+        float m = red[slot][0];
 #pragma unroll
-        for (int q = 1; q < kNsThreads / kWave; ++q) m = fmax(m, red[slot][q]);
-        return m;
+        for (int q = 1; q < kNsThreads / kWave; ++q) m = fmaxf(m, red[slot][q]);
+        return (double)m;
     };
     // node q into registers: the thread's values idx = tid + kNsThreads * r (float4 groups
     // with kVec), and ro, co of line tid
@@ -116,8 +118,9 @@ __global__ __launch_bounds__(kNsThreads) void k_node_scan_log(NodeScanArgs a) {
     fetch(0);
     double co_cur = cov, co_next = 0.0;
     put(0);
-    if (tid < C) vs[tid] = 0.0;
     double W = safe_shift_d(block_max(tid < C ? rov : -INFINITY, 0));
+    if (tid < C) wsf[tid] = (float)(rov - W);
+    __syncthreads();
     if (K > 1) fetch(1);
     const int j = tid % kNodeScanMaxLabels, part = tid / kNodeScanMaxLabels;
     const int rows = (C + kNsParts - 1) / kNsParts;
@@ -136,8 +139,8 @@ __global__ __launch_bounds__(kNsThreads) void k_node_scan_log(NodeScanArgs a) {
             co_next = cov;
         }
         if (q + 2 < K) fetch(q + 2);
-        // y[j] = LSE_i (v[i] + ro[i] - W + M[i][j]) over this thread's part of the rows: the
-        // row weight formed in float64 and rounded once; eight rows' reads in flight
+        // y[j] = LSE_i (v[i] + ro[i] - W + M[i][j]) over this thread's part of the rows (the
+        // row weights from LDS); eight rows' reads in flight
         if (j < C) {
             float m = -INFINITY, s = 0.f;
             int i = i0;
@@ -146,11 +149,11 @@ __global__ __launch_bounds__(kNsThreads) void k_node_scan_log(NodeScanArgs a) {
 #pragma unroll
                 for (int r = 0; r < 8; ++r) x[r] = M[(i + r) * C + j];
 #pragma unroll
-                for (int r = 0; r < 8; ++r) x[r] += (float)(vs[i + r] + ro[i + r] - W);
+                for (int r = 0; r < 8; ++r) x[r] += wsf[i + r];
                 lse_fold<8>(m, s, x);
             }
             for (; i < i1; ++i) {
-                const float x[1] = {(float)(vs[i] + ro[i] - W) + M[i * C + j]};
+                const float x[1] = {wsf[i] + M[i * C + j]};
                 lse_fold<1>(m, s, x);
             }
             pm[part][j] = m;
@@ -175,10 +178,13 @@ __global__ __launch_bounds__(kNsThreads) void k_node_scan_log(NodeScanArgs a) {
                 }
             }
             if (m != -INFINITY) z = co_cur + W + (double)m + (double)flog(s);
-            vs[tid] = z;   // (every read of v_q was before the barrier above)
         }
         vlast = z;
         W = safe_shift_d(block_max(q + 1 < K ? z + ro_next : z, (int)((q + 1) & 1)));
+        if (q + 1 < K) {
+            if (tid < C) wsf[tid] = (float)(z + ro_next - W);
+            __syncthreads();
+        }
         co_cur = co_next;
     }
     // log Z = LSE_j v_K[j]; W is max_j v_K[j]
