@@ -500,11 +500,11 @@ def main():
             if t_mem >= t_cmp:
                 a = alg["marg_bytes"] / sec / 1e9
                 r = {"bound": "hbm", "achieved": round(a, 2), "peak": HBM_PEAK / 1e9,
-                     "unit": "GB/s", "frac": round(a / (HBM_PEAK / 1e9), 5)}
+                     "unit": "GB/s", "frac": float(f"{a / (HBM_PEAK / 1e9):.4g}")}
             else:
                 a = alg["marg_flops"] / sec / 1e12
                 r = {"bound": "mfma", "achieved": round(a, 3), "peak": round(cmp_peak / 1e12, 2),
-                     "unit": "TFLOP/s", "frac": round(a / (cmp_peak / 1e12), 5),
+                     "unit": "TFLOP/s", "frac": float(f"{a / (cmp_peak / 1e12):.4g}"),
                      "peak_note": ("bf16 dense 2500 TFLOP/s / 6: six bf16 products per float32 "
                                    "product (three-part split of each operand)" if bf16x6 else
                                    "fp32 dense MFMA")}
@@ -515,11 +515,11 @@ def main():
             if t_mem >= t_cmp:
                 a = alg["vit_bytes"] / sec / 1e9
                 r = {"bound": "hbm", "achieved": round(a, 2), "peak": HBM_PEAK / 1e9,
-                     "unit": "GB/s", "frac": round(a / (HBM_PEAK / 1e9), 5)}
+                     "unit": "GB/s", "frac": float(f"{a / (HBM_PEAK / 1e9):.4g}")}
             else:
                 a = alg["vit_ops"] / sec / 1e12
                 r = {"bound": "alu", "achieved": round(a, 3), "peak": VALU_F64_OPS_PEAK / 1e12,
-                     "unit": "T fp64 add/max per s", "frac": round(a / (VALU_F64_OPS_PEAK / 1e12), 5)}
+                     "unit": "T fp64 add/max per s", "frac": float(f"{a / (VALU_F64_OPS_PEAK / 1e12):.4g}")}
             r["algorithmic_bytes"] = alg["vit_bytes"]
             r["algorithmic_fp64_ops"] = alg["vit_ops"]
         r["roofline_ms"] = round(max(t_mem, t_cmp) * 1e3, 6)
