@@ -61,6 +61,9 @@ __device__ __forceinline__ void buffer_store4(float4 v, __amdgpu_buffer_rsrc_t r
 __device__ __forceinline__ float buffer_load1(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff) {
     return __int_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
 }
+__device__ __forceinline__ void buffer_store1(float v, __amdgpu_buffer_rsrc_t r, unsigned voff, int soff) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_int(v), r, voff, soff, 0);
+}
 __device__ __forceinline__ float flog(float x) { return __builtin_amdgcn_logf(x) * 0.6931471805599453f; }
 
 // Full-wave reductions with DPP inside each row of 16 lanes and readlane across the four
@@ -83,6 +86,15 @@ __device__ __forceinline__ float wave_max_fast(float x) {
     x = fmaxf(x, dpp_f(x, 0x141));  // mirror within 8
     x = fmaxf(x, dpp_f(x, 0x140));  // mirror within 16
     return fmaxf(fmaxf(rl(x, 0), rl(x, 16)), fmaxf(rl(x, 32), rl(x, 48)));
+}
+// Maximum over the 32 lanes of the calling lane's half-wave (DPP inside each row of 16
+// lanes, then one exchange between the two rows); every lane of the half gets it
+__device__ __forceinline__ float half_max32(float x) {
+    x = fmaxf(x, dpp_f(x, 0xB1));   // lanes i ^ 1
+    x = fmaxf(x, dpp_f(x, 0x4E));   // lanes i ^ 2
+    x = fmaxf(x, dpp_f(x, 0x141));  // mirror within 8
+    x = fmaxf(x, dpp_f(x, 0x140));  // mirror within 16
+    return fmaxf(x, __shfl_xor(x, 16, kWave));
 }
 __device__ __forceinline__ float wave_sum_fast(float x) {
     x += dpp_f(x, 0xB1);

@@ -971,11 +971,9 @@ __global__ __launch_bounds__(kUpThreads) void k_up_log_small(UpLogArgs a) {
 // An operand is exp2(fma(x, log2 e, o log2 e) - s log2 e), the thread's shifts scaled once.
 template <int TM>
 struct UpFullSmem {
-    static constexpr int LDA = kSlice + 4, LDB = TM + 4, LDT = TM + 8;
+    static constexpr int LDA = kSlice + 4, LDB = TM + 4;
     static constexpr int kBuf = TM * LDA + kSlice * LDB;
-    static constexpr int kTRows = TM;               // tile rows staged at once by the epilogue
-    static constexpr int kTileF = kTRows * LDT;
-    static constexpr int kMain = (2 * kBuf > kTileF ? 2 * kBuf : kTileF);
+    static constexpr int kMain = 2 * kBuf;          // (the epilogue's [2][TM] maxima fit)
     // cohs, rohs [kMaxLabels]; sa, sb, cof, rof [TM]; red [2 doubles per wave]
     static constexpr int kFloats = kMain + 2 * kMaxLabels + 4 * TM + 4 * (kUpThreads / kWave);
     static constexpr size_t kBytes = sizeof(float) * kFloats;
@@ -994,17 +992,14 @@ struct UpFullSmem {
 // padding, the two 16-byte halves of line r swapped when bit 2 xor bit 3 of r is set (so
 // that rows r .. r + 7 and r .. r + 15 of one half, aligned, land on distinct 16-byte bank
 // groups, whether a 16-byte access is served 8 or 16 lanes at a time), and an epilogue that
-// stages the tile half by half.
+// works from the registers.
 template <int TM>
 struct UpBfSmem {
     static constexpr int kK = 16;                   // contracted indices per slice
     static constexpr int LDK = kK;                  // bf16 per staged line (32 bytes)
     static constexpr int kPlane = TM * LDK;         // bf16 per part plane
     static constexpr int kBufF = 6 * kPlane / 2;    // A and B, three parts each, in floats
-    static constexpr int LDT = TM + 8;
-    static constexpr int kTRows = TM / 2;
-    static constexpr int kTileF = kTRows * LDT;
-    static constexpr int kMain = (2 * kBufF > kTileF ? 2 * kBufF : kTileF);
+    static constexpr int kMain = 2 * kBufF;
     static constexpr int kFloats = kMain + 2 * kMaxLabels + 4 * TM + 4 * (kUpThreads / kWave);
     static constexpr size_t kBytes = sizeof(float) * kFloats;
     static constexpr int kBlocksPerCU = 3;
@@ -1047,7 +1042,6 @@ __global__ __launch_bounds__(kUpThreads,
                              (kBf ? UpBfSmem<TM>::kBlocksPerCU : UpFullSmem<TM>::kBlocksPerCU))
 void k_up_log_full(UpLogArgs a) {
     using Sm = std::conditional_t<kBf, UpBfSmem<TM>, UpFullSmem<TM>>;
-    constexpr int LDT = Sm::LDT;
     constexpr int BR = TM / 64;                 // 32 x 32 blocks per wave per dimension
     constexpr int QW = TM / 2;                  // a wave's quarter edge
     constexpr float kL2E = 1.4426950408889634f;
@@ -1123,16 +1117,13 @@ void k_up_log_full(UpLogArgs a) {
     // and the tile's row and column shifts; every global read of it goes out at once, after
     // the first slices' loads
     double coLshift = 0.0, roRshift = 0.0;
-    // ro_L of the tile's row and co_R of its column handled by this thread in the epilogue
-    // (float32 variant: read with the set-up; bf16: after the products, which hold more
-    // registers)
-    double lro_t = 0.0, rco_t = 0.0;
     auto shifts = [&]() {
         static_assert(kMaxLabels <= kUpThreads, "one offset of the contracted index per thread");
         static_assert(TM <= kUpThreads, "one output row and column per thread");
         const double lco = (Lco && tid < C) ? Lco[tid] : -INFINITY;
         const double rro = (Rro && tid < C) ? Rro[tid] : -INFINITY;
-        if (!kBf && tid < TM) {
+        double lro_t = 0.0, rco_t = 0.0;   // ro_L of row a0 + tid, co_R of column c0 + tid
+        if (tid < TM) {
             lro_t = Lro ? Lro[a0 + tid] : 0.0;
             rco_t = Rco ? Rco[c0 + tid] : 0.0;
         }
@@ -1165,8 +1156,17 @@ void k_up_log_full(UpLogArgs a) {
             rohs[tid] = rh * kL2E;
         }
         if (tid < TM) {
-            sa[tid] = safe_shift(pa - (float)coLshift);
-            sb[tid] = safe_shift(pb - (float)roRshift);
+            const float sav = safe_shift(pa - (float)coLshift), sbv = safe_shift(pb - (float)roRshift);
+            sa[tid] = sav;
+            sb[tid] = sbv;
+            // the output node's offsets for the tile's rows and columns (known now; the
+            // epilogue reads them from LDS)
+            const double ro = lro_t + coLshift + sav;
+            const double co = rco_t + roRshift + sbv;
+            rof[tid] = (float)ro;
+            cof[tid] = (float)co;
+            if (tn == 0) Pro[a0 + tid] = ro;
+            if (tm == 0) Pco[c0 + tid] = co;
         }
         __syncthreads();
     };
@@ -1476,121 +1476,123 @@ void k_up_log_full(UpLogArgs a) {
             slice(s + 1, 1, ra[1], rb[1], ra[0], rb[0]);
         }
     }
-    // ---- epilogue: core = log S through an LDS tile of kTRows rows (the whole tile, or for
-    // the bf16 variant one half at a time: the waves whose rows it holds write it); entries
-    // whose S underflowed are recomputed by a direct log-sum-exp (a rare, non-unrolled path)
-    constexpr int kTRows = Sm::kTRows, kPasses = TM / kTRows;
-    static_assert(kPasses == 1 || kTRows == QW, "a pass holds whole wave rows");
-    float* T = smem;   // [kTRows][LDT], over the slice buffers (all reads are done)
-    // the output node's offsets for the tile's rows and columns: thread TM + t (or t for a
-    // single pass) takes row and column t, during the first pass (whose tile rows belong to
-    // the other waves) when there are two
-    const int ot = kPasses == 1 ? tid : tid - TM;
-    const bool oth = ot >= 0 && ot < TM;
-    if (kPasses != 1 && oth) {
-        lro_t = Lro ? Lro[a0 + ot] : 0.0;
-        rco_t = Rco ? Rco[c0 + ot] : 0.0;
+    // ---- epilogue, from the registers: S -> log S in place (entries whose S underflowed are
+    // recomputed by a direct log-sum-exp: a rare, non-unrolled path), the partial maxima for
+    // the next level by lane reductions (each merged over the two waves that share its line
+    // through LDS), and the tile stored straight from the registers: one store instruction of
+    // a wave writes two rows' 128-byte segments.
+    float smin = INFINITY;   // the lane's smallest sum: one compare per entry on the hot path
+#pragma unroll
+    for (int i = 0; i < BR; ++i)
+#pragma unroll
+        for (int j = 0; j < BR; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) smin = fminf(smin, acc[i][j][r]);
+    uint64_t under = 0;
+    if (!(smin >= kUnderflow)) {
+        // rare: which entries underflowed
+#pragma unroll
+        for (int i = 0; i < BR; ++i)
+#pragma unroll
+            for (int j = 0; j < BR; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    if (!(acc[i][j][r] >= kUnderflow)) under |= 1ull << ((i * BR + j) * 16 + r);
     }
-    auto offsets = [&]() {
-        if (oth) {
-            const double ro = lro_t + coLshift + sa[ot];
-            const double co = rco_t + roRshift + sb[ot];
-            rof[ot] = (float)ro;
-            cof[ot] = (float)co;
-            if (tn == 0) Pro[a0 + ot] = ro;
-            if (tm == 0) Pco[c0 + ot] = co;
+#pragma unroll
+    for (int i = 0; i < BR; ++i)
+#pragma unroll
+        for (int j = 0; j < BR; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = flog(acc[i][j][r]);
+    const int lc = lane & 31, lh = lane >> 5;
+    while (under) {
+        const int bit = __builtin_ctzll(under);
+        under &= under - 1;
+        const int ij = bit >> 4, rr = bit & 15, bi = ij / BR, bj = ij % BR;
+        const int row = wm * QW + bi * 32 + (rr >> 2) * 8 + lh * 4 + (rr & 3);
+        const int col = wn * QW + bj * 32 + lc;
+        const int gr = a0 + row, gc = c0 + col;
+        const float sr = sa[row], sc = sb[col];
+        const float* lrow = Lc + (size_t)gr * C;
+        // one term of the sum, with the contracted index's offsets formed as the staging
+        // formed them (before the log2 e scale)
+        auto fb_term = [&](int bb) {
+            const float ch = Lco ? (float)(Lco[bb] - coLshift) : 0.f;
+            const float rh = Rro ? (float)(Rro[bb] - roRshift) : 0.f;
+            return (lrow[bb] + ch - sr) + (Rc[(size_t)bb * C + gc] + rh - sc);
+        };
+        float q = -INFINITY;
+        for (int bb = 0; bb < C; ++bb) q = fmaxf(q, fb_term(bb));
+        float val = -INFINITY;
+        if (q != -INFINITY) {
+            float sum = 0.f;
+            for (int bb = 0; bb < C; ++bb) sum += fexp(fb_term(bb) - q);
+            val = q + flog(sum);
         }
-    };
-    static_assert(kPasses == 1 || TM == 2 * QW, "the second half's waves are threads TM ..");
-    if (kPasses == 1) offsets();
-    float cm[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};   // column maxima (TM <= tid < 2 TM)
-    for (int h = 0; h < kPasses; ++h) {
-        const int rb = h * kTRows;   // first tile row held in T
-        if (kPasses == 1 || wm == h) {
-            float smin = INFINITY;   // the lane's smallest sum: one compare per entry on the hot path
 #pragma unroll
-            for (int i = 0; i < BR; ++i)
+        for (int i = 0; i < BR; ++i)
 #pragma unroll
-                for (int j = 0; j < BR; ++j)
+            for (int j = 0; j < BR; ++j)
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int row = wm * QW + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-                        const int col = wn * QW + j * 32 + (lane & 31);
-                        const float S = acc[i][j][r];
-                        T[(row - rb) * LDT + col] = flog(S);
-                        smin = fminf(smin, S);
-                    }
-            uint64_t under = 0;
-            if (!(smin >= kUnderflow)) {
-                // rare: which entries underflowed
-#pragma unroll
-                for (int i = 0; i < BR; ++i)
-#pragma unroll
-                    for (int j = 0; j < BR; ++j)
-#pragma unroll
-                        for (int r = 0; r < 16; ++r)
-                            if (!(acc[i][j][r] >= kUnderflow)) under |= 1ull << ((i * BR + j) * 16 + r);
-            }
-            while (under) {
-                const int bit = __builtin_ctzll(under);
-                under &= under - 1;
-                const int ij = bit >> 4, r = bit & 15, i = ij / BR, j = ij % BR;
-                const int row = wm * QW + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-                const int col = wn * QW + j * 32 + (lane & 31);
-                const int gr = a0 + row, gc = c0 + col;
-                const float sr = sa[row], sc = sb[col];
-                const float* lrow = Lc + (size_t)gr * C;
-                // one term of the sum, with the contracted index's offsets formed as the staging
-                // formed them (before the log2 e scale)
-                auto fb_term = [&](int bb) {
-                    const float ch = Lco ? (float)(Lco[bb] - coLshift) : 0.f;
-                    const float rh = Rro ? (float)(Rro[bb] - roRshift) : 0.f;
-                    return (lrow[bb] + ch - sr) + (Rc[(size_t)bb * C + gc] + rh - sc);
-                };
-                float q = -INFINITY;
-                for (int bb = 0; bb < C; ++bb) q = fmaxf(q, fb_term(bb));
-                float val = -INFINITY;
-                if (q != -INFINITY) {
-                    float sum = 0.f;
-                    for (int bb = 0; bb < C; ++bb) sum += fexp(fb_term(bb) - q);
-                    val = q + flog(sum);
-                }
-                T[(row - rb) * LDT + col] = val;
-            }
-        }
-        if (kPasses != 1 && h == 0) offsets();
-        __syncthreads();
-        // partial maxima for the next level: thread t < kTRows row rb + t; TM <= t < 2 TM
-        // column t - TM (over the passes)
-        if (tid < kTRows) {
-            float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-            // (16-byte reads: the tile's rows are 16-byte aligned.  Lanes t and t + 8 share a
-            // bank group; starting each lane at its own column group avoids that but made the
-            // kernel slower, the addresses no longer being immediate offsets.)
-            for (int c = 0; c < TM; c += 4) {
-                const float4 v = *(const float4*)(T + tid * LDT + c), o = *(const float4*)(cof + c);
-                m[0] = fmaxf(m[0], v.x + o.x);
-                m[1] = fmaxf(m[1], v.y + o.y);
-                m[2] = fmaxf(m[2], v.z + o.z);
-                m[3] = fmaxf(m[3], v.w + o.w);
-            }
-            Pmr[(size_t)(a0 + rb + tid) * nt + tn] = fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3]));
-        } else if (tid >= TM && tid < 2 * TM) {
-            const int c = tid - TM;
-            for (int r = 0; r < kTRows; r += 4)
-#pragma unroll
-                for (int u = 0; u < 4; ++u) cm[u] = fmaxf(cm[u], T[(r + u) * LDT + c] + rof[rb + r + u]);
-        }
-        // the rows held, 16 bytes per store
-        constexpr int kQ = TM / 4;
-        for (int idx = tid; idx < kTRows * kQ; idx += kUpThreads) {
-            const int r = idx / kQ, c4 = idx % kQ;
-            *(float4*)(Pc + (size_t)(a0 + rb + r) * C + c0 + 4 * c4) = *(const float4*)(T + r * LDT + 4 * c4);
-        }
-        if (h + 1 < kPasses) __syncthreads();
+                for (int r = 0; r < 16; ++r)
+                    if ((i * BR + j) * 16 + r == bit) acc[i][j][r] = val;
     }
-    if (tid >= TM && tid < 2 * TM)
-        Pmc[(size_t)(c0 + tid - TM) * nt + tm] = fmaxf(fmaxf(cm[0], cm[1]), fmaxf(cm[2], cm[3]));
+    // partial maxima: rows of T + co over the wave's columns, columns of T + ro over its rows
+    // (lane l holds rows .. + 4 (l / 32) + (r & 3) of each group of 8 and column l % 32 of each
+    // 32-wide block)
+    float* rowp = smem;            // [2][TM], by column half wn (the slice buffers are free)
+    float* colp = smem + 2 * TM;   // [2][TM], by row half wm
+    float cofv[BR], cmx[BR];
+#pragma unroll
+    for (int j = 0; j < BR; ++j) {
+        cofv[j] = cof[wn * QW + j * 32 + lc];
+        cmx[j] = -INFINITY;
+    }
+#pragma unroll
+    for (int i = 0; i < BR; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int row0 = wm * QW + i * 32 + g * 8 + lh * 4;
+            const float4 ro4 = *(const float4*)(rof + row0);
+            const float rov[4] = {ro4.x, ro4.y, ro4.z, ro4.w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int r = 4 * g + q;
+                float m = acc[i][0][r] + cofv[0];
+#pragma unroll
+                for (int j = 1; j < BR; ++j) m = fmaxf(m, acc[i][j][r] + cofv[j]);
+                m = half_max32(m);
+                if (lc == 0) rowp[wn * TM + row0 + q] = m;
+#pragma unroll
+                for (int j = 0; j < BR; ++j) cmx[j] = fmaxf(cmx[j], acc[i][j][r] + rov[q]);
+            }
+        }
+#pragma unroll
+    for (int j = 0; j < BR; ++j) {
+        const float m = fmaxf(cmx[j], __shfl_xor(cmx[j], 32, kWave));
+        if (lh == 0) colp[wm * TM + wn * QW + j * 32 + lc] = m;
+    }
+    // the tile: a lane's 32-bit offset at its first row and column, each entry's row and
+    // block in the scalar offset
+    {
+        const __amdgpu_buffer_rsrc_t rsP = make_rsrc(Pc, C * C);
+        const unsigned pv = 4u * (unsigned)((a0 + wm * QW + lh * 4) * C + c0 + wn * QW + lc);
+#pragma unroll
+        for (int i = 0; i < BR; ++i)
+#pragma unroll
+            for (int j = 0; j < BR; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    buffer_store1(acc[i][j][r], rsP, pv, 4 * ((i * 32 + (r >> 2) * 8 + (r & 3)) * C + j * 32));
+    }
+    __syncthreads();
+    if (tid < TM) {
+        Pmr[(size_t)(a0 + tid) * nt + tn] = fmaxf(rowp[tid], rowp[TM + tid]);
+    } else if (tid < 2 * TM) {
+        const int c = tid - TM;
+        Pmc[(size_t)(c0 + c) * nt + tm] = fmaxf(colp[c], colp[TM + c]);
+    }
 }
 
 // ---------------------------------------------------------------- root: log Z
