@@ -40,3 +40,22 @@ def test_wide_tiles_wide_dynamic_range(B, N, C, lens):
     # recomputation
     pot, lens = W.random_case(5000 + N + C, B, N, C, sigma=40.0, lengths=lens)
     check_all(pot, lens, f"wide tiles, sigma=40 B={B} N={N} C={C}")
+
+
+def test_wide_tiles_product_underflow():
+    # level-1 products on the 128-wide full tiles with entries whose shifted sum underflows
+    # (S < 2^-80: every term below 2^-126) and takes the direct log-sum-exp: rows 5 and 77
+    # of every even edge keep their mass on one contracted index, columns 9 and 200 of every
+    # odd edge on another, so those entries of each level-1 product are about 2 e^-150 after
+    # the shifts (the edges also reach magnitude 16: the float64 formation)
+    B, N, C = 2, 257, 256
+    pot, lens = W.random_case(6000, B, N, C, sigma=1.0, lengths=[257, 190])
+    for t in range(0, N - 1, 2):
+        for i, k0 in ((5, 3), (77, 100)):
+            pot[:, t, i, :] -= 150.0
+            pot[:, t, i, k0] += 150.0
+    for t in range(1, N - 1, 2):
+        for j, k1 in ((9, 50), (200, 201)):
+            pot[:, t, :, j] -= 150.0
+            pot[:, t, k1, j] += 150.0
+    check_all(pot, lens, f"wide tiles, underflowing products B={B} N={N} C={C}")
