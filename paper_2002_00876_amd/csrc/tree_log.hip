@@ -981,8 +981,9 @@ struct UpFullSmem {
 };
 
 // The bf16 variant (kBf) stages each exponentiated operand x as three bf16 parts
-// x = hi + mid + lo (hi = bf16(x), mid = bf16(x - hi), lo = bf16(x - hi - mid): 24 significant
-// bits, float32's own precision, and float32's exponent range), in slices of 16 contracted
+// x = hi + mid + lo (hi = x truncated to bf16, mid = x - hi truncated, lo = x - hi - mid, which
+// bf16 holds exactly: 24 significant bits, float32's own precision, and float32's exponent
+// range), in slices of 16 contracted
 // indices, A as [row][k] and B transposed as [column][k], and sums the six products
 //   hi.hi + hi.mid + mid.hi + hi.lo + lo.hi + mid.mid
 // with the bf16 matrix instructions (32x32x16, float32 accumulation), which run 16 times the
