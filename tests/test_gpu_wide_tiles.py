@@ -18,6 +18,7 @@ CASES = [
     (2, 257, 256, [257, 190]),
     (2, 257, 130, [257, 101]),    # two tiles per dimension, the second one ragged
     (3, 300, 192, [300, 299, 150]),
+    (4, 257, 256, [257, 1, 2, 3]),    # sequences of one to three tokens beside a full one
 ]
 
 
