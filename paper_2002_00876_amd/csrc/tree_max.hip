@@ -24,7 +24,7 @@ namespace tsc {
 namespace {
 
 constexpr int kMT = 64;    // output tile edge
-constexpr int kMK = 32;    // k slice of the narrow kernel
+constexpr int kMK = 16;    // k slice of the narrow kernel (16: fewer staging registers, more waves)
 constexpr int kMThreads = 256;
 constexpr int64_t kFewTiles = 512;   // two 128-wide tiles per compute unit
 
@@ -121,7 +121,7 @@ __global__ __launch_bounds__(kMThreads) void k_up_max_narrow(UpMaxArgs a) {
     for (int64_t k0 = 0; k0 < C; k0 += kMK) {
         const bool more = k0 + kMK < C;
         if (more) load(k0 + kMK);
-#pragma unroll 4
+#pragma unroll 2
         for (int kk = 0; kk < kMK; ++kk) {
             double av[4], bv[4];
 #pragma unroll
