@@ -1574,19 +1574,9 @@ void k_up_log_full(UpLogArgs a) {
         const float m = fmaxf(cmx[j], __shfl_xor(cmx[j], 32, kWave));
         if (lh == 0) colp[wm * TM + wn * QW + j * 32 + lc] = m;
     }
-    // the tile: a lane's 32-bit offset at its first row and column, each entry's row and
-    // block in the scalar offset
-    {
-        const __amdgpu_buffer_rsrc_t rsP = make_rsrc(Pc, C * C);
-        const unsigned pv = 4u * (unsigned)((a0 + wm * QW + lh * 4) * C + c0 + wn * QW + lc);
-#pragma unroll
-        for (int i = 0; i < BR; ++i)
-#pragma unroll
-            for (int j = 0; j < BR; ++j)
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    buffer_store1(acc[i][j][r], rsP, pv, 4 * ((i * 32 + (r >> 2) * 8 + (r & 3)) * C + j * 32));
-    }
+    // the merged maxima first (a barrier waits for the stores issued before it), then the
+    // tile: a lane's 32-bit offset at its first row and column, each entry's row and block in
+    // the scalar offset; nothing waits for these stores
     __syncthreads();
     if (tid < TM) {
         Pmr[(size_t)(a0 + tid) * nt + tn] = fmaxf(rowp[tid], rowp[TM + tid]);
@@ -1594,6 +1584,15 @@ void k_up_log_full(UpLogArgs a) {
         const int c = tid - TM;
         Pmc[(size_t)(c0 + c) * nt + tm] = fmaxf(colp[c], colp[TM + c]);
     }
+    const __amdgpu_buffer_rsrc_t rsP = make_rsrc(Pc, C * C);
+    const unsigned pv = 4u * (unsigned)((a0 + wm * QW + lh * 4) * C + c0 + wn * QW + lc);
+#pragma unroll
+    for (int i = 0; i < BR; ++i)
+#pragma unroll
+        for (int j = 0; j < BR; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                buffer_store1(acc[i][j][r], rsP, pv, 4 * ((i * 32 + (r >> 2) * 8 + (r & 3)) * C + j * 32));
 }
 
 // ---------------------------------------------------------------- root: log Z
