@@ -2155,12 +2155,18 @@ __global__ __launch_bounds__(kVecThreads) void k_form_reg(FormArgs a) {
 
 // The per-pair computation for C = 256, where two leaves do not fit a workgroup's registers:
 // the left leaf is held in registers (1024 threads, 64 values each) and read once, the right
-// one is streamed twice (once for its row pass, once for its marginals): 1.5 reads per edge
-// instead of 2.  Thread t = 64 w + g holds columns 4g .. 4g+3 of rows w + 16 q (q < 16), so
+// one is streamed for its row pass and again for its marginals, except the rows kept in LDS
+// from the first read: 1.28 reads per edge instead of 2.  Thread t = 64 w + g holds columns
+// 4g .. 4g+3 of rows w + 16 q (q < 16), so
 // each row of a leaf is one wave's contiguous 1 KiB: the row pass of the right leaf reduces
 // within a wave, the column pass of the left leaf merges the 16 waves' states through LDS.
 constexpr int kBigLabels = 256;
 constexpr int kBigThreads = 1024;
+// rows of the right leaf each wave keeps in LDS from its first read (of the 16 it handles):
+// the second read takes them from there (7 of 16 rows: 112 KB beside the kernel's 40 KB of
+// static LDS, one workgroup per CU as its registers already allow)
+constexpr int kBigKeep = 7;
+constexpr size_t kBigKeepBytes = sizeof(float4) * kBigKeep * (kBigThreads / kWave) * kWave;
 
 // (m, s) += (m2, s2) for log-sum-exp states; value = m + log s, m = -inf: empty
 template <typename Tm>
@@ -2219,6 +2225,7 @@ __global__ __launch_bounds__(kBigThreads) void k_form_big(FormArgs a) {
     __shared__ double yraw[C], zraw[C];
     __shared__ float pm[kW][C], ps[kW][C];
     __shared__ double nrm[2];
+    extern __shared__ __align__(16) float4 rkeep[];   // [kBigKeep][kW][64]: right-leaf rows
     const int64_t npairs = (a.N - 1 + 1) / 2;
     const int64_t b = blockIdx.x / npairs, k = blockIdx.x % npairs;
     const int64_t Eb = clamp_len(a.lengths, b, a.N) - 1;
@@ -2282,6 +2289,9 @@ __global__ __launch_bounds__(kBigThreads) void k_form_big(FormArgs a) {
             float4 rv[kChunk];
 #pragma unroll
             for (int q = 0; q < kChunk; ++q) rv[q] = buffer_load4(rsR, voff, kRowStep * (q0 + q));
+#pragma unroll
+            for (int q = 0; q < kChunk; ++q)
+                if (q0 + q < kBigKeep) rkeep[((q0 + q) * kW + w) * kWave + g] = rv[q];
             Tm m[kChunk];
             float sm[kChunk];
 #pragma unroll
@@ -2358,7 +2368,9 @@ __global__ __launch_bounds__(kBigThreads) void k_form_big(FormArgs a) {
         for (int q0 = 0; q0 < kR; q0 += kChunk) {
             float4 rv[kChunk];
 #pragma unroll
-            for (int q = 0; q < kChunk; ++q) rv[q] = buffer_load4(rsR, voff, kRowStep * (q0 + q));
+            for (int q = 0; q < kChunk; ++q)   // (the kept rows from LDS; each thread reads its own)
+                rv[q] = q0 + q < kBigKeep ? rkeep[((q0 + q) * kW + w) * kWave + g]
+                                          : buffer_load4(rsR, voff, kRowStep * (q0 + q));
 #pragma unroll
             for (int q = 0; q < kChunk; ++q)
                 buffer_store4(emit(rv[q], sv, n, (double)ya[w + kW * (q0 + q)]), rsO, voff,
@@ -2484,6 +2496,18 @@ hipError_t allow_up_lds() {
         hipError_t e = hipFuncSetAttribute((const void*)k_up_log<TM, VEC, kBits>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize,
                                            (int)UpSmem<TM>::kBytes);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    return hipSuccess;
+}
+
+template <bool kExact>
+hipError_t allow_form_big_lds() {
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute((const void*)k_form_big<kExact>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)kBigKeepBytes);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
@@ -2663,7 +2687,9 @@ hipError_t launch_marginals_tree(const Plan& p, const float* pot, const int32_t*
         hipLaunchKernelGGL((k_form_reg<8, true>), grid, dim3(kVecThreads), 0, s, f);
     } else if (p.C == kBigLabels) {
         // (pairs of large magnitude: the two-read kernel, whose float64 terms fit its registers)
-        hipLaunchKernelGGL((k_form_big<false>), grid, dim3(kBigThreads), 0, s, f);
+        hipError_t e = allow_form_big_lds<false>();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((k_form_big<false>), grid, dim3(kBigThreads), kBigKeepBytes, s, f);
         hipLaunchKernelGGL((k_form_log<true, true>), grid, dim3(kVecThreads), 0, s, f);
     } else if (p.C % 4 == 0) {
         hipLaunchKernelGGL((k_form_log<true, false>), grid, dim3(kVecThreads), 0, s, f);
