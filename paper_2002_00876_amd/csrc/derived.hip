@@ -23,7 +23,10 @@ constexpr int kEntThreads = 256;
 // row per lane): all the group's loads are issued before any reduction, so a wave keeps
 // kGroup * kPer coalesced row loads in flight.  Per row:
 //   m = sum_j p,   m * H(row / m) = -sum_j p (log p - log m).
+// Entries (and rows) below the smallest normal float are left out: each such term is below
+// 1e-36, and the hardware logarithm reads a subnormal input as zero (its log as -inf).
 constexpr int kGroup = 8;
+constexpr float kTiny = 1.17549435e-38f;   // the smallest normal float
 
 template <int kPer>
 __global__ __launch_bounds__(kEntThreads) void k_entropy_edges(const float* mu,
@@ -54,12 +57,12 @@ __global__ __launch_bounds__(kEntThreads) void k_entropy_edges(const float* mu,
 #pragma unroll
             for (int q = 0; q < kPer; ++q) rs += v[g][q];
             const float mi = wave_sum(rs);
-            if (!(mi > 0.f)) continue;   // wave-uniform
+            if (!(mi >= kTiny)) continue;   // wave-uniform
             const float lm = flog(mi);
             float hg = 0.f;
 #pragma unroll
             for (int q = 0; q < kPer; ++q)
-                if (v[g][q] > 0.f) hg -= v[g][q] * (flog(v[g][q]) - lm);
+                if (v[g][q] >= kTiny) hg -= v[g][q] * (flog(v[g][q]) - lm);
             if (t == 0 && lane == 0) hg -= mi * lm;
             h += hg;
         }

@@ -82,6 +82,18 @@ def test_named_workloads(name):
     _check(pot, lens, labels, f"{name} random labels")
 
 
+def test_entropy_with_subnormal_marginals():
+    # scale-10 potentials: dozens of edge marginals of the first two sequences lie below the
+    # smallest normal float (the oracle's, rounded to float32), where the hardware log reads
+    # zero; those terms are below 1e-36 and must not turn the entropy into inf
+    pot, lens = W.random_case(1010, 3, 60, 48, sigma=10.0, lengths=[60, 33, 5])
+    _, mo = oracle.marginals(pot, lens)
+    m32 = mo.astype(np.float32)
+    assert ((m32 > 0) & (m32 < np.finfo(np.float32).tiny)).sum() > 0
+    labels = np.random.default_rng(7).integers(0, 48, size=(3, 60)).astype(np.int32)
+    _check(pot, lens, labels, "subnormal marginals")
+
+
 def test_uniform_and_single_token():
     pot = np.zeros((3, 6, 4, 4), np.float32)
     lens = np.array([7, 1, 3], np.int32)
