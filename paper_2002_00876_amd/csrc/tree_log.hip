@@ -1038,7 +1038,7 @@ __device__ __forceinline__ void split_bf16x3(const float (&x)[8], bf16x8& hi, bf
     lo = __builtin_bit_cast(bf16x8, l);
 }
 
-template <int TM, bool kBf>
+template <int TM, bool kBf, int kNS = 0>
 __global__ __launch_bounds__(kUpThreads,
                              (kBf ? UpBfSmem<TM>::kBlocksPerCU : UpFullSmem<TM>::kBlocksPerCU))
 void k_up_log_full(UpLogArgs a) {
@@ -1354,9 +1354,11 @@ void k_up_log_full(UpLogArgs a) {
             float4 oa0, oa1, ob0, ob1;   // offsets (log2 units) of ka.., kb..
             float x[8];                  // exponentials of the phase's side
         };
-        auto stage_offsets = [&](StageRegs& g, int ks) {
+        auto stage_offsets_a = [&](StageRegs& g, int ks) {
             g.oa0 = *(const float4*)(cohs + ks + ka);
             g.oa1 = *(const float4*)(cohs + ks + ka + 4);
+        };
+        auto stage_offsets_b = [&](StageRegs& g, int ks) {
             g.ob0 = *(const float4*)(rohs + ks + kb);
             g.ob1 = *(const float4*)(rohs + ks + kb + 4);
         };
@@ -1392,13 +1394,17 @@ void k_up_log_full(UpLogArgs a) {
         };
         auto stage = [&](const float4 (&xa)[2], const float (&xb)[8], int ks, int buf) {
             StageRegs g;
-            stage_offsets(g, ks);
+            stage_offsets_a(g, ks);
+            stage_offsets_b(g, ks);
             stage_exp_a(g, xa);
             stage_store(g, 0, buf);
             stage_exp_b(g, xb);
             stage_store(g, 1, buf);
         };
-        const int nslices = C / kK;   // even: C is a multiple of 128
+        // (C = 128 or 256: the slice count is a compile-time constant, so that the slice loop
+        // below unrolls completely and each slice's offsets are immediates)
+        static_assert(kNS == 8 || kNS == 16, "bf16 parts: C = 128 or 256");
+        constexpr int nslices = kNS;
         gload(ra[0], rb[0], 0);
         gload(ra[1], rb[1], kK);
         shifts();
@@ -1432,6 +1438,9 @@ void k_up_log_full(UpLogArgs a) {
         // scheduler interleaves the two within the group but keeps the groups in order.
         auto slice = [&](int s, int cur, float4 (&xa0)[2], float (&xb0)[8], float4 (&xa1)[2],
                          float (&xb1)[8]) {
+            // (no instruction moves between slices: the unrolled slices would otherwise
+            // interleave and hold more registers than three workgroups per CU leave)
+            __builtin_amdgcn_sched_barrier(0);
             gload(xa0, xb0, min(s + 2, nslices - 1) * kK);
             // the operands of the first two groups now, those of the other four during the
             // first group (fewer registers held at once)
@@ -1452,16 +1461,18 @@ void k_up_log_full(UpLogArgs a) {
                             A[kTerms[t][0]][i], Bv[kTerms[t][1]][j], acc[i][j], 0, 0, 0);
             };
             const int ks1 = min(s + 1, nslices - 1) * kK;
+            // (each side's offsets are read just before that side's exponentials need them)
             term(0);
             read_a(A[1], cur, 1);
             read_b(Bv[1], cur, 1);
-            stage_offsets(g, ks1);
+            stage_offsets_a(g, ks1);
             __builtin_amdgcn_sched_barrier(0);
             term(1);
             stage_exp_a(g, xa1);
             __builtin_amdgcn_sched_barrier(0);
             term(2);
             stage_store(g, 0, cur ^ 1);
+            stage_offsets_b(g, ks1);
             __builtin_amdgcn_sched_barrier(0);
             term(3);
             stage_exp_b(g, xb1);
@@ -1472,6 +1483,7 @@ void k_up_log_full(UpLogArgs a) {
             term(5);
             __syncthreads();
         };
+#pragma unroll
         for (int s = 0; s < nslices; s += 2) {
             slice(s, 0, ra[0], rb[0], ra[1], rb[1]);
             slice(s + 1, 1, ra[1], rb[1], ra[0], rb[0]);
@@ -2527,12 +2539,12 @@ hipError_t allow_leaf_lds() {
     return hipSuccess;
 }
 
-template <int TM, bool kBf>
+template <int TM, bool kBf, int kNS = 0>
 hipError_t allow_up_full_lds() {
     static bool attr_set = false;
     if (!attr_set) {
         using Sm = std::conditional_t<kBf, UpBfSmem<TM>, UpFullSmem<TM>>;
-        hipError_t e = hipFuncSetAttribute((const void*)k_up_log_full<TM, kBf>,
+        hipError_t e = hipFuncSetAttribute((const void*)k_up_log_full<TM, kBf, kNS>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize,
                                            (int)Sm::kBytes);
         if (e != hipSuccess) return e;
@@ -2548,7 +2560,14 @@ hipError_t up_sweep_vec(const Plan& p, const float* pot, const int32_t* lengths,
     // full tiles (every tile edge divides C; dense chains): the scheduled kernel
     const bool full64 = !kBits && p.C % 64 == 0, full128 = !kBits && p.C % 128 == 0;
     if (e == hipSuccess && full64) e = allow_up_full_lds<64, false>();
-    if (e == hipSuccess && full128) e = allow_up_full_lds<128, kUpBf16>();
+    // (C <= kMaxLabels = 256, so full 128-wide tiles mean C = 128 or 256: 8 or 16 slices)
+    static_assert(kMaxLabels <= 256, "the bf16 product is instantiated for C = 128 and 256");
+    if (e == hipSuccess && full128) {
+        if constexpr (kUpBf16)
+            e = p.C == 128 ? allow_up_full_lds<128, true, 8>() : allow_up_full_lds<128, true, 16>();
+        else
+            e = allow_up_full_lds<128, false>();
+    }
     if (e != hipSuccess) return e;
     // the leaves' row and column maxima (shifts of the level-1 products)
     LeafMaxArgs m{pot, lengths, p.N, p.C, p.lrmax, p.lcmax, p.rbits[0], p.cbits[0], p.bw, p.wide};
@@ -2594,9 +2613,19 @@ hipError_t up_sweep_vec(const Plan& p, const float* pot, const int32_t* lengths,
         else if (tm == 64 && full64)
             hipLaunchKernelGGL((k_up_log_full<64, false>), dim3((unsigned)a.ngrid), dim3(kUpThreads),
                                UpFullSmem<64>::kBytes, s, a);
-        else if (tm == 128 && full128)
-            hipLaunchKernelGGL((k_up_log_full<128, kUpBf16>), dim3((unsigned)a.ngrid), dim3(kUpThreads),
-                               (std::conditional_t<kUpBf16, UpBfSmem<128>, UpFullSmem<128>>::kBytes), s, a);
+        else if (tm == 128 && full128) {
+            if constexpr (kUpBf16) {
+                if (p.C == 128)
+                    hipLaunchKernelGGL((k_up_log_full<128, true, 8>), dim3((unsigned)a.ngrid),
+                                       dim3(kUpThreads), UpBfSmem<128>::kBytes, s, a);
+                else
+                    hipLaunchKernelGGL((k_up_log_full<128, true, 16>), dim3((unsigned)a.ngrid),
+                                       dim3(kUpThreads), UpBfSmem<128>::kBytes, s, a);
+            } else {
+                hipLaunchKernelGGL((k_up_log_full<128, false>), dim3((unsigned)a.ngrid), dim3(kUpThreads),
+                                   UpFullSmem<128>::kBytes, s, a);
+            }
+        }
         else if (tm == 64)
             hipLaunchKernelGGL((k_up_log<64, VEC, kBits>), dim3((unsigned)a.ngrid), dim3(kUpThreads),
                                UpSmem<64>::kBytes, s, a);
