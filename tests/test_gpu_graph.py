@@ -20,15 +20,19 @@ def _outputs(dev, B, N, C):
             torch.empty(B, dtype=torch.float32, device=dev))
 
 
-@pytest.mark.parametrize("case", ["paper", "tree_c40"])
+@pytest.mark.parametrize("case", ["paper", "tree_c40", "chunk_c64", "bf16_c128"])
 def test_graph_replay_matches_eager(case, monkeypatch):
     import torch
     from paper_2002_00876_amd import binding
     if case == "paper":
         pot_h, lens_h = W.generate("paper")
-    else:
+    elif case == "tree_c40":
         monkeypatch.setenv("TS_PATH", "tree")
         pot_h, lens_h = W.random_case(11, 3, 37, 40)
+    elif case == "chunk_c64":      # the chunk path (C <= 64, long chains)
+        pot_h, lens_h = W.random_case(13, 4, 300, 64, lengths=[300, 257, 64, 2])
+    else:                          # the tree with the bf16-split 128-wide tiles
+        pot_h, lens_h = W.random_case(14, 4, 257, 128, lengths=[257, 200, 131, 64])
     say(f"graph replay case {case}: shape {pot_h.shape}")
     dev = torch.device("cuda:0")
     pot = torch.from_numpy(pot_h).to(dev)
@@ -82,7 +86,7 @@ def test_graph_replay_matches_eager(case, monkeypatch):
     say(f"graph replay case {case}: 4 replays bitwise equal to eager")
 
 
-@pytest.mark.parametrize("case", ["paper", "tree_c40"])
+@pytest.mark.parametrize("case", ["paper", "tree_c40", "bf16_c128"])
 def test_graph_replay_of_the_combined_call(case, monkeypatch):
     """The combined call captured as it stands: on the multi-launch tree it forks its Viterbi
     half onto the library's side stream and joins it back, which the capture must follow."""
@@ -90,9 +94,11 @@ def test_graph_replay_of_the_combined_call(case, monkeypatch):
     from paper_2002_00876_amd import binding
     if case == "paper":
         pot_h, lens_h = W.generate("paper")
-    else:
+    elif case == "tree_c40":
         monkeypatch.setenv("TS_PATH", "tree")
         pot_h, lens_h = W.random_case(13, 3, 37, 40)
+    else:
+        pot_h, lens_h = W.random_case(15, 4, 257, 128, lengths=[257, 190, 77, 3])
     say(f"combined-call graph case {case}: shape {pot_h.shape}")
     dev = torch.device("cuda:0")
     pot = torch.from_numpy(pot_h).to(dev)
