@@ -1,8 +1,9 @@
 """Parity at the full sizes of the larger workloads (B=32 N=512 C=64, B=16 N=1024 C=256,
-B=4 N=8192 C=128), in the launch configuration the benchmark uses: log Z and Viterbi
-path and score of every sequence, and the marginals of EVERY edge of every sequence,
-element by element, against the float64 oracle's forward-backward messages streamed
-edge range by edge range (the marginal tensor is never held in float64 at once).
+B=4 N=8192 C=128, and B=33 N=1024 C=256, past 2^31 elements per array), in the launch
+configuration the benchmark uses: log Z and Viterbi path and score of every sequence, and
+the marginals of EVERY edge of every sequence, element by element, against the float64
+oracle's forward-backward messages streamed edge range by edge range (the marginal tensor
+is never held in float64 at once).
 Padding edges must be exactly 0.  The combined marginals + Viterbi call must reproduce
 the separate calls bitwise."""
 import numpy as np
@@ -45,15 +46,22 @@ def compare_every_edge(m, pot, lens, name):
     return worst, where, msg.logz
 
 
-@pytest.mark.parametrize("name", ["mid", "long", "hmm"])
-def test_full_size(name):
+# past 2^31 elements per array: the HMM-style construction with 33 sequences (2.21e9
+# elements, 8.8 GB of potentials and as much of marginals)
+PAST_2_31 = W.Workload("hmm_b33", 33, 1024, 256, seed=9, kind="hmm")
+
+
+@pytest.mark.parametrize("workload", ["mid", "long", "hmm", PAST_2_31],
+                         ids=["mid", "long", "hmm", "hmm_b33"])
+def test_full_size(workload):
     import torch
 
     import oracle
     from paper_2002_00876_amd import binding
 
+    name = workload if isinstance(workload, str) else workload.name
     say(f"{name}: generating")
-    pot, lens = W.generate(name)
+    pot, lens = W.generate(workload)
     B, E, C, _ = pot.shape
     tp = torch.from_numpy(pot).cuda()
     tl = torch.from_numpy(lens).cuda()
